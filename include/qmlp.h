@@ -1,0 +1,185 @@
+/*
+ * qmlp.h -- C ABI of the MI355X (gfx950) W4/W2-GateUp decode-MLP library.
+ *
+ * The library runs the inference hot path of the W4/W2-GateUp deployment
+ * with Recover-LoRA adapters (arXiv 2606.04238): one gated-MLP block whose
+ * gate and up projections are 2-bit group-quantized, each carrying an
+ * unmerged low-rank correction x A^T B^T, followed by SiLU(gate) * up and a
+ * 4-bit group-quantized down projection.
+ *
+ *   Sec. 3.1, Eq. (1)  LoRA-augmented linear  Y = W X + alpha B A X.
+ *   Sec. 3.3           W4/W2-GateUp: gate/up at 2 bits, every other linear
+ *                      (down included) at 4 bits, group-wise quantization.
+ *   Sec. 4.1           Stage 1: gate/up to INT2 by post-training quantization.
+ *   Sec. 4.2           adapters on the quantized gate/up, kept as a separate
+ *                      module at inference (not merged into the 2-bit grid).
+ *   Sec. 5             the MLP is one fused gate-activation-down operator;
+ *                      decode is bound by the bandwidth of loading weights.
+ *   Sec. 7             deployment: quantize gate/up to INT2 (step 1), the rest
+ *                      to INT4 (step 4), deploy with attached adapters (step 5).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every pointer except the qmlp_qweight/qmlp_mlp descriptors and the
+ *    status-string result is a DEVICE pointer into memory the caller owns.
+ *    The library never allocates or frees device memory and keeps no pointer
+ *    after a call returns.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream)
+ *    and runs asynchronously; nothing synchronizes.
+ *  - Arguments are validated first.  On any error nothing is enqueued and no
+ *    output is written.  A HIP launch error maps to QMLP_ERR_HIP; a fault
+ *    inside a kernel surfaces at the caller's next synchronization.
+ *  - Calls are reentrant: there is no global mutable state.  Inputs and
+ *    outputs of one call must not overlap.
+ *
+ * Storage format of a quantized matrix W [n][k] (nn.Linear orientation:
+ * n outputs, k inputs; groups of g consecutive inputs of one row):
+ *  - codes: row-major, each row a run of little-endian 32-bit words; code i
+ *    of a row sits at bits [b*(i mod 32/b), +b) of word i/(32/b) of that row
+ *    (16 codes per word at b=2, 8 at b=4).  Size n*k*b/8 bytes.
+ *  - meta: row-major [n][k/g] pairs of binary16 (scale, zero), scale first.
+ *    Size n*(k/g)*4 bytes.  The dequantized weight is scale * (q - zero).
+ *  - Quantizer (round-to-nearest, asymmetric min-max; the paper fixes only
+ *    the bit width and grouping): per group lo = min(0, min w),
+ *    hi = max(0, max w), s = (hi - lo)/(2^b - 1) in fp64, scale = s rounded
+ *    once to binary16 (nearest-even; 0 becomes 1.0),
+ *    zero = clamp(rint(-lo/scale), 0, 2^b - 1) (an integer),
+ *    q = clamp(rint(w/scale) + zero, 0, 2^b - 1); rint is nearest-even and
+ *    every quotient an IEEE fp64 division.
+ *
+ * Activation types: x, h, y and the LoRA factors are binary16 (QMLP_F16) on
+ * the decode path (1 <= M <= 16) and bfloat16 (QMLP_BF16) on the
+ * prefill-chunk path (M a multiple of 128); accumulation is fp32.
+ */
+#ifndef QMLP_H
+#define QMLP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    QMLP_OK = 0,
+    QMLP_ERR_NULL = 1,          /* a required pointer is NULL */
+    QMLP_ERR_SHAPE = 2,         /* sizes inconsistent or not a supported multiple */
+    QMLP_ERR_ALIGN = 3,         /* a device pointer is not 16-byte aligned */
+    QMLP_ERR_UNSUPPORTED = 4,   /* bits / group / rank / M / dtype combination not built */
+    QMLP_ERR_WORKSPACE = 5,     /* workspace NULL or smaller than qmlp_workspace_bytes() */
+    QMLP_ERR_HIP = 6            /* a HIP runtime call failed (launch, attribute, device query) */
+} qmlp_status;
+
+typedef enum { QMLP_F16 = 0, QMLP_BF16 = 1 } qmlp_dtype;
+
+/* A hipStream_t passed as an opaque pointer (NULL = the null stream). */
+typedef void *qmlp_stream;
+
+/* Non-owning view of one packed quantized matrix in device memory. */
+typedef struct {
+    int32_t bits;     /* 2 (gate/up) or 4 (down) */
+    int32_t n_out;    /* rows n of the logical W [n][k] */
+    int32_t k_in;     /* columns k; groups run along k */
+    int32_t group;    /* g: 64 or 128; k_in % g == 0 */
+    void *codes;      /* qmlp_codes_bytes(bits, n_out, k_in) bytes, 16-B aligned */
+    void *meta;       /* qmlp_meta_bytes(n_out, k_in, group) bytes, 16-B aligned */
+} qmlp_qweight;
+
+/* One W4/W2-GateUp MLP block with its Recover-LoRA adapters (Sec. 3.3, 4.2). */
+typedef struct {
+    qmlp_qweight gate;      /* bits 2, [f][d] */
+    qmlp_qweight up;        /* bits 2, [f][d], same group as gate */
+    qmlp_qweight down;      /* bits 4, [d][f] */
+    const void *A_gate;     /* [rank][d] activation type (nn.Linear / PEFT "lora_A") */
+    const void *B_gate;     /* [f][rank] activation type (PEFT "lora_B")            */
+    const void *A_up;       /* [rank][d] */
+    const void *B_up;       /* [f][rank] */
+    int32_t rank;           /* r: 0 (no adapter), 8, 16 or 32 */
+    float lora_scale;       /* multiplies B A x (Eq. (1)'s alpha; PEFT: alpha/r) */
+} qmlp_mlp;
+
+/* ---------------------------------------------------------------- sizes */
+
+/* Bytes of packed codes for an [n_out][k_in] matrix at `bits` (0 if invalid). */
+size_t qmlp_codes_bytes(int bits, int n_out, int k_in);
+
+/* Bytes of (scale, zero) metadata for [n_out][k_in] at group `group` (0 if invalid). */
+size_t qmlp_meta_bytes(int n_out, int k_in, int group);
+
+/* Workspace bytes qmlp_forward / qmlp_gateup_w2_lora need for this block at
+ * M tokens (0 if the combination is unsupported).  The workspace holds the
+ * rank-r projections t = A x (fp32) and the intermediate h; its contents
+ * need no initialization and are dead after the call's kernels finish. */
+size_t qmlp_workspace_bytes(const qmlp_mlp *mlp, int M, qmlp_dtype dtype);
+
+/* ----------------------------------------------------- packing (offline) */
+
+/*
+ * Sec. 4.1 / Sec. 7 step 1: quantize fp32 W [n_out][k_in] (row-major,
+ * device) to 2-bit codes, group `group` along k_in, writing out->codes and
+ * out->meta (caller-allocated, sizes from qmlp_codes_bytes/qmlp_meta_bytes).
+ * On success out->bits/n_out/k_in/group are filled in.
+ * A group holding a non-finite weight or whose scale overflows binary16 is
+ * written as codes 0, scale NaN (0x7E00), zero 0, and bit 0 of *d_status
+ * (a device int32, may be NULL) is set with an atomic OR; the caller zeroes
+ * *d_status beforehand.  Requires k_in % 64 == 0, group in {64, 128}.
+ */
+qmlp_status qmlp_pack_w2(const float *W, int n_out, int k_in, int group,
+                         qmlp_qweight *out, int32_t *d_status, qmlp_stream stream);
+
+/* Sec. 3.3 / Sec. 7 step 4: the same at 4 bits (down projection and every
+ * other non-gate/up linear).  Requires k_in % 32 == 0, group in {64, 128}. */
+qmlp_status qmlp_pack_w4(const float *W, int n_out, int k_in, int group,
+                         qmlp_qweight *out, int32_t *d_status, qmlp_stream stream);
+
+/* ------------------------------------------------------ the hot path */
+
+/*
+ * Sec. 3.1 Eq. (1) on the gate and up projections, then the activation of
+ * the fused gate-activation-down operator (Sec. 5):
+ *   G = W2gate x + lora_scale * B_gate (A_gate x)
+ *   U = W2up   x + lora_scale * B_up   (A_up   x)
+ *   h = SiLU(G) * U = G / (1 + exp(-G)) * U
+ * x [M][d] and h [M][f] are row-major in the activation type `dtype`.
+ * ws/ws_bytes: workspace of at least qmlp_workspace_bytes(mlp, M, dtype).
+ * M == 0 enqueues nothing and returns QMLP_OK.
+ */
+qmlp_status qmlp_gateup_w2_lora(const qmlp_mlp *mlp, const void *x, int M, qmlp_dtype dtype,
+                                void *h, void *ws, size_t ws_bytes, qmlp_stream stream);
+
+/*
+ * The 4-bit down projection (Sec. 3.3): y [M][n_out] = W4down h, with
+ * h [M][k_in] and y row-major in the activation type.  No workspace.
+ */
+qmlp_status qmlp_down_w4(const qmlp_qweight *down, const void *h, int M, qmlp_dtype dtype,
+                         void *y, qmlp_stream stream);
+
+/*
+ * The whole block, y = W4down(SiLU(G) * U) (Sec. 3.3, 4.2, 5), x [M][d] ->
+ * y [M][d].  The intermediate h lives only in the workspace.
+ */
+qmlp_status qmlp_forward(const qmlp_mlp *mlp, const void *x, int M, qmlp_dtype dtype,
+                         void *y, void *ws, size_t ws_bytes, qmlp_stream stream);
+
+/* ---------------------------------------------- inspection (not timed) */
+
+/*
+ * Unpack a packed matrix into canonical form: codes uint8 [n][k] and the
+ * binary16 bits of scale and zero [n][k/g] (QDQ view, Sec. 6.3).
+ */
+qmlp_status qmlp_unpack(const qmlp_qweight *w, uint8_t *codes, uint16_t *scales,
+                        uint16_t *zeros, qmlp_stream stream);
+
+/* The dequantized weight scale * (q - zero), rounded once to binary16
+ * (nearest-even; q == zero gives +0), [n][k] row-major. */
+qmlp_status qmlp_dequant(const qmlp_qweight *w, uint16_t *w_f16, qmlp_stream stream);
+
+/* A static, human-readable name of a status code. */
+const char *qmlp_status_string(qmlp_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QMLP_H */

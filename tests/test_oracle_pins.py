@@ -1,0 +1,321 @@
+"""Pins of the fp64 oracle against facts that do not come from the oracle.
+
+The paper prints no worked example of the quantizer or of an MLP output, so
+the pins are: hand-derived worked examples (tests/golden), closed forms
+(exact reconstruction of on-grid weights), invariants (error bound, zero on
+the grid, B = 0 equals the base path), library routines (numpy's binary16
+cast, numpy fp64 matmul, scipy's expit) and brute force on small shapes.
+Each is chosen so that a plausible slip in the oracle -- a dropped zero
+point, a wrong rounding mode, a transposed LoRA factor, a missing LoRA
+term, a wrong group index -- fails at least one of them.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+from scipy.special import expit
+
+import oracle as orc
+import workloads as wl
+
+
+def _hex(s):
+    return int(s, 16)
+
+
+def _golden(golden_dir):
+    with open(os.path.join(golden_dir, "quantizer_worked_examples.json")) as fh:
+        return json.load(fh)
+
+
+# ------------------------------------------------------------- conversions
+def test_f16_to_f64_matches_numpy_on_every_pattern():
+    bits = np.arange(65536, dtype=np.uint16)
+    ref = bits.view(np.float16).astype(np.float64)
+    got = orc.act_to_f64(bits, bf16=False)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    # sign of zero survives
+    assert np.signbit(got[0x8000]) and not np.signbit(got[0])
+
+
+def test_bf16_to_f64_matches_numpy_on_every_pattern():
+    bits = np.arange(65536, dtype=np.uint16)
+    ref = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    got = orc.act_to_f64(bits, bf16=True)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+
+
+def _f64_to_f16_numpy(v):
+    return np.asarray(v, np.float64).astype(np.float16).view(np.uint16)
+
+
+def test_f64_to_f16_roundtrips_every_finite_pattern():
+    bits = np.arange(65536, dtype=np.uint16)
+    vals = bits.view(np.float16).astype(np.float64)
+    for b, v in zip(bits[::37], vals[::37]):
+        if np.isnan(v):
+            assert orc.f64_to_f16(v) == 0x7E00
+        else:
+            assert orc.f64_to_f16(v) == int(b)
+
+
+def test_f64_to_f16_midpoints_and_neighbours_match_numpy():
+    # midpoints between adjacent binary16 values, and values one fp64 ulp
+    # either side: nearest-even must decide the tie, the neighbours must not.
+    rng = np.random.default_rng(1)
+    b = rng.integers(0, 0x7BFF, size=3000).astype(np.uint16)
+    lo = b.view(np.float16).astype(np.float64)
+    hi = (b + 1).astype(np.uint16).view(np.float16).astype(np.float64)
+    mid = (lo + hi) / 2
+    cases = np.concatenate([mid, np.nextafter(mid, 0), np.nextafter(mid, np.inf),
+                            -mid, [65504.0, 65519.99, 65520.0, 65536.0, 2.0**-25,
+                                   np.nextafter(2.0**-25, 1), 2.0**-24, 3 * 2.0**-26]])
+    ref = _f64_to_f16_numpy(cases)
+    got = np.array([orc.f64_to_f16(v) for v in cases], np.uint16)
+    assert np.array_equal(got, ref)
+
+
+def test_f64_to_f16_single_rounding_not_via_f32():
+    # 1 + 2^-11 + 2^-40 lies just above a binary16 tie: a detour through
+    # binary32 drops the 2^-40 and rounds the tie to even (1.0).
+    v = 1.0 + 2.0**-11 + 2.0**-40
+    assert orc.f64_to_f16(v) == 0x3C01
+    assert int(_f64_to_f16_numpy(v)) == 0x3C01
+
+
+def test_f64_to_f16_random_doubles_match_numpy():
+    rng = np.random.default_rng(2)
+    mag = np.exp2(rng.uniform(-30, 17, size=200_000))
+    v = mag * rng.choice([-1.0, 1.0], size=mag.size)
+    ref = _f64_to_f16_numpy(v)
+    f = np.vectorize(orc.f64_to_f16, otypes=[np.uint16])
+    assert np.array_equal(f(v), ref)
+
+
+# --------------------------------------------------- quantizer worked examples
+def test_quantizer_hand_derived_examples(golden_dir):
+    for case in _golden(golden_dir)["cases"]:
+        w = np.array([[np.nan if v == "nan" else v for v in case["w"]]], np.float32)
+        q = orc.quantize(w, case["bits"], case["group"])
+        assert q.bad == (1 if case.get("invalid") else 0), case["name"]
+        assert int(q.scale[0, 0]) == _hex(case["scale"]), case["name"]
+        assert int(q.zero[0, 0]) == _hex(case["zero"]), case["name"]
+        assert q.codes[0].tolist() == case["codes"], case["name"]
+        if "w_hat_f16" in case:
+            assert [int(v) for v in q.dequant_f16()[0]] == [_hex(h) for h in case["w_hat_f16"]], case["name"]
+
+
+def test_packing_hand_written_words(golden_dir):
+    for case in _golden(golden_dir)["packing"]["cases"]:
+        codes = np.array([case["codes"]], np.uint8)
+        words = orc.pack(codes, case["bits"])
+        assert [int(v) for v in words[0]] == [_hex(h) for h in case["words"]]
+        assert np.array_equal(orc.unpack(words, codes.shape[1], case["bits"]), codes)
+
+
+@pytest.mark.parametrize("bits", [2, 4])
+def test_pack_unpack_roundtrip(bits):
+    rng = np.random.default_rng(3)
+    codes = rng.integers(0, 1 << bits, size=(37, 256), dtype=np.uint8)
+    words = orc.pack(codes, bits)
+    assert words.shape == (37, 256 * bits // 32)
+    assert np.array_equal(orc.unpack(words, 256, bits), codes)
+    # the bit pattern, independently: reassemble words with numpy shifts
+    per = 32 // bits
+    c = codes.reshape(37, -1, per).astype(np.uint64)
+    ref = np.sum(c << (bits * np.arange(per, dtype=np.uint64)), axis=2).astype(np.uint32)
+    assert np.array_equal(words, ref)
+
+
+def test_meta_interleave_is_scale_then_zero():
+    s = np.array([[0x3C00, 0x1234]], np.uint16)
+    z = np.array([[0x4000, 0x0000]], np.uint16)
+    assert orc.meta_interleave(s, z).reshape(-1).tolist() == [0x3C00, 0x4000, 0x1234, 0x0000]
+
+
+# ------------------------------------------------------ quantizer closed forms
+@pytest.mark.parametrize("bits,group", [(2, 64), (2, 128), (4, 64), (4, 128)])
+def test_on_grid_weights_reconstruct_exactly(bits, group):
+    """Weights w = s (q - z) with s binary16, integer z, and both 0 and qmax
+    present in every group reconstruct exactly: hi - lo = s*qmax exactly, so
+    the quantizer recovers s, z and q, and w_hat == w bit for bit."""
+    qmax = (1 << bits) - 1
+    rng = np.random.default_rng(4 + bits)
+    n, k = 24, 4 * group
+    ng = k // group
+    s = np.exp2(rng.uniform(-20, 4, size=(n, ng))).astype(np.float16).astype(np.float64)
+    z = rng.integers(0, qmax + 1, size=(n, ng))
+    q = rng.integers(0, qmax + 1, size=(n, k))
+    q[:, ::group] = 0
+    q[:, 1::group] = qmax
+    w = (np.repeat(s, group, axis=1) * (q - np.repeat(z, group, axis=1))).astype(np.float32)
+    assert np.array_equal(w.astype(np.float64),
+                          np.repeat(s, group, axis=1) * (q - np.repeat(z, group, axis=1)))
+    qt = orc.quantize(w, bits, group)
+    assert qt.bad == 0
+    assert np.array_equal(qt.scale.view(np.float16).astype(np.float64), s)
+    assert np.array_equal(qt.zero.view(np.float16).astype(np.float64), z.astype(np.float64))
+    assert np.array_equal(qt.codes, q.astype(np.uint8))
+    assert np.array_equal(qt.dequant(), w.astype(np.float64))
+    # binary16 image: numpy's cast of the exact value
+    assert np.array_equal(qt.dequant_f16(), _f64_to_f16_numpy(w.astype(np.float64)))
+
+
+@pytest.mark.parametrize("bits,group,outliers", [(2, 64, False), (2, 128, True), (4, 128, False),
+                                                 (4, 64, True)])
+def test_error_bound_and_zero_on_grid(bits, group, outliers):
+    """|w - w_hat| <= s16/2 + qmax |s - s16| for every weight, with s the exact
+    fp64 range/qmax computed here by numpy; zero weights dequantize to 0."""
+    qmax = (1 << bits) - 1
+    rng = np.random.default_rng(7)
+    w = (0.02 * rng.standard_normal((64, 8 * group))).astype(np.float32)
+    if outliers:
+        idx = rng.choice(w.size, size=w.size // 200, replace=False)
+        w.reshape(-1)[idx] = np.float32(0.5) * rng.choice([-1, 1], size=idx.size)
+    w[:, 3] = 0.0
+    qt = orc.quantize(w, bits, group)
+    wd = w.astype(np.float64).reshape(64, -1, group)
+    lo = np.minimum(0.0, wd.min(axis=2))
+    hi = np.maximum(0.0, wd.max(axis=2))
+    s = (hi - lo) / qmax
+    s16 = qt.scale.view(np.float16).astype(np.float64)
+    bound = s16 / 2 + qmax * np.abs(s - s16)
+    err = np.abs(qt.dequant().reshape(64, -1, group) - wd)
+    assert np.all(err <= bound[:, :, None] * (1 + 1e-12))
+    assert np.all(qt.dequant()[:, 3] == 0.0)
+    # scales are the nearest binary16 of the range
+    assert np.array_equal(qt.scale, _f64_to_f16_numpy(s))
+
+
+def test_quantizer_is_per_row_and_per_group():
+    """Scaling one group must change only that group's outputs (group index
+    and row index are not mixed)."""
+    rng = np.random.default_rng(8)
+    w = (0.02 * rng.standard_normal((4, 256))).astype(np.float32)
+    a = orc.quantize(w, 2, 64)
+    w2 = w.copy()
+    w2[2, 64:128] *= 4
+    b = orc.quantize(w2, 2, 64)
+    diff_s = a.scale != b.scale
+    assert diff_s[2, 1] and diff_s.sum() == 1
+    assert np.array_equal(a.codes[:, :64], b.codes[:, :64])
+    assert np.array_equal(a.codes[:2], b.codes[:2])
+
+
+# ------------------------------------------------------------ forward pins
+def _small_cfg(**kw):
+    base = dict(name="pin", M=3, d=256, f=384, g=64, r=8, L=1)
+    base.update(kw)
+    return wl.Config(**base)
+
+
+def _numpy_forward(cfg, layer, qg, qu, qd, lora_scale=1.0):
+    """Brute force with numpy: dense fp64 matmuls over dequantized weights
+    rebuilt here from codes/scale/zero, SiLU via scipy's expit."""
+    def deq(q):
+        s = q.scale.view(np.float16).astype(np.float64)
+        z = q.zero.view(np.float16).astype(np.float64)
+        return (q.codes.astype(np.float64) - np.repeat(z, q.group, axis=1)) * np.repeat(s, q.group, axis=1)
+    act = orc.act_to_f64
+    x = act(layer.x, cfg.bf16)
+    Ag, Bg, Au, Bu = (act(a, cfg.bf16) for a in (layer.A_gate, layer.B_gate, layer.A_up, layer.B_up))
+    G = x @ deq(qg).T + lora_scale * (x @ Ag.T) @ Bg.T
+    U = x @ deq(qu).T + lora_scale * (x @ Au.T) @ Bu.T
+    h = G * expit(G) * U
+    return h @ deq(qd).T, h
+
+
+@pytest.mark.parametrize("cfgkw", [dict(), dict(M=1, d=512, f=1536, g=64, r=8),
+                                   dict(M=5, g=128, r=16), dict(act="bf16", M=4, r=32)])
+def test_forward_matches_numpy_brute_force(cfgkw):
+    cfg = _small_cfg(**cfgkw)
+    L = wl.layer(cfg, 0)
+    qg = orc.quantize(L.W_gate, 2, cfg.g)
+    qu = orc.quantize(L.W_up, 2, cfg.g)
+    qd = orc.quantize(L.W_down, 4, cfg.g)
+    y, h = orc.forward(qg, qu, qd, L.A_gate, L.B_gate, L.A_up, L.B_up, L.x,
+                       lora_scale=0.75, bf16=cfg.bf16, return_h=True)
+    y_ref, h_ref = _numpy_forward(cfg, L, qg, qu, qd, lora_scale=0.75)
+    assert orc.max_rel_err(h, h_ref) < 1e-12
+    assert orc.max_rel_err(y, y_ref) < 1e-12
+    # the down-only entry on the same intermediate
+    assert orc.max_rel_err(orc.down(qd, h), y_ref) < 1e-12
+
+
+def test_lora_a_matches_numpy():
+    cfg = _small_cfg()
+    L = wl.layer(cfg, 1)
+    t = orc.lora_a(L.A_gate, L.x)
+    ref = orc.act_to_f64(L.x, False) @ orc.act_to_f64(L.A_gate, False).T
+    assert orc.max_rel_err(t, ref) < 1e-13
+
+
+def test_zero_B_equals_base_path_exactly():
+    cfg = _small_cfg(M=2)
+    L = wl.layer(cfg, 2)
+    qg, qu, qd = (orc.quantize(L.W_gate, 2, 64), orc.quantize(L.W_up, 2, 64),
+                  orc.quantize(L.W_down, 4, 64))
+    zB = np.zeros_like(L.B_gate)
+    y0 = orc.forward(qg, qu, qd, L.A_gate, zB, L.A_up, zB, L.x)
+    y_norank = orc.forward(qg, qu, qd, None, None, None, None, L.x)
+    y_noscale = orc.forward(qg, qu, qd, L.A_gate, L.B_gate, L.A_up, L.B_up, L.x, lora_scale=0.0)
+    assert np.array_equal(y0, y_norank)
+    assert np.array_equal(y0, y_noscale)
+    # and the adapters do matter when present
+    y1 = orc.forward(qg, qu, qd, L.A_gate, L.B_gate, L.A_up, L.B_up, L.x)
+    assert not np.array_equal(y0, y1)
+
+
+def test_lora_only_path_when_base_weights_are_zero():
+    """W = 0 quantizes to s16 = 1, z = 0, q = 0, so G and U are the pure
+    low-rank terms: h = SiLU(s B_g A_g x) * (s B_u A_u x)."""
+    cfg = _small_cfg(M=2)
+    L = wl.layer(cfg, 3)
+    zero = np.zeros_like(L.W_gate)
+    qg, qu = orc.quantize(zero, 2, 64), orc.quantize(zero, 2, 64)
+    assert np.all(qg.scale == 0x3C00) and np.all(qg.zero == 0) and not qg.codes.any()
+    Bg = wl.to_act_bits(np.random.default_rng(9).normal(0, 0.05, L.B_gate.shape), "f16")
+    h = orc.gateup(qg, qu, L.A_gate, Bg, L.A_up, L.B_up, L.x, lora_scale=2.0)
+    x = orc.act_to_f64(L.x, False)
+    G = 2.0 * (x @ orc.act_to_f64(L.A_gate, False).T) @ orc.act_to_f64(Bg, False).T
+    U = 2.0 * (x @ orc.act_to_f64(L.A_up, False).T) @ orc.act_to_f64(L.B_up, False).T
+    assert orc.max_rel_err(h, G * expit(G) * U) < 1e-12
+
+
+def test_low_rank_equals_merged_dense_update():
+    """B (A x) == (B A) x: the unmerged adapter is the rank-r dense update."""
+    cfg = _small_cfg(M=2)
+    L = wl.layer(cfg, 4)
+    qg, qu = orc.quantize(L.W_gate, 2, 64), orc.quantize(L.W_up, 2, 64)
+    h, G, U = orc.gateup(qg, qu, L.A_gate, L.B_gate, L.A_up, L.B_up, L.x, return_gu=True)
+    x = orc.act_to_f64(L.x, False)
+    dense_g = qg.dequant() + orc.act_to_f64(L.B_gate, False) @ orc.act_to_f64(L.A_gate, False)
+    dense_u = qu.dequant() + orc.act_to_f64(L.B_up, False) @ orc.act_to_f64(L.A_up, False)
+    assert orc.max_rel_err(G, x @ dense_g.T) < 1e-12
+    assert orc.max_rel_err(U, x @ dense_u.T) < 1e-12
+
+
+def test_silu_is_v_times_sigmoid():
+    # a 1x... block whose gate output is known: W_up chosen so U == 1
+    # exactly is awkward with 2-bit weights, so check SiLU through G and h/U.
+    cfg = _small_cfg(M=4)
+    L = wl.layer(cfg, 5)
+    qg, qu = orc.quantize(L.W_gate, 2, 64), orc.quantize(L.W_up, 2, 64)
+    h, G, U = orc.gateup(qg, qu, L.A_gate, L.B_gate, L.A_up, L.B_up, L.x, return_gu=True)
+    assert orc.max_rel_err(h, G * expit(G) * U) < 1e-13
+
+
+def test_rows_are_independent_tokens():
+    cfg = _small_cfg(M=4)
+    L = wl.layer(cfg, 6)
+    qg, qu, qd = (orc.quantize(L.W_gate, 2, 64), orc.quantize(L.W_up, 2, 64),
+                  orc.quantize(L.W_down, 4, 64))
+    y = orc.forward(qg, qu, qd, L.A_gate, L.B_gate, L.A_up, L.B_up, L.x)
+    for m in range(4):
+        ym = orc.forward(qg, qu, qd, L.A_gate, L.B_gate, L.A_up, L.B_up, L.x[m:m + 1])
+        assert np.array_equal(ym[0], y[m])
