@@ -1,0 +1,303 @@
+#!/usr/bin/env python3
+"""Benchmark of the W4/W2-GateUp decode MLP on one MI355X.
+
+A step is one pass over the layer stack of the Qwen3-4B-shaped workload
+(d=2560, f=9728, 2-bit gate/up and 4-bit down at group 128, LoRA rank 16,
+M=1 token, 36 independently seeded layers run back to back, one forward per
+layer on one stream).  Inputs are packed and resident in HBM before the
+timed region.  Prints one JSON line:
+
+  value    = achieved HBM GB/s = L * B(M) / t_step, where B(M) are the
+             algorithmic bytes of one MLP step (packed codes + fp16
+             scale/zero + LoRA factors + x in + y out; the intermediate h
+             excluded, as the fused gate-activation-down keeps it on-chip);
+  roofline = the dominant kernel's algorithmic bytes per launch over its
+             average launch duration (HIP events on the launch stream);
+  cpu_baseline = the fp64 oracle timed on a bounded sample of the same
+             stack on this host (reported baseline only).
+"""
+from __future__ import annotations
+
+import argparse
+import concurrent.futures
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads as wl  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
+METRIC = BASE_METRIC = ("achieved HBM GB/s (% of MI355X peak) and µs per W4/W2-GateUp MLP "
+                        "decode step")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+# --------------------------------------------------------------------- stack
+class Stack:
+    def __init__(self, cfg, mlps, xs, ys, ws):
+        self.cfg, self.mlps, self.xs, self.ys, self.ws = cfg, mlps, xs, ys, ws
+
+
+def _gen_layer(cfg, i, seed):
+    return wl.layer(cfg, i, seed)
+
+
+def build_stack(cfg: wl.Config, seed: int = 0, layers: int | None = None, threads: int = 16) -> Stack:
+    """Generate the seeded layers on the host (parallel), pack them on the GPU."""
+    import torch
+    import paper_2606_04238_amd as q
+    L = cfg.L if layers is None else layers
+    mlps, xs, ys = [], [], []
+    t0 = time.time()
+    with concurrent.futures.ThreadPoolExecutor(max_workers=threads) as ex:
+        futs = [ex.submit(_gen_layer, cfg, i, seed) for i in range(L)]
+        for fut in futs:
+            lay = fut.result()
+            dt = torch.bfloat16 if cfg.bf16 else torch.float16
+
+            def act(a):
+                return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(dt).cuda()
+            g = q.pack_w2(torch.from_numpy(lay.W_gate).cuda(), cfg.g)
+            u = q.pack_w2(torch.from_numpy(lay.W_up).cuda(), cfg.g)
+            d = q.pack_w4(torch.from_numpy(lay.W_down).cuda(), cfg.g)
+            mlps.append(q.MLP(g, u, d, act(lay.A_gate), act(lay.B_gate), act(lay.A_up),
+                              act(lay.B_up), lora_scale=cfg.lora_scale))
+            xs.append(act(lay.x))
+            ys.append(torch.empty((cfg.M, cfg.d), dtype=dt, device="cuda"))
+            fut._result = None          # drop the fp32 host copies
+    torch.cuda.synchronize()
+    for m in mlps:
+        for w in (m.gate, m.up, m.down):
+            if w.invalid_groups():
+                raise RuntimeError("packer flagged invalid groups")
+    ws = q.workspace(mlps[0], cfg.M, ys[0].dtype)
+    log("built %d layers in %.1f s" % (L, time.time() - t0))
+    return Stack(cfg, mlps, xs, ys, ws)
+
+
+def run_stack_once(stack: Stack):
+    import paper_2606_04238_amd as q
+    for m, x, y in zip(stack.mlps, stack.xs, stack.ys):
+        q.forward(m, x, y=y, ws=stack.ws)
+    return stack.ys
+
+
+# --------------------------------------------------------------------- timing
+def time_passes(fn, steps: int, warmup: int):
+    """Per-pass durations (ms) with HIP events on the current stream."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    t0 = time.perf_counter()
+    evs[0].record(st)
+    for i in range(steps):
+        fn()
+        evs[i + 1].record(st)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)], wall
+
+
+def kernel_durations(stack: Stack, passes: int = 5):
+    """Average launch duration (us) of the layer's kernels, each bracketed by
+    events on the launch stream.  With the one-kernel-per-layer forward that
+    is the fused kernel; otherwise the gate/up half (LoRA-A + fused gate/up)
+    and the 4-bit down kernel are bracketed separately."""
+    import torch
+    import paper_2606_04238_amd as q
+    st = torch.cuda.current_stream()
+    fused = q.forward_launches(stack.mlps[0], stack.cfg.M) == 1
+    h = torch.empty((stack.cfg.M, stack.cfg.f), dtype=stack.ys[0].dtype, device="cuda")
+    a, b = [], []
+    for _ in range(passes):
+        marks = []
+        for m, x, y in zip(stack.mlps, stack.xs, stack.ys):
+            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            e0.record(st)
+            if fused:
+                q.forward(m, x, y=y, ws=stack.ws)
+                e1.record(st)
+                e2.record(st)
+            else:
+                q.gateup_w2_lora(m, x, h=h, ws=stack.ws)
+                e1.record(st)
+                q.down_w4(m.down, h, y=y)
+                e2.record(st)
+            marks.append((e0, e1, e2))
+        torch.cuda.synchronize()
+        for e0, e1, e2 in marks:
+            a.append(e0.elapsed_time(e1) * 1e3)
+            b.append(e1.elapsed_time(e2) * 1e3)
+    return fused, statistics.mean(a), statistics.mean(b)
+
+
+def kernel_bytes(cfg: wl.Config):
+    """Algorithmic bytes per launch of each half (each includes the h it writes/reads)."""
+    M, d, f, g, r = cfg.M, cfg.d, cfg.f, cfg.g, cfg.r
+    gateup = f * d // 2 + 8 * f * d // g + 4 * r * (d + f) + 2 * M * d + 2 * M * f
+    down = d * f // 2 + 4 * d * f // g + 2 * M * f + 2 * M * d
+    return gateup, down
+
+
+# --------------------------------------------------------------------- cpu baseline
+def cpu_baseline(cfg: wl.Config, seed: int, budget_s: float = 12.0, max_layers: int | None = None):
+    """The fp64 oracle forward (single thread) over the first layers of the
+    same stack until ~budget_s of CPU time; quantization is untimed."""
+    import oracle as orc
+    L = cfg.L if max_layers is None else max_layers
+    total_t, n = 0.0, 0
+    for i in range(L):
+        lay = wl.layer(cfg, i, seed)
+        qg, qu, qd = (orc.quantize(lay.W_gate, 2, cfg.g), orc.quantize(lay.W_up, 2, cfg.g),
+                      orc.quantize(lay.W_down, 4, cfg.g))
+        t0 = time.perf_counter()
+        orc.forward(qg, qu, qd, lay.A_gate, lay.B_gate, lay.A_up, lay.B_up, lay.x,
+                    lora_scale=cfg.lora_scale, bf16=cfg.bf16)
+        total_t += time.perf_counter() - t0
+        n += 1
+        if total_t >= budget_s:
+            break
+    gbs = n * cfg.alg_bytes() / total_t / 1e9
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "oracle forward (fp64, one thread) over layers 0..%d of the %d-layer stack, "
+                      "%.2f s; quantization untimed; us per MLP step %.0f" % (n - 1, cfg.L, total_t,
+                                                                            total_t / n * 1e6)}
+
+
+def parity_layer0(stack: Stack, seed: int):
+    import oracle as orc
+    cfg = stack.cfg
+    lay = wl.layer(cfg, 0, seed)
+    qg, qu, qd = (orc.quantize(lay.W_gate, 2, cfg.g), orc.quantize(lay.W_up, 2, cfg.g),
+                  orc.quantize(lay.W_down, 4, cfg.g))
+    y_ref = orc.forward(qg, qu, qd, lay.A_gate, lay.B_gate, lay.A_up, lay.B_up, lay.x,
+                        lora_scale=cfg.lora_scale, bf16=cfg.bf16)
+    import torch
+    bits = stack.ys[0].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    return orc.max_rel_err(orc.act_to_f64(bits, cfg.bf16), y_ref)
+
+
+# --------------------------------------------------------------------- main
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="qwen3_4b", choices=sorted(wl.CONFIGS))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--mode", default="graph", choices=["graph", "eager"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this library's decode MLP runs on a single "
+              "MI355X (data-parallel scale-out needs no communication); run with --gpus 1.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2606_04238_amd as q
+    q.library()
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        return 2
+    cfg = wl.CONFIGS[args.config]
+    if cfg.M > 16:
+        print("the prefill-chunk path is not part of this build", file=sys.stderr)
+        return 2
+    stack = build_stack(cfg, args.seed)
+
+    # eager timing
+    eager_ms, _ = time_passes(lambda: run_stack_once(stack), args.steps, args.warmup)
+    # graph timing: the whole stack captured once, replayed per step
+    graph_ms = None
+    if args.mode == "graph":
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            run_stack_once(stack)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=s):
+                run_stack_once(stack)
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        graph_ms, wall = time_passes(g.replay, args.steps, args.warmup)
+    head = graph_ms if graph_ms is not None else eager_ms
+    t_step = statistics.median(head)
+    L = cfg.L
+    B = cfg.alg_bytes()
+    gbs = L * B / (t_step * 1e-3) / 1e9
+    us_layer = t_step * 1e3 / L
+
+    fused, k1_us, k2_us = kernel_durations(stack)
+    if fused:
+        dom_name, dom_us, dom_b = "fused_layer_kernel (whole MLP step)", k1_us, B
+        kernel_us = {"fused_layer": round(k1_us, 3)}
+    else:
+        gu_b, dn_b = kernel_bytes(cfg)
+        kernel_us = {"gateup_half": round(k1_us, 3), "down_w4": round(k2_us, 3)}
+        dom_name, dom_us, dom_b = ("gateup_w2 (LoRA-A + fused gate/up)", k1_us, gu_b) \
+            if k1_us >= k2_us else ("down_w4", k2_us, dn_b)
+    achieved = dom_b / (dom_us * 1e-6) / 1e9
+    err0 = parity_layer0(stack, args.seed)
+
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s decode MLP stack: M=%d, d=%d, f=%d, group %d, LoRA rank %d, %d layers"
+                        % (cfg.name, cfg.M, cfg.d, cfg.f, cfg.g, cfg.r, L),
+            "us_per_mlp_step": round(us_layer, 3),
+            "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+            "alg_bytes_per_mlp_step": B,
+            "mode": "hip_graph" if graph_ms is not None else "eager",
+            "eager_us_per_mlp_step": round(statistics.median(eager_ms) * 1e3 / L, 3),
+            "p10_p90_ms_per_step": [round(float(np.percentile(head, 10)), 4),
+                                    round(float(np.percentile(head, 90)), 4)],
+            "kernel_us": kernel_us,
+            "launches_per_layer": q.forward_launches(stack.mlps[0], cfg.M),
+            "parity_layer0_max_rel_err": float("%.3e" % err0),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": dom_name,
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, args.seed)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -108,9 +108,15 @@ size_t qmlp_codes_bytes(int bits, int n_out, int k_in);
 size_t qmlp_meta_bytes(int n_out, int k_in, int group);
 
 /* Workspace bytes qmlp_forward / qmlp_gateup_w2_lora need for this block at
- * M tokens (0 if the combination is unsupported).  The workspace holds the
- * rank-r projections t = A x (fp32) and the intermediate h; its contents
- * need no initialization and are dead after the call's kernels finish. */
+ * M tokens (0 if the combination is unsupported).  Layout: 256 bytes of
+ * control words (uint32: [0] LoRA-A rows published, [1] blocks whose h is
+ * published, [2] blocks done, [3] sticky error bits: 1 = LoRA-A wait timed
+ * out, 2 = h wait timed out), then t = A x (fp32 [M][2r]), then h
+ * (activation type [M][f]).  The control words must be ZERO before the
+ * first call on a workspace; every completed call leaves them zero.  After
+ * an error bit appears the results of that call are invalid and the caller
+ * must zero the control words again.  One workspace serves one call at a
+ * time: calls that overlap in time on the same workspace race. */
 size_t qmlp_workspace_bytes(const qmlp_mlp *mlp, int M, qmlp_dtype dtype);
 
 /* ----------------------------------------------------- packing (offline) */
@@ -174,6 +180,12 @@ qmlp_status qmlp_unpack(const qmlp_qweight *w, uint8_t *codes, uint16_t *scales,
 /* The dequantized weight scale * (q - zero), rounded once to binary16
  * (nearest-even; q == zero gives +0), [n][k] row-major. */
 qmlp_status qmlp_dequant(const qmlp_qweight *w, uint16_t *w_f16, qmlp_stream stream);
+
+/* Number of kernel launches qmlp_forward makes for this block at M tokens:
+ * 1 when the whole layer runs as one fused kernel (the decode shapes it
+ * covers), 2 or 3 when it runs as the LoRA-A, gate/up and down kernels in
+ * stream order, 0 if the call would be rejected.  Host-only, enqueues nothing. */
+int qmlp_forward_launches(const qmlp_mlp *mlp, int M, qmlp_dtype dtype);
 
 /* A static, human-readable name of a status code. */
 const char *qmlp_status_string(qmlp_status s);

@@ -1,0 +1,324 @@
+// C ABI of libqmlp: argument validation, workspace layout and kernel dispatch.
+// Every check runs before the first launch, so a rejected call enqueues
+// nothing and writes nothing.
+#include <stddef.h>
+#include <stdint.h>
+
+#include "qmlp.h"
+#include "qmlp_internal.h"
+
+namespace {
+
+using namespace qmlp;
+
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+inline size_t round256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+qmlp_status from_hip(hipError_t e) { return e == hipSuccess ? QMLP_OK : QMLP_ERR_HIP; }
+
+// Structural checks of one packed-weight view.
+qmlp_status check_qweight(const qmlp_qweight* w, int bits) {
+    if (!w || !w->codes || !w->meta)
+        return QMLP_ERR_NULL;
+    if (w->bits != bits)
+        return QMLP_ERR_UNSUPPORTED;
+    if (w->n_out <= 0 || w->k_in <= 0)
+        return QMLP_ERR_SHAPE;
+    if (w->group != 64 && w->group != 128)
+        return QMLP_ERR_UNSUPPORTED;
+    if (w->k_in % w->group != 0)
+        return QMLP_ERR_SHAPE;
+    if (!aligned16(w->codes) || !aligned16(w->meta))
+        return QMLP_ERR_ALIGN;
+    return QMLP_OK;
+}
+
+// Shape, pointer and type checks of a whole block at M tokens.
+qmlp_status check_mlp(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
+    if (!mlp)
+        return QMLP_ERR_NULL;
+    qmlp_status s;
+    if ((s = check_qweight(&mlp->gate, 2)) != QMLP_OK) return s;
+    if ((s = check_qweight(&mlp->up, 2)) != QMLP_OK) return s;
+    if ((s = check_qweight(&mlp->down, 4)) != QMLP_OK) return s;
+    const int f = mlp->gate.n_out, d = mlp->gate.k_in;
+    if (mlp->up.n_out != f || mlp->up.k_in != d || mlp->down.n_out != d || mlp->down.k_in != f)
+        return QMLP_ERR_SHAPE;
+    if (mlp->up.group != mlp->gate.group)
+        return QMLP_ERR_SHAPE;
+    if (d % 64 != 0 || f % 64 != 0)
+        return QMLP_ERR_SHAPE;
+    if (mlp->rank != 0 && mlp->rank != 8 && mlp->rank != 16 && mlp->rank != 32)
+        return QMLP_ERR_UNSUPPORTED;
+    if (mlp->rank > 0) {
+        if (!mlp->A_gate || !mlp->B_gate || !mlp->A_up || !mlp->B_up)
+            return QMLP_ERR_NULL;
+        if (!aligned16(mlp->A_gate) || !aligned16(mlp->B_gate) || !aligned16(mlp->A_up) ||
+            !aligned16(mlp->B_up))
+            return QMLP_ERR_ALIGN;
+    }
+    if (M < 0)
+        return QMLP_ERR_SHAPE;
+    if (M > 16)
+        return QMLP_ERR_UNSUPPORTED;             // prefill-chunk path: not in this build
+    if (dtype != QMLP_F16)
+        return QMLP_ERR_UNSUPPORTED;             // decode runs in binary16
+    if (!decode_shape_supported(d, f))
+        return QMLP_ERR_UNSUPPORTED;
+    return QMLP_OK;
+}
+
+// Workspace: [control words, 256 B][t: M x 2r fp32][h: M x f binary16].
+constexpr size_t kCtlBytes = 256;
+
+struct Workspace {
+    unsigned* ctl;
+    float* t;
+    uint16_t* h;
+};
+
+size_t ws_t_bytes(const qmlp_mlp* mlp, int M) { return round256((size_t)M * 2 * mlp->rank * 4); }
+size_t ws_h_bytes(const qmlp_mlp* mlp, int M) { return round256((size_t)M * mlp->gate.n_out * 2); }
+
+Workspace carve(const qmlp_mlp* mlp, int M, void* ws) {
+    char* base = static_cast<char*>(ws);
+    return {reinterpret_cast<unsigned*>(base), reinterpret_cast<float*>(base + kCtlBytes),
+            reinterpret_cast<uint16_t*>(base + kCtlBytes + ws_t_bytes(mlp, M))};
+}
+
+GateUpArgs gateup_args(const qmlp_mlp* mlp, const void* x, int M, uint16_t* h, const float* t) {
+    GateUpArgs a;
+    a.cg = static_cast<const uint32_t*>(mlp->gate.codes);
+    a.mg = static_cast<const uint32_t*>(mlp->gate.meta);
+    a.cu = static_cast<const uint32_t*>(mlp->up.codes);
+    a.mu = static_cast<const uint32_t*>(mlp->up.meta);
+    // With rank 0 the kernels still issue (unused) loads of the LoRA-B
+    // slices; point them at x, which is always readable.
+    a.Bg = static_cast<const uint16_t*>(mlp->rank > 0 ? mlp->B_gate : x);
+    a.Bu = static_cast<const uint16_t*>(mlp->rank > 0 ? mlp->B_up : x);
+    a.t = t;
+    a.x = static_cast<const uint16_t*>(x);
+    a.h = h;
+    a.M = M;
+    a.d = mlp->gate.k_in;
+    a.f = mlp->gate.n_out;
+    a.g = mlp->gate.group;
+    a.r = mlp->rank;
+    a.uc = 0;
+    a.lora_scale = mlp->lora_scale;
+    return a;
+}
+
+DownArgs down_args(const qmlp_qweight* down, const void* h, int M, void* y) {
+    DownArgs a;
+    a.cd = static_cast<const uint32_t*>(down->codes);
+    a.md = static_cast<const uint32_t*>(down->meta);
+    a.h = static_cast<const uint16_t*>(h);
+    a.y = static_cast<uint16_t*>(y);
+    a.M = M;
+    a.d = down->n_out;
+    a.f = down->k_in;
+    a.g = down->group;
+    a.uc = 0;
+    return a;
+}
+
+// The gate/up half: LoRA-A projection then the fused kernel.
+qmlp_status run_gateup(const qmlp_mlp* mlp, const void* x, int M, uint16_t* h, float* t,
+                       hipStream_t st) {
+    if (mlp->rank > 0) {
+        hipError_t e = launch_lora_a(static_cast<const uint16_t*>(mlp->A_gate),
+                                     static_cast<const uint16_t*>(mlp->A_up),
+                                     static_cast<const uint16_t*>(x), M, mlp->gate.k_in,
+                                     mlp->rank, t, st);
+        if (e != hipSuccess)
+            return QMLP_ERR_HIP;
+    }
+    return from_hip(launch_gateup(gateup_args(mlp, x, M, h, t), st));
+}
+
+qmlp_status pack_common(int bits, const float* W, int n_out, int k_in, int group,
+                        qmlp_qweight* out, int32_t* d_status, qmlp_stream stream) {
+    if (!W || !out || !out->codes || !out->meta)
+        return QMLP_ERR_NULL;
+    if (n_out <= 0 || k_in <= 0)
+        return QMLP_ERR_SHAPE;
+    if (group != 64 && group != 128)
+        return QMLP_ERR_UNSUPPORTED;
+    if (k_in % group != 0)
+        return QMLP_ERR_SHAPE;
+    if (!aligned16(W) || !aligned16(out->codes) || !aligned16(out->meta))
+        return QMLP_ERR_ALIGN;
+    if (d_status && ((uintptr_t)d_status & 3u))
+        return QMLP_ERR_ALIGN;
+    hipError_t e = launch_pack(bits, W, n_out, k_in, group, static_cast<uint32_t*>(out->codes),
+                               static_cast<uint32_t*>(out->meta), d_status,
+                               static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return QMLP_ERR_HIP;
+    out->bits = bits;
+    out->n_out = n_out;
+    out->k_in = k_in;
+    out->group = group;
+    return QMLP_OK;
+}
+
+qmlp_status check_inspect(const qmlp_qweight* w) {
+    if (!w)
+        return QMLP_ERR_NULL;
+    if (w->bits != 2 && w->bits != 4)
+        return QMLP_ERR_UNSUPPORTED;
+    return check_qweight(w, w->bits);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t qmlp_codes_bytes(int bits, int n_out, int k_in) {
+    if ((bits != 2 && bits != 4) || n_out <= 0 || k_in <= 0 || k_in % (32 / bits) != 0)
+        return 0;
+    return (size_t)n_out * (size_t)k_in * (size_t)bits / 8;
+}
+
+size_t qmlp_meta_bytes(int n_out, int k_in, int group) {
+    if (n_out <= 0 || k_in <= 0 || group <= 0 || k_in % group != 0)
+        return 0;
+    return (size_t)n_out * (size_t)(k_in / group) * 4;
+}
+
+size_t qmlp_workspace_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
+    if (check_mlp(mlp, M, dtype) != QMLP_OK)
+        return 0;
+    if (M == 0)
+        return 0;
+    return kCtlBytes + ws_t_bytes(mlp, M) + ws_h_bytes(mlp, M);
+}
+
+qmlp_status qmlp_pack_w2(const float* W, int n_out, int k_in, int group, qmlp_qweight* out,
+                         int32_t* d_status, qmlp_stream stream) {
+    return pack_common(2, W, n_out, k_in, group, out, d_status, stream);
+}
+
+qmlp_status qmlp_pack_w4(const float* W, int n_out, int k_in, int group, qmlp_qweight* out,
+                         int32_t* d_status, qmlp_stream stream) {
+    return pack_common(4, W, n_out, k_in, group, out, d_status, stream);
+}
+
+qmlp_status qmlp_gateup_w2_lora(const qmlp_mlp* mlp, const void* x, int M, qmlp_dtype dtype,
+                                void* h, void* ws, size_t ws_bytes, qmlp_stream stream) {
+    qmlp_status s = check_mlp(mlp, M, dtype);
+    if (s != QMLP_OK)
+        return s;
+    if (M == 0)
+        return QMLP_OK;
+    if (!x || !h)
+        return QMLP_ERR_NULL;
+    if (!aligned16(x) || !aligned16(h))
+        return QMLP_ERR_ALIGN;
+    if (!ws || ws_bytes < qmlp_workspace_bytes(mlp, M, dtype))
+        return QMLP_ERR_WORKSPACE;
+    if (!aligned16(ws))
+        return QMLP_ERR_ALIGN;
+    Workspace w = carve(mlp, M, ws);
+    return run_gateup(mlp, x, M, static_cast<uint16_t*>(h), w.t, static_cast<hipStream_t>(stream));
+}
+
+qmlp_status qmlp_down_w4(const qmlp_qweight* down, const void* h, int M, qmlp_dtype dtype,
+                         void* y, qmlp_stream stream) {
+    qmlp_status s = check_qweight(down, 4);
+    if (s != QMLP_OK)
+        return s;
+    if (down->k_in % 64 != 0 || down->n_out % 64 != 0)
+        return QMLP_ERR_SHAPE;
+    if (M < 0)
+        return QMLP_ERR_SHAPE;
+    if (M > 16 || dtype != QMLP_F16 || !decode_shape_supported(down->n_out, down->k_in))
+        return QMLP_ERR_UNSUPPORTED;
+    if (M == 0)
+        return QMLP_OK;
+    if (!h || !y)
+        return QMLP_ERR_NULL;
+    if (!aligned16(h) || !aligned16(y))
+        return QMLP_ERR_ALIGN;
+    return from_hip(launch_down(down_args(down, h, M, y), static_cast<hipStream_t>(stream)));
+}
+
+qmlp_status qmlp_forward(const qmlp_mlp* mlp, const void* x, int M, qmlp_dtype dtype, void* y,
+                         void* ws, size_t ws_bytes, qmlp_stream stream) {
+    qmlp_status s = check_mlp(mlp, M, dtype);
+    if (s != QMLP_OK)
+        return s;
+    if (M == 0)
+        return QMLP_OK;
+    if (!x || !y)
+        return QMLP_ERR_NULL;
+    if (!aligned16(x) || !aligned16(y))
+        return QMLP_ERR_ALIGN;
+    if (!ws || ws_bytes < qmlp_workspace_bytes(mlp, M, dtype))
+        return QMLP_ERR_WORKSPACE;
+    if (!aligned16(ws))
+        return QMLP_ERR_ALIGN;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    Workspace w = carve(mlp, M, ws);
+    if (fused_supported(M, mlp->gate.k_in, mlp->gate.n_out, mlp->gate.group, mlp->rank))
+        return from_hip(launch_fused(gateup_args(mlp, x, M, w.h, w.t),
+                                     down_args(&mlp->down, w.h, M, y),
+                                     static_cast<const uint16_t*>(mlp->A_gate),
+                                     static_cast<const uint16_t*>(mlp->A_up), w.t, w.h, w.ctl, st));
+    s = run_gateup(mlp, x, M, w.h, w.t, st);
+    if (s != QMLP_OK)
+        return s;
+    return from_hip(launch_down(down_args(&mlp->down, w.h, M, y), st));
+}
+
+qmlp_status qmlp_unpack(const qmlp_qweight* w, uint8_t* codes, uint16_t* scales, uint16_t* zeros,
+                        qmlp_stream stream) {
+    qmlp_status s = check_inspect(w);
+    if (s != QMLP_OK)
+        return s;
+    if (!codes || !scales || !zeros)
+        return QMLP_ERR_NULL;
+    if (((uintptr_t)scales & 1u) || ((uintptr_t)zeros & 1u))
+        return QMLP_ERR_ALIGN;
+    return from_hip(launch_unpack(w->bits, static_cast<const uint32_t*>(w->codes),
+                                  static_cast<const uint32_t*>(w->meta), w->n_out, w->k_in,
+                                  w->group, codes, scales, zeros, static_cast<hipStream_t>(stream)));
+}
+
+qmlp_status qmlp_dequant(const qmlp_qweight* w, uint16_t* w_f16, qmlp_stream stream) {
+    qmlp_status s = check_inspect(w);
+    if (s != QMLP_OK)
+        return s;
+    if (!w_f16)
+        return QMLP_ERR_NULL;
+    if ((uintptr_t)w_f16 & 1u)
+        return QMLP_ERR_ALIGN;
+    return from_hip(launch_dequant(w->bits, static_cast<const uint32_t*>(w->codes),
+                                   static_cast<const uint32_t*>(w->meta), w->n_out, w->k_in,
+                                   w->group, w_f16, static_cast<hipStream_t>(stream)));
+}
+
+int qmlp_forward_launches(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
+    if (check_mlp(mlp, M, dtype) != QMLP_OK || M == 0)
+        return 0;
+    if (fused_supported(M, mlp->gate.k_in, mlp->gate.n_out, mlp->gate.group, mlp->rank))
+        return 1;
+    return mlp->rank > 0 ? 3 : 2;
+}
+
+const char* qmlp_status_string(qmlp_status s) {
+    switch (s) {
+    case QMLP_OK: return "ok";
+    case QMLP_ERR_NULL: return "null pointer";
+    case QMLP_ERR_SHAPE: return "invalid shape";
+    case QMLP_ERR_ALIGN: return "misaligned pointer";
+    case QMLP_ERR_UNSUPPORTED: return "unsupported combination";
+    case QMLP_ERR_WORKSPACE: return "workspace missing or too small";
+    case QMLP_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

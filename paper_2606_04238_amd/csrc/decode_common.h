@@ -1,0 +1,751 @@
+// Building blocks of the decode kernels (1 <= M <= 16, binary16), gfx950.
+//
+// The block (arXiv 2606.04238):
+//   G = W2gate x + s_L B_g (A_g x),  U = W2up x + s_L B_u (A_u x)   (Sec. 3.1 Eq. (1), Sec. 4.2)
+//   h = SiLU(G) * U                                                 (Sec. 3.3, Sec. 5)
+//   y = W4down h                                                    (Sec. 3.3)
+// Decode is bound by the bandwidth of loading weights (Sec. 3.3, Sec. 5): each
+// lane issues all 128-bit loads of its packed codes before any arithmetic,
+// the activation sits in LDS, and rows are reduced with lane butterflies.
+//
+// Dot products without per-code int->float conversion: a code OR-ed into the
+// fraction of binary16 1024.0 reads 1024 + q * 2^j (j = its fraction bit
+// position, 4..8).  The activation copy in LDS is pre-scaled by 2^-j per
+// position, so v_dot2_f32_f16 over the raw codes yields
+//   acc = sum_i q_i x_i + 1024 * sum_i x'_i .
+// Per 64-code (2-bit) / 32-code (4-bit) unit u of a row with group scale s and
+// zero z:   sum_i s (q_i - z) x_i = s (acc - C_u - z X_u),
+// with C_u = 1024 * sum x'_i and X_u = sum x_i staged next to the activation.
+//
+// Work items: S lanes share one output row; lane s owns the 16-byte units
+// u = s, s + S, s + 2S, ... of that row (the S lanes of a row read S
+// consecutive units: coalesced), so a wave-item covers 64/S rows.
+#pragma once
+
+#include "qmlp_device.h"
+#include "qmlp_internal.h"
+
+namespace qmlp {
+
+constexpr int GU_UNIT_BYTES = 8 * 16 + 8;   // LDS bytes per (token, 2-bit unit): x' + (C, X)
+constexpr int DN_UNIT_BYTES = 4 * 16 + 8;   // LDS bytes per (token, 4-bit unit): h' + (C, X)
+
+// --------------------------------------------------------------- staging
+// The activation (x for gate/up, h for down) is staged in LDS pre-scaled per
+// fraction position.  Staging is split into a load phase (registers) and a
+// convert phase so a kernel can issue these small loads BEFORE its weight
+// loads: loads retire in order, so data loaded first is usable while the
+// weight stream is still in flight.
+//
+// x' for 2-bit units [u0, u0+uc): per (token m, unit) eight 16-byte chunks
+// (4 code words x 2), chunk c stored at c ^ (unit & 7) so lanes reading
+// different units hit different banks; then (C_u, X_u).  One staging "word"
+// covers 16 codes of one token (two 16-byte loads).
+struct XWord { uint4 lo, hi; };
+
+// Always loads (from word 0 of token 0 when idx has no word or the token is
+// padding: a valid address); the convert step zeroes what is not live.
+template <int MT>
+__device__ __forceinline__ XWord stage_x_load(const uint16_t* x, int M, int d, int u0, int uc,
+                                              int idx) {
+    const int words = MT * uc * 4;
+    const int m = idx / (uc * 4);
+    const bool ok = idx < words && m < M;
+    const int wl = ok ? idx - m * uc * 4 : 0;
+    const uint4* src = reinterpret_cast<const uint4*>(x + (long)(ok ? m : 0) * d + (long)(u0 + (wl >> 2)) * 64 + (wl & 3) * 16);
+    return XWord{src[0], src[1]};
+}
+
+// Convert one staged word; all lanes of the wave must call it (shuffles).
+template <int MT>
+__device__ __forceinline__ void stage_x_store(uint4* xs, float2* cx, int UC, int uc, int M, int idx,
+                                              XWord v) {
+    const int words = MT * uc * 4;
+    const bool live = idx < words;
+    const int m = live ? idx / (uc * 4) : 0;
+    const int wl = live ? idx - m * uc * 4 : 0;
+    const int ul = wl >> 2, w = wl & 3;
+    const bool data = live && m < M;           // padding tokens stage zeros
+    const uint32_t xl[4] = {data ? v.lo.x : 0u, data ? v.lo.y : 0u, data ? v.lo.z : 0u, data ? v.lo.w : 0u};
+    const uint32_t xh[4] = {data ? v.hi.x : 0u, data ? v.hi.y : 0u, data ? v.hi.z : 0u, data ? v.hi.w : 0u};
+    uint32_t pr[8];
+    float csum = 0.0f, xsum = 0.0f;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+        // pair p = (x[p], x[8 + p]); x[i] is half (i & 1) of word i >> 1
+        const uint32_t a16 = (xl[p >> 1] >> (16 * (p & 1))) & 0xFFFFu;
+        const uint32_t b16 = (xh[p >> 1] >> (16 * (p & 1))) & 0xFFFFu;
+        const float sc = w2_pair_scale(p);
+        const uint32_t ha = f2h(h2f(a16) * sc), hb = f2h(h2f(b16) * sc);
+        pr[p] = ha | (hb << 16);
+        csum += h2f(ha) + h2f(hb);
+        xsum += h2f(a16) + h2f(b16);
+    }
+    csum += __shfl_xor(csum, 1, 64);
+    csum += __shfl_xor(csum, 2, 64);
+    xsum += __shfl_xor(xsum, 1, 64);
+    xsum += __shfl_xor(xsum, 2, 64);
+    if (live) {
+        uint4* dst = xs + (m * UC + ul) * 8;
+        dst[(2 * w) ^ (ul & 7)] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
+        dst[(2 * w + 1) ^ (ul & 7)] = make_uint4(pr[4], pr[5], pr[6], pr[7]);
+        if (w == 0)
+            cx[m * UC + ul] = make_float2(1024.0f * csum, xsum);
+    }
+}
+
+// Whole staging of a chunk by the block (load-convert per word).
+template <int MT>
+__device__ __forceinline__ void stage_x(uint4* xs, float2* cx, int UC, const uint16_t* x, int M,
+                                        int d, int u0, int uc, int tid, int nthreads) {
+    const int words = MT * uc * 4;
+    for (int idx = tid; idx < ((words + 63) & ~63); idx += nthreads)
+        stage_x_store<MT>(xs, cx, UC, uc, M, idx, stage_x_load<MT>(x, M, d, u0, uc, idx));
+}
+
+// h' for 4-bit units [u0, u0+uc): per (m, unit) four 16-byte chunks (one per
+// code word, 4 pairs), chunk c stored at c ^ ((unit >> 1) & 3); then (C_u, X_u).
+// One staging word covers 8 codes of one token (one 16-byte load).
+template <int MT>
+__device__ __forceinline__ uint4 stage_h_load(const uint16_t* h, int M, int f, int u0, int uc,
+                                              int idx) {
+    const int words = MT * uc * 4;
+    const int m = idx / (uc * 4);
+    const bool ok = idx < words && m < M;
+    const int wl = ok ? idx - m * uc * 4 : 0;
+    return *reinterpret_cast<const uint4*>(h + (long)(ok ? m : 0) * f + (long)(u0 + (wl >> 2)) * 32 + (wl & 3) * 8);
+}
+
+template <int MT>
+__device__ __forceinline__ void stage_h_store(uint4* hs, float2* cx, int UC, int uc, int M, int idx,
+                                              uint4 v) {
+    const int words = MT * uc * 4;
+    const bool live = idx < words;
+    const int m = live ? idx / (uc * 4) : 0;
+    const int wl = live ? idx - m * uc * 4 : 0;
+    const int ul = wl >> 2, w = wl & 3;
+    const bool data = live && m < M;           // padding tokens stage zeros
+    const uint32_t hl[4] = {data ? v.x : 0u, data ? v.y : 0u, data ? v.z : 0u, data ? v.w : 0u};
+    uint32_t pr[4];
+    float csum = 0.0f, xsum = 0.0f;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        // pair p = (h[p], h[4 + p])
+        const uint32_t a16 = (hl[p >> 1] >> (16 * (p & 1))) & 0xFFFFu;
+        const uint32_t b16 = (hl[2 + (p >> 1)] >> (16 * (p & 1))) & 0xFFFFu;
+        const float sc = w4_pair_scale(p);
+        const uint32_t ha = f2h(h2f(a16) * sc), hb = f2h(h2f(b16) * sc);
+        pr[p] = ha | (hb << 16);
+        csum += h2f(ha) + h2f(hb);
+        xsum += h2f(a16) + h2f(b16);
+    }
+    csum += __shfl_xor(csum, 1, 64);
+    csum += __shfl_xor(csum, 2, 64);
+    xsum += __shfl_xor(xsum, 1, 64);
+    xsum += __shfl_xor(xsum, 2, 64);
+    if (live) {
+        hs[(m * UC + ul) * 4 + (w ^ ((ul >> 1) & 3))] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
+        if (w == 0)
+            cx[m * UC + ul] = make_float2(1024.0f * csum, xsum);
+    }
+}
+
+template <int MT>
+__device__ __forceinline__ void stage_h(uint4* hs, float2* cx, int UC, const uint16_t* h, int M,
+                                        int f, int u0, int uc, int tid, int nthreads) {
+    const int words = MT * uc * 4;
+    for (int idx = tid; idx < ((words + 63) & ~63); idx += nthreads)
+        stage_h_store<MT>(hs, cx, UC, uc, M, idx, stage_h_load<MT>(h, M, f, u0, uc, idx));
+}
+
+// --------------------------------------------------------------- gate/up item
+template <int MT, int S, int MAXJ>
+struct GuItem {
+    uint4 qg[MAXJ], qu[MAXJ];
+    uint32_t mg[MAXJ], mu[MAXJ];
+    uint32_t bg[4], bu[4];          // LoRA-B row slice, raw binary16
+    float G[MT], U[MT];
+    int row;
+    bool ok;
+};
+
+// Issue the loads of one gate/up item: S lanes per row, rows row0 + lane/S.
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ>& it, const GateUpArgs& a, int row0,
+                                        bool active, int lane) {
+    const int s = lane % S;
+    const int U = a.d / 64;
+    const int J = (U + S - 1) / S;
+    it.row = row0 + lane / S;
+    it.ok = active && it.row < a.f;
+    const int ng = a.d / a.g;
+    const int upg = a.g / 64;
+    // Loads go out from a clamped, always valid address (unit 0 of row 0 for
+    // lanes without work) straight into the slot registers: no select and no
+    // conversion touches a loaded value here, since loads retire in order and
+    // any use would stall issue until every earlier load of the wave arrived.
+    // Values of lanes without work are never used (the compute skips units
+    // past the row and the epilogue skips rows past f).
+    const long rowc = it.ok ? it.row : 0;
+    const uint4* cg = reinterpret_cast<const uint4*>(a.cg) + rowc * U;
+    const uint4* cu = reinterpret_cast<const uint4*>(a.cu) + rowc * U;
+    const uint32_t* mg = a.mg + rowc * ng;
+    const uint32_t* mu = a.mu + rowc * ng;
+#pragma unroll
+    for (int i = 0; i < MAXJ; ++i) {
+        if (i < J && active) {                     // wave-uniform; unloaded slots are never read
+            const int u = s + S * i;
+            const int uu = u < U ? u : 0;
+            it.qg[i] = load_stream(cg + uu);
+            it.qu[i] = load_stream(cu + uu);
+            it.mg[i] = load_stream(mg + uu / upg);
+            it.mu[i] = load_stream(mu + uu / upg);
+        }
+    }
+    // LoRA-B row slices stay raw binary16 until the epilogue: four loads per
+    // lane, branch-free from clamped offsets (with rank 0 the pointers are a
+    // readable dummy), so nothing converts them at issue time.
+    const int CPL = (a.r + S - 1) / S;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const int rc = s * CPL + c;
+        const long off = rowc * a.r + ((c < CPL && rc < a.r) ? rc : 0);
+        it.bg[c] = a.Bg[off];
+        it.bu[c] = a.Bu[off];
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m) it.G[m] = it.U[m] = 0.0f;
+}
+
+// Dot products of the item's units that fall in the staged chunk [u0, u0+uc).
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ>& it, const uint4* xs,
+                                              const float2* cx, int UC, int d, int u0, int uc,
+                                              int lane) {
+    const int s = lane % S;
+    const int J = (d / 64 + S - 1) / S;
+#pragma unroll
+    for (int i = 0; i < MAXJ; ++i) {
+        const int u = s + S * i;
+        if (i < J && u >= u0 && u < u0 + uc) {
+            const int ul = u - u0;
+            float ag[MT], au[MT];
+#pragma unroll
+            for (int m = 0; m < MT; ++m) ag[m] = au[m] = 0.0f;
+            uint32_t wg[4] = {it.qg[i].x, it.qg[i].y, it.qg[i].z, it.qg[i].w};
+            uint32_t wu[4] = {it.qu[i].x, it.qu[i].y, it.qu[i].z, it.qu[i].w};
+            uint32_t mgi = it.mg[i], mui = it.mu[i];
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                pin(wg[w]);
+                pin(wu[w]);
+            }
+            pin(mgi);
+            pin(mui);
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                uint32_t eg[8], eu[8];
+                extract_w2(wg[w], eg);
+                extract_w2(wu[w], eu);
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    const uint4* src = xs + (m * UC + ul) * 8;
+                    const uint4 p0 = src[(2 * w) ^ (ul & 7)];
+                    const uint4 p1 = src[(2 * w + 1) ^ (ul & 7)];
+                    const uint32_t xp[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+                    for (int p = 0; p < 8; ++p) {
+                        ag[m] = dot2(eg[p], xp[p], ag[m]);
+                        au[m] = dot2(eu[p], xp[p], au[m]);
+                    }
+                }
+            }
+            const float sg = h2f(mgi & 0xFFFFu), zg = h2f(mgi >> 16);
+            const float su = h2f(mui & 0xFFFFu), zu = h2f(mui >> 16);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const float2 k = cx[m * UC + ul];
+                it.G[m] += sg * (ag[m] - k.x - zg * k.y);
+                it.U[m] += su * (au[m] - k.x - zu * k.y);
+            }
+        }
+    }
+}
+
+// LoRA-B on the lane's rank slice, reduction over the S lanes of each row,
+// and the epilogue h = SiLU(G) * U (t: [M][2r] fp32, gate ranks then up).
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void gu_finish(GuItem<MT, S, MAXJ>& it, const GateUpArgs& a,
+                                          const float* t, uint16_t* h, int lane) {
+    const int s = lane % S;
+    if (a.r > 0) {
+        const int CPL = (a.r + S - 1) / S;
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            if (m < a.M) {
+                float lg = 0.0f, lu = 0.0f;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int rc = s * CPL + c;
+                    if (c < CPL && rc < a.r) {
+                        uint32_t bgc = it.bg[c], buc = it.bu[c];
+                        pin(bgc);
+                        pin(buc);
+                        lg += h2f(bgc) * t[m * 2 * a.r + rc];
+                        lu += h2f(buc) * t[m * 2 * a.r + a.r + rc];
+                    }
+                }
+                it.G[m] += a.lora_scale * lg;
+                it.U[m] += a.lora_scale * lu;
+            }
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        const float gv = group_sum<S>(it.G[m]);
+        const float uv = group_sum<S>(it.U[m]);
+        if (it.ok && m < a.M && (m % S) == s) {
+            const float hv = gv / (1.0f + __expf(-gv)) * uv;
+            h[(long)m * a.f + it.row] = (uint16_t)f2h(hv);
+        }
+    }
+}
+
+// --------------------------------------------------------------- down item
+template <int MT, int S, int MAXJ>
+struct DnItem {
+    uint4 q[MAXJ];
+    uint32_t mt[MAXJ];
+    float Y[MT];
+    int row;
+    bool ok;          // this lane's row exists
+    bool active;      // the wave holds this item (wave-uniform)
+};
+
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void dn_load(DnItem<MT, S, MAXJ>& it, const DownArgs& a, int row0,
+                                        bool active, int lane) {
+    const int s = lane % S;
+    const int U = a.f / 32;
+    const int J = (U + S - 1) / S;
+    it.row = row0 + lane / S;
+    it.ok = active && it.row < a.d;
+    it.active = active;
+    const int ng = a.f / a.g;
+    const int upg = a.g / 32;
+    const long rowc = it.ok ? it.row : 0;          // clamped, unselected: see gu_load
+    const uint4* cd = reinterpret_cast<const uint4*>(a.cd) + rowc * U;
+    const uint32_t* md = a.md + rowc * ng;
+#pragma unroll
+    for (int i = 0; i < MAXJ; ++i) {
+        if (i < J && active) {                     // wave-uniform; unloaded slots are never read
+            const int u = s + S * i;
+            const int uu = u < U ? u : 0;
+            it.q[i] = load_stream(cd + uu);
+            it.mt[i] = load_stream(md + uu / upg);
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m) it.Y[m] = 0.0f;
+}
+
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void dn_accumulate(DnItem<MT, S, MAXJ>& it, const uint4* hs,
+                                              const float2* cx, int UC, int f, int u0, int uc,
+                                              int lane) {
+    const int s = lane % S;
+    const int J = (f / 32 + S - 1) / S;
+    if (!it.active)
+        return;
+#pragma unroll
+    for (int i = 0; i < MAXJ; ++i) {
+        const int u = s + S * i;
+        if (i < J && u >= u0 && u < u0 + uc) {
+            const int ul = u - u0;
+            float acc[MT];
+#pragma unroll
+            for (int m = 0; m < MT; ++m) acc[m] = 0.0f;
+            uint32_t wv[4] = {it.q[i].x, it.q[i].y, it.q[i].z, it.q[i].w};
+            uint32_t mti = it.mt[i];
+#pragma unroll
+            for (int w = 0; w < 4; ++w)
+                pin(wv[w]);
+            pin(mti);
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                uint32_t e[4];
+                extract_w4(wv[w], e);
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    const uint4 p = hs[(m * UC + ul) * 4 + (w ^ ((ul >> 1) & 3))];
+                    acc[m] = dot2(e[0], p.x, acc[m]);
+                    acc[m] = dot2(e[1], p.y, acc[m]);
+                    acc[m] = dot2(e[2], p.z, acc[m]);
+                    acc[m] = dot2(e[3], p.w, acc[m]);
+                }
+            }
+            const float sc = h2f(mti & 0xFFFFu), zc = h2f(mti >> 16);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const float2 k = cx[m * UC + ul];
+                it.Y[m] += sc * (acc[m] - k.x - zc * k.y);
+            }
+        }
+    }
+}
+
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void dn_finish(DnItem<MT, S, MAXJ>& it, const DownArgs& a, int lane) {
+    const int s = lane % S;
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        const float v = group_sum<S>(it.Y[m]);
+        if (it.ok && m < a.M && (m % S) == s)
+            a.y[(long)m * a.d + it.row] = (uint16_t)f2h(v);
+    }
+}
+
+
+// --------------------------------------------------------------- fused-kernel items
+// Straight-line load sequences for the fused layer kernel: exactly the same
+// number of loads on every lane and path, so the wait before each use covers
+// exactly the loads issued before it.  Lanes without work read a clamped,
+// valid address and their values are never used.
+//
+// Scale/zero metadata is loaded WIDE: the rows of a wave-item have
+// consecutive metadata words, which the wave pulls in with 16-byte loads
+// (one or two instructions instead of one 4-byte load per slot) and parks in
+// a per-wave LDS area; each lane then reads its groups' words from LDS.
+template <int MT, int S, int MAXJ, int KMETA>
+struct FGuItem {
+    uint4 qg[MAXJ], qu[MAXJ];
+    uint4 meta[KMETA];           // metadata chunks, gate rows then up rows (KMETA per lane)
+    uint32_t bg[2], bu[2];       // LoRA-B row slice, raw binary16 (up to 4 halves)
+    float G[MT], U[MT];
+    int row, row0;
+    bool ok;
+};
+
+// Loads: metadata chunks first (they retire first), then codes, then LoRA-B.
+template <int MT, int S, int MAXJ, int KMETA>
+__device__ __forceinline__ void fgu_load(FGuItem<MT, S, MAXJ, KMETA>& it, const GateUpArgs& a, int row0,
+                                         int lane) {
+    constexpr int RPW = 64 / S;
+    const int s = lane % S;
+    const int U = a.d / 64;
+    const int ng = a.d / a.g;
+    it.row0 = row0;
+    it.row = row0 + lane / S;
+    it.ok = it.row < a.f;
+    const long rowc = it.ok ? it.row : 0;
+    // metadata of rows row0 .. row0+RPW-1: RPW*ng words per matrix, 16-byte
+    // aligned (row0 is a multiple of RPW and RPW*ng*4 a multiple of 16)
+    const int chunks = RPW * ng / 4;                       // per matrix
+    const uint4* mg = reinterpret_cast<const uint4*>(a.mg + (long)row0 * ng);
+    const uint4* mu = reinterpret_cast<const uint4*>(a.mu + (long)row0 * ng);
+#pragma unroll
+    for (int k = 0; k < KMETA; ++k) {
+        const int c = lane + 64 * k;                       // chunk over [gate | up]
+        const uint4* src = c < chunks ? mg + c : (c < 2 * chunks ? mu + (c - chunks) : mg);
+        it.meta[k] = load_stream(src);
+    }
+    const uint4* cg = reinterpret_cast<const uint4*>(a.cg) + rowc * U;
+    const uint4* cu = reinterpret_cast<const uint4*>(a.cu) + rowc * U;
+#pragma unroll
+    for (int i = 0; i < MAXJ; ++i) {
+        const int u = s + S * i;
+        const int uu = u < U ? u : 0;
+        it.qg[i] = load_stream(cg + uu);
+        it.qu[i] = load_stream(cu + uu);
+    }
+    // LoRA-B: lane s takes ranks [s*CPL, s*CPL + CPL), one load per matrix
+    const int CPL = (a.r + S - 1) / S;
+    const long off = rowc * a.r + (s * CPL < a.r ? s * CPL : 0);
+    if (CPL <= 1) {
+        it.bg[0] = a.Bg[off];
+        it.bu[0] = a.Bu[off];
+    } else if (CPL == 2) {
+        it.bg[0] = *reinterpret_cast<const uint32_t*>(a.Bg + off);
+        it.bu[0] = *reinterpret_cast<const uint32_t*>(a.Bu + off);
+    } else {
+        const uint2 vg = *reinterpret_cast<const uint2*>(a.Bg + off);
+        const uint2 vu = *reinterpret_cast<const uint2*>(a.Bu + off);
+        it.bg[0] = vg.x; it.bg[1] = vg.y;
+        it.bu[0] = vu.x; it.bu[1] = vu.y;
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m) it.G[m] = it.U[m] = 0.0f;
+}
+
+// Park the metadata chunks in the wave's LDS area (gate rows, then up rows).
+template <int MT, int S, int MAXJ, int KMETA>
+__device__ __forceinline__ void fgu_meta_to_lds(const FGuItem<MT, S, MAXJ, KMETA>& it, const GateUpArgs& a,
+                                                uint4* wmeta, int lane) {
+    constexpr int RPW = 64 / S;
+    const int chunks = RPW * (a.d / a.g) / 4;
+#pragma unroll
+    for (int k = 0; k < KMETA; ++k) {
+        const int c = lane + 64 * k;
+        if (c < 2 * chunks)
+            wmeta[c] = it.meta[k];
+    }
+}
+
+template <int MT, int S, int MAXJ, int KMETA>
+__device__ __forceinline__ void fgu_accumulate(FGuItem<MT, S, MAXJ, KMETA>& it, const uint4* xs,
+                                               const float2* cx, int UC, int d, int g,
+                                               const uint32_t* wmeta, int lane) {
+    constexpr int RPW = 64 / S;
+    const int s = lane % S, r = lane / S;
+    const int U = d / 64, ng = d / g, upg = g / 64;
+#pragma unroll
+    for (int i = 0; i < MAXJ; ++i) {
+        const int u = s + S * i;
+        if (u < U) {
+            const int ul = u;
+            float ag[MT], au[MT];
+#pragma unroll
+            for (int m = 0; m < MT; ++m) ag[m] = au[m] = 0.0f;
+            uint32_t wg[4] = {it.qg[i].x, it.qg[i].y, it.qg[i].z, it.qg[i].w};
+            uint32_t wu[4] = {it.qu[i].x, it.qu[i].y, it.qu[i].z, it.qu[i].w};
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                pin(wg[w]);
+                pin(wu[w]);
+            }
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                uint32_t eg[8], eu[8];
+                extract_w2(wg[w], eg);
+                extract_w2(wu[w], eu);
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    const uint4* src = xs + (m * UC + ul) * 8;
+                    const uint4 p0 = src[(2 * w) ^ (ul & 7)];
+                    const uint4 p1 = src[(2 * w + 1) ^ (ul & 7)];
+                    const uint32_t xp[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+                    for (int p = 0; p < 8; ++p) {
+                        ag[m] = dot2(eg[p], xp[p], ag[m]);
+                        au[m] = dot2(eu[p], xp[p], au[m]);
+                    }
+                }
+            }
+            const uint32_t mgi = wmeta[r * ng + u / upg];
+            const uint32_t mui = wmeta[(RPW + r) * ng + u / upg];
+            const float sg = h2f(mgi & 0xFFFFu), zg = h2f(mgi >> 16);
+            const float su = h2f(mui & 0xFFFFu), zu = h2f(mui >> 16);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const float2 k = cx[m * UC + ul];
+                it.G[m] += sg * (ag[m] - k.x - zg * k.y);
+                it.U[m] += su * (au[m] - k.x - zu * k.y);
+            }
+        }
+    }
+}
+
+// LoRA-B, row reduction, h = SiLU(G) * U written with device-coherent
+// stores (other compute units read h right after the hand-off).
+template <int MT, int S, int MAXJ, int KMETA>
+__device__ __forceinline__ void fgu_finish(FGuItem<MT, S, MAXJ, KMETA>& it, const GateUpArgs& a,
+                                           const float* t, uint16_t* h, int lane) {
+    const int s = lane % S;
+    if (a.r > 0) {
+        const int CPL = (a.r + S - 1) / S;
+        uint32_t b0 = it.bg[0], b1 = it.bg[1], c0 = it.bu[0], c1 = it.bu[1];
+        pin(b0); pin(b1); pin(c0); pin(c1);
+        const uint32_t bgw[2] = {b0, b1}, buw[2] = {c0, c1};
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            if (m < a.M) {
+                float lg = 0.0f, lu = 0.0f;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int rc = s * CPL + c;
+                    if (c < CPL && rc < a.r) {
+                        lg += h2f(bgw[c >> 1] >> (16 * (c & 1))) * t[m * 2 * a.r + rc];
+                        lu += h2f(buw[c >> 1] >> (16 * (c & 1))) * t[m * 2 * a.r + a.r + rc];
+                    }
+                }
+                it.G[m] += a.lora_scale * lg;
+                it.U[m] += a.lora_scale * lu;
+            }
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        const float gv = group_sum<S>(it.G[m]);
+        const float uv = group_sum<S>(it.U[m]);
+        if (it.ok && m < a.M && (m % S) == s) {
+            const float hv = gv / (1.0f + __expf(-gv)) * uv;
+            __hip_atomic_store(h + (long)m * a.f + it.row, (uint16_t)f2h(hv), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
+template <int MT, int S, int MAXJ>
+struct FDnItem {
+    uint4 q[MAXJ];
+    uint4 meta;                  // one 16-byte metadata chunk per lane
+    float Y[MT];
+    int row, row0;
+    bool ok, active;
+};
+
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void fdn_load(FDnItem<MT, S, MAXJ>& it, const DownArgs& a, int row0,
+                                         bool active, int lane) {
+    constexpr int RPW = 64 / S;
+    const int s = lane % S;
+    const int U = a.f / 32;
+    const int ng = a.f / a.g;
+    it.row0 = row0;
+    it.row = row0 + lane / S;
+    it.ok = active && it.row < a.d;
+    it.active = active;
+    const long rowc = it.ok ? it.row : 0;
+    const int chunks = RPW * ng / 4;                       // <= 64 (checked by the planner)
+    const uint4* md = reinterpret_cast<const uint4*>(a.md + (long)(active ? row0 : 0) * ng);
+    it.meta = load_stream(md + (lane < chunks ? lane : 0));
+    const uint4* cd = reinterpret_cast<const uint4*>(a.cd) + rowc * U;
+#pragma unroll
+    for (int i = 0; i < MAXJ; ++i) {
+        const int u = s + S * i;
+        it.q[i] = load_stream(cd + (u < U ? u : 0));
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m) it.Y[m] = 0.0f;
+}
+
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void fdn_meta_to_lds(const FDnItem<MT, S, MAXJ>& it, const DownArgs& a,
+                                                uint4* wmeta, int lane) {
+    constexpr int RPW = 64 / S;
+    if (lane < RPW * (a.f / a.g) / 4)
+        wmeta[lane] = it.meta;
+}
+
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void fdn_accumulate(FDnItem<MT, S, MAXJ>& it, const uint4* hs,
+                                               const float2* cx, int UC, int f, int g,
+                                               const uint32_t* wmeta, int lane) {
+    const int s = lane % S, r = lane / S;
+    const int U = f / 32, ng = f / g, upg = g / 32;
+    if (!it.active)
+        return;
+#pragma unroll
+    for (int i = 0; i < MAXJ; ++i) {
+        const int u = s + S * i;
+        if (u < U) {
+            const int ul = u;
+            float acc[MT];
+#pragma unroll
+            for (int m = 0; m < MT; ++m) acc[m] = 0.0f;
+            uint32_t wv[4] = {it.q[i].x, it.q[i].y, it.q[i].z, it.q[i].w};
+#pragma unroll
+            for (int w = 0; w < 4; ++w)
+                pin(wv[w]);
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                uint32_t e[4];
+                extract_w4(wv[w], e);
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    const uint4 p = hs[(m * UC + ul) * 4 + (w ^ ((ul >> 1) & 3))];
+                    acc[m] = dot2(e[0], p.x, acc[m]);
+                    acc[m] = dot2(e[1], p.y, acc[m]);
+                    acc[m] = dot2(e[2], p.z, acc[m]);
+                    acc[m] = dot2(e[3], p.w, acc[m]);
+                }
+            }
+            const uint32_t mti = wmeta[r * ng + u / upg];
+            const float sc = h2f(mti & 0xFFFFu), zc = h2f(mti >> 16);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const float2 k = cx[m * UC + ul];
+                it.Y[m] += sc * (acc[m] - k.x - zc * k.y);
+            }
+        }
+    }
+}
+
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void fdn_finish(FDnItem<MT, S, MAXJ>& it, const DownArgs& a, int lane) {
+    const int s = lane % S;
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        const float v = group_sum<S>(it.Y[m]);
+        if (it.ok && m < a.M && (m % S) == s)
+            a.y[(long)m * a.d + it.row] = (uint16_t)f2h(v);
+    }
+}
+
+// Device-coherent read of one staging word of h (written by other compute
+// units with device-coherent stores): four agent-scope dword loads.
+template <int MT>
+__device__ __forceinline__ uint4 stage_h_load_coherent(const uint16_t* h, int M, int f, int u0,
+                                                       int uc, int idx) {
+    const int words = MT * uc * 4;
+    const int m = idx / (uc * 4);
+    const bool ok = idx < words && m < M;
+    const int wl = ok ? idx - m * uc * 4 : 0;
+    const uint32_t* src = reinterpret_cast<const uint32_t*>(h + (long)(ok ? m : 0) * f + (long)(u0 + (wl >> 2)) * 32 + (wl & 3) * 8);
+    uint4 v;
+    v.x = __hip_atomic_load(src + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    v.y = __hip_atomic_load(src + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    v.z = __hip_atomic_load(src + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    v.w = __hip_atomic_load(src + 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return v;
+}
+
+// --------------------------------------------------------------- LoRA-A row
+// t[m][c] = sum_i A[c][i] x[m][i] for one row c of [A_g; A_u], by one wave.
+// Every load of the row is issued before the first multiply (KA = most
+// 8-element chunks per lane, d <= 512 * KA): in a memory system saturated by
+// weight streams a load-use chain would pay one queueing delay per step.
+template <int MT, int KA>
+__device__ __forceinline__ void lora_a_row(const uint16_t* Ag, const uint16_t* Au,
+                                           const uint16_t* x, int M, int d, int r, int c,
+                                           float* t, int lane) {
+    const uint16_t* a = c < r ? Ag + (long)c * d : Au + (long)(c - r) * d;
+    const int nch = d / 8;
+    float acc[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m] = 0.0f;
+    for (int base = 0; base < nch; base += 64 * KA) {
+        uint4 av[KA], xv[KA][MT];
+#pragma unroll
+        for (int k = 0; k < KA; ++k) {
+            const int ch = base + lane + 64 * k;
+            const int cc = ch < nch ? ch : 0;
+            av[k] = *reinterpret_cast<const uint4*>(a + cc * 8);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const int mm = m < M ? m : 0;
+                xv[k][m] = *reinterpret_cast<const uint4*>(x + (long)mm * d + cc * 8);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < KA; ++k) {
+            if (base + lane + 64 * k < nch) {
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    acc[m] = dot2(av[k].x, xv[k][m].x, acc[m]);
+                    acc[m] = dot2(av[k].y, xv[k][m].y, acc[m]);
+                    acc[m] = dot2(av[k].z, xv[k][m].z, acc[m]);
+                    acc[m] = dot2(av[k].w, xv[k][m].w, acc[m]);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        const float v = group_sum<64>(acc[m]);
+        if (lane == 0 && m < M)   // device-coherent: read by other compute units
+            __hip_atomic_store(t + m * 2 * r + c, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+}  // namespace qmlp

@@ -1,0 +1,321 @@
+// One kernel per MLP layer for decode (M <= 4 tokens, binary16), gfx950.
+//
+// The whole block -- LoRA-A projection, fused 2-bit gate/up with LoRA-B and
+// SiLU(G) * U, and the 4-bit down projection (Sec. 3.1 Eq. (1), Sec. 3.3,
+// Sec. 4.2) -- runs as one launch, the fused gate-activation-down operator of
+// Sec. 5.  Decode is bound by loading weights, and on MI355X a dependent
+// kernel boundary costs about as much time as streaming one projection's
+// weights, so the layer is not split into kernels:
+//
+//   * every wave issues the loads of ALL its packed weights at kernel start:
+//     its gate/up rows and its down rows (the down weights do not depend on
+//     h, so they stream in while gate/up computes);
+//   * a few waves compute t = [A_g; A_u] x and publish it (release add on a
+//     counter); each block acquires it once, for the LoRA-B epilogue;
+//   * each block writes its rows of h and publishes them; every block then
+//     waits for all blocks' h (acquire) and finishes its down rows.
+// Polling uses relaxed loads and each block takes one acquire fence and one
+// release per hand-off: agent-scope fences write back / invalidate the L2
+// and must not sit in a polling loop or run once per wave.
+//
+// The grid is one block per compute unit, so every block is resident and
+// every wait ends; each wait is also bounded (it sets an error bit and
+// proceeds instead of spinning forever).  The control words live at the
+// start of the caller's workspace and are returned to zero by the last block
+// of every call.
+#include "decode_common.h"
+#include "decode_launch.h"
+
+namespace qmlp {
+
+constexpr int FW = 8;                          // waves per block
+constexpr unsigned kSpinLimit = 1u << 21;      // ~0.1 s of polling before giving up
+constexpr size_t kFusedLds = 144 * 1024;       // one block per CU: most of the 160 KB LDS
+
+// ctl[0]: rows of t published, ctl[1]: blocks whose h rows are published,
+// ctl[2]: blocks past the h wait, ctl[3]: sticky error bits.
+struct FusedArgs {
+    GateUpArgs gu;
+    DownArgs dn;
+    const uint16_t* Ag;
+    const uint16_t* Au;
+    float* t;
+    uint16_t* h;
+    unsigned* ctl;
+    int gu_items;                              // gate/up wave-items (8 rows each)
+    int dn_items;                              // down wave-items (64/SD rows each)
+    int nguw;                                  // waves per block that hold a gate/up item
+    int lds_stage;                             // bytes of the x' / h' staging area
+    int gu_meta_bytes;                         // per-wave LDS bytes for gate/up metadata
+    int wmeta_bytes;                           // per-wave LDS metadata area
+};
+
+// Hand-offs between compute units (t, then h) use device-coherent accesses
+// only: the producer writes with agent-scope stores (written through to the
+// coherence point), waits for them to complete (s_waitcnt), then bumps a
+// counter with a relaxed agent-scope atomic; the consumer polls the counter
+// with relaxed agent-scope loads and, once it is seen, reads the data with
+// agent-scope loads.  Loads issue in order after the poll returns, so they
+// observe the completed stores.  No cache write-back or invalidate is needed
+// (agent-scope fences on this GPU write back / invalidate the whole L2).
+// Bounded: returns false instead of spinning forever.
+__device__ __forceinline__ bool wait_at_least(unsigned* p, unsigned target) {
+    for (unsigned it = 0; it < kSpinLimit; ++it) {
+        if (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target)
+            return true;
+        __builtin_amdgcn_s_sleep(1);
+    }
+    return false;
+}
+
+// Waves take one of two roles (the role is wave-uniform and branched on a
+// scalar, so every wave runs exactly one path and meets the same barriers):
+//   gate/up waves (wave < nguw): metadata, gate/up codes, LoRA-B, then down
+//     items -- a straight-line load sequence, so each slot's wait covers
+//     exactly the loads before it and the gate/up math overlaps the stream;
+//   staging waves (the rest): x' staging and LoRA-A first (small loads that
+//     retire early), then their down items; the last wave also waits for t
+//     and copies it into LDS while the gate/up waves compute.
+// LDS: [x' or h' staging][t, 1 KB][per-wave metadata areas].
+template <int MT, int JG, int KM, int SD, int JD, int NDN>
+__global__ void __launch_bounds__(FW * 64)
+fused_layer_kernel(FusedArgs fa) {
+    constexpr int SG = 8, RPWG = 8, RPWD = 64 / SD;
+    extern __shared__ uint4 smem[];
+    __shared__ int s_ok;
+    const GateUpArgs& a = fa.gu;
+    const DownArgs& b = fa.dn;
+    unsigned* ctl = fa.ctl;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int G = gridDim.x;
+    const int Ug = a.d / 64, Ud = b.f / 32;     // the whole row is one LDS chunk
+    const int nguw = fa.nguw;
+    char* lds = reinterpret_cast<char*>(smem);
+    uint4* xs = smem;
+    float2* cxg = reinterpret_cast<float2*>(smem + MT * Ug * 8);
+    float* ts = reinterpret_cast<float*>(lds + fa.lds_stage);
+    uint4* wmeta = reinterpret_cast<uint4*>(lds + fa.lds_stage + 1024 + wave * fa.wmeta_bytes);
+    uint4* wmeta_dn = wmeta + fa.gu_meta_bytes / 16;
+    const int dn_meta_chunks = RPWD * (b.f / b.g) / 4;
+
+    FGuItem<MT, SG, JG, KM> gi;
+    FDnItem<MT, SD, JD> di[NDN];
+    const int gitem = blockIdx.x + wave * G;
+
+    if (wave < nguw) {
+        const bool real = gitem < fa.gu_items;
+        fgu_load(gi, a, (real ? gitem : 0) * RPWG, lane);
+        if (!real)
+            gi.ok = false;                      // a dummy item: computed, never stored
+#pragma unroll
+        for (int k = 0; k < NDN; ++k) {
+            const int item = blockIdx.x + ((FW - 1 - wave) + k * FW) * G;
+            const bool act = item < fa.dn_items;
+            fdn_load(di[k], b, (act ? item : 0) * RPWD, act, lane);
+        }
+    } else {
+        // x' staging: the staging waves share the M * Ug * 4 words.
+        const int sthreads = (FW - nguw) * 64, st = tid - nguw * 64;
+        const int words = MT * Ug * 4;
+        for (int idx0 = 0; idx0 < words; idx0 += sthreads * MT) {
+            XWord xw[MT];
+#pragma unroll
+            for (int k = 0; k < MT; ++k)
+                xw[k] = stage_x_load<MT>(a.x, a.M, a.d, 0, Ug, idx0 + st + k * sthreads);
+#pragma unroll
+            for (int k = 0; k < MT; ++k)
+                stage_x_store<MT>(xs, cxg, Ug, Ug, a.M, idx0 + st + k * sthreads, xw[k]);
+        }
+        // LoRA-A rows: the highest waves of the first blocks.
+        const int c = blockIdx.x + G * (FW - 1 - wave);
+        if (a.r > 0 && c < 2 * a.r) {
+            lora_a_row<MT, 12 / MT>(fa.Ag, fa.Au, a.x, a.M, a.d, a.r, c, fa.t, lane);
+            __builtin_amdgcn_s_waitcnt(0);      // t stored (device-coherent) before the count
+            if (lane == 0)
+                __hip_atomic_fetch_add(&ctl[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+#pragma unroll
+        for (int k = 0; k < NDN; ++k) {
+            const int item = blockIdx.x + ((FW - 1 - wave) + k * FW) * G;
+            const bool act = item < fa.dn_items;
+            fdn_load(di[k], b, (act ? item : 0) * RPWD, act, lane);
+        }
+    }
+    __syncthreads();                            // x' staged
+
+    if (wave < nguw) {
+        // Gate/up dot products, slot by slot as the stream arrives.
+        fgu_meta_to_lds(gi, a, wmeta, lane);
+        fgu_accumulate(gi, xs, cxg, Ug, a.d, a.g, reinterpret_cast<const uint32_t*>(wmeta), lane);
+    } else if (wave == FW - 1 && a.r > 0) {
+        // t = [A_g; A_u] x from the LoRA-A waves, into LDS.
+        if (!wait_at_least(&ctl[0], 2u * a.r) && lane == 0)
+            atomicOr(&ctl[3], 1u);
+        for (int i = lane; i < a.M * 2 * a.r; i += 64)
+            ts[i] = __hip_atomic_load(fa.t + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();                            // t in LDS
+    if (wave < nguw)
+        fgu_finish(gi, a, ts, fa.h, lane);
+
+    // Publish this block's h rows (device-coherent stores complete, block
+    // barrier, one relaxed count by thread 0), then wait for every block's.
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+        __hip_atomic_fetch_add(&ctl[1], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_ok = wait_at_least(&ctl[1], (unsigned)G);
+        if (!s_ok)
+            atomicOr(&ctl[3], 2u);
+    }
+    __syncthreads();
+
+    // Down projection over the staged intermediate.
+    {
+#pragma unroll
+        for (int k = 0; k < NDN; ++k)
+            fdn_meta_to_lds(di[k], b, wmeta_dn + k * dn_meta_chunks, lane);
+        uint4 hw[4 * MT];
+#pragma unroll
+        for (int k = 0; k < 4 * MT; ++k)
+            hw[k] = stage_h_load_coherent<MT>(fa.h, b.M, b.f, 0, Ud, tid + k * FW * 64);
+        uint4* hs = smem;
+        float2* cx = reinterpret_cast<float2*>(smem + MT * Ud * 4);
+#pragma unroll
+        for (int k = 0; k < 4 * MT; ++k)
+            stage_h_store<MT>(hs, cx, Ud, Ud, b.M, tid + k * FW * 64, hw[k]);
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < NDN; ++k)
+            fdn_accumulate(di[k], hs, cx, Ud, b.f, b.g,
+                           reinterpret_cast<const uint32_t*>(wmeta_dn + k * dn_meta_chunks), lane);
+    }
+#pragma unroll
+    for (int k = 0; k < NDN; ++k)
+        fdn_finish(di[k], b, lane);
+
+    // The last block past the h wait returns the counters to zero (no block
+    // reads them after passing that wait).
+    if (tid == 0) {
+        const unsigned old = __hip_atomic_fetch_add(&ctl[2], 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+        if (old == (unsigned)G - 1) {
+            __hip_atomic_store(&ctl[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctl[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctl[2], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
+// --------------------------------------------------------------- host side
+namespace {
+
+// Compute units of the current device (an immutable device property, cached).
+int cu_count() {
+    static int cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 0;
+    if (cache[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
+
+struct FusedPlan {
+    int mt, jg, km, sd, jd, ndn, nguw, grid, gu_items, dn_items;
+    int lds_stage, gu_meta_bytes, wmeta_bytes;
+    size_t lds;
+    bool ok;
+};
+
+FusedPlan plan_fused(int M, int d, int f, int g, int r) {
+    FusedPlan p{};
+    p.ok = false;
+    p.mt = mtile_for(M);
+    if (p.mt > 4)
+        return p;
+    const int Ug = d / 64, Ud = f / 32, ng = d / g, ngd = f / g;
+    if (lanes_gateup(Ug) != 8)
+        return p;
+    p.sd = lanes_down(Ud);
+    p.jg = (Ug + 7) / 8;
+    p.jd = (Ud + p.sd - 1) / p.sd;
+    if (p.jg > 8 || (p.sd != 8 && p.sd != 64) || p.jd > 8)
+        return p;
+    // metadata loads: gate+up chunks of 8 rows (16 B each) over 64 lanes;
+    // down: one 16-byte chunk per lane
+    p.km = (2 * 8 * ng / 4 + 63) / 64;
+    const int rpwd = 64 / p.sd;
+    if (p.km > 6 || (rpwd * ngd) % 4 != 0 || rpwd * ngd / 4 > 64)
+        return p;
+    p.grid = cu_count();
+    if (p.grid <= 0)
+        return p;
+    p.gu_items = (f + 7) / 8;
+    p.dn_items = (d + rpwd - 1) / rpwd;
+    p.nguw = (p.gu_items + p.grid - 1) / p.grid;
+    if (p.nguw >= FW)                          // at least one staging wave
+        return p;
+    if (2 * r > p.grid * (FW - p.nguw))         // LoRA-A rows on staging waves
+        return p;
+    p.ndn = (p.dn_items + FW * p.grid - 1) / (FW * p.grid);
+    if (p.ndn > 2)
+        return p;
+    // The h' staging holds at most 4*MT words per thread.
+    if (p.mt * Ud * 4 > 4 * p.mt * FW * 64)
+        return p;
+    const size_t lg = (size_t)p.mt * Ug * GU_UNIT_BYTES;
+    const size_t ld = (size_t)p.mt * Ud * DN_UNIT_BYTES;
+    p.lds_stage = (int)((lg > ld ? lg : ld) + 15) / 16 * 16;
+    p.gu_meta_bytes = 2 * 8 * ng * 4;
+    p.wmeta_bytes = p.gu_meta_bytes + p.ndn * rpwd * ngd * 4;
+    p.lds = (size_t)p.lds_stage + 1024 + (size_t)FW * p.wmeta_bytes;
+    p.ok = p.lds <= kFusedLds;
+    return p;
+}
+
+}  // namespace
+
+bool fused_supported(int M, int d, int f, int g, int r) { return plan_fused(M, d, f, g, r).ok; }
+
+// Exact slot counts for the common shapes, else the 8-slot generic instance
+// (slots past the row are dummies).
+#define QMLP_FU_EXACT(MT_, JG_, KM_, SD_, JD_, NDN_)                                      \
+    if (p.mt == MT_ && p.jg == JG_ && p.km == KM_ && p.sd == SD_ && p.jd == JD_ &&        \
+        p.ndn == NDN_)                                                                    \
+        return run(fused_layer_kernel<MT_, JG_, KM_, SD_, JD_, NDN_>);
+#define QMLP_FU_GENERIC(MT_, SD_, NDN_)                                                   \
+    if (p.mt == MT_ && p.sd == SD_ && p.ndn == NDN_)                                      \
+        return run(fused_layer_kernel<MT_, 8, 6, SD_, 8, NDN_>);
+#define QMLP_FU_MT(MT_)                                                                   \
+    QMLP_FU_EXACT(MT_, 5, 2, 64, 5, 2) QMLP_FU_EXACT(MT_, 8, 2, 64, 6, 2)               \
+    QMLP_FU_EXACT(MT_, 1, 1, 8, 6, 1)                                                     \
+    QMLP_FU_GENERIC(MT_, 8, 1) QMLP_FU_GENERIC(MT_, 8, 2)                                 \
+    QMLP_FU_GENERIC(MT_, 64, 1) QMLP_FU_GENERIC(MT_, 64, 2)
+
+hipError_t launch_fused(GateUpArgs gu, DownArgs dn, const uint16_t* Ag, const uint16_t* Au,
+                        float* t, uint16_t* h, unsigned* ctl, hipStream_t st) {
+    const FusedPlan p = plan_fused(gu.M, gu.d, gu.f, gu.g, gu.r);
+    if (!p.ok)
+        return hipErrorInvalidValue;
+    gu.uc = gu.d / 64;
+    dn.uc = dn.f / 32;
+    FusedArgs fa{gu, dn, Ag, Au, t, h, ctl, p.gu_items, p.dn_items, p.nguw,
+                 p.lds_stage, p.gu_meta_bytes, p.wmeta_bytes};
+    auto run = [&](auto kernel) -> hipError_t {
+        hipError_t e = set_lds(kernel, p.lds);
+        if (e != hipSuccess)
+            return e;
+        kernel<<<p.grid, FW * 64, p.lds, st>>>(fa);
+        return hipGetLastError();
+    };
+    QMLP_FU_MT(1) QMLP_FU_MT(2) QMLP_FU_MT(4)
+    return hipErrorInvalidValue;
+}
+
+}  // namespace qmlp

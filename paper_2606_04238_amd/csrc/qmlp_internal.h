@@ -1,0 +1,54 @@
+// Kernel argument blocks and launchers shared between the C-ABI layer and
+// the kernel translation units of libqmlp (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace qmlp {
+
+struct GateUpArgs {
+    const uint32_t* cg;      // gate codes [f][d/16] words
+    const uint32_t* mg;      // gate meta  [f][d/g]  (scale | zero << 16)
+    const uint32_t* cu;      // up codes
+    const uint32_t* mu;      // up meta
+    const uint16_t* Bg;      // [f][r] binary16
+    const uint16_t* Bu;      // [f][r] binary16
+    const float* t;          // [M][2r] fp32: A_g x then A_u x
+    const uint16_t* x;       // [M][d] binary16
+    uint16_t* h;             // [M][f] binary16
+    int M, d, f, g, r;
+    int uc;                  // units per LDS chunk (set by the launcher)
+    float lora_scale;
+};
+
+struct DownArgs {
+    const uint32_t* cd;      // down codes [d][f/8] words
+    const uint32_t* md;      // down meta  [d][f/g]
+    const uint16_t* h;       // [M][f] binary16
+    uint16_t* y;             // [M][d] binary16
+    int M, d, f, g;
+    int uc;
+};
+
+hipError_t launch_pack(int bits, const float* W, int n, int k, int g, uint32_t* codes,
+                       uint32_t* meta, int32_t* status, hipStream_t st);
+hipError_t launch_unpack(int bits, const uint32_t* codes, const uint32_t* meta, int n, int k,
+                         int g, uint8_t* out_codes, uint16_t* scales, uint16_t* zeros,
+                         hipStream_t st);
+hipError_t launch_dequant(int bits, const uint32_t* codes, const uint32_t* meta, int n, int k,
+                          int g, uint16_t* out, hipStream_t st);
+
+hipError_t launch_lora_a(const uint16_t* Ag, const uint16_t* Au, const uint16_t* x, int M, int d,
+                         int r, float* t, hipStream_t st);
+hipError_t launch_gateup(GateUpArgs args, hipStream_t st);
+hipError_t launch_down(DownArgs args, hipStream_t st);
+bool decode_shape_supported(int d, int f);
+
+// One kernel per layer (decode_fused.hip).  ctl: 4 control words at the start
+// of the workspace, zero before the first call and left zero by every call.
+bool fused_supported(int M, int d, int f, int g, int r);
+hipError_t launch_fused(GateUpArgs gu, DownArgs dn, const uint16_t* Ag, const uint16_t* Au,
+                        float* t, uint16_t* h, unsigned* ctl, hipStream_t st);
+
+}  // namespace qmlp
