@@ -108,15 +108,15 @@ size_t qmlp_codes_bytes(int bits, int n_out, int k_in);
 size_t qmlp_meta_bytes(int n_out, int k_in, int group);
 
 /* Workspace bytes qmlp_forward / qmlp_gateup_w2_lora need for this block at
- * M tokens (0 if the combination is unsupported).  Layout: 256 bytes of
- * control words (uint32: [0] LoRA-A rows published, [1] blocks whose h is
- * published, [2] blocks done, [3] sticky error bits: 1 = LoRA-A wait timed
- * out, 2 = h wait timed out), then t = A x (fp32 [M][2r]), then h
- * (activation type [M][f]).  The control words must be ZERO before the
- * first call on a workspace; every completed call leaves them zero.  After
- * an error bit appears the results of that call are invalid and the caller
- * must zero the control words again.  One workspace serves one call at a
- * time: calls that overlap in time on the same workspace race. */
+ * M tokens (0 if the combination is unsupported).  Layout: a 1024-byte
+ * control block (uint32 words: the one-kernel layer's counters and flags on
+ * separate 128-byte lines; word 160 holds sticky error bits, 1 = LoRA-A wait
+ * timed out, 2 = h wait timed out), then t = A x (fp32 [M][2r]), then h
+ * (activation type [M][f]).  The control block must be ZERO before the
+ * first call on a workspace; every completed call leaves it zero.  After an
+ * error bit appears the results of that call are invalid and the caller must
+ * zero the control block again.  One workspace serves one call at a time:
+ * calls that overlap in time on the same workspace race. */
 size_t qmlp_workspace_bytes(const qmlp_mlp *mlp, int M, qmlp_dtype dtype);
 
 /* ----------------------------------------------------- packing (offline) */

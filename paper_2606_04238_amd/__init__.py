@@ -207,12 +207,12 @@ def forward_launches(mlp: MLP, M: int, dtype=torch.float16) -> int:
 def workspace(mlp: MLP, M: int, dtype=torch.float16, device="cuda") -> torch.Tensor:
     """A zeroed workspace (its leading control words must start at zero)."""
     n = workspace_bytes(mlp, M, dtype)
-    return torch.zeros(max(n, 256), dtype=torch.uint8, device=device)
+    return torch.zeros(max(n, 1024), dtype=torch.uint8, device=device)
 
 
 def workspace_errors(ws: torch.Tensor) -> int:
     """Sticky error bits of a workspace's control block (syncs)."""
-    return int(ws[12:16].view(torch.int32).item())
+    return int(ws[640:644].view(torch.int32).item())
 
 
 def gateup_w2_lora(mlp: MLP, x: torch.Tensor, h: torch.Tensor | None = None,

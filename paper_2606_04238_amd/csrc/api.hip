@@ -69,8 +69,8 @@ qmlp_status check_mlp(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
     return QMLP_OK;
 }
 
-// Workspace: [control words, 256 B][t: M x 2r fp32][h: M x f binary16].
-constexpr size_t kCtlBytes = 256;
+// Workspace: [control words, 1 KB][t: M x 2r fp32][h: M x f binary16].
+constexpr size_t kCtlBytes = 1024;
 
 struct Workspace {
     unsigned* ctl;

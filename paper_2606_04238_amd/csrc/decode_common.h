@@ -59,7 +59,7 @@ __device__ __forceinline__ XWord stage_x_load(const uint16_t* x, int M, int d, i
 // Convert one staged word; all lanes of the wave must call it (shuffles).
 template <int MT>
 __device__ __forceinline__ void stage_x_store(uint4* xs, float2* cx, int UC, int uc, int M, int idx,
-                                              XWord v) {
+                                              XWord v, uint4* xplain = nullptr) {
     const int words = MT * uc * 4;
     const bool live = idx < words;
     const int m = live ? idx / (uc * 4) : 0;
@@ -91,6 +91,11 @@ __device__ __forceinline__ void stage_x_store(uint4* xs, float2* cx, int UC, int
         dst[(2 * w + 1) ^ (ul & 7)] = make_uint4(pr[4], pr[5], pr[6], pr[7]);
         if (w == 0)
             cx[m * UC + ul] = make_float2(1024.0f * csum, xsum);
+        if (xplain) {                          // unscaled copy (single-chunk staging only)
+            uint4* dp = xplain + (m * uc + ul) * 8 + w * 2;
+            dp[0] = make_uint4(xl[0], xl[1], xl[2], xl[3]);
+            dp[1] = make_uint4(xh[0], xh[1], xh[2], xh[3]);
+        }
     }
 }
 
@@ -588,11 +593,24 @@ __device__ __forceinline__ void fgu_finish(FGuItem<MT, S, MAXJ, KMETA>& it, cons
 template <int MT, int S, int MAXJ>
 struct FDnItem {
     uint4 q[MAXJ];
+    uint32_t e[MAXJ][4][4];      // codes unpacked to binary16 pairs (off the critical path)
     uint4 meta;                  // one 16-byte metadata chunk per lane
     float Y[MT];
     int row, row0;
     bool ok, active;
 };
+
+// Unpack the item's codes into binary16 pairs while waiting for h.
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void fdn_extract(FDnItem<MT, S, MAXJ>& it) {
+#pragma unroll
+    for (int i = 0; i < MAXJ; ++i) {
+        uint32_t wv[4] = {it.q[i].x, it.q[i].y, it.q[i].z, it.q[i].w};
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+            extract_w4(wv[w], it.e[i][w]);
+    }
+}
 
 template <int MT, int S, int MAXJ>
 __device__ __forceinline__ void fdn_load(FDnItem<MT, S, MAXJ>& it, const DownArgs& a, int row0,
@@ -643,21 +661,15 @@ __device__ __forceinline__ void fdn_accumulate(FDnItem<MT, S, MAXJ>& it, const u
             float acc[MT];
 #pragma unroll
             for (int m = 0; m < MT; ++m) acc[m] = 0.0f;
-            uint32_t wv[4] = {it.q[i].x, it.q[i].y, it.q[i].z, it.q[i].w};
-#pragma unroll
-            for (int w = 0; w < 4; ++w)
-                pin(wv[w]);
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
-                uint32_t e[4];
-                extract_w4(wv[w], e);
 #pragma unroll
                 for (int m = 0; m < MT; ++m) {
                     const uint4 p = hs[(m * UC + ul) * 4 + (w ^ ((ul >> 1) & 3))];
-                    acc[m] = dot2(e[0], p.x, acc[m]);
-                    acc[m] = dot2(e[1], p.y, acc[m]);
-                    acc[m] = dot2(e[2], p.z, acc[m]);
-                    acc[m] = dot2(e[3], p.w, acc[m]);
+                    acc[m] = dot2(it.e[i][w][0], p.x, acc[m]);
+                    acc[m] = dot2(it.e[i][w][1], p.y, acc[m]);
+                    acc[m] = dot2(it.e[i][w][2], p.z, acc[m]);
+                    acc[m] = dot2(it.e[i][w][3], p.w, acc[m]);
                 }
             }
             const uint32_t mti = wmeta[r * ng + u / upg];
@@ -683,21 +695,69 @@ __device__ __forceinline__ void fdn_finish(FDnItem<MT, S, MAXJ>& it, const DownA
 }
 
 // Device-coherent read of one staging word of h (written by other compute
-// units with device-coherent stores): four agent-scope dword loads.
+// units with device-coherent stores): a 128-bit buffer load with the
+// device-scope cache policy (sc1), so no stale cache line can be returned.
 template <int MT>
-__device__ __forceinline__ uint4 stage_h_load_coherent(const uint16_t* h, int M, int f, int u0,
-                                                       int uc, int idx) {
+__device__ __forceinline__ uint4 stage_h_load_coherent(__amdgpu_buffer_rsrc_t hrs, int f, int M,
+                                                       int u0, int uc, int idx) {
     const int words = MT * uc * 4;
     const int m = idx / (uc * 4);
     const bool ok = idx < words && m < M;
     const int wl = ok ? idx - m * uc * 4 : 0;
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(h + (long)(ok ? m : 0) * f + (long)(u0 + (wl >> 2)) * 32 + (wl & 3) * 8);
-    uint4 v;
-    v.x = __hip_atomic_load(src + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    v.y = __hip_atomic_load(src + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    v.z = __hip_atomic_load(src + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    v.w = __hip_atomic_load(src + 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return v;
+    const int off = (int)(((long)(ok ? m : 0) * f + (long)(u0 + (wl >> 2)) * 32 + (wl & 3) * 8) * 2);
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(hrs, off, 0, 16 /* sc1 */);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// LoRA-A for the fused kernel, split so its loads go out early and the
+// arithmetic runs later: one row c of [A_g; A_u] in KA 8-element chunks per
+// lane (d <= 512 * KA); x is read from the plain copy staged in LDS.
+template <int KA>
+struct LoraRow {
+    uint4 av[KA];
+};
+
+template <int KA>
+__device__ __forceinline__ void lora_a_load(LoraRow<KA>& lr, const uint16_t* Ag, const uint16_t* Au,
+                                            int d, int r, int c, int lane) {
+    const uint16_t* a = c < r ? Ag + (long)c * d : Au + (long)(c - r) * d;
+    const int nch = d / 8;
+#pragma unroll
+    for (int k = 0; k < KA; ++k) {
+        const int ch = lane + 64 * k;
+        lr.av[k] = *reinterpret_cast<const uint4*>(a + (ch < nch ? ch : 0) * 8);
+    }
+}
+
+// t[m][c] with device-coherent stores (read by other compute units).
+// xplain: the staged activation, [MT][d] binary16 in LDS.
+template <int MT, int KA>
+__device__ __forceinline__ void lora_a_finish(const LoraRow<KA>& lr, const uint4* xplain, int M,
+                                              int d, int r, int c, float* t, int lane) {
+    const int nch = d / 8;
+    float acc[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m] = 0.0f;
+#pragma unroll
+    for (int k = 0; k < KA; ++k) {
+        const int ch = lane + 64 * k;
+        if (ch < nch) {
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const uint4 xv = xplain[m * nch + ch];
+                acc[m] = dot2(lr.av[k].x, xv.x, acc[m]);
+                acc[m] = dot2(lr.av[k].y, xv.y, acc[m]);
+                acc[m] = dot2(lr.av[k].z, xv.z, acc[m]);
+                acc[m] = dot2(lr.av[k].w, xv.w, acc[m]);
+            }
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        const float v = group_sum<64>(acc[m]);
+        if (lane == 0 && m < M)
+            __hip_atomic_store(t + m * 2 * r + c, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 }
 
 // --------------------------------------------------------------- LoRA-A row

@@ -29,7 +29,7 @@
 namespace qmlp {
 
 constexpr int FW = 8;                          // waves per block
-constexpr unsigned kSpinLimit = 1u << 21;      // ~0.1 s of polling before giving up
+constexpr unsigned kSpinLimit = 1u << 20;      // ~0.2 s of polling before giving up
 constexpr size_t kFusedLds = 144 * 1024;       // one block per CU: most of the 160 KB LDS
 
 // ctl[0]: rows of t published, ctl[1]: blocks whose h rows are published,
@@ -59,25 +59,32 @@ struct FusedArgs {
 // observe the completed stores.  No cache write-back or invalidate is needed
 // (agent-scope fences on this GPU write back / invalidate the whole L2).
 // Bounded: returns false instead of spinning forever.
-__device__ __forceinline__ bool wait_at_least(unsigned* p, unsigned target) {
+__device__ __forceinline__ bool wait_flag(unsigned* p) {
     for (unsigned it = 0; it < kSpinLimit; ++it) {
-        if (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target)
+        if (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)
             return true;
-        __builtin_amdgcn_s_sleep(1);
+        __builtin_amdgcn_s_sleep(4);
     }
     return false;
 }
+
+// Control words (uint32 indices into the workspace head; each counter or
+// flag on its own 128-byte line, so pollers never contend with the adds).
+constexpr int C_TCNT = 0, C_TFLAG = 32, C_HCNT = 64, C_HFLAG = 96, C_DONE = 128, C_ERR = 160;
 
 // Waves take one of two roles (the role is wave-uniform and branched on a
 // scalar, so every wave runs exactly one path and meets the same barriers):
 //   gate/up waves (wave < nguw): metadata, gate/up codes, LoRA-B, then down
 //     items -- a straight-line load sequence, so each slot's wait covers
 //     exactly the loads before it and the gate/up math overlaps the stream;
-//   staging waves (the rest): x' staging and LoRA-A first (small loads that
-//     retire early), then their down items; the last wave also waits for t
-//     and copies it into LDS while the gate/up waves compute.
-// LDS: [x' or h' staging][t, 1 KB][per-wave metadata areas].
-template <int MT, int JG, int KM, int SD, int JD, int NDN>
+//   staging waves (the rest): their down items, and on a few of them the
+//     LoRA-A rows, computed while the gate/up waves work; the last wave also
+//     collects t into LDS.
+// Every wave first issues its share of the activation loads, then its weight
+// loads, then converts the activation into LDS: the activation is at the
+// head of every memory queue, and the weight stream is already in flight.
+// LDS: [x' | (C,X) | plain x  -- later h' | (C,X)][t, 1 KB][per-wave metadata].
+template <int MT, int JG, int KM, int KA, int SD, int JD, int NDN>
 __global__ void __launch_bounds__(FW * 64)
 fused_layer_kernel(FusedArgs fa) {
     constexpr int SG = 8, RPWG = 8, RPWD = 64 / SD;
@@ -94,92 +101,108 @@ fused_layer_kernel(FusedArgs fa) {
     char* lds = reinterpret_cast<char*>(smem);
     uint4* xs = smem;
     float2* cxg = reinterpret_cast<float2*>(smem + MT * Ug * 8);
+    uint4* xplain = smem + MT * Ug * 8 + (MT * Ug * 8 + 15) / 16;
     float* ts = reinterpret_cast<float*>(lds + fa.lds_stage);
     uint4* wmeta = reinterpret_cast<uint4*>(lds + fa.lds_stage + 1024 + wave * fa.wmeta_bytes);
     uint4* wmeta_dn = wmeta + fa.gu_meta_bytes / 16;
     const int dn_meta_chunks = RPWD * (b.f / b.g) / 4;
 
+    // 1. Activation loads first (MT words per thread cover M * Ug * 4 words).
+    XWord xw[MT];
+#pragma unroll
+    for (int k = 0; k < MT; ++k)
+        xw[k] = stage_x_load<MT>(a.x, a.M, a.d, 0, Ug, tid + k * FW * 64);
+
+    // 2. Weight loads by role.
     FGuItem<MT, SG, JG, KM> gi;
     FDnItem<MT, SD, JD> di[NDN];
+    LoraRow<KA> lr;
     const int gitem = blockIdx.x + wave * G;
-
+    const int c = blockIdx.x + G * (FW - 1 - wave);          // LoRA-A row of a staging wave
+    const bool lora_wave = wave >= nguw && a.r > 0 && c < 2 * a.r;
     if (wave < nguw) {
         const bool real = gitem < fa.gu_items;
         fgu_load(gi, a, (real ? gitem : 0) * RPWG, lane);
         if (!real)
             gi.ok = false;                      // a dummy item: computed, never stored
-#pragma unroll
-        for (int k = 0; k < NDN; ++k) {
-            const int item = blockIdx.x + ((FW - 1 - wave) + k * FW) * G;
-            const bool act = item < fa.dn_items;
-            fdn_load(di[k], b, (act ? item : 0) * RPWD, act, lane);
-        }
-    } else {
-        // x' staging: the staging waves share the M * Ug * 4 words.
-        const int sthreads = (FW - nguw) * 64, st = tid - nguw * 64;
-        const int words = MT * Ug * 4;
-        for (int idx0 = 0; idx0 < words; idx0 += sthreads * MT) {
-            XWord xw[MT];
-#pragma unroll
-            for (int k = 0; k < MT; ++k)
-                xw[k] = stage_x_load<MT>(a.x, a.M, a.d, 0, Ug, idx0 + st + k * sthreads);
-#pragma unroll
-            for (int k = 0; k < MT; ++k)
-                stage_x_store<MT>(xs, cxg, Ug, Ug, a.M, idx0 + st + k * sthreads, xw[k]);
-        }
-        // LoRA-A rows: the highest waves of the first blocks.
-        const int c = blockIdx.x + G * (FW - 1 - wave);
-        if (a.r > 0 && c < 2 * a.r) {
-            lora_a_row<MT, 12 / MT>(fa.Ag, fa.Au, a.x, a.M, a.d, a.r, c, fa.t, lane);
-            __builtin_amdgcn_s_waitcnt(0);      // t stored (device-coherent) before the count
-            if (lane == 0)
-                __hip_atomic_fetch_add(&ctl[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-#pragma unroll
-        for (int k = 0; k < NDN; ++k) {
-            const int item = blockIdx.x + ((FW - 1 - wave) + k * FW) * G;
-            const bool act = item < fa.dn_items;
-            fdn_load(di[k], b, (act ? item : 0) * RPWD, act, lane);
-        }
+    } else if (lora_wave) {
+        lora_a_load(lr, fa.Ag, fa.Au, a.d, a.r, c, lane);
     }
-    __syncthreads();                            // x' staged
+#pragma unroll
+    for (int k = 0; k < NDN; ++k) {
+        const int item = blockIdx.x + ((FW - 1 - wave) + k * FW) * G;
+        const bool act = item < fa.dn_items;
+        fdn_load(di[k], b, (act ? item : 0) * RPWD, act, lane);
+    }
 
+    // 3. Activation into LDS (waits for the activation loads only).
+#pragma unroll
+    for (int k = 0; k < MT; ++k)
+        stage_x_store<MT>(xs, cxg, Ug, Ug, a.M, tid + k * FW * 64, xw[k], xplain);
+    __syncthreads();
+
+    // 4. Gate/up dot products as the stream arrives; meanwhile LoRA-A.
     if (wave < nguw) {
-        // Gate/up dot products, slot by slot as the stream arrives.
         fgu_meta_to_lds(gi, a, wmeta, lane);
         fgu_accumulate(gi, xs, cxg, Ug, a.d, a.g, reinterpret_cast<const uint32_t*>(wmeta), lane);
-    } else if (wave == FW - 1 && a.r > 0) {
-        // t = [A_g; A_u] x from the LoRA-A waves, into LDS.
-        if (!wait_at_least(&ctl[0], 2u * a.r) && lane == 0)
-            atomicOr(&ctl[3], 1u);
-        for (int i = lane; i < a.M * 2 * a.r; i += 64)
-            ts[i] = __hip_atomic_load(fa.t + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+        if (lora_wave) {
+            lora_a_finish<MT, KA>(lr, xplain, a.M, a.d, a.r, c, fa.t, lane);
+            __builtin_amdgcn_s_waitcnt(0);      // t stored before it is counted
+            if (lane == 0) {
+                const unsigned old = __hip_atomic_fetch_add(&ctl[C_TCNT], 1u, __ATOMIC_RELAXED,
+                                                            __HIP_MEMORY_SCOPE_AGENT);
+                if (old == 2u * a.r - 1)
+                    __hip_atomic_store(&ctl[C_TFLAG], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        if (wave == FW - 1 && a.r > 0) {
+            if (!wait_flag(&ctl[C_TFLAG]) && lane == 0)
+                atomicOr(&ctl[C_ERR], 1u);
+            for (int i = lane; i < a.M * 2 * a.r; i += 64)
+                ts[i] = __hip_atomic_load(fa.t + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
     __syncthreads();                            // t in LDS
     if (wave < nguw)
         fgu_finish(gi, a, ts, fa.h, lane);
 
-    // Publish this block's h rows (device-coherent stores complete, block
-    // barrier, one relaxed count by thread 0), then wait for every block's.
+    // 5. Unpack the down codes while the other blocks finish gate/up (when
+    //    the unpacked items fit in registers; else each just before its use).
+    constexpr bool kPre = NDN * JD * 16 <= 160;
+    if constexpr (kPre) {
+#pragma unroll
+        for (int k = 0; k < NDN; ++k)
+            fdn_extract(di[k]);
+    }
+
+    // 6. Publish this block's h rows (device-coherent stores complete, block
+    //    barrier, one count by thread 0; the last block raises the flag),
+    //    then wait for the flag.
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0) {
-        __hip_atomic_fetch_add(&ctl[1], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_ok = wait_at_least(&ctl[1], (unsigned)G);
+        const unsigned old = __hip_atomic_fetch_add(&ctl[C_HCNT], 1u, __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
+        if (old == (unsigned)G - 1)
+            __hip_atomic_store(&ctl[C_HFLAG], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_ok = wait_flag(&ctl[C_HFLAG]);
         if (!s_ok)
-            atomicOr(&ctl[3], 2u);
+            atomicOr(&ctl[C_ERR], 2u);
     }
     __syncthreads();
 
-    // Down projection over the staged intermediate.
+    // 7. Down projection over the staged intermediate.
     {
 #pragma unroll
         for (int k = 0; k < NDN; ++k)
             fdn_meta_to_lds(di[k], b, wmeta_dn + k * dn_meta_chunks, lane);
+        const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(
+            fa.h, 0, b.M * b.f * 2, 0x00020000);
         uint4 hw[4 * MT];
 #pragma unroll
         for (int k = 0; k < 4 * MT; ++k)
-            hw[k] = stage_h_load_coherent<MT>(fa.h, b.M, b.f, 0, Ud, tid + k * FW * 64);
+            hw[k] = stage_h_load_coherent<MT>(hrs, b.f, b.M, 0, Ud, tid + k * FW * 64);
         uint4* hs = smem;
         float2* cx = reinterpret_cast<float2*>(smem + MT * Ud * 4);
 #pragma unroll
@@ -187,23 +210,28 @@ fused_layer_kernel(FusedArgs fa) {
             stage_h_store<MT>(hs, cx, Ud, Ud, b.M, tid + k * FW * 64, hw[k]);
         __syncthreads();
 #pragma unroll
-        for (int k = 0; k < NDN; ++k)
+        for (int k = 0; k < NDN; ++k) {
+            if constexpr (!kPre)
+                fdn_extract(di[k]);
             fdn_accumulate(di[k], hs, cx, Ud, b.f, b.g,
                            reinterpret_cast<const uint32_t*>(wmeta_dn + k * dn_meta_chunks), lane);
+        }
     }
 #pragma unroll
     for (int k = 0; k < NDN; ++k)
         fdn_finish(di[k], b, lane);
 
-    // The last block past the h wait returns the counters to zero (no block
-    // reads them after passing that wait).
+    // 8. The last block past the h wait returns the control words to zero
+    //    (no block reads them after passing that wait).
     if (tid == 0) {
-        const unsigned old = __hip_atomic_fetch_add(&ctl[2], 1u, __ATOMIC_RELAXED,
+        const unsigned old = __hip_atomic_fetch_add(&ctl[C_DONE], 1u, __ATOMIC_RELAXED,
                                                     __HIP_MEMORY_SCOPE_AGENT);
         if (old == (unsigned)G - 1) {
-            __hip_atomic_store(&ctl[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&ctl[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&ctl[2], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctl[C_TCNT], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctl[C_TFLAG], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctl[C_HCNT], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctl[C_HFLAG], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctl[C_DONE], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }
@@ -227,7 +255,7 @@ int cu_count() {
 }
 
 struct FusedPlan {
-    int mt, jg, km, sd, jd, ndn, nguw, grid, gu_items, dn_items;
+    int mt, jg, km, ka, sd, jd, ndn, nguw, grid, gu_items, dn_items;
     int lds_stage, gu_meta_bytes, wmeta_bytes;
     size_t lds;
     bool ok;
@@ -251,7 +279,7 @@ FusedPlan plan_fused(int M, int d, int f, int g, int r) {
     // down: one 16-byte chunk per lane
     p.km = (2 * 8 * ng / 4 + 63) / 64;
     const int rpwd = 64 / p.sd;
-    if (p.km > 6 || (rpwd * ngd) % 4 != 0 || rpwd * ngd / 4 > 64)
+    if (p.km > 4 || (rpwd * ngd) % 4 != 0 || rpwd * ngd / 4 > 64)
         return p;
     p.grid = cu_count();
     if (p.grid <= 0)
@@ -267,14 +295,23 @@ FusedPlan plan_fused(int M, int d, int f, int g, int r) {
     if (p.ndn > 2)
         return p;
     // The h' staging holds at most 4*MT words per thread.
-    if (p.mt * Ud * 4 > 4 * p.mt * FW * 64)
+    if (p.mt * Ud * 4 > 4 * p.mt * FW * 64 || Ug > 128)
         return p;
-    const size_t lg = (size_t)p.mt * Ug * GU_UNIT_BYTES;
+    p.ka = (d / 8 + 63) / 64;                   // LoRA-A chunks per lane (<= 8 as d <= 4096)
+    // x' + (C, X) + the plain activation, or h' + (C, X)
+    const size_t lg = (size_t)p.mt * Ug * GU_UNIT_BYTES + 16 + (size_t)p.mt * d * 2;
     const size_t ld = (size_t)p.mt * Ud * DN_UNIT_BYTES;
     p.lds_stage = (int)((lg > ld ? lg : ld) + 15) / 16 * 16;
     p.gu_meta_bytes = 2 * 8 * ng * 4;
     p.wmeta_bytes = p.gu_meta_bytes + p.ndn * rpwd * ngd * 4;
     p.lds = (size_t)p.lds_stage + 1024 + (size_t)FW * p.wmeta_bytes;
+    // The generic 8-slot instance at 4 tokens with two down items a wave
+    // does not fit in registers: such shapes take the three-kernel path.
+    const bool exact = (p.jg == 5 && p.km == 2 && p.ka == 5 && p.sd == 64 && p.jd == 5 && p.ndn == 2) ||
+                       (p.jg == 8 && p.km == 2 && p.ka == 8 && p.sd == 64 && p.jd == 6 && p.ndn == 2) ||
+                       (p.jg == 1 && p.km == 1 && p.ka == 1 && p.sd == 8 && p.jd == 6 && p.ndn == 1);
+    if (!exact && p.mt == 4 && p.ndn == 2)
+        return p;
     p.ok = p.lds <= kFusedLds;
     return p;
 }
@@ -285,18 +322,18 @@ bool fused_supported(int M, int d, int f, int g, int r) { return plan_fused(M, d
 
 // Exact slot counts for the common shapes, else the 8-slot generic instance
 // (slots past the row are dummies).
-#define QMLP_FU_EXACT(MT_, JG_, KM_, SD_, JD_, NDN_)                                      \
-    if (p.mt == MT_ && p.jg == JG_ && p.km == KM_ && p.sd == SD_ && p.jd == JD_ &&        \
-        p.ndn == NDN_)                                                                    \
-        return run(fused_layer_kernel<MT_, JG_, KM_, SD_, JD_, NDN_>);
+#define QMLP_FU_EXACT(MT_, JG_, KM_, KA_, SD_, JD_, NDN_)                                 \
+    if (p.mt == MT_ && p.jg == JG_ && p.km == KM_ && p.ka == KA_ && p.sd == SD_ &&        \
+        p.jd == JD_ && p.ndn == NDN_)                                                     \
+        return run(fused_layer_kernel<MT_, JG_, KM_, KA_, SD_, JD_, NDN_>);
 #define QMLP_FU_GENERIC(MT_, SD_, NDN_)                                                   \
     if (p.mt == MT_ && p.sd == SD_ && p.ndn == NDN_)                                      \
-        return run(fused_layer_kernel<MT_, 8, 6, SD_, 8, NDN_>);
+        return run(fused_layer_kernel<MT_, 8, 4, 8, SD_, 8, NDN_>);
 #define QMLP_FU_MT(MT_)                                                                   \
-    QMLP_FU_EXACT(MT_, 5, 2, 64, 5, 2) QMLP_FU_EXACT(MT_, 8, 2, 64, 6, 2)               \
-    QMLP_FU_EXACT(MT_, 1, 1, 8, 6, 1)                                                     \
-    QMLP_FU_GENERIC(MT_, 8, 1) QMLP_FU_GENERIC(MT_, 8, 2)                                 \
-    QMLP_FU_GENERIC(MT_, 64, 1) QMLP_FU_GENERIC(MT_, 64, 2)
+    QMLP_FU_EXACT(MT_, 5, 2, 5, 64, 5, 2) QMLP_FU_EXACT(MT_, 8, 2, 8, 64, 6, 2)         \
+    QMLP_FU_EXACT(MT_, 1, 1, 1, 8, 6, 1)                                                  \
+    QMLP_FU_GENERIC(MT_, 8, 1) QMLP_FU_GENERIC(MT_, 64, 1)
+#define QMLP_FU_MT2(MT_) QMLP_FU_GENERIC(MT_, 8, 2) QMLP_FU_GENERIC(MT_, 64, 2)
 
 hipError_t launch_fused(GateUpArgs gu, DownArgs dn, const uint16_t* Ag, const uint16_t* Au,
                         float* t, uint16_t* h, unsigned* ctl, hipStream_t st) {
@@ -314,7 +351,7 @@ hipError_t launch_fused(GateUpArgs gu, DownArgs dn, const uint16_t* Ag, const ui
         kernel<<<p.grid, FW * 64, p.lds, st>>>(fa);
         return hipGetLastError();
     };
-    QMLP_FU_MT(1) QMLP_FU_MT(2) QMLP_FU_MT(4)
+    QMLP_FU_MT(1) QMLP_FU_MT(2) QMLP_FU_MT(4) QMLP_FU_MT2(1) QMLP_FU_MT2(2)
     return hipErrorInvalidValue;
 }
 

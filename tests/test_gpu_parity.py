@@ -175,7 +175,7 @@ def test_zero_B_equals_zero_scale_bitwise_and_rank0_within_tol(q):
     m_zero_scale = gpu_mlp(L, lora_scale=0.0)
     m_rank0 = gpu_mlp(L, rank=False)
     ws = q.workspace(m_zero_b, cfg.M)
-    ws[256:].fill_(0x7F)                # garbage in the data part of the workspace
+    ws[1024:].fill_(0x7F)               # garbage in the data part of the workspace
     y0 = q.forward(m_zero_b, x, ws=ws)
     y1 = q.forward(m_zero_scale, x)
     y2 = q.forward(m_rank0, x)
@@ -262,7 +262,7 @@ def test_empty_batch_is_a_noop(q):
     L = wl.layer(cfg, 0)
     mlp = gpu_mlp(L)
     x = torch.empty((0, cfg.d), dtype=torch.float16, device="cuda")
-    y = q.forward(mlp, x, ws=torch.empty(16, dtype=torch.uint8, device="cuda"))
+    y = q.forward(mlp, x, ws=torch.zeros(1024, dtype=torch.uint8, device="cuda"))
     assert y.shape == (0, cfg.d)
 
 
@@ -298,7 +298,7 @@ def test_fused_forward_leaves_control_words_zero(q, name):
     ws = q.workspace(mlp, cfg.M)
     ys = [q.forward(mlp, x, ws=ws) for _ in range(5)]
     torch.cuda.synchronize()
-    assert int(ws[:16].view(torch.int32).abs().sum().item()) == 0
+    assert int(ws[:1024].view(torch.int32).abs().sum().item()) == 0
     assert q.workspace_errors(ws) == 0
     for y in ys[1:]:
         assert torch.equal(y.view(torch.int16), ys[0].view(torch.int16))
