@@ -12,7 +12,10 @@ timed region.  Prints one JSON line:
              scale/zero + LoRA factors + x in + y out; the intermediate h
              excluded, as the fused gate-activation-down keeps it on-chip);
   roofline = the dominant kernel's algorithmic bytes per launch over its
-             average launch duration (HIP events on the launch stream);
+             average launch duration (HIP events on the launch stream over
+             the timed region); traffic = HBM bytes per launch from the
+             rocprofv3 byte counters summarized under profiles/, reported
+             only while the HIP sources match the ones profiled;
   cpu_baseline = the fp64 oracle timed on a bounded sample of the same
              stack on this host (reported baseline only).
 """
@@ -33,6 +36,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 import workloads as wl  # noqa: E402
+from paper_2606_04238_amd.profiling import read_traffic  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
 METRIC = BASE_METRIC = ("achieved HBM GB/s (% of MI355X peak) and µs per W4/W2-GateUp MLP "
@@ -201,6 +205,9 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--mode", default="graph", choices=["graph", "eager"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="after timing, run one copy-like elementwise kernel over this many MiB "
+                         "(read N, write N) as the reference dispatch for HBM byte counters")
     args = ap.parse_args(argv)
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -238,16 +245,24 @@ def main(argv=None):
         torch.cuda.synchronize()
         graph_ms, wall = time_passes(g.replay, args.steps, args.warmup)
     head = graph_ms if graph_ms is not None else eager_ms
-    t_step = statistics.median(head)
+    t_step = sum(head) / len(head)          # the K timed steps, back to back
     L = cfg.L
     B = cfg.alg_bytes()
     gbs = L * B / (t_step * 1e-3) / 1e9
     us_layer = t_step * 1e3 / L
 
     fused, k1_us, k2_us = kernel_durations(stack)
+    traffic = None
     if fused:
-        dom_name, dom_us, dom_b = "fused_layer_kernel (whole MLP step)", k1_us, B
-        kernel_us = {"fused_layer": round(k1_us, 3)}
+        # One launch per layer: the timed region holds K * L launches of the
+        # fused kernel back to back on the replay stream, so its events give
+        # the average launch duration (inter-launch gaps included).
+        dom_name, dom_b = "fused_layer_kernel", B
+        dom_us = t_step * 1e3 / L
+        kernel_us = {"fused_layer_timed_region_avg": round(dom_us, 3),
+                     "fused_layer_event_bracketed": round(k1_us, 3)}
+        traffic = read_traffic(os.path.join(ROOT, "profiles", "fused_layer_%s.md" % cfg.name),
+                               dom_name)
     else:
         gu_b, dn_b = kernel_bytes(cfg)
         kernel_us = {"gateup_half": round(k1_us, 3), "down_w4": round(k2_us, 3)}
@@ -277,6 +292,7 @@ def main(argv=None):
             "alg_bytes_per_mlp_step": B,
             "mode": "hip_graph" if graph_ms is not None else "eager",
             "eager_us_per_mlp_step": round(statistics.median(eager_ms) * 1e3 / L, 3),
+            "median_ms_per_step": round(statistics.median(head), 4),
             "p10_p90_ms_per_step": [round(float(np.percentile(head, 10)), 4),
                                     round(float(np.percentile(head, 90)), 4)],
             "kernel_us": kernel_us,
@@ -290,9 +306,18 @@ def main(argv=None):
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": None if traffic is None else int(traffic),
         },
     }
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib << 20
+        src = torch.ones(n // 2, dtype=torch.float16, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        log("copy calibration: %d bytes read, %d bytes written" % (n, n))
+        del src, dst
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, args.seed)
     print(json.dumps(out), flush=True)
