@@ -60,31 +60,75 @@ qmlp_status check_mlp(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
     }
     if (M < 0)
         return QMLP_ERR_SHAPE;
-    if (M > 16)
-        return QMLP_ERR_UNSUPPORTED;             // prefill-chunk path: not in this build
+    if (dtype == QMLP_BF16) {                    // prefill-chunk path
+        if (M != 0 && !prefill_supported(M, d, f, mlp->gate.group, mlp->rank))
+            return QMLP_ERR_UNSUPPORTED;
+        return QMLP_OK;
+    }
     if (dtype != QMLP_F16)
-        return QMLP_ERR_UNSUPPORTED;             // decode runs in binary16
+        return QMLP_ERR_UNSUPPORTED;
+    if (M > 16)                                  // decode runs in binary16 at 1..16 tokens
+        return QMLP_ERR_UNSUPPORTED;
     if (!decode_shape_supported(d, f))
         return QMLP_ERR_UNSUPPORTED;
     return QMLP_OK;
 }
 
-// Workspace: [control words, 1 KB][t: M x 2r fp32][h: M x f binary16].
+// Workspace: [control words, 1 KB][t: fp32][h: M x f activation type]
+// [T: M x 2r bfloat16, prefill only].  t is M x 2r on the decode path and
+// S x M x 2r split-K partials on the prefill path.
 constexpr size_t kCtlBytes = 1024;
 
 struct Workspace {
     unsigned* ctl;
     float* t;
     uint16_t* h;
+    uint16_t* T;
 };
 
-size_t ws_t_bytes(const qmlp_mlp* mlp, int M) { return round256((size_t)M * 2 * mlp->rank * 4); }
+size_t ws_t_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
+    const size_t S = dtype == QMLP_BF16 ? (size_t)prefill_splits(mlp->gate.k_in) : 1;
+    return round256(S * (size_t)M * 2 * mlp->rank * 4);
+}
 size_t ws_h_bytes(const qmlp_mlp* mlp, int M) { return round256((size_t)M * mlp->gate.n_out * 2); }
+size_t ws_T_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
+    return dtype == QMLP_BF16 ? round256((size_t)M * 2 * mlp->rank * 2) : 0;
+}
 
-Workspace carve(const qmlp_mlp* mlp, int M, void* ws) {
+Workspace carve(const qmlp_mlp* mlp, int M, qmlp_dtype dtype, void* ws) {
     char* base = static_cast<char*>(ws);
+    const size_t tb = ws_t_bytes(mlp, M, dtype), hb = ws_h_bytes(mlp, M);
     return {reinterpret_cast<unsigned*>(base), reinterpret_cast<float*>(base + kCtlBytes),
-            reinterpret_cast<uint16_t*>(base + kCtlBytes + ws_t_bytes(mlp, M))};
+            reinterpret_cast<uint16_t*>(base + kCtlBytes + tb),
+            reinterpret_cast<uint16_t*>(base + kCtlBytes + tb + hb)};
+}
+
+// The prefill-chunk gate/up half: LoRA-A (split K + reduction), then the
+// MFMA gate/up kernel with the LoRA products and SiLU(G) * U.
+qmlp_status run_prefill_gateup(const qmlp_mlp* mlp, const void* x, int M, uint16_t* h,
+                               const Workspace& w, hipStream_t st) {
+    const int d = mlp->gate.k_in, f = mlp->gate.n_out, r = mlp->rank;
+    if (r > 0) {
+        hipError_t e = launch_prefill_lora(static_cast<const uint16_t*>(mlp->A_gate),
+                                           static_cast<const uint16_t*>(mlp->A_up),
+                                           static_cast<const uint16_t*>(x), M, d, r,
+                                           mlp->lora_scale, w.t, w.T, st);
+        if (e != hipSuccess)
+            return QMLP_ERR_HIP;
+    }
+    return from_hip(launch_prefill_gateup(
+        static_cast<const uint32_t*>(mlp->gate.codes), static_cast<const uint32_t*>(mlp->gate.meta),
+        static_cast<const uint32_t*>(mlp->up.codes), static_cast<const uint32_t*>(mlp->up.meta),
+        static_cast<const uint16_t*>(x), w.T, static_cast<const uint16_t*>(mlp->B_gate),
+        static_cast<const uint16_t*>(mlp->B_up), h, M, d, f, mlp->gate.group, r, st));
+}
+
+qmlp_status run_prefill_down(const qmlp_qweight* down, const void* h, int M, void* y,
+                             hipStream_t st) {
+    return from_hip(launch_prefill_down(static_cast<const uint32_t*>(down->codes),
+                                        static_cast<const uint32_t*>(down->meta),
+                                        static_cast<const uint16_t*>(h), static_cast<uint16_t*>(y),
+                                        M, down->n_out, down->k_in, down->group, st));
 }
 
 GateUpArgs gateup_args(const qmlp_mlp* mlp, const void* x, int M, uint16_t* h, const float* t) {
@@ -193,7 +237,7 @@ size_t qmlp_workspace_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
         return 0;
     if (M == 0)
         return 0;
-    return kCtlBytes + ws_t_bytes(mlp, M) + ws_h_bytes(mlp, M);
+    return kCtlBytes + ws_t_bytes(mlp, M, dtype) + ws_h_bytes(mlp, M) + ws_T_bytes(mlp, M, dtype);
 }
 
 qmlp_status qmlp_pack_w2(const float* W, int n_out, int k_in, int group, qmlp_qweight* out,
@@ -221,7 +265,10 @@ qmlp_status qmlp_gateup_w2_lora(const qmlp_mlp* mlp, const void* x, int M, qmlp_
         return QMLP_ERR_WORKSPACE;
     if (!aligned16(ws))
         return QMLP_ERR_ALIGN;
-    Workspace w = carve(mlp, M, ws);
+    Workspace w = carve(mlp, M, dtype, ws);
+    if (dtype == QMLP_BF16)
+        return run_prefill_gateup(mlp, x, M, static_cast<uint16_t*>(h), w,
+                                  static_cast<hipStream_t>(stream));
     return run_gateup(mlp, x, M, static_cast<uint16_t*>(h), w.t, static_cast<hipStream_t>(stream));
 }
 
@@ -234,14 +281,20 @@ qmlp_status qmlp_down_w4(const qmlp_qweight* down, const void* h, int M, qmlp_dt
         return QMLP_ERR_SHAPE;
     if (M < 0)
         return QMLP_ERR_SHAPE;
-    if (M > 16 || dtype != QMLP_F16 || !decode_shape_supported(down->n_out, down->k_in))
+    if (dtype == QMLP_BF16) {
+        if (M != 0 && (M % 128 != 0 || down->n_out % 128 != 0))
+            return QMLP_ERR_UNSUPPORTED;
+    } else if (M > 16 || dtype != QMLP_F16 || !decode_shape_supported(down->n_out, down->k_in)) {
         return QMLP_ERR_UNSUPPORTED;
+    }
     if (M == 0)
         return QMLP_OK;
     if (!h || !y)
         return QMLP_ERR_NULL;
     if (!aligned16(h) || !aligned16(y))
         return QMLP_ERR_ALIGN;
+    if (dtype == QMLP_BF16)
+        return run_prefill_down(down, h, M, y, static_cast<hipStream_t>(stream));
     return from_hip(launch_down(down_args(down, h, M, y), static_cast<hipStream_t>(stream)));
 }
 
@@ -261,7 +314,13 @@ qmlp_status qmlp_forward(const qmlp_mlp* mlp, const void* x, int M, qmlp_dtype d
     if (!aligned16(ws))
         return QMLP_ERR_ALIGN;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    Workspace w = carve(mlp, M, ws);
+    Workspace w = carve(mlp, M, dtype, ws);
+    if (dtype == QMLP_BF16) {
+        s = run_prefill_gateup(mlp, x, M, w.h, w, st);
+        if (s != QMLP_OK)
+            return s;
+        return run_prefill_down(&mlp->down, w.h, M, y, st);
+    }
     if (fused_supported(M, mlp->gate.k_in, mlp->gate.n_out, mlp->gate.group, mlp->rank))
         return from_hip(launch_fused(gateup_args(mlp, x, M, w.h, w.t),
                                      down_args(&mlp->down, w.h, M, y),
@@ -303,6 +362,8 @@ qmlp_status qmlp_dequant(const qmlp_qweight* w, uint16_t* w_f16, qmlp_stream str
 int qmlp_forward_launches(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
     if (check_mlp(mlp, M, dtype) != QMLP_OK || M == 0)
         return 0;
+    if (dtype == QMLP_BF16)
+        return mlp->rank > 0 ? 4 : 2;
     if (fused_supported(M, mlp->gate.k_in, mlp->gate.n_out, mlp->gate.group, mlp->rank))
         return 1;
     return mlp->rank > 0 ? 3 : 2;

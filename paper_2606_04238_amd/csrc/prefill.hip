@@ -1,0 +1,472 @@
+// Prefill-chunk path of libqmlp (gfx950): M a multiple of 128 tokens,
+// bfloat16 activations.  At this size the block is a dense contraction
+// (Sec. 3.3 gated MLP over the quantized weights, Sec. 3.1 Eq. (1) for the
+// adapters), so it runs on the matrix cores: weight tiles are dequantized to
+// bfloat16 in LDS and multiplied with v_mfma_f32_32x32x16_bf16 (fp32
+// accumulation).
+//
+// Kernels (stream order):
+//   pf_lora_a  : partial t over a slice of the input dimension (split K),
+//   pf_lora_t  : t = lora_scale * sum of the partials, rounded to bfloat16,
+//   pf_gateup  : G, U tiles + the rank-r LoRA products + SiLU(G) * U -> h,
+//   pf_down    : y = dequant4(W_down) h.
+//
+// Tile engine shared by the three GEMM kernels: a block of 256 threads
+// (4 waves in a 2 x 2 grid) owns a 128-token x BN-weight-row tile and walks
+// the input dimension in steps of 64.  Each step stages the activation tile
+// (128 x 64 bf16) and the dequantized weight tile (BN x 64 bf16) in LDS,
+// rows of eight 16-byte chunks with chunk c of row r stored at c ^ (r & 7),
+// so the 16-byte fragment reads of an MFMA (32 rows, one chunk) hit 32
+// distinct banks per 8 lanes.  Two LDS buffers; the global loads of step
+// k + 1 are in flight while step k runs on the matrix cores.
+#include "qmlp_device.h"
+#include "qmlp_internal.h"
+
+namespace qmlp {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int PF_BM = 128;     // tokens per block tile
+constexpr int PF_BK = 64;      // input elements per step
+constexpr int PF_NT = 256;     // threads per block
+
+__device__ __forceinline__ int swz(int r, int c) { return r * 8 + (c ^ (r & 7)); }
+
+// 16-byte global load / LDS store through a plain vector type (HIP's uint4
+// copies are lowered to memcpy, which keeps a register tile in scratch).
+__device__ __forceinline__ uint4 ld16(const void* p) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void st16(uint4* p, const uint4& v) {
+    *reinterpret_cast<u32x4*>(p) = u32x4{v.x, v.y, v.z, v.w};
+}
+
+// Two fp32 values rounded to bfloat16 (nearest-even), packed low/high.
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+    const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ float bf2f(uint32_t bits16) {
+    return __builtin_bit_cast(float, bits16 << 16);
+}
+
+__device__ __forceinline__ f32x16_t mfma(const uint4& a, const uint4& b, const f32x16_t& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+// ------------------------------------------------------------ activation tile
+// 128 rows x 64 bf16 = 1024 chunks, 4 per thread; chunk id = tid + 256 i.
+struct ActRegs {
+    uint4 v[4];
+};
+
+__device__ __forceinline__ void act_load(ActRegs& ar, const uint16_t* A, int K, int m0, int k0,
+                                         int tid) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int id = tid + PF_NT * i, row = id >> 3, c = id & 7;
+        ar.v[i] = ld16(A + (long)(m0 + row) * K + k0 + c * 8);
+    }
+}
+
+__device__ __forceinline__ void act_store(uint4* lds, const ActRegs& ar, int tid) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int id = tid + PF_NT * i;
+        st16(&lds[swz(id >> 3, id & 7)], ar.v[i]);
+    }
+}
+
+// --------------------------------------------------------- quantized weights
+// Thread t owns tile row t >> 1 and half t & 1 (32 codes) of a 128-row tile.
+template <int BITS>
+struct QRegs {
+    uint32_t w[BITS];           // 32 codes: 2 words at 2 bits, 4 words at 4 bits
+    uint32_t meta;              // scale | zero << 16 of the row's group
+};
+
+template <int BITS>
+__device__ __forceinline__ void q_load(QRegs<BITS>& qr, const uint32_t* codes_row,
+                                       const uint32_t* meta_row, int k0, int g, int half) {
+    const uint32_t* p = codes_row + (k0 + half * 32) * BITS / 32;
+    if constexpr (BITS == 2) {
+        const uint2 v = *reinterpret_cast<const uint2*>(p);
+        qr.w[0] = v.x;
+        qr.w[1] = v.y;
+    } else {
+        const uint4 v = ld16(p);
+        qr.w[0] = v.x;
+        qr.w[1] = v.y;
+        qr.w[2] = v.z;
+        qr.w[3] = v.w;
+    }
+    qr.meta = meta_row[k0 / g];
+}
+
+// Dequantize 32 codes to bfloat16 scale * (q - zero) (one rounding: the fp32
+// value is exact, since scale has 11 significant bits and |q - zero| < 16)
+// and store them as chunks half*4 .. half*4+3 of the tile row.
+template <int BITS>
+__device__ __forceinline__ void q_store(uint4* lds, const QRegs<BITS>& qr, int row, int half) {
+    const float s = h2f(qr.meta & 0xFFFFu);
+    const float nsz = -s * h2f(qr.meta >> 16);
+    if constexpr (BITS == 2) {
+#pragma unroll
+        for (int wi = 0; wi < 2; ++wi) {
+            // byte b of m[i] holds code 4b + i of the word
+            uint32_t m[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) m[i] = (qr.w[wi] >> (2 * i)) & 0x03030303u;
+            float v[16];
+#pragma unroll
+            for (int c = 0; c < 16; ++c)
+                v[c] = __builtin_fmaf((float)((m[c & 3] >> (8 * (c >> 2))) & 0xFFu), s, nsz);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const uint4 o = make_uint4(pack_bf16(v[8 * j + 0], v[8 * j + 1]),
+                                           pack_bf16(v[8 * j + 2], v[8 * j + 3]),
+                                           pack_bf16(v[8 * j + 4], v[8 * j + 5]),
+                                           pack_bf16(v[8 * j + 6], v[8 * j + 7]));
+                st16(&lds[swz(row, half * 4 + wi * 2 + j)], o);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int wi = 0; wi < 4; ++wi) {
+            // byte b of m0 holds code 2b, of m1 code 2b + 1
+            const uint32_t m0 = qr.w[wi] & 0x0F0F0F0Fu, m1 = (qr.w[wi] >> 4) & 0x0F0F0F0Fu;
+            float v[8];
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                v[2 * b] = __builtin_fmaf((float)((m0 >> (8 * b)) & 0xFFu), s, nsz);
+                v[2 * b + 1] = __builtin_fmaf((float)((m1 >> (8 * b)) & 0xFFu), s, nsz);
+            }
+            st16(&lds[swz(row, half * 4 + wi)],
+                 make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]), pack_bf16(v[4], v[5]),
+                            pack_bf16(v[6], v[7])));
+        }
+    }
+}
+
+// ------------------------------------------------------------- MFMA step
+// One 64-wide step over LDS tiles: wave (wm, wn) multiplies its WM 32-row
+// activation tiles with its WN 32-row weight tiles.
+template <int WM, int WN>
+__device__ __forceinline__ void mfma_step(const uint4* xs, const uint4* ws, f32x16_t (&acc)[WM][WN],
+                                          int wm, int wn, int lane) {
+    const int r = lane & 31, hk = lane >> 5;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        uint4 a[WM], b[WN];
+#pragma unroll
+        for (int i = 0; i < WM; ++i) a[i] = ld16(&xs[swz(wm * 32 * WM + i * 32 + r, 2 * s + hk)]);
+#pragma unroll
+        for (int j = 0; j < WN; ++j) b[j] = ld16(&ws[swz(wn * 32 * WN + j * 32 + r, 2 * s + hk)]);
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+#pragma unroll
+            for (int j = 0; j < WN; ++j) acc[i][j] = mfma(a[i], b[j], acc[i][j]);
+    }
+}
+
+// Row of accumulator element v of lane `lane` within a 32 x 32 tile (the
+// column is lane & 31).
+__device__ __forceinline__ int acc_row(int v, int lane) {
+    return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+}
+
+// ------------------------------------------------------------ kernels
+struct PfGateUpArgs {
+    const uint32_t *cg, *mg, *cu, *mu;   // gate / up codes and meta
+    const uint16_t* x;                    // [M][d] bf16
+    const uint16_t* T;                    // [M][2r] bf16: lora_scale * (A_g x, A_u x)
+    const uint16_t *Bg, *Bu;              // [f][r] bf16
+    uint16_t* h;                          // [M][f] bf16
+    int M, d, f, g, r;
+};
+
+// Block tile: 128 tokens x 64 columns of h; the 128 weight rows are
+// gate rows n0..n0+31, up n0..n0+31, gate n0+32.., up n0+32.., so wave
+// (wm, wn) holds G and U of the same 64 x 32 outputs.
+__global__ void __launch_bounds__(PF_NT) pf_gateup_kernel(PfGateUpArgs a) {
+    constexpr int BN = 128;
+    __shared__ uint4 lds[2][(PF_BM + BN) * 8];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave & 1, wn = wave >> 1;
+    const int mtiles = a.M / PF_BM;
+    const int mt0 = blockIdx.x % mtiles, nt0 = blockIdx.x / mtiles;
+    const int m0 = mt0 * PF_BM, n0 = nt0 * 64;
+
+    const int trow = tid >> 1, half = tid & 1;
+    const int mat = (trow >> 5) & 1;
+    const int wrow = n0 + (trow >> 6) * 32 + (trow & 31);
+    const int wpr = a.d / 16, ng = a.d / a.g;
+    const uint32_t* crow = (mat ? a.cu : a.cg) + (long)wrow * wpr;
+    const uint32_t* mrow = (mat ? a.mu : a.mg) + (long)wrow * ng;
+
+    f32x16_t acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
+
+    ActRegs ar;
+    QRegs<2> qr;
+    act_load(ar, a.x, a.d, m0, 0, tid);
+    q_load<2>(qr, crow, mrow, 0, a.g, half);
+    const int nk = a.d / PF_BK;
+    for (int kt = 0; kt < nk; ++kt) {
+        uint4* xs = lds[kt & 1];
+        uint4* ws = xs + PF_BM * 8;
+        act_store(xs, ar, tid);
+        q_store<2>(ws, qr, trow, half);
+        __syncthreads();
+        {   // the next step's tiles (the last step re-reads its own: no branch)
+            const int k1 = (kt + 1 < nk ? kt + 1 : kt) * PF_BK;
+            act_load(ar, a.x, a.d, m0, k1, tid);
+            q_load<2>(qr, crow, mrow, k1, a.g, half);
+        }
+        mfma_step<2, 2>(xs, ws, acc, wm, wn, lane);
+    }
+
+    // LoRA: G += T_g B_g^T, U += T_u B_u^T over k < r (zero-padded to 16).
+    if (a.r > 0) {
+        const int r = lane & 31, hk = lane >> 5;
+        const int ncol = n0 + wn * 32 + r;
+        for (int s = 0; s * 16 < a.r; ++s) {
+            const int kk = 16 * s + 8 * hk;
+            const bool in = kk < a.r;
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const uint16_t* Bm = j ? a.Bu : a.Bg;
+                const uint4 b = in ? ld16(Bm + (long)ncol * a.r + kk) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+                for (int i = 0; i < 2; ++i) {
+                    const int m = m0 + wm * 64 + i * 32 + r;
+                    const uint4 t = in ? ld16(a.T + (long)m * 2 * a.r + j * a.r + kk)
+                                       : make_uint4(0, 0, 0, 0);
+                    acc[i][j] = mfma(t, b, acc[i][j]);
+                }
+            }
+        }
+    }
+
+    // SiLU(G) * U -> h (bf16)
+    const int col = n0 + wn * 32 + (lane & 31);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int m = m0 + wm * 64 + i * 32 + acc_row(v, lane);
+            const float G = acc[i][0][v], U = acc[i][1][v];
+            const float hv = G / (1.0f + __expf(-G)) * U;
+            const bf16x2_t p = {(__bf16)hv, (__bf16)0.0f};
+            a.h[(long)m * a.f + col] = (uint16_t)(__builtin_bit_cast(uint32_t, p) & 0xFFFFu);
+        }
+}
+
+struct PfDownArgs {
+    const uint32_t *cd, *md;     // down codes [d][f/8], meta [d][f/g]
+    const uint16_t* h;           // [M][f] bf16
+    uint16_t* y;                 // [M][d] bf16
+    int M, d, f, g;
+};
+
+__global__ void __launch_bounds__(PF_NT) pf_down_kernel(PfDownArgs a) {
+    constexpr int BN = 128;
+    __shared__ uint4 lds[2][(PF_BM + BN) * 8];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave & 1, wn = wave >> 1;
+    const int mtiles = a.M / PF_BM;
+    const int mt0 = blockIdx.x % mtiles, nt0 = blockIdx.x / mtiles;
+    const int m0 = mt0 * PF_BM, n0 = nt0 * BN;
+
+    const int trow = tid >> 1, half = tid & 1;
+    const int wpr = a.f / 8, ng = a.f / a.g;
+    const uint32_t* crow = a.cd + (long)(n0 + trow) * wpr;
+    const uint32_t* mrow = a.md + (long)(n0 + trow) * ng;
+
+    f32x16_t acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
+
+    ActRegs ar;
+    QRegs<4> qr;
+    act_load(ar, a.h, a.f, m0, 0, tid);
+    q_load<4>(qr, crow, mrow, 0, a.g, half);
+    const int nk = a.f / PF_BK;
+    for (int kt = 0; kt < nk; ++kt) {
+        uint4* xs = lds[kt & 1];
+        uint4* ws = xs + PF_BM * 8;
+        act_store(xs, ar, tid);
+        q_store<4>(ws, qr, trow, half);
+        __syncthreads();
+        {
+            const int k1 = (kt + 1 < nk ? kt + 1 : kt) * PF_BK;
+            act_load(ar, a.h, a.f, m0, k1, tid);
+            q_load<4>(qr, crow, mrow, k1, a.g, half);
+        }
+        mfma_step<2, 2>(xs, ws, acc, wm, wn, lane);
+    }
+
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int col = n0 + wn * 64 + j * 32 + (lane & 31);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = m0 + wm * 64 + i * 32 + acc_row(v, lane);
+                const bf16x2_t p = {(__bf16)acc[i][j][v], (__bf16)0.0f};
+                a.y[(long)m * a.d + col] = (uint16_t)(__builtin_bit_cast(uint32_t, p) & 0xFFFFu);
+            }
+    }
+}
+
+struct PfLoraArgs {
+    const uint16_t *Ag, *Au;     // [r][d] bf16
+    const uint16_t* x;           // [M][d] bf16
+    float* part;                 // [S][M][2r] fp32
+    int M, d, r, S;
+};
+
+// Partial t over one of S slices of the input dimension: a 128-token x
+// 64-row tile (rows >= 2r are zero).
+__global__ void __launch_bounds__(PF_NT) pf_lora_a_kernel(PfLoraArgs a) {
+    constexpr int BN = 64;
+    __shared__ uint4 lds[2][(PF_BM + BN) * 8];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave & 1, wn = wave >> 1;
+    const int mtiles = a.M / PF_BM;
+    const int mt0 = blockIdx.x % mtiles, sl = blockIdx.x / mtiles;
+    const int m0 = mt0 * PF_BM;
+    const int nk = a.d / PF_BK / a.S, kbeg = sl * nk * PF_BK;
+
+    f32x16_t acc[2][1];
+    acc[0][0] = f32x16_t{};
+    acc[1][0] = f32x16_t{};
+
+    // weight rows: 64 rows x 8 chunks = 2 chunks per thread (rows >= 2r read
+    // row 0 and are zeroed)
+    const uint16_t* src[2];
+    uint32_t live[2];                   // all ones for rows < 2r, else zero
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int id = tid + PF_NT * i, row = id >> 3, c = id & 7;
+        live[i] = row < 2 * a.r ? ~0u : 0u;
+        const uint16_t* base = row >= 2 * a.r ? a.Ag : row < a.r ? a.Ag + (long)row * a.d
+                                                                  : a.Au + (long)(row - a.r) * a.d;
+        src[i] = base + c * 8;
+    }
+    auto masked = [](uint4 v, uint32_t m) { return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m); };
+    ActRegs ar;
+    uint4 wv[2];
+    act_load(ar, a.x, a.d, m0, kbeg, tid);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        wv[i] = masked(ld16(src[i] + kbeg), live[i]);
+    }
+    for (int kt = 0; kt < nk; ++kt) {
+        uint4* xs = lds[kt & 1];
+        uint4* ws = xs + PF_BM * 8;
+        act_store(xs, ar, tid);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int id = tid + PF_NT * i;
+            st16(&ws[swz(id >> 3, id & 7)], wv[i]);
+        }
+        __syncthreads();
+        {
+            const int k1 = kbeg + (kt + 1 < nk ? kt + 1 : kt) * PF_BK;
+            act_load(ar, a.x, a.d, m0, k1, tid);
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                wv[i] = masked(ld16(src[i] + k1), live[i]);
+            }
+        }
+        mfma_step<2, 1>(xs, ws, acc, wm, wn, lane);
+    }
+    const int c = wn * 32 + (lane & 31);
+    if (c < 2 * a.r) {
+        float* out = a.part + (long)sl * a.M * 2 * a.r;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = m0 + wm * 64 + i * 32 + acc_row(v, lane);
+                out[(long)m * 2 * a.r + c] = acc[i][0][v];
+            }
+    }
+}
+
+// T[m][c] = bf16(lora_scale * sum over slices, in slice order).
+__global__ void pf_lora_t_kernel(const float* part, uint16_t* T, int M, int r, int S,
+                                 float lora_scale) {
+    const long n = (long)M * 2 * r;
+    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n)
+        return;
+    float s = 0.0f;
+    for (int k = 0; k < S; ++k) s += part[(long)k * n + i];
+    const bf16x2_t p = {(__bf16)(lora_scale * s), (__bf16)0.0f};
+    T[i] = (uint16_t)(__builtin_bit_cast(uint32_t, p) & 0xFFFFu);
+}
+
+}  // namespace
+
+bool prefill_supported(int M, int d, int f, int g, int r) {
+    (void)g;
+    (void)r;
+    return M > 0 && M % PF_BM == 0 && d % 128 == 0 && f % 64 == 0;
+}
+
+int prefill_splits(int d) {
+    const int nk = d / PF_BK;
+    for (int s = nk < 24 ? nk : 24; s > 1; --s)
+        if (nk % s == 0 && nk / s >= 2)
+            return s;
+    return 1;
+}
+
+hipError_t launch_prefill_lora(const uint16_t* Ag, const uint16_t* Au, const uint16_t* x, int M,
+                               int d, int r, float lora_scale, float* part, uint16_t* T,
+                               hipStream_t st) {
+    const int S = prefill_splits(d);
+    PfLoraArgs a{Ag, Au, x, part, M, d, r, S};
+    pf_lora_a_kernel<<<(M / PF_BM) * S, PF_NT, 0, st>>>(a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    const long n = (long)M * 2 * r;
+    pf_lora_t_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(part, T, M, r, S, lora_scale);
+    return hipGetLastError();
+}
+
+hipError_t launch_prefill_gateup(const uint32_t* cg, const uint32_t* mg, const uint32_t* cu,
+                                 const uint32_t* mu, const uint16_t* x, const uint16_t* T,
+                                 const uint16_t* Bg, const uint16_t* Bu, uint16_t* h, int M, int d,
+                                 int f, int g, int r, hipStream_t st) {
+    PfGateUpArgs a{cg, mg, cu, mu, x, T, Bg, Bu, h, M, d, f, g, r};
+    pf_gateup_kernel<<<(M / PF_BM) * (f / 64), PF_NT, 0, st>>>(a);
+    return hipGetLastError();
+}
+
+hipError_t launch_prefill_down(const uint32_t* cd, const uint32_t* md, const uint16_t* h,
+                               uint16_t* y, int M, int d, int f, int g, hipStream_t st) {
+    PfDownArgs a{cd, md, h, y, M, d, f, g};
+    pf_down_kernel<<<(M / PF_BM) * (d / 128), PF_NT, 0, st>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace qmlp

@@ -51,4 +51,17 @@ bool fused_supported(int M, int d, int f, int g, int r);
 hipError_t launch_fused(GateUpArgs gu, DownArgs dn, const uint16_t* Ag, const uint16_t* Au,
                         float* t, uint16_t* h, unsigned* ctl, hipStream_t st);
 
+// Prefill-chunk path (prefill.hip): M a multiple of 128 tokens, bfloat16.
+bool prefill_supported(int M, int d, int f, int g, int r);
+int prefill_splits(int d);
+hipError_t launch_prefill_lora(const uint16_t* Ag, const uint16_t* Au, const uint16_t* x, int M,
+                               int d, int r, float lora_scale, float* part, uint16_t* T,
+                               hipStream_t st);
+hipError_t launch_prefill_gateup(const uint32_t* cg, const uint32_t* mg, const uint32_t* cu,
+                                 const uint32_t* mu, const uint16_t* x, const uint16_t* T,
+                                 const uint16_t* Bg, const uint16_t* Bu, uint16_t* h, int M, int d,
+                                 int f, int g, int r, hipStream_t st);
+hipError_t launch_prefill_down(const uint32_t* cd, const uint32_t* md, const uint16_t* h,
+                               uint16_t* y, int M, int d, int f, int g, hipStream_t st);
+
 }  // namespace qmlp

@@ -100,6 +100,27 @@ def test_forward_validation(q, lib):
     assert _fwd(lib, m, M=0) == OK
 
 
+def test_prefill_validation(q, lib):
+    m = _mlp(q)                                     # d=256, f=512, g=64, r=8
+    # bfloat16 runs the prefill-chunk path: M a multiple of 128, d of 128
+    assert _fwd(lib, m, M=128, dtype=1, ws=0) == WS
+    assert _fwd(lib, m, M=128, dtype=1, wsb=16) == WS
+    assert _fwd(lib, m, M=100, dtype=1) == UNSUP
+    assert _fwd(lib, m, M=128, dtype=0) == UNSUP    # binary16 decode stops at 16 tokens
+    assert _fwd(lib, _mlp(q, d=320, f=448), M=128, dtype=1) == UNSUP
+    assert _fwd(lib, m, M=0, dtype=1) == OK
+    assert lib.qmlp_forward_launches(ctypes.byref(m), 256, 1) == 4
+    assert lib.qmlp_forward_launches(ctypes.byref(_mlp(q, rank=0)), 256, 1) == 2
+    assert lib.qmlp_forward_launches(ctypes.byref(m), 100, 1) == 0
+    big = _mlp(q, d=6144, f=16384, g=128, rank=32)
+    n = lib.qmlp_workspace_bytes(ctypes.byref(big), 512, 1)
+    assert n >= 1024 + 512 * 16384 * 2 + 512 * 64 * 2 + 512 * 64 * 4
+    w = _qw(q, bits=4, n=256, k=512)
+    assert lib.qmlp_down_w4(ctypes.byref(w), ctypes.c_void_p(FAKE), 100, 1,
+                            ctypes.c_void_p(FAKE), None) == UNSUP
+    assert lib.qmlp_down_w4(ctypes.byref(w), None, 128, 1, ctypes.c_void_p(FAKE), None) == NULL
+
+
 def test_workspace_bytes(q, lib):
     m = _mlp(q, d=2560, f=9728, g=128, rank=16)
     n = lib.qmlp_workspace_bytes(ctypes.byref(m), 1, 0)
