@@ -109,14 +109,16 @@ size_t qmlp_meta_bytes(int n_out, int k_in, int group);
 
 /* Workspace bytes qmlp_forward / qmlp_gateup_w2_lora need for this block at
  * M tokens (0 if the combination is unsupported).  Layout: a 1024-byte
- * control block (uint32 words: the one-kernel layer's counters and flags on
- * separate 128-byte lines; word 160 holds sticky error bits, 1 = LoRA-A wait
- * timed out, 2 = h wait timed out), then t = A x (fp32 [M][2r]), then h
- * (activation type [M][f]).  The control block must be ZERO before the
- * first call on a workspace; every completed call leaves it zero.  After an
- * error bit appears the results of that call are invalid and the caller must
- * zero the control block again.  One workspace serves one call at a time:
- * calls that overlap in time on the same workspace race. */
+ * control block (uint32 words, each on its own 128-byte line: word 0 counts
+ * the one-kernel layer's calls, word 32 its finished blocks, word 160 holds
+ * sticky error bits: 1 = t wait timed out, 2 = h wait timed out), then t
+ * (fp32), h (activation type [M][f]), on the prefill path lora_scale * t in
+ * bfloat16, and on the decode path the one-kernel layer's tagged hand-off
+ * words (one [4][64] block of 64-bit words per compute unit, [4][f] 32-bit).  The workspace must be ZERO before
+ * its first call, and zeroed again before it serves a block of another shape
+ * or after an error bit appeared (the results of that call are invalid).
+ * One workspace serves one call at a time: calls that overlap in time on the
+ * same workspace race. */
 size_t qmlp_workspace_bytes(const qmlp_mlp *mlp, int M, qmlp_dtype dtype);
 
 /* ----------------------------------------------------- packing (offline) */

@@ -205,7 +205,8 @@ def forward_launches(mlp: MLP, M: int, dtype=torch.float16) -> int:
 
 
 def workspace(mlp: MLP, M: int, dtype=torch.float16, device="cuda") -> torch.Tensor:
-    """A zeroed workspace (its leading control words must start at zero)."""
+    """A zeroed workspace (it must start at zero; zero it again before it
+    serves a block of another shape or after an error bit)."""
     n = workspace_bytes(mlp, M, dtype)
     return torch.zeros(max(n, 1024), dtype=torch.uint8, device=device)
 

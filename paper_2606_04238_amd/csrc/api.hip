@@ -75,8 +75,11 @@ qmlp_status check_mlp(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
 }
 
 // Workspace: [control words, 1 KB][t: fp32][h: M x f activation type]
-// [T: M x 2r bfloat16, prefill only].  t is M x 2r on the decode path and
-// S x M x 2r split-K partials on the prefill path.
+// [T: M x 2r bfloat16, prefill only][t64: one [4][64] copy of tagged words
+// per block of the one-kernel layer, h32: 4 x f tagged words -- decode only,
+// that kernel's hand-offs].  t is
+// M x 2r on the decode path and S x M x 2r split-K partials on the prefill
+// path.
 constexpr size_t kCtlBytes = 1024;
 
 struct Workspace {
@@ -84,6 +87,8 @@ struct Workspace {
     float* t;
     uint16_t* h;
     uint16_t* T;
+    unsigned long long* t64;
+    uint32_t* h32;
 };
 
 size_t ws_t_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
@@ -94,13 +99,20 @@ size_t ws_h_bytes(const qmlp_mlp* mlp, int M) { return round256((size_t)M * mlp-
 size_t ws_T_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
     return dtype == QMLP_BF16 ? round256((size_t)M * 2 * mlp->rank * 2) : 0;
 }
+size_t ws_t64_bytes() { return (size_t)fused_grid() * 256 * 8; }
+size_t ws_tag_bytes(const qmlp_mlp* mlp, qmlp_dtype dtype) {
+    return dtype == QMLP_F16 ? ws_t64_bytes() + round256((size_t)4 * mlp->gate.n_out * 4) : 0;
+}
 
 Workspace carve(const qmlp_mlp* mlp, int M, qmlp_dtype dtype, void* ws) {
     char* base = static_cast<char*>(ws);
     const size_t tb = ws_t_bytes(mlp, M, dtype), hb = ws_h_bytes(mlp, M);
+    char* tag = base + kCtlBytes + tb + hb + ws_T_bytes(mlp, M, dtype);
     return {reinterpret_cast<unsigned*>(base), reinterpret_cast<float*>(base + kCtlBytes),
             reinterpret_cast<uint16_t*>(base + kCtlBytes + tb),
-            reinterpret_cast<uint16_t*>(base + kCtlBytes + tb + hb)};
+            reinterpret_cast<uint16_t*>(base + kCtlBytes + tb + hb),
+            reinterpret_cast<unsigned long long*>(tag),
+            reinterpret_cast<uint32_t*>(tag + (dtype == QMLP_F16 ? ws_t64_bytes() : 0))};
 }
 
 // The prefill-chunk gate/up half: LoRA-A (split K + reduction), then the
@@ -237,7 +249,8 @@ size_t qmlp_workspace_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
         return 0;
     if (M == 0)
         return 0;
-    return kCtlBytes + ws_t_bytes(mlp, M, dtype) + ws_h_bytes(mlp, M) + ws_T_bytes(mlp, M, dtype);
+    return kCtlBytes + ws_t_bytes(mlp, M, dtype) + ws_h_bytes(mlp, M) + ws_T_bytes(mlp, M, dtype) +
+           ws_tag_bytes(mlp, dtype);
 }
 
 qmlp_status qmlp_pack_w2(const float* W, int n_out, int k_in, int group, qmlp_qweight* out,
@@ -325,7 +338,8 @@ qmlp_status qmlp_forward(const qmlp_mlp* mlp, const void* x, int M, qmlp_dtype d
         return from_hip(launch_fused(gateup_args(mlp, x, M, w.h, w.t),
                                      down_args(&mlp->down, w.h, M, y),
                                      static_cast<const uint16_t*>(mlp->A_gate),
-                                     static_cast<const uint16_t*>(mlp->A_up), w.t, w.h, w.ctl, st));
+                                     static_cast<const uint16_t*>(mlp->A_up), w.t64, w.h32, w.ctl,
+                                     st));
     s = run_gateup(mlp, x, M, w.h, w.t, st);
     if (s != QMLP_OK)
         return s;

@@ -81,10 +81,8 @@ __device__ __forceinline__ void stage_x_store(uint4* xs, float2* cx, int UC, int
         csum += h2f(ha) + h2f(hb);
         xsum += h2f(a16) + h2f(b16);
     }
-    csum += __shfl_xor(csum, 1, 64);
-    csum += __shfl_xor(csum, 2, 64);
-    xsum += __shfl_xor(xsum, 1, 64);
-    xsum += __shfl_xor(xsum, 2, 64);
+    csum = group_sum<4>(csum);
+    xsum = group_sum<4>(xsum);
     if (live) {
         uint4* dst = xs + (m * UC + ul) * 8;
         dst[(2 * w) ^ (ul & 7)] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
@@ -144,10 +142,8 @@ __device__ __forceinline__ void stage_h_store(uint4* hs, float2* cx, int UC, int
         csum += h2f(ha) + h2f(hb);
         xsum += h2f(a16) + h2f(b16);
     }
-    csum += __shfl_xor(csum, 1, 64);
-    csum += __shfl_xor(csum, 2, 64);
-    xsum += __shfl_xor(xsum, 1, 64);
-    xsum += __shfl_xor(xsum, 2, 64);
+    csum = group_sum<4>(csum);
+    xsum = group_sum<4>(xsum);
     if (live) {
         hs[(m * UC + ul) * 4 + (w ^ ((ul >> 1) & 3))] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
         if (w == 0)
@@ -227,6 +223,7 @@ template <int MT, int S, int MAXJ>
 __device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ>& it, const uint4* xs,
                                               const float2* cx, int UC, int d, int u0, int uc,
                                               int lane) {
+    const uint32_t mv = 0x64006400u;           // (the standalone kernels keep the literal)
     const int s = lane % S;
     const int J = (d / 64 + S - 1) / S;
 #pragma unroll
@@ -250,8 +247,8 @@ __device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ>& it, const uin
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
                 uint32_t eg[8], eu[8];
-                extract_w2(wg[w], eg);
-                extract_w2(wu[w], eu);
+                extract_w2(wg[w], eg, mv);
+                extract_w2(wu[w], eu, mv);
 #pragma unroll
                 for (int m = 0; m < MT; ++m) {
                     const uint4* src = xs + (m * UC + ul) * 8;
@@ -358,6 +355,7 @@ template <int MT, int S, int MAXJ>
 __device__ __forceinline__ void dn_accumulate(DnItem<MT, S, MAXJ>& it, const uint4* hs,
                                               const float2* cx, int UC, int f, int u0, int uc,
                                               int lane) {
+    const uint32_t mv = 0x64006400u;           // (the standalone kernels keep the literal)
     const int s = lane % S;
     const int J = (f / 32 + S - 1) / S;
     if (!it.active)
@@ -379,7 +377,7 @@ __device__ __forceinline__ void dn_accumulate(DnItem<MT, S, MAXJ>& it, const uin
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
                 uint32_t e[4];
-                extract_w4(wv[w], e);
+                extract_w4(wv[w], e, mv);
 #pragma unroll
                 for (int m = 0; m < MT; ++m) {
                     const uint4 p = hs[(m * UC + ul) * 4 + (w ^ ((ul >> 1) & 3))];
@@ -432,7 +430,7 @@ struct FGuItem {
 };
 
 // Loads: metadata chunks first (they retire first), then codes, then LoRA-B.
-template <int MT, int S, int MAXJ, int KMETA>
+template <int MT, int S, int MAXJ, int KMETA, int WIN = 0>
 __device__ __forceinline__ void fgu_load(FGuItem<MT, S, MAXJ, KMETA>& it, const GateUpArgs& a, int row0,
                                          int lane) {
     constexpr int RPW = 64 / S;
@@ -460,6 +458,10 @@ __device__ __forceinline__ void fgu_load(FGuItem<MT, S, MAXJ, KMETA>& it, const 
     for (int i = 0; i < MAXJ; ++i) {
         const int u = s + S * i;
         const int uu = u < U ? u : 0;
+        if constexpr (WIN > 0) {
+            if (2 * i + KMETA >= WIN)
+                vm_window<WIN - 2>();
+        }
         it.qg[i] = load_stream(cg + uu);
         it.qu[i] = load_stream(cu + uu);
     }
@@ -496,18 +498,103 @@ __device__ __forceinline__ void fgu_meta_to_lds(const FGuItem<MT, S, MAXJ, KMETA
     }
 }
 
+// Branch-free over the unit slots (a slot past the row's last unit re-reads
+// unit 0 and adds it with scale 0).  At one token the eight 16-byte x' reads
+// of slot i + 1 are issued before slot i is computed (the compiler would
+// otherwise wait on each read in turn).
+template <int MT, int S, int MAXJ, int KMETA>
+__device__ __forceinline__ void fgu_slot(FGuItem<MT, S, MAXJ, KMETA>& it, int i, int ul, bool valid,
+                                         const uint4 (&xv)[MT][8], const float2* cx, int UC, int ng,
+                                         int gsh, const uint32_t* wmeta, int r) {
+    const uint32_t mv = MT >= 4 ? 0x64006400u : magic_vgpr();   // a VGPR, except at 4 tokens
+    constexpr int RPW = 64 / S;
+    float ag[MT], au[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) ag[m] = au[m] = 0.0f;
+    uint32_t wg[4] = {it.qg[i].x, it.qg[i].y, it.qg[i].z, it.qg[i].w};
+    uint32_t wu[4] = {it.qu[i].x, it.qu[i].y, it.qu[i].z, it.qu[i].w};
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        pin(wg[w]);
+        pin(wu[w]);
+    }
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        uint32_t eg[8], eu[8];
+        extract_w2(wg[w], eg, mv);
+        extract_w2(wu[w], eu, mv);
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            const uint4 p0 = xv[m][2 * w], p1 = xv[m][2 * w + 1];
+            const uint32_t xp[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+            for (int p = 0; p < 8; ++p) {
+                ag[m] = dot2(eg[p], xp[p], ag[m]);
+                au[m] = dot2(eu[p], xp[p], au[m]);
+            }
+        }
+    }
+    const uint32_t mgi = wmeta[r * ng + (ul >> gsh)];
+    const uint32_t mui = wmeta[(RPW + r) * ng + (ul >> gsh)];
+    const float sg = valid ? h2f(mgi & 0xFFFFu) : 0.0f, zg = h2f(mgi >> 16);
+    const float su = valid ? h2f(mui & 0xFFFFu) : 0.0f, zu = h2f(mui >> 16);
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        const float2 k = cx[m * UC + ul];
+        it.G[m] += sg * (ag[m] - k.x - zg * k.y);
+        it.U[m] += su * (au[m] - k.x - zu * k.y);
+    }
+}
+
+template <int MT>
+__device__ __forceinline__ void fgu_read_x(uint4 (&xv)[MT][8], const uint4* xs, int UC, int ul) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        const uint4* src = xs + (m * UC + ul) * 8;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) xv[m][c] = src[c ^ (ul & 7)];
+    }
+}
+
 template <int MT, int S, int MAXJ, int KMETA>
 __device__ __forceinline__ void fgu_accumulate(FGuItem<MT, S, MAXJ, KMETA>& it, const uint4* xs,
                                                const float2* cx, int UC, int d, int g,
                                                const uint32_t* wmeta, int lane) {
-    constexpr int RPW = 64 / S;
+    const uint32_t mv = MT >= 4 ? 0x64006400u : magic_vgpr();   // a VGPR, except at 4 tokens
     const int s = lane % S, r = lane / S;
-    const int U = d / 64, ng = d / g, upg = g / 64;
+    const int U = d / 64, ng = d / g, gsh = g == 128 ? 1 : 0;   // units of 64 per group: 1 << gsh
+    if constexpr (MT == 1) {
+        // two buffers in turn: the reads of slot i + 1 go out before slot i
+        uint4 bx[2][1][8];
+        fgu_read_x<1>(bx[0], xs, UC, s < U ? s : 0);
 #pragma unroll
-    for (int i = 0; i < MAXJ; ++i) {
-        const int u = s + S * i;
-        if (u < U) {
-            const int ul = u;
+        for (int i = 0; i < MAXJ; ++i) {
+            const int u = s + S * i, un = u + S;
+            const bool valid = u < U;
+            if (i + 1 < MAXJ)
+                fgu_read_x<1>(bx[(i + 1) & 1], xs, UC, un < U ? un : 0);
+#pragma unroll
+            for (int c = 0; c < 8; ++c) pin4(bx[i & 1][0][c]);
+            fgu_slot(it, i, valid ? u : 0, valid, bx[i & 1], cx, UC, ng, gsh, wmeta, r);
+        }
+    } else if constexpr (MT == 2) {
+#pragma unroll
+        for (int i = 0; i < MAXJ; ++i) {
+            const int u = s + S * i;
+            const bool valid = u < U;
+            uint4 xv[MT][8];
+            fgu_read_x<MT>(xv, xs, UC, valid ? u : 0);
+            fgu_slot(it, i, valid ? u : 0, valid, xv, cx, UC, ng, gsh, wmeta, r);
+        }
+    } else {
+        // four tokens: read x' word by word (a slot's 32 reads would not fit
+        // in registers next to the weights)
+        constexpr int RPW = 64 / S;
+#pragma unroll
+        for (int i = 0; i < MAXJ; ++i) {
+            const int u = s + S * i;
+            const bool valid = u < U;
+            const int ul = valid ? u : 0;
             float ag[MT], au[MT];
 #pragma unroll
             for (int m = 0; m < MT; ++m) ag[m] = au[m] = 0.0f;
@@ -521,8 +608,8 @@ __device__ __forceinline__ void fgu_accumulate(FGuItem<MT, S, MAXJ, KMETA>& it, 
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
                 uint32_t eg[8], eu[8];
-                extract_w2(wg[w], eg);
-                extract_w2(wu[w], eu);
+                extract_w2(wg[w], eg, mv);
+                extract_w2(wu[w], eu, mv);
 #pragma unroll
                 for (int m = 0; m < MT; ++m) {
                     const uint4* src = xs + (m * UC + ul) * 8;
@@ -536,10 +623,10 @@ __device__ __forceinline__ void fgu_accumulate(FGuItem<MT, S, MAXJ, KMETA>& it, 
                     }
                 }
             }
-            const uint32_t mgi = wmeta[r * ng + u / upg];
-            const uint32_t mui = wmeta[(RPW + r) * ng + u / upg];
-            const float sg = h2f(mgi & 0xFFFFu), zg = h2f(mgi >> 16);
-            const float su = h2f(mui & 0xFFFFu), zu = h2f(mui >> 16);
+            const uint32_t mgi = wmeta[r * ng + (ul >> gsh)];
+            const uint32_t mui = wmeta[(RPW + r) * ng + (ul >> gsh)];
+            const float sg = valid ? h2f(mgi & 0xFFFFu) : 0.0f, zg = h2f(mgi >> 16);
+            const float su = valid ? h2f(mui & 0xFFFFu) : 0.0f, zu = h2f(mui >> 16);
 #pragma unroll
             for (int m = 0; m < MT; ++m) {
                 const float2 k = cx[m * UC + ul];
@@ -550,11 +637,14 @@ __device__ __forceinline__ void fgu_accumulate(FGuItem<MT, S, MAXJ, KMETA>& it, 
     }
 }
 
-// LoRA-B, row reduction, h = SiLU(G) * U written with device-coherent
-// stores (other compute units read h right after the hand-off).
+// LoRA-B, row reduction, h = SiLU(G) * U.  h is published to the other
+// compute units as tagged 32-bit words (binary16 value | tag << 16) with
+// device-coherent stores: a consumer that reads the current tag has read the
+// current value (an aligned 32-bit store is seen whole), so no flag or
+// completion wait is needed.
 template <int MT, int S, int MAXJ, int KMETA>
 __device__ __forceinline__ void fgu_finish(FGuItem<MT, S, MAXJ, KMETA>& it, const GateUpArgs& a,
-                                           const float* t, uint16_t* h, int lane) {
+                                           const float* t, uint32_t* h32, uint32_t tag, int lane) {
     const int s = lane % S;
     if (a.r > 0) {
         const int CPL = (a.r + S - 1) / S;
@@ -584,8 +674,8 @@ __device__ __forceinline__ void fgu_finish(FGuItem<MT, S, MAXJ, KMETA>& it, cons
         const float uv = group_sum<S>(it.U[m]);
         if (it.ok && m < a.M && (m % S) == s) {
             const float hv = gv / (1.0f + __expf(-gv)) * uv;
-            __hip_atomic_store(h + (long)m * a.f + it.row, (uint16_t)f2h(hv), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(h32 + (long)m * a.f + it.row, f2h(hv) | (tag << 16),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }
@@ -603,16 +693,20 @@ struct FDnItem {
 // Unpack the item's codes into binary16 pairs while waiting for h.
 template <int MT, int S, int MAXJ>
 __device__ __forceinline__ void fdn_extract(FDnItem<MT, S, MAXJ>& it) {
+    const uint32_t mv = MT >= 4 ? 0x64006400u : magic_vgpr();   // a VGPR, except at 4 tokens
 #pragma unroll
     for (int i = 0; i < MAXJ; ++i) {
         uint32_t wv[4] = {it.q[i].x, it.q[i].y, it.q[i].z, it.q[i].w};
 #pragma unroll
-        for (int w = 0; w < 4; ++w)
-            extract_w4(wv[w], it.e[i][w]);
+        for (int w = 0; w < 4; ++w) {
+            extract_w4(wv[w], it.e[i][w], mv);
+#pragma unroll
+            for (int p = 0; p < 4; ++p) pin(it.e[i][w][p]);    // computed here, not at use
+        }
     }
 }
 
-template <int MT, int S, int MAXJ>
+template <int MT, int S, int MAXJ, int WIN = 0>
 __device__ __forceinline__ void fdn_load(FDnItem<MT, S, MAXJ>& it, const DownArgs& a, int row0,
                                          bool active, int lane) {
     constexpr int RPW = 64 / S;
@@ -631,6 +725,8 @@ __device__ __forceinline__ void fdn_load(FDnItem<MT, S, MAXJ>& it, const DownArg
 #pragma unroll
     for (int i = 0; i < MAXJ; ++i) {
         const int u = s + S * i;
+        if constexpr (WIN > 0)
+            vm_window<WIN - 1>();               // the wave's earlier loads count too
         it.q[i] = load_stream(cd + (u < U ? u : 0));
     }
 #pragma unroll
@@ -645,19 +741,71 @@ __device__ __forceinline__ void fdn_meta_to_lds(const FDnItem<MT, S, MAXJ>& it, 
         wmeta[lane] = it.meta;
 }
 
+// Branch-free over the unit slots like fgu_accumulate (an inactive item is
+// skipped by a wave-uniform branch); at one token the h' reads of slot i + 1
+// are in flight while slot i is computed.
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void fdn_read_h(uint4 (&hv)[MT][4], const uint4* hs, int UC, int ul) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) hv[m][w] = hs[(m * UC + ul) * 4 + (w ^ ((ul >> 1) & 3))];
+}
+
+template <int MT, int S, int MAXJ>
+__device__ __forceinline__ void fdn_slot(FDnItem<MT, S, MAXJ>& it, int i, int ul, bool valid,
+                                         const uint4 (&hv)[MT][4], const float2* cx, int UC, int ng,
+                                         int gsh, const uint32_t* wmeta, int r) {
+    float acc[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m] = 0.0f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            const uint4 p = hv[m][w];
+            acc[m] = dot2(it.e[i][w][0], p.x, acc[m]);
+            acc[m] = dot2(it.e[i][w][1], p.y, acc[m]);
+            acc[m] = dot2(it.e[i][w][2], p.z, acc[m]);
+            acc[m] = dot2(it.e[i][w][3], p.w, acc[m]);
+        }
+    }
+    const uint32_t mti = wmeta[r * ng + (ul >> gsh)];
+    const float sc = valid ? h2f(mti & 0xFFFFu) : 0.0f, zc = h2f(mti >> 16);
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+        const float2 k = cx[m * UC + ul];
+        it.Y[m] += sc * (acc[m] - k.x - zc * k.y);
+    }
+}
+
 template <int MT, int S, int MAXJ>
 __device__ __forceinline__ void fdn_accumulate(FDnItem<MT, S, MAXJ>& it, const uint4* hs,
                                                const float2* cx, int UC, int f, int g,
                                                const uint32_t* wmeta, int lane) {
     const int s = lane % S, r = lane / S;
-    const int U = f / 32, ng = f / g, upg = g / 32;
+    const int U = f / 32, ng = f / g, gsh = g == 128 ? 2 : 1;   // units of 32 per group: 1 << gsh
     if (!it.active)
         return;
+    if constexpr (MT == 1) {
+        uint4 bh[2][1][4];
+        fdn_read_h<1, S, MAXJ>(bh[0], hs, UC, s < U ? s : 0);
 #pragma unroll
-    for (int i = 0; i < MAXJ; ++i) {
-        const int u = s + S * i;
-        if (u < U) {
-            const int ul = u;
+        for (int i = 0; i < MAXJ; ++i) {
+            const int u = s + S * i, un = u + S;
+            const bool valid = u < U;
+            if (i + 1 < MAXJ)
+                fdn_read_h<1, S, MAXJ>(bh[(i + 1) & 1], hs, UC, un < U ? un : 0);
+#pragma unroll
+            for (int w = 0; w < 4; ++w) pin4(bh[i & 1][0][w]);
+            fdn_slot(it, i, valid ? u : 0, valid, bh[i & 1], cx, UC, ng, gsh, wmeta, r);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < MAXJ; ++i) {
+            const int u = s + S * i;
+            const bool valid = u < U;
+            const int ul = valid ? u : 0;
             float acc[MT];
 #pragma unroll
             for (int m = 0; m < MT; ++m) acc[m] = 0.0f;
@@ -672,8 +820,8 @@ __device__ __forceinline__ void fdn_accumulate(FDnItem<MT, S, MAXJ>& it, const u
                     acc[m] = dot2(it.e[i][w][3], p.w, acc[m]);
                 }
             }
-            const uint32_t mti = wmeta[r * ng + u / upg];
-            const float sc = h2f(mti & 0xFFFFu), zc = h2f(mti >> 16);
+            const uint32_t mti = wmeta[r * ng + (ul >> gsh)];
+            const float sc = valid ? h2f(mti & 0xFFFFu) : 0.0f, zc = h2f(mti >> 16);
 #pragma unroll
             for (int m = 0; m < MT; ++m) {
                 const float2 k = cx[m * UC + ul];
@@ -694,19 +842,25 @@ __device__ __forceinline__ void fdn_finish(FDnItem<MT, S, MAXJ>& it, const DownA
     }
 }
 
-// Device-coherent read of one staging word of h (written by other compute
-// units with device-coherent stores): a 128-bit buffer load with the
-// device-scope cache policy (sc1), so no stale cache line can be returned.
+// Device-coherent read of one staging word of h (8 values) from the tagged
+// words written by fgu_finish: two 128-bit buffer loads with the
+// device-scope cache policy (sc1).  *ok is false while any of the 8 words
+// still carries another call's tag.
 template <int MT>
-__device__ __forceinline__ uint4 stage_h_load_coherent(__amdgpu_buffer_rsrc_t hrs, int f, int M,
-                                                       int u0, int uc, int idx) {
+__device__ __forceinline__ uint4 stage_h_load_tagged(__amdgpu_buffer_rsrc_t hrs, int f, int M,
+                                                     int uc, int idx, uint32_t tag, bool& ok) {
     const int words = MT * uc * 4;
     const int m = idx / (uc * 4);
-    const bool ok = idx < words && m < M;
-    const int wl = ok ? idx - m * uc * 4 : 0;
-    const int off = (int)(((long)(ok ? m : 0) * f + (long)(u0 + (wl >> 2)) * 32 + (wl & 3) * 8) * 2);
-    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(hrs, off, 0, 16 /* sc1 */);
-    return make_uint4(v.x, v.y, v.z, v.w);
+    const bool live = idx < words && m < M;
+    const int wl = live ? idx - m * uc * 4 : 0;
+    const int off = (int)(((long)(live ? m : 0) * f + (long)(wl >> 2) * 32 + (wl & 3) * 8) * 4);
+    const u32x4 a = __builtin_amdgcn_raw_buffer_load_b128(hrs, off, 0, 16 /* sc1 */);
+    const u32x4 b = __builtin_amdgcn_raw_buffer_load_b128(hrs, off + 16, 0, 16 /* sc1 */);
+    const uint32_t tt = tag * 0x10001u;
+    ok = ((a.x >> 16) | (a.y & 0xFFFF0000u)) == tt && ((a.z >> 16) | (a.w & 0xFFFF0000u)) == tt &&
+         ((b.x >> 16) | (b.y & 0xFFFF0000u)) == tt && ((b.z >> 16) | (b.w & 0xFFFF0000u)) == tt;
+    return make_uint4((a.x & 0xFFFFu) | (a.y << 16), (a.z & 0xFFFFu) | (a.w << 16),
+                      (b.x & 0xFFFFu) | (b.y << 16), (b.z & 0xFFFFu) | (b.w << 16));
 }
 
 // LoRA-A for the fused kernel, split so its loads go out early and the
@@ -729,11 +883,15 @@ __device__ __forceinline__ void lora_a_load(LoraRow<KA>& lr, const uint16_t* Ag,
     }
 }
 
-// t[m][c] with device-coherent stores (read by other compute units).
+// t[m][c], published as tagged 64-bit words (fp32 bits | tag << 32) with
+// device-coherent stores into one private copy per block (t64 + b * 256,
+// [4][2r] words each): every block then polls lines no other block reads,
+// instead of all blocks polling the same few lines.
 // xplain: the staged activation, [MT][d] binary16 in LDS.
 template <int MT, int KA>
 __device__ __forceinline__ void lora_a_finish(const LoraRow<KA>& lr, const uint4* xplain, int M,
-                                              int d, int r, int c, float* t, int lane) {
+                                              int d, int r, int c, unsigned long long* t64,
+                                              uint32_t tag, int blocks, int lane) {
     const int nch = d / 8;
     float acc[MT];
 #pragma unroll
@@ -755,8 +913,12 @@ __device__ __forceinline__ void lora_a_finish(const LoraRow<KA>& lr, const uint4
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
         const float v = group_sum<64>(acc[m]);
-        if (lane == 0 && m < M)
-            __hip_atomic_store(t + m * 2 * r + c, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const unsigned long long word =
+            (unsigned long long)__float_as_uint(v) | ((unsigned long long)tag << 32);
+        if (m < M)
+            for (int blk = lane; blk < blocks; blk += 64)
+                __hip_atomic_store(t64 + (long)blk * 256 + m * 2 * r + c, word, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 

@@ -42,24 +42,33 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
 // top of the fraction (j >= 4) so the 1024 offset, removed after the fp32
 // dot products, stays small next to the code term (the cancellation error
 // of the fp32 accumulation shrinks with 2^j).
-__device__ __forceinline__ uint32_t magic(uint32_t w, uint32_t mask) {
-    return (w & mask) | 0x64006400u;
+// With mv = magic_vgpr() (0x64006400 in a VGPR the compiler cannot see
+// through) this is one v_and_or_b32, the mask in an SGPR: a VOP3 instruction
+// on gfx950 reads at most one SGPR or literal, so with the constant as a
+// literal the compiler splits the expression into v_and + v_or.
+__device__ __forceinline__ uint32_t magic_vgpr() {
+    uint32_t v;
+    __asm__ volatile("v_mov_b32 %0, 0x64006400" : "=v"(v));
+    return v;
+}
+__device__ __forceinline__ uint32_t magic(uint32_t w, uint32_t mask, uint32_t mv) {
+    return (w & mask) | mv;
 }
 
 // Code pairs of one 32-bit word of 2-bit codes (code i at bits 2i).  Pair p
 // holds (code p, code 8+p) at fraction bits 2k(p), k(p) = {2,3,2,3,4,2,3,4},
 // i.e. each half reads 1024 + q * 4^k(p).  Two shifts + eight and-or.
-__device__ __forceinline__ void extract_w2(uint32_t w, uint32_t e[8]) {
+__device__ __forceinline__ void extract_w2(uint32_t w, uint32_t e[8], uint32_t mv) {
     const uint32_t l = w << 4;          // codes 0,1 -> bits 4-7
     const uint32_t r = w >> 6;          // codes 5,6,7 -> bits 4-9
-    e[0] = magic(l, 0x00300030u);
-    e[1] = magic(l, 0x00C000C0u);
-    e[2] = magic(w, 0x00300030u);
-    e[3] = magic(w, 0x00C000C0u);
-    e[4] = magic(w, 0x03000300u);
-    e[5] = magic(r, 0x00300030u);
-    e[6] = magic(r, 0x00C000C0u);
-    e[7] = magic(r, 0x03000300u);
+    e[0] = magic(l, 0x00300030u, mv);
+    e[1] = magic(l, 0x00C000C0u, mv);
+    e[2] = magic(w, 0x00300030u, mv);
+    e[3] = magic(w, 0x00C000C0u, mv);
+    e[4] = magic(w, 0x03000300u, mv);
+    e[5] = magic(r, 0x00300030u, mv);
+    e[6] = magic(r, 0x00C000C0u, mv);
+    e[7] = magic(r, 0x03000300u, mv);
 }
 
 // 4^-k(p) for the 2-bit pair positions above (k packed 4 bits per pair).
@@ -71,11 +80,11 @@ __device__ __forceinline__ float w2_pair_scale(int p) {
 // Code pairs of one word of 4-bit codes (code i at bits 4i).  Pair p holds
 // (code p, code 4+p): pairs 0,1 at fraction bits 4-7 (1024 + 16q), pairs 2,3
 // at bits 6-9 (1024 + 64q).  Three shifts + four and-or.
-__device__ __forceinline__ void extract_w4(uint32_t w, uint32_t e[4]) {
-    e[0] = magic(w << 4, 0x00F000F0u);
-    e[1] = magic(w, 0x00F000F0u);
-    e[2] = magic(w >> 2, 0x03C003C0u);
-    e[3] = magic(w >> 6, 0x03C003C0u);
+__device__ __forceinline__ void extract_w4(uint32_t w, uint32_t e[4], uint32_t mv) {
+    e[0] = magic(w << 4, 0x00F000F0u, mv);
+    e[1] = magic(w, 0x00F000F0u, mv);
+    e[2] = magic(w >> 2, 0x03C003C0u, mv);
+    e[3] = magic(w >> 6, 0x03C003C0u, mv);
 }
 
 // 16^-1 / 64^-1 for the 4-bit pair positions above.
@@ -85,14 +94,47 @@ __device__ __forceinline__ float w4_pair_scale(int p) { return p < 2 ? 1.0f / 16
 // from registers preloaded before a loop is not hoisted out of the loop
 // (which would keep every unpacked code live at once).
 __device__ __forceinline__ void pin(uint32_t& v) { __asm__ volatile("" : "+v"(v)); }
+// The four words of v are materialized here: the loads that produce them
+// complete before this point, later loads stay in flight.
+__device__ __forceinline__ void pin4(uint4& v) {
+    __asm__ volatile("" : "+v"(v.x), "+v"(v.y), "+v"(v.z), "+v"(v.w));
+}
 
-// Sum over the `width` consecutive lanes sharing an output row (xor butterfly;
-// every lane of the group ends with the total).
+// Wait until at most N vector-memory loads of this wave are outstanding
+// (s_waitcnt vmcnt(N); expcnt and lgkmcnt are left alone).  Used to bound
+// the loads a wave keeps in flight while it streams weights, so that the
+// memory queues stay short and the small hand-off messages of the other
+// compute units are not queued behind the whole stream.
+template <int N>
+__device__ __forceinline__ void vm_window() {
+    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Lane permutations within rows of 16 lanes (DPP, no LDS round trip).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                                  0xF, 0xF, false));
+}
+constexpr int DPP_QUAD_XOR1 = 0xB1;     // quad_perm [1,0,3,2]
+constexpr int DPP_QUAD_XOR2 = 0x4E;     // quad_perm [2,3,0,1]
+constexpr int DPP_HALF_MIRROR = 0x141;  // lane i <- lane 7 - i within 8
+constexpr int DPP_MIRROR = 0x140;       // lane i <- lane 15 - i within 16
+
+// Sum over the WIDTH consecutive lanes sharing an output row (every lane of
+// the group ends with the total).  Within 16 lanes the steps are DPP moves
+// (two quad swaps, then the mirrors, which pair each lane with one of the
+// other half once every half holds its own sum); wider groups add xor
+// shuffles across rows.
 template <int WIDTH>
 __device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-    for (int off = WIDTH / 2; off >= 1; off >>= 1)
-        v += __shfl_xor(v, off, 64);
+    if constexpr (WIDTH >= 2) v += dpp<DPP_QUAD_XOR1>(v);
+    if constexpr (WIDTH >= 4) v += dpp<DPP_QUAD_XOR2>(v);
+    if constexpr (WIDTH >= 8) v += dpp<DPP_HALF_MIRROR>(v);
+    if constexpr (WIDTH >= 16) v += dpp<DPP_MIRROR>(v);
+    if constexpr (WIDTH >= 32) v += __shfl_xor(v, 16, 64);
+    if constexpr (WIDTH >= 64) v += __shfl_xor(v, 32, 64);
     return v;
 }
 

@@ -45,11 +45,13 @@ hipError_t launch_gateup(GateUpArgs args, hipStream_t st);
 hipError_t launch_down(DownArgs args, hipStream_t st);
 bool decode_shape_supported(int d, int f);
 
-// One kernel per layer (decode_fused.hip).  ctl: 4 control words at the start
-// of the workspace, zero before the first call and left zero by every call.
+// One kernel per layer (decode_fused.hip).  ctl: the 1 KB control block at
+// the start of the workspace (zero before the first call); t64 [grid][256]
+// and h32 [4][f]: the tagged hand-off words (zero before the first call).
 bool fused_supported(int M, int d, int f, int g, int r);
+int fused_grid();                              // blocks of the one-kernel layer (CU count)
 hipError_t launch_fused(GateUpArgs gu, DownArgs dn, const uint16_t* Ag, const uint16_t* Au,
-                        float* t, uint16_t* h, unsigned* ctl, hipStream_t st);
+                        unsigned long long* t64, uint32_t* h32, unsigned* ctl, hipStream_t st);
 
 // Prefill-chunk path (prefill.hip): M a multiple of 128 tokens, bfloat16.
 bool prefill_supported(int M, int d, int f, int g, int r);
