@@ -3,9 +3,11 @@
 
 A step is one pass over the layer stack of the Qwen3-4B-shaped workload
 (d=2560, f=9728, 2-bit gate/up and 4-bit down at group 128, LoRA rank 16,
-M=1 token, 36 independently seeded layers run back to back, one forward per
-layer on one stream).  Inputs are packed and resident in HBM before the
-timed region.  Prints one JSON line:
+M=1 token, 36 independently seeded layers).  The layers sit on a residual
+stream as in a decoder (x_{l+1} = x_l + y_l, attention and norms left out),
+so each layer's input depends on the previous layer's output; the stack runs
+through qmlp_forward_stack (one persistent launch at this shape).  Inputs are
+packed and resident in HBM before the timed region.  Prints one JSON line:
 
   value    = achieved HBM GB/s = L * B(M) / t_step, where B(M) are the
              algorithmic bytes of one MLP step (packed codes + fp16
@@ -51,6 +53,11 @@ def log(*a):
 class Stack:
     def __init__(self, cfg, mlps, xs, ys, ws):
         self.cfg, self.mlps, self.xs, self.ys, self.ws = cfg, mlps, xs, ys, ws
+        import torch
+        import paper_2606_04238_amd as q
+        self.st = q.Stack(mlps)
+        self.Y = torch.empty((len(mlps), cfg.M, cfg.d), dtype=ys[0].dtype, device="cuda")
+        self.sws = q.stack_workspace(self.st, cfg.M, ys[0].dtype)
 
 
 def _gen_layer(cfg, i, seed):
@@ -91,10 +98,35 @@ def build_stack(cfg: wl.Config, seed: int = 0, layers: int | None = None, thread
 
 
 def run_stack_once(stack: Stack):
+    """One step: the whole stack on the residual stream from layer 0's x."""
+    import paper_2606_04238_amd as q
+    q.forward_stack(stack.st, stack.xs[0], y=stack.Y, ws=stack.sws)
+    return stack.Y
+
+
+def run_layers_once(stack: Stack):
+    """The per-layer path for comparison: one qmlp_forward per layer, each on
+    its own seeded input."""
     import paper_2606_04238_amd as q
     for m, x, y in zip(stack.mlps, stack.xs, stack.ys):
         q.forward(m, x, y=y, ws=stack.ws)
     return stack.ys
+
+
+def capture(fn):
+    """fn captured once in a HIP graph on a side stream."""
+    import torch
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            fn()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    return g
 
 
 # --------------------------------------------------------------------- timing
@@ -182,17 +214,27 @@ def cpu_baseline(cfg: wl.Config, seed: int, budget_s: float = 12.0, max_layers: 
                                                                             total_t / n * 1e6)}
 
 
-def parity_layer0(stack: Stack, seed: int):
+def parity_sampled(stack: Stack, seed: int, sample=(0,)):
+    """Max-rel error of the sampled layers' outputs of the last timed step
+    against the oracle on each layer's residual-stream input (recomputed
+    from x_0 and the GPU outputs: x_{l+1} = x_l + y_l, binary16)."""
+    import torch
     import oracle as orc
     cfg = stack.cfg
-    lay = wl.layer(cfg, 0, seed)
-    qg, qu, qd = (orc.quantize(lay.W_gate, 2, cfg.g), orc.quantize(lay.W_up, 2, cfg.g),
-                  orc.quantize(lay.W_down, 4, cfg.g))
-    y_ref = orc.forward(qg, qu, qd, lay.A_gate, lay.B_gate, lay.A_up, lay.B_up, lay.x,
-                        lora_scale=cfg.lora_scale, bf16=cfg.bf16)
-    import torch
-    bits = stack.ys[0].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
-    return orc.max_rel_err(orc.act_to_f64(bits, cfg.bf16), y_ref)
+    Y = stack.Y.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    x = stack.xs[0].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    out = {}
+    for i in range(max(sample) + 1):
+        if i in sample:
+            lay = wl.layer(cfg, i, seed)
+            qg, qu, qd = (orc.quantize(lay.W_gate, 2, cfg.g), orc.quantize(lay.W_up, 2, cfg.g),
+                          orc.quantize(lay.W_down, 4, cfg.g))
+            y_ref = orc.forward(qg, qu, qd, lay.A_gate, lay.B_gate, lay.A_up, lay.B_up, x,
+                                lora_scale=cfg.lora_scale, bf16=cfg.bf16)
+            out[i] = orc.max_rel_err(orc.act_to_f64(Y[i], cfg.bf16), y_ref)
+        s64 = x.view(np.float16).astype(np.float64) + Y[i].view(np.float16).astype(np.float64)
+        x = s64.astype(np.float16).view(np.uint16)
+    return out
 
 
 # --------------------------------------------------------------------- prefill
@@ -303,49 +345,55 @@ def main(argv=None):
     if cfg.M > 16:
         return prefill_main(cfg, args)
     stack = build_stack(cfg, args.seed)
+    L = cfg.L
+    B = cfg.alg_bytes()
+    launches = q.stack_launches(stack.st, cfg.M, stack.Y.dtype)
+    persistent = launches < L
 
-    # eager timing
+    # the timed step: the whole stack on the residual stream
     eager_ms, _ = time_passes(lambda: run_stack_once(stack), args.steps, args.warmup)
-    # graph timing: the whole stack captured once, replayed per step
     graph_ms = None
     if args.mode == "graph":
-        g = torch.cuda.CUDAGraph()
-        s = torch.cuda.Stream()
-        s.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(s):
-            run_stack_once(stack)
-            torch.cuda.synchronize()
-            with torch.cuda.graph(g, stream=s):
-                run_stack_once(stack)
-        torch.cuda.current_stream().wait_stream(s)
-        torch.cuda.synchronize()
+        g = capture(lambda: run_stack_once(stack))
         graph_ms, wall = time_passes(g.replay, args.steps, args.warmup)
     head = graph_ms if graph_ms is not None else eager_ms
     t_step = sum(head) / len(head)          # the K timed steps, back to back
-    L = cfg.L
-    B = cfg.alg_bytes()
     gbs = L * B / (t_step * 1e-3) / 1e9
     us_layer = t_step * 1e3 / L
+    if stack.sws is not None and persistent:
+        err_bits = q.stack_errors(stack.st, stack.sws, cfg.M, stack.Y.dtype)
+        if err_bits:
+            raise RuntimeError("stack kernel reported error bits %#x" % err_bits)
+    err = parity_sampled(stack, args.seed, sample=(0, L // 2, L - 1))
 
-    fused, k1_us, k2_us = kernel_durations(stack)
+    # context: the per-layer path (one qmlp_forward launch per layer), graph replay
+    gl = capture(lambda: run_layers_once(stack))
+    layer_ms, _ = time_passes(gl.replay, max(5, args.steps // 2), 2)
+    per_layer_us = sum(layer_ms) / len(layer_ms) * 1e3 / L
+
     traffic = None
-    if fused:
-        # One launch per layer: the timed region holds K * L launches of the
-        # fused kernel back to back on the replay stream, so its events give
-        # the average launch duration (inter-launch gaps included).
-        dom_name, dom_b = "fused_layer_kernel", B
-        dom_us = t_step * 1e3 / L
-        kernel_us = {"fused_layer_timed_region_avg": round(dom_us, 3),
-                     "fused_layer_event_bracketed": round(k1_us, 3)}
-        traffic = read_traffic(os.path.join(ROOT, "profiles", "fused_layer_%s.md" % cfg.name),
+    if persistent:
+        # the timed region holds K steps of `launches` back-to-back launches
+        # of the stack kernel on the replay stream, so its events give the
+        # average launch duration (inter-launch gaps included)
+        dom_name = "stack_kernel"
+        dom_us = t_step * 1e3 / launches
+        dom_b = L * B / launches
+        kernel_us = {"stack_kernel_avg_launch": round(dom_us, 3), "launches_per_step": launches}
+        traffic = read_traffic(os.path.join(ROOT, "profiles", "stack_kernel_%s.md" % cfg.name),
                                dom_name)
     else:
-        gu_b, dn_b = kernel_bytes(cfg)
-        kernel_us = {"gateup_half": round(k1_us, 3), "down_w4": round(k2_us, 3)}
-        dom_name, dom_us, dom_b = ("gateup_w2 (LoRA-A + fused gate/up)", k1_us, gu_b) \
-            if k1_us >= k2_us else ("down_w4", k2_us, dn_b)
+        fused, k1_us, k2_us = kernel_durations(stack)
+        if fused:
+            dom_name, dom_b = "fused_layer_kernel", B
+            dom_us = per_layer_us
+            kernel_us = {"fused_layer_event_bracketed": round(k1_us, 3)}
+        else:
+            gu_b, dn_b = kernel_bytes(cfg)
+            kernel_us = {"gateup_half": round(k1_us, 3), "down_w4": round(k2_us, 3)}
+            dom_name, dom_us, dom_b = ("gateup_w2 (LoRA-A + fused gate/up)", k1_us, gu_b) \
+                if k1_us >= k2_us else ("down_w4", k2_us, dn_b)
     achieved = dom_b / (dom_us * 1e-6) / 1e9
-    err0 = parity_layer0(stack, args.seed)
 
     out = {
         "metric": METRIC,
@@ -361,19 +409,20 @@ def main(argv=None):
         "dtype": "f16",
         "data": "synthetic",
         "config": {
-            "workload": "%s decode MLP stack: M=%d, d=%d, f=%d, group %d, LoRA rank %d, %d layers"
-                        % (cfg.name, cfg.M, cfg.d, cfg.f, cfg.g, cfg.r, L),
+            "workload": "%s decode MLP stack: M=%d, d=%d, f=%d, group %d, LoRA rank %d, %d layers "
+                        "on a residual stream" % (cfg.name, cfg.M, cfg.d, cfg.f, cfg.g, cfg.r, L),
             "us_per_mlp_step": round(us_layer, 3),
             "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
             "alg_bytes_per_mlp_step": B,
             "mode": "hip_graph" if graph_ms is not None else "eager",
+            "path": "persistent stack kernel" if persistent else "per-layer forward",
             "eager_us_per_mlp_step": round(statistics.median(eager_ms) * 1e3 / L, 3),
+            "per_layer_path_us_per_mlp_step": round(per_layer_us, 3),
             "median_ms_per_step": round(statistics.median(head), 4),
             "p10_p90_ms_per_step": [round(float(np.percentile(head, 10)), 4),
                                     round(float(np.percentile(head, 90)), 4)],
             "kernel_us": kernel_us,
-            "launches_per_layer": q.forward_launches(stack.mlps[0], cfg.M),
-            "parity_layer0_max_rel_err": float("%.3e" % err0),
+            "parity_max_rel_err": {str(k): float("%.3e" % v) for k, v in err.items()},
         },
         "roofline": {
             "bound": "hbm",

@@ -11,6 +11,7 @@ Functions keep the names of the C entry points:
 * ``gateup_w2_lora``              -- h = SiLU(W2g x + s B_g A_g x) * (W2u x + s B_u A_u x)
 * ``down_w4``                     -- y = W4down h
 * ``forward``                     -- the whole block x -> y
+* ``forward_stack``               -- L blocks on a residual stream, x_{l+1} = x_l + y_l
 * ``unpack`` / ``dequant``        -- inspection of a packed matrix (not timed)
 """
 from __future__ import annotations
@@ -72,6 +73,9 @@ def _lib():
             "qmlp_unpack": (I, [pq, P, P, P, P]),
             "qmlp_dequant": (I, [pq, P, P]),
             "qmlp_forward_launches": (I, [pm, I, I]),
+            "qmlp_stack_workspace_bytes": (Z, [pm, I, I, I]),
+            "qmlp_forward_stack": (I, [pm, I, P, I, I, P, P, P, Z, P]),
+            "qmlp_stack_launches": (I, [pm, I, I, I]),
             "qmlp_status_string": (ctypes.c_char_p, [I]),
         }
         for name, (res, args) in sig.items():
@@ -268,3 +272,65 @@ def dequant(w: QWeight) -> torch.Tensor:
     qc = w.c()
     _check(_lib().qmlp_dequant(ctypes.byref(qc), _ptr(out), _stream()), "dequant")
     return out
+
+
+class Stack:
+    """L blocks of one shape on a residual stream (x_{l+1} = x_l + y_l);
+    holds the C descriptor array the stack entry points take."""
+
+    def __init__(self, mlps):
+        self.mlps = list(mlps)
+        self._arr = (MlpC * len(self.mlps))(*[m.c() for m in self.mlps])
+
+    def __len__(self):
+        return len(self.mlps)
+
+    def c(self):
+        return self._arr
+
+
+def stack_workspace_bytes(stack: Stack, M: int, dtype=torch.float16) -> int:
+    code = F16 if dtype == torch.float16 else BF16
+    return int(_lib().qmlp_stack_workspace_bytes(stack.c(), len(stack), M, code))
+
+
+def stack_launches(stack: Stack, M: int, dtype=torch.float16) -> int:
+    """Launches forward_stack makes (persistent launches, or the per-layer kernels)."""
+    code = F16 if dtype == torch.float16 else BF16
+    return int(_lib().qmlp_stack_launches(stack.c(), len(stack), M, code))
+
+
+def stack_workspace(stack: Stack, M: int, dtype=torch.float16, device="cuda") -> torch.Tensor:
+    """A zeroed workspace for forward_stack."""
+    n = stack_workspace_bytes(stack, M, dtype)
+    return torch.zeros(max(n, 1024), dtype=torch.uint8, device=device)
+
+
+def stack_errors(stack: Stack, ws: torch.Tensor, M: int = 1, dtype=torch.float16) -> int:
+    """Sticky error bits of the persistent stack launch (syncs): 1/2/4 = a wait for
+    the activation / h / the cross-XCD partials gave up, 8 = a workgroup had no place."""
+    base = stack_workspace_bytes(stack, M, dtype) - _stack_area_bytes(stack)
+    return int(ws[base + 256: base + 260].view(torch.int32).item())
+
+
+def _stack_area_bytes(stack: Stack) -> int:
+    m = stack.mlps[0]
+    d, f, r = m.d, m.f, m.rank
+    xw = d + 4 * r * 32
+    rnd = lambda v: (v + 255) // 256 * 256  # noqa: E731
+    return 1024 + rnd(8 * xw * 4) + rnd(f * 4) + 2 * 8 * d * 8
+
+
+def forward_stack(stack: Stack, x: torch.Tensor, y: torch.Tensor | None = None,
+                  ws: torch.Tensor | None = None, x_out: torch.Tensor | None = None) -> torch.Tensor:
+    """y [L][M][d]: every block's output on the residual stream x_{l+1} = x_l + y_l
+    (x_out, if given, receives x_L)."""
+    M = x.shape[0]
+    d = stack.mlps[0].d
+    if y is None:
+        y = torch.empty((len(stack), M, d), dtype=x.dtype, device=x.device)
+    if ws is None:
+        ws = stack_workspace(stack, M, x.dtype, x.device)
+    _check(_lib().qmlp_forward_stack(stack.c(), len(stack), _ptr(x), M, _dtype_code(x), _ptr(y),
+                                     _ptr(x_out), _ptr(ws), ws.numel(), _stream()), "forward_stack")
+    return y

@@ -228,6 +228,52 @@ qmlp_status check_inspect(const qmlp_qweight* w) {
     return check_qweight(w, w->bits);
 }
 
+// A stack of blocks of one shape: layer l+1's input is layer l's output.
+qmlp_status check_stack(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    if (!layers)
+        return QMLP_ERR_NULL;
+    if (L <= 0)
+        return QMLP_ERR_SHAPE;
+    for (int i = 0; i < L; ++i) {
+        qmlp_status s = check_mlp(&layers[i], M, dtype);
+        if (s != QMLP_OK)
+            return s;
+        const qmlp_mlp& a = layers[0];
+        const qmlp_mlp& b = layers[i];
+        if (b.gate.k_in != a.gate.k_in || b.gate.n_out != a.gate.n_out || b.gate.group != a.gate.group ||
+            b.down.group != a.down.group || b.rank != a.rank)
+            return QMLP_ERR_SHAPE;
+    }
+    return QMLP_OK;
+}
+
+bool stack_persistent(const qmlp_mlp* layers, int M, qmlp_dtype dtype) {
+    const qmlp_mlp& a = layers[0];
+    return dtype == QMLP_F16 && a.down.group == a.gate.group &&
+           stack_supported(M, a.gate.k_in, a.gate.n_out, a.gate.group, a.rank);
+}
+
+size_t stack_layer_ws(const qmlp_mlp* layers, int M, qmlp_dtype dtype) {
+    return round256(kCtlBytes + ws_t_bytes(layers, M, dtype) + ws_h_bytes(layers, M) +
+                    ws_T_bytes(layers, M, dtype) + ws_tag_bytes(layers, dtype));
+}
+
+StackLayerDesc stack_desc(const qmlp_mlp& m) {
+    StackLayerDesc s;
+    s.cg = static_cast<const uint32_t*>(m.gate.codes);
+    s.mg = static_cast<const uint32_t*>(m.gate.meta);
+    s.cu = static_cast<const uint32_t*>(m.up.codes);
+    s.mu = static_cast<const uint32_t*>(m.up.meta);
+    s.cd = static_cast<const uint32_t*>(m.down.codes);
+    s.md = static_cast<const uint32_t*>(m.down.meta);
+    s.Bg = static_cast<const uint16_t*>(m.B_gate);
+    s.Bu = static_cast<const uint16_t*>(m.B_up);
+    s.Ag = static_cast<const uint16_t*>(m.A_gate);
+    s.Au = static_cast<const uint16_t*>(m.A_up);
+    s.lora_scale = m.lora_scale;
+    return s;
+}
+
 }  // namespace
 
 extern "C" {
@@ -381,6 +427,83 @@ int qmlp_forward_launches(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
     if (fused_supported(M, mlp->gate.k_in, mlp->gate.n_out, mlp->gate.group, mlp->rank))
         return 1;
     return mlp->rank > 0 ? 3 : 2;
+}
+
+size_t qmlp_stack_workspace_bytes(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    if (check_stack(layers, L, M, dtype) != QMLP_OK || M == 0)
+        return 0;
+    size_t n = stack_layer_ws(layers, M, dtype) + 2 * round256((size_t)M * layers[0].gate.k_in * 2);
+    if (stack_persistent(layers, M, dtype))
+        n += stack_ws_bytes(layers[0].gate.k_in, layers[0].gate.n_out, layers[0].rank);
+    return n;
+}
+
+int qmlp_stack_launches(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    if (check_stack(layers, L, M, dtype) != QMLP_OK || M == 0)
+        return 0;
+    if (stack_persistent(layers, M, dtype))
+        return (L + stack_max_layers() - 1) / stack_max_layers();
+    int n = 0;
+    for (int i = 0; i < L; ++i) n += qmlp_forward_launches(&layers[i], M, dtype) + 1;
+    return n - 1;
+}
+
+qmlp_status qmlp_forward_stack(const qmlp_mlp* layers, int L, const void* x, int M, qmlp_dtype dtype,
+                               void* y, void* x_out, void* ws, size_t ws_bytes, qmlp_stream stream) {
+    qmlp_status s = check_stack(layers, L, M, dtype);
+    if (s != QMLP_OK)
+        return s;
+    if (M == 0)
+        return QMLP_OK;
+    if (!x || !y)
+        return QMLP_ERR_NULL;
+    if (!aligned16(x) || !aligned16(y) || (x_out && !aligned16(x_out)))
+        return QMLP_ERR_ALIGN;
+    if (!ws || ws_bytes < qmlp_stack_workspace_bytes(layers, L, M, dtype))
+        return QMLP_ERR_WORKSPACE;
+    if (!aligned16(ws))
+        return QMLP_ERR_ALIGN;
+    const int d = layers[0].gate.k_in;
+    const size_t step = (size_t)M * d * 2;
+    const size_t lws = stack_layer_ws(layers, M, dtype);
+    char* pp[2] = {static_cast<char*>(ws) + lws, static_cast<char*>(ws) + lws + round256(step)};
+    char* area = static_cast<char*>(ws) + lws + 2 * round256(step);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    char* yb = static_cast<char*>(y);
+    if (stack_persistent(layers, M, dtype)) {
+        StackLayerDesc desc[64];
+        const int per = stack_max_layers();
+        const uint16_t* xin = static_cast<const uint16_t*>(x);
+        for (int l0 = 0, c = 0; l0 < L; l0 += per, ++c) {
+            const int n = L - l0 < per ? L - l0 : per;
+            for (int i = 0; i < n; ++i) desc[i] = stack_desc(layers[l0 + i]);
+            // a later launch reads the residual stream the previous one left
+            uint16_t* xl = l0 + n == L ? static_cast<uint16_t*>(x_out) : reinterpret_cast<uint16_t*>(pp[c & 1]);
+            hipError_t e = launch_stack(desc, n, d, layers[0].gate.n_out, layers[0].gate.group, layers[0].rank,
+                                        xin, reinterpret_cast<uint16_t*>(yb + l0 * step), xl, area, st);
+            if (e != hipSuccess)
+                return QMLP_ERR_HIP;
+            xin = xl;
+        }
+        return QMLP_OK;
+    }
+    // per block: y_l = MLP_l(x_l), then x_{l+1} = x_l + y_l
+    const void* xin = x;
+    for (int i = 0; i < L; ++i) {
+        s = qmlp_forward(&layers[i], xin, M, dtype, yb + i * step, ws, lws, st);
+        if (s != QMLP_OK)
+            return s;
+        void* next = i + 1 == L ? x_out : pp[i & 1];
+        if (next) {
+            hipError_t e = launch_residual(static_cast<const uint16_t*>(xin),
+                                           reinterpret_cast<const uint16_t*>(yb + i * step),
+                                           static_cast<uint16_t*>(next), M * d, dtype == QMLP_BF16, st);
+            if (e != hipSuccess)
+                return QMLP_ERR_HIP;
+        }
+        xin = next;
+    }
+    return QMLP_OK;
 }
 
 const char* qmlp_status_string(qmlp_status s) {

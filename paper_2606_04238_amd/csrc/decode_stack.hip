@@ -1,0 +1,886 @@
+// A stack of decode MLP blocks in one persistent launch (M = 1, binary16),
+// gfx950.
+//
+// Each block of the stack is the W4/W2-GateUp MLP with Recover-LoRA
+// adapters (Sec. 3.1 Eq. (1), Sec. 3.3, Sec. 4.2):
+//   G = W2gate x + s B_g (A_g x),  U = W2up x + s B_u (A_u x),
+//   h = SiLU(G) * U,  y = W4down h,
+// and the blocks sit on a residual stream as in a decoder: block l+1 reads
+// x_{l+1} = x_l + y_l (each y_l rounded to binary16 and returned, the sum
+// rounded once to binary16), with the attention blocks and norms between
+// them left out.  Decode is bound by loading
+// weights (Sec. 3.3, Sec. 5); what a per-layer launch cannot hide is the
+// chain of dependent steps inside a layer.  Here the weights of block l+1
+// stream into registers while block l runs its hand-offs: weights do not
+// depend on activations, so every register set is reloaded with the next
+// block's weights right after its last use.  No step of block l+1 starts
+// before block l's output is complete.
+//
+// Work split (8 XCDs x 32 compute units, one 512-thread workgroup each):
+//   * XCD x owns the slice F_x = [x f/8, (x+1) f/8) of the intermediate
+//     dimension.  Its block j computes gate/up rows F_x,j (f/256 rows) and
+//     publishes h for them to the other blocks of the same XCD;
+//   * block j then computes the partial down product over F_x for the
+//     output rows D_j = [j d/32, (j+1) d/32) and publishes it to the blocks
+//     j of the other XCDs;
+//   * block j of every XCD sums the eight partials of D_j in XCD order (the
+//     same sum on every XCD), rounds y to binary16, adds the residual
+//     x[D_j], computes its share of the next block's LoRA-A product
+//     (A[:, D_j] x_{l+1}[D_j], fp32) and publishes both to the blocks of its
+//     own XCD, which add the 32 shares in order.
+// So every layer has one hand-off between XCDs and two inside an XCD,
+// through that XCD's L2.  The XCD of a workgroup is read from HW_REG_XCC_ID
+// and its rank inside the XCD from a per-XCD counter, so producer and
+// consumer of an XCD-local word are on the same L2 by construction.
+//
+// Hand-offs carry their own validity: each published value sits in one
+// aligned word with a 16-bit tag that changes with every layer step (32-bit
+// words: binary16 | tag << 16; 64-bit words: fp32 bits | tag << 32).
+// XCD-local words are written with plain stores and polled with sc0|nt
+// loads (they miss the CU's L1 and hit the XCD's L2); cross-XCD words are
+// written and polled device-coherent (sc1), double-buffered by layer parity
+// (an XCD can run at most one layer ahead of another).  Waves 0-5 hold and
+// stream weights and compute; waves 6-7 only poll, so their polls are never
+// queued behind the weight stream of their own wave.  Every wait is bounded:
+// a timeout sets an error bit, later polls of that wave are skipped and the
+// kernel exits normally.
+#include "decode_common.h"
+#include "decode_launch.h"
+
+namespace qmlp {
+
+namespace {
+
+constexpr int SX = 8;                     // XCDs
+constexpr int SB = 32;                    // workgroups per XCD
+constexpr int SGRID = SX * SB;
+constexpr int SCW = 6;                    // weight / compute waves
+constexpr int SPW = 2;                    // polling waves
+constexpr int SPT = SPW * 64;             // polling threads
+constexpr int STHREADS = (SCW + SPW) * 64;
+constexpr unsigned kStackSpin = 1u << 17;
+constexpr int KA = 3;                     // LoRA-A slice loads per compute thread (max)
+constexpr int KXW = 2;                    // activation staging words per polling thread (max)
+constexpr int KHW = 2;                    // h staging words per polling thread (max)
+
+// Control words (uint32 index into the stack's control block).
+constexpr int C_SEQ = 0, C_DONE = 32, C_ERR = 64, C_XC = 96;
+
+// Cache policy bits of the hand-off loads (bit 31: volatile to the compiler).
+constexpr int POL_INTRA = (int)0x80000003u;   // sc0 | nt: through to this XCD's L2
+constexpr int POL_CROSS = (int)0x80000010u;   // sc1: device-coherent
+
+__device__ __forceinline__ uint32_t stag(uint32_t s) { return s % 65535u + 1u; }
+
+// Compiler-only fence: the next layer's weight loads are not hoisted above
+// the arithmetic on the current layer's registers (which would keep both
+// register sets live).
+__device__ __forceinline__ void sk_order() { __asm__ volatile("" ::: "memory"); }
+
+__device__ __forceinline__ void st_intra32(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void st_intra64(unsigned long long* p, unsigned long long v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void st_cross64(unsigned long long* p, unsigned long long v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+struct StackLayer {
+    const uint32_t *cg, *mg, *cu, *mu, *cd, *md;   // packed codes and (scale | zero << 16) words
+    const uint16_t *Bg, *Bu, *Ag, *Au;             // LoRA factors, binary16
+    float lora_scale;
+};
+
+}  // namespace
+
+constexpr int kStackMaxLayers = 40;            // layers per launch (kernel-argument block < 4 KB)
+
+struct StackArgs {
+    StackLayer lay[kStackMaxLayers];
+    int L, d, f, g, r;
+    const uint16_t* x0;          // [d] input of the first layer
+    uint16_t* y;                 // [L][d] output of every layer
+    uint16_t* xl;                // [d] the residual stream after the last layer (may be null)
+    uint32_t* xb;                // [8][xw] XCD-local: d y words, then [2r][32] 64-bit LoRA-A shares
+    uint32_t* hb;                // [f] XCD-local h words (XCD x owns [x f/8, (x+1) f/8))
+    unsigned long long* pb;      // [2][8][d] cross-XCD partial down sums
+    unsigned* ctl;
+    int xw;                      // 32-bit words per XCD in xb
+    int o_xs, o_cx, o_t, o_hs, o_hcx, o_a, o_y, o_xr, o_xn, o_meta, meta_bytes;   // LDS byte offsets
+};
+
+namespace {
+
+// Poll K 16-byte words at byte offsets off[k] (only those whose bit is set
+// in `valid`) until each shows `tag`: in the high half of every 32-bit word
+// (k < K64), or in the high word of both 64-bit halves (k >= K64).  Loads of
+// one round go out together; only words still pending are read again.
+template <int K, int K64, int POL>
+__device__ __forceinline__ bool sk_poll(__amdgpu_buffer_rsrc_t rs, const int (&off)[K], uint32_t valid,
+                                        u32x4 (&v)[K], uint32_t tag, bool skip) {
+    uint32_t pending = skip ? 0u : valid;
+    for (unsigned it = 0; pending != 0u && it < kStackSpin; ++it) {
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+            if (pending & (1u << k)) v[k] = __builtin_amdgcn_raw_buffer_load_b128(rs, off[k], 0, POL);
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            if (pending & (1u << k)) {
+                const bool ok = k >= K64 ? (v[k].y == tag && v[k].w == tag)
+                                         : ((v[k].x >> 16) == tag && (v[k].y >> 16) == tag &&
+                                            (v[k].z >> 16) == tag && (v[k].w >> 16) == tag);
+                if (ok) pending &= ~(1u << k);
+            }
+        }
+        if (pending != 0u)
+            __builtin_amdgcn_s_sleep(1);
+    }
+    return pending == 0u;
+}
+
+// One staging word of the activation: 16 binary16 values x[16w .. 16w+16)
+// (low halves of four tagged 16-byte words) pre-scaled per fraction position
+// into the x' layout of the gate/up units: chunk-major, xs[c * XS + ul] for
+// chunk c (0..7) of 64-code unit ul = w / 4, so the 8 lanes of a row read 8
+// consecutive 16-byte entries (no bank conflict) at one base address plus
+// immediates; and per unit (1024 sum x', sum x).  Every lane of the wave
+// calls it (quad reductions); lanes with valid == false store nothing.
+template <int XS>
+__device__ __forceinline__ void sk_stage_x(uint4* xs, float2* cx, const u32x4* v, bool valid, int w) {
+    uint32_t xv[16];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        xv[4 * q + 0] = valid ? v[q].x & 0xFFFFu : 0u;
+        xv[4 * q + 1] = valid ? v[q].y & 0xFFFFu : 0u;
+        xv[4 * q + 2] = valid ? v[q].z & 0xFFFFu : 0u;
+        xv[4 * q + 3] = valid ? v[q].w & 0xFFFFu : 0u;
+    }
+    uint32_t pr[8];
+    float csum = 0.0f, xsum = 0.0f;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+        const float sc = w2_pair_scale(p);
+        const uint32_t ha = f2h(h2f(xv[p]) * sc), hb = f2h(h2f(xv[8 + p]) * sc);
+        pr[p] = ha | (hb << 16);
+        csum += h2f(ha) + h2f(hb);
+        xsum += h2f(xv[p]) + h2f(xv[8 + p]);
+    }
+    csum = group_sum<4>(csum);
+    xsum = group_sum<4>(xsum);
+    if (valid) {
+        const int ul = w >> 2, wi = w & 3;
+        xs[(2 * wi) * XS + ul] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
+        xs[(2 * wi + 1) * XS + ul] = make_uint4(pr[4], pr[5], pr[6], pr[7]);
+        if (wi == 0)
+            cx[ul] = make_float2(1024.0f * csum, xsum);
+    }
+}
+
+// One staging word of h: 8 binary16 values h[8w .. 8w+8) of this XCD's
+// slice into the h' layout of the down units, chunk-major hs[c * HS + ul]
+// for chunk c (0..3) of 32-code unit ul = w / 4; and per unit
+// (1024 sum h', sum h).
+template <int HS>
+__device__ __forceinline__ void sk_stage_h(uint4* hs, float2* cx, const u32x4* v, bool valid, int w) {
+    uint32_t hv[8];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        hv[4 * q + 0] = valid ? v[q].x & 0xFFFFu : 0u;
+        hv[4 * q + 1] = valid ? v[q].y & 0xFFFFu : 0u;
+        hv[4 * q + 2] = valid ? v[q].z & 0xFFFFu : 0u;
+        hv[4 * q + 3] = valid ? v[q].w & 0xFFFFu : 0u;
+    }
+    uint32_t pr[4];
+    float csum = 0.0f, xsum = 0.0f;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const float sc = w4_pair_scale(p);
+        const uint32_t ha = f2h(h2f(hv[p]) * sc), hb = f2h(h2f(hv[4 + p]) * sc);
+        pr[p] = ha | (hb << 16);
+        csum += h2f(ha) + h2f(hb);
+        xsum += h2f(hv[p]) + h2f(hv[4 + p]);
+    }
+    csum = group_sum<4>(csum);
+    xsum = group_sum<4>(xsum);
+    if (valid) {
+        const int ul = w >> 2, wi = w & 3;
+        hs[wi * HS + ul] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
+        if (wi == 0)
+            cx[ul] = make_float2(1024.0f * csum, xsum);
+    }
+}
+
+// Loads of one gate/up wave-item: 8 rows from row0 (rows at or past row_end
+// belong to another workgroup and are computed but never stored), 8 lanes
+// per row.  Metadata of the 8 rows is contiguous per matrix; a 16-byte chunk
+// whose row lies past the matrix is read from the item's first chunk instead.
+template <int JG, int KM>
+__device__ __forceinline__ void sk_gu_load(FGuItem<1, 8, JG, KM>& it, const StackLayer& w, int row0,
+                                           int row_end, int f, int d, int g, int r, int lane) {
+    const int s = lane & 7, U = d / 64, ng = d / g, chunks = 2 * ng;
+    it.row0 = row0;
+    it.row = row0 + (lane >> 3);
+    it.ok = it.row < row_end;
+    const long rowc = it.ok ? it.row : row0;
+    const uint4* mg4 = reinterpret_cast<const uint4*>(w.mg);
+    const uint4* mu4 = reinterpret_cast<const uint4*>(w.mu);
+    const long mbase = (long)row0 * ng / 4;
+#pragma unroll
+    for (int k = 0; k < KM; ++k) {
+        const int c = lane + 64 * k;
+        const bool up = c >= chunks && c < 2 * chunks;
+        const int cc = c < chunks ? c : (up ? c - chunks : 0);
+        const bool inside = row0 + (4 * cc) / ng < f;
+        it.meta[k] = load_stream((up ? mu4 : mg4) + mbase + (inside ? cc : 0));
+    }
+    const uint4* cg = reinterpret_cast<const uint4*>(w.cg) + rowc * U + s;
+    const uint4* cu = reinterpret_cast<const uint4*>(w.cu) + rowc * U + s;
+#pragma unroll
+    for (int i = 0; i < JG; ++i) {          // U == 8 * JG: every slot is inside the row
+        it.qg[i] = load_stream(cg + 8 * i);
+        it.qu[i] = load_stream(cu + 8 * i);
+    }
+    if (r > 0) {
+        const int CPL = r / 8;                  // ranks per lane: 1, 2 or 4
+        const long off = rowc * r + s * CPL;
+        if (CPL == 1) {
+            it.bg[0] = w.Bg[off];
+            it.bu[0] = w.Bu[off];
+        } else if (CPL == 2) {
+            it.bg[0] = *reinterpret_cast<const uint32_t*>(w.Bg + off);
+            it.bu[0] = *reinterpret_cast<const uint32_t*>(w.Bu + off);
+        } else {
+            const uint2 vg = *reinterpret_cast<const uint2*>(w.Bg + off);
+            const uint2 vu = *reinterpret_cast<const uint2*>(w.Bu + off);
+            it.bg[0] = vg.x; it.bg[1] = vg.y;
+            it.bu[0] = vu.x; it.bu[1] = vu.y;
+        }
+    }
+    it.G[0] = it.U[0] = 0.0f;
+}
+
+// Gate/up dot products of one wave-item over the staged x' (one token, 8
+// lanes per row, U == 8 * JG units): slot i of lane s is unit s + 8 i, its
+// eight x' chunks read just before its arithmetic.  The per-group
+// (scale, zero) words come from the wave's metadata area in LDS.
+template <int JG, int KM>
+__device__ __forceinline__ void sk_gu_accumulate(FGuItem<1, 8, JG, KM>& it, const uint4* xs,
+                                                 const float2* cx, int g, const uint32_t* wmeta,
+                                                 int lane) {
+    constexpr int XS = 8 * JG;
+    const uint32_t mv = magic_vgpr();
+    const int s = lane & 7, r = lane >> 3;
+    const int ng = XS * 64 / g, gsh = g == 128 ? 1 : 0;
+    const uint4* xl = xs + s;
+    const float2* cl = cx + s;
+    const uint32_t* mgl = wmeta + r * ng + (s >> gsh);
+    const uint32_t* mul = wmeta + (8 + r) * ng + (s >> gsh);
+#pragma unroll
+    for (int i = 0; i < JG; ++i) {
+        uint4 xv[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) xv[c] = xl[c * XS + 8 * i];
+        uint32_t wg[4] = {it.qg[i].x, it.qg[i].y, it.qg[i].z, it.qg[i].w};
+        uint32_t wu[4] = {it.qu[i].x, it.qu[i].y, it.qu[i].z, it.qu[i].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            pin(wg[q]);
+            pin(wu[q]);
+        }
+        float ag = 0.0f, au = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t eg[8], eu[8];
+            extract_w2(wg[q], eg, mv);
+            extract_w2(wu[q], eu, mv);
+            const uint32_t xp[8] = {xv[2 * q].x, xv[2 * q].y, xv[2 * q].z, xv[2 * q].w,
+                                    xv[2 * q + 1].x, xv[2 * q + 1].y, xv[2 * q + 1].z, xv[2 * q + 1].w};
+#pragma unroll
+            for (int p = 0; p < 8; ++p) {
+                ag = dot2(eg[p], xp[p], ag);
+                au = dot2(eu[p], xp[p], au);
+            }
+        }
+        const int gi = (8 * i) >> gsh;
+        const uint32_t mgi = mgl[gi], mui = mul[gi];
+        const float2 k = cl[8 * i];
+        it.G[0] += h2f(mgi & 0xFFFFu) * (ag - k.x - h2f(mgi >> 16) * k.y);
+        it.U[0] += h2f(mui & 0xFFFFu) * (au - k.x - h2f(mui >> 16) * k.y);
+    }
+}
+
+// LoRA-B on the lane's ranks, the row reduction over 8 lanes and
+// h = SiLU(G) * U, published as tagged words to the XCD-local h buffer.
+template <int JG, int KM>
+__device__ __forceinline__ void sk_gu_finish(FGuItem<1, 8, JG, KM>& it, const float* ts, int r,
+                                             float ls, uint32_t* hb, uint32_t tag, int lane) {
+    const int s = lane & 7;
+    float G = it.G[0], U = it.U[0];
+    if (r > 0) {
+        const int CPL = r / 8;
+        uint32_t b0 = it.bg[0], b1 = it.bg[1], c0 = it.bu[0], c1 = it.bu[1];
+        pin(b0); pin(b1); pin(c0); pin(c1);
+        const uint32_t bgw[2] = {b0, b1}, buw[2] = {c0, c1};
+        float lg = 0.0f, lu = 0.0f;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            if (c < CPL) {
+                const int rc = s * CPL + c;
+                lg += h2f(bgw[c >> 1] >> (16 * (c & 1))) * ts[rc];
+                lu += h2f(buw[c >> 1] >> (16 * (c & 1))) * ts[r + rc];
+            }
+        }
+        G += ls * lg;
+        U += ls * lu;
+    }
+    G = group_sum<8>(G);
+    U = group_sum<8>(U);
+    if (it.ok && s == 0) {
+        const float hv = G / (1.0f + __expf(-G)) * U;
+        st_intra32(hb + it.row, f2h(hv) | (tag << 16));
+    }
+}
+
+// One down wave-item: 8 output rows of D_j, 8 lanes per row; lane s owns the
+// 32-code units s, s+8, ... of this XCD's column slice (UF units).  Each
+// unit's (scale | zero) word is loaded with it (groups need not align with
+// the slice).
+template <int JD>
+struct SkDn {
+    uint4 q[JD];
+    uint32_t mt[JD];
+};
+
+template <int JD>
+__device__ __forceinline__ void sk_dn_load(SkDn<JD>& it, const StackLayer& w, int o, int xcc, int f,
+                                           int g, int lane) {
+    const int s = lane & 7, FX = f / SX, UF = FX / 32, Uf = f / 32, ngd = f / g;
+    const uint4* cd = reinterpret_cast<const uint4*>(w.cd) + (long)o * Uf + xcc * UF;
+    const uint32_t* md = w.md + (long)o * ngd;
+#pragma unroll
+    for (int i = 0; i < JD; ++i) {
+        // only the last slot can run past the slice: it re-reads the slice's
+        // last unit, and its contribution is dropped
+        const int u = i + 1 < JD ? s + 8 * i : (s + 8 * i < UF ? s + 8 * i : UF - 1);
+        it.q[i] = load_stream(cd + u);
+        it.mt[i] = load_stream(md + (xcc * FX + 32 * u) / g);
+    }
+}
+
+template <int JD>
+__device__ __forceinline__ float sk_dn_compute(SkDn<JD>& it, const uint4* hs, const float2* hcx,
+                                               int UF, int lane) {
+    constexpr int HS = 8 * JD;
+    const uint32_t mv = magic_vgpr();
+    const int s = lane & 7;
+    const uint4* hl = hs + s;
+    const float2* cl = hcx + s;
+    float Y = 0.0f;
+#pragma unroll
+    for (int i = 0; i < JD; ++i) {
+        uint32_t wv[4] = {it.q[i].x, it.q[i].y, it.q[i].z, it.q[i].w};
+        uint32_t mti = it.mt[i];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) pin(wv[q]);
+        pin(mti);
+        float acc = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t e[4];
+            extract_w4(wv[q], e, mv);
+            const uint4 p = hl[q * HS + 8 * i];
+            acc = dot2(e[0], p.x, acc);
+            acc = dot2(e[1], p.y, acc);
+            acc = dot2(e[2], p.z, acc);
+            acc = dot2(e[3], p.w, acc);
+        }
+        const float2 k = cl[8 * i];
+        const float c = h2f(mti & 0xFFFFu) * (acc - k.x - h2f(mti >> 16) * k.y);
+        if (i + 1 < JD || s + 8 * i < UF)
+            Y += c;
+    }
+    return group_sum<8>(Y);
+}
+
+// The LoRA-A columns D_j of the next layer, [2r][DJ] binary16 (gate ranks
+// then up ranks), KA 16-byte pieces per compute thread.
+__device__ __forceinline__ void sk_a_load(uint4 (&av)[KA], const StackLayer& w, int r, int d, int DJ,
+                                          int j, int ct) {
+    const int per = DJ / 8, total = 2 * r * per;
+#pragma unroll
+    for (int k = 0; k < KA; ++k) {
+        const int q = ct + SCW * 64 * k;
+        const int qq = q < total ? q : 0;
+        const int rk = qq / per, c8 = qq - rk * per;
+        const uint16_t* row = rk < r ? w.Ag + (long)rk * d : w.Au + (long)(rk - r) * d;
+        if (total > 0)
+            av[k] = *reinterpret_cast<const uint4*>(row + j * DJ + 8 * c8);
+    }
+}
+
+__device__ __forceinline__ void sk_a_store(const uint4 (&av)[KA], uint4* as, int r, int DJ, int ct) {
+    const int total = 2 * r * (DJ / 8);
+#pragma unroll
+    for (int k = 0; k < KA; ++k) {
+        const int q = ct + SCW * 64 * k;
+        if (q < total)
+            as[q] = av[k];
+    }
+}
+
+// Polling wave 0: block j's rows D_j of the next layer's input (binary16
+// pairs in xn) and its share of that layer's LoRA-A product go to the
+// XCD-local activation buffer; lanes l < DJ/2 hold rows 2l, 2l+1.
+__device__ __forceinline__ void sk_publish_x(uint32_t* xb, const uint32_t* xn, const uint16_t* as,
+                                             int d, int r, int DJ, int j, uint32_t tag, int lane) {
+    if (lane < DJ / 2) {
+        const uint32_t v = xn[lane];
+        const unsigned long long wv = (unsigned long long)((v & 0xFFFFu) | (tag << 16)) |
+                                      ((unsigned long long)((v >> 16) | (tag << 16)) << 32);
+        st_intra64(reinterpret_cast<unsigned long long*>(xb + j * DJ) + lane, wv);
+    }
+    if (lane < 2 * r) {
+        const uint32_t* a32 = reinterpret_cast<const uint32_t*>(as) + lane * (DJ / 2);
+        float acc = 0.0f;
+        for (int c = 0; c < DJ / 2; ++c)
+            acc = dot2(a32[c], xn[c], acc);
+        unsigned long long* t64 = reinterpret_cast<unsigned long long*>(xb + d);
+        st_intra64(t64 + lane * SB + j, (unsigned long long)__float_as_uint(acc) |
+                                            ((unsigned long long)tag << 32));
+    }
+}
+
+typedef const StackArgs __attribute__((address_space(4))) KArgs;
+
+// Layer i's descriptor, read in place from the kernel-argument segment (the
+// argument block sits at its start): indexing the by-value argument with a
+// run-time layer index would copy the whole block to scratch.
+__device__ __forceinline__ StackLayer sk_layer(KArgs* ka, int i) {
+    StackLayer w;
+    w.cg = ka->lay[i].cg; w.mg = ka->lay[i].mg; w.cu = ka->lay[i].cu; w.mu = ka->lay[i].mu;
+    w.cd = ka->lay[i].cd; w.md = ka->lay[i].md; w.Bg = ka->lay[i].Bg; w.Bu = ka->lay[i].Bu;
+    w.Ag = ka->lay[i].Ag; w.Au = ka->lay[i].Au; w.lora_scale = ka->lay[i].lora_scale;
+    return w;
+}
+
+struct SkLds {
+    uint4* xs;          // x' of the activation (gate/up units)
+    float2* cxg;        // per unit (1024 sum x', sum x)
+    float* ts;          // t = [A_g; A_u] x, fp32 [2r]
+    uint4* hs;          // h' of this XCD's slice (down units)
+    float2* hcx;        // per unit (1024 sum h', sum h)
+    uint4* as;          // next layer's LoRA-A columns D_j, binary16 [2r][DJ]
+    uint32_t* ys;       // y[D_j] binary16 pairs
+    uint16_t* xr;       // x[D_j] of the current layer (the residual)
+    uint32_t* xn;       // x[D_j] of the next layer, binary16 pairs
+    char* meta;         // per-wave gate/up metadata areas
+};
+
+struct SkPlace {
+    int xcc, j;
+    uint32_t seq0;
+};
+
+// The weight waves: stream every layer's weights into registers (each set
+// reloaded for the next layer right after its last use), compute gate/up
+// rows and the partial down sums.  One barrier before the layers and three
+// per layer, matching sk_poll_role.
+template <int JG, int KM, int JD, int NDN>
+__device__ __forceinline__ void sk_compute_role(const StackArgs& sa, KArgs* ka, const SkLds& m,
+                                                const SkPlace& pl, int wave, int lane) {
+    const int d = sa.d, f = sa.f, g = sa.g, r = sa.r, L = sa.L;
+    const int FX = f / SX, UF = FX / 32, DJ = d / SB, RG = f / SGRID;
+    const int xcc = pl.xcc, j = pl.j, ct = wave * 64 + lane;
+    const int row_begin = xcc * FX + j * RG, row_end = row_begin + RG;
+    const int gu_items = (RG + 7) / 8, dn_items = DJ / 8;
+    const bool has_gu = wave < gu_items;
+    FGuItem<1, 8, JG, KM> gi;
+    SkDn<JD> di[NDN];
+    uint4 av[KA];
+    {
+        const StackLayer w0 = sk_layer(ka, 0);
+        sk_a_load(av, w0, r, d, DJ, j, ct);
+        if (has_gu)
+            sk_gu_load(gi, w0, row_begin + 8 * wave, row_end, f, d, g, r, lane);
+#pragma unroll
+        for (int k = 0; k < NDN; ++k) {
+            const int item = wave + SCW * k;
+            if (item < dn_items)
+                sk_dn_load(di[k], w0, j * DJ + 8 * item + (lane >> 3), xcc, f, g, lane);
+        }
+        sk_a_store(av, m.as, r, DJ, ct);
+    }
+    __syncthreads();                                            // B0
+    uint4* wmeta = reinterpret_cast<uint4*>(m.meta + wave * sa.meta_bytes);
+    for (int i = 0; i < L; ++i) {
+        const uint32_t ti = stag(pl.seq0 + 1 + i);
+        __syncthreads();                                        // B1: x', t staged
+        if (has_gu) {
+            GateUpArgs ga{};
+            ga.d = d;
+            ga.g = g;
+            fgu_meta_to_lds(gi, ga, wmeta, lane);
+            sk_gu_accumulate(gi, m.xs, m.cxg, g, reinterpret_cast<const uint32_t*>(wmeta), lane);
+            sk_gu_finish(gi, m.ts, r, sk_layer(ka, i).lora_scale, sa.hb, ti, lane);
+        }
+        sk_order();
+        if (i + 1 < L) {
+            const StackLayer wn = sk_layer(ka, i + 1);
+            sk_a_load(av, wn, r, d, DJ, j, ct);
+            if (has_gu)
+                sk_gu_load(gi, wn, row_begin + 8 * wave, row_end, f, d, g, r, lane);
+        }
+        __syncthreads();                                        // B2: h' staged
+        unsigned long long* pb = sa.pb + (long)(i & 1) * SX * d + (long)xcc * d;
+#pragma unroll
+        for (int k = 0; k < NDN; ++k) {
+            const int item = wave + SCW * k;
+            if (item < dn_items) {
+                const float yv = sk_dn_compute<JD>(di[k], m.hs, m.hcx, UF, lane);
+                const int o = j * DJ + 8 * item + (lane >> 3);
+                if ((lane & 7) == 0)
+                    st_cross64(pb + o, (unsigned long long)__float_as_uint(yv) | ((unsigned long long)ti << 32));
+            }
+        }
+        sk_order();
+        if (i + 1 < L) {
+            const StackLayer wn = sk_layer(ka, i + 1);
+            sk_a_store(av, m.as, r, DJ, ct);
+#pragma unroll
+            for (int k = 0; k < NDN; ++k) {
+                const int item = wave + SCW * k;
+                if (item < dn_items)
+                    sk_dn_load(di[k], wn, j * DJ + 8 * item + (lane >> 3), xcc, f, g, lane);
+            }
+        }
+        __syncthreads();                                        // B3: y[D_j], next A in LDS
+    }
+}
+
+// The polling waves: stage the activation and t, then h, then sum the
+// cross-XCD partials and publish y and the next layer's LoRA-A shares.
+// Offsets of the polled words are affine in the lane (one base register);
+// which of them exist is a bit mask.
+template <int XS, int HS>
+__device__ __forceinline__ void sk_poll_role(const StackArgs& sa, const SkLds& m, const SkPlace& pl,
+                                             int wave, int lane) {
+    const int d = sa.d, f = sa.f, r = sa.r, L = sa.L;
+    const int FX = f / SX, DJ = d / SB;
+    const int xcc = pl.xcc, j = pl.j, pt = (wave - SCW) * 64 + lane;
+    unsigned* ctl = sa.ctl;
+    uint32_t* xb = sa.xb + (long)xcc * sa.xw;
+    const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(xb, 0, sa.xw * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t hrs =
+        __builtin_amdgcn_make_buffer_rsrc(sa.hb + (long)xcc * FX, 0, FX * 4, 0x00020000);
+    bool dead = false;                                          // this wave gave up a wait
+    if (wave == SCW && lane < DJ / 2)
+        m.xn[lane] = reinterpret_cast<const uint32_t*>(sa.x0 + j * DJ)[lane];
+    __syncthreads();                                            // B0
+    if (wave == SCW)
+        sk_publish_x(xb, m.xn, reinterpret_cast<const uint16_t*>(m.as), d, r, DJ, j, stag(pl.seq0), lane);
+
+    // activation words: staging word w = pt + SPT kk covers x[16w, 16w+16)
+    // (four 16-byte words of tagged values); LoRA-A shares of rank pt (< 2r):
+    // 32 64-bit words after the d activation words
+    int xoff[4 * KXW + 16];
+    uint32_t xvalid = 0;
+#pragma unroll
+    for (int kk = 0; kk < KXW; ++kk) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) xoff[4 * kk + q] = 64 * pt + 64 * SPT * kk + 16 * q;
+        if (pt + SPT * kk < d / 16) xvalid |= 0xFu << (4 * kk);
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) xoff[4 * KXW + q] = d * 4 + pt * SB * 8 + 16 * q;
+    if (pt < 2 * r) xvalid |= 0xFFFFu << (4 * KXW);
+    // h words of this XCD's slice: staging word w = pt + SPT kk covers h[8w, 8w+8)
+    int hoff[2 * KHW];
+    uint32_t hvalid = 0;
+#pragma unroll
+    for (int kk = 0; kk < KHW; ++kk) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) hoff[2 * kk + q] = 32 * pt + 32 * SPT * kk + 16 * q;
+        if (pt + SPT * kk < FX / 8) hvalid |= 0x3u << (2 * kk);
+    }
+
+    for (int i = 0; i < L; ++i) {
+        const uint32_t tx = stag(pl.seq0 + i), ti = stag(pl.seq0 + 1 + i);
+        {   // the activation and the LoRA-A shares of this XCD
+            u32x4 v[4 * KXW + 16];
+            dead |= !sk_poll<4 * KXW + 16, 4 * KXW, POL_INTRA>(xrs, xoff, xvalid, v, tx, dead);
+#pragma unroll
+            for (int kk = 0; kk < KXW; ++kk) {
+                const int w = pt + SPT * kk;
+                sk_stage_x<XS>(m.xs, m.cxg, v + 4 * kk, w < d / 16, w);
+                const int wr = w - j * (DJ / 16);             // this block's residual rows D_j
+                if (wr >= 0 && wr < DJ / 16) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const u32x4 t = v[4 * kk + q];
+                        reinterpret_cast<uint32_t*>(m.xr)[8 * wr + 2 * q] = (t.x & 0xFFFFu) | (t.y << 16);
+                        reinterpret_cast<uint32_t*>(m.xr)[8 * wr + 2 * q + 1] = (t.z & 0xFFFFu) | (t.w << 16);
+                    }
+                }
+            }
+            if (pt < 2 * r) {
+                float t = 0.0f;
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    t += __uint_as_float(v[4 * KXW + q].x);
+                    t += __uint_as_float(v[4 * KXW + q].z);
+                }
+                m.ts[pt] = t;
+            }
+            dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
+            if (dead && lane == 0)
+                atomicOr(&ctl[C_ERR], 1u);
+        }
+        __syncthreads();                                        // B1
+        {   // h of this XCD's slice
+            u32x4 v[2 * KHW];
+            dead |= !sk_poll<2 * KHW, 2 * KHW, POL_INTRA>(hrs, hoff, hvalid, v, ti, dead);
+#pragma unroll
+            for (int kk = 0; kk < KHW; ++kk) {
+                const int w = pt + SPT * kk;
+                sk_stage_h<HS>(m.hs, m.hcx, v + 2 * kk, w < FX / 8, w);
+            }
+            dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
+            if (dead && lane == 0)
+                atomicOr(&ctl[C_ERR], 2u);
+        }
+        __syncthreads();                                        // B2
+        if (wave == SCW) {   // the eight partials of rows D_j, summed in XCD order
+            const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
+                sa.pb + (long)(i & 1) * SX * d + j * DJ, 0, (SX - 1) * d * 8 + DJ * 8, 0x00020000);
+            int off[SX];
+#pragma unroll
+            for (int xx = 0; xx < SX; ++xx) off[xx] = 16 * lane + xx * d * 8;
+            u32x4 v[SX];
+            dead |= !sk_poll<SX, 0, POL_CROSS>(prs, off, lane < DJ / 2 ? 0xFFu : 0u, v, ti, dead);
+            float y0 = 0.0f, y1 = 0.0f;
+#pragma unroll
+            for (int xx = 0; xx < SX; ++xx) {
+                y0 += __uint_as_float(v[xx].x);
+                y1 += __uint_as_float(v[xx].z);
+            }
+            if (lane < DJ / 2)
+                m.ys[lane] = f2h(y0) | (f2h(y1) << 16);
+            dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
+            if (dead && lane == 0)
+                atomicOr(&ctl[C_ERR], 4u);
+        }
+        __syncthreads();                                        // B3
+        if (wave == SCW) {
+            if (lane < DJ / 2) {
+                // x_{l+1} = x_l + y_l: two binary16 values summed exactly in fp32, rounded once
+                const uint32_t yv = m.ys[lane], xv = reinterpret_cast<const uint32_t*>(m.xr)[lane];
+                const uint32_t nv = f2h(h2f(xv & 0xFFFFu) + h2f(yv & 0xFFFFu)) |
+                                    (f2h(h2f(xv >> 16) + h2f(yv >> 16)) << 16);
+                m.xn[lane] = nv;
+                if (xcc == 0) {
+                    reinterpret_cast<uint32_t*>(sa.y + (long)i * d + j * DJ)[lane] = yv;
+                    if (i + 1 == L && sa.xl)
+                        reinterpret_cast<uint32_t*>(sa.xl + j * DJ)[lane] = nv;
+                }
+            }
+            if (i + 1 < L)
+                sk_publish_x(xb, m.xn, reinterpret_cast<const uint16_t*>(m.as), d, r, DJ, j, ti, lane);
+        }
+    }
+}
+
+template <int JG, int KM, int JD, int NDN>
+__global__ void __launch_bounds__(STHREADS) stack_kernel(StackArgs sa) {
+    extern __shared__ uint4 smem[];
+    char* lds = reinterpret_cast<char*>(smem);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    unsigned* ctl = sa.ctl;
+    int* info = reinterpret_cast<int*>(lds);
+
+    // Placement: the XCD from the hardware, the rank from a per-XCD counter.
+    const uint32_t xcc = __builtin_amdgcn_s_getreg(20 | (0 << 6) | (3 << 11));   // HW_REG_XCC_ID[3:0]
+    if (tid == 0)
+        info[0] = xcc < (uint32_t)SX ? (int)__hip_atomic_fetch_add(&ctl[C_XC + xcc], 1u, __ATOMIC_RELAXED,
+                                                                   __HIP_MEMORY_SCOPE_AGENT)
+                                     : SB;
+    const uint32_t seq0 = __builtin_amdgcn_readfirstlane(
+        __hip_atomic_load(&ctl[C_SEQ], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    __syncthreads();
+    const int j = __builtin_amdgcn_readfirstlane(info[0]);
+
+    if (j < SB) {
+        const SkLds m{reinterpret_cast<uint4*>(lds + sa.o_xs), reinterpret_cast<float2*>(lds + sa.o_cx),
+                      reinterpret_cast<float*>(lds + sa.o_t), reinterpret_cast<uint4*>(lds + sa.o_hs),
+                      reinterpret_cast<float2*>(lds + sa.o_hcx), reinterpret_cast<uint4*>(lds + sa.o_a),
+                      reinterpret_cast<uint32_t*>(lds + sa.o_y), reinterpret_cast<uint16_t*>(lds + sa.o_xr),
+                      reinterpret_cast<uint32_t*>(lds + sa.o_xn), lds + sa.o_meta};
+        const SkPlace pl{(int)xcc, j, seq0};
+        if (wave < SCW)
+            sk_compute_role<JG, KM, JD, NDN>(sa, (KArgs*)__builtin_amdgcn_kernarg_segment_ptr(), m, pl, wave, lane);
+        else
+            sk_poll_role<8 * JG, 8 * JD>(sa, m, pl, wave, lane);
+    } else if (tid == 0) {
+        atomicOr(&ctl[C_ERR], 8u);              // a workgroup without a place: results invalid
+    }
+
+    // The last workgroup to finish advances the step counter and clears the
+    // placement counters.
+    if (tid == 0) {
+        const unsigned old = __hip_atomic_fetch_add(&ctl[C_DONE], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (old == (unsigned)gridDim.x - 1) {
+            __hip_atomic_store(&ctl[C_DONE], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (int x = 0; x < SX; ++x)
+                __hip_atomic_store(&ctl[C_XC + x], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctl[C_SEQ], seq0 + (uint32_t)sa.L + 1u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
+// out = x + y elementwise, the exact fp32 sum of two binary16 (bfloat16)
+// values rounded once to nearest-even: the residual stream between blocks on
+// the per-layer path.
+__global__ void residual_kernel(const uint16_t* x, const uint16_t* y, uint16_t* out, int n, int bf16) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n)
+        return;
+    if (bf16) {
+        const float v = __uint_as_float((uint32_t)x[i] << 16) + __uint_as_float((uint32_t)y[i] << 16);
+        const uint32_t u = __float_as_uint(v);
+        out[i] = (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+    } else {
+        out[i] = (uint16_t)f2h(h2f(x[i]) + h2f(y[i]));
+    }
+}
+
+int stack_cu_count() {
+    static int cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 0;
+    if (cache[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
+
+struct StackPlan {
+    int jg, km, jd, ndn;
+    int o_xs, o_cx, o_t, o_hs, o_hcx, o_a, o_y, o_xr, o_xn, o_meta, meta_bytes;
+    size_t lds;
+    bool ok;
+};
+
+StackPlan plan_stack(int M, int d, int f, int g, int r) {
+    StackPlan p{};
+    p.ok = false;
+    if (M != 1 || d <= 0 || f <= 0 || (g != 64 && g != 128))
+        return p;
+    if (f % SGRID != 0 || (f / SX) % 32 != 0 || d % (SB * 8) != 0 || d % g != 0 || f % g != 0)
+        return p;
+    const int RG = f / SGRID, UG = d / 64, ng = d / g, UF = f / SX / 32, DJ = d / SB;
+    if ((RG + 7) / 8 > SCW || ng % 4 != 0 || DJ > 128 || DJ % 16 != 0 || 2 * r > 64)
+        return p;
+    if (r != 0 && r != 8 && r != 16 && r != 32)
+        return p;
+    if (UG % 8 != 0)                             // 8 lanes per row, no partial slot
+        return p;
+    p.jg = UG / 8;
+    p.km = (4 * ng + 63) / 64;
+    p.jd = (UF + 7) / 8;
+    p.ndn = (DJ / 8 + SCW - 1) / SCW;
+    if ((d / 16 + SPT - 1) / SPT > KXW || (f / SX / 8 + SPT - 1) / SPT > KHW)
+        return p;
+    if ((2 * r * (DJ / 8) + SCW * 64 - 1) / (SCW * 64) > KA)
+        return p;
+    const bool inst = (p.jg == 5 && p.km == 2 && p.jd == 5 && p.ndn == 2) ||
+                      (p.jg == 8 && p.km == 2 && p.jd == 6 && p.ndn == 3) ||
+                      (p.jg == 1 && p.km == 1 && p.jd == 1 && p.ndn == 1);
+    if (!inst)
+        return p;
+    if (stack_cu_count() != SGRID)
+        return p;
+    size_t o = 16;
+    auto take = [&](size_t bytes) { const size_t at = o; o = (o + bytes + 15) / 16 * 16; return (int)at; };
+    p.o_xs = take((size_t)UG * 8 * 16);
+    p.o_cx = take((size_t)UG * 8);
+    p.o_t = take((size_t)2 * r * 4 + 4);
+    p.o_hs = take((size_t)p.jd * 8 * 4 * 16);     // chunk stride 8 JD >= UF units
+    p.o_hcx = take((size_t)p.jd * 8 * 8);
+    p.o_a = take((size_t)2 * r * DJ * 2 + 16);
+    p.o_y = take((size_t)DJ * 2);
+    p.o_xr = take((size_t)DJ * 2);
+    p.o_xn = take((size_t)DJ * 2);
+    p.meta_bytes = 2 * 8 * ng * 4;
+    p.o_meta = take((size_t)SCW * p.meta_bytes);
+    p.lds = o;
+    p.ok = p.lds <= 64 * 1024;
+    return p;
+}
+
+}  // namespace
+
+bool stack_supported(int M, int d, int f, int g, int r) { return plan_stack(M, d, f, g, r).ok; }
+
+size_t stack_ws_bytes(int d, int f, int r) {
+    const size_t xw = (size_t)d + 4 * (size_t)r * SB;
+    return 1024 + ((SX * xw * 4 + 255) & ~(size_t)255) + (((size_t)f * 4 + 255) & ~(size_t)255) +
+           (size_t)2 * SX * d * 8;
+}
+
+int stack_max_layers() { return kStackMaxLayers; }
+
+hipError_t launch_residual(const uint16_t* x, const uint16_t* y, uint16_t* out, int n, bool bf16,
+                           hipStream_t st) {
+    if (n <= 0)
+        return hipSuccess;
+    residual_kernel<<<(n + 255) / 256, 256, 0, st>>>(x, y, out, n, bf16 ? 1 : 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_stack(const StackLayerDesc* layers, int L, int d, int f, int g, int r,
+                        const uint16_t* x0, uint16_t* y, uint16_t* x_last, void* ws, hipStream_t st) {
+    const StackPlan p = plan_stack(1, d, f, g, r);
+    if (!p.ok || L <= 0 || L > kStackMaxLayers)
+        return hipErrorInvalidValue;
+    StackArgs a{};
+    for (int i = 0; i < L; ++i) {
+        const StackLayerDesc& s = layers[i];
+        a.lay[i] = StackLayer{s.cg, s.mg, s.cu, s.mu, s.cd, s.md, s.Bg, s.Bu, s.Ag, s.Au, s.lora_scale};
+    }
+    a.L = L;
+    a.d = d;
+    a.f = f;
+    a.g = g;
+    a.r = r;
+    a.x0 = x0;
+    a.y = y;
+    a.xl = x_last;
+    char* base = static_cast<char*>(ws);
+    a.ctl = reinterpret_cast<unsigned*>(base);
+    const size_t xw = (size_t)d + 4 * (size_t)r * SB;
+    a.xw = (int)xw;
+    a.xb = reinterpret_cast<uint32_t*>(base + 1024);
+    const size_t xbytes = (SX * xw * 4 + 255) & ~(size_t)255;
+    a.hb = reinterpret_cast<uint32_t*>(base + 1024 + xbytes);
+    a.pb = reinterpret_cast<unsigned long long*>(base + 1024 + xbytes + (((size_t)f * 4 + 255) & ~(size_t)255));
+    a.o_xs = p.o_xs; a.o_cx = p.o_cx; a.o_t = p.o_t; a.o_hs = p.o_hs; a.o_hcx = p.o_hcx;
+    a.o_a = p.o_a; a.o_y = p.o_y; a.o_xr = p.o_xr; a.o_xn = p.o_xn; a.o_meta = p.o_meta; a.meta_bytes = p.meta_bytes;
+    auto run = [&](auto kernel) -> hipError_t {
+        kernel<<<SGRID, STHREADS, p.lds, st>>>(a);
+        return hipGetLastError();
+    };
+    if (p.jg == 5)
+        return run(stack_kernel<5, 2, 5, 2>);
+    if (p.jg == 8)
+        return run(stack_kernel<8, 2, 6, 3>);
+    return run(stack_kernel<1, 1, 1, 1>);
+}
+
+}  // namespace qmlp

@@ -66,4 +66,21 @@ hipError_t launch_prefill_gateup(const uint32_t* cg, const uint32_t* mg, const u
 hipError_t launch_prefill_down(const uint32_t* cd, const uint32_t* md, const uint16_t* h,
                                uint16_t* y, int M, int d, int f, int g, hipStream_t st);
 
+// A stack of decode blocks in one persistent launch per up to
+// stack_max_layers() layers (decode_stack.hip): M = 1, binary16, layer l+1
+// reads x_{l+1} = x_l + y_l.  ws: the stack area (stack_ws_bytes, zero before
+// the first call).  launch_residual: out = x + y (binary16 or bfloat16).
+struct StackLayerDesc {
+    const uint32_t *cg, *mg, *cu, *mu, *cd, *md;
+    const uint16_t *Bg, *Bu, *Ag, *Au;
+    float lora_scale;
+};
+bool stack_supported(int M, int d, int f, int g, int r);
+size_t stack_ws_bytes(int d, int f, int r);
+int stack_max_layers();
+hipError_t launch_stack(const StackLayerDesc* layers, int L, int d, int f, int g, int r,
+                        const uint16_t* x0, uint16_t* y, uint16_t* x_last, void* ws, hipStream_t st);
+hipError_t launch_residual(const uint16_t* x, const uint16_t* y, uint16_t* out, int n, bool bf16,
+                           hipStream_t st);
+
 }  // namespace qmlp

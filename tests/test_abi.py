@@ -156,3 +156,34 @@ def test_binding_fails_loudly_without_library(q, monkeypatch, tmp_path):
     monkeypatch.setattr(q, "_LIB", None)
     with pytest.raises(ImportError):
         q.library()
+
+
+def _stack_arr(q, *mlps):
+    return (q.MlpC * len(mlps))(*mlps)
+
+
+def test_stack_validation(q, lib):
+    m = _mlp(q)
+    arr = _stack_arr(q, m, _mlp(q))
+    P = ctypes.c_void_p
+
+    def fs(a, L, M=1, x=FAKE, y=FAKE, ws=FAKE, wsb=1 << 30):
+        return lib.qmlp_forward_stack(a, L, P(x), M, 0, P(y), None, P(ws), wsb, None)
+
+    assert lib.qmlp_forward_stack(None, 2, None, 1, 0, None, None, None, 0, None) == NULL
+    assert fs(arr, 0) == SHAPE
+    assert fs(arr, 2, x=0) == NULL
+    assert fs(arr, 2, y=FAKE + 8) == ALIGN
+    assert fs(arr, 2, M=17) == UNSUP
+    assert fs(arr, 2, ws=0) == WS
+    assert fs(arr, 2, wsb=16) == WS
+    # layers of different shapes are rejected
+    odd = _stack_arr(q, m, _mlp(q, d=320, f=448))
+    assert fs(odd, 2) == SHAPE
+    assert lib.qmlp_stack_workspace_bytes(odd, 2, 1, 0) == 0
+    assert lib.qmlp_stack_launches(odd, 2, 1, 0) == 0
+    # an invalid block anywhere in the stack is reported
+    bad = _stack_arr(q, m, _mlp(q, rank=7))
+    assert fs(bad, 2) == UNSUP
+    # the stack workspace covers at least the per-block workspace
+    assert lib.qmlp_stack_workspace_bytes(arr, 2, 1, 0) >= lib.qmlp_workspace_bytes(ctypes.byref(m), 1, 0)
