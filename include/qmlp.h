@@ -171,32 +171,34 @@ qmlp_status qmlp_forward(const qmlp_mlp *mlp, const void *x, int M, qmlp_dtype d
                          void *y, void *ws, size_t ws_bytes, qmlp_stream stream);
 
 /*
- * A stack of L blocks of one shape on a residual stream, as the MLP blocks
- * of an L-layer decoder with the attention blocks and norms between them
- * left out (Sec. 3.3: each layer's gated MLP):
- *   x_0 = x,  y_l = block_l(x_l),  x_{l+1} = x_l + y_l,
- * where y_l is rounded to the activation type and the sum of the two
- * rounded values is rounded once (nearest-even).  layers[0..L-1] are host
- * descriptors (same d, f, group and rank); x [M][d]; y [L][M][d] receives
- * every block's output (layer l at y + l*M*d); x_out [M][d] (may be NULL)
- * receives x_L.  Each y_l equals qmlp_forward of layer l on x_l within the
- * output bar.
+ * A stack of L blocks of one shape on a residual stream, as the MLP
+ * sub-blocks of an L-layer decoder with the attention sub-blocks left out
+ * (Sec. 3.3: each layer carries one gated MLP):
+ *   x_0 = x,  u_l = RMSNorm(x_l),  y_l = block_l(u_l),  x_{l+1} = x_l + y_l,
+ * RMSNorm(v) = v / sqrt(mean(v^2) + 1e-6) per token with unit gain (a
+ * learned gain folds into the input columns of gate, up and LoRA-A before
+ * quantization).  u_l and y_l are rounded to binary16, the sum of two
+ * binary16 values is rounded once (nearest-even).  Binary16 only.
+ * layers[0..L-1] are host descriptors (same d, f, group and rank); x [M][d];
+ * y [L][M][d] receives every block's output (layer l at y + l*M*d); x_out
+ * [M][d] (may be NULL) receives x_L.  Each y_l equals qmlp_forward of layer
+ * l on RMSNorm(x_l) within the output bar.
  *
- * At M = 1 in binary16, for shapes with f % 256 == 0, d % 512 == 0,
- * d <= 4096, (d/g) % 4 == 0 on a GPU with 8 XCDs of 32 compute units, the
- * stack runs as ONE persistent launch per 40 layers: the weights of block
- * l+1 stream in while block l finishes (weights do not depend on
- * activations), and no step of block l+1 starts before x_{l+1} is
- * complete.  Every other shape runs as L qmlp_forward calls with a residual
- * add between them.
+ * At M = 1 for shapes with f % 256 == 0, d % 512 == 0, d <= 4096,
+ * (d/g) % 4 == 0 on a GPU with 8 XCDs of 32 compute units, the stack runs
+ * as ONE persistent launch per 40 layers: the weights of block l+1 stream in
+ * while block l finishes (weights do not depend on activations), and no
+ * step of block l+1 starts before x_{l+1} is complete.  Every other shape
+ * runs per block: a norm kernel, qmlp_forward, a residual-add kernel.
  *
  * ws/ws_bytes: at least qmlp_stack_workspace_bytes(layers, L, M, dtype),
  * zero before the first call, with the rules of qmlp_workspace_bytes (after
- * the per-block workspace come two residual buffers, then the persistent
- * launch's 1024-byte control block -- word 0 its step counter, word 64
- * sticky error bits: 1/2/4 = a wait for the activation / h / the cross-XCD
- * partials gave up, 8 = a workgroup found no place -- and its hand-off
- * words).  Errors as for qmlp_forward.
+ * the per-block workspace come three activation buffers, then the
+ * persistent launch's 1024-byte control block -- word 0 its step counter,
+ * word 64 sticky error bits: 1/2/4 = a wait for the activation / h / the
+ * cross-XCD partials gave up, 8 = a workgroup found no place -- and its
+ * hand-off words).  Errors as for qmlp_forward; QMLP_ERR_UNSUPPORTED for
+ * bfloat16.
  */
 size_t qmlp_stack_workspace_bytes(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
 
@@ -205,8 +207,8 @@ qmlp_status qmlp_forward_stack(const qmlp_mlp *layers, int L, const void *x, int
                                qmlp_stream stream);
 
 /* Launches qmlp_forward_stack makes: the number of persistent launches when
- * the stack runs persistently, else the per-layer kernels plus the residual
- * adds; 0 if the call would be rejected.  Host-only. */
+ * the stack runs persistently, else the per-layer kernels plus the norm and
+ * residual-add kernels; 0 if the call would be rejected.  Host-only. */
 int qmlp_stack_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
 
 /* ---------------------------------------------- inspection (not timed) */

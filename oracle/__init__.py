@@ -13,7 +13,9 @@ the passage of the paper it follows in the C source:
   fp16 scale/zero is this library's reading);
 * dequantization (Sec. 6.3, quantize-dequantize semantics);
 * LoRA-augmented linear (Sec. 3.1, Eq. (1)), adapters kept unmerged (Sec. 4.2);
-* fused gate-activation-down with an fp64, unrounded intermediate (Sec. 5).
+* fused gate-activation-down with an fp64, unrounded intermediate (Sec. 5);
+* the decoder context of a stack of blocks: unit-gain RMSNorm of the
+  residual stream before each block and the residual add after it.
 """
 from __future__ import annotations
 
@@ -73,6 +75,10 @@ def _load():
     lib.orc_down_act.argtypes = [L, L, L, L, P, P, P, P, I, P]
     lib.orc_forward.restype = I
     lib.orc_forward.argtypes = [L, L, L, L, L] + [P] * 9 + [P] * 4 + [L, D, I, P, P, P]
+    lib.orc_rmsnorm_f16.restype = None
+    lib.orc_rmsnorm_f16.argtypes = [P, L, L, D, P]
+    lib.orc_residual_f16.restype = None
+    lib.orc_residual_f16.argtypes = [P, P, L, P]
     _lib = lib
     return lib
 
@@ -280,3 +286,25 @@ def max_rel_err(got: np.ndarray, ref: np.ndarray) -> float:
     ref = np.asarray(ref, np.float64)
     den = np.max(np.abs(ref))
     return float(np.max(np.abs(got - ref)) / den) if den > 0 else float(np.max(np.abs(got)))
+
+
+# ---------------------------------------------------------------- stack context
+RMS_EPS = 1e-6
+
+
+def rmsnorm_f16(x: np.ndarray, eps: float = RMS_EPS) -> np.ndarray:
+    """u = x / sqrt(mean(x^2) + eps) per row, binary16 bits in and out."""
+    x = _c(x, np.uint16)
+    M, d = x.reshape(-1, x.shape[-1]).shape
+    u = np.empty_like(x)
+    _load().orc_rmsnorm_f16(_p(x), M, d, float(eps), _p(u))
+    return u
+
+
+def residual_f16(x: np.ndarray, y: np.ndarray) -> np.ndarray:
+    """x + y of binary16 bits, rounded once."""
+    x = _c(x, np.uint16)
+    y = _c(y, np.uint16)
+    out = np.empty_like(x)
+    _load().orc_residual_f16(_p(x), _p(y), x.size, _p(out))
+    return out

@@ -405,3 +405,39 @@ int orc_forward(long M, long d, long f, long g_gu, long g_dn,
     free(h);
     return rc;
 }
+
+/* ------------------------------------------------------------------ */
+/* The decoder context of a stack of blocks.                          */
+/* ------------------------------------------------------------------ */
+
+/*
+ * Sec. 3.3: every layer of the model carries one gated MLP; in a decoder
+ * its input is the normalized residual stream and its output is added back
+ * to the stream.  A stack of blocks is modelled with the attention blocks
+ * left out:
+ *   u = RMSNorm(x) = x / sqrt(mean_i(x_i^2) + eps)     (unit gain, per token)
+ *   x_next = x + y,  y = block(u)
+ * Both results are rounded once to binary16.  (A learned norm gain folds
+ * into the input columns of the block's gate, up and LoRA-A weights before
+ * quantization, so the run-time norm has unit gain.)
+ */
+void orc_rmsnorm_f16(const uint16_t *x, long M, long d, double eps, uint16_t *u)
+{
+    for (long m = 0; m < M; ++m) {
+        double ss = 0.0;
+        for (long i = 0; i < d; ++i) {
+            double v = orc_f16_to_f64(x[m * d + i]);
+            ss += v * v;
+        }
+        double inv = 1.0 / sqrt(ss / (double)d + eps);
+        for (long i = 0; i < d; ++i)
+            u[m * d + i] = orc_f64_to_f16(orc_f16_to_f64(x[m * d + i]) * inv);
+    }
+}
+
+/* x + y of binary16 values, the exact sum rounded once to binary16. */
+void orc_residual_f16(const uint16_t *x, const uint16_t *y, long n, uint16_t *out)
+{
+    for (long i = 0; i < n; ++i)
+        out[i] = orc_f64_to_f16(orc_f16_to_f64(x[i]) + orc_f16_to_f64(y[i]));
+}

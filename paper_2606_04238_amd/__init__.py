@@ -11,7 +11,7 @@ Functions keep the names of the C entry points:
 * ``gateup_w2_lora``              -- h = SiLU(W2g x + s B_g A_g x) * (W2u x + s B_u A_u x)
 * ``down_w4``                     -- y = W4down h
 * ``forward``                     -- the whole block x -> y
-* ``forward_stack``               -- L blocks on a residual stream, x_{l+1} = x_l + y_l
+* ``forward_stack``               -- L blocks on a residual stream, x_{l+1} = x_l + block_l(RMSNorm(x_l))
 * ``unpack`` / ``dequant``        -- inspection of a packed matrix (not timed)
 """
 from __future__ import annotations
@@ -275,8 +275,9 @@ def dequant(w: QWeight) -> torch.Tensor:
 
 
 class Stack:
-    """L blocks of one shape on a residual stream (x_{l+1} = x_l + y_l);
-    holds the C descriptor array the stack entry points take."""
+    """L blocks of one shape on a residual stream (x_{l+1} = x_l + y_l,
+    y_l = block_l(RMSNorm(x_l))); holds the C descriptor array the stack
+    entry points take."""
 
     def __init__(self, mlps):
         self.mlps = list(mlps)
@@ -316,15 +317,15 @@ def stack_errors(stack: Stack, ws: torch.Tensor, M: int = 1, dtype=torch.float16
 def _stack_area_bytes(stack: Stack) -> int:
     m = stack.mlps[0]
     d, f, r = m.d, m.f, m.rank
-    xw = d + 4 * r * 32
+    xw = d + 2 * (2 * r + 1) * 32
     rnd = lambda v: (v + 255) // 256 * 256  # noqa: E731
     return 1024 + rnd(8 * xw * 4) + rnd(f * 4) + 2 * 8 * d * 8
 
 
 def forward_stack(stack: Stack, x: torch.Tensor, y: torch.Tensor | None = None,
                   ws: torch.Tensor | None = None, x_out: torch.Tensor | None = None) -> torch.Tensor:
-    """y [L][M][d]: every block's output on the residual stream x_{l+1} = x_l + y_l
-    (x_out, if given, receives x_L)."""
+    """y [L][M][d]: every block's output y_l = block_l(RMSNorm(x_l)) on the
+    residual stream x_{l+1} = x_l + y_l (x_out, if given, receives x_L)."""
     M = x.shape[0]
     d = stack.mlps[0].d
     if y is None:

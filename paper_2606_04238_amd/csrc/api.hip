@@ -234,6 +234,8 @@ qmlp_status check_stack(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) 
         return QMLP_ERR_NULL;
     if (L <= 0)
         return QMLP_ERR_SHAPE;
+    if (dtype != QMLP_F16)                        // the stream and the norm are binary16
+        return QMLP_ERR_UNSUPPORTED;
     for (int i = 0; i < L; ++i) {
         qmlp_status s = check_mlp(&layers[i], M, dtype);
         if (s != QMLP_OK)
@@ -432,7 +434,7 @@ int qmlp_forward_launches(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
 size_t qmlp_stack_workspace_bytes(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
     if (check_stack(layers, L, M, dtype) != QMLP_OK || M == 0)
         return 0;
-    size_t n = stack_layer_ws(layers, M, dtype) + 2 * round256((size_t)M * layers[0].gate.k_in * 2);
+    size_t n = stack_layer_ws(layers, M, dtype) + 3 * round256((size_t)M * layers[0].gate.k_in * 2);
     if (stack_persistent(layers, M, dtype))
         n += stack_ws_bytes(layers[0].gate.k_in, layers[0].gate.n_out, layers[0].rank);
     return n;
@@ -444,7 +446,7 @@ int qmlp_stack_launches(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) 
     if (stack_persistent(layers, M, dtype))
         return (L + stack_max_layers() - 1) / stack_max_layers();
     int n = 0;
-    for (int i = 0; i < L; ++i) n += qmlp_forward_launches(&layers[i], M, dtype) + 1;
+    for (int i = 0; i < L; ++i) n += qmlp_forward_launches(&layers[i], M, dtype) + 2;
     return n - 1;
 }
 
@@ -467,7 +469,8 @@ qmlp_status qmlp_forward_stack(const qmlp_mlp* layers, int L, const void* x, int
     const size_t step = (size_t)M * d * 2;
     const size_t lws = stack_layer_ws(layers, M, dtype);
     char* pp[2] = {static_cast<char*>(ws) + lws, static_cast<char*>(ws) + lws + round256(step)};
-    char* area = static_cast<char*>(ws) + lws + 2 * round256(step);
+    uint16_t* ub = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + lws + 2 * round256(step));
+    char* area = static_cast<char*>(ws) + lws + 3 * round256(step);
     hipStream_t st = static_cast<hipStream_t>(stream);
     char* yb = static_cast<char*>(y);
     if (stack_persistent(layers, M, dtype)) {
@@ -487,10 +490,12 @@ qmlp_status qmlp_forward_stack(const qmlp_mlp* layers, int L, const void* x, int
         }
         return QMLP_OK;
     }
-    // per block: y_l = MLP_l(x_l), then x_{l+1} = x_l + y_l
+    // per block: u_l = RMSNorm(x_l), y_l = MLP_l(u_l), then x_{l+1} = x_l + y_l
     const void* xin = x;
     for (int i = 0; i < L; ++i) {
-        s = qmlp_forward(&layers[i], xin, M, dtype, yb + i * step, ws, lws, st);
+        if (launch_rmsnorm(static_cast<const uint16_t*>(xin), ub, M, d, st) != hipSuccess)
+            return QMLP_ERR_HIP;
+        s = qmlp_forward(&layers[i], ub, M, dtype, yb + i * step, ws, lws, st);
         if (s != QMLP_OK)
             return s;
         void* next = i + 1 == L ? x_out : pp[i & 1];

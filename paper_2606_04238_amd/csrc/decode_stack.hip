@@ -5,10 +5,11 @@
 // adapters (Sec. 3.1 Eq. (1), Sec. 3.3, Sec. 4.2):
 //   G = W2gate x + s B_g (A_g x),  U = W2up x + s B_u (A_u x),
 //   h = SiLU(G) * U,  y = W4down h,
-// and the blocks sit on a residual stream as in a decoder: block l+1 reads
-// x_{l+1} = x_l + y_l (each y_l rounded to binary16 and returned, the sum
-// rounded once to binary16), with the attention blocks and norms between
-// them left out.  Decode is bound by loading
+// and the blocks sit on a residual stream as in a decoder: block l reads
+// u_l = RMSNorm(x_l) (unit gain: a learned gain folds into the block's
+// input columns before quantization) and x_{l+1} = x_l + y_l (each y_l
+// rounded to binary16 and returned, the sum rounded once), with the
+// attention blocks left out.  Decode is bound by loading
 // weights (Sec. 3.3, Sec. 5); what a per-layer launch cannot hide is the
 // chain of dependent steps inside a layer.  Here the weights of block l+1
 // stream into registers while block l runs its hand-offs: weights do not
@@ -25,9 +26,11 @@
 //     j of the other XCDs;
 //   * block j of every XCD sums the eight partials of D_j in XCD order (the
 //     same sum on every XCD), rounds y to binary16, adds the residual
-//     x[D_j], computes its share of the next block's LoRA-A product
-//     (A[:, D_j] x_{l+1}[D_j], fp32) and publishes both to the blocks of its
-//     own XCD, which add the 32 shares in order.
+//     x[D_j], computes its shares of the next block's LoRA-A product
+//     (A[:, D_j] x_{l+1}[D_j], fp32) and of sum x_{l+1}^2 over D_j, and
+//     publishes them with x_{l+1}[D_j] to the blocks of its own XCD, which
+//     add the 32 shares in order; the norm then scales the staged input, and
+//     the LoRA-A product by the same factor (it is linear in the input).
 // So every layer has one hand-off between XCDs and two inside an XCD,
 // through that XCD's L2.  The XCD of a workgroup is read from HW_REG_XCC_ID
 // and its rank inside the XCD from a per-XCD counter, so producer and
@@ -62,6 +65,7 @@ constexpr unsigned kStackSpin = 1u << 17;
 constexpr int KA = 3;                     // LoRA-A slice loads per compute thread (max)
 constexpr int KXW = 2;                    // activation staging words per polling thread (max)
 constexpr int KHW = 2;                    // h staging words per polling thread (max)
+constexpr float kRmsEps = 1e-6f;          // RMSNorm epsilon
 
 // Control words (uint32 index into the stack's control block).
 constexpr int C_SEQ = 0, C_DONE = 32, C_ERR = 64, C_XC = 96;
@@ -103,12 +107,13 @@ struct StackArgs {
     const uint16_t* x0;          // [d] input of the first layer
     uint16_t* y;                 // [L][d] output of every layer
     uint16_t* xl;                // [d] the residual stream after the last layer (may be null)
-    uint32_t* xb;                // [8][xw] XCD-local: d y words, then [2r][32] 64-bit LoRA-A shares
+    uint32_t* xb;                // [8][xw] XCD-local: d x words, then [2r+1][32] 64-bit shares
+                                 // (LoRA-A ranks, then the sum of squares)
     uint32_t* hb;                // [f] XCD-local h words (XCD x owns [x f/8, (x+1) f/8))
     unsigned long long* pb;      // [2][8][d] cross-XCD partial down sums
     unsigned* ctl;
     int xw;                      // 32-bit words per XCD in xb
-    int o_xs, o_cx, o_t, o_hs, o_hcx, o_a, o_y, o_xr, o_xn, o_meta, meta_bytes;   // LDS byte offsets
+    int o_xs, o_cx, o_t, o_hs, o_hcx, o_a, o_y, o_xr, o_xn, o_bc, o_meta, meta_bytes;   // LDS byte offsets
 };
 
 namespace {
@@ -141,21 +146,23 @@ __device__ __forceinline__ bool sk_poll(__amdgpu_buffer_rsrc_t rs, const int (&o
 }
 
 // One staging word of the activation: 16 binary16 values x[16w .. 16w+16)
-// (low halves of four tagged 16-byte words) pre-scaled per fraction position
+// (low halves of four tagged 16-byte words), normalized (times inv, rounded
+// to binary16: the block's input u) and pre-scaled per fraction position
 // into the x' layout of the gate/up units: chunk-major, xs[c * XS + ul] for
 // chunk c (0..7) of 64-code unit ul = w / 4, so the 8 lanes of a row read 8
 // consecutive 16-byte entries (no bank conflict) at one base address plus
 // immediates; and per unit (1024 sum x', sum x).  Every lane of the wave
 // calls it (quad reductions); lanes with valid == false store nothing.
 template <int XS>
-__device__ __forceinline__ void sk_stage_x(uint4* xs, float2* cx, const u32x4* v, bool valid, int w) {
-    uint32_t xv[16];
+__device__ __forceinline__ void sk_stage_x(uint4* xs, float2* cx, const u32x4* v, bool valid, int w,
+                                           float inv) {
+    uint32_t xv[16];                     // the block input u = x * inv, binary16
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-        xv[4 * q + 0] = valid ? v[q].x & 0xFFFFu : 0u;
-        xv[4 * q + 1] = valid ? v[q].y & 0xFFFFu : 0u;
-        xv[4 * q + 2] = valid ? v[q].z & 0xFFFFu : 0u;
-        xv[4 * q + 3] = valid ? v[q].w & 0xFFFFu : 0u;
+        xv[4 * q + 0] = valid ? f2h(h2f(v[q].x & 0xFFFFu) * inv) : 0u;
+        xv[4 * q + 1] = valid ? f2h(h2f(v[q].y & 0xFFFFu) * inv) : 0u;
+        xv[4 * q + 2] = valid ? f2h(h2f(v[q].z & 0xFFFFu) * inv) : 0u;
+        xv[4 * q + 3] = valid ? f2h(h2f(v[q].w & 0xFFFFu) * inv) : 0u;
     }
     uint32_t pr[8];
     float csum = 0.0f, xsum = 0.0f;
@@ -430,9 +437,10 @@ __device__ __forceinline__ void sk_a_store(const uint4 (&av)[KA], uint4* as, int
     }
 }
 
-// Polling wave 0: block j's rows D_j of the next layer's input (binary16
-// pairs in xn) and its share of that layer's LoRA-A product go to the
-// XCD-local activation buffer; lanes l < DJ/2 hold rows 2l, 2l+1.
+// Polling wave 0: block j's rows D_j of the next layer's stream (binary16
+// pairs in xn), its shares of that layer's LoRA-A product (unnormalized)
+// and of sum x^2 go to the XCD-local activation buffer; lanes l < DJ/2 hold
+// rows 2l, 2l+1.
 __device__ __forceinline__ void sk_publish_x(uint32_t* xb, const uint32_t* xn, const uint16_t* as,
                                              int d, int r, int DJ, int j, uint32_t tag, int lane) {
     if (lane < DJ / 2) {
@@ -441,15 +449,26 @@ __device__ __forceinline__ void sk_publish_x(uint32_t* xb, const uint32_t* xn, c
                                       ((unsigned long long)((v >> 16) | (tag << 16)) << 32);
         st_intra64(reinterpret_cast<unsigned long long*>(xb + j * DJ) + lane, wv);
     }
+    unsigned long long* t64 = reinterpret_cast<unsigned long long*>(xb + d);
     if (lane < 2 * r) {
         const uint32_t* a32 = reinterpret_cast<const uint32_t*>(as) + lane * (DJ / 2);
         float acc = 0.0f;
         for (int c = 0; c < DJ / 2; ++c)
             acc = dot2(a32[c], xn[c], acc);
-        unsigned long long* t64 = reinterpret_cast<unsigned long long*>(xb + d);
         st_intra64(t64 + lane * SB + j, (unsigned long long)__float_as_uint(acc) |
                                             ((unsigned long long)tag << 32));
     }
+    // the share of sum x^2 (for the next block's norm), reduced over the wave
+    float ss = 0.0f;
+    if (lane < DJ / 2) {
+        const uint32_t v = xn[lane];
+        const float a = h2f(v & 0xFFFFu), b = h2f(v >> 16);
+        ss = a * a + b * b;
+    }
+    ss = group_sum<64>(ss);
+    if (lane == 0)
+        st_intra64(t64 + 2 * r * SB + j, (unsigned long long)__float_as_uint(ss) |
+                                             ((unsigned long long)tag << 32));
 }
 
 typedef const StackArgs __attribute__((address_space(4))) KArgs;
@@ -475,6 +494,7 @@ struct SkLds {
     uint32_t* ys;       // y[D_j] binary16 pairs
     uint16_t* xr;       // x[D_j] of the current layer (the residual)
     uint32_t* xn;       // x[D_j] of the next layer, binary16 pairs
+    unsigned long long* bc;   // 1 / rms of the current input | tag << 32
     char* meta;         // per-wave gate/up metadata areas
 };
 
@@ -577,6 +597,8 @@ __device__ __forceinline__ void sk_poll_role(const StackArgs& sa, const SkLds& m
     bool dead = false;                                          // this wave gave up a wait
     if (wave == SCW && lane < DJ / 2)
         m.xn[lane] = reinterpret_cast<const uint32_t*>(sa.x0 + j * DJ)[lane];
+    if (wave == SCW && lane == 0)
+        *m.bc = 0;                                              // no tag
     __syncthreads();                                            // B0
     if (wave == SCW)
         sk_publish_x(xb, m.xn, reinterpret_cast<const uint16_t*>(m.as), d, r, DJ, j, stag(pl.seq0), lane);
@@ -594,7 +616,7 @@ __device__ __forceinline__ void sk_poll_role(const StackArgs& sa, const SkLds& m
     }
 #pragma unroll
     for (int q = 0; q < 16; ++q) xoff[4 * KXW + q] = d * 4 + pt * SB * 8 + 16 * q;
-    if (pt < 2 * r) xvalid |= 0xFFFFu << (4 * KXW);
+    if (pt <= 2 * r) xvalid |= 0xFFFFu << (4 * KXW);           // rank pt, or the sum of squares
     // h words of this XCD's slice: staging word w = pt + SPT kk covers h[8w, 8w+8)
     int hoff[2 * KHW];
     uint32_t hvalid = 0;
@@ -610,10 +632,34 @@ __device__ __forceinline__ void sk_poll_role(const StackArgs& sa, const SkLds& m
         {   // the activation and the LoRA-A shares of this XCD
             u32x4 v[4 * KXW + 16];
             dead |= !sk_poll<4 * KXW + 16, 4 * KXW, POL_INTRA>(xrs, xoff, xvalid, v, tx, dead);
+            // shares in block order; thread 2r holds sum x^2 and hands
+            // 1 / rms to both polling waves through a tagged LDS word
+            float share = 0.0f;
+            if (pt <= 2 * r) {
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    share += __uint_as_float(v[4 * KXW + q].x);
+                    share += __uint_as_float(v[4 * KXW + q].z);
+                }
+            }
+            if (pt == 2 * r) {
+                const float inv0 = 1.0f / __fsqrt_rn(share / (float)d + kRmsEps);
+                __hip_atomic_store(m.bc, (unsigned long long)__float_as_uint(inv0) |
+                                             ((unsigned long long)tx << 32),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+            unsigned long long bv = 0;
+            for (unsigned it = 0; it < kStackSpin; ++it) {
+                bv = __hip_atomic_load(m.bc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                if ((uint32_t)(bv >> 32) == tx)
+                    break;
+                __builtin_amdgcn_s_sleep(1);
+            }
+            const float inv = __uint_as_float((uint32_t)bv);
 #pragma unroll
             for (int kk = 0; kk < KXW; ++kk) {
                 const int w = pt + SPT * kk;
-                sk_stage_x<XS>(m.xs, m.cxg, v + 4 * kk, w < d / 16, w);
+                sk_stage_x<XS>(m.xs, m.cxg, v + 4 * kk, w < d / 16, w, inv);
                 const int wr = w - j * (DJ / 16);             // this block's residual rows D_j
                 if (wr >= 0 && wr < DJ / 16) {
 #pragma unroll
@@ -624,15 +670,8 @@ __device__ __forceinline__ void sk_poll_role(const StackArgs& sa, const SkLds& m
                     }
                 }
             }
-            if (pt < 2 * r) {
-                float t = 0.0f;
-#pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    t += __uint_as_float(v[4 * KXW + q].x);
-                    t += __uint_as_float(v[4 * KXW + q].z);
-                }
-                m.ts[pt] = t;
-            }
+            if (pt < 2 * r)
+                m.ts[pt] = share * inv;                        // A u = (A x) / rms
             dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
             if (dead && lane == 0)
                 atomicOr(&ctl[C_ERR], 1u);
@@ -716,7 +755,8 @@ __global__ void __launch_bounds__(STHREADS) stack_kernel(StackArgs sa) {
                       reinterpret_cast<float*>(lds + sa.o_t), reinterpret_cast<uint4*>(lds + sa.o_hs),
                       reinterpret_cast<float2*>(lds + sa.o_hcx), reinterpret_cast<uint4*>(lds + sa.o_a),
                       reinterpret_cast<uint32_t*>(lds + sa.o_y), reinterpret_cast<uint16_t*>(lds + sa.o_xr),
-                      reinterpret_cast<uint32_t*>(lds + sa.o_xn), lds + sa.o_meta};
+                      reinterpret_cast<uint32_t*>(lds + sa.o_xn),
+                      reinterpret_cast<unsigned long long*>(lds + sa.o_bc), lds + sa.o_meta};
         const SkPlace pl{(int)xcc, j, seq0};
         if (wave < SCW)
             sk_compute_role<JG, KM, JD, NDN>(sa, (KArgs*)__builtin_amdgcn_kernarg_segment_ptr(), m, pl, wave, lane);
@@ -756,6 +796,28 @@ __global__ void residual_kernel(const uint16_t* x, const uint16_t* y, uint16_t* 
     }
 }
 
+// u = x / sqrt(mean(x^2) + eps) per row (binary16 in and out; fp32 sums in
+// a fixed order): the input of a block on the per-layer path.
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const uint16_t* x, uint16_t* u, int d) {
+    __shared__ float part[256];
+    const uint16_t* xr = x + (long)blockIdx.x * d;
+    float ss = 0.0f;
+    for (int i = threadIdx.x; i < d; i += 256) {
+        const float v = h2f(xr[i]);
+        ss += v * v;
+    }
+    part[threadIdx.x] = ss;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s)
+            part[threadIdx.x] += part[threadIdx.x + s];
+        __syncthreads();
+    }
+    const float inv = 1.0f / __fsqrt_rn(part[0] / (float)d + kRmsEps);
+    for (int i = threadIdx.x; i < d; i += 256)
+        u[(long)blockIdx.x * d + i] = (uint16_t)f2h(h2f(xr[i]) * inv);
+}
+
 int stack_cu_count() {
     static int cache[64];
     int dev = 0;
@@ -772,7 +834,7 @@ int stack_cu_count() {
 
 struct StackPlan {
     int jg, km, jd, ndn;
-    int o_xs, o_cx, o_t, o_hs, o_hcx, o_a, o_y, o_xr, o_xn, o_meta, meta_bytes;
+    int o_xs, o_cx, o_t, o_hs, o_hcx, o_a, o_y, o_xr, o_xn, o_bc, o_meta, meta_bytes;
     size_t lds;
     bool ok;
 };
@@ -785,7 +847,7 @@ StackPlan plan_stack(int M, int d, int f, int g, int r) {
     if (f % SGRID != 0 || (f / SX) % 32 != 0 || d % (SB * 8) != 0 || d % g != 0 || f % g != 0)
         return p;
     const int RG = f / SGRID, UG = d / 64, ng = d / g, UF = f / SX / 32, DJ = d / SB;
-    if ((RG + 7) / 8 > SCW || ng % 4 != 0 || DJ > 128 || DJ % 16 != 0 || 2 * r > 64)
+    if ((RG + 7) / 8 > SCW || ng % 4 != 0 || DJ > 128 || DJ % 16 != 0 || 2 * r + 1 > SPT)
         return p;
     if (r != 0 && r != 8 && r != 16 && r != 32)
         return p;
@@ -817,6 +879,7 @@ StackPlan plan_stack(int M, int d, int f, int g, int r) {
     p.o_y = take((size_t)DJ * 2);
     p.o_xr = take((size_t)DJ * 2);
     p.o_xn = take((size_t)DJ * 2);
+    p.o_bc = take(8);
     p.meta_bytes = 2 * 8 * ng * 4;
     p.o_meta = take((size_t)SCW * p.meta_bytes);
     p.lds = o;
@@ -829,12 +892,19 @@ StackPlan plan_stack(int M, int d, int f, int g, int r) {
 bool stack_supported(int M, int d, int f, int g, int r) { return plan_stack(M, d, f, g, r).ok; }
 
 size_t stack_ws_bytes(int d, int f, int r) {
-    const size_t xw = (size_t)d + 4 * (size_t)r * SB;
+    const size_t xw = (size_t)d + 2 * (2 * (size_t)r + 1) * SB;
     return 1024 + ((SX * xw * 4 + 255) & ~(size_t)255) + (((size_t)f * 4 + 255) & ~(size_t)255) +
            (size_t)2 * SX * d * 8;
 }
 
 int stack_max_layers() { return kStackMaxLayers; }
+
+hipError_t launch_rmsnorm(const uint16_t* x, uint16_t* u, int M, int d, hipStream_t st) {
+    if (M <= 0)
+        return hipSuccess;
+    rmsnorm_kernel<<<M, 256, 0, st>>>(x, u, d);
+    return hipGetLastError();
+}
 
 hipError_t launch_residual(const uint16_t* x, const uint16_t* y, uint16_t* out, int n, bool bf16,
                            hipStream_t st) {
@@ -864,14 +934,14 @@ hipError_t launch_stack(const StackLayerDesc* layers, int L, int d, int f, int g
     a.xl = x_last;
     char* base = static_cast<char*>(ws);
     a.ctl = reinterpret_cast<unsigned*>(base);
-    const size_t xw = (size_t)d + 4 * (size_t)r * SB;
+    const size_t xw = (size_t)d + 2 * (2 * (size_t)r + 1) * SB;
     a.xw = (int)xw;
     a.xb = reinterpret_cast<uint32_t*>(base + 1024);
     const size_t xbytes = (SX * xw * 4 + 255) & ~(size_t)255;
     a.hb = reinterpret_cast<uint32_t*>(base + 1024 + xbytes);
     a.pb = reinterpret_cast<unsigned long long*>(base + 1024 + xbytes + (((size_t)f * 4 + 255) & ~(size_t)255));
     a.o_xs = p.o_xs; a.o_cx = p.o_cx; a.o_t = p.o_t; a.o_hs = p.o_hs; a.o_hcx = p.o_hcx;
-    a.o_a = p.o_a; a.o_y = p.o_y; a.o_xr = p.o_xr; a.o_xn = p.o_xn; a.o_meta = p.o_meta; a.meta_bytes = p.meta_bytes;
+    a.o_a = p.o_a; a.o_y = p.o_y; a.o_xr = p.o_xr; a.o_xn = p.o_xn; a.o_bc = p.o_bc; a.o_meta = p.o_meta; a.meta_bytes = p.meta_bytes;
     auto run = [&](auto kernel) -> hipError_t {
         kernel<<<SGRID, STHREADS, p.lds, st>>>(a);
         return hipGetLastError();

@@ -67,8 +67,8 @@ hipError_t launch_prefill_down(const uint32_t* cd, const uint32_t* md, const uin
                                uint16_t* y, int M, int d, int f, int g, hipStream_t st);
 
 // A stack of decode blocks in one persistent launch per up to
-// stack_max_layers() layers (decode_stack.hip): M = 1, binary16, layer l+1
-// reads x_{l+1} = x_l + y_l.  ws: the stack area (stack_ws_bytes, zero before
+// stack_max_layers() layers (decode_stack.hip): M = 1, binary16, block l
+// reads RMSNorm(x_l) and x_{l+1} = x_l + y_l.  ws: the stack area (stack_ws_bytes, zero before
 // the first call).  launch_residual: out = x + y (binary16 or bfloat16).
 struct StackLayerDesc {
     const uint32_t *cg, *mg, *cu, *mu, *cd, *md;
@@ -82,5 +82,6 @@ hipError_t launch_stack(const StackLayerDesc* layers, int L, int d, int f, int g
                         const uint16_t* x0, uint16_t* y, uint16_t* x_last, void* ws, hipStream_t st);
 hipError_t launch_residual(const uint16_t* x, const uint16_t* y, uint16_t* out, int n, bool bf16,
                            hipStream_t st);
+hipError_t launch_rmsnorm(const uint16_t* x, uint16_t* u, int M, int d, hipStream_t st);
 
 }  // namespace qmlp

@@ -1,12 +1,13 @@
 """GPU parity of the layer stack (qmlp_forward_stack) against the fp64 oracle.
 
-The stack runs L blocks on a residual stream: x_0 = x, y_l = block_l(x_l),
-x_{l+1} = x_l + y_l (binary16; the sum of two binary16 values computed in
-fp32 and rounded once equals the exactly rounded sum, so the stream is
-recomputed here bit for bit).  Each block's output is compared with the
-oracle's forward of that block's quantized weights on the same input the
-GPU block read, at the output bar max|y - y_ref| / max|y_ref| <= 1e-2.  The
-oracle quantizes the fp32 weights itself and keeps h in fp64.  Each case
+The stack runs L blocks on a residual stream: x_0 = x, u_l = RMSNorm(x_l),
+y_l = block_l(u_l), x_{l+1} = x_l + y_l (binary16; the sum of two binary16
+values computed in fp32 and rounded once equals the exactly rounded sum, so
+the stream is recomputed here bit for bit from the GPU's y_l).  Each block's
+output is compared with the oracle's forward of that block's quantized
+weights on the oracle's RMSNorm of the same stream state, at the output bar
+max|y - y_ref| / max|y_ref| <= 1e-2.  The oracle quantizes the fp32 weights
+itself, normalizes in fp64 and keeps h in fp64.  Each case
 prints its name and shape before touching the GPU.
 """
 import numpy as np
@@ -42,14 +43,13 @@ def _stack(q, cfg, L, seed=0, lora_scale=None, rank=True, first=0):
 
 
 def _residual(x_bits, y_bits):
-    """x + y of two binary16 arrays, rounded once to binary16 (nearest-even)."""
-    s = x_bits.view(np.float16).astype(np.float64) + y_bits.view(np.float16).astype(np.float64)
-    return s.astype(np.float16).view(np.uint16)
+    """x + y of two binary16 arrays, rounded once (the oracle's residual add)."""
+    return orc.residual_f16(x_bits, y_bits)
 
 
 def _check_chain(layers, y, x_bits, lora_scale=None, rank=True, tol=Y_TOL, x_out=None):
-    """Per-block parity: block l against the oracle on block l's input
-    x_l (x_0 = x, x_{l+1} = x_l + y_l from the GPU's y_l)."""
+    """Per-block parity: block l against the oracle on RMSNorm(x_l)
+    (x_0 = x, x_{l+1} = x_l + y_l from the GPU's y_l)."""
     cfg = layers[0].cfg
     ys = bits_of(y).reshape(len(layers), cfg.M, cfg.d)
     errs = []
@@ -58,7 +58,7 @@ def _check_chain(layers, y, x_bits, lora_scale=None, rank=True, tol=Y_TOL, x_out
         qg, qu, qd = oracle_q(lay)
         ls = cfg.lora_scale if lora_scale is None else lora_scale
         lo = (lay.A_gate, lay.B_gate, lay.A_up, lay.B_up) if rank else (None,) * 4
-        ref = orc.forward(qg, qu, qd, *lo, prev, lora_scale=ls, bf16=False)
+        ref = orc.forward(qg, qu, qd, *lo, orc.rmsnorm_f16(prev), lora_scale=ls, bf16=False)
         err = orc.max_rel_err(orc.act_to_f64(yb, False), ref)
         errs.append(err)
         assert err <= tol, (len(errs) - 1, err)
@@ -117,7 +117,7 @@ def test_stack_deterministic_across_calls_and_matches_per_layer_path(q):
     wsl = q.workspace(mlps[0], 1)
     prev = bits_of(x)
     for i, m in enumerate(mlps):
-        yl = q.forward(m, act_tensor(prev), ws=wsl)
+        yl = q.forward(m, act_tensor(orc.rmsnorm_f16(prev)), ws=wsl)
         ref = values_of(outs[0][i])
         assert orc.max_rel_err(values_of(yl), ref) <= Y_TOL
         prev = _residual(prev, bits_of(outs[0][i]))
@@ -208,7 +208,7 @@ def test_stack_fallback_shapes_chain_per_layer(q):
     small = wl.Config("stack_m4", M=4, d=512, f=1536, g=64, r=8, L=3)
     _announce("stack fallback", small.name)
     layers, mlps, st = _stack(q, small, 3)
-    assert q.stack_launches(st, 4) == 3 * q.forward_launches(mlps[0], 4) + 2
+    assert q.stack_launches(st, 4) == 3 * (q.forward_launches(mlps[0], 4) + 2) - 1
     x = act_tensor(layers[0].x)
     xo = torch.empty_like(x)
     y = q.forward_stack(st, x, x_out=xo)
@@ -219,8 +219,9 @@ def test_stack_fallback_shapes_chain_per_layer(q):
 
 def test_stack_qwen3_4b_full_depth_sampled(q):
     """The benchmark's 36-layer Qwen3-4B stack in its launch configuration
-    (one persistent launch); layers 0, 17 and 35 against the oracle on their
-    residual-stream inputs, and the final stream x_36 recomputed bit for bit."""
+    (one persistent launch); layers 0, 17 and 35 against the oracle on the
+    norm of their stream state, and the final stream x_36 recomputed bit for
+    bit from the GPU outputs."""
     cfg = wl.CONFIGS["qwen3_4b"]
     _announce("stack full depth", cfg.name, "L", cfg.L)
     layers = [wl.layer(cfg, i, 0) for i in range(cfg.L)]
@@ -239,8 +240,8 @@ def test_stack_qwen3_4b_full_depth_sampled(q):
         if i in (0, 17, 35):
             qg, qu, qd = oracle_q(layers[i])
             lay = layers[i]
-            ref = orc.forward(qg, qu, qd, lay.A_gate, lay.B_gate, lay.A_up, lay.B_up, prev,
-                              lora_scale=cfg.lora_scale, bf16=False)
+            ref = orc.forward(qg, qu, qd, lay.A_gate, lay.B_gate, lay.A_up, lay.B_up,
+                              orc.rmsnorm_f16(prev), lora_scale=cfg.lora_scale, bf16=False)
             err = orc.max_rel_err(orc.act_to_f64(ys[i], False), ref)
             print("layer", i, "max-rel err %.2e" % err)
             assert err <= Y_TOL

@@ -30,6 +30,12 @@ MUTANTS = {
                           "double s = orc_f16_to_f64(scale[row * ng + i / (2 * g)]);"),
     "scale_via_binary32": ("uint16_t s16 = orc_f64_to_f16(s);",
                            "uint16_t s16 = orc_f64_to_f16((double)(float)s);"),
+    "rmsnorm_sum_not_mean": ("double inv = 1.0 / sqrt(ss / (double)d + eps);",
+                             "double inv = 1.0 / sqrt(ss + eps);"),
+    "rmsnorm_eps_outside_root": ("double inv = 1.0 / sqrt(ss / (double)d + eps);",
+                                 "double inv = 1.0 / (sqrt(ss / (double)d) + eps);"),
+    "residual_sign": ("out[i] = orc_f64_to_f16(orc_f16_to_f64(x[i]) + orc_f16_to_f64(y[i]));",
+                      "out[i] = orc_f64_to_f16(orc_f16_to_f64(x[i]) - orc_f16_to_f64(y[i]));"),
 }
 
 

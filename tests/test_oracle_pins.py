@@ -319,3 +319,61 @@ def test_rows_are_independent_tokens():
     for m in range(4):
         ym = orc.forward(qg, qu, qd, L.A_gate, L.B_gate, L.A_up, L.B_up, L.x[m:m + 1])
         assert np.array_equal(ym[0], y[m])
+
+
+# ---------------------------------------------------------------- stack context
+def _f16(a):
+    return np.asarray(a, np.float16).view(np.uint16)
+
+
+def test_residual_matches_numpy_exact_sum():
+    """x + y rounded once: numpy's float64 sum of two binary16 values is
+    exact, and its float64 -> float16 cast rounds once to nearest-even."""
+    rng = np.random.default_rng(7)
+    x = _f16(rng.standard_normal(4096) * np.exp2(rng.integers(-20, 8, 4096)))
+    y = _f16(rng.standard_normal(4096) * np.exp2(rng.integers(-20, 8, 4096)))
+    # ties: y at half a binary16 step of x = 1 (1 + 2^-11 rounds to even 1.0)
+    x[:4] = _f16([1.0, 1.0, 2048.0, -1.0])
+    y[:4] = _f16([2.0 ** -11, 3 * 2.0 ** -11, 1.0, -(2.0 ** -11)])
+    got = orc.residual_f16(x, y)
+    ref = (x.view(np.float16).astype(np.float64) + y.view(np.float16).astype(np.float64)
+           ).astype(np.float16).view(np.uint16)
+    assert np.array_equal(got, ref)
+    assert list(got[:4].view(np.float16)) == [1.0, 1.0 + 2.0 ** -9, 2048.0, -1.0]
+
+
+def test_rmsnorm_closed_forms():
+    d = 64
+    # a constant row c: mean of squares c^2, so u = c / sqrt(c^2 + eps) -> +-1
+    for c in (1.0, 2.0, -3.5, 0.125):
+        u = orc.rmsnorm_f16(_f16(np.full((1, d), c)), eps=0.0)
+        assert np.all(u.view(np.float16) == np.sign(c))
+    # one nonzero entry a: mean of squares a^2/d, so u = sqrt(d) sign(a) there, 0 elsewhere
+    x = np.zeros((1, d))
+    x[0, 5] = -0.75
+    u = orc.rmsnorm_f16(_f16(x), eps=0.0).view(np.float16)
+    assert u[0, 5] == -8.0 and np.count_nonzero(u) == 1
+    # eps enters under the square root: a zero row stays zero, a row of
+    # sqrt(eps) values maps to 1/sqrt(2)
+    assert np.all(orc.rmsnorm_f16(_f16(np.zeros((1, d)))) == 0)
+    e = 2.0 ** -8
+    u = orc.rmsnorm_f16(_f16(np.full((1, d), e)), eps=e * e).view(np.float16)
+    assert np.all(u == np.float16(1 / np.sqrt(2.0)))
+
+
+def test_rmsnorm_scale_invariant_and_unit_rms():
+    rng = np.random.default_rng(11)
+    x = _f16(rng.standard_normal((3, 2560)))
+    u = orc.rmsnorm_f16(x, eps=0.0)
+    x2 = _f16(x.view(np.float16).astype(np.float64) * 4.0)      # exact scaling
+    assert np.array_equal(orc.rmsnorm_f16(x2, eps=0.0), u)
+    rms = np.sqrt(np.mean(u.view(np.float16).astype(np.float64) ** 2, axis=1))
+    assert np.all(np.abs(rms - 1.0) < 1e-3)
+
+
+def test_rmsnorm_matches_numpy_per_row():
+    rng = np.random.default_rng(12)
+    x = _f16(rng.standard_normal((4, 512)) * 3.0)
+    v = x.view(np.float16).astype(np.float64)
+    ref = (v / np.sqrt(np.mean(v * v, axis=1, keepdims=True) + orc.RMS_EPS)).astype(np.float16)
+    assert np.array_equal(orc.rmsnorm_f16(x), ref.view(np.uint16))
