@@ -317,7 +317,7 @@ def stack_errors(stack: Stack, ws: torch.Tensor, M: int = 1, dtype=torch.float16
 def _stack_area_bytes(stack: Stack) -> int:
     m = stack.mlps[0]
     d, f, r = m.d, m.f, m.rank
-    xw = d + 2 * (2 * r + 1) * 32
+    xw = d + d // 4 + 2 * (2 * r + 1) * 32
     rnd = lambda v: (v + 255) // 256 * 256  # noqa: E731
     return 1024 + rnd(8 * xw * 4) + rnd(f * 4) + 2 * 8 * d * 8
 

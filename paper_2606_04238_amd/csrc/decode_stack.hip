@@ -107,13 +107,13 @@ struct StackArgs {
     const uint16_t* x0;          // [d] input of the first layer
     uint16_t* y;                 // [L][d] output of every layer
     uint16_t* xl;                // [d] the residual stream after the last layer (may be null)
-    uint32_t* xb;                // [8][xw] XCD-local: d x words, then [2r+1][32] 64-bit shares
-                                 // (LoRA-A ranks, then the sum of squares)
+    uint32_t* xb;                // [8][xw] XCD-local, 64-bit tagged words: x' pairs [d/2], per-word
+                                 // sums [d/8], shares [2r+1][32] (LoRA-A ranks, sum of squares)
     uint32_t* hb;                // [f] XCD-local h words (XCD x owns [x f/8, (x+1) f/8))
     unsigned long long* pb;      // [2][8][d] cross-XCD partial down sums
     unsigned* ctl;
     int xw;                      // 32-bit words per XCD in xb
-    int o_xs, o_cx, o_t, o_hs, o_hcx, o_a, o_y, o_xr, o_xn, o_bc, o_meta, meta_bytes;   // LDS byte offsets
+    int o_xs, o_cx, o_t, o_hs, o_hcx, o_a, o_y, o_xn, o_meta, meta_bytes;   // LDS byte offsets
 };
 
 namespace {
@@ -143,46 +143,6 @@ __device__ __forceinline__ bool sk_poll(__amdgpu_buffer_rsrc_t rs, const int (&o
             __builtin_amdgcn_s_sleep(1);
     }
     return pending == 0u;
-}
-
-// One staging word of the activation: 16 binary16 values x[16w .. 16w+16)
-// (low halves of four tagged 16-byte words), normalized (times inv, rounded
-// to binary16: the block's input u) and pre-scaled per fraction position
-// into the x' layout of the gate/up units: chunk-major, xs[c * XS + ul] for
-// chunk c (0..7) of 64-code unit ul = w / 4, so the 8 lanes of a row read 8
-// consecutive 16-byte entries (no bank conflict) at one base address plus
-// immediates; and per unit (1024 sum x', sum x).  Every lane of the wave
-// calls it (quad reductions); lanes with valid == false store nothing.
-template <int XS>
-__device__ __forceinline__ void sk_stage_x(uint4* xs, float2* cx, const u32x4* v, bool valid, int w,
-                                           float inv) {
-    uint32_t xv[16];                     // the block input u = x * inv, binary16
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        xv[4 * q + 0] = valid ? f2h(h2f(v[q].x & 0xFFFFu) * inv) : 0u;
-        xv[4 * q + 1] = valid ? f2h(h2f(v[q].y & 0xFFFFu) * inv) : 0u;
-        xv[4 * q + 2] = valid ? f2h(h2f(v[q].z & 0xFFFFu) * inv) : 0u;
-        xv[4 * q + 3] = valid ? f2h(h2f(v[q].w & 0xFFFFu) * inv) : 0u;
-    }
-    uint32_t pr[8];
-    float csum = 0.0f, xsum = 0.0f;
-#pragma unroll
-    for (int p = 0; p < 8; ++p) {
-        const float sc = w2_pair_scale(p);
-        const uint32_t ha = f2h(h2f(xv[p]) * sc), hb = f2h(h2f(xv[8 + p]) * sc);
-        pr[p] = ha | (hb << 16);
-        csum += h2f(ha) + h2f(hb);
-        xsum += h2f(xv[p]) + h2f(xv[8 + p]);
-    }
-    csum = group_sum<4>(csum);
-    xsum = group_sum<4>(xsum);
-    if (valid) {
-        const int ul = w >> 2, wi = w & 3;
-        xs[(2 * wi) * XS + ul] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
-        xs[(2 * wi + 1) * XS + ul] = make_uint4(pr[4], pr[5], pr[6], pr[7]);
-        if (wi == 0)
-            cx[ul] = make_float2(1024.0f * csum, xsum);
-    }
 }
 
 // One staging word of h: 8 binary16 values h[8w .. 8w+8) of this XCD's
@@ -318,12 +278,14 @@ __device__ __forceinline__ void sk_gu_accumulate(FGuItem<1, 8, JG, KM>& it, cons
     }
 }
 
-// LoRA-B on the lane's ranks, the row reduction over 8 lanes and
-// h = SiLU(G) * U, published as tagged words to the XCD-local h buffer.
+// LoRA-B on the lane's ranks (t unscaled: A x), the row reduction over 8
+// lanes, the norm's 1/rms (G and U are linear in the block input x * inv)
+// and h = SiLU(G) * U, published as tagged words to the XCD-local h buffer.
 template <int JG, int KM>
 __device__ __forceinline__ void sk_gu_finish(FGuItem<1, 8, JG, KM>& it, const float* ts, int r,
                                              float ls, uint32_t* hb, uint32_t tag, int lane) {
     const int s = lane & 7;
+    const float inv = ts[2 * r];           // 1 / rms of the stream: the block input is x * inv
     float G = it.G[0], U = it.U[0];
     if (r > 0) {
         const int CPL = r / 8;
@@ -342,8 +304,9 @@ __device__ __forceinline__ void sk_gu_finish(FGuItem<1, 8, JG, KM>& it, const fl
         G += ls * lg;
         U += ls * lu;
     }
-    G = group_sum<8>(G);
-    U = group_sum<8>(U);
+    // everything above is linear in the input: scale by 1/rms once per row
+    G = group_sum<8>(G) * inv;
+    U = group_sum<8>(U) * inv;
     if (it.ok && s == 0) {
         const float hv = G / (1.0f + __expf(-G)) * U;
         st_intra32(hb + it.row, f2h(hv) | (tag << 16));
@@ -437,39 +400,76 @@ __device__ __forceinline__ void sk_a_store(const uint4 (&av)[KA], uint4* as, int
     }
 }
 
-// Polling wave 0: block j's rows D_j of the next layer's stream (binary16
-// pairs in xn), its shares of that layer's LoRA-A product (unnormalized)
-// and of sum x^2 go to the XCD-local activation buffer; lanes l < DJ/2 hold
-// rows 2l, 2l+1.
+// Polling wave 0: block j's rows D_j of the next layer's stream x (binary16
+// pairs (2l, 2l+1) in xn, LDS) go to the XCD-local activation buffer already
+// in the gate/up x' layout, so consumers only move words into LDS:
+//   * staging word w (16 values) holds pairs p = 0..7 of (x[16w+p],
+//     x[16w+8+p]), each half pre-scaled by its fraction position, as
+//     64-bit words pair | tag << 32 at [8w + p];
+//   * its sums (1024 sum x', sum x) as two tagged 64-bit words at
+//     [d/2 + 2w], [d/2 + 2w + 1];
+//   * block j's shares of A x (per rank, unnormalized) and of sum x^2 at
+//     [d/2 + d/8 + k 32 + j] (k = 2r: the sum of squares).
+// Lane l < DJ/2 covers staging word l / 8 of D_j, pair l % 8.
 __device__ __forceinline__ void sk_publish_x(uint32_t* xb, const uint32_t* xn, const uint16_t* as,
                                              int d, int r, int DJ, int j, uint32_t tag, int lane) {
-    if (lane < DJ / 2) {
-        const uint32_t v = xn[lane];
-        const unsigned long long wv = (unsigned long long)((v & 0xFFFFu) | (tag << 16)) |
-                                      ((unsigned long long)((v >> 16) | (tag << 16)) << 32);
-        st_intra64(reinterpret_cast<unsigned long long*>(xb + j * DJ) + lane, wv);
+    unsigned long long* x64 = reinterpret_cast<unsigned long long*>(xb);
+    const unsigned long long tg = (unsigned long long)tag << 32;
+    const uint16_t* xh = reinterpret_cast<const uint16_t*>(xn);
+    const bool live = lane < DJ / 2;
+    const int wl = lane >> 3, p = lane & 7;
+    const uint32_t a = live ? xh[16 * wl + p] : 0u, b = live ? xh[16 * wl + 8 + p] : 0u;
+    const float sc = w2_pair_scale(p);
+    const uint32_t ha = f2h(h2f(a) * sc), hb = f2h(h2f(b) * sc);
+    const int gw = j * (DJ / 16) + wl;
+    if (live)
+        st_intra64(x64 + 8 * gw + p, (unsigned long long)(ha | (hb << 16)) | tg);
+    const float cs = group_sum<8>(h2f(ha) + h2f(hb));
+    const float xs = group_sum<8>(h2f(a) + h2f(b));
+    if (live && p == 0) {
+        st_intra64(x64 + d / 2 + 2 * gw, (unsigned long long)__float_as_uint(1024.0f * cs) | tg);
+        st_intra64(x64 + d / 2 + 2 * gw + 1, (unsigned long long)__float_as_uint(xs) | tg);
     }
-    unsigned long long* t64 = reinterpret_cast<unsigned long long*>(xb + d);
-    if (lane < 2 * r) {
-        const uint32_t* a32 = reinterpret_cast<const uint32_t*>(as) + lane * (DJ / 2);
+    unsigned long long* sh = x64 + d / 2 + d / 8;
+    // shares of A x: lanes in groups of 64 / 2r per rank, each over a
+    // contiguous run of pairs read 16 bytes at a time
+    if (r > 0) {
+        const int lpr = 64 / (2 * r), k = lane / lpr, sub = lane - k * lpr;
+        const int ppl = DJ / 2 / lpr;                          // pairs per lane
+        const uint32_t* a32 = reinterpret_cast<const uint32_t*>(as) + k * (DJ / 2) + sub * ppl;
+        const uint32_t* x32 = xn + sub * ppl;
         float acc = 0.0f;
-        for (int c = 0; c < DJ / 2; ++c)
-            acc = dot2(a32[c], xn[c], acc);
-        st_intra64(t64 + lane * SB + j, (unsigned long long)__float_as_uint(acc) |
-                                            ((unsigned long long)tag << 32));
+        if ((ppl & 3) == 0) {
+#pragma unroll 4
+            for (int c = 0; c < ppl; c += 4) {
+                const uint4 av = *reinterpret_cast<const uint4*>(a32 + c);
+                const uint4 xv = *reinterpret_cast<const uint4*>(x32 + c);
+                acc = dot2(av.x, xv.x, acc);
+                acc = dot2(av.y, xv.y, acc);
+                acc = dot2(av.z, xv.z, acc);
+                acc = dot2(av.w, xv.w, acc);
+            }
+        } else {
+            for (int c = 0; c < ppl; ++c)
+                acc = dot2(a32[c], x32[c], acc);
+        }
+        if (lpr >= 2) acc += dpp<DPP_QUAD_XOR1>(acc);
+        if (lpr >= 4) acc += dpp<DPP_QUAD_XOR2>(acc);
+        if (sub == 0)
+            st_intra64(sh + k * SB + j, (unsigned long long)__float_as_uint(acc) | tg);
     }
-    // the share of sum x^2 (for the next block's norm), reduced over the wave
+    // the share of sum x^2 (for the next block's norm)
     float ss = 0.0f;
-    if (lane < DJ / 2) {
+    if (live) {
         const uint32_t v = xn[lane];
-        const float a = h2f(v & 0xFFFFu), b = h2f(v >> 16);
-        ss = a * a + b * b;
+        const float u0 = h2f(v & 0xFFFFu), u1 = h2f(v >> 16);
+        ss = u0 * u0 + u1 * u1;
     }
     ss = group_sum<64>(ss);
     if (lane == 0)
-        st_intra64(t64 + 2 * r * SB + j, (unsigned long long)__float_as_uint(ss) |
-                                             ((unsigned long long)tag << 32));
+        st_intra64(sh + 2 * r * SB + j, (unsigned long long)__float_as_uint(ss) | tg);
 }
+
 
 typedef const StackArgs __attribute__((address_space(4))) KArgs;
 
@@ -487,14 +487,12 @@ __device__ __forceinline__ StackLayer sk_layer(KArgs* ka, int i) {
 struct SkLds {
     uint4* xs;          // x' of the activation (gate/up units)
     float2* cxg;        // per unit (1024 sum x', sum x)
-    float* ts;          // t = [A_g; A_u] x, fp32 [2r]
+    float* ts;          // [A_g; A_u] x (unnormalized), fp32 [2r], then 1 / rms
     uint4* hs;          // h' of this XCD's slice (down units)
     float2* hcx;        // per unit (1024 sum h', sum h)
     uint4* as;          // next layer's LoRA-A columns D_j, binary16 [2r][DJ]
     uint32_t* ys;       // y[D_j] binary16 pairs
-    uint16_t* xr;       // x[D_j] of the current layer (the residual)
-    uint32_t* xn;       // x[D_j] of the next layer, binary16 pairs
-    unsigned long long* bc;   // 1 / rms of the current input | tag << 32
+    uint32_t* xn;       // the stream x[D_j], binary16 pairs (current, then next layer)
     char* meta;         // per-wave gate/up metadata areas
 };
 
@@ -579,8 +577,9 @@ __device__ __forceinline__ void sk_compute_role(const StackArgs& sa, KArgs* ka, 
     }
 }
 
-// The polling waves: stage the activation and t, then h, then sum the
-// cross-XCD partials and publish y and the next layer's LoRA-A shares.
+// The polling waves: move the activation (published in the x' layout) and
+// the shares into LDS, stage h, then sum the cross-XCD partials, add the
+// residual and publish the next layer's stream rows and shares.
 // Offsets of the polled words are affine in the lane (one base register);
 // which of them exist is a bit mask.
 template <int XS, int HS>
@@ -597,26 +596,25 @@ __device__ __forceinline__ void sk_poll_role(const StackArgs& sa, const SkLds& m
     bool dead = false;                                          // this wave gave up a wait
     if (wave == SCW && lane < DJ / 2)
         m.xn[lane] = reinterpret_cast<const uint32_t*>(sa.x0 + j * DJ)[lane];
-    if (wave == SCW && lane == 0)
-        *m.bc = 0;                                              // no tag
     __syncthreads();                                            // B0
     if (wave == SCW)
         sk_publish_x(xb, m.xn, reinterpret_cast<const uint16_t*>(m.as), d, r, DJ, j, stag(pl.seq0), lane);
 
-    // activation words: staging word w = pt + SPT kk covers x[16w, 16w+16)
-    // (four 16-byte words of tagged values); LoRA-A shares of rank pt (< 2r):
-    // 32 64-bit words after the d activation words
-    int xoff[4 * KXW + 16];
+    // activation: staging word w = pt + SPT kk in the x' layout (four 16-byte
+    // words of tagged pairs and one of tagged sums); shares of rank pt <= 2r
+    // (2r: the sum of squares), 32 64-bit words
+    int xoff[5 * KXW + 16];
     uint32_t xvalid = 0;
 #pragma unroll
     for (int kk = 0; kk < KXW; ++kk) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) xoff[4 * kk + q] = 64 * pt + 64 * SPT * kk + 16 * q;
-        if (pt + SPT * kk < d / 16) xvalid |= 0xFu << (4 * kk);
+        for (int q = 0; q < 4; ++q) xoff[5 * kk + q] = 64 * (pt + SPT * kk) + 16 * q;
+        xoff[5 * kk + 4] = 4 * d + 16 * (pt + SPT * kk);
+        if (pt + SPT * kk < d / 16) xvalid |= 0x1Fu << (5 * kk);
     }
 #pragma unroll
-    for (int q = 0; q < 16; ++q) xoff[4 * KXW + q] = d * 4 + pt * SB * 8 + 16 * q;
-    if (pt <= 2 * r) xvalid |= 0xFFFFu << (4 * KXW);           // rank pt, or the sum of squares
+    for (int q = 0; q < 16; ++q) xoff[5 * KXW + q] = (d / 2 + d / 8 + pt * SB) * 8 + 16 * q;
+    if (pt <= 2 * r) xvalid |= 0xFFFFu << (5 * KXW);
     // h words of this XCD's slice: staging word w = pt + SPT kk covers h[8w, 8w+8)
     int hoff[2 * KHW];
     uint32_t hvalid = 0;
@@ -629,49 +627,33 @@ __device__ __forceinline__ void sk_poll_role(const StackArgs& sa, const SkLds& m
 
     for (int i = 0; i < L; ++i) {
         const uint32_t tx = stag(pl.seq0 + i), ti = stag(pl.seq0 + 1 + i);
-        {   // the activation and the LoRA-A shares of this XCD
-            u32x4 v[4 * KXW + 16];
-            dead |= !sk_poll<4 * KXW + 16, 4 * KXW, POL_INTRA>(xrs, xoff, xvalid, v, tx, dead);
-            // shares in block order; thread 2r holds sum x^2 and hands
-            // 1 / rms to both polling waves through a tagged LDS word
-            float share = 0.0f;
-            if (pt <= 2 * r) {
-#pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    share += __uint_as_float(v[4 * KXW + q].x);
-                    share += __uint_as_float(v[4 * KXW + q].z);
-                }
-            }
-            if (pt == 2 * r) {
-                const float inv0 = 1.0f / __fsqrt_rn(share / (float)d + kRmsEps);
-                __hip_atomic_store(m.bc, (unsigned long long)__float_as_uint(inv0) |
-                                             ((unsigned long long)tx << 32),
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            }
-            unsigned long long bv = 0;
-            for (unsigned it = 0; it < kStackSpin; ++it) {
-                bv = __hip_atomic_load(m.bc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-                if ((uint32_t)(bv >> 32) == tx)
-                    break;
-                __builtin_amdgcn_s_sleep(1);
-            }
-            const float inv = __uint_as_float((uint32_t)bv);
+        {   // the activation (already in the x' layout) and the shares of this XCD
+            u32x4 v[5 * KXW + 16];
+            dead |= !sk_poll<5 * KXW + 16, 0, POL_INTRA>(xrs, xoff, xvalid, v, tx, dead);
 #pragma unroll
             for (int kk = 0; kk < KXW; ++kk) {
                 const int w = pt + SPT * kk;
-                sk_stage_x<XS>(m.xs, m.cxg, v + 4 * kk, w < d / 16, w, inv);
-                const int wr = w - j * (DJ / 16);             // this block's residual rows D_j
-                if (wr >= 0 && wr < DJ / 16) {
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const u32x4 t = v[4 * kk + q];
-                        reinterpret_cast<uint32_t*>(m.xr)[8 * wr + 2 * q] = (t.x & 0xFFFFu) | (t.y << 16);
-                        reinterpret_cast<uint32_t*>(m.xr)[8 * wr + 2 * q + 1] = (t.z & 0xFFFFu) | (t.w << 16);
-                    }
+                const bool valid = w < d / 16;
+                const u32x4* vw = v + 5 * kk;
+                const float cs = group_sum<4>(valid ? __uint_as_float(vw[4].x) : 0.0f);
+                const float xs = group_sum<4>(valid ? __uint_as_float(vw[4].z) : 0.0f);
+                if (valid) {
+                    const int ul = w >> 2, wi = w & 3;
+                    m.xs[(2 * wi) * XS + ul] = make_uint4(vw[0].x, vw[0].z, vw[1].x, vw[1].z);
+                    m.xs[(2 * wi + 1) * XS + ul] = make_uint4(vw[2].x, vw[2].z, vw[3].x, vw[3].z);
+                    if (wi == 0)
+                        m.cxg[ul] = make_float2(cs, xs);
                 }
             }
-            if (pt < 2 * r)
-                m.ts[pt] = share * inv;                        // A u = (A x) / rms
+            if (pt <= 2 * r) {   // shares in block order; thread 2r: 1 / rms
+                float share = 0.0f;
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    share += __uint_as_float(v[5 * KXW + q].x);
+                    share += __uint_as_float(v[5 * KXW + q].z);
+                }
+                m.ts[pt] = pt < 2 * r ? share : 1.0f / __fsqrt_rn(share / (float)d + kRmsEps);
+            }
             dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
             if (dead && lane == 0)
                 atomicOr(&ctl[C_ERR], 1u);
@@ -714,7 +696,7 @@ __device__ __forceinline__ void sk_poll_role(const StackArgs& sa, const SkLds& m
         if (wave == SCW) {
             if (lane < DJ / 2) {
                 // x_{l+1} = x_l + y_l: two binary16 values summed exactly in fp32, rounded once
-                const uint32_t yv = m.ys[lane], xv = reinterpret_cast<const uint32_t*>(m.xr)[lane];
+                const uint32_t yv = m.ys[lane], xv = m.xn[lane];
                 const uint32_t nv = f2h(h2f(xv & 0xFFFFu) + h2f(yv & 0xFFFFu)) |
                                     (f2h(h2f(xv >> 16) + h2f(yv >> 16)) << 16);
                 m.xn[lane] = nv;
@@ -754,9 +736,8 @@ __global__ void __launch_bounds__(STHREADS) stack_kernel(StackArgs sa) {
         const SkLds m{reinterpret_cast<uint4*>(lds + sa.o_xs), reinterpret_cast<float2*>(lds + sa.o_cx),
                       reinterpret_cast<float*>(lds + sa.o_t), reinterpret_cast<uint4*>(lds + sa.o_hs),
                       reinterpret_cast<float2*>(lds + sa.o_hcx), reinterpret_cast<uint4*>(lds + sa.o_a),
-                      reinterpret_cast<uint32_t*>(lds + sa.o_y), reinterpret_cast<uint16_t*>(lds + sa.o_xr),
-                      reinterpret_cast<uint32_t*>(lds + sa.o_xn),
-                      reinterpret_cast<unsigned long long*>(lds + sa.o_bc), lds + sa.o_meta};
+                      reinterpret_cast<uint32_t*>(lds + sa.o_y), reinterpret_cast<uint32_t*>(lds + sa.o_xn),
+                      lds + sa.o_meta};
         const SkPlace pl{(int)xcc, j, seq0};
         if (wave < SCW)
             sk_compute_role<JG, KM, JD, NDN>(sa, (KArgs*)__builtin_amdgcn_kernarg_segment_ptr(), m, pl, wave, lane);
@@ -834,7 +815,7 @@ int stack_cu_count() {
 
 struct StackPlan {
     int jg, km, jd, ndn;
-    int o_xs, o_cx, o_t, o_hs, o_hcx, o_a, o_y, o_xr, o_xn, o_bc, o_meta, meta_bytes;
+    int o_xs, o_cx, o_t, o_hs, o_hcx, o_a, o_y, o_xn, o_meta, meta_bytes;
     size_t lds;
     bool ok;
 };
@@ -872,14 +853,12 @@ StackPlan plan_stack(int M, int d, int f, int g, int r) {
     auto take = [&](size_t bytes) { const size_t at = o; o = (o + bytes + 15) / 16 * 16; return (int)at; };
     p.o_xs = take((size_t)UG * 8 * 16);
     p.o_cx = take((size_t)UG * 8);
-    p.o_t = take((size_t)2 * r * 4 + 4);
+    p.o_t = take((size_t)(2 * r + 1) * 4);
     p.o_hs = take((size_t)p.jd * 8 * 4 * 16);     // chunk stride 8 JD >= UF units
     p.o_hcx = take((size_t)p.jd * 8 * 8);
     p.o_a = take((size_t)2 * r * DJ * 2 + 16);
     p.o_y = take((size_t)DJ * 2);
-    p.o_xr = take((size_t)DJ * 2);
     p.o_xn = take((size_t)DJ * 2);
-    p.o_bc = take(8);
     p.meta_bytes = 2 * 8 * ng * 4;
     p.o_meta = take((size_t)SCW * p.meta_bytes);
     p.lds = o;
@@ -892,7 +871,7 @@ StackPlan plan_stack(int M, int d, int f, int g, int r) {
 bool stack_supported(int M, int d, int f, int g, int r) { return plan_stack(M, d, f, g, r).ok; }
 
 size_t stack_ws_bytes(int d, int f, int r) {
-    const size_t xw = (size_t)d + 2 * (2 * (size_t)r + 1) * SB;
+    const size_t xw = (size_t)d + d / 4 + 2 * (2 * (size_t)r + 1) * SB;
     return 1024 + ((SX * xw * 4 + 255) & ~(size_t)255) + (((size_t)f * 4 + 255) & ~(size_t)255) +
            (size_t)2 * SX * d * 8;
 }
@@ -934,14 +913,14 @@ hipError_t launch_stack(const StackLayerDesc* layers, int L, int d, int f, int g
     a.xl = x_last;
     char* base = static_cast<char*>(ws);
     a.ctl = reinterpret_cast<unsigned*>(base);
-    const size_t xw = (size_t)d + 2 * (2 * (size_t)r + 1) * SB;
+    const size_t xw = (size_t)d + d / 4 + 2 * (2 * (size_t)r + 1) * SB;
     a.xw = (int)xw;
     a.xb = reinterpret_cast<uint32_t*>(base + 1024);
     const size_t xbytes = (SX * xw * 4 + 255) & ~(size_t)255;
     a.hb = reinterpret_cast<uint32_t*>(base + 1024 + xbytes);
     a.pb = reinterpret_cast<unsigned long long*>(base + 1024 + xbytes + (((size_t)f * 4 + 255) & ~(size_t)255));
     a.o_xs = p.o_xs; a.o_cx = p.o_cx; a.o_t = p.o_t; a.o_hs = p.o_hs; a.o_hcx = p.o_hcx;
-    a.o_a = p.o_a; a.o_y = p.o_y; a.o_xr = p.o_xr; a.o_xn = p.o_xn; a.o_bc = p.o_bc; a.o_meta = p.o_meta; a.meta_bytes = p.meta_bytes;
+    a.o_a = p.o_a; a.o_y = p.o_y; a.o_xn = p.o_xn; a.o_meta = p.o_meta; a.meta_bytes = p.meta_bytes;
     auto run = [&](auto kernel) -> hipError_t {
         kernel<<<SGRID, STHREADS, p.lds, st>>>(a);
         return hipGetLastError();
