@@ -66,6 +66,12 @@ constexpr int KA = 3;                     // LoRA-A slice loads per compute thre
 constexpr int KXW = 2;                    // activation staging words per polling thread (max)
 constexpr int KHW = 2;                    // h staging words per polling thread (max)
 constexpr float kRmsEps = 1e-6f;          // RMSNorm epsilon
+// Where the next layer's gate/up codes are requested: 0 right after this
+// layer's gate/up arithmetic, 1 after the down arithmetic (with the down
+// codes), 2 after the last barrier of the layer.  A burst of requests delays
+// the hand-off polls issued behind it on the same compute unit, so the
+// choice decides which hand-off overlaps the gate/up half of the stream.
+constexpr int kGuPrefetchAt = 0;
 
 // Control words (uint32 index into the stack's control block).
 constexpr int C_SEQ = 0, C_DONE = 32, C_ERR = 64, C_XC = 96;
@@ -547,7 +553,7 @@ __device__ __forceinline__ void sk_compute_role(const StackArgs& sa, KArgs* ka, 
         if (i + 1 < L) {
             const StackLayer wn = sk_layer(ka, i + 1);
             sk_a_load(av, wn, r, d, DJ, j, ct);
-            if (has_gu)
+            if (has_gu && kGuPrefetchAt == 0)
                 sk_gu_load(gi, wn, row_begin + 8 * wave, row_end, f, d, g, r, lane);
         }
         __syncthreads();                                        // B2: h' staged
@@ -572,8 +578,12 @@ __device__ __forceinline__ void sk_compute_role(const StackArgs& sa, KArgs* ka, 
                 if (item < dn_items)
                     sk_dn_load(di[k], wn, j * DJ + 8 * item + (lane >> 3), xcc, f, g, lane);
             }
+            if (has_gu && kGuPrefetchAt == 1)
+                sk_gu_load(gi, wn, row_begin + 8 * wave, row_end, f, d, g, r, lane);
         }
         __syncthreads();                                        // B3: y[D_j], next A in LDS
+        if (i + 1 < L && has_gu && kGuPrefetchAt == 2)
+            sk_gu_load(gi, sk_layer(ka, i + 1), row_begin + 8 * wave, row_end, f, d, g, r, lane);
     }
 }
 
