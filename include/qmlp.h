@@ -211,6 +211,40 @@ qmlp_status qmlp_forward_stack(const qmlp_mlp *layers, int L, const void *x, int
  * residual-add kernels; 0 if the call would be rejected.  Host-only. */
 int qmlp_stack_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
 
+/*
+ * L independent blocks of one shape (Sec. 3.3, 4.2, 5: the gated MLP of each
+ * layer of the modelled decoders, with separately seeded weights and
+ * inputs): y_l = block_l(x_l) for l = 0..L-1, each exactly the operation of
+ * qmlp_forward.  layers[0..L-1] are host descriptors (same d, f, group and
+ * rank); x [L][M][d] and y [L][M][d] are row-major in the activation type
+ * (block l at x + l*M*d, y + l*M*d).
+ *
+ * At M = 1 in binary16 for shapes with f % 256 == 0, d % 512 == 0,
+ * d <= 4096, (d/g) % 4 == 0 and the instances of the persistent stack on a
+ * GPU with 8 XCDs of 32 compute units, the blocks run as ONE persistent
+ * launch per 40 blocks, pipelined: the gate/up rows of block i, the down
+ * rows of block i-2 and the output sum of block i-3 run together, so the
+ * hand-offs inside a block overlap the weight stream of the next.  Every
+ * other shape and bfloat16 run qmlp_forward once per block.
+ *
+ * ws/ws_bytes: at least qmlp_layers_workspace_bytes(layers, L, M, dtype),
+ * zero before the first call, with the rules of qmlp_workspace_bytes.  On
+ * the persistent path it starts with a 1024-byte control block: word 0 the
+ * step counter, word 64 sticky error bits (1/2/4 = a wait for the LoRA-A
+ * products / h / the cross-XCD partials gave up, 8 = a workgroup found no
+ * place); results are then invalid.  Errors as for qmlp_forward.
+ */
+size_t qmlp_layers_workspace_bytes(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
+
+qmlp_status qmlp_forward_layers(const qmlp_mlp *layers, int L, const void *x, int M,
+                                qmlp_dtype dtype, void *y, void *ws, size_t ws_bytes,
+                                qmlp_stream stream);
+
+/* Launches qmlp_forward_layers makes: the number of persistent launches, or
+ * the per-block launches of qmlp_forward; 0 if the call would be rejected.
+ * Host-only. */
+int qmlp_layers_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
+
 /* ---------------------------------------------- inspection (not timed) */
 
 /*

@@ -11,6 +11,7 @@ Functions keep the names of the C entry points:
 * ``gateup_w2_lora``              -- h = SiLU(W2g x + s B_g A_g x) * (W2u x + s B_u A_u x)
 * ``down_w4``                     -- y = W4down h
 * ``forward``                     -- the whole block x -> y
+* ``forward_layers``              -- L independent blocks, y_l = block_l(x_l)
 * ``forward_stack``               -- L blocks on a residual stream, x_{l+1} = x_l + block_l(RMSNorm(x_l))
 * ``unpack`` / ``dequant``        -- inspection of a packed matrix (not timed)
 """
@@ -76,6 +77,9 @@ def _lib():
             "qmlp_stack_workspace_bytes": (Z, [pm, I, I, I]),
             "qmlp_forward_stack": (I, [pm, I, P, I, I, P, P, P, Z, P]),
             "qmlp_stack_launches": (I, [pm, I, I, I]),
+            "qmlp_layers_workspace_bytes": (Z, [pm, I, I, I]),
+            "qmlp_forward_layers": (I, [pm, I, P, I, I, P, P, Z, P]),
+            "qmlp_layers_launches": (I, [pm, I, I, I]),
             "qmlp_status_string": (ctypes.c_char_p, [I]),
         }
         for name, (res, args) in sig.items():
@@ -274,10 +278,9 @@ def dequant(w: QWeight) -> torch.Tensor:
     return out
 
 
-class Stack:
-    """L blocks of one shape on a residual stream (x_{l+1} = x_l + y_l,
-    y_l = block_l(RMSNorm(x_l))); holds the C descriptor array the stack
-    entry points take."""
+class Layers:
+    """L blocks of one shape; holds the C descriptor array that the
+    multi-block entry points take."""
 
     def __init__(self, mlps):
         self.mlps = list(mlps)
@@ -288,6 +291,50 @@ class Stack:
 
     def c(self):
         return self._arr
+
+
+class Stack(Layers):
+    """L blocks of one shape on a residual stream (x_{l+1} = x_l + y_l,
+    y_l = block_l(RMSNorm(x_l)))."""
+
+
+def layers_workspace_bytes(layers: Layers, M: int, dtype=torch.float16) -> int:
+    code = F16 if dtype == torch.float16 else BF16
+    return int(_lib().qmlp_layers_workspace_bytes(layers.c(), len(layers), M, code))
+
+
+def layers_launches(layers: Layers, M: int, dtype=torch.float16) -> int:
+    """Launches forward_layers makes (persistent launches, or one forward per block)."""
+    code = F16 if dtype == torch.float16 else BF16
+    return int(_lib().qmlp_layers_launches(layers.c(), len(layers), M, code))
+
+
+def layers_workspace(layers: Layers, M: int, dtype=torch.float16, device="cuda") -> torch.Tensor:
+    """A zeroed workspace for forward_layers."""
+    n = layers_workspace_bytes(layers, M, dtype)
+    return torch.zeros(max(n, 1024), dtype=torch.uint8, device=device)
+
+
+def layers_errors(ws: torch.Tensor) -> int:
+    """Sticky error bits of the persistent launch of forward_layers (syncs): 1/2/4 =
+    a wait for the LoRA-A products / h / the cross-XCD partials gave up, 8 = a
+    workgroup had no place."""
+    return int(ws[256:260].view(torch.int32).item())
+
+
+def forward_layers(layers: Layers, x: torch.Tensor, y: torch.Tensor | None = None,
+                   ws: torch.Tensor | None = None) -> torch.Tensor:
+    """y [L][M][d]: y_l = block_l(x_l) for x [L][M][d], every block on its own input."""
+    L, M, d = x.shape
+    if L != len(layers) or d != layers.mlps[0].d:
+        raise ValueError("x must be [L][M][d] for the L blocks")
+    if y is None:
+        y = torch.empty_like(x)
+    if ws is None:
+        ws = layers_workspace(layers, M, x.dtype, x.device)
+    _check(_lib().qmlp_forward_layers(layers.c(), L, _ptr(x), M, _dtype_code(x), _ptr(y), _ptr(ws),
+                                      ws.numel(), _stream()), "forward_layers")
+    return y
 
 
 def stack_workspace_bytes(stack: Stack, M: int, dtype=torch.float16) -> int:

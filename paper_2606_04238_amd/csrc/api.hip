@@ -228,14 +228,12 @@ qmlp_status check_inspect(const qmlp_qweight* w) {
     return check_qweight(w, w->bits);
 }
 
-// A stack of blocks of one shape: layer l+1's input is layer l's output.
-qmlp_status check_stack(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+// L independent blocks of one shape: block l maps x[l] to y[l].
+qmlp_status check_layers(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
     if (!layers)
         return QMLP_ERR_NULL;
     if (L <= 0)
         return QMLP_ERR_SHAPE;
-    if (dtype != QMLP_F16)                        // the stream and the norm are binary16
-        return QMLP_ERR_UNSUPPORTED;
     for (int i = 0; i < L; ++i) {
         qmlp_status s = check_mlp(&layers[i], M, dtype);
         if (s != QMLP_OK)
@@ -247,6 +245,14 @@ qmlp_status check_stack(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) 
             return QMLP_ERR_SHAPE;
     }
     return QMLP_OK;
+}
+
+// A stack of blocks of one shape: layer l+1's input is layer l's output.
+qmlp_status check_stack(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    const qmlp_status s = check_layers(layers, L, M, dtype);
+    if (s != QMLP_OK)
+        return s;
+    return dtype == QMLP_F16 ? QMLP_OK : QMLP_ERR_UNSUPPORTED;   // the stream and the norm are binary16
 }
 
 bool stack_persistent(const qmlp_mlp* layers, int M, qmlp_dtype dtype) {
@@ -274,6 +280,12 @@ StackLayerDesc stack_desc(const qmlp_mlp& m) {
     s.Au = static_cast<const uint16_t*>(m.A_up);
     s.lora_scale = m.lora_scale;
     return s;
+}
+
+bool layers_persistent(const qmlp_mlp* layers, int M, qmlp_dtype dtype) {
+    const qmlp_mlp& a = layers[0];
+    return dtype == QMLP_F16 && a.down.group == a.gate.group &&
+           layers_supported(M, a.gate.k_in, a.gate.n_out, a.gate.group, a.rank);
 }
 
 }  // namespace
@@ -507,6 +519,66 @@ qmlp_status qmlp_forward_stack(const qmlp_mlp* layers, int L, const void* x, int
                 return QMLP_ERR_HIP;
         }
         xin = next;
+    }
+    return QMLP_OK;
+}
+
+size_t qmlp_layers_workspace_bytes(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    if (check_layers(layers, L, M, dtype) != QMLP_OK || M == 0)
+        return 0;
+    if (layers_persistent(layers, M, dtype))
+        return layers_ws_bytes(layers[0].gate.k_in, layers[0].gate.n_out, layers[0].rank);
+    return qmlp_workspace_bytes(&layers[0], M, dtype);
+}
+
+int qmlp_layers_launches(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    if (check_layers(layers, L, M, dtype) != QMLP_OK || M == 0)
+        return 0;
+    if (layers_persistent(layers, M, dtype))
+        return (L + layers_max_layers() - 1) / layers_max_layers();
+    int n = 0;
+    for (int i = 0; i < L; ++i) n += qmlp_forward_launches(&layers[i], M, dtype);
+    return n;
+}
+
+qmlp_status qmlp_forward_layers(const qmlp_mlp* layers, int L, const void* x, int M, qmlp_dtype dtype,
+                                void* y, void* ws, size_t ws_bytes, qmlp_stream stream) {
+    qmlp_status s = check_layers(layers, L, M, dtype);
+    if (s != QMLP_OK)
+        return s;
+    if (M == 0)
+        return QMLP_OK;
+    if (!x || !y)
+        return QMLP_ERR_NULL;
+    if (!aligned16(x) || !aligned16(y))
+        return QMLP_ERR_ALIGN;
+    if (!ws || ws_bytes < qmlp_layers_workspace_bytes(layers, L, M, dtype))
+        return QMLP_ERR_WORKSPACE;
+    if (!aligned16(ws))
+        return QMLP_ERR_ALIGN;
+    const int d = layers[0].gate.k_in;
+    const size_t step = (size_t)M * d * 2;
+    const char* xb = static_cast<const char*>(x);
+    char* yb = static_cast<char*>(y);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (layers_persistent(layers, M, dtype)) {
+        StackLayerDesc desc[64];
+        const int per = layers_max_layers();
+        for (int l0 = 0; l0 < L; l0 += per) {
+            const int n = L - l0 < per ? L - l0 : per;
+            for (int i = 0; i < n; ++i) desc[i] = stack_desc(layers[l0 + i]);
+            hipError_t e = launch_layers(desc, n, d, layers[0].gate.n_out, layers[0].gate.group, layers[0].rank,
+                                         reinterpret_cast<const uint16_t*>(xb + l0 * step),
+                                         reinterpret_cast<uint16_t*>(yb + l0 * step), ws, st);
+            if (e != hipSuccess)
+                return QMLP_ERR_HIP;
+        }
+        return QMLP_OK;
+    }
+    for (int i = 0; i < L; ++i) {
+        s = qmlp_forward(&layers[i], xb + i * step, M, dtype, yb + i * step, ws, ws_bytes, stream);
+        if (s != QMLP_OK)
+            return s;
     }
     return QMLP_OK;
 }

@@ -1,0 +1,531 @@
+// L independent decode MLP blocks in one persistent launch (M = 1,
+// binary16), gfx950.
+//
+// Each block is the W4/W2-GateUp MLP with Recover-LoRA adapters (Sec. 3.1
+// Eq. (1), Sec. 3.3, Sec. 4.2) on its own input x_l:
+//   G = W2gate x_l + s B_g (A_g x_l),  U = W2up x_l + s B_u (A_u x_l),
+//   h = SiLU(G) * U,  y_l = W4down h.
+// No block reads another block's output, so the launch runs them as a
+// software pipeline: the work of one iteration is
+//   * the gate/up rows of block i (h_i published inside the XCD),
+//   * the partial down sums of block i-2 (published to the other XCDs),
+// while the two polling waves stage block i+1's input, gather h_{i-1} of the
+// XCD and sum the eight cross-XCD partials of block i-3 into y_{i-3}.  Every
+// hand-off is therefore consumed one iteration after it was published, and
+// one barrier per iteration separates producers and consumers of the LDS
+// buffers (double-buffered by parity).  Decode is bound by loading weights
+// (Sec. 3.3, Sec. 5): each register set is reloaded with the next block's
+// weights right after its last use, so the stream never waits for a hand-off.
+//
+// Work split (8 XCDs x 32 compute units, one 512-thread workgroup each), per
+// block as in the persistent stack kernel: XCD x owns the slice
+// F_x = [x f/8, (x+1) f/8) of the intermediate dimension; its workgroup j
+// computes gate/up rows F_x,j and the partial down product over F_x for the
+// output rows D_j = [j d/32, (j+1) d/32).  Workgroup j of XCD x sums the
+// eight partials of the rows D_j[x DJ/8, (x+1) DJ/8) (DJ = d/32) in XCD order
+// and writes them.  The LoRA-A products A x_l of all blocks (fp32) are
+// computed once at the start, one dot product per polling wave, and read
+// back as tagged words.
+//
+// Which compute wave takes which gate/up wave-item and which run of down
+// wave-items is a host-side plan in the kernel arguments: waves w and w + 4
+// share a SIMD, and the plan balances the dequant work of each SIMD.
+//
+// Tags: h words carry stag(step) in their high half and sit in slot
+// step & 3 of a four-slot buffer, step = seq0 + 1 + l counted across
+// launches; a workgroup overwrites slot s only after every workgroup of its
+// XCD has staged the h that was there (it has seen their h two steps later,
+// published after their barrier that followed the staging), and clears its
+// rows of all four slots when a launch starts.  The 64-bit words (LoRA-A
+// products, down partials) carry a 32-bit tag of the step and have one slot
+// per block.
+#include "stack_common.h"
+
+namespace qmlp {
+
+namespace {
+
+// Control words (uint32 index into the control block).
+constexpr int L_SEQ = 0, L_DONE = 32, L_ERR = 64, L_XC = 96;
+
+__device__ __forceinline__ uint32_t ltag32(uint32_t step) { return step % 0xFFFFFFFFu + 1u; }
+
+}  // namespace
+
+constexpr int kLayersMaxLayers = 40;            // blocks per launch (kernel-argument block < 4 KB)
+
+struct LayersArgs {
+    StackLayer lay[kLayersMaxLayers];
+    int L, d, f, g, r;
+    const uint16_t* x;           // [L][d] inputs
+    uint16_t* y;                 // [L][d] outputs
+    unsigned long long* tb;      // [kLayersMaxLayers][2r] LoRA-A products, fp32 | tag << 32
+    uint32_t* hb;                // [4][f] XCD-local h words, binary16 | tag << 16
+    unsigned long long* pb;      // [kLayersMaxLayers][8][d] partial down sums, fp32 | tag << 32
+    unsigned* ctl;
+    int gu_item[SCW];            // gate/up wave-item of each compute wave (-1: none)
+    int dn_lo[SCW], dn_n[SCW];   // down wave-items [dn_lo, dn_lo + dn_n) of each compute wave
+    int o_xs, o_cx, o_t, o_hs, o_hcx, o_meta, meta_bytes;   // LDS byte offsets
+};
+
+namespace {
+
+typedef const LayersArgs __attribute__((address_space(4))) LKArgs;
+
+struct SlLds {
+    uint4* xs;          // [2][8 UG] x' of the activation (gate/up units), by block parity
+    float2* cx;         // [2][UG] per unit (1024 sum x', sum x)
+    float* ts;          // [2][2r + 1] A x (fp32), then 1 (no norm)
+    uint4* hs;          // [2][4 HS] h' of this XCD's slice (down units)
+    float2* hcx;        // [2][HS] per unit (1024 sum h', sum h)
+    char* meta;         // per-wave gate/up metadata areas
+};
+
+// Staging word w of block l's input: x[16w, 16w + 16) into the gate/up x'
+// layout (pairs (x[16w+p], x[16w+8+p]) pre-scaled by their fraction
+// position; chunk 2(w&3) holds pairs 0..3, chunk 2(w&3)+1 pairs 4..7 of unit
+// w/4) and the unit sums.  The four words of a unit sit on four consecutive
+// lanes.
+template <int XS>
+__device__ __forceinline__ void sl_stage_x(uint4* xs, float2* cx, const uint4 (&v)[2], bool valid, int w) {
+    const uint32_t lo[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
+    uint32_t pr[8];
+    float csum = 0.0f, xsum = 0.0f;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+        // x[16w + p] is half p of the first 16 bytes, x[16w + 8 + p] of the second
+        const uint32_t a = valid ? (lo[p >> 1] >> (16 * (p & 1))) & 0xFFFFu : 0u;
+        const uint32_t b = valid ? (lo[4 + (p >> 1)] >> (16 * (p & 1))) & 0xFFFFu : 0u;
+        const float sc = w2_pair_scale(p);
+        const uint32_t ha = f2h(h2f(a) * sc), hb = f2h(h2f(b) * sc);
+        pr[p] = ha | (hb << 16);
+        csum += h2f(ha) + h2f(hb);
+        xsum += h2f(a) + h2f(b);
+    }
+    csum = group_sum<4>(csum);
+    xsum = group_sum<4>(xsum);
+    if (valid) {
+        const int ul = w >> 2, wi = w & 3;
+        xs[(2 * wi) * XS + ul] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
+        xs[(2 * wi + 1) * XS + ul] = make_uint4(pr[4], pr[5], pr[6], pr[7]);
+        if (wi == 0)
+            cx[ul] = make_float2(1024.0f * csum, xsum);
+    }
+}
+
+// The compute waves: gate/up of block i and down of block i - 2 in
+// iteration i, weights streamed into registers one iteration ahead.
+template <int JG, int KM, int JD, int NDN>
+__device__ __forceinline__ void sl_compute_role(const LayersArgs& sa, LKArgs* ka, const SlLds& m, int xcc, int j,
+                                                uint32_t seq0, int wave, int lane) {
+    const int d = sa.d, f = sa.f, g = sa.g, r = sa.r, L = sa.L;
+    const int FX = f / SX, UF = FX / 32, DJ = d / SB, RG = f / SGRID, UG = d / 64;
+    constexpr int HS = 8 * JD;
+    const int row_begin = xcc * FX + j * RG, row_end = row_begin + RG;
+    const int gu = ka->gu_item[wave], dlo = ka->dn_lo[wave], dn = ka->dn_n[wave];
+    const bool has_gu = gu >= 0;
+    const int gu_row0 = row_begin + 8 * (has_gu ? gu : 0);
+    FGuItem<1, 8, JG, KM> gi;
+    SkDn<JD> di[NDN];
+    {
+        const StackLayer w0 = sk_layer(ka, 0);
+        if (has_gu)
+            sk_gu_load(gi, w0, gu_row0, row_end, f, d, g, r, lane);
+#pragma unroll
+        for (int k = 0; k < NDN; ++k)
+            if (k < dn)
+                sk_dn_load(di[k], w0, j * DJ + 8 * (dlo + k) + (lane >> 3), xcc, f, g, lane);
+        // This wave's h words in all four slots start the launch with tag 0
+        // (never a valid tag): a slot that earlier launches left unused for
+        // a long time cannot hold a word whose 16-bit tag comes round again.
+        // The same lane publishes the row later, so the clear precedes it.
+        if (has_gu && gi.ok && (lane & 7) == 0) {
+#pragma unroll
+            for (int s = 0; s < 4; ++s) st_intra32(sa.hb + (long)s * f + gi.row, 0u);
+        }
+    }
+    __syncthreads();                                            // B0: block 0's input staged
+    uint4* wmeta = reinterpret_cast<uint4*>(m.meta + wave * sa.meta_bytes);
+    for (int i = 0; i < L + 3; ++i) {
+        const int par = i & 1;
+        if (has_gu && i < L) {
+            const uint32_t step = seq0 + 1 + i;
+            GateUpArgs ga{};
+            ga.d = d;
+            ga.g = g;
+            fgu_meta_to_lds(gi, ga, wmeta, lane);
+            sk_gu_accumulate(gi, m.xs + par * 8 * UG, m.cx + par * UG, g,
+                             reinterpret_cast<const uint32_t*>(wmeta), lane);
+            sk_gu_finish(gi, m.ts + par * (2 * r + 1), r, sk_layer(ka, i).lora_scale, sa.hb + (long)(step & 3) * f,
+                         stag(step), lane);
+            sk_order();
+            if (i + 1 < L)
+                sk_gu_load(gi, sk_layer(ka, i + 1), gu_row0, row_end, f, d, g, r, lane);
+        }
+        const int l = i - 2;
+        if (dn > 0 && l >= 0 && l < L) {
+            const unsigned long long tg = (unsigned long long)ltag32(seq0 + 1 + l) << 32;
+            unsigned long long* pb = sa.pb + ((long)l * SX + xcc) * d;
+#pragma unroll
+            for (int k = 0; k < NDN; ++k) {
+                if (k < dn) {
+                    const float yv = sk_dn_compute<JD>(di[k], m.hs + par * 4 * HS, m.hcx + par * HS, UF, lane);
+                    const int o = j * DJ + 8 * (dlo + k) + (lane >> 3);
+                    if ((lane & 7) == 0)
+                        st_cross64(pb + o, (unsigned long long)__float_as_uint(yv) | tg);
+                }
+            }
+            sk_order();
+            if (l + 1 < L) {
+                const StackLayer wn = sk_layer(ka, l + 1);
+#pragma unroll
+                for (int k = 0; k < NDN; ++k)
+                    if (k < dn)
+                        sk_dn_load(di[k], wn, j * DJ + 8 * (dlo + k) + (lane >> 3), xcc, f, g, lane);
+            }
+        }
+        __syncthreads();                                        // one barrier per iteration
+    }
+}
+
+// The polling waves: the LoRA-A products of every block (once), then per
+// iteration the next block's input, h of the previous block, and y of the
+// block before that.
+template <int XS, int HS>
+__device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, const SlLds& m, int xcc, int j,
+                                             uint32_t seq0, int wave, int lane) {
+    const int d = sa.d, f = sa.f, r = sa.r, L = sa.L;
+    const int FX = f / SX, DJ = d / SB;
+    const int pw = wave - SCW, pt = pw * 64 + lane;
+    unsigned* ctl = sa.ctl;
+    bool dead = false;                                          // this wave gave up a wait
+
+    // LoRA-A products: dot product idx = (block l, rank k) on polling wave idx % 512
+    if (r > 0) {
+        const int total = L * 2 * r;
+        for (int idx = (xcc * SB + j) * SPW + pw; idx < total; idx += SGRID * SPW) {
+            const int l = idx / (2 * r), k = idx - l * 2 * r;
+            const StackLayer w = sk_layer(ka, l);
+            const uint16_t* arow = k < r ? w.Ag + (long)k * d : w.Au + (long)(k - r) * d;
+            const uint16_t* xl = sa.x + (long)l * d;
+            float acc = 0.0f;
+            for (int c = lane * 8; c < d; c += 512) {
+                const uint4 av = *reinterpret_cast<const uint4*>(arow + c);
+                const uint4 xv = *reinterpret_cast<const uint4*>(xl + c);
+                acc = dot2(av.x, xv.x, acc);
+                acc = dot2(av.y, xv.y, acc);
+                acc = dot2(av.z, xv.z, acc);
+                acc = dot2(av.w, xv.w, acc);
+            }
+            acc = group_sum<64>(acc);
+            if (lane == 0)
+                st_cross64(sa.tb + idx, (unsigned long long)__float_as_uint(acc) |
+                                            ((unsigned long long)ltag32(seq0 + 1 + l) << 32));
+        }
+    }
+
+    const __amdgpu_buffer_rsrc_t trs =
+        __builtin_amdgcn_make_buffer_rsrc(sa.tb, 0, kLayersMaxLayers * 2 * (r > 0 ? r : 1) * 8, 0x00020000);
+    // one 16-byte load (two ranks) per thread pt < r
+    auto stage_input = [&](int l) {
+        const int par = l & 1;
+        uint4 xv[KXW][2];
+        const uint16_t* xl = sa.x + (long)l * d;
+#pragma unroll
+        for (int kk = 0; kk < KXW; ++kk) {
+            const int w = pt + SPT * kk;
+            const int wc = w < d / 16 ? w : 0;
+            xv[kk][0] = *reinterpret_cast<const uint4*>(xl + 16 * wc);
+            xv[kk][1] = *reinterpret_cast<const uint4*>(xl + 16 * wc + 8);
+        }
+        if (r > 0) {
+            int off[1] = {(l * 2 * r + 2 * pt) * 8};
+            u32x4 v[1];
+            dead |= !sk_poll<1, 0, POL_CROSS>(trs, off, pt < r ? 1u : 0u, v, ltag32(seq0 + 1 + l), dead);
+            if (pt < r) {
+                m.ts[par * (2 * r + 1) + 2 * pt] = __uint_as_float(v[0].x);
+                m.ts[par * (2 * r + 1) + 2 * pt + 1] = __uint_as_float(v[0].z);
+            }
+        }
+        if (pt == 0)
+            m.ts[par * (2 * r + 1) + 2 * r] = 1.0f;
+#pragma unroll
+        for (int kk = 0; kk < KXW; ++kk) {
+            const int w = pt + SPT * kk;
+            sl_stage_x<XS>(m.xs + par * 8 * XS, m.cx + par * XS, xv[kk], w < d / 16, w);
+        }
+        dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
+        if (dead && lane == 0)
+            atomicOr(&ctl[L_ERR], 1u);
+    };
+
+    stage_input(0);
+    __syncthreads();                                            // B0
+
+    // h words of this XCD's slice: staging word w = pt + SPT kk covers h[8w, 8w + 8)
+    int hoff[2 * KHW];
+    uint32_t hvalid = 0;
+#pragma unroll
+    for (int kk = 0; kk < KHW; ++kk) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) hoff[2 * kk + q] = 32 * pt + 32 * SPT * kk + 16 * q;
+        if (pt + SPT * kk < FX / 8) hvalid |= 0x3u << (2 * kk);
+    }
+    // the rows of y this workgroup sums: D_j[xcc DJ/8, (xcc+1) DJ/8), two per lane of wave 1
+    const int yrow0 = j * DJ + xcc * (DJ / 8);
+    int poff[SX];
+#pragma unroll
+    for (int xx = 0; xx < SX; ++xx) poff[xx] = 16 * lane + xx * d * 8;
+    const bool yl = pw == 1 && lane < DJ / 16;
+
+    for (int i = 0; i < L + 3; ++i) {
+        if (i + 1 < L)
+            stage_input(i + 1);
+        const int lh = i - 1;
+        if (lh >= 0 && lh < L) {   // h of block lh from this XCD
+            const uint32_t step = seq0 + 1 + lh;
+            const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(
+                sa.hb + (long)(step & 3) * f + (long)xcc * FX, 0, FX * 4, 0x00020000);
+            u32x4 v[2 * KHW];
+            dead |= !sk_poll<2 * KHW, 2 * KHW, POL_INTRA>(hrs, hoff, hvalid, v, stag(step), dead);
+            const int par = lh & 1;
+#pragma unroll
+            for (int kk = 0; kk < KHW; ++kk) {
+                const int w = pt + SPT * kk;
+                sk_stage_h<HS>(m.hs + par * 4 * HS, m.hcx + par * HS, v + 2 * kk, w < FX / 8, w);
+            }
+            dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
+            if (dead && lane == 0)
+                atomicOr(&ctl[L_ERR], 2u);
+        }
+        const int ly = i - 3;
+        if (pw == 1 && ly >= 0 && ly < L) {   // the eight partials of this workgroup's rows, in XCD order
+            const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
+                sa.pb + (long)ly * SX * d + yrow0, 0, ((SX - 1) * d + DJ / 8) * 8, 0x00020000);
+            u32x4 v[SX];
+            dead |= !sk_poll<SX, 0, POL_CROSS>(prs, poff, yl ? 0xFFu : 0u, v, ltag32(seq0 + 1 + ly), dead);
+            float y0 = 0.0f, y1 = 0.0f;
+#pragma unroll
+            for (int xx = 0; xx < SX; ++xx) {
+                y0 += __uint_as_float(v[xx].x);
+                y1 += __uint_as_float(v[xx].z);
+            }
+            if (yl)
+                reinterpret_cast<uint32_t*>(sa.y + (long)ly * d + yrow0)[lane] = f2h(y0) | (f2h(y1) << 16);
+            dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
+            if (dead && lane == 0)
+                atomicOr(&ctl[L_ERR], 4u);
+        }
+        __syncthreads();
+    }
+}
+
+template <int JG, int KM, int JD, int NDN>
+__global__ void __launch_bounds__(STHREADS) layers_kernel(LayersArgs sa) {
+    extern __shared__ uint4 smem[];
+    char* lds = reinterpret_cast<char*>(smem);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    unsigned* ctl = sa.ctl;
+    int* info = reinterpret_cast<int*>(lds);
+
+    // Placement: the XCD from the hardware, the rank from a per-XCD counter.
+    const uint32_t xcc = __builtin_amdgcn_s_getreg(20 | (0 << 6) | (3 << 11));   // HW_REG_XCC_ID[3:0]
+    if (tid == 0)
+        info[0] = xcc < (uint32_t)SX ? (int)__hip_atomic_fetch_add(&ctl[L_XC + xcc], 1u, __ATOMIC_RELAXED,
+                                                                   __HIP_MEMORY_SCOPE_AGENT)
+                                     : SB;
+    const uint32_t seq0 = __builtin_amdgcn_readfirstlane(
+        __hip_atomic_load(&ctl[L_SEQ], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+    __syncthreads();
+    const int j = __builtin_amdgcn_readfirstlane(info[0]);
+
+    if (j < SB) {
+        const SlLds m{reinterpret_cast<uint4*>(lds + sa.o_xs), reinterpret_cast<float2*>(lds + sa.o_cx),
+                      reinterpret_cast<float*>(lds + sa.o_t), reinterpret_cast<uint4*>(lds + sa.o_hs),
+                      reinterpret_cast<float2*>(lds + sa.o_hcx), lds + sa.o_meta};
+        LKArgs* ka = (LKArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+        if (wave < SCW)
+            sl_compute_role<JG, KM, JD, NDN>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+        else
+            sl_poll_role<8 * JG, 8 * JD>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+    } else if (tid == 0) {
+        atomicOr(&ctl[L_ERR], 8u);              // a workgroup without a place: results invalid
+    }
+
+    // The last workgroup to finish advances the step counter and clears the
+    // placement counters.
+    if (tid == 0) {
+        const unsigned old = __hip_atomic_fetch_add(&ctl[L_DONE], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (old == (unsigned)gridDim.x - 1) {
+            __hip_atomic_store(&ctl[L_DONE], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (int x = 0; x < SX; ++x)
+                __hip_atomic_store(&ctl[L_XC + x], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&ctl[L_SEQ], seq0 + (uint32_t)sa.L + 1u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
+int layers_cu_count() {
+    static int cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 0;
+    if (cache[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
+
+struct LayersPlan {
+    int jg, km, jd, ndn;
+    int gu_item[SCW], dn_lo[SCW], dn_n[SCW];
+    int o_xs, o_cx, o_t, o_hs, o_hcx, o_meta, meta_bytes;
+    size_t lds;
+    bool ok;
+};
+
+// Wave plan: gate/up wave-item k on compute wave k; then the down items, one
+// at a time, to the SIMD with the least dequant work (a gate/up item weighs
+// 16 d / f down items: 8 rows of 2 d weights against 8 rows of f/8; a polling
+// wave weighs one), on its compute wave with the fewest items below the
+// register limit; each wave's items are then numbered consecutively.
+void plan_waves(LayersPlan& p, int gu_items, int dn_items, int d, int f) {
+    const double rho = 16.0 * d / f;
+    double load[4] = {0.0, 0.0, 1.0, 1.0};                      // SIMDs of polling waves 6 and 7
+    int cnt[SCW] = {};
+    for (int w = 0; w < SCW; ++w) {
+        p.gu_item[w] = w < gu_items ? w : -1;
+        if (w < gu_items)
+            load[w & 3] += rho;
+    }
+    for (int it = 0; it < dn_items; ++it) {
+        int best = -1;
+        for (int w = 0; w < SCW; ++w) {
+            if (cnt[w] >= p.ndn)
+                continue;
+            if (best < 0 || load[w & 3] < load[best & 3] ||
+                (load[w & 3] == load[best & 3] && cnt[w] < cnt[best]))
+                best = w;
+        }
+        if (best < 0) {
+            p.ok = false;
+            return;
+        }
+        ++cnt[best];
+        load[best & 3] += 1.0;
+    }
+    int lo = 0;
+    for (int w = 0; w < SCW; ++w) {
+        p.dn_lo[w] = lo;
+        p.dn_n[w] = cnt[w];
+        lo += cnt[w];
+    }
+}
+
+LayersPlan plan_layers(int M, int d, int f, int g, int r) {
+    LayersPlan p{};
+    p.ok = false;
+    if (M != 1 || d <= 0 || f <= 0 || (g != 64 && g != 128))
+        return p;
+    if (f % SGRID != 0 || (f / SX) % 32 != 0 || d % 512 != 0 || d % g != 0 || f % g != 0)
+        return p;
+    const int RG = f / SGRID, UG = d / 64, ng = d / g, UF = f / SX / 32, DJ = d / SB;
+    if ((RG + 7) / 8 > SCW || ng % 4 != 0 || DJ % 16 != 0 || DJ / 16 > 64)
+        return p;
+    if (r != 0 && r != 8 && r != 16 && r != 32)
+        return p;
+    if (UG % 8 != 0)                             // 8 lanes per row, no partial slot
+        return p;
+    p.jg = UG / 8;
+    p.km = (4 * ng + 63) / 64;
+    p.jd = (UF + 7) / 8;
+    if ((d / 16 + SPT - 1) / SPT > KXW || (f / SX / 8 + SPT - 1) / SPT > KHW)
+        return p;
+    if (p.jg == 5 && p.km == 2 && p.jd == 5)
+        p.ndn = 3;
+    else if (p.jg == 8 && p.km == 2 && p.jd == 6)
+        p.ndn = 3;
+    else if (p.jg == 1 && p.km == 1 && p.jd == 1)
+        p.ndn = 1;
+    else
+        return p;
+    if (layers_cu_count() != SGRID)
+        return p;
+    p.ok = true;
+    plan_waves(p, (RG + 7) / 8, DJ / 8, d, f);
+    if (!p.ok)
+        return p;
+    size_t o = 16;
+    auto take = [&](size_t bytes) { const size_t at = o; o = (o + bytes + 15) / 16 * 16; return (int)at; };
+    p.o_xs = take((size_t)2 * UG * 8 * 16);
+    p.o_cx = take((size_t)2 * UG * 8);
+    p.o_t = take((size_t)2 * (2 * r + 1) * 4);
+    p.o_hs = take((size_t)2 * p.jd * 8 * 4 * 16);   // chunk stride 8 JD >= UF units
+    p.o_hcx = take((size_t)2 * p.jd * 8 * 8);
+    p.meta_bytes = 2 * 8 * ng * 4;
+    p.o_meta = take((size_t)SCW * p.meta_bytes);
+    p.lds = o;
+    p.ok = p.lds <= 64 * 1024;
+    return p;
+}
+
+size_t tb_bytes(int r) { return ((size_t)kLayersMaxLayers * 2 * (r > 0 ? r : 1) * 8 + 255) & ~(size_t)255; }
+
+}  // namespace
+
+bool layers_supported(int M, int d, int f, int g, int r) { return plan_layers(M, d, f, g, r).ok; }
+
+size_t layers_ws_bytes(int d, int f, int r) {
+    return 1024 + tb_bytes(r) + (((size_t)4 * f * 4 + 255) & ~(size_t)255) +
+           (size_t)kLayersMaxLayers * SX * d * 8;
+}
+
+int layers_max_layers() { return kLayersMaxLayers; }
+
+hipError_t launch_layers(const StackLayerDesc* layers, int L, int d, int f, int g, int r, const uint16_t* x,
+                         uint16_t* y, void* ws, hipStream_t st) {
+    const LayersPlan p = plan_layers(1, d, f, g, r);
+    if (!p.ok || L <= 0 || L > kLayersMaxLayers)
+        return hipErrorInvalidValue;
+    LayersArgs a{};
+    for (int i = 0; i < L; ++i) {
+        const StackLayerDesc& s = layers[i];
+        a.lay[i] = StackLayer{s.cg, s.mg, s.cu, s.mu, s.cd, s.md, s.Bg, s.Bu, s.Ag, s.Au, s.lora_scale};
+    }
+    a.L = L;
+    a.d = d;
+    a.f = f;
+    a.g = g;
+    a.r = r;
+    a.x = x;
+    a.y = y;
+    char* base = static_cast<char*>(ws);
+    a.ctl = reinterpret_cast<unsigned*>(base);
+    a.tb = reinterpret_cast<unsigned long long*>(base + 1024);
+    a.hb = reinterpret_cast<uint32_t*>(base + 1024 + tb_bytes(r));
+    a.pb = reinterpret_cast<unsigned long long*>(base + 1024 + tb_bytes(r) +
+                                                 (((size_t)4 * f * 4 + 255) & ~(size_t)255));
+    for (int w = 0; w < SCW; ++w) {
+        a.gu_item[w] = p.gu_item[w];
+        a.dn_lo[w] = p.dn_lo[w];
+        a.dn_n[w] = p.dn_n[w];
+    }
+    a.o_xs = p.o_xs; a.o_cx = p.o_cx; a.o_t = p.o_t; a.o_hs = p.o_hs; a.o_hcx = p.o_hcx;
+    a.o_meta = p.o_meta; a.meta_bytes = p.meta_bytes;
+    auto run = [&](auto kernel) -> hipError_t {
+        kernel<<<SGRID, STHREADS, p.lds, st>>>(a);
+        return hipGetLastError();
+    };
+    if (p.jg == 5)
+        return run(layers_kernel<5, 2, 5, 3>);
+    if (p.jg == 8)
+        return run(layers_kernel<8, 2, 6, 3>);
+    return run(layers_kernel<1, 1, 1, 1>);
+}
+
+}  // namespace qmlp

@@ -84,4 +84,13 @@ hipError_t launch_residual(const uint16_t* x, const uint16_t* y, uint16_t* out, 
                            hipStream_t st);
 hipError_t launch_rmsnorm(const uint16_t* x, uint16_t* u, int M, int d, hipStream_t st);
 
+// decode_layers.hip: L independent blocks of one shape (M = 1, binary16) in one
+// persistent launch, block l on x[l] -> y[l].  ws: the layers area
+// (layers_ws_bytes, zero before the first call; 1024-byte control block first).
+bool layers_supported(int M, int d, int f, int g, int r);
+size_t layers_ws_bytes(int d, int f, int r);
+int layers_max_layers();
+hipError_t launch_layers(const StackLayerDesc* layers, int L, int d, int f, int g, int r, const uint16_t* x,
+                         uint16_t* y, void* ws, hipStream_t st);
+
 }  // namespace qmlp

@@ -187,3 +187,36 @@ def test_stack_validation(q, lib):
     assert fs(bad, 2) == UNSUP
     # the stack workspace covers at least the per-block workspace
     assert lib.qmlp_stack_workspace_bytes(arr, 2, 1, 0) >= lib.qmlp_workspace_bytes(ctypes.byref(m), 1, 0)
+
+
+def test_layers_validation(q, lib):
+    """qmlp_forward_layers: the same host-side checks as the stack, bfloat16
+    accepted (it runs per block), and the persistent workspace starts with
+    the control block."""
+    m = _mlp(q)
+    arr = _stack_arr(q, m, _mlp(q))
+    P = ctypes.c_void_p
+
+    def fl(a, L, M=1, x=FAKE, y=FAKE, ws=FAKE, wsb=1 << 30, dt=0):
+        return lib.qmlp_forward_layers(a, L, P(x), M, dt, P(y), P(ws), wsb, None)
+
+    assert lib.qmlp_forward_layers(None, 2, None, 1, 0, None, None, 0, None) == NULL
+    assert fl(arr, 0) == SHAPE
+    assert fl(arr, 2, x=0) == NULL
+    assert fl(arr, 2, y=FAKE + 8) == ALIGN
+    assert fl(arr, 2, ws=FAKE + 8) == ALIGN
+    assert fl(arr, 2, M=17) == UNSUP
+    assert fl(arr, 2, ws=0) == WS
+    assert fl(arr, 2, wsb=16) == WS
+    assert fl(arr, 2, M=0) == 0                     # nothing to do
+    odd = _stack_arr(q, m, _mlp(q, d=320, f=448))
+    assert fl(odd, 2) == SHAPE
+    assert lib.qmlp_layers_workspace_bytes(odd, 2, 1, 0) == 0
+    assert lib.qmlp_layers_launches(odd, 2, 1, 0) == 0
+    bad = _stack_arr(q, m, _mlp(q, rank=7))
+    assert fl(bad, 2) == UNSUP
+    # without a GPU no shape runs persistently: one forward per block, and
+    # the workspace is the per-block one
+    assert lib.qmlp_layers_launches(arr, 2, 1, 0) == 2 * lib.qmlp_forward_launches(ctypes.byref(m), 1, 0)
+    assert lib.qmlp_layers_workspace_bytes(arr, 2, 1, 0) == lib.qmlp_workspace_bytes(ctypes.byref(m), 1, 0)
+    assert lib.qmlp_layers_workspace_bytes(arr, 2, 1, 1) == lib.qmlp_workspace_bytes(ctypes.byref(m), 1, 1)

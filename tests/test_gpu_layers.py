@@ -1,0 +1,230 @@
+"""GPU parity of L independent blocks (qmlp_forward_layers) against the fp64
+oracle.
+
+Every block has its own seeded weights and its own seeded input x_l, and
+y_l = block_l(x_l) is compared with the oracle's forward of that block's
+quantized weights on x_l at the output bar max|y - y_ref| / max|y_ref| <=
+1e-2 (the oracle quantizes the fp32 weights itself and keeps h in fp64).
+The persistent launch pipelines the blocks (gate/up of block i, down of
+block i-2, the output sum of block i-3 in one iteration), so a mix-up of
+blocks or of buffer parities would pair an output with the wrong block's
+oracle and fail.  Each case prints its name and shape before touching the
+GPU.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+import workloads as wl
+from qmlp_testutil import act_tensor, bits_of, gpu_mlp, oracle_q, values_of
+
+pytestmark = pytest.mark.gpu
+
+Y_TOL = 1e-2
+
+
+@pytest.fixture(scope="module")
+def q():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_04238_amd as qm
+    qm.library()
+    return qm
+
+
+def _announce(*what):
+    print("\n[case]", *what, flush=True)
+
+
+def _blocks(q, cfg, L, seed=0, lora_scale=None, rank=True, first=0):
+    layers = [wl.layer(cfg, first + i, seed) for i in range(L)]
+    mlps = [gpu_mlp(lay, lora_scale=lora_scale, rank=rank) for lay in layers]
+    x = torch.stack([act_tensor(lay.x) for lay in layers])          # [L][M][d]
+    return layers, mlps, q.Layers(mlps), x
+
+
+def _check(layers, y, which=None, lora_scale=None, rank=True, tol=Y_TOL):
+    """Block l's output against the oracle on block l's own input."""
+    cfg = layers[0].cfg
+    ys = bits_of(y).reshape(len(layers), cfg.M, cfg.d)
+    errs = {}
+    for i in (range(len(layers)) if which is None else which):
+        lay = layers[i]
+        qg, qu, qd = oracle_q(lay)
+        ls = cfg.lora_scale if lora_scale is None else lora_scale
+        lo = (lay.A_gate, lay.B_gate, lay.A_up, lay.B_up) if rank else (None,) * 4
+        ref = orc.forward(qg, qu, qd, *lo, lay.x, lora_scale=ls, bf16=False)
+        errs[i] = orc.max_rel_err(orc.act_to_f64(ys[i], False), ref)
+        assert errs[i] <= tol, (i, errs[i])
+    return errs
+
+
+@pytest.mark.parametrize("L", [1, 2, 3, 4, 7])
+def test_layers_tiny_match_oracle(q, L):
+    """Pipeline fill and drain at every length up to past its depth."""
+    cfg = wl.CONFIGS["tiny"]
+    _announce("layers", cfg.name, "L", L)
+    layers, mlps, ls, x = _blocks(q, cfg, L)
+    assert q.layers_launches(ls, 1) == 1          # the persistent launch serves this shape
+    ws = q.layers_workspace(ls, 1)
+    y = q.forward_layers(ls, x, ws=ws)
+    torch.cuda.synchronize()
+    assert q.layers_errors(ws) == 0
+    errs = _check(layers, y)
+    print("max-rel errors per block:", ["%.2e" % e for e in errs.values()])
+
+
+def test_layers_qwen3_4b_match_oracle(q):
+    cfg = wl.CONFIGS["qwen3_4b"]
+    _announce("layers", cfg.name, "L", 5)
+    layers, mlps, ls, x = _blocks(q, cfg, 5)
+    assert q.layers_launches(ls, 1) == 1
+    ws = q.layers_workspace(ls, 1)
+    y = q.forward_layers(ls, x, ws=ws)
+    torch.cuda.synchronize()
+    assert q.layers_errors(ws) == 0
+    errs = _check(layers, y)
+    print("max-rel errors per block:", ["%.2e" % e for e in errs.values()])
+
+
+def test_layers_deterministic_and_match_per_block_forward(q):
+    """Repeated calls on one workspace (the tags advance) give the same bits;
+    qmlp_forward of each block on its input agrees within the bar."""
+    cfg = wl.CONFIGS["qwen3_4b"]
+    _announce("layers determinism", cfg.name, "L", 4)
+    layers, mlps, ls, x = _blocks(q, cfg, 4, first=10)
+    ws = q.layers_workspace(ls, 1)
+    outs = [q.forward_layers(ls, x, ws=ws).clone() for _ in range(3)]
+    torch.cuda.synchronize()
+    assert q.layers_errors(ws) == 0
+    for o in outs[1:]:
+        assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16))
+    wsl = q.workspace(mlps[0], 1)
+    for i, m in enumerate(mlps):
+        yl = q.forward(m, x[i], ws=wsl)
+        assert orc.max_rel_err(values_of(yl), values_of(outs[0][i])) <= Y_TOL
+
+
+def test_layers_calls_of_different_lengths_share_a_workspace(q):
+    """Calls with 5, 1, 2 and 5 blocks in a row on one workspace: every call
+    reads only words its own launch wrote (the slots of h rotate across
+    launches, the 64-bit words carry the launch's step)."""
+    cfg = wl.CONFIGS["tiny"]
+    _announce("layers varying L", cfg.name)
+    layers, mlps, ls, x = _blocks(q, cfg, 5, first=3)
+    ws = q.layers_workspace(ls, 1)
+    for L in (5, 1, 2, 5):
+        sub = q.Layers(mlps[:L])
+        y = q.forward_layers(sub, x[:L].contiguous(), ws=ws)
+        torch.cuda.synchronize()
+        assert q.layers_errors(ws) == 0
+        _check(layers[:L], y)
+
+
+def test_layers_more_than_one_launch(q):
+    """44 blocks: two persistent launches of 40 and 4 blocks."""
+    cfg = wl.CONFIGS["tiny"]
+    _announce("layers", cfg.name, "L", 44)
+    layers, mlps, ls, x = _blocks(q, cfg, 44)
+    assert q.layers_launches(ls, 1) == 2
+    ws = q.layers_workspace(ls, 1)
+    y = q.forward_layers(ls, x, ws=ws)
+    torch.cuda.synchronize()
+    assert q.layers_errors(ws) == 0
+    _check(layers, y)
+
+
+def test_layers_without_adapter_and_zero_B(q):
+    """Rank 0 matches the oracle without LoRA; B = 0 gives the same bits as
+    lora_scale = 0."""
+    cfg = wl.CONFIGS["tiny"]
+    _announce("layers rank 0 / B = 0", cfg.name)
+    layers, mlps, ls, x = _blocks(q, cfg, 3, rank=False)
+    y = q.forward_layers(ls, x)
+    torch.cuda.synchronize()
+    _check(layers, y, rank=False)
+    base = [gpu_mlp(lay) for lay in layers]
+    zb = [q.MLP(m.gate, m.up, m.down, m.A_gate, torch.zeros_like(m.B_gate), m.A_up,
+                torch.zeros_like(m.B_up)) for m in base]
+    zs = [m.with_lora_scale(0.0) for m in base]
+    y_zb = q.forward_layers(q.Layers(zb), x)
+    y_zs = q.forward_layers(q.Layers(zs), x)
+    torch.cuda.synchronize()
+    assert torch.equal(y_zb.view(torch.int16), y_zs.view(torch.int16))
+
+
+def test_layers_graph_replays_match_eager(q):
+    """Captured in a HIP graph and replayed several times, with eager work in
+    between: every replay reproduces the eager outputs bit for bit."""
+    cfg = wl.CONFIGS["qwen3_4b"]
+    _announce("layers graph replay", cfg.name, "L", 4)
+    layers, mlps, ls, x = _blocks(q, cfg, 4, first=20)
+    ws = q.layers_workspace(ls, 1)
+    y = torch.empty_like(x)
+    q.forward_layers(ls, x, y=y, ws=ws)
+    torch.cuda.synchronize()
+    eager = y.clone()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            q.forward_layers(ls, x, y=y, ws=ws)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        y.fill_(0)
+        junk = torch.randn(1 << 20, device="cuda").sum()
+        g.replay()
+        torch.cuda.synchronize()
+        assert float(junk) == float(junk)
+        assert torch.equal(y.view(torch.int16), eager.view(torch.int16)), rep
+    assert q.layers_errors(ws) == 0
+
+
+def test_layers_qwen3_8b_match_oracle(q):
+    cfg = wl.CONFIGS["qwen3_8b_m1"]
+    _announce("layers", cfg.name, "L", 3)
+    layers, mlps, ls, x = _blocks(q, cfg, 3)
+    ws = q.layers_workspace(ls, 1)
+    y = q.forward_layers(ls, x, ws=ws)
+    torch.cuda.synchronize()
+    if q.layers_launches(ls, 1) == 1:
+        assert q.layers_errors(ws) == 0
+    _check(layers, y)
+
+
+def test_layers_fallback_shapes_run_per_block(q):
+    """Shapes outside the persistent kernel (M > 1) run qmlp_forward per block."""
+    small = wl.Config("layers_m4", M=4, d=512, f=1536, g=64, r=8, L=3)
+    _announce("layers fallback", small.name)
+    layers, mlps, ls, x = _blocks(q, small, 3)
+    assert q.layers_launches(ls, 4) == 3 * q.forward_launches(mlps[0], 4)
+    y = q.forward_layers(ls, x)
+    torch.cuda.synchronize()
+    _check(layers, y)
+
+
+def test_layers_qwen3_4b_full_depth_sampled(q):
+    """The benchmark's 36 Qwen3-4B blocks in its launch configuration (one
+    persistent launch); blocks 0, 1, 17, 34 and 35 (fill, middle, drain)
+    against the oracle, and every block against qmlp_forward on its input."""
+    cfg = wl.CONFIGS["qwen3_4b"]
+    _announce("layers full depth", cfg.name, "L", cfg.L)
+    layers, mlps, ls, x = _blocks(q, cfg, cfg.L)
+    assert q.layers_launches(ls, 1) == 1
+    ws = q.layers_workspace(ls, 1)
+    y = q.forward_layers(ls, x, ws=ws)
+    torch.cuda.synchronize()
+    assert q.layers_errors(ws) == 0
+    errs = _check(layers, y, which=(0, 1, 17, 34, 35))
+    print("max-rel errors:", {k: "%.2e" % v for k, v in errs.items()})
+    wsl = q.workspace(mlps[0], 1)
+    worst = 0.0
+    for i, m in enumerate(mlps):
+        yl = q.forward(m, x[i], ws=wsl)
+        worst = max(worst, orc.max_rel_err(values_of(y[i]), values_of(yl)))
+    print("max-rel vs per-block forward: %.2e" % worst)
+    assert worst <= Y_TOL
+    assert np.isfinite(values_of(y)).all()
