@@ -50,6 +50,10 @@ constexpr int L_SEQ = 0, L_DONE = 32, L_ERR = 64, L_XC = 96;
 
 __device__ __forceinline__ uint32_t ltag32(uint32_t step) { return step % 0xFFFFFFFFu + 1u; }
 
+constexpr int LCW = 10;                  // compute waves: gate/up waves first, then down waves
+constexpr int LTHREADS = (LCW + SPW) * 64;
+constexpr int LGU_MAX = 6;               // gate/up waves (one wave-item each) at most
+
 }  // namespace
 
 constexpr int kLayersMaxLayers = 40;            // blocks per launch (kernel-argument block < 4 KB)
@@ -63,8 +67,8 @@ struct LayersArgs {
     uint32_t* hb;                // [4][f] XCD-local h words, binary16 | tag << 16
     unsigned long long* pb;      // [kLayersMaxLayers][8][d] partial down sums, fp32 | tag << 32
     unsigned* ctl;
-    int gu_item[SCW];            // gate/up wave-item of each compute wave (-1: none)
-    int dn_lo[SCW], dn_n[SCW];   // down wave-items [dn_lo, dn_lo + dn_n) of each compute wave
+    int n_gu;                    // compute waves 0 .. n_gu-1 each run gate/up wave-item `wave`
+    int dn_lo[LCW], dn_n[LCW];   // down wave-items [dn_lo, dn_lo + dn_n) of the other compute waves
     int o_xs, o_cx, o_t, o_hs, o_hcx, o_meta, meta_bytes;   // LDS byte offsets
 };
 
@@ -113,79 +117,98 @@ __device__ __forceinline__ void sl_stage_x(uint4* xs, float2* cx, const uint4 (&
     }
 }
 
-// The compute waves: gate/up of block i and down of block i - 2 in
-// iteration i, weights streamed into registers one iteration ahead.
-template <int JG, int KM, int JD, int NDN>
-__device__ __forceinline__ void sl_compute_role(const LayersArgs& sa, LKArgs* ka, const SlLds& m, int xcc, int j,
-                                                uint32_t seq0, int wave, int lane) {
+// A gate/up wave: gate/up wave-item `wave` of block i in iteration i; its
+// registers are reloaded with block i+1's codes right after the arithmetic.
+// A wave runs one kind of arithmetic only, and its loop body issues its loads
+// without a condition (the last block is peeled off), so the loads it waits
+// for are always exactly the oldest ones it has in flight.
+template <int JG, int KM>
+__device__ __forceinline__ void sl_gu_role(const LayersArgs& sa, LKArgs* ka, const SlLds& m, int xcc, int j,
+                                           uint32_t seq0, int wave, int lane) {
     const int d = sa.d, f = sa.f, g = sa.g, r = sa.r, L = sa.L;
-    const int FX = f / SX, UF = FX / 32, DJ = d / SB, RG = f / SGRID, UG = d / 64;
-    constexpr int HS = 8 * JD;
+    const int FX = f / SX, RG = f / SGRID, UG = d / 64;
     const int row_begin = xcc * FX + j * RG, row_end = row_begin + RG;
-    const int gu = ka->gu_item[wave], dlo = ka->dn_lo[wave], dn = ka->dn_n[wave];
-    const bool has_gu = gu >= 0;
-    const int gu_row0 = row_begin + 8 * (has_gu ? gu : 0);
+    const int row0 = row_begin + 8 * wave;
     FGuItem<1, 8, JG, KM> gi;
-    SkDn<JD> di[NDN];
-    {
-        const StackLayer w0 = sk_layer(ka, 0);
-        if (has_gu)
-            sk_gu_load(gi, w0, gu_row0, row_end, f, d, g, r, lane);
+    sk_gu_load(gi, sk_layer(ka, 0), row0, row_end, f, d, g, r, lane);
+    // This wave's h words in all four slots start the launch with tag 0
+    // (never a valid tag): a slot that earlier launches left unused for a
+    // long time cannot hold a word whose 16-bit tag comes round again.  The
+    // same lane publishes the row later, so the clear precedes it.
+    if (gi.ok && (lane & 7) == 0) {
 #pragma unroll
-        for (int k = 0; k < NDN; ++k)
-            if (k < dn)
-                sk_dn_load(di[k], w0, j * DJ + 8 * (dlo + k) + (lane >> 3), xcc, f, g, lane);
-        // This wave's h words in all four slots start the launch with tag 0
-        // (never a valid tag): a slot that earlier launches left unused for
-        // a long time cannot hold a word whose 16-bit tag comes round again.
-        // The same lane publishes the row later, so the clear precedes it.
-        if (has_gu && gi.ok && (lane & 7) == 0) {
-#pragma unroll
-            for (int s = 0; s < 4; ++s) st_intra32(sa.hb + (long)s * f + gi.row, 0u);
-        }
+        for (int s = 0; s < 4; ++s) st_intra32(sa.hb + (long)s * f + gi.row, 0u);
     }
     __syncthreads();                                            // B0: block 0's input staged
     uint4* wmeta = reinterpret_cast<uint4*>(m.meta + wave * sa.meta_bytes);
-    for (int i = 0; i < L + 3; ++i) {
+    auto compute = [&](int i) {
         const int par = i & 1;
-        if (has_gu && i < L) {
-            const uint32_t step = seq0 + 1 + i;
-            GateUpArgs ga{};
-            ga.d = d;
-            ga.g = g;
-            fgu_meta_to_lds(gi, ga, wmeta, lane);
-            sk_gu_accumulate(gi, m.xs + par * 8 * UG, m.cx + par * UG, g,
-                             reinterpret_cast<const uint32_t*>(wmeta), lane);
-            sk_gu_finish(gi, m.ts + par * (2 * r + 1), r, sk_layer(ka, i).lora_scale, sa.hb + (long)(step & 3) * f,
-                         stag(step), lane);
-            sk_order();
-            if (i + 1 < L)
-                sk_gu_load(gi, sk_layer(ka, i + 1), gu_row0, row_end, f, d, g, r, lane);
-        }
-        const int l = i - 2;
-        if (dn > 0 && l >= 0 && l < L) {
-            const unsigned long long tg = (unsigned long long)ltag32(seq0 + 1 + l) << 32;
-            unsigned long long* pb = sa.pb + ((long)l * SX + xcc) * d;
-#pragma unroll
-            for (int k = 0; k < NDN; ++k) {
-                if (k < dn) {
-                    const float yv = sk_dn_compute<JD>(di[k], m.hs + par * 4 * HS, m.hcx + par * HS, UF, lane);
-                    const int o = j * DJ + 8 * (dlo + k) + (lane >> 3);
-                    if ((lane & 7) == 0)
-                        st_cross64(pb + o, (unsigned long long)__float_as_uint(yv) | tg);
-                }
-            }
-            sk_order();
-            if (l + 1 < L) {
-                const StackLayer wn = sk_layer(ka, l + 1);
-#pragma unroll
-                for (int k = 0; k < NDN; ++k)
-                    if (k < dn)
-                        sk_dn_load(di[k], wn, j * DJ + 8 * (dlo + k) + (lane >> 3), xcc, f, g, lane);
-            }
-        }
+        const uint32_t step = seq0 + 1 + i;
+        GateUpArgs ga{};
+        ga.d = d;
+        ga.g = g;
+        fgu_meta_to_lds(gi, ga, wmeta, lane);
+        sk_gu_accumulate(gi, m.xs + par * 8 * UG, m.cx + par * UG, g, reinterpret_cast<const uint32_t*>(wmeta),
+                         lane);
+        sk_gu_finish(gi, m.ts + par * (2 * r + 1), r, sk_layer(ka, i).lora_scale, sa.hb + (long)(step & 3) * f,
+                     stag(step), lane, wmeta + 4 * (d / g));
+        sk_order();
+    };
+    for (int i = 0; i + 1 < L; ++i) {
+        compute(i);
+        sk_gu_load(gi, sk_layer(ka, i + 1), row0, row_end, f, d, g, r, lane);
         __syncthreads();                                        // one barrier per iteration
     }
+    compute(L - 1);
+    for (int i = L - 1; i < L + 3; ++i) __syncthreads();       // iterations L-1 .. L+2
+}
+
+// A down wave with N down wave-items: the items of block i - 2 in iteration
+// i, each item's registers reloaded with block i-1's codes right after its
+// arithmetic (the last block peeled off, as for the gate/up waves).
+template <int JD, int N>
+__device__ __forceinline__ void sl_dn_role(const LayersArgs& sa, LKArgs* ka, const SlLds& m, int xcc, int j,
+                                           uint32_t seq0, int wave, int lane) {
+    const int d = sa.d, f = sa.f, g = sa.g, L = sa.L;
+    const int UF = f / SX / 32, DJ = d / SB;
+    constexpr int HS = 8 * JD;
+    const int o = j * DJ + 8 * ka->dn_lo[wave] + (lane >> 3);  // output row of item 0 on this lane
+    SkDn<JD> di[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) sk_dn_load(di[k], sk_layer(ka, 0), o + 8 * k, xcc, f, g, lane);
+    __syncthreads();                                            // B0
+    __syncthreads();                                            // iteration 0
+    __syncthreads();                                            // iteration 1
+    // All items' arithmetic first, then their stores, then the reloads: a
+    // store counts in the same in-order counter as the loads, so a store
+    // between two items would make the second item wait for its completion.
+    auto items = [&](int l) {
+        float yv[N];
+#pragma unroll
+        for (int k = 0; k < N; ++k)
+            yv[k] = sk_dn_compute<JD>(di[k], m.hs + (l & 1) * 4 * HS, m.hcx + (l & 1) * HS, UF, lane);
+        const unsigned long long tg = (unsigned long long)ltag32(seq0 + 1 + l) << 32;
+#pragma unroll
+        for (int k = 0; k < N; ++k)
+            if ((lane & 7) == 0)
+                st_cross64(sa.pb + ((long)l * SX + xcc) * d + o + 8 * k, (unsigned long long)__float_as_uint(yv[k]) | tg);
+        sk_order();
+    };
+    for (int l = 0; l + 1 < L; ++l) {                           // iteration l + 2
+        items(l);
+        const StackLayer wn = sk_layer(ka, l + 1);
+#pragma unroll
+        for (int k = 0; k < N; ++k) sk_dn_load(di[k], wn, o + 8 * k, xcc, f, g, lane);
+        __syncthreads();
+    }
+    items(L - 1);                                               // iteration L + 1
+    __syncthreads();
+    __syncthreads();                                            // iteration L + 2
+}
+
+// A compute wave without work in this plan: the barriers only.
+__device__ __forceinline__ void sl_idle_role(int L) {
+    for (int i = 0; i < L + 4; ++i) __syncthreads();           // B0 and L + 3 iterations
 }
 
 // The polling waves: the LoRA-A products of every block (once), then per
@@ -196,7 +219,7 @@ __device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, c
                                              uint32_t seq0, int wave, int lane) {
     const int d = sa.d, f = sa.f, r = sa.r, L = sa.L;
     const int FX = f / SX, DJ = d / SB;
-    const int pw = wave - SCW, pt = pw * 64 + lane;
+    const int pw = wave - LCW, pt = pw * 64 + lane;
     unsigned* ctl = sa.ctl;
     bool dead = false;                                          // this wave gave up a wait
 
@@ -226,42 +249,6 @@ __device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, c
 
     const __amdgpu_buffer_rsrc_t trs =
         __builtin_amdgcn_make_buffer_rsrc(sa.tb, 0, kLayersMaxLayers * 2 * (r > 0 ? r : 1) * 8, 0x00020000);
-    // one 16-byte load (two ranks) per thread pt < r
-    auto stage_input = [&](int l) {
-        const int par = l & 1;
-        uint4 xv[KXW][2];
-        const uint16_t* xl = sa.x + (long)l * d;
-#pragma unroll
-        for (int kk = 0; kk < KXW; ++kk) {
-            const int w = pt + SPT * kk;
-            const int wc = w < d / 16 ? w : 0;
-            xv[kk][0] = *reinterpret_cast<const uint4*>(xl + 16 * wc);
-            xv[kk][1] = *reinterpret_cast<const uint4*>(xl + 16 * wc + 8);
-        }
-        if (r > 0) {
-            int off[1] = {(l * 2 * r + 2 * pt) * 8};
-            u32x4 v[1];
-            dead |= !sk_poll<1, 0, POL_CROSS>(trs, off, pt < r ? 1u : 0u, v, ltag32(seq0 + 1 + l), dead);
-            if (pt < r) {
-                m.ts[par * (2 * r + 1) + 2 * pt] = __uint_as_float(v[0].x);
-                m.ts[par * (2 * r + 1) + 2 * pt + 1] = __uint_as_float(v[0].z);
-            }
-        }
-        if (pt == 0)
-            m.ts[par * (2 * r + 1) + 2 * r] = 1.0f;
-#pragma unroll
-        for (int kk = 0; kk < KXW; ++kk) {
-            const int w = pt + SPT * kk;
-            sl_stage_x<XS>(m.xs + par * 8 * XS, m.cx + par * XS, xv[kk], w < d / 16, w);
-        }
-        dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
-        if (dead && lane == 0)
-            atomicOr(&ctl[L_ERR], 1u);
-    };
-
-    stage_input(0);
-    __syncthreads();                                            // B0
-
     // h words of this XCD's slice: staging word w = pt + SPT kk covers h[8w, 8w + 8)
     int hoff[2 * KHW];
     uint32_t hvalid = 0;
@@ -278,37 +265,89 @@ __device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, c
     for (int xx = 0; xx < SX; ++xx) poff[xx] = 16 * lane + xx * d * 8;
     const bool yl = pw == 1 && lane < DJ / 16;
 
+    // Per iteration the first round of every load (the next block's input
+    // and LoRA-A products, h of the previous block, the partials of the
+    // block before that) goes out together; then each is resolved in turn.
+    uint4 xv[KXW][2];
+    u32x4 tv[1];
+    int toff[1] = {0};
+    auto issue_input = [&](int l) {
+        const uint16_t* xl = sa.x + (long)l * d;
+#pragma unroll
+        for (int kk = 0; kk < KXW; ++kk) {
+            const int w = pt + SPT * kk;
+            const int wc = w < d / 16 ? w : 0;
+            xv[kk][0] = *reinterpret_cast<const uint4*>(xl + 16 * wc);
+            xv[kk][1] = *reinterpret_cast<const uint4*>(xl + 16 * wc + 8);
+        }
+        toff[0] = (l * 2 * r + 2 * pt) * 8;              // ranks 2 pt, 2 pt + 1
+        if (r > 0)
+            sk_poll_issue<1, POL_CROSS>(trs, toff, pt < r && !dead ? 1u : 0u, tv);
+    };
+    auto finish_input = [&](int l) {
+        const int par = l & 1;
+        if (r > 0) {
+            if (!dead)
+                dead = !sk_poll_finish<1, 0, POL_CROSS>(trs, toff, pt < r ? 1u : 0u, tv, ltag32(seq0 + 1 + l));
+            if (pt < r) {
+                m.ts[par * (2 * r + 1) + 2 * pt] = __uint_as_float(tv[0].x);
+                m.ts[par * (2 * r + 1) + 2 * pt + 1] = __uint_as_float(tv[0].z);
+            }
+        }
+        if (pt == 0)
+            m.ts[par * (2 * r + 1) + 2 * r] = 1.0f;
+#pragma unroll
+        for (int kk = 0; kk < KXW; ++kk) {
+            const int w = pt + SPT * kk;
+            sl_stage_x<XS>(m.xs + par * 8 * XS, m.cx + par * XS, xv[kk], w < d / 16, w);
+        }
+        dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
+        if (dead && lane == 0)
+            atomicOr(&ctl[L_ERR], 1u);
+    };
+
+    issue_input(0);
+    finish_input(0);
+    __syncthreads();                                            // B0
+
     for (int i = 0; i < L + 3; ++i) {
-        if (i + 1 < L)
-            stage_input(i + 1);
-        const int lh = i - 1;
-        if (lh >= 0 && lh < L) {   // h of block lh from this XCD
-            const uint32_t step = seq0 + 1 + lh;
-            const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(
-                sa.hb + (long)(step & 3) * f + (long)xcc * FX, 0, FX * 4, 0x00020000);
-            u32x4 v[2 * KHW];
-            dead |= !sk_poll<2 * KHW, 2 * KHW, POL_INTRA>(hrs, hoff, hvalid, v, stag(step), dead);
+        const int lh = i - 1, ly = i - 3;
+        const bool dx = i + 1 < L, dh = lh >= 0 && lh < L, dy = pw == 1 && ly >= 0 && ly < L;
+        const uint32_t hstep = seq0 + 1 + lh;
+        const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(
+            sa.hb + (long)(hstep & 3) * f + (long)xcc * FX, 0, FX * 4, 0x00020000);
+        const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
+            sa.pb + (long)(ly >= 0 ? ly : 0) * SX * d + yrow0, 0, ((SX - 1) * d + DJ / 8) * 8, 0x00020000);
+        u32x4 hv[2 * KHW], pv[SX];
+        if (dx)
+            issue_input(i + 1);
+        if (dh && !dead)
+            sk_poll_issue<2 * KHW, POL_INTRA>(hrs, hoff, hvalid, hv);
+        if (dy && !dead)
+            sk_poll_issue<SX, POL_CROSS>(prs, poff, yl ? 0xFFu : 0u, pv);
+        if (dx)
+            finish_input(i + 1);
+        if (dh) {   // h of block lh from this XCD
+            if (!dead)
+                dead = !sk_poll_finish<2 * KHW, 2 * KHW, POL_INTRA>(hrs, hoff, hvalid, hv, stag(hstep));
             const int par = lh & 1;
 #pragma unroll
             for (int kk = 0; kk < KHW; ++kk) {
                 const int w = pt + SPT * kk;
-                sk_stage_h<HS>(m.hs + par * 4 * HS, m.hcx + par * HS, v + 2 * kk, w < FX / 8, w);
+                sk_stage_h<HS>(m.hs + par * 4 * HS, m.hcx + par * HS, hv + 2 * kk, w < FX / 8, w);
             }
             dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
             if (dead && lane == 0)
                 atomicOr(&ctl[L_ERR], 2u);
         }
-        const int ly = i - 3;
-        if (pw == 1 && ly >= 0 && ly < L) {   // the eight partials of this workgroup's rows, in XCD order
-            const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
-                sa.pb + (long)ly * SX * d + yrow0, 0, ((SX - 1) * d + DJ / 8) * 8, 0x00020000);
-            u32x4 v[SX];
-            dead |= !sk_poll<SX, 0, POL_CROSS>(prs, poff, yl ? 0xFFu : 0u, v, ltag32(seq0 + 1 + ly), dead);
+        if (dy) {   // the eight partials of this workgroup's rows, in XCD order
+            if (!dead)
+                dead = !sk_poll_finish<SX, 0, POL_CROSS>(prs, poff, yl ? 0xFFu : 0u, pv, ltag32(seq0 + 1 + ly));
             float y0 = 0.0f, y1 = 0.0f;
 #pragma unroll
             for (int xx = 0; xx < SX; ++xx) {
-                y0 += __uint_as_float(v[xx].x);
-                y1 += __uint_as_float(v[xx].z);
+                y0 += __uint_as_float(pv[xx].x);
+                y1 += __uint_as_float(pv[xx].z);
             }
             if (yl)
                 reinterpret_cast<uint32_t*>(sa.y + (long)ly * d + yrow0)[lane] = f2h(y0) | (f2h(y1) << 16);
@@ -321,7 +360,7 @@ __device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, c
 }
 
 template <int JG, int KM, int JD, int NDN>
-__global__ void __launch_bounds__(STHREADS) layers_kernel(LayersArgs sa) {
+__global__ void __launch_bounds__(LTHREADS) layers_kernel(LayersArgs sa) {
     extern __shared__ uint4 smem[];
     char* lds = reinterpret_cast<char*>(smem);
     const int tid = threadIdx.x, lane = tid & 63;
@@ -345,8 +384,21 @@ __global__ void __launch_bounds__(STHREADS) layers_kernel(LayersArgs sa) {
                       reinterpret_cast<float*>(lds + sa.o_t), reinterpret_cast<uint4*>(lds + sa.o_hs),
                       reinterpret_cast<float2*>(lds + sa.o_hcx), lds + sa.o_meta};
         LKArgs* ka = (LKArgs*)__builtin_amdgcn_kernarg_segment_ptr();
-        if (wave < SCW)
-            sl_compute_role<JG, KM, JD, NDN>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+        if (wave < sa.n_gu)
+            sl_gu_role<JG, KM>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+        else if (wave < LCW) {
+            const int n = ka->dn_n[wave];
+            if (n == 1)
+                sl_dn_role<JD, 1>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+            else if (n == 2 && NDN >= 2)
+                sl_dn_role<JD, (NDN >= 2 ? 2 : 1)>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+            else if (n == 3 && NDN >= 3)
+                sl_dn_role<JD, (NDN >= 3 ? 3 : 1)>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+            else if (n == 4 && NDN >= 4)
+                sl_dn_role<JD, (NDN >= 4 ? 4 : 1)>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+            else
+                sl_idle_role(sa.L);
+        }
         else
             sl_poll_role<8 * JG, 8 * JD>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
     } else if (tid == 0) {
@@ -383,29 +435,30 @@ int layers_cu_count() {
 
 struct LayersPlan {
     int jg, km, jd, ndn;
-    int gu_item[SCW], dn_lo[SCW], dn_n[SCW];
+    int n_gu, dn_lo[LCW], dn_n[LCW];
     int o_xs, o_cx, o_t, o_hs, o_hcx, o_meta, meta_bytes;
     size_t lds;
     bool ok;
 };
 
-// Wave plan: gate/up wave-item k on compute wave k; then the down items, one
-// at a time, to the SIMD with the least dequant work (a gate/up item weighs
-// 16 d / f down items: 8 rows of 2 d weights against 8 rows of f/8; a polling
-// wave weighs one), on its compute wave with the fewest items below the
-// register limit; each wave's items are then numbered consecutively.
+// Wave plan: gate/up wave-item k on compute wave k; the down items go one at
+// a time to the SIMD with the least dequant work (waves w and w + 4 share a
+// SIMD; a gate/up item weighs 12 d / f down items, which is about what one
+// 8-row item of 2 d two-bit weights costs against 8 rows of f/8 four-bit
+// weights with their unpack; a polling wave weighs one), on its down wave
+// with the fewest items below the register limit; each wave's items are then
+// numbered consecutively.
 void plan_waves(LayersPlan& p, int gu_items, int dn_items, int d, int f) {
-    const double rho = 16.0 * d / f;
-    double load[4] = {0.0, 0.0, 1.0, 1.0};                      // SIMDs of polling waves 6 and 7
-    int cnt[SCW] = {};
-    for (int w = 0; w < SCW; ++w) {
-        p.gu_item[w] = w < gu_items ? w : -1;
-        if (w < gu_items)
-            load[w & 3] += rho;
-    }
+    const double rho = 12.0 * d / f;
+    double load[4] = {0.0, 0.0, 0.0, 0.0};
+    load[LCW & 3] += 1.0;                                       // the polling waves
+    load[(LCW + 1) & 3] += 1.0;
+    int cnt[LCW] = {};
+    p.n_gu = gu_items;
+    for (int w = 0; w < gu_items; ++w) load[w & 3] += rho;
     for (int it = 0; it < dn_items; ++it) {
         int best = -1;
-        for (int w = 0; w < SCW; ++w) {
+        for (int w = gu_items; w < LCW; ++w) {
             if (cnt[w] >= p.ndn)
                 continue;
             if (best < 0 || load[w & 3] < load[best & 3] ||
@@ -420,7 +473,7 @@ void plan_waves(LayersPlan& p, int gu_items, int dn_items, int d, int f) {
         load[best & 3] += 1.0;
     }
     int lo = 0;
-    for (int w = 0; w < SCW; ++w) {
+    for (int w = 0; w < LCW; ++w) {
         p.dn_lo[w] = lo;
         p.dn_n[w] = cnt[w];
         lo += cnt[w];
@@ -435,7 +488,7 @@ LayersPlan plan_layers(int M, int d, int f, int g, int r) {
     if (f % SGRID != 0 || (f / SX) % 32 != 0 || d % 512 != 0 || d % g != 0 || f % g != 0)
         return p;
     const int RG = f / SGRID, UG = d / 64, ng = d / g, UF = f / SX / 32, DJ = d / SB;
-    if ((RG + 7) / 8 > SCW || ng % 4 != 0 || DJ % 16 != 0 || DJ / 16 > 64)
+    if ((RG + 7) / 8 > LGU_MAX || ng % 4 != 0 || DJ % 16 != 0 || DJ / 16 > 64)
         return p;
     if (r != 0 && r != 8 && r != 16 && r != 32)
         return p;
@@ -449,7 +502,7 @@ LayersPlan plan_layers(int M, int d, int f, int g, int r) {
     if (p.jg == 5 && p.km == 2 && p.jd == 5)
         p.ndn = 3;
     else if (p.jg == 8 && p.km == 2 && p.jd == 6)
-        p.ndn = 3;
+        p.ndn = 4;
     else if (p.jg == 1 && p.km == 1 && p.jd == 1)
         p.ndn = 1;
     else
@@ -467,8 +520,8 @@ LayersPlan plan_layers(int M, int d, int f, int g, int r) {
     p.o_t = take((size_t)2 * (2 * r + 1) * 4);
     p.o_hs = take((size_t)2 * p.jd * 8 * 4 * 16);   // chunk stride 8 JD >= UF units
     p.o_hcx = take((size_t)2 * p.jd * 8 * 8);
-    p.meta_bytes = 2 * 8 * ng * 4;
-    p.o_meta = take((size_t)SCW * p.meta_bytes);
+    p.meta_bytes = 2 * 8 * ng * 4 + 32 * r;      // metadata, then LoRA-B rows
+    p.o_meta = take((size_t)LGU_MAX * p.meta_bytes);
     p.lds = o;
     p.ok = p.lds <= 64 * 1024;
     return p;
@@ -510,21 +563,21 @@ hipError_t launch_layers(const StackLayerDesc* layers, int L, int d, int f, int 
     a.hb = reinterpret_cast<uint32_t*>(base + 1024 + tb_bytes(r));
     a.pb = reinterpret_cast<unsigned long long*>(base + 1024 + tb_bytes(r) +
                                                  (((size_t)4 * f * 4 + 255) & ~(size_t)255));
-    for (int w = 0; w < SCW; ++w) {
-        a.gu_item[w] = p.gu_item[w];
+    a.n_gu = p.n_gu;
+    for (int w = 0; w < LCW; ++w) {
         a.dn_lo[w] = p.dn_lo[w];
         a.dn_n[w] = p.dn_n[w];
     }
     a.o_xs = p.o_xs; a.o_cx = p.o_cx; a.o_t = p.o_t; a.o_hs = p.o_hs; a.o_hcx = p.o_hcx;
     a.o_meta = p.o_meta; a.meta_bytes = p.meta_bytes;
     auto run = [&](auto kernel) -> hipError_t {
-        kernel<<<SGRID, STHREADS, p.lds, st>>>(a);
+        kernel<<<SGRID, LTHREADS, p.lds, st>>>(a);
         return hipGetLastError();
     };
     if (p.jg == 5)
         return run(layers_kernel<5, 2, 5, 3>);
     if (p.jg == 8)
-        return run(layers_kernel<8, 2, 6, 3>);
+        return run(layers_kernel<8, 2, 6, 4>);
     return run(layers_kernel<1, 1, 1, 1>);
 }
 

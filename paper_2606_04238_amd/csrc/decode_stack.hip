@@ -239,7 +239,7 @@ __device__ __forceinline__ void sk_compute_role(const StackArgs& sa, KArgs* ka, 
             ga.g = g;
             fgu_meta_to_lds(gi, ga, wmeta, lane);
             sk_gu_accumulate(gi, m.xs, m.cxg, g, reinterpret_cast<const uint32_t*>(wmeta), lane);
-            sk_gu_finish(gi, m.ts, r, sk_layer(ka, i).lora_scale, sa.hb, ti, lane);
+            sk_gu_finish(gi, m.ts, r, sk_layer(ka, i).lora_scale, sa.hb, ti, lane, wmeta + 4 * (d / g));
         }
         sk_order();
         if (i + 1 < L) {
@@ -561,7 +561,7 @@ StackPlan plan_stack(int M, int d, int f, int g, int r) {
     p.o_a = take((size_t)2 * r * DJ * 2 + 16);
     p.o_y = take((size_t)DJ * 2);
     p.o_xn = take((size_t)DJ * 2);
-    p.meta_bytes = 2 * 8 * ng * 4;
+    p.meta_bytes = 2 * 8 * ng * 4 + 32 * r;      // metadata, then LoRA-B rows
     p.o_meta = take((size_t)SCW * p.meta_bytes);
     p.lds = o;
     p.ok = p.lds <= 64 * 1024;

@@ -62,27 +62,49 @@ struct StackLayer {
 // in `valid`) until each shows `tag`: in the high half of every 32-bit word
 // (k < K64), or in the high word of both 64-bit halves (k >= K64).  Loads of
 // one round go out together; only words still pending are read again.
+// sk_poll_issue sends the first round and sk_poll_finish checks it and polls
+// on, so several polls can have their first round in flight at once.
+template <int K, int POL>
+__device__ __forceinline__ void sk_poll_issue(__amdgpu_buffer_rsrc_t rs, const int (&off)[K], uint32_t valid,
+                                              u32x4 (&v)[K]) {
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+        if (valid & (1u << k)) v[k] = __builtin_amdgcn_raw_buffer_load_b128(rs, off[k], 0, POL);
+}
+
+template <int K, int K64>
+__device__ __forceinline__ uint32_t sk_poll_check(const u32x4 (&v)[K], uint32_t pending, uint32_t tag) {
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        if (pending & (1u << k)) {
+            const bool ok = k >= K64 ? (v[k].y == tag && v[k].w == tag)
+                                     : ((v[k].x >> 16) == tag && (v[k].y >> 16) == tag &&
+                                        (v[k].z >> 16) == tag && (v[k].w >> 16) == tag);
+            if (ok) pending &= ~(1u << k);
+        }
+    }
+    return pending;
+}
+
+template <int K, int K64, int POL>
+__device__ __forceinline__ bool sk_poll_finish(__amdgpu_buffer_rsrc_t rs, const int (&off)[K], uint32_t valid,
+                                               u32x4 (&v)[K], uint32_t tag) {
+    uint32_t pending = sk_poll_check<K, K64>(v, valid, tag);
+    for (unsigned it = 0; pending != 0u && it < kStackSpin; ++it) {
+        __builtin_amdgcn_s_sleep(1);
+        sk_poll_issue<K, POL>(rs, off, pending, v);
+        pending = sk_poll_check<K, K64>(v, pending, tag);
+    }
+    return pending == 0u;
+}
+
 template <int K, int K64, int POL>
 __device__ __forceinline__ bool sk_poll(__amdgpu_buffer_rsrc_t rs, const int (&off)[K], uint32_t valid,
                                         u32x4 (&v)[K], uint32_t tag, bool skip) {
-    uint32_t pending = skip ? 0u : valid;
-    for (unsigned it = 0; pending != 0u && it < kStackSpin; ++it) {
-#pragma unroll
-        for (int k = 0; k < K; ++k)
-            if (pending & (1u << k)) v[k] = __builtin_amdgcn_raw_buffer_load_b128(rs, off[k], 0, POL);
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            if (pending & (1u << k)) {
-                const bool ok = k >= K64 ? (v[k].y == tag && v[k].w == tag)
-                                         : ((v[k].x >> 16) == tag && (v[k].y >> 16) == tag &&
-                                            (v[k].z >> 16) == tag && (v[k].w >> 16) == tag);
-                if (ok) pending &= ~(1u << k);
-            }
-        }
-        if (pending != 0u)
-            __builtin_amdgcn_s_sleep(1);
-    }
-    return pending == 0u;
+    if (skip)
+        return false;
+    sk_poll_issue<K, POL>(rs, off, valid, v);
+    return sk_poll_finish<K, K64, POL>(rs, off, valid, v, tag);
 }
 
 // One staging word of h: 8 binary16 values h[8w .. 8w+8) of this XCD's
@@ -149,21 +171,22 @@ __device__ __forceinline__ void sk_gu_load(FGuItem<1, 8, JG, KM>& it, const Stac
         it.qg[i] = load_stream(cg + 8 * i);
         it.qu[i] = load_stream(cu + 8 * i);
     }
-    if (r > 0) {
-        const int CPL = r / 8;                  // ranks per lane: 1, 2 or 4
-        const long off = rowc * r + s * CPL;
-        if (CPL == 1) {
-            it.bg[0] = w.Bg[off];
-            it.bu[0] = w.Bu[off];
-        } else if (CPL == 2) {
-            it.bg[0] = *reinterpret_cast<const uint32_t*>(w.Bg + off);
-            it.bu[0] = *reinterpret_cast<const uint32_t*>(w.Bu + off);
-        } else {
-            const uint2 vg = *reinterpret_cast<const uint2*>(w.Bg + off);
-            const uint2 vu = *reinterpret_cast<const uint2*>(w.Bu + off);
-            it.bg[0] = vg.x; it.bg[1] = vg.y;
-            it.bu[0] = vu.x; it.bu[1] = vu.y;
-        }
+    // LoRA-B rows of the item, B_g then B_u: each matrix's 8 rows are r
+    // contiguous 16-byte chunks, and lane c < 2r loads chunk c with one
+    // branch-free load (a chunk past the matrix, and every lane at rank 0,
+    // re-reads a valid chunk).  sk_gu_finish parks them in LDS.  Loads of
+    // different widths under a rank-dependent branch would make the compiler
+    // wait for every outstanding load where the branches merge, which turns
+    // the next layer's prefetch into a synchronous load.
+    {
+        const int c = lane < 2 * r ? lane : 0;
+        const bool up = c >= r && r > 0;
+        const int cc = up ? c - r : c;
+        const bool in = r > 0 && row0 + (8 * cc) / r < f;
+        const uint4* base = r > 0 ? reinterpret_cast<const uint4*>(up ? w.Bu : w.Bg) + (long)row0 * r / 8
+                                  : reinterpret_cast<const uint4*>(w.cg);
+        const uint4 b = load_stream(base + (in ? cc : 0));
+        it.bg[0] = b.x; it.bg[1] = b.y; it.bu[0] = b.z; it.bu[1] = b.w;
     }
     it.G[0] = it.U[0] = 0.0f;
 }
@@ -218,27 +241,28 @@ __device__ __forceinline__ void sk_gu_accumulate(FGuItem<1, 8, JG, KM>& it, cons
     }
 }
 
-// LoRA-B on the lane's ranks (t unscaled: A x), the row reduction over 8
-// lanes, the norm's 1/rms (G and U are linear in the block input x * inv)
+// LoRA-B on the lane's ranks (t unscaled: A x; the item's B rows go through
+// the wave's LDS area wb, 32 r bytes), the row reduction over 8 lanes, the norm's 1/rms (G and U are linear in the block input x * inv)
 // and h = SiLU(G) * U, published as tagged words to the XCD-local h buffer.
 template <int JG, int KM>
 __device__ __forceinline__ void sk_gu_finish(FGuItem<1, 8, JG, KM>& it, const float* ts, int r,
-                                             float ls, uint32_t* hb, uint32_t tag, int lane) {
+                                             float ls, uint32_t* hb, uint32_t tag, int lane, uint4* wb) {
     const int s = lane & 7;
     const float inv = ts[2 * r];           // 1 / rms of the stream: the block input is x * inv
     float G = it.G[0], U = it.U[0];
     if (r > 0) {
+        // the item's LoRA-B rows into the wave's LDS area: [B_g rows | B_u rows], r halves per row
+        if (lane < 2 * r)
+            wb[lane] = make_uint4(it.bg[0], it.bg[1], it.bu[0], it.bu[1]);
+        const uint16_t* bh = reinterpret_cast<const uint16_t*>(wb) + (lane >> 3) * r;
         const int CPL = r / 8;
-        uint32_t b0 = it.bg[0], b1 = it.bg[1], c0 = it.bu[0], c1 = it.bu[1];
-        pin(b0); pin(b1); pin(c0); pin(c1);
-        const uint32_t bgw[2] = {b0, b1}, buw[2] = {c0, c1};
         float lg = 0.0f, lu = 0.0f;
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             if (c < CPL) {
                 const int rc = s * CPL + c;
-                lg += h2f(bgw[c >> 1] >> (16 * (c & 1))) * ts[rc];
-                lu += h2f(buw[c >> 1] >> (16 * (c & 1))) * ts[r + rc];
+                lg += h2f(bh[rc]) * ts[rc];
+                lu += h2f(bh[8 * r + rc]) * ts[r + rc];
             }
         }
         G += ls * lg;
