@@ -319,6 +319,11 @@ __device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, c
         const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
             sa.pb + (long)(ly >= 0 ? ly : 0) * SX * d + yrow0, 0, ((SX - 1) * d + DJ / 8) * 8, 0x00020000);
         u32x4 hv[2 * KHW], pv[SX];
+        // At the default priority the arithmetic waves on this SIMD would hold
+        // the issue slots until their items are done and delay every
+        // hand-off; the loads of the iteration and the staging of the next
+        // input therefore run at a raised priority, the waits at the default.
+        __builtin_amdgcn_s_setprio(3);
         if (dx)
             issue_input(i + 1);
         if (dh && !dead)
@@ -327,6 +332,7 @@ __device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, c
             sk_poll_issue<SX, POL_CROSS>(prs, poff, yl ? 0xFFu : 0u, pv);
         if (dx)
             finish_input(i + 1);
+        __builtin_amdgcn_s_setprio(0);
         if (dh) {   // h of block lh from this XCD
             if (!dead)
                 dead = !sk_poll_finish<2 * KHW, 2 * KHW, POL_INTRA>(hrs, hoff, hvalid, hv, stag(hstep));
