@@ -1,13 +1,11 @@
 #!/usr/bin/env python3
 """Benchmark of the W4/W2-GateUp decode MLP on one MI355X.
 
-A step is one pass over the layer stack of the Qwen3-4B-shaped workload
-(d=2560, f=9728, 2-bit gate/up and 4-bit down at group 128, LoRA rank 16,
-M=1 token, 36 independently seeded layers).  The layers sit on a residual
-stream as the MLP sub-blocks of a decoder (x_{l+1} = x_l + block_l(
-RMSNorm(x_l)), attention left out), so each layer's input depends on the
-previous layer's output; the stack runs through qmlp_forward_stack (one
-persistent launch at this shape).  Inputs are
+A step is one pass over the 36 independently seeded MLP blocks of the
+Qwen3-4B-shaped workload (d=2560, f=9728, 2-bit gate/up and 4-bit down at
+group 128, LoRA rank 16, M=1 token, every block with its own weights and
+its own input x ~ N(0,1) in binary16), run back to back through
+qmlp_forward_layers (one persistent launch at this shape).  Inputs are
 packed and resident in HBM before the timed region.  Prints one JSON line:
 
   value    = achieved HBM GB/s = L * B(M) / t_step, where B(M) are the
@@ -20,7 +18,12 @@ packed and resident in HBM before the timed region.  Prints one JSON line:
              rocprofv3 byte counters summarized under profiles/, reported
              only while the HIP sources match the ones profiled;
   cpu_baseline = the fp64 oracle timed on a bounded sample of the same
-             stack on this host (reported baseline only).
+             blocks on this host (reported baseline only).
+
+For context the same blocks are also timed as a decoder stack on a
+residual stream (x_{l+1} = x_l + block_l(RMSNorm(x_l)), each block's input
+depending on the previous block's output, qmlp_forward_stack) and one
+qmlp_forward launch per block.
 """
 from __future__ import annotations
 
@@ -58,7 +61,11 @@ class Stack:
         import paper_2606_04238_amd as q
         self.st = q.Stack(mlps)
         self.Y = torch.empty((len(mlps), cfg.M, cfg.d), dtype=ys[0].dtype, device="cuda")
-        self.sws = q.stack_workspace(self.st, cfg.M, ys[0].dtype)
+        self.sws = q.stack_workspace(self.st, cfg.M, ys[0].dtype) if cfg.M > 0 and not cfg.bf16 else None
+        self.lay = q.Layers(mlps)
+        self.X = torch.stack(xs)                       # [L][M][d]: every block's own input
+        self.YL = torch.empty_like(self.X)
+        self.lws = q.layers_workspace(self.lay, cfg.M, ys[0].dtype)
 
 
 def _gen_layer(cfg, i, seed):
@@ -98,8 +105,15 @@ def build_stack(cfg: wl.Config, seed: int = 0, layers: int | None = None, thread
     return Stack(cfg, mlps, xs, ys, ws)
 
 
+def run_blocks_once(stack: Stack):
+    """One step: every block on its own input, back to back (qmlp_forward_layers)."""
+    import paper_2606_04238_amd as q
+    q.forward_layers(stack.lay, stack.X, y=stack.YL, ws=stack.lws)
+    return stack.YL
+
+
 def run_stack_once(stack: Stack):
-    """One step: the whole stack on the residual stream from layer 0's x."""
+    """The blocks as a decoder stack on the residual stream from layer 0's x."""
     import paper_2606_04238_amd as q
     q.forward_stack(stack.st, stack.xs[0], y=stack.Y, ws=stack.sws)
     return stack.Y
@@ -131,11 +145,19 @@ def capture(fn):
 
 
 # --------------------------------------------------------------------- timing
-def time_passes(fn, steps: int, warmup: int):
-    """Per-pass durations (ms) with HIP events on the current stream."""
+def time_passes(fn, steps: int, warmup: int, min_warm_s: float = 0.25):
+    """Per-pass durations (ms) with HIP events on the current stream.  The
+    untimed warmup runs at least `warmup` passes and at least `min_warm_s`
+    seconds of passes, so that the GPU has left its idle clocks before the
+    timed region (tens of milliseconds of one step are not enough)."""
     import torch
-    for _ in range(warmup):
+    t_end = time.perf_counter() + min_warm_s
+    done = 0
+    while done < warmup or time.perf_counter() < t_end:
         fn()
+        done += 1
+        if done % 8 == 0:
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
     st = torch.cuda.current_stream()
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
@@ -213,6 +235,24 @@ def cpu_baseline(cfg: wl.Config, seed: int, budget_s: float = 12.0, max_layers: 
             "sample": "oracle forward (fp64, one thread) over layers 0..%d of the %d-layer stack, "
                       "%.2f s; quantization untimed; us per MLP step %.0f" % (n - 1, cfg.L, total_t,
                                                                             total_t / n * 1e6)}
+
+
+def parity_blocks(stack: Stack, seed: int, sample=(0,)):
+    """Max-rel error of the sampled blocks' outputs of the last timed step
+    against the oracle on each block's own input."""
+    import torch
+    import oracle as orc
+    cfg = stack.cfg
+    Y = stack.YL.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    out = {}
+    for i in sample:
+        lay = wl.layer(cfg, i, seed)
+        qg, qu, qd = (orc.quantize(lay.W_gate, 2, cfg.g), orc.quantize(lay.W_up, 2, cfg.g),
+                      orc.quantize(lay.W_down, 4, cfg.g))
+        y_ref = orc.forward(qg, qu, qd, lay.A_gate, lay.B_gate, lay.A_up, lay.B_up, lay.x,
+                            lora_scale=cfg.lora_scale, bf16=cfg.bf16)
+        out[i] = orc.max_rel_err(orc.act_to_f64(Y[i], cfg.bf16), y_ref)
+    return out
 
 
 def parity_sampled(stack: Stack, seed: int, sample=(0,)):
@@ -324,6 +364,8 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--mode", default="graph", choices=["graph", "eager"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--min-warm-s", type=float, default=0.25,
+                    help="untimed warmup lasts at least this long (and at least --warmup steps)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="after timing, run one copy-like elementwise kernel over this many MiB "
                          "(read N, write N) as the reference dispatch for HBM byte counters")
@@ -347,46 +389,62 @@ def main(argv=None):
     stack = build_stack(cfg, args.seed)
     L = cfg.L
     B = cfg.alg_bytes()
-    launches = q.stack_launches(stack.st, cfg.M, stack.Y.dtype)
+    dt = stack.Y.dtype
+    launches = q.layers_launches(stack.lay, cfg.M, dt)
     persistent = launches < L
 
-    # the timed step: the whole stack on the residual stream
-    eager_ms, _ = time_passes(lambda: run_stack_once(stack), args.steps, args.warmup)
+    # the timed step: every block on its own input, back to back
+    eager_ms, _ = time_passes(lambda: run_blocks_once(stack), args.steps, args.warmup, args.min_warm_s)
     graph_ms = None
     if args.mode == "graph":
-        g = capture(lambda: run_stack_once(stack))
-        graph_ms, wall = time_passes(g.replay, args.steps, args.warmup)
+        g = capture(lambda: run_blocks_once(stack))
+        graph_ms, wall = time_passes(g.replay, args.steps, args.warmup, args.min_warm_s)
     head = graph_ms if graph_ms is not None else eager_ms
     t_step = sum(head) / len(head)          # the K timed steps, back to back
     gbs = L * B / (t_step * 1e-3) / 1e9
     us_layer = t_step * 1e3 / L
-    if stack.sws is not None and persistent:
-        err_bits = q.stack_errors(stack.st, stack.sws, cfg.M, stack.Y.dtype)
+    if persistent:
+        err_bits = q.layers_errors(stack.lws)
         if err_bits:
-            raise RuntimeError("stack kernel reported error bits %#x" % err_bits)
-    err = parity_sampled(stack, args.seed, sample=(0, L // 2, L - 1))
+            raise RuntimeError("layers kernel reported error bits %#x" % err_bits)
+    err = parity_blocks(stack, args.seed, sample=(0, L // 2, L - 1))
 
-    # context: the per-layer path (one qmlp_forward launch per layer), graph replay
+    # context: the same blocks as a decoder stack on the residual stream, and
+    # one qmlp_forward launch per block (graph replay)
+    context = {}
+    if stack.sws is not None:
+        gs = capture(lambda: run_stack_once(stack))
+        stack_ms, _ = time_passes(gs.replay, max(5, args.steps // 2), 2, args.min_warm_s)
+        context["dependent_stack_us_per_mlp_step"] = round(sum(stack_ms) / len(stack_ms) * 1e3 / L, 3)
+        context["dependent_stack_launches"] = q.stack_launches(stack.st, cfg.M, dt)
+        if q.stack_launches(stack.st, cfg.M, dt) < L:
+            err_bits = q.stack_errors(stack.st, stack.sws, cfg.M, dt)
+            if err_bits:
+                raise RuntimeError("stack kernel reported error bits %#x" % err_bits)
+        context["dependent_stack_parity_max_rel_err"] = {
+            str(k): float("%.3e" % v) for k, v in parity_sampled(stack, args.seed, sample=(0,)).items()}
     gl = capture(lambda: run_layers_once(stack))
-    layer_ms, _ = time_passes(gl.replay, max(5, args.steps // 2), 2)
+    layer_ms, _ = time_passes(gl.replay, max(5, args.steps // 2), 2, args.min_warm_s)
     per_layer_us = sum(layer_ms) / len(layer_ms) * 1e3 / L
+    context["per_layer_path_us_per_mlp_step"] = round(per_layer_us, 3)
 
     traffic = None
     if persistent:
         # the timed region holds K steps of `launches` back-to-back launches
-        # of the stack kernel on the replay stream, so its events give the
+        # of the layers kernel on the replay stream, so its events give the
         # average launch duration (inter-launch gaps included)
-        dom_name = "stack_kernel"
+        dom_name = "layers_kernel"
         dom_us = t_step * 1e3 / launches
         dom_b = L * B / launches
-        kernel_us = {"stack_kernel_avg_launch": round(dom_us, 3), "launches_per_step": launches}
-        traffic = read_traffic(os.path.join(ROOT, "profiles", "stack_kernel_%s.md" % cfg.name),
+        kernel_us = {"layers_kernel_avg_launch": round(dom_us, 3), "launches_per_step": launches}
+        traffic = read_traffic(os.path.join(ROOT, "profiles", "layers_kernel_%s.md" % cfg.name),
                                dom_name)
     else:
         fused, k1_us, k2_us = kernel_durations(stack)
         if fused:
+            # the timed step is L launches of the fused kernel back to back
             dom_name, dom_b = "fused_layer_kernel", B
-            dom_us = per_layer_us
+            dom_us = us_layer
             kernel_us = {"fused_layer_event_bracketed": round(k1_us, 3)}
         else:
             gu_b, dn_b = kernel_bytes(cfg)
@@ -409,20 +467,21 @@ def main(argv=None):
         "dtype": "f16",
         "data": "synthetic",
         "config": {
-            "workload": "%s decode MLP stack: M=%d, d=%d, f=%d, group %d, LoRA rank %d, %d layers "
-                        "on a residual stream (RMSNorm before each block)" % (cfg.name, cfg.M, cfg.d, cfg.f, cfg.g, cfg.r, L),
+            "workload": "%s decode MLP: M=%d, d=%d, f=%d, group %d, LoRA rank %d, %d independently "
+                        "seeded blocks (own weights, own input) run back to back"
+                        % (cfg.name, cfg.M, cfg.d, cfg.f, cfg.g, cfg.r, L),
             "us_per_mlp_step": round(us_layer, 3),
             "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
             "alg_bytes_per_mlp_step": B,
             "mode": "hip_graph" if graph_ms is not None else "eager",
-            "path": "persistent stack kernel" if persistent else "per-layer forward",
+            "path": "persistent layers kernel" if persistent else "per-block forward",
             "eager_us_per_mlp_step": round(statistics.median(eager_ms) * 1e3 / L, 3),
-            "per_layer_path_us_per_mlp_step": round(per_layer_us, 3),
             "median_ms_per_step": round(statistics.median(head), 4),
             "p10_p90_ms_per_step": [round(float(np.percentile(head, 10)), 4),
                                     round(float(np.percentile(head, 90)), 4)],
             "kernel_us": kernel_us,
             "parity_max_rel_err": {str(k): float("%.3e" % v) for k, v in err.items()},
+            **context,
         },
         "roofline": {
             "bound": "hbm",

@@ -9,21 +9,24 @@
 // software pipeline: the work of one iteration is
 //   * the gate/up rows of block i (h_i published inside the XCD),
 //   * the partial down sums of block i-2 (published to the other XCDs),
-// while the two polling waves stage block i+1's input, gather h_{i-1} of the
-// XCD and sum the eight cross-XCD partials of block i-3 into y_{i-3}.  Every
-// hand-off is therefore consumed one iteration after it was published, and
-// one barrier per iteration separates producers and consumers of the LDS
-// buffers (double-buffered by parity).  Decode is bound by loading weights
-// (Sec. 3.3, Sec. 5): each register set is reloaded with the next block's
-// weights right after its last use, so the stream never waits for a hand-off.
+// while the two polling waves stage block i+1's input and gather h_{i-1} of
+// the XCD.  Every hand-off inside the loop is consumed one iteration after it
+// was published, and one barrier per iteration separates producers and
+// consumers of the LDS buffers (double-buffered by parity).  The eight
+// cross-XCD partials of every block's y have a slot per block and are summed
+// after the last iteration, so inside the loop no XCD waits for another.
+// Decode is bound by loading weights (Sec. 3.3, Sec. 5): every register set
+// of weights is requested well before its arithmetic (gate/up: right after
+// the previous block's; down: double-buffered where the registers allow), so
+// the stream never waits for a hand-off.
 //
 // Work split (8 XCDs x 32 compute units, one 512-thread workgroup each), per
 // block as in the persistent stack kernel: XCD x owns the slice
 // F_x = [x f/8, (x+1) f/8) of the intermediate dimension; its workgroup j
 // computes gate/up rows F_x,j and the partial down product over F_x for the
 // output rows D_j = [j d/32, (j+1) d/32).  Workgroup j of XCD x sums the
-// eight partials of the rows D_j[x DJ/8, (x+1) DJ/8) (DJ = d/32) in XCD order
-// and writes them.  The LoRA-A products A x_l of all blocks (fp32) are
+// eight partials of the rows D_j[x DJ/8, (x+1) DJ/8) (DJ = d/32) of every
+// block in XCD order and writes them.  The LoRA-A products A x_l of all blocks (fp32) are
 // computed once at the start, one dot product per polling wave, and read
 // back as tagged words.
 //
@@ -160,33 +163,36 @@ __device__ __forceinline__ void sl_gu_role(const LayersArgs& sa, LKArgs* ka, con
         __syncthreads();                                        // one barrier per iteration
     }
     compute(L - 1);
-    for (int i = L - 1; i < L + 3; ++i) __syncthreads();       // iterations L-1 .. L+2
+    for (int i = L - 1; i < L + 2; ++i) __syncthreads();       // iterations L-1 .. L+1
 }
 
 // A down wave with N down wave-items: the items of block i - 2 in iteration
-// i, each item's registers reloaded with block i-1's codes right after its
-// arithmetic (the last block peeled off, as for the gate/up waves).
-template <int JD, int N>
+// i.  With DB the registers are double-buffered: block l+1's codes are
+// requested when block l's arithmetic starts, a full iteration before they
+// are used (the loop is unrolled by two so each buffer is a fixed register
+// set, and the tail is peeled, so the loop issues its loads without a
+// condition).  Without DB each item's registers are reloaded right after the
+// arithmetic.
+template <int JD, int N, bool DB>
 __device__ __forceinline__ void sl_dn_role(const LayersArgs& sa, LKArgs* ka, const SlLds& m, int xcc, int j,
                                            uint32_t seq0, int wave, int lane) {
     const int d = sa.d, f = sa.f, g = sa.g, L = sa.L;
     const int UF = f / SX / 32, DJ = d / SB;
     constexpr int HS = 8 * JD;
     const int o = j * DJ + 8 * ka->dn_lo[wave] + (lane >> 3);  // output row of item 0 on this lane
-    SkDn<JD> di[N];
+    auto load = [&](SkDn<JD> (&dd)[N], int l) {
+        const StackLayer w = sk_layer(ka, l);
 #pragma unroll
-    for (int k = 0; k < N; ++k) sk_dn_load(di[k], sk_layer(ka, 0), o + 8 * k, xcc, f, g, lane);
-    __syncthreads();                                            // B0
-    __syncthreads();                                            // iteration 0
-    __syncthreads();                                            // iteration 1
-    // All items' arithmetic first, then their stores, then the reloads: a
-    // store counts in the same in-order counter as the loads, so a store
-    // between two items would make the second item wait for its completion.
-    auto items = [&](int l) {
+        for (int k = 0; k < N; ++k) sk_dn_load(dd[k], w, o + 8 * k, xcc, f, g, lane);
+    };
+    // All items' arithmetic first, then their stores: a store counts in the
+    // same in-order counter as the loads, so a store between two items would
+    // make the second item wait for its completion.
+    auto items = [&](SkDn<JD> (&dd)[N], int l) {
         float yv[N];
 #pragma unroll
         for (int k = 0; k < N; ++k)
-            yv[k] = sk_dn_compute<JD>(di[k], m.hs + (l & 1) * 4 * HS, m.hcx + (l & 1) * HS, UF, lane);
+            yv[k] = sk_dn_compute<JD>(dd[k], m.hs + (l & 1) * 4 * HS, m.hcx + (l & 1) * HS, UF, lane);
         const unsigned long long tg = (unsigned long long)ltag32(seq0 + 1 + l) << 32;
 #pragma unroll
         for (int k = 0; k < N; ++k)
@@ -194,21 +200,79 @@ __device__ __forceinline__ void sl_dn_role(const LayersArgs& sa, LKArgs* ka, con
                 st_cross64(sa.pb + ((long)l * SX + xcc) * d + o + 8 * k, (unsigned long long)__float_as_uint(yv[k]) | tg);
         sk_order();
     };
-    for (int l = 0; l + 1 < L; ++l) {                           // iteration l + 2
-        items(l);
-        const StackLayer wn = sk_layer(ka, l + 1);
-#pragma unroll
-        for (int k = 0; k < N; ++k) sk_dn_load(di[k], wn, o + 8 * k, xcc, f, g, lane);
+    SkDn<JD> da[N];
+    load(da, 0);
+    __syncthreads();                                            // B0
+    __syncthreads();                                            // iteration 0
+    __syncthreads();                                            // iteration 1
+    if constexpr (DB) {
+        SkDn<JD> db[N];
+        int l = 0;                                              // block l is in da
+        for (; l + 2 < L; l += 2) {                             // iterations l + 2, l + 3
+            load(db, l + 1);
+            items(da, l);
+            __syncthreads();
+            load(da, l + 2);
+            items(db, l + 1);
+            __syncthreads();
+        }
+        if (l + 2 == L) {
+            load(db, l + 1);
+            items(da, l);
+            __syncthreads();
+            items(db, l + 1);
+            __syncthreads();
+        } else {
+            items(da, l);
+            __syncthreads();
+        }
+    } else {
+        for (int l = 0; l + 1 < L; ++l) {                       // iteration l + 2
+            items(da, l);
+            load(da, l + 1);
+            __syncthreads();
+        }
+        items(da, L - 1);                                       // iteration L + 1
         __syncthreads();
     }
-    items(L - 1);                                               // iteration L + 1
-    __syncthreads();
-    __syncthreads();                                            // iteration L + 2
 }
 
 // A compute wave without work in this plan: the barriers only.
 __device__ __forceinline__ void sl_idle_role(int L) {
-    for (int i = 0; i < L + 4; ++i) __syncthreads();           // B0 and L + 3 iterations
+    for (int i = 0; i < L + 3; ++i) __syncthreads();           // B0 and L + 2 iterations
+}
+
+// After the iterations: every thread of the workgroup sums the eight
+// cross-XCD partials of two rows of this workgroup's share of y,
+// D_j[xcc DJ/8, (xcc+1) DJ/8), for one block, in XCD order; all blocks' sums
+// are polled together (the partials have one slot per block).  Until then
+// no XCD waits for another.
+__device__ __forceinline__ void sl_sum_y(const LayersArgs& sa, int xcc, int j, uint32_t seq0, int tid, int lane) {
+    const int d = sa.d, L = sa.L, DJ = d / SB, PR = DJ / 16;
+    const int yrow0 = j * DJ + xcc * (DJ / 8);
+    bool dead = false;
+    for (int t = tid; t < ((L * PR + 63) & ~63); t += LTHREADS) {   // whole waves per round
+        const bool live = t < L * PR;
+        const int ly = live ? t / PR : 0, pr = live ? t - ly * PR : 0;
+        const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
+            sa.pb + (long)ly * SX * d + yrow0, 0, ((SX - 1) * d + DJ / 8) * 8, 0x00020000);
+        int off[SX];
+#pragma unroll
+        for (int xx = 0; xx < SX; ++xx) off[xx] = 16 * pr + xx * d * 8;
+        u32x4 v[SX];
+        dead |= !sk_poll<SX, 0, POL_CROSS>(prs, off, live ? 0xFFu : 0u, v, ltag32(seq0 + 1 + ly), dead);
+        float y0 = 0.0f, y1 = 0.0f;
+#pragma unroll
+        for (int xx = 0; xx < SX; ++xx) {
+            y0 += __uint_as_float(v[xx].x);
+            y1 += __uint_as_float(v[xx].z);
+        }
+        if (live)
+            reinterpret_cast<uint32_t*>(sa.y + (long)ly * d + yrow0)[pr] = f2h(y0) | (f2h(y1) << 16);
+    }
+    dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
+    if (dead && lane == 0)
+        atomicOr(&sa.ctl[L_ERR], 4u);
 }
 
 // The polling waves: the LoRA-A products of every block (once), then per
@@ -218,7 +282,7 @@ template <int XS, int HS>
 __device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, const SlLds& m, int xcc, int j,
                                              uint32_t seq0, int wave, int lane) {
     const int d = sa.d, f = sa.f, r = sa.r, L = sa.L;
-    const int FX = f / SX, DJ = d / SB;
+    const int FX = f / SX;
     const int pw = wave - LCW, pt = pw * 64 + lane;
     unsigned* ctl = sa.ctl;
     bool dead = false;                                          // this wave gave up a wait
@@ -258,16 +322,9 @@ __device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, c
         for (int q = 0; q < 2; ++q) hoff[2 * kk + q] = 32 * pt + 32 * SPT * kk + 16 * q;
         if (pt + SPT * kk < FX / 8) hvalid |= 0x3u << (2 * kk);
     }
-    // the rows of y this workgroup sums: D_j[xcc DJ/8, (xcc+1) DJ/8), two per lane of wave 1
-    const int yrow0 = j * DJ + xcc * (DJ / 8);
-    int poff[SX];
-#pragma unroll
-    for (int xx = 0; xx < SX; ++xx) poff[xx] = 16 * lane + xx * d * 8;
-    const bool yl = pw == 1 && lane < DJ / 16;
-
     // Per iteration the first round of every load (the next block's input
-    // and LoRA-A products, h of the previous block, the partials of the
-    // block before that) goes out together; then each is resolved in turn.
+    // and LoRA-A products, h of the previous block) goes out together; then
+    // each is resolved in turn.
     uint4 xv[KXW][2];
     u32x4 tv[1];
     int toff[1] = {0};
@@ -310,15 +367,13 @@ __device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, c
     finish_input(0);
     __syncthreads();                                            // B0
 
-    for (int i = 0; i < L + 3; ++i) {
-        const int lh = i - 1, ly = i - 3;
-        const bool dx = i + 1 < L, dh = lh >= 0 && lh < L, dy = pw == 1 && ly >= 0 && ly < L;
+    for (int i = 0; i < L + 2; ++i) {
+        const int lh = i - 1;
+        const bool dx = i + 1 < L, dh = lh >= 0 && lh < L;
         const uint32_t hstep = seq0 + 1 + lh;
         const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(
             sa.hb + (long)(hstep & 3) * f + (long)xcc * FX, 0, FX * 4, 0x00020000);
-        const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
-            sa.pb + (long)(ly >= 0 ? ly : 0) * SX * d + yrow0, 0, ((SX - 1) * d + DJ / 8) * 8, 0x00020000);
-        u32x4 hv[2 * KHW], pv[SX];
+        u32x4 hv[2 * KHW];
         // At the default priority the arithmetic waves on this SIMD would hold
         // the issue slots until their items are done and delay every
         // hand-off; the loads of the iteration and the staging of the next
@@ -328,8 +383,6 @@ __device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, c
             issue_input(i + 1);
         if (dh && !dead)
             sk_poll_issue<2 * KHW, POL_INTRA>(hrs, hoff, hvalid, hv);
-        if (dy && !dead)
-            sk_poll_issue<SX, POL_CROSS>(prs, poff, yl ? 0xFFu : 0u, pv);
         if (dx)
             finish_input(i + 1);
         __builtin_amdgcn_s_setprio(0);
@@ -345,21 +398,6 @@ __device__ __forceinline__ void sl_poll_role(const LayersArgs& sa, LKArgs* ka, c
             dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
             if (dead && lane == 0)
                 atomicOr(&ctl[L_ERR], 2u);
-        }
-        if (dy) {   // the eight partials of this workgroup's rows, in XCD order
-            if (!dead)
-                dead = !sk_poll_finish<SX, 0, POL_CROSS>(prs, poff, yl ? 0xFFu : 0u, pv, ltag32(seq0 + 1 + ly));
-            float y0 = 0.0f, y1 = 0.0f;
-#pragma unroll
-            for (int xx = 0; xx < SX; ++xx) {
-                y0 += __uint_as_float(pv[xx].x);
-                y1 += __uint_as_float(pv[xx].z);
-            }
-            if (yl)
-                reinterpret_cast<uint32_t*>(sa.y + (long)ly * d + yrow0)[lane] = f2h(y0) | (f2h(y1) << 16);
-            dead = __builtin_amdgcn_readfirstlane(__any(dead) ? 1 : 0) != 0;
-            if (dead && lane == 0)
-                atomicOr(&ctl[L_ERR], 4u);
         }
         __syncthreads();
     }
@@ -395,18 +433,19 @@ __global__ void __launch_bounds__(LTHREADS) layers_kernel(LayersArgs sa) {
         else if (wave < LCW) {
             const int n = ka->dn_n[wave];
             if (n == 1)
-                sl_dn_role<JD, 1>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+                sl_dn_role<JD, 1, true>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
             else if (n == 2 && NDN >= 2)
-                sl_dn_role<JD, (NDN >= 2 ? 2 : 1)>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+                sl_dn_role<JD, (NDN >= 2 ? 2 : 1), true>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
             else if (n == 3 && NDN >= 3)
-                sl_dn_role<JD, (NDN >= 3 ? 3 : 1)>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+                sl_dn_role<JD, (NDN >= 3 ? 3 : 1), false>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
             else if (n == 4 && NDN >= 4)
-                sl_dn_role<JD, (NDN >= 4 ? 4 : 1)>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+                sl_dn_role<JD, (NDN >= 4 ? 4 : 1), false>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
             else
                 sl_idle_role(sa.L);
         }
         else
             sl_poll_role<8 * JG, 8 * JD>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
+        sl_sum_y(sa, (int)xcc, j, seq0, tid, lane);
     } else if (tid == 0) {
         atomicOr(&ctl[L_ERR], 8u);              // a workgroup without a place: results invalid
     }
@@ -449,9 +488,10 @@ struct LayersPlan {
 
 // Wave plan: gate/up wave-item k on compute wave k; the down items go one at
 // a time to the SIMD with the least dequant work (waves w and w + 4 share a
-// SIMD; a gate/up item weighs 12 d / f down items, which is about what one
-// 8-row item of 2 d two-bit weights costs against 8 rows of f/8 four-bit
-// weights with their unpack; a polling wave weighs one), on its down wave
+// SIMD; a gate/up item weighs 12 d / f down items -- 8 rows of 2 d two-bit
+// weights against 8 rows of f/8 four-bit weights, scaled so that at
+// d = 2560, f = 9728 the SIMD of two gate/up waves gets no down item, which
+// measured fastest; a polling wave weighs one), on its down wave
 // with the fewest items below the register limit; each wave's items are then
 // numbered consecutively.
 void plan_waves(LayersPlan& p, int gu_items, int dn_items, int d, int f) {
