@@ -20,15 +20,15 @@
 // the previous block's; down: double-buffered where the registers allow), so
 // the stream never waits for a hand-off.
 //
-// Work split (8 XCDs x 32 compute units, one 512-thread workgroup each), per
+// Work split (8 XCDs x 32 compute units, one 768-thread workgroup each), per
 // block as in the persistent stack kernel: XCD x owns the slice
 // F_x = [x f/8, (x+1) f/8) of the intermediate dimension; its workgroup j
 // computes gate/up rows F_x,j and the partial down product over F_x for the
 // output rows D_j = [j d/32, (j+1) d/32).  Workgroup j of XCD x sums the
 // eight partials of the rows D_j[x DJ/8, (x+1) DJ/8) (DJ = d/32) of every
-// block in XCD order and writes them.  The LoRA-A products A x_l of all blocks (fp32) are
-// computed once at the start, one dot product per polling wave, and read
-// back as tagged words.
+// block in XCD order and writes them.  The LoRA-A products A x_l of all
+// blocks (fp32) are computed once at the start, one dot product per polling
+// wave, and read back as tagged words.
 //
 // Which compute wave takes which gate/up wave-item and which run of down
 // wave-items is a host-side plan in the kernel arguments: waves w and w + 4
@@ -42,6 +42,8 @@
 // rows of all four slots when a launch starts.  The 64-bit words (LoRA-A
 // products, down partials) carry a 32-bit tag of the step and have one slot
 // per block.
+#include <type_traits>
+
 #include "stack_common.h"
 
 namespace qmlp {
@@ -73,6 +75,7 @@ struct LayersArgs {
     int n_gu;                    // compute waves 0 .. n_gu-1 each run gate/up wave-item `wave`
     int dn_lo[LCW], dn_n[LCW];   // down wave-items [dn_lo, dn_lo + dn_n) of the other compute waves
     int o_xs, o_cx, o_t, o_hs, o_hcx, o_meta, meta_bytes;   // LDS byte offsets
+    int o_dmeta;                 // LDS: down metadata areas, 512 B per (compute wave, item)
 };
 
 namespace {
@@ -86,6 +89,7 @@ struct SlLds {
     uint4* hs;          // [2][4 HS] h' of this XCD's slice (down units)
     float2* hcx;        // [2][HS] per unit (1024 sum h', sum h)
     char* meta;         // per-wave gate/up metadata areas
+    uint4* dmeta;       // down metadata: 32 16-byte chunks per (compute wave, item)
 };
 
 // Staging word w of block l's input: x[16w, 16w + 16) into the gate/up x'
@@ -120,11 +124,120 @@ __device__ __forceinline__ void sl_stage_x(uint4* xs, float2* cx, const uint4 (&
     }
 }
 
+// Per-lane offsets of a gate/up wave-item's loads (the same for every block:
+// only the base pointers change), in the order sk_gu_load issues them.
+template <int KM>
+struct SlGuAddr {
+    long moff[KM];      // metadata chunk (16-byte units) and whether it is an up chunk
+    bool mup[KM];
+    long coff;          // codes of slot 0 (16-byte units); slot i at coff + 8 i
+    long boff;          // LoRA-B chunk (16-byte units) and whether it is an up chunk
+    bool bup;
+};
+
+template <int KM>
+__device__ __forceinline__ SlGuAddr<KM> sl_gu_addr(int row0, int row_end, int f, int d, int g, int r, int lane) {
+    SlGuAddr<KM> a;
+    const int s = lane & 7, U = d / 64, ng = d / g, chunks = 2 * ng;
+    const int row = row0 + (lane >> 3);
+    const long rowc = row < row_end ? row : row0;
+    const long mbase = (long)row0 * ng / 4;
+#pragma unroll
+    for (int k = 0; k < KM; ++k) {
+        const int c = lane + 64 * k;
+        const bool up = c >= chunks && c < 2 * chunks;
+        const int cc = c < chunks ? c : (up ? c - chunks : 0);
+        const bool inside = row0 + (4 * cc) / ng < f;
+        a.moff[k] = mbase + (inside ? cc : 0);
+        a.mup[k] = up;
+    }
+    a.coff = rowc * U + s;
+    const int c = lane < 2 * r ? lane : 0;
+    a.bup = c >= r && r > 0;
+    const int cc = a.bup ? c - r : c;
+    const bool in = r > 0 && row0 + (8 * cc) / r < f;
+    a.boff = (r > 0 ? (long)row0 * r / 8 : 0) + (in ? cc : 0);
+    return a;
+}
+
+template <int KM>
+__device__ __forceinline__ void sl_meta_load(uint4 (&meta)[KM], const StackLayer& w, const SlGuAddr<KM>& a) {
+#pragma unroll
+    for (int k = 0; k < KM; ++k)
+        meta[k] = load_stream(reinterpret_cast<const uint4*>(a.mup[k] ? w.mu : w.mg) + a.moff[k]);
+}
+
+template <int JG, int KM>
+__device__ __forceinline__ void sl_b_load(FGuItem<1, 8, JG, KM>& it, const StackLayer& w, const SlGuAddr<KM>& a,
+                                          int r) {
+    const uint4* base = r > 0 ? reinterpret_cast<const uint4*>(a.bup ? w.Bu : w.Bg)
+                              : reinterpret_cast<const uint4*>(w.cg);
+    const uint4 b = load_stream(base + a.boff);
+    it.bg[0] = b.x; it.bg[1] = b.y; it.bu[0] = b.z; it.bu[1] = b.w;
+}
+
+// sk_gu_accumulate with the next block's codes of slot i requested right
+// after slot i's arithmetic (RELOAD), so the gate/up stream of block i+1
+// starts while block i's dot products are still running.
+template <int JG, int KM, bool RELOAD>
+__device__ __forceinline__ void sl_gu_accumulate(FGuItem<1, 8, JG, KM>& it, const uint4* xs, const float2* cx,
+                                                 int g, const uint32_t* wmeta, int lane, const StackLayer& wn,
+                                                 const SlGuAddr<KM>& a) {
+    constexpr int XS = 8 * JG;
+    const uint32_t mv = magic_vgpr();
+    const int s = lane & 7, r = lane >> 3;
+    const int ng = XS * 64 / g, gsh = g == 128 ? 1 : 0;
+    const uint4* xl = xs + s;
+    const float2* cl = cx + s;
+    const uint32_t* mgl = wmeta + r * ng + (s >> gsh);
+    const uint32_t* mul = wmeta + (8 + r) * ng + (s >> gsh);
+    const uint4* cg = reinterpret_cast<const uint4*>(wn.cg) + a.coff;
+    const uint4* cu = reinterpret_cast<const uint4*>(wn.cu) + a.coff;
+#pragma unroll
+    for (int i = 0; i < JG; ++i) {
+        uint4 xv[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) xv[c] = xl[c * XS + 8 * i];
+        uint32_t wg[4] = {it.qg[i].x, it.qg[i].y, it.qg[i].z, it.qg[i].w};
+        uint32_t wu[4] = {it.qu[i].x, it.qu[i].y, it.qu[i].z, it.qu[i].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            pin(wg[q]);
+            pin(wu[q]);
+        }
+        float ag = 0.0f, au = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t eg[8], eu[8];
+            extract_w2(wg[q], eg, mv);
+            extract_w2(wu[q], eu, mv);
+            const uint32_t xp[8] = {xv[2 * q].x, xv[2 * q].y, xv[2 * q].z, xv[2 * q].w,
+                                    xv[2 * q + 1].x, xv[2 * q + 1].y, xv[2 * q + 1].z, xv[2 * q + 1].w};
+#pragma unroll
+            for (int p = 0; p < 8; ++p) {
+                ag = dot2(eg[p], xp[p], ag);
+                au = dot2(eu[p], xp[p], au);
+            }
+        }
+        const int gi = (8 * i) >> gsh;
+        const uint32_t mgi = mgl[gi], mui = mul[gi];
+        const float2 k = cl[8 * i];
+        it.G[0] += h2f(mgi & 0xFFFFu) * (ag - k.x - h2f(mgi >> 16) * k.y);
+        it.U[0] += h2f(mui & 0xFFFFu) * (au - k.x - h2f(mui >> 16) * k.y);
+        if constexpr (RELOAD) {
+            sk_order();
+            it.qg[i] = load_stream(cg + 8 * i);
+            it.qu[i] = load_stream(cu + 8 * i);
+        }
+    }
+}
+
 // A gate/up wave: gate/up wave-item `wave` of block i in iteration i; its
-// registers are reloaded with block i+1's codes right after the arithmetic.
-// A wave runs one kind of arithmetic only, and its loop body issues its loads
-// without a condition (the last block is peeled off), so the loads it waits
-// for are always exactly the oldest ones it has in flight.
+// registers are reloaded with block i+1's codes as they fall free (metadata
+// once parked in LDS, each slot's codes after its arithmetic, LoRA-B after
+// the row sums).  A wave runs one kind of arithmetic only, and its loop body
+// issues its loads without a condition (the last block is peeled off), so the
+// loads it waits for are always exactly the oldest ones it has in flight.
 template <int JG, int KM>
 __device__ __forceinline__ void sl_gu_role(const LayersArgs& sa, LKArgs* ka, const SlLds& m, int xcc, int j,
                                            uint32_t seq0, int wave, int lane) {
@@ -132,6 +245,7 @@ __device__ __forceinline__ void sl_gu_role(const LayersArgs& sa, LKArgs* ka, con
     const int FX = f / SX, RG = f / SGRID, UG = d / 64;
     const int row_begin = xcc * FX + j * RG, row_end = row_begin + RG;
     const int row0 = row_begin + 8 * wave;
+    const SlGuAddr<KM> ga = sl_gu_addr<KM>(row0, row_end, f, d, g, r, lane);
     FGuItem<1, 8, JG, KM> gi;
     sk_gu_load(gi, sk_layer(ka, 0), row0, row_end, f, d, g, r, lane);
     // This wave's h words in all four slots start the launch with tag 0
@@ -144,26 +258,106 @@ __device__ __forceinline__ void sl_gu_role(const LayersArgs& sa, LKArgs* ka, con
     }
     __syncthreads();                                            // B0: block 0's input staged
     uint4* wmeta = reinterpret_cast<uint4*>(m.meta + wave * sa.meta_bytes);
-    auto compute = [&](int i) {
+    auto compute = [&](int i, auto reload) {
+        constexpr bool RL = decltype(reload)::value;
         const int par = i & 1;
         const uint32_t step = seq0 + 1 + i;
-        GateUpArgs ga{};
-        ga.d = d;
-        ga.g = g;
-        fgu_meta_to_lds(gi, ga, wmeta, lane);
-        sk_gu_accumulate(gi, m.xs + par * 8 * UG, m.cx + par * UG, g, reinterpret_cast<const uint32_t*>(wmeta),
-                         lane);
+        const StackLayer wn = sk_layer(ka, RL ? i + 1 : i);
+        GateUpArgs gargs{};
+        gargs.d = d;
+        gargs.g = g;
+        fgu_meta_to_lds(gi, gargs, wmeta, lane);
+        if constexpr (RL) {
+            sk_order();
+            sl_meta_load<KM>(gi.meta, wn, ga);
+        }
+        sl_gu_accumulate<JG, KM, RL>(gi, m.xs + par * 8 * UG, m.cx + par * UG, g,
+                                     reinterpret_cast<const uint32_t*>(wmeta), lane, wn, ga);
         sk_gu_finish(gi, m.ts + par * (2 * r + 1), r, sk_layer(ka, i).lora_scale, sa.hb + (long)(step & 3) * f,
                      stag(step), lane, wmeta + 4 * (d / g));
         sk_order();
+        if constexpr (RL)
+            sl_b_load(gi, wn, ga, r);
     };
     for (int i = 0; i + 1 < L; ++i) {
-        compute(i);
-        sk_gu_load(gi, sk_layer(ka, i + 1), row0, row_end, f, d, g, r, lane);
+        compute(i, std::true_type{});
+        gi.G[0] = gi.U[0] = 0.0f;
         __syncthreads();                                        // one barrier per iteration
     }
-    compute(L - 1);
+    compute(L - 1, std::false_type{});
     for (int i = L - 1; i < L + 2; ++i) __syncthreads();       // iterations L-1 .. L+1
+}
+
+// One down wave-item (8 output rows, 8 lanes per row) with its metadata
+// loaded wide: the groups of the XCD's column slice F_x in the item's 8 rows
+// are words [cb, cb + 16) of each row's (scale | zero) words, cb = the slice's
+// first group rounded down to a multiple of 4; lane l < 32 loads 16-byte chunk
+// l & 3 of row l >> 2, and the arithmetic reads each lane's word from LDS.
+// (One load per lane for the item, against one 4-byte load per lane and slot.)
+template <int JD>
+struct SlDn {
+    uint4 q[JD];
+    uint4 mc;
+};
+
+template <int JD>
+__device__ __forceinline__ void sl_dn_load(SlDn<JD>& it, const StackLayer& w, int o0, int xcc, int f, int g,
+                                           int lane) {
+    const int s = lane & 7, FX = f / SX, UF = FX / 32, Uf = f / 32, ngd = f / g;
+    const int o = o0 + (lane >> 3);
+    const uint4* cd = reinterpret_cast<const uint4*>(w.cd) + (long)o * Uf + xcc * UF;
+#pragma unroll
+    for (int i = 0; i < JD; ++i) {
+        // only the last slot can run past the slice: it re-reads the slice's
+        // last unit, and its contribution is dropped
+        const int u = i + 1 < JD ? s + 8 * i : (s + 8 * i < UF ? s + 8 * i : UF - 1);
+        it.q[i] = load_stream(cd + u);
+    }
+    const int cb = ((xcc * FX) / g) & ~3;
+    const int l32 = lane & 31, w0 = cb + 4 * (l32 & 3);
+    const int wc = w0 + 4 <= ngd ? w0 : cb;                      // a chunk past the row re-reads the first
+    it.mc = load_stream(reinterpret_cast<const uint4*>(w.md + (long)(o0 + (l32 >> 2)) * ngd + wc));
+}
+
+template <int JD>
+__device__ __forceinline__ float sl_dn_compute(const SlDn<JD>& it, const uint4* hs, const float2* hcx, int xcc,
+                                               int f, int g, int lane, uint4* wm) {
+    constexpr int HS = 8 * JD;
+    const int FX = f / SX, UF = FX / 32;
+    const uint32_t mv = magic_vgpr();
+    const int s = lane & 7;
+    const int cb = ((xcc * FX) / g) & ~3;
+    if (lane < 32)
+        wm[lane] = it.mc;
+    const uint32_t* wrow = reinterpret_cast<const uint32_t*>(wm) + (lane >> 3) * 16 - cb;
+    const uint4* hl = hs + s;
+    const float2* cl = hcx + s;
+    float Y = 0.0f;
+#pragma unroll
+    for (int i = 0; i < JD; ++i) {
+        const int u = s + 8 * i;
+        const int uc = i + 1 < JD ? u : (u < UF ? u : UF - 1);
+        uint32_t wv[4] = {it.q[i].x, it.q[i].y, it.q[i].z, it.q[i].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) pin(wv[q]);
+        float acc = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t e[4];
+            extract_w4(wv[q], e, mv);
+            const uint4 p = hl[q * HS + 8 * i];
+            acc = dot2(e[0], p.x, acc);
+            acc = dot2(e[1], p.y, acc);
+            acc = dot2(e[2], p.z, acc);
+            acc = dot2(e[3], p.w, acc);
+        }
+        const uint32_t mti = wrow[(xcc * FX + 32 * uc) / g];
+        const float2 k = cl[8 * i];
+        const float c = h2f(mti & 0xFFFFu) * (acc - k.x - h2f(mti >> 16) * k.y);
+        if (i + 1 < JD || u < UF)
+            Y += c;
+    }
+    return group_sum<8>(Y);
 }
 
 // A down wave with N down wave-items: the items of block i - 2 in iteration
@@ -177,22 +371,25 @@ template <int JD, int N, bool DB>
 __device__ __forceinline__ void sl_dn_role(const LayersArgs& sa, LKArgs* ka, const SlLds& m, int xcc, int j,
                                            uint32_t seq0, int wave, int lane) {
     const int d = sa.d, f = sa.f, g = sa.g, L = sa.L;
-    const int UF = f / SX / 32, DJ = d / SB;
+    const int DJ = d / SB;
     constexpr int HS = 8 * JD;
-    const int o = j * DJ + 8 * ka->dn_lo[wave] + (lane >> 3);  // output row of item 0 on this lane
-    auto load = [&](SkDn<JD> (&dd)[N], int l) {
+    const int o0 = j * DJ + 8 * ka->dn_lo[wave];                 // first output row of item 0
+    const int o = o0 + (lane >> 3);                             // output row of item 0 on this lane
+    uint4* wm = m.dmeta + wave * 4 * 32;                        // 32 chunks per item, up to 4 items
+    auto load = [&](SlDn<JD> (&dd)[N], int l) {
         const StackLayer w = sk_layer(ka, l);
 #pragma unroll
-        for (int k = 0; k < N; ++k) sk_dn_load(dd[k], w, o + 8 * k, xcc, f, g, lane);
+        for (int k = 0; k < N; ++k) sl_dn_load(dd[k], w, o0 + 8 * k, xcc, f, g, lane);
     };
     // All items' arithmetic first, then their stores: a store counts in the
     // same in-order counter as the loads, so a store between two items would
     // make the second item wait for its completion.
-    auto items = [&](SkDn<JD> (&dd)[N], int l) {
+    auto items = [&](SlDn<JD> (&dd)[N], int l) {
         float yv[N];
 #pragma unroll
         for (int k = 0; k < N; ++k)
-            yv[k] = sk_dn_compute<JD>(dd[k], m.hs + (l & 1) * 4 * HS, m.hcx + (l & 1) * HS, UF, lane);
+            yv[k] = sl_dn_compute<JD>(dd[k], m.hs + (l & 1) * 4 * HS, m.hcx + (l & 1) * HS, xcc, f, g, lane,
+                                      wm + 32 * k);
         const unsigned long long tg = (unsigned long long)ltag32(seq0 + 1 + l) << 32;
 #pragma unroll
         for (int k = 0; k < N; ++k)
@@ -200,13 +397,13 @@ __device__ __forceinline__ void sl_dn_role(const LayersArgs& sa, LKArgs* ka, con
                 st_cross64(sa.pb + ((long)l * SX + xcc) * d + o + 8 * k, (unsigned long long)__float_as_uint(yv[k]) | tg);
         sk_order();
     };
-    SkDn<JD> da[N];
+    SlDn<JD> da[N];
     load(da, 0);
     __syncthreads();                                            // B0
     __syncthreads();                                            // iteration 0
     __syncthreads();                                            // iteration 1
     if constexpr (DB) {
-        SkDn<JD> db[N];
+        SlDn<JD> db[N];
         int l = 0;                                              // block l is in da
         for (; l + 2 < L; l += 2) {                             // iterations l + 2, l + 3
             load(db, l + 1);
@@ -426,7 +623,8 @@ __global__ void __launch_bounds__(LTHREADS) layers_kernel(LayersArgs sa) {
     if (j < SB) {
         const SlLds m{reinterpret_cast<uint4*>(lds + sa.o_xs), reinterpret_cast<float2*>(lds + sa.o_cx),
                       reinterpret_cast<float*>(lds + sa.o_t), reinterpret_cast<uint4*>(lds + sa.o_hs),
-                      reinterpret_cast<float2*>(lds + sa.o_hcx), lds + sa.o_meta};
+                      reinterpret_cast<float2*>(lds + sa.o_hcx), lds + sa.o_meta,
+                      reinterpret_cast<uint4*>(lds + sa.o_dmeta)};
         LKArgs* ka = (LKArgs*)__builtin_amdgcn_kernarg_segment_ptr();
         if (wave < sa.n_gu)
             sl_gu_role<JG, KM>(sa, ka, m, (int)xcc, j, seq0, wave, lane);
@@ -481,7 +679,7 @@ int layers_cu_count() {
 struct LayersPlan {
     int jg, km, jd, ndn;
     int n_gu, dn_lo[LCW], dn_n[LCW];
-    int o_xs, o_cx, o_t, o_hs, o_hcx, o_meta, meta_bytes;
+    int o_xs, o_cx, o_t, o_hs, o_hcx, o_meta, meta_bytes, o_dmeta;
     size_t lds;
     bool ok;
 };
@@ -536,6 +734,15 @@ LayersPlan plan_layers(int M, int d, int f, int g, int r) {
     const int RG = f / SGRID, UG = d / 64, ng = d / g, UF = f / SX / 32, DJ = d / SB;
     if ((RG + 7) / 8 > LGU_MAX || ng % 4 != 0 || DJ % 16 != 0 || DJ / 16 > 64)
         return p;
+    // down metadata: rows 16-byte aligned, and each XCD slice's groups inside a
+    // 16-word window that starts at a multiple of 4
+    if ((f / g) % 4 != 0)
+        return p;
+    for (int x = 0; x < SX; ++x) {
+        const int lo = x * (f / SX) / g, hi = ((x + 1) * (f / SX) - 1) / g;
+        if (hi - (lo & ~3) >= 16)
+            return p;
+    }
     if (r != 0 && r != 8 && r != 16 && r != 32)
         return p;
     if (UG % 8 != 0)                             // 8 lanes per row, no partial slot
@@ -568,6 +775,7 @@ LayersPlan plan_layers(int M, int d, int f, int g, int r) {
     p.o_hcx = take((size_t)2 * p.jd * 8 * 8);
     p.meta_bytes = 2 * 8 * ng * 4 + 32 * r;      // metadata, then LoRA-B rows
     p.o_meta = take((size_t)LGU_MAX * p.meta_bytes);
+    p.o_dmeta = take((size_t)LCW * 4 * 32 * 16);
     p.lds = o;
     p.ok = p.lds <= 64 * 1024;
     return p;
@@ -615,7 +823,7 @@ hipError_t launch_layers(const StackLayerDesc* layers, int L, int d, int f, int 
         a.dn_n[w] = p.dn_n[w];
     }
     a.o_xs = p.o_xs; a.o_cx = p.o_cx; a.o_t = p.o_t; a.o_hs = p.o_hs; a.o_hcx = p.o_hcx;
-    a.o_meta = p.o_meta; a.meta_bytes = p.meta_bytes;
+    a.o_meta = p.o_meta; a.meta_bytes = p.meta_bytes; a.o_dmeta = p.o_dmeta;
     auto run = [&](auto kernel) -> hipError_t {
         kernel<<<SGRID, LTHREADS, p.lds, st>>>(a);
         return hipGetLastError();
