@@ -53,7 +53,6 @@ namespace {
 // Control words (uint32 index into the control block).
 constexpr int L_SEQ = 0, L_DONE = 32, L_ERR = 64, L_XC = 96;
 
-__device__ __forceinline__ uint32_t ltag32(uint32_t step) { return step % 0xFFFFFFFFu + 1u; }
 
 constexpr int LCW = 10;                  // compute waves: gate/up waves first, then down waves
 constexpr int LTHREADS = (LCW + SPW) * 64;

@@ -37,12 +37,14 @@
 // consumer of an XCD-local word are on the same L2 by construction.
 //
 // Hand-offs carry their own validity: each published value sits in one
-// aligned word with a 16-bit tag that changes with every layer step (32-bit
-// words: binary16 | tag << 16; 64-bit words: fp32 bits | tag << 32).
-// XCD-local words are written with plain stores and polled with sc0|nt
-// loads (they miss the CU's L1 and hit the XCD's L2); cross-XCD words are
-// written and polled device-coherent (sc1), double-buffered by layer parity
-// (an XCD can run at most one layer ahead of another).  Waves 0-5 hold and
+// aligned word with a tag that changes with every layer step (32-bit words:
+// binary16 | 16-bit tag << 16; 64-bit words: fp32 bits | tag << 32, the
+// cross-XCD partials with a 32-bit tag, since a slot of their parity-double
+// buffer can go unwritten for many launches of one layer).  XCD-local words
+// are written with plain stores and polled with sc0|nt loads (they miss the
+// CU's L1 and hit the XCD's L2); cross-XCD words are written and polled
+// device-coherent (sc1), double-buffered by layer parity (an XCD can run at
+// most one layer ahead of another).  Waves 0-5 hold and
 // stream weights and compute; waves 6-7 only poll, so their polls are never
 // queued behind the weight stream of their own wave.  Every wait is bounded:
 // a timeout sets an error bit, later polls of that wave are skipped and the
@@ -257,7 +259,7 @@ __device__ __forceinline__ void sk_compute_role(const StackArgs& sa, KArgs* ka, 
                 const float yv = sk_dn_compute<JD>(di[k], m.hs, m.hcx, UF, lane);
                 const int o = j * DJ + 8 * item + (lane >> 3);
                 if ((lane & 7) == 0)
-                    st_cross64(pb + o, (unsigned long long)__float_as_uint(yv) | ((unsigned long long)ti << 32));
+                    st_cross64(pb + o, (unsigned long long)__float_as_uint(yv) | ((unsigned long long)ltag32(pl.seq0 + 1 + i) << 32));
             }
         }
         sk_order();
@@ -381,7 +383,7 @@ __device__ __forceinline__ void sk_poll_role(const StackArgs& sa, const SkLds& m
 #pragma unroll
             for (int xx = 0; xx < SX; ++xx) off[xx] = 16 * lane + xx * d * 8;
             u32x4 v[SX];
-            dead |= !sk_poll<SX, 0, POL_CROSS>(prs, off, lane < DJ / 2 ? 0xFFu : 0u, v, ti, dead);
+            dead |= !sk_poll<SX, 0, POL_CROSS>(prs, off, lane < DJ / 2 ? 0xFFu : 0u, v, ltag32(pl.seq0 + 1 + i), dead);
             float y0 = 0.0f, y1 = 0.0f;
 #pragma unroll
             for (int xx = 0; xx < SX; ++xx) {

@@ -36,6 +36,8 @@ constexpr int POL_INTRA = (int)0x80000003u;   // sc0 | nt: through to this XCD's
 constexpr int POL_CROSS = (int)0x80000010u;   // sc1: device-coherent
 
 __device__ __forceinline__ uint32_t stag(uint32_t s) { return s % 65535u + 1u; }
+// 32-bit tag of a step, for the 64-bit hand-off words (never 0)
+__device__ __forceinline__ uint32_t ltag32(uint32_t step) { return step % 0xFFFFFFFFu + 1u; }
 
 // Compiler-only fence: the next layer's weight loads are not hoisted above
 // the arithmetic on the current layer's registers (which would keep both

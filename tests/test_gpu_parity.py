@@ -276,15 +276,17 @@ def test_empty_batch_is_a_noop(q):
 
 
 def test_full_stack_sampled_layers(q):
-    """The 36-layer Qwen3-4B-shaped stack exactly as the benchmark runs it
-    (one forward per layer, shared workspace, same stream); layers 0, 17 and
-    35 checked in full against the oracle."""
+    """The 36 Qwen3-4B-shaped blocks exactly as the benchmark times them (one
+    qmlp_forward_layers call over every block's own input, the bench's
+    workspace and stream); blocks 0, 17 and 35 checked in full against the
+    oracle."""
     cfg = wl.CONFIGS["qwen3_4b"]
     _announce("full stack", cfg.name, "L", cfg.L)
     import bench
     stack = bench.build_stack(cfg, seed=0)
-    ys = bench.run_stack_once(stack)
+    ys = bench.run_blocks_once(stack)
     torch.cuda.synchronize()
+    assert q.layers_errors(stack.lws) == 0
     for i in (0, 17, cfg.L - 1):
         L = wl.layer(cfg, i)
         y_ref, _ = oracle_forward(L)
