@@ -24,6 +24,15 @@ For context the same blocks are also timed as a decoder stack on a
 residual stream (x_{l+1} = x_l + block_l(RMSNorm(x_l)), each block's input
 depending on the previous block's output, qmlp_forward_stack) and one
 qmlp_forward launch per block.
+
+precision_comparison: the MLP-level analogue of the paper's Gain and
+Capture (Sec. 5.2) on this GPU.  The same fp32 weights are packed as uniform
+W4 (gate/up and down at 4 bits), uniform W2, W4/W2-GateUp with its LoRA
+adapters, and W4/W2-GateUp with the paper's INT2 group of 32; all four run
+on the same stand-alone decode kernels (qmlp_forward_batch: LoRA-A, gate/up
+and down of every block in one launch each; one pass over the 36 blocks
+captured in a HIP graph), so the comparison isolates the bit widths:  Gain = TPS_mix / TPS_W4 - 1,  Capture = (TPS_mix - TPS_W4) /
+(TPS_W2 - TPS_W4), with TPS = 1 / (us per MLP step).
 """
 from __future__ import annotations
 
@@ -55,8 +64,9 @@ def log(*a):
 
 # --------------------------------------------------------------------- stack
 class Stack:
-    def __init__(self, cfg, mlps, xs, ys, ws):
+    def __init__(self, cfg, mlps, xs, ys, ws, variants=None):
         self.cfg, self.mlps, self.xs, self.ys, self.ws = cfg, mlps, xs, ys, ws
+        self.variants = variants or {}                 # name -> [MLP] at other widths
         import torch
         import paper_2606_04238_amd as q
         self.st = q.Stack(mlps)
@@ -72,12 +82,40 @@ def _gen_layer(cfg, i, seed):
     return wl.layer(cfg, i, seed)
 
 
-def build_stack(cfg: wl.Config, seed: int = 0, layers: int | None = None, threads: int = 16) -> Stack:
-    """Generate the seeded layers on the host (parallel), pack them on the GPU."""
+# The precision comparison (Sec. 5.2): (gate/up bits, gate/up group, down
+# bits, down group, adapters); group None = the workload's group.
+VARIANTS = {
+    "w4_uniform": (4, None, 4, None, False),
+    "w2_uniform": (2, None, 2, None, False),
+    "w4w2_gateup_lora": (2, None, 4, None, True),
+    "w4w2_gateup_g32_lora": (2, 32, 4, None, True),
+}
+
+
+def variant_widths(cfg: wl.Config, name: str):
+    bg, gg, bd, gd, lora = VARIANTS[name]
+    return bg, gg or cfg.g, bd, gd or cfg.g, lora
+
+
+def variant_bytes(cfg: wl.Config, name: str) -> int:
+    """Algorithmic bytes of one MLP step at a variant's widths: codes
+    (2 f d bg/8 + d f bd/8), fp16 scale+zero (8 f d/gg + 4 d f/gd), the
+    LoRA factors when the variant carries adapters, x in and y out."""
+    bg, gg, bd, gd, lora = variant_widths(cfg, name)
+    f, d, M, r = cfg.f, cfg.d, cfg.M, cfg.r
+    n = 2 * f * d * bg // 8 + d * f * bd // 8 + 8 * f * d // gg + 4 * d * f // gd + 4 * M * d
+    return n + (4 * r * (d + f) if lora else 0)
+
+
+def build_stack(cfg: wl.Config, seed: int = 0, layers: int | None = None, threads: int = 16,
+                variants: bool = False) -> Stack:
+    """Generate the seeded layers on the host (parallel), pack them on the GPU
+    (with `variants`, also at the other widths of the precision comparison)."""
     import torch
     import paper_2606_04238_amd as q
     L = cfg.L if layers is None else layers
     mlps, xs, ys = [], [], []
+    var = {k: [] for k in VARIANTS} if variants else {}
     t0 = time.time()
     with concurrent.futures.ThreadPoolExecutor(max_workers=threads) as ex:
         futs = [ex.submit(_gen_layer, cfg, i, seed) for i in range(L)]
@@ -87,22 +125,31 @@ def build_stack(cfg: wl.Config, seed: int = 0, layers: int | None = None, thread
 
             def act(a):
                 return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(dt).cuda()
-            g = q.pack_w2(torch.from_numpy(lay.W_gate).cuda(), cfg.g)
-            u = q.pack_w2(torch.from_numpy(lay.W_up).cuda(), cfg.g)
-            d = q.pack_w4(torch.from_numpy(lay.W_down).cuda(), cfg.g)
-            mlps.append(q.MLP(g, u, d, act(lay.A_gate), act(lay.B_gate), act(lay.A_up),
-                              act(lay.B_up), lora_scale=cfg.lora_scale))
+            Wg, Wu, Wd = (torch.from_numpy(w).cuda() for w in (lay.W_gate, lay.W_up, lay.W_down))
+            g = q.pack_w2(Wg, cfg.g)
+            u = q.pack_w2(Wu, cfg.g)
+            d = q.pack_w4(Wd, cfg.g)
+            lo = (act(lay.A_gate), act(lay.B_gate), act(lay.A_up), act(lay.B_up))
+            mlps.append(q.MLP(g, u, d, *lo, lora_scale=cfg.lora_scale))
+            for name in var:
+                bg, gg, bd, gd, lora = variant_widths(cfg, name)
+                pk = {2: q.pack_w2, 4: q.pack_w4}
+                vg, vu, vd = pk[bg](Wg, gg), pk[bg](Wu, gg), pk[bd](Wd, gd)
+                var[name].append(q.MLP(vg, vu, vd, *(lo if lora else ()),
+                                       lora_scale=cfg.lora_scale))
+            del Wg, Wu, Wd
             xs.append(act(lay.x))
             ys.append(torch.empty((cfg.M, cfg.d), dtype=dt, device="cuda"))
             fut._result = None          # drop the fp32 host copies
     torch.cuda.synchronize()
-    for m in mlps:
+    for m in mlps + [v for vs in var.values() for v in vs]:
         for w in (m.gate, m.up, m.down):
             if w.invalid_groups():
                 raise RuntimeError("packer flagged invalid groups")
     ws = q.workspace(mlps[0], cfg.M, ys[0].dtype)
-    log("built %d layers in %.1f s" % (L, time.time() - t0))
-    return Stack(cfg, mlps, xs, ys, ws)
+    log("built %d layers%s in %.1f s" % (L, " (+%d width variants)" % len(var) if var else "",
+                                         time.time() - t0))
+    return Stack(cfg, mlps, xs, ys, ws, var)
 
 
 def run_blocks_once(stack: Stack):
@@ -126,6 +173,73 @@ def run_layers_once(stack: Stack):
     for m, x, y in zip(stack.mlps, stack.xs, stack.ys):
         q.forward(m, x, y=y, ws=stack.ws)
     return stack.ys
+
+
+def run_variant_once(stack: Stack, name: str):
+    """One pass of a width variant over every block: qmlp_forward_batch, the
+    stand-alone decode kernels in batches of up to 40 blocks (LoRA-A,
+    gate/up and down of every block of a batch)."""
+    import paper_2606_04238_amd as q
+    lay, ws = stack.variant_layers[name]
+    return q.forward_batch(lay, stack.X, y=stack.YB, ws=ws)
+
+
+def precision_comparison(stack: Stack, seed: int, steps: int, min_warm_s: float, mix_us: float):
+    """us per MLP step of each width variant (graph replay of one pass over
+    the blocks), its achieved GB/s, the oracle parity of block 0 and block
+    L-1, and the MLP-level Gain / Capture of the two W4/W2-GateUp variants;
+    beside them the Gain of the persistent W4/W2-GateUp launch (mix_us) over
+    uniform W4 on the batched kernels."""
+    import torch
+    import oracle as orc
+    import paper_2606_04238_amd as q
+    cfg = stack.cfg
+    L = len(stack.mlps)
+    stack.YB = torch.empty_like(stack.X)
+    stack.variant_layers = {}
+    samples = {i: wl.layer(cfg, i, seed) for i in (0, L - 1)}
+    res = {}
+    for name in VARIANTS:
+        lay = q.Layers(stack.variants[name])
+        stack.variant_layers[name] = (lay, q.batch_workspace(lay, cfg.M))
+        g = capture(lambda: run_variant_once(stack, name))
+        ms, _ = time_passes(g.replay, steps, 2, min_warm_s)
+        us = sum(ms) / len(ms) * 1e3 / L
+        run_variant_once(stack, name)
+        torch.cuda.synchronize()
+        Y = stack.YB.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        bg, gg, bd, gd, lora = variant_widths(cfg, name)
+        errs = []
+        for i, ly in samples.items():
+            qg, qu, qd = (orc.quantize(ly.W_gate, bg, gg), orc.quantize(ly.W_up, bg, gg),
+                          orc.quantize(ly.W_down, bd, gd))
+            lo = (ly.A_gate, ly.B_gate, ly.A_up, ly.B_up) if lora else (None,) * 4
+            y_ref = orc.forward(qg, qu, qd, *lo, ly.x, lora_scale=cfg.lora_scale)
+            errs.append(orc.max_rel_err(orc.act_to_f64(Y[i], False), y_ref))
+        b = variant_bytes(cfg, name)
+        res[name] = {"us_per_mlp_step": round(us, 3), "alg_bytes_per_mlp_step": b,
+                     "gbs": round(b / (us * 1e-6) / 1e9, 1),
+                     "frac_of_hbm_peak": round(b / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                     "launches_per_step": (L + 39) // 40 * (3 if lora else 2),
+                     "parity_max_rel_err_blocks_0_last": float("%.3e" % max(errs))}
+    t4, t2 = res["w4_uniform"]["us_per_mlp_step"], res["w2_uniform"]["us_per_mlp_step"]
+    b4, b2 = variant_bytes(cfg, "w4_uniform"), variant_bytes(cfg, "w2_uniform")
+    out = {"kernels": "qmlp_forward_batch: stand-alone decode kernels, one launch each for "
+                      "LoRA-A, gate/up and down of up to 40 blocks; HIP graph over %d blocks" % L,
+           "variants": res}
+    for name in ("w4w2_gateup_lora", "w4w2_gateup_g32_lora"):
+        tm, bm = res[name]["us_per_mlp_step"], variant_bytes(cfg, name)
+        out[name] = {
+            "gain_pct": round((t4 / tm - 1) * 100, 1),
+            "capture_pct": round((1 / tm - 1 / t4) / (1 / t2 - 1 / t4) * 100, 1),
+            # the same two figures if every variant moved its bytes at one bandwidth
+            "bytes_model_gain_pct": round((b4 / bm - 1) * 100, 1),
+            "bytes_model_capture_pct": round((1 / bm - 1 / b4) / (1 / b2 - 1 / b4) * 100, 1)}
+    out["persistent_w4w2_gateup_lora"] = {
+        "us_per_mlp_step": round(mix_us, 3),
+        "gain_pct_over_batched_w4": round((t4 / mix_us - 1) * 100, 1),
+        "capture_pct_batched_w2_w4": round((1 / mix_us - 1 / t4) / (1 / t2 - 1 / t4) * 100, 1)}
+    return out
 
 
 def capture(fn):
@@ -367,6 +481,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--min-warm-s", type=float, default=0.25,
                     help="untimed warmup lasts at least this long (and at least --warmup steps)")
+    ap.add_argument("--no-precision-comparison", action="store_true",
+                    help="skip the uniform-W4 / uniform-W2 / W4/W2-GateUp comparison (Sec. 5.2)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="after timing, run one copy-like elementwise kernel over this many MiB "
                          "(read N, write N) as the reference dispatch for HBM byte counters")
@@ -387,12 +503,14 @@ def main(argv=None):
     cfg = wl.CONFIGS[args.config]
     if cfg.M > 16:
         return prefill_main(cfg, args)
-    stack = build_stack(cfg, args.seed)
+    stack = build_stack(cfg, args.seed, variants=not args.no_precision_comparison)
     L = cfg.L
     B = cfg.alg_bytes()
     dt = stack.Y.dtype
     launches = q.layers_launches(stack.lay, cfg.M, dt)
-    persistent = launches < L
+    chunks = (L + 39) // 40
+    persistent = launches == chunks                     # one persistent launch per 40 blocks
+    batched = not persistent and launches == chunks * (3 if cfg.r else 2)
 
     # the timed step: every block on its own input, back to back
     # timed in both launch modes; `value` is the one --mode names, the other is
@@ -428,6 +546,10 @@ def main(argv=None):
     layer_ms, _ = time_passes(gl.replay, max(5, args.steps // 2), 2, args.min_warm_s)
     per_layer_us = sum(layer_ms) / len(layer_ms) * 1e3 / L
     context["per_layer_path_us_per_mlp_step"] = round(per_layer_us, 3)
+    if stack.variants:
+        context["precision_comparison"] = precision_comparison(stack, args.seed,
+                                                               max(5, args.steps // 2),
+                                                               args.min_warm_s, us_layer)
 
     traffic = None
     if persistent:
@@ -440,6 +562,13 @@ def main(argv=None):
         kernel_us = {"layers_kernel_avg_launch": round(dom_us, 3), "launches_per_step": launches}
         traffic = read_traffic(os.path.join(ROOT, "profiles", "layers_kernel_%s.md" % cfg.name),
                                dom_name)
+    elif batched:
+        # the batched path's launches (LoRA-A, gate/up, down of up to 40
+        # blocks each) are internal to one call: the step is the unit timed
+        # here, the per-kernel split comes from the kernel trace
+        dom_name = "batched step (LoRA-A, gate/up and down launches of qmlp_forward_batch)"
+        dom_us, dom_b = t_step * 1e3, L * B
+        kernel_us = {"batched_step": round(dom_us, 3), "launches_per_step": launches}
     else:
         fused, k1_us, k2_us = kernel_durations(stack)
         if fused:
@@ -475,7 +604,8 @@ def main(argv=None):
             "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
             "alg_bytes_per_mlp_step": B,
             "mode": "hip_graph" if args.mode == "graph" else "eager",
-            "path": "persistent layers kernel" if persistent else "per-block forward",
+            "path": "persistent layers kernel" if persistent else
+                    "batched stand-alone kernels" if batched else "per-block forward",
             "eager_us_per_mlp_step": round(sum(eager_ms) / len(eager_ms) * 1e3 / L, 3),
             "graph_us_per_mlp_step": round(sum(graph_ms) / len(graph_ms) * 1e3 / L, 3),
             "median_ms_per_step": round(statistics.median(head), 4),

@@ -78,19 +78,27 @@ typedef void *qmlp_stream;
 
 /* Non-owning view of one packed quantized matrix in device memory. */
 typedef struct {
-    int32_t bits;     /* 2 (gate/up) or 4 (down) */
+    int32_t bits;     /* 2 (gate/up) or 4 (down); see qmlp_mlp for the other widths */
     int32_t n_out;    /* rows n of the logical W [n][k] */
     int32_t k_in;     /* columns k; groups run along k */
-    int32_t group;    /* g: 64 or 128; k_in % g == 0 */
+    int32_t group;    /* g: 32, 64 or 128; k_in % g == 0 */
     void *codes;      /* qmlp_codes_bytes(bits, n_out, k_in) bytes, 16-B aligned */
     void *meta;       /* qmlp_meta_bytes(n_out, k_in, group) bytes, 16-B aligned */
 } qmlp_qweight;
 
-/* One W4/W2-GateUp MLP block with its Recover-LoRA adapters (Sec. 3.3, 4.2). */
+/* One W4/W2-GateUp MLP block with its Recover-LoRA adapters (Sec. 3.3, 4.2).
+ * gate/up at 2 bits and down at 4 bits, groups of 64 or 128, is the block
+ * every path takes.  The binary16 decode path (qmlp_forward,
+ * qmlp_forward_layers, qmlp_forward_batch; not the one-kernel layer nor the
+ * persistent launches, which take only that form) also runs the comparison
+ * points of the throughput analysis (Sec. 5.2) and the paper's INT2 grouping
+ * (Sec. 3.3, Sec. 4.1): gate/up at 4 bits (uniform W4), down at 2 bits
+ * (uniform W2, groups of 64 or 128), and group 32 for gate/up (either
+ * width) and for a 4-bit down. */
 typedef struct {
-    qmlp_qweight gate;      /* bits 2, [f][d] */
-    qmlp_qweight up;        /* bits 2, [f][d], same group as gate */
-    qmlp_qweight down;      /* bits 4, [d][f] */
+    qmlp_qweight gate;      /* bits 2 (or 4), [f][d] */
+    qmlp_qweight up;        /* same bits and group as gate, [f][d] */
+    qmlp_qweight down;      /* bits 4 (or 2), [d][f] */
     const void *A_gate;     /* [rank][d] activation type (nn.Linear / PEFT "lora_A") */
     const void *B_gate;     /* [f][rank] activation type (PEFT "lora_B")            */
     const void *A_up;       /* [rank][d] */
@@ -131,13 +139,14 @@ size_t qmlp_workspace_bytes(const qmlp_mlp *mlp, int M, qmlp_dtype dtype);
  * A group holding a non-finite weight or whose scale overflows binary16 is
  * written as codes 0, scale NaN (0x7E00), zero 0, and bit 0 of *d_status
  * (a device int32, may be NULL) is set with an atomic OR; the caller zeroes
- * *d_status beforehand.  Requires k_in % 64 == 0, group in {64, 128}.
+ * *d_status beforehand.  Requires group in {32, 64, 128}, k_in % group == 0
+ * (32 is the paper's INT2 group).
  */
 qmlp_status qmlp_pack_w2(const float *W, int n_out, int k_in, int group,
                          qmlp_qweight *out, int32_t *d_status, qmlp_stream stream);
 
 /* Sec. 3.3 / Sec. 7 step 4: the same at 4 bits (down projection and every
- * other non-gate/up linear).  Requires k_in % 32 == 0, group in {64, 128}. */
+ * other non-gate/up linear).  Requires group in {32, 64, 128}, k_in % group == 0. */
 qmlp_status qmlp_pack_w4(const float *W, int n_out, int k_in, int group,
                          qmlp_qweight *out, int32_t *d_status, qmlp_stream stream);
 
@@ -151,7 +160,8 @@ qmlp_status qmlp_pack_w4(const float *W, int n_out, int k_in, int group,
  *   h = SiLU(G) * U = G / (1 + exp(-G)) * U
  * x [M][d] and h [M][f] are row-major in the activation type `dtype`.
  * ws/ws_bytes: workspace of at least qmlp_workspace_bytes(mlp, M, dtype).
- * M == 0 enqueues nothing and returns QMLP_OK.
+ * M == 0 enqueues nothing and returns QMLP_OK.  Gate and up must be 2-bit
+ * (group 32 allowed on the decode path); QMLP_ERR_UNSUPPORTED otherwise.
  */
 qmlp_status qmlp_gateup_w2_lora(const qmlp_mlp *mlp, const void *x, int M, qmlp_dtype dtype,
                                 void *h, void *ws, size_t ws_bytes, qmlp_stream stream);
@@ -159,6 +169,7 @@ qmlp_status qmlp_gateup_w2_lora(const qmlp_mlp *mlp, const void *x, int M, qmlp_
 /*
  * The 4-bit down projection (Sec. 3.3): y [M][n_out] = W4down h, with
  * h [M][k_in] and y row-major in the activation type.  No workspace.
+ * Group 32 only on the binary16 decode path.
  */
 qmlp_status qmlp_down_w4(const qmlp_qweight *down, const void *h, int M, qmlp_dtype dtype,
                          void *y, qmlp_stream stream);
@@ -225,7 +236,8 @@ int qmlp_stack_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
  * launch per 40 blocks, pipelined: the gate/up rows of block i, the down
  * rows of block i-2 and the output sum of block i-3 run together, so the
  * hand-offs inside a block overlap the weight stream of the next.  Every
- * other shape and bfloat16 run qmlp_forward once per block.
+ * other binary16 shape runs as qmlp_forward_batch does; bfloat16 runs
+ * qmlp_forward once per block.
  *
  * ws/ws_bytes: at least qmlp_layers_workspace_bytes(layers, L, M, dtype),
  * zero before the first call, with the rules of qmlp_workspace_bytes.  On
@@ -240,10 +252,33 @@ qmlp_status qmlp_forward_layers(const qmlp_mlp *layers, int L, const void *x, in
                                 qmlp_dtype dtype, void *y, void *ws, size_t ws_bytes,
                                 qmlp_stream stream);
 
-/* Launches qmlp_forward_layers makes: the number of persistent launches, or
+/* Launches qmlp_forward_layers makes: the number of persistent launches, the
+ * launches of the batched path (3 per 40 blocks, 2 without adapters), or
  * the per-block launches of qmlp_forward; 0 if the call would be rejected.
  * Host-only. */
 int qmlp_layers_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
+
+/*
+ * The same L independent blocks as qmlp_forward_layers, always on the
+ * stand-alone decode kernels, in batches of up to 40 blocks: the LoRA-A
+ * products of every block of a batch (one launch, skipped at rank 0), then
+ * gate/up with SiLU(G) * U of every block (one launch), then down of every
+ * block (one launch).  Binary16 only (1 <= M <= 16), any width combination
+ * qmlp_mlp lists: it is the path of the width comparison (Sec. 5.2), where
+ * every precision must run on the same kernels, and of callers that do not
+ * want a launch holding every compute unit.  h and t of a batch stay in the
+ * workspace between the launches.
+ *
+ * ws/ws_bytes: at least qmlp_batch_workspace_bytes(layers, L, M, dtype):
+ * a 1024-byte block left at zero, t [min(L,40)][M][2r] fp32, h
+ * [min(L,40)][M][f] binary16.  No state is kept between calls.  Errors as
+ * for qmlp_forward_layers; QMLP_ERR_UNSUPPORTED for bfloat16.
+ */
+size_t qmlp_batch_workspace_bytes(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
+
+qmlp_status qmlp_forward_batch(const qmlp_mlp *layers, int L, const void *x, int M,
+                               qmlp_dtype dtype, void *y, void *ws, size_t ws_bytes,
+                               qmlp_stream stream);
 
 /* ---------------------------------------------- inspection (not timed) */
 

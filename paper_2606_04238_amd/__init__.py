@@ -80,6 +80,8 @@ def _lib():
             "qmlp_layers_workspace_bytes": (Z, [pm, I, I, I]),
             "qmlp_forward_layers": (I, [pm, I, P, I, I, P, P, Z, P]),
             "qmlp_layers_launches": (I, [pm, I, I, I]),
+            "qmlp_batch_workspace_bytes": (Z, [pm, I, I, I]),
+            "qmlp_forward_batch": (I, [pm, I, P, I, I, P, P, Z, P]),
             "qmlp_status_string": (ctypes.c_char_p, [I]),
         }
         for name, (res, args) in sig.items():
@@ -174,7 +176,9 @@ def pack_w4(W: torch.Tensor, group: int) -> QWeight:
 
 
 class MLP:
-    """One W4/W2-GateUp block with Recover-LoRA adapters (device tensors)."""
+    """One W4/W2-GateUp block with Recover-LoRA adapters (device tensors); the
+    decode path also takes the uniform-W4 / uniform-W2 comparison widths and
+    group 32 (see qmlp_mlp in include/qmlp.h)."""
 
     def __init__(self, gate: QWeight, up: QWeight, down: QWeight, A_gate=None, B_gate=None,
                  A_up=None, B_up=None, lora_scale: float = 1.0):
@@ -304,7 +308,8 @@ def layers_workspace_bytes(layers: Layers, M: int, dtype=torch.float16) -> int:
 
 
 def layers_launches(layers: Layers, M: int, dtype=torch.float16) -> int:
-    """Launches forward_layers makes (persistent launches, or one forward per block)."""
+    """Launches forward_layers makes (persistent launches, the batched path's
+    launches, or one forward per block)."""
     code = F16 if dtype == torch.float16 else BF16
     return int(_lib().qmlp_layers_launches(layers.c(), len(layers), M, code))
 
@@ -334,6 +339,33 @@ def forward_layers(layers: Layers, x: torch.Tensor, y: torch.Tensor | None = Non
         ws = layers_workspace(layers, M, x.dtype, x.device)
     _check(_lib().qmlp_forward_layers(layers.c(), L, _ptr(x), M, _dtype_code(x), _ptr(y), _ptr(ws),
                                       ws.numel(), _stream()), "forward_layers")
+    return y
+
+
+def batch_workspace_bytes(layers: Layers, M: int, dtype=torch.float16) -> int:
+    code = F16 if dtype == torch.float16 else BF16
+    return int(_lib().qmlp_batch_workspace_bytes(layers.c(), len(layers), M, code))
+
+
+def batch_workspace(layers: Layers, M: int, dtype=torch.float16, device="cuda") -> torch.Tensor:
+    """A zeroed workspace for forward_batch."""
+    n = batch_workspace_bytes(layers, M, dtype)
+    return torch.zeros(max(n, 1024), dtype=torch.uint8, device=device)
+
+
+def forward_batch(layers: Layers, x: torch.Tensor, y: torch.Tensor | None = None,
+                  ws: torch.Tensor | None = None) -> torch.Tensor:
+    """forward_layers on the stand-alone kernels whatever the shape: LoRA-A,
+    gate/up and down of every block of a batch of up to 40, three launches."""
+    L, M, d = x.shape
+    if L != len(layers) or d != layers.mlps[0].d:
+        raise ValueError("x must be [L][M][d] for the L blocks")
+    if y is None:
+        y = torch.empty_like(x)
+    if ws is None:
+        ws = batch_workspace(layers, M, x.dtype, x.device)
+    _check(_lib().qmlp_forward_batch(layers.c(), L, _ptr(x), M, _dtype_code(x), _ptr(y), _ptr(ws),
+                                     ws.numel(), _stream()), "forward_batch")
     return y
 
 

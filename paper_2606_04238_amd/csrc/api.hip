@@ -17,15 +17,15 @@ inline size_t round256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 qmlp_status from_hip(hipError_t e) { return e == hipSuccess ? QMLP_OK : QMLP_ERR_HIP; }
 
-// Structural checks of one packed-weight view.
+// Structural checks of one packed-weight view (bits 0 = either width).
 qmlp_status check_qweight(const qmlp_qweight* w, int bits) {
     if (!w || !w->codes || !w->meta)
         return QMLP_ERR_NULL;
-    if (w->bits != bits)
+    if (bits ? w->bits != bits : (w->bits != 2 && w->bits != 4))
         return QMLP_ERR_UNSUPPORTED;
     if (w->n_out <= 0 || w->k_in <= 0)
         return QMLP_ERR_SHAPE;
-    if (w->group != 64 && w->group != 128)
+    if (w->group != 32 && w->group != 64 && w->group != 128)
         return QMLP_ERR_UNSUPPORTED;
     if (w->k_in % w->group != 0)
         return QMLP_ERR_SHAPE;
@@ -34,19 +34,31 @@ qmlp_status check_qweight(const qmlp_qweight* w, int bits) {
     return QMLP_OK;
 }
 
+// The W4/W2-GateUp block (2-bit gate/up, 4-bit down, groups of 64 or 128):
+// the only form the fused, persistent and prefill kernels take.  The other
+// widths (uniform W4, uniform W2) and group 32 -- the comparison points of
+// Sec. 5.2 and the paper's own INT2 grouping -- run on the stand-alone
+// decode kernels.
+bool standard_mlp(const qmlp_mlp* mlp) {
+    return mlp->gate.bits == 2 && mlp->down.bits == 4 && mlp->gate.group >= 64 &&
+           mlp->down.group >= 64;
+}
+
 // Shape, pointer and type checks of a whole block at M tokens.
 qmlp_status check_mlp(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
     if (!mlp)
         return QMLP_ERR_NULL;
     qmlp_status s;
-    if ((s = check_qweight(&mlp->gate, 2)) != QMLP_OK) return s;
-    if ((s = check_qweight(&mlp->up, 2)) != QMLP_OK) return s;
-    if ((s = check_qweight(&mlp->down, 4)) != QMLP_OK) return s;
+    if ((s = check_qweight(&mlp->gate, 0)) != QMLP_OK) return s;
+    if ((s = check_qweight(&mlp->up, mlp->gate.bits)) != QMLP_OK) return s;
+    if ((s = check_qweight(&mlp->down, 0)) != QMLP_OK) return s;
     const int f = mlp->gate.n_out, d = mlp->gate.k_in;
     if (mlp->up.n_out != f || mlp->up.k_in != d || mlp->down.n_out != d || mlp->down.k_in != f)
         return QMLP_ERR_SHAPE;
     if (mlp->up.group != mlp->gate.group)
         return QMLP_ERR_SHAPE;
+    if (mlp->down.bits == 2 && mlp->down.group == 32)
+        return QMLP_ERR_UNSUPPORTED;
     if (d % 64 != 0 || f % 64 != 0)
         return QMLP_ERR_SHAPE;
     if (mlp->rank != 0 && mlp->rank != 8 && mlp->rank != 16 && mlp->rank != 32)
@@ -61,7 +73,8 @@ qmlp_status check_mlp(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
     if (M < 0)
         return QMLP_ERR_SHAPE;
     if (dtype == QMLP_BF16) {                    // prefill-chunk path
-        if (M != 0 && !prefill_supported(M, d, f, mlp->gate.group, mlp->rank))
+        if (!standard_mlp(mlp) ||
+            (M != 0 && !prefill_supported(M, d, f, mlp->gate.group, mlp->rank)))
             return QMLP_ERR_UNSUPPORTED;
         return QMLP_OK;
     }
@@ -69,7 +82,9 @@ qmlp_status check_mlp(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
         return QMLP_ERR_UNSUPPORTED;
     if (M > 16)                                  // decode runs in binary16 at 1..16 tokens
         return QMLP_ERR_UNSUPPORTED;
-    if (!decode_shape_supported(d, f))
+    if (!decode_shape_supported(d, f) ||
+        !decode_variant_supported(d, f, mlp->gate.bits, mlp->gate.group, mlp->down.bits,
+                                  mlp->down.group))
         return QMLP_ERR_UNSUPPORTED;
     return QMLP_OK;
 }
@@ -163,6 +178,7 @@ GateUpArgs gateup_args(const qmlp_mlp* mlp, const void* x, int M, uint16_t* h, c
     a.r = mlp->rank;
     a.uc = 0;
     a.lora_scale = mlp->lora_scale;
+    a.bits = mlp->gate.bits;
     return a;
 }
 
@@ -177,6 +193,7 @@ DownArgs down_args(const qmlp_qweight* down, const void* h, int M, void* y) {
     a.f = down->k_in;
     a.g = down->group;
     a.uc = 0;
+    a.bits = down->bits;
     return a;
 }
 
@@ -200,7 +217,7 @@ qmlp_status pack_common(int bits, const float* W, int n_out, int k_in, int group
         return QMLP_ERR_NULL;
     if (n_out <= 0 || k_in <= 0)
         return QMLP_ERR_SHAPE;
-    if (group != 64 && group != 128)
+    if (group != 32 && group != 64 && group != 128)
         return QMLP_ERR_UNSUPPORTED;
     if (k_in % group != 0)
         return QMLP_ERR_SHAPE;
@@ -223,9 +240,7 @@ qmlp_status pack_common(int bits, const float* W, int n_out, int k_in, int group
 qmlp_status check_inspect(const qmlp_qweight* w) {
     if (!w)
         return QMLP_ERR_NULL;
-    if (w->bits != 2 && w->bits != 4)
-        return QMLP_ERR_UNSUPPORTED;
-    return check_qweight(w, w->bits);
+    return check_qweight(w, 0);
 }
 
 // L independent blocks of one shape: block l maps x[l] to y[l].
@@ -241,7 +256,8 @@ qmlp_status check_layers(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype)
         const qmlp_mlp& a = layers[0];
         const qmlp_mlp& b = layers[i];
         if (b.gate.k_in != a.gate.k_in || b.gate.n_out != a.gate.n_out || b.gate.group != a.gate.group ||
-            b.down.group != a.down.group || b.rank != a.rank)
+            b.down.group != a.down.group || b.rank != a.rank || b.gate.bits != a.gate.bits ||
+            b.down.bits != a.down.bits)
             return QMLP_ERR_SHAPE;
     }
     return QMLP_OK;
@@ -257,7 +273,7 @@ qmlp_status check_stack(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) 
 
 bool stack_persistent(const qmlp_mlp* layers, int M, qmlp_dtype dtype) {
     const qmlp_mlp& a = layers[0];
-    return dtype == QMLP_F16 && a.down.group == a.gate.group &&
+    return dtype == QMLP_F16 && standard_mlp(&a) && a.down.group == a.gate.group &&
            stack_supported(M, a.gate.k_in, a.gate.n_out, a.gate.group, a.rank);
 }
 
@@ -284,8 +300,58 @@ StackLayerDesc stack_desc(const qmlp_mlp& m) {
 
 bool layers_persistent(const qmlp_mlp* layers, int M, qmlp_dtype dtype) {
     const qmlp_mlp& a = layers[0];
-    return dtype == QMLP_F16 && a.down.group == a.gate.group &&
+    return dtype == QMLP_F16 && standard_mlp(&a) && a.down.group == a.gate.group &&
            layers_supported(M, a.gate.k_in, a.gate.n_out, a.gate.group, a.rank);
+}
+
+// Independent blocks that do not take the persistent launch run in batches
+// of up to kBatchMax blocks on the stand-alone kernels: LoRA-A of every
+// block of the batch, then gate/up of every block, then down of every block
+// (three launches per batch, two without adapters).  Binary16 decode only;
+// bfloat16 runs qmlp_forward per block.
+bool layers_batched(const qmlp_mlp* layers, int M, qmlp_dtype dtype) {
+    return dtype == QMLP_F16 && !layers_persistent(layers, M, dtype);
+}
+
+size_t batch_t_bytes(const qmlp_mlp* a, int nb, int M) {
+    return round256((size_t)nb * M * 2 * a->rank * 4);
+}
+size_t batch_h_bytes(const qmlp_mlp* a, int nb, int M) {
+    return round256((size_t)nb * M * a->gate.n_out * 2);
+}
+int batch_size(int L) { return L < kBatchMax ? L : kBatchMax; }
+
+qmlp_status run_layers_batched(const qmlp_mlp* layers, int L, const char* xb, int M, char* yb,
+                               void* ws, hipStream_t st) {
+    const qmlp_mlp& a = layers[0];
+    const int d = a.gate.k_in;
+    const size_t step = (size_t)M * d * 2;
+    char* base = static_cast<char*>(ws);
+    BatchArgs b{};
+    b.t = reinterpret_cast<float*>(base + kCtlBytes);
+    b.h = reinterpret_cast<uint16_t*>(base + kCtlBytes + batch_t_bytes(&a, batch_size(L), M));
+    b.M = M;
+    b.d = d;
+    b.f = a.gate.n_out;
+    b.r = a.rank;
+    b.gg = a.gate.group;
+    b.bg = a.gate.bits;
+    b.gd = a.down.group;
+    b.bd = a.down.bits;
+    for (int l0 = 0; l0 < L; l0 += kBatchMax) {
+        const int n = batch_size(L - l0);
+        for (int i = 0; i < n; ++i) b.lay[i] = stack_desc(layers[l0 + i]);
+        b.x = reinterpret_cast<const uint16_t*>(xb + l0 * step);
+        b.y = reinterpret_cast<uint16_t*>(yb + l0 * step);
+        hipError_t e = b.r > 0 ? launch_lora_a_batch(b, n, st) : hipSuccess;
+        if (e == hipSuccess)
+            e = launch_gateup_batch(b, n, st);
+        if (e == hipSuccess)
+            e = launch_down_batch(b, n, st);
+        if (e != hipSuccess)
+            return QMLP_ERR_HIP;
+    }
+    return QMLP_OK;
 }
 
 }  // namespace
@@ -328,6 +394,8 @@ qmlp_status qmlp_gateup_w2_lora(const qmlp_mlp* mlp, const void* x, int M, qmlp_
     qmlp_status s = check_mlp(mlp, M, dtype);
     if (s != QMLP_OK)
         return s;
+    if (mlp->gate.bits != 2)
+        return QMLP_ERR_UNSUPPORTED;
     if (M == 0)
         return QMLP_OK;
     if (!x || !h)
@@ -355,7 +423,7 @@ qmlp_status qmlp_down_w4(const qmlp_qweight* down, const void* h, int M, qmlp_dt
     if (M < 0)
         return QMLP_ERR_SHAPE;
     if (dtype == QMLP_BF16) {
-        if (M != 0 && (M % 128 != 0 || down->n_out % 128 != 0))
+        if (down->group == 32 || (M != 0 && (M % 128 != 0 || down->n_out % 128 != 0)))
             return QMLP_ERR_UNSUPPORTED;
     } else if (M > 16 || dtype != QMLP_F16 || !decode_shape_supported(down->n_out, down->k_in)) {
         return QMLP_ERR_UNSUPPORTED;
@@ -394,7 +462,8 @@ qmlp_status qmlp_forward(const qmlp_mlp* mlp, const void* x, int M, qmlp_dtype d
             return s;
         return run_prefill_down(&mlp->down, w.h, M, y, st);
     }
-    if (fused_supported(M, mlp->gate.k_in, mlp->gate.n_out, mlp->gate.group, mlp->rank))
+    if (standard_mlp(mlp) &&
+        fused_supported(M, mlp->gate.k_in, mlp->gate.n_out, mlp->gate.group, mlp->rank))
         return from_hip(launch_fused(gateup_args(mlp, x, M, w.h, w.t),
                                      down_args(&mlp->down, w.h, M, y),
                                      static_cast<const uint16_t*>(mlp->A_gate),
@@ -438,7 +507,8 @@ int qmlp_forward_launches(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
         return 0;
     if (dtype == QMLP_BF16)
         return mlp->rank > 0 ? 4 : 2;
-    if (fused_supported(M, mlp->gate.k_in, mlp->gate.n_out, mlp->gate.group, mlp->rank))
+    if (standard_mlp(mlp) &&
+        fused_supported(M, mlp->gate.k_in, mlp->gate.n_out, mlp->gate.group, mlp->rank))
         return 1;
     return mlp->rank > 0 ? 3 : 2;
 }
@@ -528,6 +598,8 @@ size_t qmlp_layers_workspace_bytes(const qmlp_mlp* layers, int L, int M, qmlp_dt
         return 0;
     if (layers_persistent(layers, M, dtype))
         return layers_ws_bytes(layers[0].gate.k_in, layers[0].gate.n_out, layers[0].rank);
+    if (layers_batched(layers, M, dtype))
+        return qmlp_batch_workspace_bytes(layers, L, M, dtype);
     return qmlp_workspace_bytes(&layers[0], M, dtype);
 }
 
@@ -536,6 +608,8 @@ int qmlp_layers_launches(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype)
         return 0;
     if (layers_persistent(layers, M, dtype))
         return (L + layers_max_layers() - 1) / layers_max_layers();
+    if (layers_batched(layers, M, dtype))
+        return (L + kBatchMax - 1) / kBatchMax * (layers[0].rank > 0 ? 3 : 2);
     int n = 0;
     for (int i = 0; i < L; ++i) n += qmlp_forward_launches(&layers[i], M, dtype);
     return n;
@@ -575,12 +649,41 @@ qmlp_status qmlp_forward_layers(const qmlp_mlp* layers, int L, const void* x, in
         }
         return QMLP_OK;
     }
+    if (layers_batched(layers, M, dtype))
+        return run_layers_batched(layers, L, xb, M, yb, ws, st);
     for (int i = 0; i < L; ++i) {
         s = qmlp_forward(&layers[i], xb + i * step, M, dtype, yb + i * step, ws, ws_bytes, stream);
         if (s != QMLP_OK)
             return s;
     }
     return QMLP_OK;
+}
+
+size_t qmlp_batch_workspace_bytes(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    if (check_layers(layers, L, M, dtype) != QMLP_OK || M == 0 || dtype != QMLP_F16)
+        return 0;
+    return kCtlBytes + batch_t_bytes(layers, batch_size(L), M) + batch_h_bytes(layers, batch_size(L), M);
+}
+
+qmlp_status qmlp_forward_batch(const qmlp_mlp* layers, int L, const void* x, int M, qmlp_dtype dtype,
+                               void* y, void* ws, size_t ws_bytes, qmlp_stream stream) {
+    qmlp_status s = check_layers(layers, L, M, dtype);
+    if (s != QMLP_OK)
+        return s;
+    if (dtype != QMLP_F16)
+        return QMLP_ERR_UNSUPPORTED;
+    if (M == 0)
+        return QMLP_OK;
+    if (!x || !y)
+        return QMLP_ERR_NULL;
+    if (!aligned16(x) || !aligned16(y))
+        return QMLP_ERR_ALIGN;
+    if (!ws || ws_bytes < qmlp_batch_workspace_bytes(layers, L, M, dtype))
+        return QMLP_ERR_WORKSPACE;
+    if (!aligned16(ws))
+        return QMLP_ERR_ALIGN;
+    return run_layers_batched(layers, L, static_cast<const char*>(x), M, static_cast<char*>(y), ws,
+                              static_cast<hipStream_t>(stream));
 }
 
 const char* qmlp_status_string(qmlp_status s) {

@@ -57,7 +57,10 @@ __device__ __forceinline__ XWord stage_x_load(const uint16_t* x, int M, int d, i
 }
 
 // Convert one staged word; all lanes of the wave must call it (shuffles).
-template <int MT>
+// SPLIT (group 32 at 2 bits: two groups per 64-code unit) stages (C, X) per
+// half unit, two float2 per (token, unit): words 0-1 hold the codes of the
+// first group, words 2-3 those of the second.
+template <int MT, bool SPLIT = false>
 __device__ __forceinline__ void stage_x_store(uint4* xs, float2* cx, int UC, int uc, int M, int idx,
                                               XWord v, uint4* xplain = nullptr) {
     const int words = MT * uc * 4;
@@ -81,14 +84,14 @@ __device__ __forceinline__ void stage_x_store(uint4* xs, float2* cx, int UC, int
         csum += h2f(ha) + h2f(hb);
         xsum += h2f(a16) + h2f(b16);
     }
-    csum = group_sum<4>(csum);
-    xsum = group_sum<4>(xsum);
+    csum = group_sum<SPLIT ? 2 : 4>(csum);
+    xsum = group_sum<SPLIT ? 2 : 4>(xsum);
     if (live) {
         uint4* dst = xs + (m * UC + ul) * 8;
         dst[(2 * w) ^ (ul & 7)] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
         dst[(2 * w + 1) ^ (ul & 7)] = make_uint4(pr[4], pr[5], pr[6], pr[7]);
-        if (w == 0)
-            cx[m * UC + ul] = make_float2(1024.0f * csum, xsum);
+        if (SPLIT ? (w & 1) == 0 : w == 0)
+            cx[SPLIT ? (m * UC + ul) * 2 + (w >> 1) : m * UC + ul] = make_float2(1024.0f * csum, xsum);
         if (xplain) {                          // unscaled copy (single-chunk staging only)
             uint4* dp = xplain + (m * uc + ul) * 8 + w * 2;
             dp[0] = make_uint4(xl[0], xl[1], xl[2], xl[3]);
@@ -98,12 +101,12 @@ __device__ __forceinline__ void stage_x_store(uint4* xs, float2* cx, int UC, int
 }
 
 // Whole staging of a chunk by the block (load-convert per word).
-template <int MT>
+template <int MT, bool SPLIT = false>
 __device__ __forceinline__ void stage_x(uint4* xs, float2* cx, int UC, const uint16_t* x, int M,
                                         int d, int u0, int uc, int tid, int nthreads) {
     const int words = MT * uc * 4;
     for (int idx = tid; idx < ((words + 63) & ~63); idx += nthreads)
-        stage_x_store<MT>(xs, cx, UC, uc, M, idx, stage_x_load<MT>(x, M, d, u0, uc, idx));
+        stage_x_store<MT, SPLIT>(xs, cx, UC, uc, M, idx, stage_x_load<MT>(x, M, d, u0, uc, idx));
 }
 
 // h' for 4-bit units [u0, u0+uc): per (m, unit) four 16-byte chunks (one per
@@ -160,10 +163,18 @@ __device__ __forceinline__ void stage_h(uint4* hs, float2* cx, int UC, const uin
 }
 
 // --------------------------------------------------------------- gate/up item
-template <int MT, int S, int MAXJ>
+// B = code width of gate and up: 2 (W4/W2-GateUp, and uniform W2) or 4
+// (uniform W4, the baseline of the precision comparison in Sec. 5.2).  A
+// 16-byte unit holds UI = 128/B codes of a row: at 2 bits the activation is
+// staged by stage_x (eight chunks per unit), at 4 bits by stage_h (four).
+// SPLIT = group 32 at 2 bits (the paper's INT2 grouping, Sec. 3.3 and
+// Sec. 4.1): a unit spans two groups, so each carries two metadata words
+// and two (C, X) pairs (stage_x<MT, true>).
+template <int MT, int S, int MAXJ, int B = 2, bool SPLIT = false>
 struct GuItem {
+    static constexpr int NM = SPLIT ? 2 : 1;     // metadata words per unit
     uint4 qg[MAXJ], qu[MAXJ];
-    uint32_t mg[MAXJ], mu[MAXJ];
+    uint32_t mg[MAXJ][NM], mu[MAXJ][NM];
     uint32_t bg[4], bu[4];          // LoRA-B row slice, raw binary16
     float G[MT], U[MT];
     int row;
@@ -171,16 +182,18 @@ struct GuItem {
 };
 
 // Issue the loads of one gate/up item: S lanes per row, rows row0 + lane/S.
-template <int MT, int S, int MAXJ>
-__device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ>& it, const GateUpArgs& a, int row0,
-                                        bool active, int lane) {
+template <int MT, int S, int MAXJ, int B, bool SPLIT>
+__device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ, B, SPLIT>& it, const GateUpArgs& a,
+                                        int row0, bool active, int lane) {
+    static_assert((B == 2 || B == 4) && (!SPLIT || B == 2), "gate/up at 2 or 4 bits");
+    constexpr int UI = 128 / B;
     const int s = lane % S;
-    const int U = a.d / 64;
+    const int U = a.d / UI;
     const int J = (U + S - 1) / S;
     it.row = row0 + lane / S;
     it.ok = active && it.row < a.f;
     const int ng = a.d / a.g;
-    const int upg = a.g / 64;
+    const int upg = SPLIT ? 1 : a.g / UI;
     // Loads go out from a clamped, always valid address (unit 0 of row 0 for
     // lanes without work) straight into the slot registers: no select and no
     // conversion touches a loaded value here, since loads retire in order and
@@ -199,8 +212,12 @@ __device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ>& it, const GateUpArg
             const int uu = u < U ? u : 0;
             it.qg[i] = load_stream(cg + uu);
             it.qu[i] = load_stream(cu + uu);
-            it.mg[i] = load_stream(mg + uu / upg);
-            it.mu[i] = load_stream(mu + uu / upg);
+#pragma unroll
+            for (int h = 0; h < GuItem<MT, S, MAXJ, B, SPLIT>::NM; ++h) {
+                const int gi = SPLIT ? 2 * uu + h : uu / upg;
+                it.mg[i][h] = load_stream(mg + gi);
+                it.mu[i][h] = load_stream(mu + gi);
+            }
         }
     }
     // LoRA-B row slices stay raw binary16 until the epilogue: four loads per
@@ -219,56 +236,85 @@ __device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ>& it, const GateUpArg
 }
 
 // Dot products of the item's units that fall in the staged chunk [u0, u0+uc).
-template <int MT, int S, int MAXJ>
-__device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ>& it, const uint4* xs,
+template <int MT, int S, int MAXJ, int B, bool SPLIT>
+__device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ, B, SPLIT>& it, const uint4* xs,
                                               const float2* cx, int UC, int d, int u0, int uc,
                                               int lane) {
+    constexpr int NM = GuItem<MT, S, MAXJ, B, SPLIT>::NM;
+    constexpr int UI = 128 / B;
     const uint32_t mv = 0x64006400u;           // (the standalone kernels keep the literal)
     const int s = lane % S;
-    const int J = (d / 64 + S - 1) / S;
+    const int J = (d / UI + S - 1) / S;
 #pragma unroll
     for (int i = 0; i < MAXJ; ++i) {
         const int u = s + S * i;
         if (i < J && u >= u0 && u < u0 + uc) {
             const int ul = u - u0;
-            float ag[MT], au[MT];
+            float ag[NM][MT], au[NM][MT];
 #pragma unroll
-            for (int m = 0; m < MT; ++m) ag[m] = au[m] = 0.0f;
+            for (int h = 0; h < NM; ++h)
+#pragma unroll
+                for (int m = 0; m < MT; ++m) ag[h][m] = au[h][m] = 0.0f;
             uint32_t wg[4] = {it.qg[i].x, it.qg[i].y, it.qg[i].z, it.qg[i].w};
             uint32_t wu[4] = {it.qu[i].x, it.qu[i].y, it.qu[i].z, it.qu[i].w};
-            uint32_t mgi = it.mg[i], mui = it.mu[i];
+            uint32_t mgi[NM], mui[NM];
+#pragma unroll
+            for (int h = 0; h < NM; ++h) {
+                mgi[h] = it.mg[i][h];
+                mui[h] = it.mu[i][h];
+                pin(mgi[h]);
+                pin(mui[h]);
+            }
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
                 pin(wg[w]);
                 pin(wu[w]);
             }
-            pin(mgi);
-            pin(mui);
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
-                uint32_t eg[8], eu[8];
-                extract_w2(wg[w], eg, mv);
-                extract_w2(wu[w], eu, mv);
+                const int hw = SPLIT ? (w >> 1) : 0;     // the group of code word w
+                if constexpr (B == 2) {
+                    uint32_t eg[8], eu[8];
+                    extract_w2(wg[w], eg, mv);
+                    extract_w2(wu[w], eu, mv);
 #pragma unroll
-                for (int m = 0; m < MT; ++m) {
-                    const uint4* src = xs + (m * UC + ul) * 8;
-                    const uint4 p0 = src[(2 * w) ^ (ul & 7)];
-                    const uint4 p1 = src[(2 * w + 1) ^ (ul & 7)];
-                    const uint32_t xp[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+                    for (int m = 0; m < MT; ++m) {
+                        const uint4* src = xs + (m * UC + ul) * 8;
+                        const uint4 p0 = src[(2 * w) ^ (ul & 7)];
+                        const uint4 p1 = src[(2 * w + 1) ^ (ul & 7)];
+                        const uint32_t xp[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
 #pragma unroll
-                    for (int p = 0; p < 8; ++p) {
-                        ag[m] = dot2(eg[p], xp[p], ag[m]);
-                        au[m] = dot2(eu[p], xp[p], au[m]);
+                        for (int p = 0; p < 8; ++p) {
+                            ag[hw][m] = dot2(eg[p], xp[p], ag[hw][m]);
+                            au[hw][m] = dot2(eu[p], xp[p], au[hw][m]);
+                        }
+                    }
+                } else {
+                    uint32_t eg[4], eu[4];
+                    extract_w4(wg[w], eg, mv);
+                    extract_w4(wu[w], eu, mv);
+#pragma unroll
+                    for (int m = 0; m < MT; ++m) {
+                        const uint4 p = xs[(m * UC + ul) * 4 + (w ^ ((ul >> 1) & 3))];
+                        const uint32_t xp[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) {
+                            ag[0][m] = dot2(eg[c], xp[c], ag[0][m]);
+                            au[0][m] = dot2(eu[c], xp[c], au[0][m]);
+                        }
                     }
                 }
             }
-            const float sg = h2f(mgi & 0xFFFFu), zg = h2f(mgi >> 16);
-            const float su = h2f(mui & 0xFFFFu), zu = h2f(mui >> 16);
 #pragma unroll
-            for (int m = 0; m < MT; ++m) {
-                const float2 k = cx[m * UC + ul];
-                it.G[m] += sg * (ag[m] - k.x - zg * k.y);
-                it.U[m] += su * (au[m] - k.x - zu * k.y);
+            for (int h = 0; h < NM; ++h) {
+                const float sg = h2f(mgi[h] & 0xFFFFu), zg = h2f(mgi[h] >> 16);
+                const float su = h2f(mui[h] & 0xFFFFu), zu = h2f(mui[h] >> 16);
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    const float2 k = cx[(m * UC + ul) * NM + h];
+                    it.G[m] += sg * (ag[h][m] - k.x - zg * k.y);
+                    it.U[m] += su * (au[h][m] - k.x - zu * k.y);
+                }
             }
         }
     }
@@ -276,8 +322,8 @@ __device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ>& it, const uin
 
 // LoRA-B on the lane's rank slice, reduction over the S lanes of each row,
 // and the epilogue h = SiLU(G) * U (t: [M][2r] fp32, gate ranks then up).
-template <int MT, int S, int MAXJ>
-__device__ __forceinline__ void gu_finish(GuItem<MT, S, MAXJ>& it, const GateUpArgs& a,
+template <int MT, int S, int MAXJ, int B, bool SPLIT>
+__device__ __forceinline__ void gu_finish(GuItem<MT, S, MAXJ, B, SPLIT>& it, const GateUpArgs& a,
                                           const float* t, uint16_t* h, int lane) {
     const int s = lane % S;
     if (a.r > 0) {
@@ -314,7 +360,10 @@ __device__ __forceinline__ void gu_finish(GuItem<MT, S, MAXJ>& it, const GateUpA
 }
 
 // --------------------------------------------------------------- down item
-template <int MT, int S, int MAXJ>
+// B = code width of the down projection: 4 (W4/W2-GateUp, uniform W4) or 2
+// (uniform W2, Sec. 5.2).  At 4 bits h is staged by stage_h (32 codes per
+// unit), at 2 bits by stage_x (64 codes per unit; groups of 64 or 128).
+template <int MT, int S, int MAXJ, int B = 4>
 struct DnItem {
     uint4 q[MAXJ];
     uint32_t mt[MAXJ];
@@ -324,17 +373,19 @@ struct DnItem {
     bool active;      // the wave holds this item (wave-uniform)
 };
 
-template <int MT, int S, int MAXJ>
-__device__ __forceinline__ void dn_load(DnItem<MT, S, MAXJ>& it, const DownArgs& a, int row0,
+template <int MT, int S, int MAXJ, int B>
+__device__ __forceinline__ void dn_load(DnItem<MT, S, MAXJ, B>& it, const DownArgs& a, int row0,
                                         bool active, int lane) {
+    static_assert(B == 2 || B == 4, "down at 2 or 4 bits");
+    constexpr int UI = 128 / B;
     const int s = lane % S;
-    const int U = a.f / 32;
+    const int U = a.f / UI;
     const int J = (U + S - 1) / S;
     it.row = row0 + lane / S;
     it.ok = active && it.row < a.d;
     it.active = active;
     const int ng = a.f / a.g;
-    const int upg = a.g / 32;
+    const int upg = a.g / UI;
     const long rowc = it.ok ? it.row : 0;          // clamped, unselected: see gu_load
     const uint4* cd = reinterpret_cast<const uint4*>(a.cd) + rowc * U;
     const uint32_t* md = a.md + rowc * ng;
@@ -351,13 +402,14 @@ __device__ __forceinline__ void dn_load(DnItem<MT, S, MAXJ>& it, const DownArgs&
     for (int m = 0; m < MT; ++m) it.Y[m] = 0.0f;
 }
 
-template <int MT, int S, int MAXJ>
-__device__ __forceinline__ void dn_accumulate(DnItem<MT, S, MAXJ>& it, const uint4* hs,
+template <int MT, int S, int MAXJ, int B>
+__device__ __forceinline__ void dn_accumulate(DnItem<MT, S, MAXJ, B>& it, const uint4* hs,
                                               const float2* cx, int UC, int f, int u0, int uc,
                                               int lane) {
+    constexpr int UI = 128 / B;
     const uint32_t mv = 0x64006400u;           // (the standalone kernels keep the literal)
     const int s = lane % S;
-    const int J = (f / 32 + S - 1) / S;
+    const int J = (f / UI + S - 1) / S;
     if (!it.active)
         return;
 #pragma unroll
@@ -376,15 +428,29 @@ __device__ __forceinline__ void dn_accumulate(DnItem<MT, S, MAXJ>& it, const uin
             pin(mti);
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
-                uint32_t e[4];
-                extract_w4(wv[w], e, mv);
+                if constexpr (B == 4) {
+                    uint32_t e[4];
+                    extract_w4(wv[w], e, mv);
 #pragma unroll
-                for (int m = 0; m < MT; ++m) {
-                    const uint4 p = hs[(m * UC + ul) * 4 + (w ^ ((ul >> 1) & 3))];
-                    acc[m] = dot2(e[0], p.x, acc[m]);
-                    acc[m] = dot2(e[1], p.y, acc[m]);
-                    acc[m] = dot2(e[2], p.z, acc[m]);
-                    acc[m] = dot2(e[3], p.w, acc[m]);
+                    for (int m = 0; m < MT; ++m) {
+                        const uint4 p = hs[(m * UC + ul) * 4 + (w ^ ((ul >> 1) & 3))];
+                        acc[m] = dot2(e[0], p.x, acc[m]);
+                        acc[m] = dot2(e[1], p.y, acc[m]);
+                        acc[m] = dot2(e[2], p.z, acc[m]);
+                        acc[m] = dot2(e[3], p.w, acc[m]);
+                    }
+                } else {
+                    uint32_t e[8];
+                    extract_w2(wv[w], e, mv);
+#pragma unroll
+                    for (int m = 0; m < MT; ++m) {
+                        const uint4* src = hs + (m * UC + ul) * 8;
+                        const uint4 p0 = src[(2 * w) ^ (ul & 7)];
+                        const uint4 p1 = src[(2 * w + 1) ^ (ul & 7)];
+                        const uint32_t hp[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+                        for (int p = 0; p < 8; ++p) acc[m] = dot2(e[p], hp[p], acc[m]);
+                    }
                 }
             }
             const float sc = h2f(mti & 0xFFFFu), zc = h2f(mti >> 16);
@@ -397,8 +463,8 @@ __device__ __forceinline__ void dn_accumulate(DnItem<MT, S, MAXJ>& it, const uin
     }
 }
 
-template <int MT, int S, int MAXJ>
-__device__ __forceinline__ void dn_finish(DnItem<MT, S, MAXJ>& it, const DownArgs& a, int lane) {
+template <int MT, int S, int MAXJ, int B>
+__device__ __forceinline__ void dn_finish(DnItem<MT, S, MAXJ, B>& it, const DownArgs& a, int lane) {
     const int s = lane % S;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {

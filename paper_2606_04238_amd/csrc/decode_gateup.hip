@@ -1,85 +1,110 @@
 // Stand-alone decode kernels of the gate/up half: the LoRA-A projection
-// t = [A_g; A_u] x and the fused 2-bit gate/up dequant-matvec with the
-// LoRA-B term and the SiLU(G) * U epilogue (Sec. 3.1 Eq. (1), Sec. 3.3,
-// Sec. 4.2, Sec. 5).  qmlp_forward normally runs the single fused layer
-// kernel instead (decode_fused.hip); these serve qmlp_gateup_w2_lora and the
-// shapes the fused kernel does not cover.
-#include "decode_common.h"
-#include "decode_launch.h"
+// t = [A_g; A_u] x and the fused gate/up dequant-matvec with the LoRA-B term
+// and the SiLU(G) * U epilogue (Sec. 3.1 Eq. (1), Sec. 3.3, Sec. 4.2,
+// Sec. 5).  qmlp_forward normally runs the single fused layer kernel instead
+// (decode_fused.hip); these serve qmlp_gateup_w2_lora, the shapes and code
+// widths the fused kernel does not cover, and batches of independent blocks
+// (blockIdx.y = block), a single block being a batch of one.
+#include "decode_standalone.h"
 
 namespace qmlp {
 
-// One wave per row c of [A_g; A_u].
+QMLP_SA_EXTERN
+
+// One wave per row c of [A_g; A_u] of block blockIdx.y.
 template <int MT>
 __global__ void __launch_bounds__(256)
-lora_a_kernel(const uint16_t* __restrict__ Ag, const uint16_t* __restrict__ Au,
-              const uint16_t* __restrict__ x, int M, int d, int r, float* __restrict__ t) {
+lora_a_kernel(BatchArgs b) {
+    const int l = blockIdx.y;
     const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-    if (wave >= 2 * r)
+    if (wave >= 2 * b.r)
         return;
-    lora_a_row<MT, (MT <= 4 ? 12 / MT : 1)>(Ag, Au, x, M, d, r, wave, t, threadIdx.x & 63);
+    lora_a_row<MT, (MT <= 4 ? 12 / MT : 1)>(b.lay[l].Ag, b.lay[l].Au, b.x + (long)l * b.M * b.d,
+                                            b.M, b.d, b.r, wave, b.t + (long)l * b.M * 2 * b.r,
+                                            threadIdx.x & 63);
 }
 
-// Four waves per block, one gate/up item (64/S row pairs) per wave.
-template <int MT, int S, int MAXJ>
-__global__ void __launch_bounds__(256)
-gateup_w2_kernel(GateUpArgs a) {
-    extern __shared__ uint4 smem[];
-    const int UC = a.uc;
-    uint4* xs = smem;
-    float2* cx = reinterpret_cast<float2*>(smem + MT * UC * 8);
-    const int tid = threadIdx.x, lane = tid & 63;
-    GuItem<MT, S, MAXJ> it;
-    gu_load(it, a, (blockIdx.x * (blockDim.x >> 6) + (tid >> 6)) * (64 / S), true, lane);
-    const int U = a.d / 64;
-    for (int u0 = 0; u0 < U; u0 += UC) {
-        const int uc = min(UC, U - u0);
-        __syncthreads();
-        stage_x<MT>(xs, cx, UC, a.x, a.M, a.d, u0, uc, tid, blockDim.x);
-        __syncthreads();
-        gu_accumulate(it, xs, cx, UC, a.d, u0, uc, lane);
-    }
-    gu_finish(it, a, a.t, a.h, lane);
-}
-
-hipError_t launch_lora_a(const uint16_t* Ag, const uint16_t* Au, const uint16_t* x, int M, int d,
-                         int r, float* t, hipStream_t st) {
-    const unsigned blocks = (unsigned)((2 * r * 64 + 255) / 256);
-    switch (mtile_for(M)) {
-    case 1: lora_a_kernel<1><<<blocks, 256, 0, st>>>(Ag, Au, x, M, d, r, t); break;
-    case 2: lora_a_kernel<2><<<blocks, 256, 0, st>>>(Ag, Au, x, M, d, r, t); break;
-    case 4: lora_a_kernel<4><<<blocks, 256, 0, st>>>(Ag, Au, x, M, d, r, t); break;
-    case 8: lora_a_kernel<8><<<blocks, 256, 0, st>>>(Ag, Au, x, M, d, r, t); break;
-    default: lora_a_kernel<16><<<blocks, 256, 0, st>>>(Ag, Au, x, M, d, r, t); break;
+hipError_t launch_lora_a_batch(const BatchArgs& b, int nb, hipStream_t st) {
+    const dim3 grid((unsigned)((2 * b.r * 64 + 255) / 256), (unsigned)nb);
+    switch (mtile_for(b.M)) {
+    case 1: lora_a_kernel<1><<<grid, 256, 0, st>>>(b); break;
+    case 2: lora_a_kernel<2><<<grid, 256, 0, st>>>(b); break;
+    case 4: lora_a_kernel<4><<<grid, 256, 0, st>>>(b); break;
+    case 8: lora_a_kernel<8><<<grid, 256, 0, st>>>(b); break;
+    default: lora_a_kernel<16><<<grid, 256, 0, st>>>(b); break;
     }
     return hipGetLastError();
 }
 
-#define QMLP_GU_CASE(MT_, S_, J_)                                                         \
-    if (mt == MT_ && S == S_ && mj == J_) {                                               \
-        auto k = gateup_w2_kernel<MT_, S_, J_>;                                           \
-        hipError_t e = set_lds(k, lds);                                                   \
-        if (e != hipSuccess) return e;                                                    \
-        k<<<grid, 256, lds, st>>>(args);                                                  \
-        return hipGetLastError();                                                         \
-    }
-#define QMLP_GU_S(MT_, S_) QMLP_GU_CASE(MT_, S_, 8) QMLP_GU_CASE(MT_, S_, 16)
-#define QMLP_GU_MT(MT_) QMLP_GU_S(MT_, 8) QMLP_GU_S(MT_, 16) QMLP_GU_S(MT_, 32) QMLP_GU_S(MT_, 64)
-
-hipError_t launch_gateup(GateUpArgs args, hipStream_t st) {
-    const int U = args.d / 64;
-    const int S = lanes_gateup(U);
-    const int J = (U + S - 1) / S;
-    const int mj = maxj_for(J);
-    const int mt = mtile_for(args.M);
-    args.uc = units_per_chunk(U, S, GU_UNIT_BYTES, mt);
-    const size_t lds = (size_t)mt * args.uc * GU_UNIT_BYTES;
-    const int rows_per_block = 4 * (64 / S);
-    const dim3 grid((args.f + rows_per_block - 1) / rows_per_block);
-    QMLP_GU_MT(1) QMLP_GU_MT(2) QMLP_GU_MT(4) QMLP_GU_MT(8) QMLP_GU_MT(16)
+// Launch shape of the gate/up kernel: 256-thread blocks with the lanes of
+// lanes_for, single blocks and batches alike (a sweep of 1024-thread blocks
+// and of the fewest lanes per row over the Qwen3-4B widths at one token
+// and the Qwen3-8B block at 4 and 16 tokens found nothing faster: x is a
+// small share of a block's bytes).
+hipError_t launch_gateup_batch(const BatchArgs& b, int nb, hipStream_t st) {
+    if (nb < 1 || nb > kBatchMax)
+        return hipErrorInvalidValue;
+    const int S = lanes_for(b.d / (128 / b.bg), b.bg);
+    if (b.bg == 4)
+        return launch_gateup_bits<4, false, 256>(b, nb, S, st);
+    if (b.bg == 2 && b.gg == 32)
+        return launch_gateup_bits<2, true, 256>(b, nb, S, st);
+    if (b.bg == 2)
+        return launch_gateup_bits<2, false, 256>(b, nb, S, st);
     return hipErrorInvalidValue;
 }
 
+// A single block as a batch of one.
+static BatchArgs single_gateup(const GateUpArgs& a) {
+    BatchArgs b{};
+    StackLayerDesc& w = b.lay[0];
+    w.cg = a.cg;
+    w.mg = a.mg;
+    w.cu = a.cu;
+    w.mu = a.mu;
+    w.Bg = a.Bg;
+    w.Bu = a.Bu;
+    w.lora_scale = a.lora_scale;
+    b.x = a.x;
+    b.h = a.h;
+    b.t = const_cast<float*>(a.t);
+    b.M = a.M;
+    b.d = a.d;
+    b.f = a.f;
+    b.r = a.r;
+    b.gg = a.g;
+    b.bg = a.bits;
+    return b;
+}
+
+hipError_t launch_lora_a(const uint16_t* Ag, const uint16_t* Au, const uint16_t* x, int M, int d,
+                         int r, float* t, hipStream_t st) {
+    BatchArgs b{};
+    b.lay[0].Ag = Ag;
+    b.lay[0].Au = Au;
+    b.x = x;
+    b.t = t;
+    b.M = M;
+    b.d = d;
+    b.r = r;
+    return launch_lora_a_batch(b, 1, st);
+}
+
+hipError_t launch_gateup(GateUpArgs args, hipStream_t st) {
+    return launch_gateup_batch(single_gateup(args), 1, st);
+}
+
 bool decode_shape_supported(int d, int f) { return decode_shape_supported_impl(d, f); }
+
+bool decode_variant_supported(int d, int f, int bg, int gg, int bd, int gd) {
+    if ((bg != 2 && bg != 4) || (bd != 2 && bd != 4))
+        return false;
+    if (gg != 32 && gg != 64 && gg != 128)
+        return false;
+    if ((gd != 32 && gd != 64 && gd != 128) || (bd == 2 && gd == 32))
+        return false;
+    return d % 64 == 0 && f % 64 == 0 && d % gg == 0 && f % gd == 0 && units_fit(d, bg) &&
+           units_fit(f, bd);
+}
 
 }  // namespace qmlp

@@ -12,6 +12,18 @@ inline int mtile_for(int M) { return M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : M <=
 inline int lanes_gateup(int U) { return U <= 128 ? 8 : U <= 256 ? 16 : U <= 512 ? 32 : 64; }
 inline int lanes_down(int U) { return U <= 64 ? 8 : U <= 128 ? 16 : U <= 256 ? 32 : 64; }
 inline int maxj_for(int J) { return J <= 8 ? 8 : 16; }
+// Lanes per row for 16-byte units of `bits`-bit codes (64 codes per unit at
+// 2 bits, 32 at 4 bits): each width keeps the policy of its own unit size.
+inline int lanes_for(int U, int bits) { return bits == 2 ? lanes_gateup(U) : lanes_down(U); }
+// The fewest lanes per row that keep every lane within 16 units: the most
+// loads in flight per lane, for launches whose parallelism comes from many
+// blocks (batches).
+inline int lanes_fewest(int U) { return U <= 128 ? 8 : U <= 256 ? 16 : U <= 512 ? 32 : 64; }
+inline bool units_fit(int k, int bits) {
+    const int U = k / (128 / bits);
+    const int S = lanes_for(U, bits);
+    return (U + S - 1) / S <= 16;
+}
 
 constexpr int kLdsBudget = 64 * 1024;
 

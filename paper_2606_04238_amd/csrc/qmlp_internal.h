@@ -20,6 +20,7 @@ struct GateUpArgs {
     int M, d, f, g, r;
     int uc;                  // units per LDS chunk (set by the launcher)
     float lora_scale;
+    int bits;                // code width of gate and up: 2, or 4 (uniform-W4 baseline)
 };
 
 struct DownArgs {
@@ -29,6 +30,7 @@ struct DownArgs {
     uint16_t* y;             // [M][d] binary16
     int M, d, f, g;
     int uc;
+    int bits;                // code width of down: 4, or 2 (uniform-W2 baseline)
 };
 
 hipError_t launch_pack(int bits, const float* W, int n, int k, int g, uint32_t* codes,
@@ -44,6 +46,10 @@ hipError_t launch_lora_a(const uint16_t* Ag, const uint16_t* Au, const uint16_t*
 hipError_t launch_gateup(GateUpArgs args, hipStream_t st);
 hipError_t launch_down(DownArgs args, hipStream_t st);
 bool decode_shape_supported(int d, int f);
+// Stand-alone decode kernels at gate/up code width bg with group gg and down
+// code width bd (bg, bd in {2, 4}; group 32 only for gate/up, at either width,
+// and for down at 4 bits).
+bool decode_variant_supported(int d, int f, int bg, int gg, int bd, int gd);
 
 // One kernel per layer (decode_fused.hip).  ctl: the 1 KB control block at
 // the start of the workspace (zero before the first call); t64 [grid][256]
@@ -76,6 +82,26 @@ struct StackLayerDesc {
     float lora_scale;
 };
 bool stack_supported(int M, int d, int f, int g, int r);
+
+// A batch of up to kBatchMax independent decode blocks of one shape for the
+// stand-alone kernels (blockIdx.y = block l): block l's weights come from
+// lay[l], its activations sit at offset l of the batch buffers: x and y
+// [nb][M][d], h [nb][M][f], t [nb][M][2r].  A single block is a batch of one.
+constexpr int kBatchMax = 40;
+struct BatchArgs {
+    StackLayerDesc lay[kBatchMax];
+    const uint16_t* x;
+    uint16_t* y;
+    uint16_t* h;
+    float* t;
+    int M, d, f, r;
+    int gg, bg;              // gate/up group and code width
+    int gd, bd;              // down group and code width
+    int uc;                  // units per LDS chunk (set by the launcher)
+};
+hipError_t launch_lora_a_batch(const BatchArgs& b, int nb, hipStream_t st);
+hipError_t launch_gateup_batch(const BatchArgs& b, int nb, hipStream_t st);
+hipError_t launch_down_batch(const BatchArgs& b, int nb, hipStream_t st);
 size_t stack_ws_bytes(int d, int f, int r);
 int stack_max_layers();
 hipError_t launch_stack(const StackLayerDesc* layers, int L, int d, int f, int g, int r,

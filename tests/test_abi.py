@@ -85,7 +85,9 @@ def test_forward_validation(q, lib):
     no_a = _mlp(q, A=0)
     assert _fwd(lib, no_a) == NULL
     m2 = _mlp(q)
-    m2.down.bits = 2
+    m2.down.bits = 3
+    assert _fwd(lib, m2) == UNSUP
+    m2.down.bits, m2.down.group = 2, 32             # 2-bit down needs whole 64-code units per group
     assert _fwd(lib, m2) == UNSUP
     m3 = _mlp(q)
     m3.up.n_out = 448
@@ -94,7 +96,9 @@ def test_forward_validation(q, lib):
     m4.gate.codes = FAKE + 8
     assert _fwd(lib, m4) == ALIGN
     m5 = _mlp(q)
-    m5.gate.group = 32
+    m5.gate.group = 32                              # gate and up must share the group
+    assert _fwd(lib, m5) == SHAPE
+    m5.gate.group = m5.up.group = 96
     assert _fwd(lib, m5) == UNSUP
     # M == 0 is a no-op that succeeds without touching the device
     assert _fwd(lib, m, M=0) == OK
@@ -215,8 +219,84 @@ def test_layers_validation(q, lib):
     assert lib.qmlp_layers_launches(odd, 2, 1, 0) == 0
     bad = _stack_arr(q, m, _mlp(q, rank=7))
     assert fl(bad, 2) == UNSUP
-    # without a GPU no shape runs persistently: one forward per block, and
-    # the workspace is the per-block one
-    assert lib.qmlp_layers_launches(arr, 2, 1, 0) == 2 * lib.qmlp_forward_launches(ctypes.byref(m), 1, 0)
-    assert lib.qmlp_layers_workspace_bytes(arr, 2, 1, 0) == lib.qmlp_workspace_bytes(ctypes.byref(m), 1, 0)
-    assert lib.qmlp_layers_workspace_bytes(arr, 2, 1, 1) == lib.qmlp_workspace_bytes(ctypes.byref(m), 1, 1)
+    # without a GPU no shape runs persistently: binary16 blocks run as one
+    # batch on the stand-alone kernels (LoRA-A, gate/up, down of every block),
+    # the workspace holding the control block, t and h of every block
+    assert lib.qmlp_layers_launches(arr, 2, 1, 0) == 3
+    r256 = lambda v: (v + 255) // 256 * 256
+    assert lib.qmlp_layers_workspace_bytes(arr, 2, 3, 0) == 1024 + r256(2 * 3 * 16 * 4) + r256(2 * 3 * 512 * 2)
+    big = _stack_arr(q, *[_mlp(q) for _ in range(41)])
+    assert lib.qmlp_layers_launches(big, 41, 1, 0) == 6        # batches of at most 40 blocks
+    assert lib.qmlp_layers_workspace_bytes(big, 41, 1, 0) == 1024 + r256(40 * 16 * 4) + r256(40 * 512 * 2)
+    # bfloat16 runs qmlp_forward per block
+    assert lib.qmlp_layers_workspace_bytes(arr, 2, 128, 1) == lib.qmlp_workspace_bytes(ctypes.byref(m), 128, 1)
+    assert lib.qmlp_layers_launches(arr, 2, 128, 1) == 2 * lib.qmlp_forward_launches(ctypes.byref(m), 128, 1)
+
+
+def _variant(q, bg=2, gg=64, bd=4, gd=64, d=256, f=512, rank=8):
+    m = _mlp(q, d=d, f=f, rank=rank)
+    m.gate.bits = m.up.bits = bg
+    m.gate.group = m.up.group = gg
+    m.down.bits, m.down.group = bd, gd
+    return m
+
+
+def test_precision_variants_validation(q, lib):
+    """Uniform W4, uniform W2 and 2-bit group 32 (Sec. 5.2, Sec. 3.3) are
+    accepted on the binary16 decode path and run on the stand-alone kernels
+    (never the one-kernel layer); they are rejected on the prefill path, by
+    qmlp_gateup_w2_lora at 4 bits, and in a stack mixing widths."""
+    P = ctypes.c_void_p
+    for kw in (dict(bg=4, gg=128, bd=4, gd=128), dict(bg=2, bd=2), dict(bg=2, gg=32),
+               dict(bg=4, gg=32, bd=4, gd=32)):
+        m = _variant(q, **kw)
+        assert lib.qmlp_workspace_bytes(ctypes.byref(m), 1, 0) > 0, kw
+        assert lib.qmlp_forward_launches(ctypes.byref(m), 1, 0) == 3, kw    # LoRA-A, gate/up, down
+        m.rank = 0
+        assert lib.qmlp_forward_launches(ctypes.byref(m), 4, 0) == 2, kw
+        assert lib.qmlp_workspace_bytes(ctypes.byref(m), 256, 1) == 0, kw   # no prefill form
+        assert _fwd(lib, m, M=256, dtype=1) == UNSUP, kw
+        assert _fwd(lib, m, M=0) == OK
+    w4 = _variant(q, bg=4)
+    assert lib.qmlp_gateup_w2_lora(ctypes.byref(w4), P(FAKE), 1, 0, P(FAKE), P(FAKE), 1 << 30,
+                                   None) == UNSUP
+    g32 = _variant(q, gg=32)
+    assert lib.qmlp_gateup_w2_lora(ctypes.byref(g32), P(FAKE), 1, 0, P(FAKE), P(0), 1 << 30,
+                                   None) == WS
+    assert _fwd(lib, _variant(q, bg=4, gg=128, d=320), M=1) == SHAPE   # d not a multiple of g
+    # the 4-bit down entry takes group 32 on the decode path, not on the prefill path
+    w = _qw(q, bits=4, n=256, k=512, g=32)
+    assert lib.qmlp_down_w4(ctypes.byref(w), None, 1, 0, P(FAKE), None) == NULL
+    assert lib.qmlp_down_w4(ctypes.byref(w), P(FAKE), 128, 1, P(FAKE), None) == UNSUP
+    # pack at group 32
+    out = _qw(q)
+    assert lib.qmlp_pack_w2(P(FAKE), 16, 200, 32, ctypes.byref(out), None, None) == SHAPE
+    # every block of a stack / layer list has the same widths
+    mixed = _stack_arr(q, _mlp(q), _variant(q, bg=4))
+    assert lib.qmlp_forward_layers(mixed, 2, P(FAKE), 1, 0, P(FAKE), P(FAKE), 1 << 30, None) == SHAPE
+    same = _stack_arr(q, _variant(q, bg=4, rank=0), _variant(q, bg=4, rank=0))
+    assert lib.qmlp_layers_launches(same, 2, 1, 0) == 2               # one batch, no LoRA-A
+
+
+def test_batch_validation(q, lib):
+    """qmlp_forward_batch: binary16 only; workspace = control block + t + h of
+    at most 40 blocks."""
+    P = ctypes.c_void_p
+    arr = _stack_arr(q, _mlp(q), _mlp(q), _mlp(q))
+
+    def fb(a, L, M=1, dt=0, x=FAKE, y=FAKE, ws=FAKE, wsb=1 << 30):
+        return lib.qmlp_forward_batch(a, L, P(x), M, dt, P(y), P(ws), wsb, None)
+
+    assert lib.qmlp_forward_batch(None, 3, None, 1, 0, None, None, 0, None) == NULL
+    assert fb(arr, 0) == SHAPE
+    assert fb(arr, 3, dt=1, M=128) == UNSUP
+    assert fb(arr, 3, x=0) == NULL
+    assert fb(arr, 3, y=FAKE + 4) == ALIGN
+    assert fb(arr, 3, M=0) == OK
+    need = lib.qmlp_batch_workspace_bytes(arr, 3, 2, 0)
+    assert need == 1024 + 512 + 3 * 2 * 512 * 2            # t: 3 x 2 x 16 fp32 in 256-B units
+    assert fb(arr, 3, M=2, wsb=need - 1) == WS
+    assert fb(arr, 3, M=2, ws=FAKE + 16 * 3 + 8) == ALIGN
+    assert lib.qmlp_batch_workspace_bytes(arr, 3, 128, 1) == 0
+    mixed = _stack_arr(q, _mlp(q), _variant(q, bd=2))
+    assert fb(mixed, 2) == SHAPE

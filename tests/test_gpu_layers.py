@@ -195,15 +195,22 @@ def test_layers_qwen3_8b_match_oracle(q):
     _check(layers, y)
 
 
-def test_layers_fallback_shapes_run_per_block(q):
-    """Shapes outside the persistent kernel (M > 1) run qmlp_forward per block."""
-    small = wl.Config("layers_m4", M=4, d=512, f=1536, g=64, r=8, L=3)
-    _announce("layers fallback", small.name)
-    layers, mlps, ls, x = _blocks(q, small, 3)
-    assert q.layers_launches(ls, 4) == 3 * q.forward_launches(mlps[0], 4)
+@pytest.mark.parametrize("M,L", [(4, 3), (13, 5), (2, 41)])
+def test_layers_batched_shapes_match_oracle(q, M, L):
+    """Shapes outside the persistent kernel (M > 1) run in batches of up to
+    40 blocks on the stand-alone kernels (LoRA-A, gate/up and down of every
+    block of a batch); 41 blocks take two batches that reuse t and h."""
+    small = wl.Config("layers_m%d" % M, M=M, d=512, f=1536, g=64, r=8, L=L)
+    _announce("layers batched", small.name, "L", L)
+    layers, mlps, ls, x = _blocks(q, small, L)
+    assert q.layers_launches(ls, M) == 3 * ((L + 39) // 40)
     y = q.forward_layers(ls, x)
     torch.cuda.synchronize()
-    _check(layers, y)
+    _check(layers, y, which=None if L <= 5 else (0, 1, 39, 40))
+    wsl = q.workspace(mlps[0], M)
+    for i in ((0, L - 1) if L > 5 else range(L)):
+        yl = q.forward(mlps[i], x[i], ws=wsl)
+        assert orc.max_rel_err(values_of(y[i]), values_of(yl)) <= Y_TOL
 
 
 def test_layers_qwen3_4b_full_depth_sampled(q):
@@ -228,3 +235,21 @@ def test_layers_qwen3_4b_full_depth_sampled(q):
     print("max-rel vs per-block forward: %.2e" % worst)
     assert worst <= Y_TOL
     assert np.isfinite(values_of(y)).all()
+
+
+def test_forward_batch_forces_standalone_kernels(q):
+    """forward_batch runs the 4B blocks (a persistent shape for forward_layers)
+    as one batch on the stand-alone kernels; both match the oracle and each
+    other within the bar; a second call on the same workspace repeats the
+    bits."""
+    cfg = wl.CONFIGS["qwen3_4b"]
+    _announce("forward_batch", cfg.name, "L", 5)
+    layers, mlps, ls, x = _blocks(q, cfg, 5, first=7)
+    ws = q.batch_workspace(ls, 1)
+    y1 = q.forward_batch(ls, x, ws=ws).clone()
+    y2 = q.forward_batch(ls, x, ws=ws)
+    yl = q.forward_layers(ls, x)
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+    _check(layers, y1)
+    assert orc.max_rel_err(values_of(y1), values_of(yl)) <= Y_TOL

@@ -139,7 +139,7 @@ def test_meta_interleave_is_scale_then_zero():
 
 
 # ------------------------------------------------------ quantizer closed forms
-@pytest.mark.parametrize("bits,group", [(2, 64), (2, 128), (4, 64), (4, 128)])
+@pytest.mark.parametrize("bits,group", [(2, 32), (2, 64), (2, 128), (4, 32), (4, 64), (4, 128)])
 def test_on_grid_weights_reconstruct_exactly(bits, group):
     """Weights w = s (q - z) with s binary16, integer z, and both 0 and qmax
     present in every group reconstruct exactly: hi - lo = s*qmax exactly, so
@@ -167,7 +167,7 @@ def test_on_grid_weights_reconstruct_exactly(bits, group):
 
 
 @pytest.mark.parametrize("bits,group,outliers", [(2, 64, False), (2, 128, True), (4, 128, False),
-                                                 (4, 64, True)])
+                                                 (4, 64, True), (2, 32, True), (4, 32, False)])
 def test_error_bound_and_zero_on_grid(bits, group, outliers):
     """|w - w_hat| <= s16/2 + qmax |s - s16| for every weight, with s the exact
     fp64 range/qmax computed here by numpy; zero weights dequantize to 0."""
@@ -230,14 +230,19 @@ def _numpy_forward(cfg, layer, qg, qu, qd, lora_scale=1.0):
     return h @ deq(qd).T, h
 
 
-@pytest.mark.parametrize("cfgkw", [dict(), dict(M=1, d=512, f=1536, g=64, r=8),
-                                   dict(M=5, g=128, r=16), dict(act="bf16", M=4, r=32)])
-def test_forward_matches_numpy_brute_force(cfgkw):
+@pytest.mark.parametrize("cfgkw,widths", [
+    (dict(), (2, None, 4, None)), (dict(M=1, d=512, f=1536, g=64, r=8), (2, None, 4, None)),
+    (dict(M=5, g=128, r=16), (2, None, 4, None)), (dict(act="bf16", M=4, r=32), (2, None, 4, None)),
+    # the comparison points of Sec. 5.2 and the paper's INT2 grouping (Sec. 3.3)
+    (dict(M=2, g=128), (4, None, 4, None)), (dict(M=3, g=64), (2, None, 2, None)),
+    (dict(M=4, g=128), (2, 32, 4, None))])
+def test_forward_matches_numpy_brute_force(cfgkw, widths):
     cfg = _small_cfg(**cfgkw)
     L = wl.layer(cfg, 0)
-    qg = orc.quantize(L.W_gate, 2, cfg.g)
-    qu = orc.quantize(L.W_up, 2, cfg.g)
-    qd = orc.quantize(L.W_down, 4, cfg.g)
+    bg, gg, bd, gd = widths
+    qg = orc.quantize(L.W_gate, bg, gg or cfg.g)
+    qu = orc.quantize(L.W_up, bg, gg or cfg.g)
+    qd = orc.quantize(L.W_down, bd, gd or cfg.g)
     y, h = orc.forward(qg, qu, qd, L.A_gate, L.B_gate, L.A_up, L.B_up, L.x,
                        lora_scale=0.75, bf16=cfg.bf16, return_h=True)
     y_ref, h_ref = _numpy_forward(cfg, L, qg, qu, qd, lora_scale=0.75)
