@@ -160,8 +160,12 @@ def quantize(W: np.ndarray, bits: int, group: int) -> QTensor:
 
 
 def pack(codes: np.ndarray, bits: int) -> np.ndarray:
+    """Codes [n][k] -> the packed words of the storage format (see qmlp_oracle.c;
+    at 3 bits the two-plane layout, k a multiple of 64)."""
     codes = _c(codes, np.uint8)
     n, k = codes.shape
+    if bits == 3 and k % 64:
+        raise ValueError("3-bit rows hold a multiple of 64 codes")
     words = np.empty((n, k * bits // 32), np.uint32)
     _load().orc_pack(_p(codes), n, k, bits, _p(words))
     return words

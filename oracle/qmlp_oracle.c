@@ -171,9 +171,46 @@ long orc_quantize(const float *W, long n, long k, long g, int bits,
 /*
  * Packed codes: row-major; each row is a run of little-endian 32-bit words,
  * code i of a row sits at bits [b*(i mod 32/b), +b) of word i / (32/b).
+ *
+ * 3 bits (the W3 variant of Appendix B; the paper fixes no layout): a row is
+ * k*3/32 words, first a plane holding the low two bits of every code in the
+ * 2-bit layout (k/16 words), then a plane holding the high bit of every code,
+ * code i at bit (i mod 32) of word i/32 of that plane (k/32 words).
  */
+static void pack3(const uint8_t *codes, long n, long k, uint32_t *words)
+{
+    const long wpr = k * 3 / 32;
+    for (long row = 0; row < n; ++row) {
+        uint32_t *lo = words + row * wpr, *hi = lo + k / 16;
+        for (long wd = 0; wd < wpr; ++wd)
+            lo[wd] = 0;
+        for (long i = 0; i < k; ++i) {
+            uint32_t c = codes[row * k + i];
+            lo[i / 16] += (c % 4) * (uint32_t)(1u << (2 * (i % 16)));
+            hi[i / 32] += (c / 4) * (uint32_t)(1u << (i % 32));
+        }
+    }
+}
+
+static void unpack3(const uint32_t *words, long n, long k, uint8_t *codes)
+{
+    const long wpr = k * 3 / 32;
+    for (long row = 0; row < n; ++row) {
+        const uint32_t *lo = words + row * wpr, *hi = lo + k / 16;
+        for (long i = 0; i < k; ++i) {
+            uint32_t l = (lo[i / 16] / (1u << (2 * (i % 16)))) % 4;
+            uint32_t h = (hi[i / 32] / (1u << (i % 32))) % 2;
+            codes[row * k + i] = (uint8_t)(l + 4 * h);
+        }
+    }
+}
+
 void orc_pack(const uint8_t *codes, long n, long k, int bits, uint32_t *words)
 {
+    if (bits == 3) {
+        pack3(codes, n, k, words);
+        return;
+    }
     const long per = 32 / bits;
     const long wpr = k / per;       /* words per row */
     for (long row = 0; row < n; ++row)
@@ -189,6 +226,10 @@ void orc_pack(const uint8_t *codes, long n, long k, int bits, uint32_t *words)
 
 void orc_unpack(const uint32_t *words, long n, long k, int bits, uint8_t *codes)
 {
+    if (bits == 3) {
+        unpack3(words, n, k, codes);
+        return;
+    }
     const long per = 32 / bits;
     const long wpr = k / per;
     const uint32_t mask = (1u << bits) - 1;

@@ -118,6 +118,17 @@ def test_packing_hand_written_words(golden_dir):
         assert np.array_equal(orc.unpack(words, codes.shape[1], case["bits"]), codes)
 
 
+def test_pack3_unpack_roundtrip():
+    """3 bits: the two planes reassemble every code; the low plane equals the
+    2-bit packing of the codes' low bits."""
+    rng = np.random.default_rng(5)
+    codes = rng.integers(0, 8, size=(19, 256), dtype=np.uint8)
+    words = orc.pack(codes, 3)
+    assert words.shape == (19, 256 * 3 // 32)
+    assert np.array_equal(orc.unpack(words, 256, 3), codes)
+    assert np.array_equal(words[:, :16], orc.pack(codes % 4, 2))
+
+
 @pytest.mark.parametrize("bits", [2, 4])
 def test_pack_unpack_roundtrip(bits):
     rng = np.random.default_rng(3)
@@ -139,7 +150,8 @@ def test_meta_interleave_is_scale_then_zero():
 
 
 # ------------------------------------------------------ quantizer closed forms
-@pytest.mark.parametrize("bits,group", [(2, 32), (2, 64), (2, 128), (4, 32), (4, 64), (4, 128)])
+@pytest.mark.parametrize("bits,group", [(2, 32), (2, 64), (2, 128), (3, 32), (3, 128), (4, 32), (4, 64),
+                                        (4, 128)])
 def test_on_grid_weights_reconstruct_exactly(bits, group):
     """Weights w = s (q - z) with s binary16, integer z, and both 0 and qmax
     present in every group reconstruct exactly: hi - lo = s*qmax exactly, so
@@ -167,7 +179,8 @@ def test_on_grid_weights_reconstruct_exactly(bits, group):
 
 
 @pytest.mark.parametrize("bits,group,outliers", [(2, 64, False), (2, 128, True), (4, 128, False),
-                                                 (4, 64, True), (2, 32, True), (4, 32, False)])
+                                                 (4, 64, True), (2, 32, True), (4, 32, False),
+                                                 (3, 32, True), (3, 64, False)])
 def test_error_bound_and_zero_on_grid(bits, group, outliers):
     """|w - w_hat| <= s16/2 + qmax |s - s16| for every weight, with s the exact
     fp64 range/qmax computed here by numpy; zero weights dequantize to 0."""
@@ -235,7 +248,7 @@ def _numpy_forward(cfg, layer, qg, qu, qd, lora_scale=1.0):
     (dict(M=5, g=128, r=16), (2, None, 4, None)), (dict(act="bf16", M=4, r=32), (2, None, 4, None)),
     # the comparison points of Sec. 5.2 and the paper's INT2 grouping (Sec. 3.3)
     (dict(M=2, g=128), (4, None, 4, None)), (dict(M=3, g=64), (2, None, 2, None)),
-    (dict(M=4, g=128), (2, 32, 4, None))])
+    (dict(M=4, g=128), (2, 32, 4, None)), (dict(M=2, g=128), (3, 32, 4, None))])
 def test_forward_matches_numpy_brute_force(cfgkw, widths):
     cfg = _small_cfg(**cfgkw)
     L = wl.layer(cfg, 0)
