@@ -28,7 +28,8 @@ qmlp_forward launch per block.
 precision_comparison: the MLP-level analogue of the paper's Gain and
 Capture (Sec. 5.2) on this GPU.  The same fp32 weights are packed as uniform
 W4 (gate/up and down at 4 bits), uniform W2, W4/W2-GateUp with its LoRA
-adapters, and W4/W2-GateUp with the paper's INT2 group of 32; all four run
+adapters, W4/W2-GateUp with the paper's INT2 group of 32, and the 3-bit
+gate/up of Appendix B at group 32; all five run
 on the same stand-alone decode kernels (qmlp_forward_batch: LoRA-A, gate/up
 and down of every block in one launch each; one pass over the 36 blocks
 captured in a HIP graph), so the comparison isolates the bit widths:  Gain = TPS_mix / TPS_W4 - 1,  Capture = (TPS_mix - TPS_W4) /
@@ -89,6 +90,7 @@ VARIANTS = {
     "w2_uniform": (2, None, 2, None, False),
     "w4w2_gateup_lora": (2, None, 4, None, True),
     "w4w2_gateup_g32_lora": (2, 32, 4, None, True),
+    "w4w3_gateup_g32_lora": (3, 32, 4, None, True),        # the W3 variant of Appendix B
 }
 
 
@@ -133,7 +135,7 @@ def build_stack(cfg: wl.Config, seed: int = 0, layers: int | None = None, thread
             mlps.append(q.MLP(g, u, d, *lo, lora_scale=cfg.lora_scale))
             for name in var:
                 bg, gg, bd, gd, lora = variant_widths(cfg, name)
-                pk = {2: q.pack_w2, 4: q.pack_w4}
+                pk = {2: q.pack_w2, 3: q.pack_w3, 4: q.pack_w4}
                 vg, vu, vd = pk[bg](Wg, gg), pk[bg](Wu, gg), pk[bd](Wd, gd)
                 var[name].append(q.MLP(vg, vu, vd, *(lo if lora else ()),
                                        lora_scale=cfg.lora_scale))
@@ -227,7 +229,7 @@ def precision_comparison(stack: Stack, seed: int, steps: int, min_warm_s: float,
     out = {"kernels": "qmlp_forward_batch: stand-alone decode kernels, one launch each for "
                       "LoRA-A, gate/up and down of up to 40 blocks; HIP graph over %d blocks" % L,
            "variants": res}
-    for name in ("w4w2_gateup_lora", "w4w2_gateup_g32_lora"):
+    for name in ("w4w2_gateup_lora", "w4w2_gateup_g32_lora", "w4w3_gateup_g32_lora"):
         tm, bm = res[name]["us_per_mlp_step"], variant_bytes(cfg, name)
         out[name] = {
             "gain_pct": round((t4 / tm - 1) * 100, 1),

@@ -37,6 +37,10 @@
  *  - codes: row-major, each row a run of little-endian 32-bit words; code i
  *    of a row sits at bits [b*(i mod 32/b), +b) of word i/(32/b) of that row
  *    (16 codes per word at b=2, 8 at b=4).  Size n*k*b/8 bytes.
+ *    At b=3 (Appendix B) a row is two planes: the low two bits of every code
+ *    in the 2-bit layout (k/16 words), then the high bit of every code, code
+ *    i at bit (i mod 32) of word i/32 of that plane (k/32 words); k % 128 == 0
+ *    (rows of 3k/8 bytes stay 16-byte aligned).
  *  - meta: row-major [n][k/g] pairs of binary16 (scale, zero), scale first.
  *    Size n*(k/g)*4 bytes.  The dequantized weight is scale * (q - zero).
  *  - Quantizer (round-to-nearest, asymmetric min-max; the paper fixes only
@@ -78,7 +82,7 @@ typedef void *qmlp_stream;
 
 /* Non-owning view of one packed quantized matrix in device memory. */
 typedef struct {
-    int32_t bits;     /* 2 (gate/up) or 4 (down); see qmlp_mlp for the other widths */
+    int32_t bits;     /* 2 (gate/up) or 4 (down); 3 for gate/up; see qmlp_mlp */
     int32_t n_out;    /* rows n of the logical W [n][k] */
     int32_t k_in;     /* columns k; groups run along k */
     int32_t group;    /* g: 32, 64 or 128; k_in % g == 0 */
@@ -93,10 +97,11 @@ typedef struct {
  * persistent launches, which take only that form) also runs the comparison
  * points of the throughput analysis (Sec. 5.2) and the paper's INT2 grouping
  * (Sec. 3.3, Sec. 4.1): gate/up at 4 bits (uniform W4), down at 2 bits
- * (uniform W2, groups of 64 or 128), and group 32 for gate/up (either
- * width) and for a 4-bit down. */
+ * (uniform W2, groups of 64 or 128), and group 32 for gate/up (any width)
+ * and for a 4-bit down; and the 3-bit gate/up of Appendix B (W3, group 32
+ * in the paper; 64 and 128 also accepted). */
 typedef struct {
-    qmlp_qweight gate;      /* bits 2 (or 4), [f][d] */
+    qmlp_qweight gate;      /* bits 2 (or 3, 4), [f][d] */
     qmlp_qweight up;        /* same bits and group as gate, [f][d] */
     qmlp_qweight down;      /* bits 4 (or 2), [d][f] */
     const void *A_gate;     /* [rank][d] activation type (nn.Linear / PEFT "lora_A") */
@@ -143,6 +148,11 @@ size_t qmlp_workspace_bytes(const qmlp_mlp *mlp, int M, qmlp_dtype dtype);
  * (32 is the paper's INT2 group).
  */
 qmlp_status qmlp_pack_w2(const float *W, int n_out, int k_in, int group,
+                         qmlp_qweight *out, int32_t *d_status, qmlp_stream stream);
+
+/* Appendix B: the same at 3 bits (the W3 gate/up variant), in the two-plane
+ * layout above.  Requires group in {32, 64, 128}, k_in % 128 == 0. */
+qmlp_status qmlp_pack_w3(const float *W, int n_out, int k_in, int group,
                          qmlp_qweight *out, int32_t *d_status, qmlp_stream stream);
 
 /* Sec. 3.3 / Sec. 7 step 4: the same at 4 bits (down projection and every

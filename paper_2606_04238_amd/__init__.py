@@ -67,6 +67,7 @@ def _lib():
             "qmlp_meta_bytes": (Z, [I, I, I]),
             "qmlp_workspace_bytes": (Z, [pm, I, I]),
             "qmlp_pack_w2": (I, [P, I, I, I, pq, P, P]),
+            "qmlp_pack_w3": (I, [P, I, I, I, pq, P, P]),
             "qmlp_pack_w4": (I, [P, I, I, I, pq, P, P]),
             "qmlp_gateup_w2_lora": (I, [pm, P, I, I, P, P, Z, P]),
             "qmlp_down_w4": (I, [pq, P, I, I, P, P]),
@@ -160,7 +161,7 @@ def _pack(bits: int, W: torch.Tensor, group: int) -> QWeight:
     meta = torch.empty(mb, dtype=torch.uint8, device=W.device)
     status = torch.zeros(1, dtype=torch.int32, device=W.device)
     qw = QWeightC(0, 0, 0, 0, codes.data_ptr(), meta.data_ptr())
-    fn = _lib().qmlp_pack_w2 if bits == 2 else _lib().qmlp_pack_w4
+    fn = {2: _lib().qmlp_pack_w2, 3: _lib().qmlp_pack_w3, 4: _lib().qmlp_pack_w4}[bits]
     _check(fn(_ptr(W), n, k, group, ctypes.byref(qw), _ptr(status), _stream()), "pack_w%d" % bits)
     return QWeight(qw.bits, qw.n_out, qw.k_in, qw.group, codes, meta, status)
 
@@ -168,6 +169,11 @@ def _pack(bits: int, W: torch.Tensor, group: int) -> QWeight:
 def pack_w2(W: torch.Tensor, group: int) -> QWeight:
     """Quantize fp32 W [n][k] (device) to 2-bit codes + fp16 scale/zero per group."""
     return _pack(2, W, group)
+
+
+def pack_w3(W: torch.Tensor, group: int) -> QWeight:
+    """Quantize fp32 W [n][k] (device) to 3-bit codes (two-plane layout) + fp16 scale/zero."""
+    return _pack(3, W, group)
 
 
 def pack_w4(W: torch.Tensor, group: int) -> QWeight:

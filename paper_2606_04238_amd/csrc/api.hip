@@ -21,13 +21,13 @@ qmlp_status from_hip(hipError_t e) { return e == hipSuccess ? QMLP_OK : QMLP_ERR
 qmlp_status check_qweight(const qmlp_qweight* w, int bits) {
     if (!w || !w->codes || !w->meta)
         return QMLP_ERR_NULL;
-    if (bits ? w->bits != bits : (w->bits != 2 && w->bits != 4))
+    if (bits ? w->bits != bits : (w->bits < 2 || w->bits > 4))
         return QMLP_ERR_UNSUPPORTED;
     if (w->n_out <= 0 || w->k_in <= 0)
         return QMLP_ERR_SHAPE;
     if (w->group != 32 && w->group != 64 && w->group != 128)
         return QMLP_ERR_UNSUPPORTED;
-    if (w->k_in % w->group != 0)
+    if (w->k_in % w->group != 0 || (w->bits == 3 && w->k_in % 128 != 0))
         return QMLP_ERR_SHAPE;
     if (!aligned16(w->codes) || !aligned16(w->meta))
         return QMLP_ERR_ALIGN;
@@ -57,7 +57,7 @@ qmlp_status check_mlp(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
         return QMLP_ERR_SHAPE;
     if (mlp->up.group != mlp->gate.group)
         return QMLP_ERR_SHAPE;
-    if (mlp->down.bits == 2 && mlp->down.group == 32)
+    if ((mlp->down.bits == 2 && mlp->down.group == 32) || mlp->down.bits == 3)
         return QMLP_ERR_UNSUPPORTED;
     if (d % 64 != 0 || f % 64 != 0)
         return QMLP_ERR_SHAPE;
@@ -219,7 +219,7 @@ qmlp_status pack_common(int bits, const float* W, int n_out, int k_in, int group
         return QMLP_ERR_SHAPE;
     if (group != 32 && group != 64 && group != 128)
         return QMLP_ERR_UNSUPPORTED;
-    if (k_in % group != 0)
+    if (k_in % group != 0 || (bits == 3 && k_in % 128 != 0))
         return QMLP_ERR_SHAPE;
     if (!aligned16(W) || !aligned16(out->codes) || !aligned16(out->meta))
         return QMLP_ERR_ALIGN;
@@ -359,7 +359,10 @@ qmlp_status run_layers_batched(const qmlp_mlp* layers, int L, const char* xb, in
 extern "C" {
 
 size_t qmlp_codes_bytes(int bits, int n_out, int k_in) {
-    if ((bits != 2 && bits != 4) || n_out <= 0 || k_in <= 0 || k_in % (32 / bits) != 0)
+    if (bits < 2 || bits > 4 || n_out <= 0 || k_in <= 0)
+        return 0;
+    // 3 bits: rows of 3k/8 bytes stay 16-byte aligned for k % 128 == 0
+    if (bits == 3 ? k_in % 128 != 0 : k_in % (32 / bits) != 0)
         return 0;
     return (size_t)n_out * (size_t)k_in * (size_t)bits / 8;
 }
@@ -382,6 +385,11 @@ size_t qmlp_workspace_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
 qmlp_status qmlp_pack_w2(const float* W, int n_out, int k_in, int group, qmlp_qweight* out,
                          int32_t* d_status, qmlp_stream stream) {
     return pack_common(2, W, n_out, k_in, group, out, d_status, stream);
+}
+
+qmlp_status qmlp_pack_w3(const float* W, int n_out, int k_in, int group, qmlp_qweight* out,
+                         int32_t* d_status, qmlp_stream stream) {
+    return pack_common(3, W, n_out, k_in, group, out, d_status, stream);
 }
 
 qmlp_status qmlp_pack_w4(const float* W, int n_out, int k_in, int group, qmlp_qweight* out,

@@ -109,6 +109,67 @@ __device__ __forceinline__ void stage_x(uint4* xs, float2* cx, int UC, const uin
         stage_x_store<MT, SPLIT>(xs, cx, UC, uc, M, idx, stage_x_load<MT>(x, M, d, u0, uc, idx));
 }
 
+// 3-bit units (stage_x3): x' exactly as stage_x for the 2-bit plane, then a
+// second region x'' (MT * UC * 8 chunks after x') for the 1-bit plane: per
+// (m, unit) 32 pairs (x[32h+i], x[32h+16+i]) / 256 in binary16, pair p in
+// chunk (p/4) ^ (unit & 7).  The (C, X) slot holds C = 1024 (sum x' + 4 sum x''),
+// both planes' magic offsets, per unit or per half unit (SPLIT).  Each lane
+// writes the 16 halves of its staging word into x'' one by one.
+template <int MT, bool SPLIT>
+__device__ __forceinline__ void stage_x3_store(uint4* xs, float2* cx, int UC, int uc, int M, int idx,
+                                               XWord v) {
+    const int words = MT * uc * 4;
+    const bool live = idx < words;
+    const int m = live ? idx / (uc * 4) : 0;
+    const int wl = live ? idx - m * uc * 4 : 0;
+    const int ul = wl >> 2, w = wl & 3;
+    const bool data = live && m < M;           // padding tokens stage zeros
+    const uint32_t xl[4] = {data ? v.lo.x : 0u, data ? v.lo.y : 0u, data ? v.lo.z : 0u, data ? v.lo.w : 0u};
+    const uint32_t xh[4] = {data ? v.hi.x : 0u, data ? v.hi.y : 0u, data ? v.hi.z : 0u, data ? v.hi.w : 0u};
+    uint32_t pr[8];
+    uint16_t x2[16];
+    float csum = 0.0f, xsum = 0.0f;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+        const uint32_t a16 = (xl[p >> 1] >> (16 * (p & 1))) & 0xFFFFu;     // x[p]
+        const uint32_t b16 = (xh[p >> 1] >> (16 * (p & 1))) & 0xFFFFu;     // x[8 + p]
+        const float sc = w2_pair_scale(p);
+        const uint32_t ha = f2h(h2f(a16) * sc), hb = f2h(h2f(b16) * sc);
+        pr[p] = ha | (hb << 16);
+        const uint32_t ta = f2h(h2f(a16) * (1.0f / 256)), tb = f2h(h2f(b16) * (1.0f / 256));
+        x2[p] = (uint16_t)ta;
+        x2[8 + p] = (uint16_t)tb;
+        csum += h2f(ha) + h2f(hb) + 4.0f * (h2f(ta) + h2f(tb));
+        xsum += h2f(a16) + h2f(b16);
+    }
+    csum = group_sum<SPLIT ? 2 : 4>(csum);
+    xsum = group_sum<SPLIT ? 2 : 4>(xsum);
+    if (live) {
+        uint4* dst = xs + (m * UC + ul) * 8;
+        dst[(2 * w) ^ (ul & 7)] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
+        dst[(2 * w + 1) ^ (ul & 7)] = make_uint4(pr[4], pr[5], pr[6], pr[7]);
+        // word w holds codes 16w..16w+15 of the unit: half h = w/2 of the pairs,
+        // the low (w even) or high (w odd) binary16 of each
+        uint16_t* d2 = reinterpret_cast<uint16_t*>(xs + MT * UC * 8 + (m * UC + ul) * 8);
+        const int h = w >> 1, part = w & 1;
+#pragma unroll
+        for (int t = 0; t < 16; ++t) {
+            const int pi = 16 * h + t;
+            d2[(((pi >> 2) ^ (ul & 7)) * 4 + (pi & 3)) * 2 + part] = x2[t];
+        }
+        if (SPLIT ? (w & 1) == 0 : w == 0)
+            cx[SPLIT ? (m * UC + ul) * 2 + (w >> 1) : m * UC + ul] = make_float2(1024.0f * csum, xsum);
+    }
+}
+
+template <int MT, bool SPLIT>
+__device__ __forceinline__ void stage_x3(uint4* xs, float2* cx, int UC, const uint16_t* x, int M,
+                                         int d, int u0, int uc, int tid, int nthreads) {
+    const int words = MT * uc * 4;
+    for (int idx = tid; idx < ((words + 63) & ~63); idx += nthreads)
+        stage_x3_store<MT, SPLIT>(xs, cx, UC, uc, M, idx, stage_x_load<MT>(x, M, d, u0, uc, idx));
+}
+
 // h' for 4-bit units [u0, u0+uc): per (m, unit) four 16-byte chunks (one per
 // code word, 4 pairs), chunk c stored at c ^ ((unit >> 1) & 3); then (C_u, X_u).
 // One staging word covers 8 codes of one token (one 16-byte load).
@@ -174,6 +235,7 @@ template <int MT, int S, int MAXJ, int B = 2, bool SPLIT = false>
 struct GuItem {
     static constexpr int NM = SPLIT ? 2 : 1;     // metadata words per unit
     uint4 qg[MAXJ], qu[MAXJ];
+    uint2 hg[B == 3 ? MAXJ : 1], hu[B == 3 ? MAXJ : 1];   // 1-bit planes (3 bits)
     uint32_t mg[MAXJ][NM], mu[MAXJ][NM];
     uint32_t bg[4], bu[4];          // LoRA-B row slice, raw binary16
     float G[MT], U[MT];
@@ -185,8 +247,8 @@ struct GuItem {
 template <int MT, int S, int MAXJ, int B, bool SPLIT>
 __device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ, B, SPLIT>& it, const GateUpArgs& a,
                                         int row0, bool active, int lane) {
-    static_assert((B == 2 || B == 4) && (!SPLIT || B == 2), "gate/up at 2 or 4 bits");
-    constexpr int UI = 128 / B;
+    static_assert((B == 2 || B == 3 || B == 4) && (!SPLIT || B != 4), "gate/up at 2, 3 or 4 bits");
+    constexpr int UI = codes_per_unit(B);
     const int s = lane % S;
     const int U = a.d / UI;
     const int J = (U + S - 1) / S;
@@ -201,8 +263,12 @@ __device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ, B, SPLIT>& it, const
     // Values of lanes without work are never used (the compute skips units
     // past the row and the epilogue skips rows past f).
     const long rowc = it.ok ? it.row : 0;
-    const uint4* cg = reinterpret_cast<const uint4*>(a.cg) + rowc * U;
-    const uint4* cu = reinterpret_cast<const uint4*>(a.cu) + rowc * U;
+    // 3 bits: a row is its 2-bit plane (d/4 bytes) then its 1-bit plane (d/8).
+    const long rstride = B == 3 ? (long)U * 3 / 2 : (long)U;      // in 16-byte units
+    const uint4* cg = reinterpret_cast<const uint4*>(a.cg) + rowc * rstride;
+    const uint4* cu = reinterpret_cast<const uint4*>(a.cu) + rowc * rstride;
+    const uint2* pg = reinterpret_cast<const uint2*>(cg + U);
+    const uint2* pu = reinterpret_cast<const uint2*>(cu + U);
     const uint32_t* mg = a.mg + rowc * ng;
     const uint32_t* mu = a.mu + rowc * ng;
 #pragma unroll
@@ -212,6 +278,10 @@ __device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ, B, SPLIT>& it, const
             const int uu = u < U ? u : 0;
             it.qg[i] = load_stream(cg + uu);
             it.qu[i] = load_stream(cu + uu);
+            if constexpr (B == 3) {
+                it.hg[i] = pg[uu];
+                it.hu[i] = pu[uu];
+            }
 #pragma unroll
             for (int h = 0; h < GuItem<MT, S, MAXJ, B, SPLIT>::NM; ++h) {
                 const int gi = SPLIT ? 2 * uu + h : uu / upg;
@@ -241,7 +311,7 @@ __device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ, B, SPLIT>& it,
                                               const float2* cx, int UC, int d, int u0, int uc,
                                               int lane) {
     constexpr int NM = GuItem<MT, S, MAXJ, B, SPLIT>::NM;
-    constexpr int UI = 128 / B;
+    constexpr int UI = codes_per_unit(B);
     const uint32_t mv = 0x64006400u;           // (the standalone kernels keep the literal)
     const int s = lane % S;
     const int J = (d / UI + S - 1) / S;
@@ -251,10 +321,15 @@ __device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ, B, SPLIT>& it,
         if (i < J && u >= u0 && u < u0 + uc) {
             const int ul = u - u0;
             float ag[NM][MT], au[NM][MT];
+            float bg1[B == 3 ? NM : 1][MT], bu1[B == 3 ? NM : 1][MT];   // 1-bit plane sums
 #pragma unroll
             for (int h = 0; h < NM; ++h)
 #pragma unroll
                 for (int m = 0; m < MT; ++m) ag[h][m] = au[h][m] = 0.0f;
+#pragma unroll
+            for (int h = 0; h < (B == 3 ? NM : 1); ++h)
+#pragma unroll
+                for (int m = 0; m < MT; ++m) bg1[h][m] = bu1[h][m] = 0.0f;
             uint32_t wg[4] = {it.qg[i].x, it.qg[i].y, it.qg[i].z, it.qg[i].w};
             uint32_t wu[4] = {it.qu[i].x, it.qu[i].y, it.qu[i].z, it.qu[i].w};
             uint32_t mgi[NM], mui[NM];
@@ -273,7 +348,7 @@ __device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ, B, SPLIT>& it,
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
                 const int hw = SPLIT ? (w >> 1) : 0;     // the group of code word w
-                if constexpr (B == 2) {
+                if constexpr (B == 2 || B == 3) {         // (at 3 bits: the 2-bit plane)
                     uint32_t eg[8], eu[8];
                     extract_w2(wg[w], eg, mv);
                     extract_w2(wu[w], eu, mv);
@@ -305,6 +380,42 @@ __device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ, B, SPLIT>& it,
                     }
                 }
             }
+            if constexpr (B == 3) {
+                // The 1-bit plane: word h holds the high bits of codes 32h..32h+31
+                // (bit i = code 32h+i); pair i = (code 32h+i, code 32h+16+i) meets
+                // x'' = x/256 staged in the same pairs (stage_x3).
+                const uint4* xs2 = xs + MT * UC * 8;
+                uint32_t hgw[2] = {it.hg[i].x, it.hg[i].y};
+                uint32_t huw[2] = {it.hu[i].x, it.hu[i].y};
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    pin(hgw[h]);
+                    pin(huw[h]);
+                }
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int hw = SPLIT ? h : 0;
+#pragma unroll
+                    for (int cc = 0; cc < 4; ++cc) {
+                        uint32_t eg[4], eu[4];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            eg[q] = bit_pair(hgw[h], 4 * cc + q, mv);
+                            eu[q] = bit_pair(huw[h], 4 * cc + q, mv);
+                        }
+#pragma unroll
+                        for (int m = 0; m < MT; ++m) {
+                            const uint4 p = xs2[(m * UC + ul) * 8 + ((4 * h + cc) ^ (ul & 7))];
+                            const uint32_t xp[4] = {p.x, p.y, p.z, p.w};
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                bg1[hw][m] = dot2(eg[q], xp[q], bg1[hw][m]);
+                                bu1[hw][m] = dot2(eu[q], xp[q], bu1[hw][m]);
+                            }
+                        }
+                    }
+                }
+            }
 #pragma unroll
             for (int h = 0; h < NM; ++h) {
                 const float sg = h2f(mgi[h] & 0xFFFFu), zg = h2f(mgi[h] >> 16);
@@ -312,8 +423,13 @@ __device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ, B, SPLIT>& it,
 #pragma unroll
                 for (int m = 0; m < MT; ++m) {
                     const float2 k = cx[(m * UC + ul) * NM + h];
-                    it.G[m] += sg * (ag[h][m] - k.x - zg * k.y);
-                    it.U[m] += su * (au[h][m] - k.x - zu * k.y);
+                    float dg = ag[h][m], du = au[h][m];
+                    if constexpr (B == 3) {       // q = q_lo + 4 q_hi; k.x holds both planes' offsets
+                        dg += 4.0f * bg1[h][m];
+                        du += 4.0f * bu1[h][m];
+                    }
+                    it.G[m] += sg * (dg - k.x - zg * k.y);
+                    it.U[m] += su * (du - k.x - zu * k.y);
                 }
             }
         }
@@ -377,7 +493,7 @@ template <int MT, int S, int MAXJ, int B>
 __device__ __forceinline__ void dn_load(DnItem<MT, S, MAXJ, B>& it, const DownArgs& a, int row0,
                                         bool active, int lane) {
     static_assert(B == 2 || B == 4, "down at 2 or 4 bits");
-    constexpr int UI = 128 / B;
+    constexpr int UI = codes_per_unit(B);
     const int s = lane % S;
     const int U = a.f / UI;
     const int J = (U + S - 1) / S;
@@ -406,7 +522,7 @@ template <int MT, int S, int MAXJ, int B>
 __device__ __forceinline__ void dn_accumulate(DnItem<MT, S, MAXJ, B>& it, const uint4* hs,
                                               const float2* cx, int UC, int f, int u0, int uc,
                                               int lane) {
-    constexpr int UI = 128 / B;
+    constexpr int UI = codes_per_unit(B);
     const uint32_t mv = 0x64006400u;           // (the standalone kernels keep the literal)
     const int s = lane % S;
     const int J = (f / UI + S - 1) / S;

@@ -21,7 +21,7 @@ hipError_t launch_down_batch(const BatchArgs& b, int nb, hipStream_t st) {
     if (nb < 1 || nb > kBatchMax)
         return hipErrorInvalidValue;
     const bool big = down_big_blocks(nb, b.M);
-    const int U = b.f / (128 / b.bd);
+    const int U = b.f / codes_per_unit(b.bd);
     const int S = nb > 1 ? lanes_fewest(U) : lanes_for(U, b.bd);
     if (b.bd == 4)
         return big ? launch_down_bits<4, 1024>(b, nb, S, st) : launch_down_bits<4, 256>(b, nb, S, st);

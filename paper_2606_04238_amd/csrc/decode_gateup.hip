@@ -44,9 +44,12 @@ hipError_t launch_lora_a_batch(const BatchArgs& b, int nb, hipStream_t st) {
 hipError_t launch_gateup_batch(const BatchArgs& b, int nb, hipStream_t st) {
     if (nb < 1 || nb > kBatchMax)
         return hipErrorInvalidValue;
-    const int S = lanes_for(b.d / (128 / b.bg), b.bg);
+    const int S = lanes_for(b.d / codes_per_unit(b.bg), b.bg);
     if (b.bg == 4)
         return launch_gateup_bits<4, false, 256>(b, nb, S, st);
+    if (b.bg == 3)
+        return b.gg == 32 ? launch_gateup_bits<3, true, 256>(b, nb, S, st)
+                          : launch_gateup_bits<3, false, 256>(b, nb, S, st);
     if (b.bg == 2 && b.gg == 32)
         return launch_gateup_bits<2, true, 256>(b, nb, S, st);
     if (b.bg == 2)
@@ -97,7 +100,7 @@ hipError_t launch_gateup(GateUpArgs args, hipStream_t st) {
 bool decode_shape_supported(int d, int f) { return decode_shape_supported_impl(d, f); }
 
 bool decode_variant_supported(int d, int f, int bg, int gg, int bd, int gd) {
-    if ((bg != 2 && bg != 4) || (bd != 2 && bd != 4))
+    if ((bg != 2 && bg != 3 && bg != 4) || (bd != 2 && bd != 4))
         return false;
     if (gg != 32 && gg != 64 && gg != 128)
         return false;

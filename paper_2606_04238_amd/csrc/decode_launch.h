@@ -14,13 +14,14 @@ inline int lanes_down(int U) { return U <= 64 ? 8 : U <= 128 ? 16 : U <= 256 ? 3
 inline int maxj_for(int J) { return J <= 8 ? 8 : 16; }
 // Lanes per row for 16-byte units of `bits`-bit codes (64 codes per unit at
 // 2 bits, 32 at 4 bits): each width keeps the policy of its own unit size.
-inline int lanes_for(int U, int bits) { return bits == 2 ? lanes_gateup(U) : lanes_down(U); }
+inline int lanes_for(int U, int bits) { return bits == 4 ? lanes_down(U) : lanes_gateup(U); }
+
 // The fewest lanes per row that keep every lane within 16 units: the most
 // loads in flight per lane, for launches whose parallelism comes from many
 // blocks (batches).
 inline int lanes_fewest(int U) { return U <= 128 ? 8 : U <= 256 ? 16 : U <= 512 ? 32 : 64; }
 inline bool units_fit(int k, int bits) {
-    const int U = k / (128 / bits);
+    const int U = k / codes_per_unit(bits);
     const int S = lanes_for(U, bits);
     return (U + S - 1) / S <= 16;
 }

@@ -1,0 +1,10 @@
+// Instantiations of the stand-alone decode kernels (decode_standalone.h)
+// for 3-bit gate/up (Appendix B), in a translation unit of their own.
+#include "decode_standalone.h"
+
+namespace qmlp {
+
+template hipError_t launch_gateup_bits<3, false, 256>(BatchArgs, int, int, hipStream_t);
+template hipError_t launch_gateup_bits<3, true, 256>(BatchArgs, int, int, hipStream_t);
+
+}  // namespace qmlp

@@ -1,5 +1,5 @@
 // Stand-alone decode kernels as templates over the code width (B), the
-// group-32 split (gate/up at 2 bits) and the block size (NT: 256 threads,
+// group-32 split (gate/up at 2 or 3 bits) and the block size (NT: 256 threads,
 // or 1024 for the down kernel of batches at several tokens).  Each width is instantiated
 // in a translation unit of its own (decode_sa_*.hip) so they build in
 // parallel; decode_gateup.hip and decode_down.hip dispatch to them.
@@ -43,7 +43,7 @@ template <int MT, int S, int MAXJ, int B, bool SPLIT, int NT>
 __global__ void __launch_bounds__(NT)
 gateup_kernel(BatchArgs b) {
     const GateUpArgs a = batch_gateup_args(b, blockIdx.y);
-    constexpr int CH = B == 2 ? 8 : 4;
+    constexpr int CH = B == 2 ? 8 : B == 3 ? 16 : 4;      // 16-byte chunks per (token, unit)
     extern __shared__ uint4 smem[];
     const int UC = a.uc;
     uint4* xs = smem;
@@ -51,12 +51,14 @@ gateup_kernel(BatchArgs b) {
     const int tid = threadIdx.x, lane = tid & 63;
     GuItem<MT, S, MAXJ, B, SPLIT> it;
     gu_load(it, a, (blockIdx.x * (blockDim.x >> 6) + (tid >> 6)) * (64 / S), true, lane);
-    const int U = a.d / (128 / B);
+    const int U = a.d / codes_per_unit(B);
     for (int u0 = 0; u0 < U; u0 += UC) {
         const int uc = min(UC, U - u0);
         __syncthreads();
         if constexpr (B == 2)
             stage_x<MT, SPLIT>(xs, cx, UC, a.x, a.M, a.d, u0, uc, tid, blockDim.x);
+        else if constexpr (B == 3)
+            stage_x3<MT, SPLIT>(xs, cx, UC, a.x, a.M, a.d, u0, uc, tid, blockDim.x);
         else
             stage_h<MT>(xs, cx, UC, a.x, a.M, a.d, u0, uc, tid, blockDim.x);
         __syncthreads();
@@ -80,11 +82,11 @@ gateup_kernel(BatchArgs b) {
 // the dispatcher.
 template <int B, bool SPLIT, int NT>
 hipError_t launch_gateup_bits(BatchArgs args, int nb, int S, hipStream_t st) {
-    const int U = args.d / (128 / B);
+    const int U = args.d / codes_per_unit(B);
     const int J = (U + S - 1) / S;
     const int mj = maxj_for(J);
     const int mt = mtile_for(args.M);
-    const size_t unit_bytes = B == 2 ? 8 * 16 + 8 * (SPLIT ? 2 : 1) : DN_UNIT_BYTES;
+    const size_t unit_bytes = B == 4 ? DN_UNIT_BYTES : (B == 3 ? 16 : 8) * 16 + 8 * (SPLIT ? 2 : 1);
     args.uc = units_per_chunk(U, S, unit_bytes, mt);
     const size_t lds = (size_t)mt * args.uc * unit_bytes;
     const int rows_per_block = (NT / 64) * (64 / S);
@@ -124,7 +126,7 @@ down_kernel(BatchArgs b) {
     const int tid = threadIdx.x, lane = tid & 63;
     DnItem<MT, S, MAXJ, B> it;
     dn_load(it, a, (blockIdx.x * (blockDim.x >> 6) + (tid >> 6)) * (64 / S), true, lane);
-    const int U = a.f / (128 / B);
+    const int U = a.f / codes_per_unit(B);
     for (int u0 = 0; u0 < U; u0 += UC) {
         const int uc = min(UC, U - u0);
         __syncthreads();
@@ -151,7 +153,7 @@ down_kernel(BatchArgs b) {
 
 template <int B, int NT>
 hipError_t launch_down_bits(BatchArgs args, int nb, int S, hipStream_t st) {
-    const int U = args.f / (128 / B);
+    const int U = args.f / codes_per_unit(B);
     const int J = (U + S - 1) / S;
     const int mj = maxj_for(J);
     const int mt = mtile_for(args.M);
@@ -168,6 +170,8 @@ hipError_t launch_down_bits(BatchArgs args, int nb, int S, hipStream_t st) {
     extern template hipError_t launch_gateup_bits<2, false, 256>(BatchArgs, int, int, hipStream_t);  \
     extern template hipError_t launch_gateup_bits<2, true, 256>(BatchArgs, int, int, hipStream_t);   \
     extern template hipError_t launch_gateup_bits<4, false, 256>(BatchArgs, int, int, hipStream_t);  \
+    extern template hipError_t launch_gateup_bits<3, false, 256>(BatchArgs, int, int, hipStream_t);  \
+    extern template hipError_t launch_gateup_bits<3, true, 256>(BatchArgs, int, int, hipStream_t);   \
     extern template hipError_t launch_down_bits<2, 256>(BatchArgs, int, int, hipStream_t);           \
     extern template hipError_t launch_down_bits<2, 1024>(BatchArgs, int, int, hipStream_t);          \
     extern template hipError_t launch_down_bits<4, 256>(BatchArgs, int, int, hipStream_t);           \

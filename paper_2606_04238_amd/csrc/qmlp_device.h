@@ -71,6 +71,13 @@ __device__ __forceinline__ void extract_w2(uint32_t w, uint32_t e[8], uint32_t m
     e[7] = magic(r, 0x03000300u, mv);
 }
 
+// The pair (bit i, bit 16 + i) of a word of 1-bit codes, moved to fraction
+// bit 8 of the two halves: each reads 1024 + 256 b.
+__device__ __forceinline__ uint32_t bit_pair(uint32_t w, int i, uint32_t mv) {
+    const uint32_t v = i <= 8 ? w << (8 - i) : w >> (i - 8);
+    return (v & 0x01000100u) | mv;
+}
+
 // 4^-k(p) for the 2-bit pair positions above (k packed 4 bits per pair).
 __device__ __forceinline__ float w2_pair_scale(int p) {
     const int k = (0x43243232 >> (4 * p)) & 15;

@@ -7,6 +7,11 @@
 
 namespace qmlp {
 
+// Codes per unit of a row's code stream: 32 at 4 bits and 64 at 2 bits (one
+// 16-byte load); at 3 bits 64 (16 bytes of the 2-bit plane and 8 bytes of
+// the 1-bit plane).
+constexpr int codes_per_unit(int bits) { return bits == 4 ? 32 : 64; }
+
 struct GateUpArgs {
     const uint32_t* cg;      // gate codes [f][d/16] words
     const uint32_t* mg;      // gate meta  [f][d/g]  (scale | zero << 16)

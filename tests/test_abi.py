@@ -46,7 +46,9 @@ def test_status_strings(lib):
 def test_size_queries(lib):
     assert lib.qmlp_codes_bytes(2, 9728, 2560) == 9728 * 2560 // 4
     assert lib.qmlp_codes_bytes(4, 2560, 9728) == 2560 * 9728 // 2
-    assert lib.qmlp_codes_bytes(3, 16, 64) == 0
+    assert lib.qmlp_codes_bytes(5, 16, 64) == 0
+    assert lib.qmlp_codes_bytes(3, 16, 128) == 16 * 128 * 3 // 8        # the two-plane 3-bit rows
+    assert lib.qmlp_codes_bytes(3, 16, 64) == 0                         # rows not 16-byte aligned
     assert lib.qmlp_codes_bytes(2, 16, 8) == 0          # k not a whole word
     assert lib.qmlp_meta_bytes(9728, 2560, 128) == 9728 * 20 * 4
     assert lib.qmlp_meta_bytes(16, 100, 64) == 0
@@ -150,7 +152,7 @@ def test_down_and_inspect_validation(q, lib):
     w2 = _qw(q, bits=2, n=256, k=512)
     assert lib.qmlp_down_w4(ctypes.byref(w2), ctypes.c_void_p(FAKE), 1, 0, ctypes.c_void_p(FAKE), None) == UNSUP
     assert lib.qmlp_unpack(ctypes.byref(w), None, None, None, None) == NULL
-    w3 = _qw(q, bits=3)
+    w3 = _qw(q, bits=5)
     assert lib.qmlp_dequant(ctypes.byref(w3), ctypes.c_void_p(FAKE), None) == UNSUP
     assert lib.qmlp_dequant(ctypes.byref(w), ctypes.c_void_p(FAKE + 1), None) == ALIGN
 
@@ -300,3 +302,24 @@ def test_batch_validation(q, lib):
     assert lib.qmlp_batch_workspace_bytes(arr, 3, 128, 1) == 0
     mixed = _stack_arr(q, _mlp(q), _variant(q, bd=2))
     assert fb(mixed, 2) == SHAPE
+
+
+def test_three_bit_validation(q, lib):
+    """3-bit codes (Appendix B): two-plane rows of a multiple of 128 codes, for
+    gate/up only, on the binary16 decode path; not through the 2-bit entry."""
+    P = ctypes.c_void_p
+    assert lib.qmlp_codes_bytes(3, 9728, 2560) == 9728 * 2560 * 3 // 8
+    assert lib.qmlp_codes_bytes(3, 16, 96) == 0                   # not whole 128-code runs
+    out = _qw(q)
+    assert lib.qmlp_pack_w3(P(FAKE), 16, 96, 32, ctypes.byref(out), None, None) == SHAPE
+    assert lib.qmlp_pack_w3(P(FAKE), 16, 256, 48, ctypes.byref(out), None, None) == UNSUP
+    w3 = _variant(q, bg=3, gg=32)
+    assert lib.qmlp_workspace_bytes(ctypes.byref(w3), 1, 0) > 0
+    assert lib.qmlp_forward_launches(ctypes.byref(w3), 1, 0) == 3
+    assert _fwd(lib, w3, M=256, dtype=1) == UNSUP
+    assert lib.qmlp_gateup_w2_lora(ctypes.byref(w3), P(FAKE), 1, 0, P(FAKE), P(FAKE), 1 << 30,
+                                   None) == UNSUP
+    d3 = _variant(q, bd=3)
+    assert _fwd(lib, d3) == UNSUP
+    odd = _variant(q, bg=3, gg=32, d=320)                        # 320 codes: not whole 128-code runs
+    assert _fwd(lib, odd) == SHAPE

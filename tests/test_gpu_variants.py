@@ -1,7 +1,8 @@
 """GPU parity of the precision variants against the fp64 oracle: the uniform
 W4 and uniform W2 blocks that bracket W4/W2-GateUp in the throughput
-comparison (Sec. 5.2: Gain and Capture are measured between them), and the
-paper's own INT2 grouping, 2-bit gate/up at group 32 (Sec. 3.3, Sec. 4.1).
+comparison (Sec. 5.2: Gain and Capture are measured between them), the
+paper's own INT2 grouping, 2-bit gate/up at group 32 (Sec. 3.3, Sec. 4.1),
+and the 3-bit gate/up of Appendix B (W3, group 32; two-plane code layout).
 
 They run on the stand-alone decode kernels (LoRA-A, gate/up, down).  The
 oracle is bit-width agnostic (it dequantizes s * (q - z) from unpacked
@@ -28,6 +29,8 @@ VARIANTS = {
     "w2_uniform": (2, None, 2, None),
     "w2g32_lora": (2, 32, 4, None),
     "w4g32_uniform": (4, 32, 4, 32),
+    "w3g32_lora": (3, 32, 4, None),
+    "w3_lora": (3, None, 4, None),
 }
 
 
@@ -51,7 +54,7 @@ def _widths(cfg, variant):
 
 def _pack(q, W, bits, group):
     t = torch.from_numpy(W).cuda()
-    return q.pack_w2(t, group) if bits == 2 else q.pack_w4(t, group)
+    return {2: q.pack_w2, 3: q.pack_w3, 4: q.pack_w4}[bits](t, group)
 
 
 def _block(q, lay, variant, rank=True):
@@ -87,7 +90,7 @@ def test_variant_tiny_matches_oracle(q, variant, M):
     cfg = wl.Config("tiny_var", M=M, d=512, f=1536, g=64, r=8, L=1)
     _announce("variant", variant, cfg.name, "M", M)
     lay = wl.layer(cfg, 0)
-    rank = variant == "w2g32_lora" or M == 3            # adapters also on the uniform blocks
+    rank = variant.endswith("_lora") or M == 3          # adapters also on the uniform blocks
     mlp = _block(q, lay, variant, rank=rank)
     assert q.forward_launches(mlp, M) == (3 if rank else 2)
     (y_ref, h_ref), (qg, qu, qd) = _oracle(lay, variant, rank=rank)
@@ -102,10 +105,12 @@ def test_variant_tiny_matches_oracle(q, variant, M):
 
 @pytest.mark.parametrize("variant", list(VARIANTS))
 def test_variant_ragged_units(q, variant):
-    """d = 704 and f = 1600: 11 (2-bit) / 22 (4-bit) units per gate/up row and
-    25 / 50 per down row, so the lanes of a row hold different unit counts."""
+    """d = 704 (640 at 3 bits, whose rows take multiples of 128 codes) and
+    f = 1600: 11 or 10 (2/3-bit) / 22 (4-bit) units per gate/up row and 25 / 50
+    per down row, so the lanes of a row hold different unit counts."""
     g = 32 if variant == "w4g32_uniform" else 64
-    cfg = wl.Config("ragged_var", M=5, d=704, f=1600, g=g, r=16, L=1)
+    d = 640 if variant.startswith("w3") else 704
+    cfg = wl.Config("ragged_var", M=5, d=d, f=1600, g=g, r=16, L=1)
     _announce("variant", variant, cfg.name)
     lay = wl.layer(cfg, 2)
     mlp = _block(q, lay, variant)
@@ -115,7 +120,7 @@ def test_variant_ragged_units(q, variant):
     assert orc.max_rel_err(values_of(y), y_ref) <= Y_TOL
 
 
-@pytest.mark.parametrize("variant", ["w4_uniform", "w2_uniform", "w2g32_lora"])
+@pytest.mark.parametrize("variant", ["w4_uniform", "w2_uniform", "w2g32_lora", "w3g32_lora"])
 @pytest.mark.parametrize("M", [1, 4])
 def test_variant_qwen3_4b_matches_oracle(q, variant, M):
     """The Qwen3-4B block shape (d 2560, f 9728, group 128) at each width."""
@@ -123,7 +128,7 @@ def test_variant_qwen3_4b_matches_oracle(q, variant, M):
     cfg = wl.Config("qwen3_4b_var", M=M, d=base.d, f=base.f, g=base.g, r=base.r, L=1)
     _announce("variant", variant, cfg.name, "M", M)
     lay = wl.layer(cfg, 1)
-    rank = variant == "w2g32_lora"
+    rank = variant.endswith("_lora")
     mlp = _block(q, lay, variant, rank=rank)
     (y_ref, h_ref), (qg, qu, qd) = _oracle(lay, variant, rank=rank)
     _check_packed(mlp.gate, qg)
@@ -168,3 +173,23 @@ def test_variant_layers_run_batched(q):
     for i, lay in enumerate(lays):
         (y_ref, _), _ = _oracle(lay, "w4_uniform", rank=False)
         assert orc.max_rel_err(orc.act_to_f64(bits_of(y[i]), False), y_ref) <= Y_TOL
+
+
+@pytest.mark.parametrize("group", [32, 128])
+def test_w3_pack_unpack_dequant_match_oracle(q, group):
+    """pack_w3 writes the oracle's two-plane words and metadata bit for bit;
+    unpack returns its codes, scales and zeros, dequant its binary16 image."""
+    cfg = wl.Config("w3pack", M=1, d=640, f=384, g=64, r=8, L=1)
+    _announce("w3 pack", "group", group)
+    W = wl.weight(cfg, 0, 0)                                     # [f][d]
+    w = q.pack_w3(torch.from_numpy(W).cuda(), group)
+    qt = orc.quantize(W, 3, group)
+    torch.cuda.synchronize()
+    assert not w.invalid_groups()
+    _check_packed(w, qt)
+    codes, scales, zeros = q.unpack(w)
+    assert np.array_equal(codes.cpu().numpy(), qt.codes)
+    assert np.array_equal(scales.cpu().numpy().view(np.uint16), qt.scale)
+    assert np.array_equal(zeros.cpu().numpy().view(np.uint16), qt.zero)
+    deq = q.dequant(w)
+    assert np.array_equal(deq.cpu().numpy().view(np.uint16), qt.dequant_f16())
