@@ -39,6 +39,7 @@ from __future__ import annotations
 
 import argparse
 import concurrent.futures
+import dataclasses
 import json
 import os
 import statistics
@@ -226,7 +227,8 @@ def precision_comparison(stack: Stack, seed: int, steps: int, min_warm_s: float,
                      "parity_max_rel_err_blocks_0_last": float("%.3e" % max(errs))}
     t4, t2 = res["w4_uniform"]["us_per_mlp_step"], res["w2_uniform"]["us_per_mlp_step"]
     b4, b2 = variant_bytes(cfg, "w4_uniform"), variant_bytes(cfg, "w2_uniform")
-    out = {"kernels": "qmlp_forward_batch: stand-alone decode kernels, one launch each for "
+    out = {"mlp_us": {k: v["us_per_mlp_step"] for k, v in res.items()},
+           "kernels": "qmlp_forward_batch: stand-alone decode kernels, one launch each for "
                       "LoRA-A, gate/up and down of up to 40 blocks; HIP graph over %d blocks" % L,
            "variants": res}
     for name in ("w4w2_gateup_lora", "w4w2_gateup_g32_lora", "w4w3_gateup_g32_lora"):
@@ -241,6 +243,89 @@ def precision_comparison(stack: Stack, seed: int, steps: int, min_warm_s: float,
         "us_per_mlp_step": round(mix_us, 3),
         "gain_pct_over_batched_w4": round((t4 / mix_us - 1) * 100, 1),
         "capture_pct_batched_w2_w4": round((1 / mix_us - 1 / t4) / (1 / t2 - 1 / t4) * 100, 1)}
+    return out
+
+
+def decoder_model(stack: Stack, seed: int, steps: int, min_warm_s: float, mlp_us: dict,
+                  threads: int = 16):
+    """Whole-model decode throughput of W4, W2 and W4/W2-GateUp on this GPU,
+    the method of Sec. 5.2 (per-token time summed over the operators, TPS =
+    1 / time) with measured operator times: per layer the q/k/v projection
+    (one [q + 2 kv][d] matrix) and the o projection (qmlp_linear_batch over
+    the layers; 4-bit, or 2-bit for W2), the MLP (mlp_us: the precision
+    comparison's pass), and the read of a BF16 KV cache of ctx positions (a
+    streaming read of those bytes stands in for attention, which is not
+    built); per token the LM head at the linears' width."""
+    import torch
+    import oracle as orc
+    import paper_2606_04238_amd as q
+    cfg = stack.cfg
+    dims = wl.DECODERS[cfg.name]
+    L, d, g = len(stack.mlps), cfg.d, cfg.g
+    shapes = {"qkv": (dims.qkv_rows(), d, wl.TID_QKV), "o": (d, dims.o_cols(), wl.TID_O)}
+    packs = {b: {k: [] for k in shapes} for b in (4, 2)}
+    t0 = time.time()
+    with concurrent.futures.ThreadPoolExecutor(max_workers=threads) as ex:
+        for name, (n, k, tid) in shapes.items():
+            futs = [ex.submit(wl.linear_weight, n, k, i, tid, seed) for i in range(L)]
+            for fut in futs:
+                W = torch.from_numpy(fut.result()).cuda()
+                packs[4][name].append(q.pack_w4(W, g))
+                packs[2][name].append(q.pack_w2(W, g))
+                del W
+                fut._result = None
+    W = torch.from_numpy(wl.linear_weight(dims.vocab, d, 0, wl.TID_LM_HEAD, seed)).cuda()
+    lm = {4: q.pack_w4(W, g), 2: q.pack_w2(W, g)}
+    del W
+    torch.cuda.synchronize()
+    log("packed the attention projections and the LM head in %.1f s" % (time.time() - t0))
+    xs = {name: torch.stack([torch.from_numpy(wl.linear_input(1, k, i, tid, seed).view(np.int16))
+                             .view(torch.float16) for i in range(L)]).cuda()
+          for name, (n, k, tid) in shapes.items()}
+    xl = torch.from_numpy(wl.linear_input(1, d, 0, wl.TID_LM_HEAD, seed).view(np.int16)).view(
+        torch.float16).cuda().reshape(1, 1, d)
+    us = {}
+    for b in (4, 2):
+        for name in shapes:
+            ys = torch.empty((L, 1, shapes[name][0]), dtype=torch.float16, device="cuda")
+            gr = capture(lambda: q.linear_batch(packs[b][name], xs[name], y=ys))
+            ms, _ = time_passes(gr.replay, steps, 2, min_warm_s)
+            us[(b, name)] = sum(ms) / len(ms) * 1e3
+            if b == 4 or name == "o":           # parity of layer 0 against the oracle
+                n, k, tid = shapes[name]
+                qt = orc.quantize(wl.linear_weight(n, k, 0, tid, seed), b, g)
+                ref = orc.down_act(qt, wl.linear_input(1, k, 0, tid, seed))
+                got = ys[0].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+                err = orc.max_rel_err(orc.act_to_f64(got, False), ref)
+                if not err <= 1e-2:
+                    raise RuntimeError("linear %s at %d bits: max-rel %.3e" % (name, b, err))
+        yl = torch.empty((1, 1, dims.vocab), dtype=torch.float16, device="cuda")
+        gr = capture(lambda: q.linear_batch([lm[b]], xl, y=yl))
+        ms, _ = time_passes(gr.replay, steps, 2, min_warm_s)
+        us[(b, "lm_head")] = sum(ms) / len(ms) * 1e3
+    # the KV stand-in: one reduction over the BF16 bytes, timed eagerly (a
+    # reduction over many blocks is kept out of HIP graphs)
+    kv = torch.ones(L * dims.kv_bytes_per_layer() // 2, dtype=torch.bfloat16, device="cuda")
+    ms, _ = time_passes(lambda: kv.sum(dtype=torch.float32), steps, 2, min_warm_s)
+    kv_us = sum(ms) / len(ms) * 1e3
+    if float(kv.sum(dtype=torch.float32)) != float(kv.numel()):
+        raise RuntimeError("KV read stand-in summed wrong")
+    del kv
+    widths = {"w4_uniform": 4, "w2_uniform": 2, "w4w2_gateup_lora": 4}
+    out = {"dims": dataclasses.asdict(dims),
+           "ops_us_per_token": {"qkv_4bit": round(us[(4, "qkv")], 2), "o_4bit": round(us[(4, "o")], 2),
+                                "qkv_2bit": round(us[(2, "qkv")], 2), "o_2bit": round(us[(2, "o")], 2),
+                                "lm_head_4bit": round(us[(4, "lm_head")], 2),
+                                "lm_head_2bit": round(us[(2, "lm_head")], 2),
+                                "kv_read_bf16": round(kv_us, 2)}}
+    tps = {}
+    for name, b in widths.items():
+        t = mlp_us[name] * L + us[(b, "qkv")] + us[(b, "o")] + us[(b, "lm_head")] + kv_us
+        tps[name] = 1e6 / t
+        out[name] = {"us_per_token": round(t, 1), "tokens_per_s": round(tps[name], 1)}
+    t4, t2, tm = tps["w4_uniform"], tps["w2_uniform"], tps["w4w2_gateup_lora"]
+    out["gain_pct"] = round((tm - t4) / t4 * 100, 1)
+    out["capture_pct"] = round((tm - t4) / (t2 - t4) * 100, 1)
     return out
 
 
@@ -552,6 +637,10 @@ def main(argv=None):
         context["precision_comparison"] = precision_comparison(stack, args.seed,
                                                                max(5, args.steps // 2),
                                                                args.min_warm_s, us_layer)
+        if cfg.name in wl.DECODERS:
+            context["decoder_model"] = decoder_model(
+                stack, args.seed, max(5, args.steps // 2), args.min_warm_s,
+                context["precision_comparison"]["mlp_us"])
 
     traffic = None
     if persistent:

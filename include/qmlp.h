@@ -290,6 +290,19 @@ qmlp_status qmlp_forward_batch(const qmlp_mlp *layers, int L, const void *x, int
                                qmlp_dtype dtype, void *y, void *ws, size_t ws_bytes,
                                qmlp_stream stream);
 
+/*
+ * L independent group-quantized linears of one shape, y_l = W_l x_l (Sec. 3.3:
+ * every linear outside gate/up is INT4 in W4/W2-GateUp; at 2 bits they are
+ * the uniform-W2 comparison point of Sec. 5.2): the attention projections of
+ * a decoder layer (q, k and v as one [q+2kv][d] matrix, o) and the LM head.
+ * w[0..L-1] are host descriptors of one shape [n][k] and width (4, or 2 with
+ * group 64/128), 1 <= L <= 40; x [L][M][k] and y [L][M][n] binary16,
+ * 1 <= M <= 16 (M == 0 is a no-op).  One launch of the stand-alone down
+ * kernel over the batch; no workspace.  n % 64 == 0, k % 64 == 0.
+ */
+qmlp_status qmlp_linear_batch(const qmlp_qweight *w, int L, const void *x, int M,
+                              qmlp_dtype dtype, void *y, qmlp_stream stream);
+
 /* ---------------------------------------------- inspection (not timed) */
 
 /*

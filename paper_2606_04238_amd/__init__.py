@@ -82,6 +82,7 @@ def _lib():
             "qmlp_forward_layers": (I, [pm, I, P, I, I, P, P, Z, P]),
             "qmlp_layers_launches": (I, [pm, I, I, I]),
             "qmlp_batch_workspace_bytes": (Z, [pm, I, I, I]),
+            "qmlp_linear_batch": (I, [ctypes.POINTER(QWeightC), I, P, I, I, P, P]),
             "qmlp_forward_batch": (I, [pm, I, P, I, I, P, P, Z, P]),
             "qmlp_status_string": (ctypes.c_char_p, [I]),
         }
@@ -372,6 +373,20 @@ def forward_batch(layers: Layers, x: torch.Tensor, y: torch.Tensor | None = None
         ws = batch_workspace(layers, M, x.dtype, x.device)
     _check(_lib().qmlp_forward_batch(layers.c(), L, _ptr(x), M, _dtype_code(x), _ptr(y), _ptr(ws),
                                      ws.numel(), _stream()), "forward_batch")
+    return y
+
+
+def linear_batch(ws, x: torch.Tensor, y: torch.Tensor | None = None) -> torch.Tensor:
+    """y [L][M][n] = W_l x_l for L quantized linears of one shape (QWeight list)
+    and x [L][M][k] binary16: one launch."""
+    L, M, k = x.shape
+    if L != len(ws) or k != ws[0].k_in:
+        raise ValueError("x must be [L][M][k] for the L linears")
+    if y is None:
+        y = torch.empty((L, M, ws[0].n_out), dtype=x.dtype, device=x.device)
+    arr = (QWeightC * L)(*[w.c() for w in ws])
+    _check(_lib().qmlp_linear_batch(arr, L, _ptr(x), M, _dtype_code(x), _ptr(y), _stream()),
+           "linear_batch")
     return y
 
 

@@ -6,6 +6,7 @@
 
 #include "qmlp.h"
 #include "qmlp_internal.h"
+#include "decode_launch.h"
 
 namespace {
 
@@ -692,6 +693,47 @@ qmlp_status qmlp_forward_batch(const qmlp_mlp* layers, int L, const void* x, int
         return QMLP_ERR_ALIGN;
     return run_layers_batched(layers, L, static_cast<const char*>(x), M, static_cast<char*>(y), ws,
                               static_cast<hipStream_t>(stream));
+}
+
+qmlp_status qmlp_linear_batch(const qmlp_qweight* w, int L, const void* x, int M, qmlp_dtype dtype,
+                              void* y, qmlp_stream stream) {
+    if (!w)
+        return QMLP_ERR_NULL;
+    if (L <= 0 || L > kBatchMax || M < 0)
+        return QMLP_ERR_SHAPE;
+    for (int i = 0; i < L; ++i) {
+        const qmlp_status s = check_qweight(&w[i], 0);
+        if (s != QMLP_OK)
+            return s;
+        if (w[i].n_out != w[0].n_out || w[i].k_in != w[0].k_in || w[i].group != w[0].group ||
+            w[i].bits != w[0].bits)
+            return QMLP_ERR_SHAPE;
+    }
+    const int n = w[0].n_out, k = w[0].k_in, bits = w[0].bits;
+    if (n % 64 != 0 || k % 64 != 0)
+        return QMLP_ERR_SHAPE;
+    if (dtype != QMLP_F16 || M > 16 || bits == 3 || (bits == 2 && w[0].group == 32) ||
+        !units_fit(k, bits))
+        return QMLP_ERR_UNSUPPORTED;
+    if (M == 0)
+        return QMLP_OK;
+    if (!x || !y)
+        return QMLP_ERR_NULL;
+    if (!aligned16(x) || !aligned16(y))
+        return QMLP_ERR_ALIGN;
+    BatchArgs b{};
+    for (int i = 0; i < L; ++i) {
+        b.lay[i].cd = static_cast<const uint32_t*>(w[i].codes);
+        b.lay[i].md = static_cast<const uint32_t*>(w[i].meta);
+    }
+    b.h = const_cast<uint16_t*>(static_cast<const uint16_t*>(x));
+    b.y = static_cast<uint16_t*>(y);
+    b.M = M;
+    b.d = n;
+    b.f = k;
+    b.gd = w[0].group;
+    b.bd = bits;
+    return from_hip(launch_down_batch(b, L, static_cast<hipStream_t>(stream)));
 }
 
 const char* qmlp_status_string(qmlp_status s) {

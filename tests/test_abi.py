@@ -323,3 +323,28 @@ def test_three_bit_validation(q, lib):
     assert _fwd(lib, d3) == UNSUP
     odd = _variant(q, bg=3, gg=32, d=320)                        # 320 codes: not whole 128-code runs
     assert _fwd(lib, odd) == SHAPE
+
+
+def test_linear_batch_validation(q, lib):
+    """qmlp_linear_batch: 1..40 linears of one shape and width (4, or 2 at
+    group 64/128), binary16 decode, n and k multiples of 64."""
+    P = ctypes.c_void_p
+
+    def arr(*ws):
+        return (q.QWeightC * len(ws))(*ws)
+
+    w = _qw(q, bits=4, n=512, k=256)
+    assert lib.qmlp_linear_batch(None, 1, P(FAKE), 1, 0, P(FAKE), None) == NULL
+    assert lib.qmlp_linear_batch(arr(w), 0, P(FAKE), 1, 0, P(FAKE), None) == SHAPE
+    assert lib.qmlp_linear_batch(arr(*[w] * 41), 41, P(FAKE), 1, 0, P(FAKE), None) == SHAPE
+    assert lib.qmlp_linear_batch(arr(w, _qw(q, bits=4, n=448, k=256)), 2, P(FAKE), 1, 0, P(FAKE),
+                                 None) == SHAPE
+    assert lib.qmlp_linear_batch(arr(w), 1, P(FAKE), 17, 0, P(FAKE), None) == UNSUP
+    assert lib.qmlp_linear_batch(arr(w), 1, P(FAKE), 1, 1, P(FAKE), None) == UNSUP
+    assert lib.qmlp_linear_batch(arr(_qw(q, bits=3, n=512, k=256)), 1, P(FAKE), 1, 0, P(FAKE),
+                                 None) == UNSUP
+    assert lib.qmlp_linear_batch(arr(_qw(q, bits=2, n=512, k=256, g=32)), 1, P(FAKE), 1, 0,
+                                 P(FAKE), None) == UNSUP
+    assert lib.qmlp_linear_batch(arr(w), 1, None, 1, 0, P(FAKE), None) == NULL
+    assert lib.qmlp_linear_batch(arr(w), 1, P(FAKE + 8), 1, 0, P(FAKE), None) == ALIGN
+    assert lib.qmlp_linear_batch(arr(w), 1, P(FAKE), 0, 0, P(FAKE), None) == OK

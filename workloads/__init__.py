@@ -19,7 +19,9 @@ adapters are not used.  Value distributions:
 
 Every tensor has its own stream ``np.random.default_rng([seed, layer, id])``
 with ids 0 W_gate, 1 W_up, 2 W_down, 3 A_gate, 4 B_gate, 5 A_up, 6 B_up, 7 x,
-8/9/10 outlier positions and signs for gate/up/down.
+8/9/10 outlier positions and signs for gate/up/down; the linears outside the
+MLP (whole-decoder throughput model) use 11 q/k/v, 12 o, 13 LM head and
+14 + 16 * id for their inputs.
 """
 from __future__ import annotations
 
@@ -151,3 +153,46 @@ def layer(cfg: Config, index: int, seed: int = 0, M: int | None = None) -> Layer
 def scaled(cfg: Config, **kw) -> Config:
     """A copy of cfg with some fields replaced (small parity shapes, other M)."""
     return dataclasses.replace(cfg, **kw)
+
+
+# ------------------------------------------------------------------ the rest of a decoder layer
+# Dimensions of the decoder around the MLP, for the whole-layer throughput
+# model of the precision comparison.  The paper gives none (Sec. 5 names the
+# models only); these are the public configuration of the model each MLP
+# shape stands in for.  Weights stay synthetic (N(0, 0.02), as above).
+@dataclasses.dataclass(frozen=True)
+class DecoderDims:
+    heads: int          # query heads
+    kv_heads: int       # key/value heads (grouped-query attention)
+    head_dim: int
+    vocab: int          # LM head rows (tied embeddings)
+    ctx: int            # context length of the KV cache the step reads
+
+    def qkv_rows(self) -> int:
+        return (self.heads + 2 * self.kv_heads) * self.head_dim
+
+    def o_cols(self) -> int:
+        return self.heads * self.head_dim
+
+    def kv_bytes_per_layer(self) -> int:
+        """BF16 K and V of ctx positions read by one decode step of one layer."""
+        return 2 * self.kv_heads * self.head_dim * self.ctx * 2
+
+
+DECODERS = {"qwen3_4b": DecoderDims(heads=32, kv_heads=8, head_dim=128, vocab=151936, ctx=1024)}
+
+TID_QKV, TID_O, TID_LM_HEAD, TID_LIN_X = 11, 12, 13, 14
+
+
+def linear_weight(n: int, k: int, layer: int, tensor_id: int, seed: int = 0) -> np.ndarray:
+    """fp32 source weight [n][k] of a linear outside the MLP (ids 11 qkv,
+    12 o, 13 LM head), N(0, 0.02)."""
+    w = rng_for(seed, layer, tensor_id).standard_normal((n, k), dtype=np.float32)
+    w *= np.float32(0.02)
+    return w
+
+
+def linear_input(M: int, k: int, layer: int, tensor_id: int, seed: int = 0) -> np.ndarray:
+    """Binary16 input bits [M][k] of a linear, N(0, 1) (stream id 14 + 16 * which)."""
+    a = rng_for(seed, layer, TID_LIN_X + 16 * tensor_id).standard_normal((M, k), dtype=np.float32)
+    return f32_to_f16_bits(a)
