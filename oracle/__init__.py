@@ -284,6 +284,23 @@ def forward(qg: QTensor, qu: QTensor, qd: QTensor, Ag, Bg, Au, Bu, x, lora_scale
     return (y, h) if return_h else y
 
 
+def moe_forward(experts, topk_idx, topk_w, x, lora_scale=1.0):
+    """The routed-expert MLP (Sec. 5, the MoE decoder): token m's output is
+    sum_j topk_w[m][j] * forward(expert topk_idx[m][j], x[m]) in fp64.
+    experts: list of (qg, qu, qd, Ag, Bg, Au, Bu); x [M][d] binary16 bits."""
+    x = _c(x, np.uint16)
+    M = x.shape[0]
+    y = None
+    for m in range(M):
+        ym = 0.0
+        for e, w in zip(np.asarray(topk_idx)[m], np.asarray(topk_w, np.float64)[m]):
+            qg, qu, qd, Ag, Bg, Au, Bu = experts[int(e)]
+            ym = ym + w * forward(qg, qu, qd, Ag, Bg, Au, Bu, x[m:m + 1], lora_scale=lora_scale)[0]
+        y = np.empty((M, ym.shape[0]), np.float64) if y is None else y
+        y[m] = ym
+    return y
+
+
 def max_rel_err(got: np.ndarray, ref: np.ndarray) -> float:
     """max |got - ref| / max |ref| over all elements, in fp64."""
     got = np.asarray(got, np.float64)

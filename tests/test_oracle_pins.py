@@ -395,3 +395,51 @@ def test_rmsnorm_matches_numpy_per_row():
     v = x.view(np.float16).astype(np.float64)
     ref = (v / np.sqrt(np.mean(v * v, axis=1, keepdims=True) + orc.RMS_EPS)).astype(np.float16)
     assert np.array_equal(orc.rmsnorm_f16(x), ref.view(np.uint16))
+
+
+# ------------------------------------------------------ routed experts (MoE)
+def _experts(E, cfg, seed=0):
+    out = []
+    for e in range(E):
+        L = wl.layer(cfg, e, seed)
+        out.append((orc.quantize(L.W_gate, 2, cfg.g), orc.quantize(L.W_up, 2, cfg.g),
+                    orc.quantize(L.W_down, 4, cfg.g), L.A_gate, L.B_gate, L.A_up, L.B_up))
+    return out
+
+
+def test_moe_forward_matches_numpy_brute_force():
+    """Each token's output is the routing-weighted sum of its experts' blocks,
+    every block rebuilt here with numpy from codes/scale/zero."""
+    cfg = _small_cfg(M=1, d=128, f=192, g=64, r=8)
+    ex = _experts(4, cfg)
+    lays = [wl.layer(cfg, e, 0) for e in range(4)]
+    x = wl.activations(cfg, 9, 0, M=3)
+    idx = np.array([[0, 2], [3, 1], [2, 3]], np.int32)
+    w = np.array([[0.25, 0.75], [0.5, 0.5], [1.0, 0.125]], np.float32)
+    y = orc.moe_forward(ex, idx, w, x)
+    for m in range(3):
+        ref = 0.0
+        for e, ww in zip(idx[m], w[m]):
+            L = lays[e]
+            one = wl.Layer(cfg, e, L.W_gate, L.W_up, L.W_down, L.A_gate, L.B_gate, L.A_up, L.B_up,
+                           x[m:m + 1])
+            ref = ref + float(ww) * _numpy_forward(cfg, one, *ex[e][:3])[0][0]
+        assert orc.max_rel_err(y[m], ref) < 1e-12
+
+
+def test_moe_single_expert_and_linearity():
+    """k = 1 with weight 1 is exactly that expert's forward; scaling every
+    weight by 2 scales the output by 2 exactly; reordering the slots changes
+    only the summation order."""
+    cfg = _small_cfg(M=1, d=128, f=192, g=64, r=8)
+    ex = _experts(3, cfg, seed=1)
+    x = wl.activations(cfg, 5, 1, M=2)
+    one = orc.moe_forward(ex, np.array([[2], [0]]), np.array([[1.0], [1.0]], np.float32), x)
+    for m, e in enumerate((2, 0)):
+        assert np.array_equal(one[m], orc.forward(*ex[e], x[m:m + 1])[0])
+    idx = np.array([[0, 1, 2], [2, 1, 0]], np.int32)
+    w = np.array([[0.2, 0.3, 0.5], [0.6, 0.3, 0.1]], np.float32)
+    y = orc.moe_forward(ex, idx, w, x)
+    assert np.array_equal(orc.moe_forward(ex, idx, 2 * w, x), 2 * y)
+    y2 = orc.moe_forward(ex, idx[:, ::-1].copy(), w[:, ::-1].copy(), x)
+    assert np.allclose(y2, y, rtol=1e-14, atol=1e-14 * np.abs(y).max())

@@ -196,3 +196,32 @@ def linear_input(M: int, k: int, layer: int, tensor_id: int, seed: int = 0) -> n
     """Binary16 input bits [M][k] of a linear, N(0, 1) (stream id 14 + 16 * which)."""
     a = rng_for(seed, layer, TID_LIN_X + 16 * tensor_id).standard_normal((M, k), dtype=np.float32)
     return f32_to_f16_bits(a)
+
+
+# ------------------------------------------------------------------ mixture of experts
+# The GPT-OSS-20B-class MoE layer (Sec. 5.1): 32 experts of hidden 2880 and
+# expert width 2880, 4 routed per token, INT4 group 64 base (Sec. 5.2); the
+# expert MLPs take the W4/W2-GateUp form with rank-16 adapters.
+@dataclasses.dataclass(frozen=True)
+class MoeConfig:
+    name: str
+    experts: int
+    topk: int
+    block: Config        # one expert's block (M = tokens per step, L = MoE layers timed)
+
+
+MOE = {"gptoss20b_moe": MoeConfig("gptoss20b_moe", experts=32, topk=4,
+                                  block=Config("gptoss20b_expert", M=1, d=2880, f=2880, g=64, r=16, L=8))}
+
+TID_ROUTE = 15
+
+
+def routing(M: int, experts: int, topk: int, layer: int, seed: int = 0):
+    """Synthetic routing: per token topk distinct expert ids uniform without
+    replacement (int32 [M][topk]) and weights = softmax of N(0, 1) logits
+    (float32 [M][topk])."""
+    rng = rng_for(seed, layer, TID_ROUTE)
+    idx = np.stack([rng.choice(experts, size=topk, replace=False) for _ in range(M)]).astype(np.int32)
+    logits = rng.standard_normal((M, topk))
+    w = np.exp(logits - logits.max(axis=1, keepdims=True))
+    return idx, (w / w.sum(axis=1, keepdims=True)).astype(np.float32)
