@@ -491,6 +491,111 @@ def prefill_flops(cfg: wl.Config):
     return gateup, down
 
 
+def moe_main(mc: wl.MoeConfig, args):
+    """The routed-expert MLP of an MoE decoder (GPT-OSS-20B-class: 24 layers of
+    32 experts, top-4, one decode token): one step is qmlp_forward_moe over
+    every layer, each layer on its own input and synthetic routing, at three
+    widths (uniform W4, uniform W2, W4/W2-GateUp with adapters) for the MoE
+    Gain / Capture.  Routing is fixed per layer, so only the 4 routed experts
+    of a layer are ever read: those carry their own seeded weights, the other
+    28 descriptors of the layer share one packed expert (never read)."""
+    import torch
+    import oracle as orc
+    import paper_2606_04238_amd as q
+    cfg = mc.block
+    L, E, k, M = 24, mc.experts, mc.topk, cfg.M
+    routes = [wl.routing(M, E, k, l, args.seed) for l in range(L)]
+    widths = {"w4_uniform": (4, 4, False), "w2_uniform": (2, 2, False),
+              "w4w2_gateup_lora": (2, 4, True)}
+    pk = {2: q.pack_w2, 4: q.pack_w4}
+
+    def act(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.float16).cuda()
+
+    t0 = time.time()
+    filler = wl.layer(cfg, 10_000, args.seed)
+    expert_lays = {}
+    mlps = {v: [] for v in widths}
+    with concurrent.futures.ThreadPoolExecutor(max_workers=16) as ex:
+        need = sorted({(l, int(e)) for l in range(L) for e in routes[l][0].reshape(-1)})
+        futs = {key: ex.submit(wl.layer, cfg, 1000 * key[0] + key[1], args.seed) for key in need}
+        for key, fut in futs.items():
+            expert_lays[key] = fut.result()
+    dev = {}
+    for key, lay in list(expert_lays.items()) + [(None, filler)]:
+        Wg, Wu, Wd = (torch.from_numpy(w).cuda() for w in (lay.W_gate, lay.W_up, lay.W_down))
+        lo = tuple(act(a) for a in (lay.A_gate, lay.B_gate, lay.A_up, lay.B_up))
+        for v, (bg, bd, lora) in widths.items():
+            dev[(key, v)] = q.MLP(pk[bg](Wg, cfg.g), pk[bg](Wu, cfg.g), pk[bd](Wd, cfg.g),
+                                  *(lo if lora else ()), lora_scale=cfg.lora_scale)
+        del Wg, Wu, Wd
+    layers = {v: [q.Layers([dev[((l, e), v)] if (l, e) in expert_lays else dev[(None, v)]
+                            for e in range(E)]) for l in range(L)] for v in widths}
+    torch.cuda.synchronize()
+    log("built %d routed experts (+1 shared filler) at 3 widths in %.1f s"
+        % (len(expert_lays), time.time() - t0))
+    xs = [act(wl.activations(cfg, 5000 + l, args.seed, M=M)) for l in range(L)]
+    idx = [torch.from_numpy(r[0]).cuda() for r in routes]
+    wts = [torch.from_numpy(r[1]).cuda() for r in routes]
+    ys = [torch.empty_like(x) for x in xs]
+    res = {}
+    for v, (bg, bd, lora) in widths.items():
+        wss = [torch.zeros(q.moe_workspace_bytes(layers[v][l], M, k), dtype=torch.uint8, device="cuda")
+               for l in range(L)]
+
+        def step():
+            for l in range(L):
+                q.forward_moe(layers[v][l], xs[l], idx[l], wts[l], y=ys[l], ws=wss[l])
+        g = capture(step)
+        ms, _ = time_passes(g.replay, args.steps, args.warmup, args.min_warm_s)
+        us = sum(ms) / len(ms) * 1e3 / L
+        step()
+        torch.cuda.synchronize()
+        errs = []
+        for l in (0, L - 1):
+            oq = []
+            for e in range(E):
+                lay = expert_lays.get((l, e), filler)
+                oq.append((orc.quantize(lay.W_gate, bg, cfg.g), orc.quantize(lay.W_up, bg, cfg.g),
+                           orc.quantize(lay.W_down, bd, cfg.g))
+                          + ((lay.A_gate, lay.B_gate, lay.A_up, lay.B_up) if lora else (None,) * 4)
+                          if (l, e) in expert_lays else None)
+            ref = orc.moe_forward(oq, routes[l][0], routes[l][1],
+                                  wl.activations(cfg, 5000 + l, args.seed, M=M),
+                                  lora_scale=cfg.lora_scale)
+            got = ys[l].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+            errs.append(orc.max_rel_err(orc.act_to_f64(got, False), ref))
+        f, d = cfg.f, cfg.d
+        b_exp = 2 * f * d * bg // 8 + d * f * bd // 8 + 12 * f * d // cfg.g + \
+            (4 * cfg.r * (d + f) if lora else 0)
+        b = k * M * b_exp + 4 * M * d
+        res[v] = {"us_per_moe_layer": round(us, 3), "alg_bytes_per_moe_layer": b,
+                  "gbs": round(b / (us * 1e-6) / 1e9, 1),
+                  "frac_of_hbm_peak": round(b / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                  "parity_max_rel_err_layers_0_last": float("%.3e" % max(errs))}
+        if not max(errs) <= 1e-2:
+            raise RuntimeError("moe parity %s: %.3e" % (v, max(errs)))
+    t4, t2, tm = (res[v]["us_per_moe_layer"] for v in ("w4_uniform", "w2_uniform", "w4w2_gateup_lora"))
+    mix = res["w4w2_gateup_lora"]
+    out = {
+        "metric": METRIC, "value": mix["gbs"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(tm * L / 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+        "config": {"workload": "%s: %d MoE layers of %d experts (d=%d, f=%d, group %d, LoRA rank %d), "
+                               "top-%d routing, M=%d, every layer on its own input and routing"
+                               % (mc.name, L, E, cfg.d, cfg.f, cfg.g, cfg.r, k, M),
+                   "path": "qmlp_forward_moe (batched stand-alone kernels over the routed instances)",
+                   "widths": res,
+                   "gain_pct": round((t4 / tm - 1) * 100, 1),
+                   "capture_pct": round((1 / tm - 1 / t4) / (1 / t2 - 1 / t4) * 100, 1)},
+        "roofline": {"bound": "hbm", "kernel": "MoE layer step (LoRA-A, gate/up, down, combine)",
+                     "achieved": mix["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": mix["frac_of_hbm_peak"], "traffic": None},
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def prefill_main(cfg: wl.Config, args):
     """One prefill chunk per step: qmlp_forward at M tokens (bf16, MFMA)."""
     import torch
@@ -561,7 +666,7 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="qwen3_4b", choices=sorted(wl.CONFIGS))
+    ap.add_argument("--config", default="qwen3_4b", choices=sorted(wl.CONFIGS) + sorted(wl.MOE))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--mode", default="eager", choices=["graph", "eager"],
                     help="how the timed steps are launched: back-to-back launches on the stream (eager) or replays of a captured HIP graph")
@@ -587,6 +692,8 @@ def main(argv=None):
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         return 2
+    if args.config in wl.MOE:
+        return moe_main(wl.MOE[args.config], args)
     cfg = wl.CONFIGS[args.config]
     if cfg.M > 16:
         return prefill_main(cfg, args)

@@ -303,6 +303,29 @@ qmlp_status qmlp_forward_batch(const qmlp_mlp *layers, int L, const void *x, int
 qmlp_status qmlp_linear_batch(const qmlp_qweight *w, int L, const void *x, int M,
                               qmlp_dtype dtype, void *y, qmlp_stream stream);
 
+/*
+ * The MLP of a mixture-of-experts decoder layer at decode (Sec. 5: the
+ * routed experts of the GPT-OSS-20B-class model; only the routed experts'
+ * weights are read per token): each of E experts is one block of
+ * qmlp_forward (W4/W2-GateUp with its own adapters, or any width qmlp_mlp
+ * lists), and token m's output is
+ *     y[m] = sum_j topk_w[m][j] * expert_{topk_idx[m][j]}(x[m]).
+ * experts[0..E-1]: host descriptors of one shape, 1 <= E <= 40.  x [M][d],
+ * y [M][d] binary16; topk_idx int32 [M][k] and topk_w fp32 [M][k] are DEVICE
+ * arrays (routing runs on the GPU); ids outside [0, E) are a precondition
+ * violation (the kernels clamp them, so nothing is read outside the
+ * table).  1 <= k <= E, M <= 16, M*k <= 40.  Every (token, slot) pair runs
+ * as one instance: an expert chosen by two tokens is read twice.  Three
+ * launches over the M*k instances (LoRA-A, gate/up, down) and one combine.
+ * ws/ws_bytes: at least qmlp_moe_workspace_bytes(...): t, h and the
+ * per-instance outputs; no state is kept between calls.
+ */
+size_t qmlp_moe_workspace_bytes(const qmlp_mlp *experts, int E, int M, int k, qmlp_dtype dtype);
+
+qmlp_status qmlp_forward_moe(const qmlp_mlp *experts, int E, const void *x, int M,
+                             qmlp_dtype dtype, const int32_t *topk_idx, const float *topk_w, int k,
+                             void *y, void *ws, size_t ws_bytes, qmlp_stream stream);
+
 /* ---------------------------------------------- inspection (not timed) */
 
 /*

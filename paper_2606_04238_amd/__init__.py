@@ -83,6 +83,8 @@ def _lib():
             "qmlp_layers_launches": (I, [pm, I, I, I]),
             "qmlp_batch_workspace_bytes": (Z, [pm, I, I, I]),
             "qmlp_linear_batch": (I, [ctypes.POINTER(QWeightC), I, P, I, I, P, P]),
+            "qmlp_moe_workspace_bytes": (Z, [pm, I, I, I, I]),
+            "qmlp_forward_moe": (I, [pm, I, P, I, I, P, P, I, P, P, Z, P]),
             "qmlp_forward_batch": (I, [pm, I, P, I, I, P, P, Z, P]),
             "qmlp_status_string": (ctypes.c_char_p, [I]),
         }
@@ -387,6 +389,30 @@ def linear_batch(ws, x: torch.Tensor, y: torch.Tensor | None = None) -> torch.Te
     arr = (QWeightC * L)(*[w.c() for w in ws])
     _check(_lib().qmlp_linear_batch(arr, L, _ptr(x), M, _dtype_code(x), _ptr(y), _stream()),
            "linear_batch")
+    return y
+
+
+def moe_workspace_bytes(experts: Layers, M: int, k: int, dtype=torch.float16) -> int:
+    code = F16 if dtype == torch.float16 else BF16
+    return int(_lib().qmlp_moe_workspace_bytes(experts.c(), len(experts), M, k, code))
+
+
+def forward_moe(experts: Layers, x: torch.Tensor, topk_idx: torch.Tensor, topk_w: torch.Tensor,
+                y: torch.Tensor | None = None, ws: torch.Tensor | None = None) -> torch.Tensor:
+    """y [M][d] = sum_j topk_w[m][j] * expert_{topk_idx[m][j]}(x[m]); topk_idx int32
+    and topk_w float32 [M][k] on the device."""
+    M, d = x.shape
+    k = topk_idx.shape[1]
+    if topk_idx.dtype != torch.int32 or topk_w.dtype != torch.float32 or topk_w.shape != topk_idx.shape:
+        raise ValueError("topk_idx int32 and topk_w float32, both [M][k]")
+    if y is None:
+        y = torch.empty_like(x)
+    if ws is None:
+        ws = torch.zeros(max(moe_workspace_bytes(experts, M, k, x.dtype), 1024), dtype=torch.uint8,
+                         device=x.device)
+    _check(_lib().qmlp_forward_moe(experts.c(), len(experts), _ptr(x), M, _dtype_code(x),
+                                   _ptr(topk_idx), _ptr(topk_w), k, _ptr(y), _ptr(ws), ws.numel(),
+                                   _stream()), "forward_moe")
     return y
 
 

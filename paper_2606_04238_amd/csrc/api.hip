@@ -736,6 +736,67 @@ qmlp_status qmlp_linear_batch(const qmlp_qweight* w, int L, const void* x, int M
     return from_hip(launch_down_batch(b, L, static_cast<hipStream_t>(stream)));
 }
 
+size_t qmlp_moe_workspace_bytes(const qmlp_mlp* experts, int E, int M, int k, qmlp_dtype dtype) {
+    if (E < 1 || E > kBatchMax || k < 1 || k > E || M < 1 || M > 16 || M * k > kBatchMax ||
+        dtype != QMLP_F16 || check_layers(experts, E, 1, dtype) != QMLP_OK)
+        return 0;
+    const int n = M * k;
+    return kCtlBytes + batch_t_bytes(experts, n, 1) + batch_h_bytes(experts, n, 1) +
+           round256((size_t)n * experts[0].gate.k_in * 2);
+}
+
+qmlp_status qmlp_forward_moe(const qmlp_mlp* experts, int E, const void* x, int M,
+                             qmlp_dtype dtype, const int32_t* topk_idx, const float* topk_w, int k,
+                             void* y, void* ws, size_t ws_bytes, qmlp_stream stream) {
+    qmlp_status s = check_layers(experts, E, 1, dtype);
+    if (s != QMLP_OK)
+        return s;
+    if (E > kBatchMax || k < 1 || k > E || M < 0)
+        return QMLP_ERR_SHAPE;
+    if (dtype != QMLP_F16 || M > 16 || M * k > kBatchMax)
+        return QMLP_ERR_UNSUPPORTED;
+    if (M == 0)
+        return QMLP_OK;
+    if (!x || !y || !topk_idx || !topk_w)
+        return QMLP_ERR_NULL;
+    if (!aligned16(x) || !aligned16(y) || ((uintptr_t)topk_idx & 3u) || ((uintptr_t)topk_w & 3u))
+        return QMLP_ERR_ALIGN;
+    if (!ws || ws_bytes < qmlp_moe_workspace_bytes(experts, E, M, k, dtype))
+        return QMLP_ERR_WORKSPACE;
+    if (!aligned16(ws))
+        return QMLP_ERR_ALIGN;
+    const qmlp_mlp& a = experts[0];
+    const int n = M * k, d = a.gate.k_in;
+    char* base = static_cast<char*>(ws);
+    BatchArgs b{};
+    for (int i = 0; i < E; ++i) b.lay[i] = stack_desc(experts[i]);
+    b.route = topk_idx;
+    b.nexp = E;
+    b.xdiv = k;                                   // instance l runs token l / k
+    b.x = static_cast<const uint16_t*>(x);
+    b.t = reinterpret_cast<float*>(base + kCtlBytes);
+    b.h = reinterpret_cast<uint16_t*>(base + kCtlBytes + batch_t_bytes(&a, n, 1));
+    b.y = reinterpret_cast<uint16_t*>(base + kCtlBytes + batch_t_bytes(&a, n, 1) +
+                                      batch_h_bytes(&a, n, 1));
+    b.M = 1;
+    b.d = d;
+    b.f = a.gate.n_out;
+    b.r = a.rank;
+    b.gg = a.gate.group;
+    b.bg = a.gate.bits;
+    b.gd = a.down.group;
+    b.bd = a.down.bits;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = b.r > 0 ? launch_lora_a_batch(b, n, st) : hipSuccess;
+    if (e == hipSuccess)
+        e = launch_gateup_batch(b, n, st);
+    if (e == hipSuccess)
+        e = launch_down_batch(b, n, st);
+    if (e == hipSuccess)
+        e = launch_moe_combine(b.y, topk_w, M, k, d, static_cast<uint16_t*>(y), st);
+    return from_hip(e);
+}
+
 const char* qmlp_status_string(qmlp_status s) {
     switch (s) {
     case QMLP_OK: return "ok";

@@ -30,6 +30,29 @@ hipError_t launch_down_batch(const BatchArgs& b, int nb, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
+// One thread per output element: the routing-weighted sum of the k expert
+// outputs of its token (Sec. 5 names the routed experts of the MoE decoder;
+// the weights come with the routing).
+__global__ void __launch_bounds__(256)
+moe_combine_kernel(const uint16_t* __restrict__ yi, const float* __restrict__ w, int M, int k,
+                   int d, uint16_t* __restrict__ y) {
+    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (long)M * d)
+        return;
+    const long m = i / d, c = i - m * d;
+    float acc = 0.0f;
+    for (int j = 0; j < k; ++j)
+        acc += w[m * k + j] * h2f(yi[(m * k + j) * d + c]);
+    y[i] = (uint16_t)f2h(acc);
+}
+
+hipError_t launch_moe_combine(const uint16_t* yi, const float* w, int M, int k, int d, uint16_t* y,
+                              hipStream_t st) {
+    const long n = (long)M * d;
+    moe_combine_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(yi, w, M, k, d, y);
+    return hipGetLastError();
+}
+
 // A single block as a batch of one.
 hipError_t launch_down(DownArgs a, hipStream_t st) {
     BatchArgs b{};

@@ -19,8 +19,9 @@ lora_a_kernel(BatchArgs b) {
     const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     if (wave >= 2 * b.r)
         return;
-    lora_a_row<MT, (MT <= 4 ? 12 / MT : 1)>(b.lay[l].Ag, b.lay[l].Au, b.x + (long)l * b.M * b.d,
-                                            b.M, b.d, b.r, wave, b.t + (long)l * b.M * 2 * b.r,
+    const int e = batch_expert(b, l);
+    lora_a_row<MT, (MT <= 4 ? 12 / MT : 1)>(b.lay[e].Ag, b.lay[e].Au, batch_x(b, l), b.M, b.d,
+                                            b.r, wave, b.t + (long)l * b.M * 2 * b.r,
                                             threadIdx.x & 63);
 }
 

@@ -10,15 +10,31 @@
 
 namespace qmlp {
 
+// The descriptor instance l of a batch runs: its own, or on a routed batch
+// the routed expert's (read once per workgroup, uniform, clamped to the
+// table so an out-of-range id cannot address outside it).
+__device__ __forceinline__ int batch_expert(const BatchArgs& b, int l) {
+    if (!b.route)
+        return l;
+    int e = __builtin_amdgcn_readfirstlane(b.route[l]);
+    e = e < 0 ? 0 : (e >= b.nexp ? b.nexp - 1 : e);
+    return e;
+}
+
+// The input of instance l: its own rows, or those of its token group.
+__device__ __forceinline__ const uint16_t* batch_x(const BatchArgs& b, int l) {
+    return b.x + (long)(b.xdiv > 1 ? l / b.xdiv : l) * b.M * b.d;
+}
+
 // Block l of a batch: weights from its descriptor, activations at offset l.
 __device__ __forceinline__ GateUpArgs batch_gateup_args(const BatchArgs& b, int l) {
-    const StackLayerDesc& w = b.lay[l];
+    const StackLayerDesc& w = b.lay[batch_expert(b, l)];
     GateUpArgs a;
     a.cg = w.cg;
     a.mg = w.mg;
     a.cu = w.cu;
     a.mu = w.mu;
-    a.x = b.x + (long)l * b.M * b.d;
+    a.x = batch_x(b, l);
     // With rank 0 the item still issues (unused) LoRA-B loads: point them at x.
     a.Bg = b.r > 0 ? w.Bg : a.x;
     a.Bu = b.r > 0 ? w.Bu : a.x;
@@ -98,8 +114,9 @@ hipError_t launch_gateup_bits(BatchArgs args, int nb, int S, hipStream_t st) {
 // Block l of a batch: weights from its descriptor, h and y at offset l.
 __device__ __forceinline__ DownArgs batch_down_args(const BatchArgs& b, int l) {
     DownArgs a;
-    a.cd = b.lay[l].cd;
-    a.md = b.lay[l].md;
+    const int e = batch_expert(b, l);
+    a.cd = b.lay[e].cd;
+    a.md = b.lay[e].md;
     a.h = b.h + (long)l * b.M * b.f;
     a.y = b.y + (long)l * b.M * b.d;
     a.M = b.M;

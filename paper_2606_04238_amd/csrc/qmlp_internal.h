@@ -103,10 +103,21 @@ struct BatchArgs {
     int gg, bg;              // gate/up group and code width
     int gd, bd;              // down group and code width
     int uc;                  // units per LDS chunk (set by the launcher)
+    // Routed batches (mixture of experts): instance l runs the weights of
+    // expert route[l] (a device array; 0 <= route[l] < nexp, clamped) on input
+    // row group l / xdiv of x.  route == nullptr: instance l runs lay[l] on
+    // x + l*M*d (xdiv 0 or 1).
+    const int32_t* route;
+    int nexp;
+    int xdiv;
 };
 hipError_t launch_lora_a_batch(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_gateup_batch(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_down_batch(const BatchArgs& b, int nb, hipStream_t st);
+// y[m] = sum_j w[m k + j] * yi[m k + j] over the k routed experts of token m
+// (fp32 sum, one rounding to binary16); yi [M k][d], w [M k], y [M][d].
+hipError_t launch_moe_combine(const uint16_t* yi, const float* w, int M, int k, int d, uint16_t* y,
+                              hipStream_t st);
 size_t stack_ws_bytes(int d, int f, int r);
 int stack_max_layers();
 hipError_t launch_stack(const StackLayerDesc* layers, int L, int d, int f, int g, int r,

@@ -348,3 +348,33 @@ def test_linear_batch_validation(q, lib):
     assert lib.qmlp_linear_batch(arr(w), 1, None, 1, 0, P(FAKE), None) == NULL
     assert lib.qmlp_linear_batch(arr(w), 1, P(FAKE + 8), 1, 0, P(FAKE), None) == ALIGN
     assert lib.qmlp_linear_batch(arr(w), 1, P(FAKE), 0, 0, P(FAKE), None) == OK
+
+
+def test_moe_validation(q, lib):
+    """qmlp_forward_moe: 1..40 experts of one shape, 1 <= k <= E, M*k <= 40,
+    binary16; routing arrays are device pointers checked for NULL and
+    alignment only."""
+    P = ctypes.c_void_p
+    E = 8
+    arr = _stack_arr(q, *[_mlp(q) for _ in range(E)])
+
+    def fm(a, n, M=1, k=2, x=FAKE, idx=FAKE, w=FAKE, y=FAKE, ws=FAKE, wsb=1 << 30, dt=0):
+        return lib.qmlp_forward_moe(a, n, P(x), M, dt, P(idx), P(w), k, P(y), P(ws), wsb, None)
+
+    assert fm(arr, E, k=0) == SHAPE
+    assert fm(arr, E, k=9) == SHAPE
+    assert fm(arr, E, M=-1) == SHAPE
+    assert fm(arr, E, M=17) == UNSUP
+    assert fm(arr, E, M=11, k=4) == UNSUP                    # 44 instances
+    assert fm(arr, E, dt=1) == UNSUP
+    assert fm(arr, E, M=0) == OK
+    assert fm(arr, E, idx=0) == NULL
+    assert fm(arr, E, w=FAKE + 2) == ALIGN
+    need = lib.qmlp_moe_workspace_bytes(arr, E, 3, 2, 0)
+    r256 = lambda v: (v + 255) // 256 * 256
+    assert need == 1024 + r256(6 * 16 * 4) + r256(6 * 512 * 2) + r256(6 * 256 * 2)
+    assert fm(arr, E, M=3, wsb=need - 1) == WS
+    big = _stack_arr(q, *[_mlp(q) for _ in range(41)])
+    assert fm(big, 41) == SHAPE
+    odd = _stack_arr(q, _mlp(q), _mlp(q, d=320, f=448))
+    assert fm(odd, 2, k=1) == SHAPE
