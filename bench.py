@@ -29,11 +29,15 @@ precision_comparison: the MLP-level analogue of the paper's Gain and
 Capture (Sec. 5.2) on this GPU.  The same fp32 weights are packed as uniform
 W4 (gate/up and down at 4 bits), uniform W2, W4/W2-GateUp with its LoRA
 adapters, W4/W2-GateUp with the paper's INT2 group of 32, and the 3-bit
-gate/up of Appendix B at group 32; all five run
-on the same stand-alone decode kernels (qmlp_forward_batch: LoRA-A, gate/up
-and down of every block in one launch each; one pass over the 36 blocks
-captured in a HIP graph), so the comparison isolates the bit widths:  Gain = TPS_mix / TPS_W4 - 1,  Capture = (TPS_mix - TPS_W4) /
-(TPS_W2 - TPS_W4), with TPS = 1 / (us per MLP step).
+gate/up of Appendix B at group 32; all five run on the same stand-alone
+decode kernels (qmlp_forward_batch: LoRA-A, gate/up and down of every block
+in one launch each; one pass over the 36 blocks captured in a HIP graph), so
+the comparison isolates the bit widths:  Gain = TPS_mix / TPS_W4 - 1,
+Capture = (TPS_mix - TPS_W4) / (TPS_W2 - TPS_W4), TPS = 1 / (us per MLP step).
+
+decoder_model: the same comparison for a whole Qwen3-4B-shaped decoder token
+(attention projections, MLPs, LM head, and a KV-cache read standing in for
+attention; Sec. 5.2's method with measured times).
 """
 from __future__ import annotations
 
@@ -250,12 +254,14 @@ def decoder_model(stack: Stack, seed: int, steps: int, min_warm_s: float, mlp_us
                   threads: int = 16):
     """Whole-model decode throughput of W4, W2 and W4/W2-GateUp on this GPU,
     the method of Sec. 5.2 (per-token time summed over the operators, TPS =
-    1 / time) with measured operator times: per layer the q/k/v projection
+    1 / time) with measured times: per layer the q/k/v projection
     (one [q + 2 kv][d] matrix) and the o projection (qmlp_linear_batch over
     the layers; 4-bit, or 2-bit for W2), the MLP (mlp_us: the precision
     comparison's pass), and the read of a BF16 KV cache of ctx positions (a
     streaming read of those bytes stands in for attention, which is not
-    built); per token the LM head at the linears' width."""
+    built); per token the LM head at the linears' width.  The weight part of
+    a token is timed as one graph per width; the per-operator times are
+    reported beside it."""
     import torch
     import oracle as orc
     import paper_2606_04238_amd as q
@@ -318,11 +324,30 @@ def decoder_model(stack: Stack, seed: int, steps: int, min_warm_s: float, mlp_us
                                 "lm_head_4bit": round(us[(4, "lm_head")], 2),
                                 "lm_head_2bit": round(us[(2, "lm_head")], 2),
                                 "kv_read_bf16": round(kv_us, 2)}}
+    # the token step as one graph per width (the linears and the MLP of every
+    # layer, the LM head): a long replay, steadier than the short per-operator
+    # launches above, whose times vary with the clocks between repeats
+    ys = {name: torch.empty((L, 1, shapes[name][0]), dtype=torch.float16, device="cuda")
+          for name in shapes}
+    yl = torch.empty((1, 1, dims.vocab), dtype=torch.float16, device="cuda")
     tps = {}
     for name, b in widths.items():
-        t = mlp_us[name] * L + us[(b, "qkv")] + us[(b, "o")] + us[(b, "lm_head")] + kv_us
+        lay, ws = stack.variant_layers[name]
+
+        def token():
+            q.linear_batch(packs[b]["qkv"], xs["qkv"], y=ys["qkv"])
+            q.linear_batch(packs[b]["o"], xs["o"], y=ys["o"])
+            q.forward_batch(lay, stack.X, y=stack.YB, ws=ws)
+            q.linear_batch([lm[b]], xl, y=yl)
+        gr = capture(token)
+        ms, _ = time_passes(gr.replay, steps, 2, min_warm_s)
+        t_w = sum(ms) / len(ms) * 1e3
+        t = t_w + kv_us
         tps[name] = 1e6 / t
-        out[name] = {"us_per_token": round(t, 1), "tokens_per_s": round(tps[name], 1)}
+        out[name] = {"us_per_token": round(t, 1), "weights_graph_us": round(t_w, 1),
+                     "sum_of_operator_us": round(mlp_us[name] * L + us[(b, "qkv")] + us[(b, "o")]
+                                                 + us[(b, "lm_head")] + kv_us, 1),
+                     "tokens_per_s": round(tps[name], 1)}
     t4, t2, tm = tps["w4_uniform"], tps["w2_uniform"], tps["w4w2_gateup_lora"]
     out["gain_pct"] = round((tm - t4) / t4 * 100, 1)
     out["capture_pct"] = round((tm - t4) / (t2 - t4) * 100, 1)
