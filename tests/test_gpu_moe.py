@@ -72,3 +72,62 @@ def test_moe_repeated_expert_and_single_slot(q):
     yr = q.forward(mlps[1], x)
     torch.cuda.synchronize()
     assert orc.max_rel_err(values_of(y), values_of(yr)) <= 1e-3
+
+
+def test_moe_and_batch_graph_replays_match_eager(q):
+    """qmlp_forward_moe and qmlp_forward_batch captured in a HIP graph and
+    replayed several times, with eager work in between: every replay gives
+    the eager bits."""
+    cfg = wl.Config("moe_graph", M=1, d=512, f=768, g=64, r=8, L=1)
+    print("\n[case] moe / batch graph replay", flush=True)
+    E, k, M = 6, 2, 3
+    lays = [wl.layer(cfg, e) for e in range(E)]
+    experts = q.Layers([gpu_mlp(lay) for lay in lays])
+    x = act_tensor(wl.activations(cfg, 11, 0, M=M))
+    idx, w = wl.routing(M, E, k, 4)
+    idx, w = torch.from_numpy(idx).cuda(), torch.from_numpy(w).cuda()
+    ws = torch.zeros(q.moe_workspace_bytes(experts, M, k), dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(x)
+    xb = torch.stack([act_tensor(lay.x) for lay in lays])
+    wsb = q.batch_workspace(experts, 1)
+    yb = torch.empty_like(xb)
+
+    def run():
+        q.forward_moe(experts, x, idx, w, y=y, ws=ws)
+        q.forward_batch(experts, xb, y=yb, ws=wsb)
+    run()
+    torch.cuda.synchronize()
+    ey, eb = y.clone(), yb.clone()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            run()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        y.fill_(0)
+        yb.fill_(0)
+        junk = torch.randn(1 << 20, device="cuda").sum()
+        g.replay()
+        torch.cuda.synchronize()
+        assert float(junk) == float(junk)
+        assert torch.equal(y.view(torch.int16), ey.view(torch.int16)), rep
+        assert torch.equal(yb.view(torch.int16), eb.view(torch.int16)), rep
+
+
+def test_moe_route_ids_outside_the_table_are_clamped(q):
+    """Expert ids beyond the table read the last expert, negative ids the
+    first (the kernels clamp; nothing is read outside the table)."""
+    cfg = wl.Config("moe_clamp", M=1, d=512, f=768, g=64, r=8, L=1)
+    print("\n[case] moe clamped ids", flush=True)
+    E = 3
+    lays = [wl.layer(cfg, e) for e in range(E)]
+    experts = q.Layers([gpu_mlp(lay) for lay in lays])
+    x = act_tensor(wl.activations(cfg, 12, 0, M=2))
+    w = torch.ones((2, 1), dtype=torch.float32, device="cuda")
+    bad = q.forward_moe(experts, x, torch.tensor([[7], [-5]], dtype=torch.int32, device="cuda"), w)
+    good = q.forward_moe(experts, x, torch.tensor([[2], [0]], dtype=torch.int32, device="cuda"), w)
+    torch.cuda.synchronize()
+    assert torch.equal(bad.view(torch.int16), good.view(torch.int16))
