@@ -397,47 +397,6 @@ def time_passes(fn, steps: int, warmup: int, min_warm_s: float = 0.25):
     return [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)], wall
 
 
-def kernel_durations(stack: Stack, passes: int = 5):
-    """Average launch duration (us) of the layer's kernels, each bracketed by
-    events on the launch stream.  With the one-kernel-per-layer forward that
-    is the fused kernel; otherwise the gate/up half (LoRA-A + fused gate/up)
-    and the 4-bit down kernel are bracketed separately."""
-    import torch
-    import paper_2606_04238_amd as q
-    st = torch.cuda.current_stream()
-    fused = q.forward_launches(stack.mlps[0], stack.cfg.M) == 1
-    h = torch.empty((stack.cfg.M, stack.cfg.f), dtype=stack.ys[0].dtype, device="cuda")
-    a, b = [], []
-    for _ in range(passes):
-        marks = []
-        for m, x, y in zip(stack.mlps, stack.xs, stack.ys):
-            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
-            e0.record(st)
-            if fused:
-                q.forward(m, x, y=y, ws=stack.ws)
-                e1.record(st)
-                e2.record(st)
-            else:
-                q.gateup_w2_lora(m, x, h=h, ws=stack.ws)
-                e1.record(st)
-                q.down_w4(m.down, h, y=y)
-                e2.record(st)
-            marks.append((e0, e1, e2))
-        torch.cuda.synchronize()
-        for e0, e1, e2 in marks:
-            a.append(e0.elapsed_time(e1) * 1e3)
-            b.append(e1.elapsed_time(e2) * 1e3)
-    return fused, statistics.mean(a), statistics.mean(b)
-
-
-def kernel_bytes(cfg: wl.Config):
-    """Algorithmic bytes per launch of each half (each includes the h it writes/reads)."""
-    M, d, f, g, r = cfg.M, cfg.d, cfg.f, cfg.g, cfg.r
-    gateup = f * d // 2 + 8 * f * d // g + 4 * r * (d + f) + 2 * M * d + 2 * M * f
-    down = d * f // 2 + 4 * d * f // g + 2 * M * f + 2 * M * d
-    return gateup, down
-
-
 # --------------------------------------------------------------------- cpu baseline
 def cpu_baseline(cfg: wl.Config, seed: int, budget_s: float = 12.0, max_layers: int | None = None):
     """The fp64 oracle forward (single thread) over the first layers of the
@@ -793,17 +752,7 @@ def main(argv=None):
         dom_us, dom_b = t_step * 1e3, L * B
         kernel_us = {"batched_step": round(dom_us, 3), "launches_per_step": launches}
     else:
-        fused, k1_us, k2_us = kernel_durations(stack)
-        if fused:
-            # the timed step is L launches of the fused kernel back to back
-            dom_name, dom_b = "fused_layer_kernel", B
-            dom_us = us_layer
-            kernel_us = {"fused_layer_event_bracketed": round(k1_us, 3)}
-        else:
-            gu_b, dn_b = kernel_bytes(cfg)
-            kernel_us = {"gateup_half": round(k1_us, 3), "down_w4": round(k2_us, 3)}
-            dom_name, dom_us, dom_b = ("gateup_w2 (LoRA-A + fused gate/up)", k1_us, gu_b) \
-                if k1_us >= k2_us else ("down_w4", k2_us, dn_b)
+        raise RuntimeError("binary16 decode runs persistently or batched; got %d launches" % launches)
     achieved = dom_b / (dom_us * 1e-6) / 1e9
 
     out = {
