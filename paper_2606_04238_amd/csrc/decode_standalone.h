@@ -5,6 +5,8 @@
 // parallel; decode_gateup.hip and decode_down.hip dispatch to them.
 #pragma once
 
+#include <type_traits>
+
 #include "decode_common.h"
 #include "decode_launch.h"
 
@@ -157,6 +159,174 @@ down_kernel(BatchArgs b) {
     dn_finish(it, a, lane);
 }
 
+// ---- software-pipelined down kernel: batches at one token.
+// Each wave owns NI consecutive items of 64/S rows; the loads of item k+1
+// are issued before item k is computed (two register sets, straight-line
+// code), so a wave keeps a load stream in flight through its arithmetic
+// instead of alternating "all loads, then all compute".  h is staged once
+// per workgroup for 4 * NI items.  JJ = units per lane, exact (every slot
+// loads, from a clamped address when past the row).
+constexpr int kPipeItems = 4;
+constexpr int kPipeMaxUnits = 6;                     // JJ: units per lane
+constexpr int kPipeStageWords = 6;                   // staging words per thread: U <= 384
+
+template <int JJ>
+struct PipeItem {
+    uint4 q[JJ];
+    uint32_t m[JJ];
+};
+
+template <int S, int JJ, int B>
+__device__ __forceinline__ void pipe_load(PipeItem<JJ>& it, const DownArgs& a, int U, int row,
+                                          int lane) {
+    const int s = lane % S;
+    const int upg = a.g / codes_per_unit(B);
+    const long rowc = row < a.d ? row : 0;
+    const uint4* cd = reinterpret_cast<const uint4*>(a.cd) + rowc * U;
+    const uint32_t* md = a.md + rowc * (a.f / a.g);
+#pragma unroll
+    for (int i = 0; i < JJ; ++i) {
+        const int u = s + S * i;
+        const int uu = u < U ? u : 0;
+        it.q[i] = load_stream(cd + uu);
+        it.m[i] = load_stream(md + uu / upg);
+    }
+}
+
+// s (sum q h' - C - z X) over the lane's units of one row (M = 1, h staged
+// whole: unit ul at chunk offset ul).
+template <int S, int JJ, int B>
+__device__ __forceinline__ float pipe_dot(PipeItem<JJ>& it, const uint4* hs, const float2* cx,
+                                          int U, int lane) {
+    const uint32_t mv = 0x64006400u;
+    const int s = lane % S;
+    float y = 0.0f;
+#pragma unroll
+    for (int i = 0; i < JJ; ++i) {
+        const int ul = s + S * i;
+        if (ul < U) {
+            uint32_t wv[4] = {it.q[i].x, it.q[i].y, it.q[i].z, it.q[i].w};
+            uint32_t mi = it.m[i];
+#pragma unroll
+            for (int w = 0; w < 4; ++w) pin(wv[w]);
+            pin(mi);
+            float acc = 0.0f;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                if constexpr (B == 4) {
+                    uint32_t e[4];
+                    extract_w4(wv[w], e, mv);
+                    const uint4 p = hs[ul * 4 + (w ^ ((ul >> 1) & 3))];
+                    acc = dot2(e[0], p.x, acc);
+                    acc = dot2(e[1], p.y, acc);
+                    acc = dot2(e[2], p.z, acc);
+                    acc = dot2(e[3], p.w, acc);
+                } else {
+                    uint32_t e[8];
+                    extract_w2(wv[w], e, mv);
+                    const uint4 p0 = hs[ul * 8 + ((2 * w) ^ (ul & 7))];
+                    const uint4 p1 = hs[ul * 8 + ((2 * w + 1) ^ (ul & 7))];
+                    const uint32_t hp[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+                    for (int p = 0; p < 8; ++p) acc = dot2(e[p], hp[p], acc);
+                }
+            }
+            const float2 k = cx[ul];
+            y += h2f(mi & 0xFFFFu) * (acc - k.x - h2f(mi >> 16) * k.y);
+        }
+    }
+    return y;
+}
+
+template <int S, int JJ, int B, int NI>
+__global__ void __launch_bounds__(256)
+down_pipe_kernel(BatchArgs b) {
+    const DownArgs a = batch_down_args(b, blockIdx.y);
+    constexpr int CH = B == 2 ? 8 : 4;
+    constexpr int RPI = 64 / S;                      // rows per item
+    extern __shared__ uint4 smem[];
+    const int U = a.f / codes_per_unit(B);
+    uint4* hs = smem;
+    float2* cx = reinterpret_cast<float2*>(smem + U * CH);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int row0 = (blockIdx.x * 4 + (tid >> 6)) * NI * RPI + lane / S;
+    // h is loaded BEFORE the first item's weights: loads retire in order, so
+    // the staging can convert it while the weight stream is still in flight
+    // (4 U staging words, at most kPipeStageWords per thread; the loads of
+    // words past the end read word 0 and are dropped by the store).
+    using HW = typename std::conditional<B == 2, XWord, uint4>::type;
+    HW hv[kPipeStageWords];
+#pragma unroll
+    for (int j = 0; j < kPipeStageWords; ++j) {
+        if constexpr (B == 2)
+            hv[j] = stage_x_load<1>(a.h, 1, a.f, 0, U, tid + 256 * j);
+        else
+            hv[j] = stage_h_load<1>(a.h, 1, a.f, 0, U, tid + 256 * j);
+    }
+    __builtin_amdgcn_sched_barrier(0);              // keep the h loads ahead of the weights
+    PipeItem<JJ> buf[2];
+    pipe_load<S, JJ, B>(buf[0], a, U, row0, lane);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < kPipeStageWords; ++j) {
+        if constexpr (B == 2)
+            stage_x_store<1>(hs, cx, U, U, 1, tid + 256 * j, hv[j]);
+        else
+            stage_h_store<1>(hs, cx, U, U, 1, tid + 256 * j, hv[j]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < NI; ++k) {
+        if (k + 1 < NI)
+            pipe_load<S, JJ, B>(buf[(k + 1) & 1], a, U, row0 + (k + 1) * RPI, lane);
+        const float v = group_sum<S>(pipe_dot<S, JJ, B>(buf[k & 1], hs, cx, U, lane));
+        const int row = row0 + k * RPI;
+        if (lane % S == 0 && row < a.d)
+            a.y[row] = (uint16_t)f2h(v);
+    }
+}
+
+
+// The pipelined kernel serves batches at M = 1 whose whole h fits the LDS
+// budget; S = the fewest lanes per row with at most kPipeMaxUnits units each.
+inline int pipe_lanes(int U) {
+    if (4 * U > 256 * kPipeStageWords)
+        return 0;
+    for (int S = 8; S <= 64; S *= 2)
+        if ((U + S - 1) / S <= kPipeMaxUnits) return S;
+    return 0;
+}
+
+#define QMLP_PIPE_CASE(S_, J_)                                                            \
+    if (S == S_ && JJ == J_) {                                                            \
+        auto k = down_pipe_kernel<S_, J_, B, kPipeItems>;                                 \
+        hipError_t e = set_lds(k, lds);                                                   \
+        if (e != hipSuccess) return e;                                                    \
+        k<<<grid, 256, lds, st>>>(args);                                                  \
+        return hipGetLastError();                                                         \
+    }
+#define QMLP_PIPE_S(S_) QMLP_PIPE_CASE(S_, 1) QMLP_PIPE_CASE(S_, 2) QMLP_PIPE_CASE(S_, 3) \
+    QMLP_PIPE_CASE(S_, 4) QMLP_PIPE_CASE(S_, 5) QMLP_PIPE_CASE(S_, 6)
+
+template <int B>
+hipError_t launch_down_pipe(const BatchArgs& args, int nb, hipStream_t st) {
+    const int U = args.f / codes_per_unit(B);
+    const int S = pipe_lanes(U);
+    const int JJ = S ? (U + S - 1) / S : 0;
+    const size_t lds = (size_t)U * (B == 2 ? GU_UNIT_BYTES : DN_UNIT_BYTES);
+    const int rows_per_block = 4 * kPipeItems * (64 / (S ? S : 64));
+    const dim3 grid((args.d + rows_per_block - 1) / rows_per_block, (unsigned)nb);
+    QMLP_PIPE_S(8) QMLP_PIPE_S(16) QMLP_PIPE_S(32) QMLP_PIPE_S(64)
+    return hipErrorInvalidValue;
+}
+
+template <int B>
+bool down_pipe_fits(const BatchArgs& args, int nb) {
+    const int U = args.f / codes_per_unit(B);
+    return nb > 1 && args.M == 1 && pipe_lanes(U) != 0 &&
+           (size_t)U * (B == 2 ? GU_UNIT_BYTES : DN_UNIT_BYTES) <= (size_t)kLdsBudget;
+}
+
 #define QMLP_DN_CASE(MT_, S_, J_)                                                         \
     if (mt == MT_ && S == S_ && mj == J_) {                                               \
         auto k = down_kernel<MT_, S_, J_, B, NT>;                                         \
@@ -170,6 +340,8 @@ down_kernel(BatchArgs b) {
 
 template <int B, int NT>
 hipError_t launch_down_bits(BatchArgs args, int nb, int S, hipStream_t st) {
+    if (NT == 256 && down_pipe_fits<B>(args, nb))
+        return launch_down_pipe<B>(args, nb, st);
     const int U = args.f / codes_per_unit(B);
     const int J = (U + S - 1) / S;
     const int mj = maxj_for(J);
