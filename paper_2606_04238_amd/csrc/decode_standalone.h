@@ -287,7 +287,7 @@ down_pipe_kernel(BatchArgs b) {
 }
 
 
-// The pipelined kernel serves batches at M = 1 whose whole h fits the LDS
+// The pipelined kernel serves M = 1 launches whose whole h fits the LDS
 // budget; S = the fewest lanes per row with at most kPipeMaxUnits units each.
 inline int pipe_lanes(int U) {
     if (4 * U > 256 * kPipeStageWords)
@@ -320,10 +320,14 @@ hipError_t launch_down_pipe(const BatchArgs& args, int nb, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
+// Batches, and single launches with rows enough to fill the chip in
+// workgroups of 4 * kPipeItems items (an LM head).
+constexpr int kPipeSingleMinRows = 16384;
+
 template <int B>
 bool down_pipe_fits(const BatchArgs& args, int nb) {
     const int U = args.f / codes_per_unit(B);
-    return nb > 1 && args.M == 1 && pipe_lanes(U) != 0 &&
+    return (nb > 1 || args.d >= kPipeSingleMinRows) && args.M == 1 && pipe_lanes(U) != 0 &&
            (size_t)U * (B == 2 ? GU_UNIT_BYTES : DN_UNIT_BYTES) <= (size_t)kLdsBudget;
 }
 
