@@ -57,6 +57,19 @@ def test_moe_gptoss20b_shape_matches_oracle(q):
     assert err <= Y_TOL
 
 
+@pytest.mark.parametrize("d", [1024, 2048])
+def test_moe_few_instances_take_more_lanes_per_row(q, d):
+    """One token routed to one or two experts fills fewer than two workgroups
+    per CU, so the gate/up launch doubles its lanes per row (16, then 32 at
+    d = 2048, one 16-byte unit per lane); the result still matches the oracle."""
+    cfg = wl.Config("moe_wide_tiny", M=1, d=d, f=768, g=64, r=8, L=1)
+    for k in (1, 2):
+        print("\n[case] moe d %d E 4 k %d M 1" % (d, k), flush=True)
+        err = _run(q, cfg, 4, k, 1, layer=k)
+        print("max-rel %.2e" % err)
+        assert err <= Y_TOL
+
+
 def test_moe_repeated_expert_and_single_slot(q):
     """Two tokens routed to the same expert with weight 1 each (k = 1) give
     that expert's qmlp_forward outputs."""
