@@ -311,7 +311,17 @@ inline int pipe_lanes(int U) {
 template <int B>
 hipError_t launch_down_pipe(const BatchArgs& args, int nb, hipStream_t st) {
     const int U = args.f / codes_per_unit(B);
-    const int S = pipe_lanes(U);
+    int S = pipe_lanes(U);
+    // Routed launches over a few expert instances: double the lanes per row
+    // while the grid has fewer than two workgroups per CU (as for gate/up).
+    if (args.route && S) {
+        const auto blocks = [&](int s) {
+            const int rpb = 4 * kPipeItems * (64 / s);
+            return (long)((args.d + rpb - 1) / rpb) * nb;
+        };
+        while (S < 64 && 2 * S <= U && blocks(S) < 2L * 256)
+            S *= 2;
+    }
     const int JJ = S ? (U + S - 1) / S : 0;
     const size_t lds = (size_t)U * (B == 2 ? GU_UNIT_BYTES : DN_UNIT_BYTES);
     const int rows_per_block = 4 * kPipeItems * (64 / (S ? S : 64));
