@@ -443,3 +443,74 @@ def test_moe_single_expert_and_linearity():
     assert np.array_equal(orc.moe_forward(ex, idx, 2 * w, x), 2 * y)
     y2 = orc.moe_forward(ex, idx[:, ::-1].copy(), w[:, ::-1].copy(), x)
     assert np.allclose(y2, y, rtol=1e-14, atol=1e-14 * np.abs(y).max())
+
+
+# ---------------------------------------- down on a given intermediate; LoRA-A
+def _numpy_act(bits, bf16):
+    """Activation bits -> float64 with numpy's own decoders (not the oracle's)."""
+    bits = np.asarray(bits, np.uint16)
+    if bf16:
+        return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return bits.view(np.float16).astype(np.float64)
+
+
+def _numpy_dequant(q):
+    s = q.scale.view(np.float16).astype(np.float64)
+    z = q.zero.view(np.float16).astype(np.float64)
+    return (q.codes.astype(np.float64) - np.repeat(z, q.group, axis=1)) * np.repeat(s, q.group, axis=1)
+
+
+@pytest.mark.parametrize("act,bits,group,M", [("f16", 4, 64, 3), ("bf16", 4, 128, 5),
+                                              ("f16", 2, 128, 1), ("bf16", 2, 64, 2)])
+def test_down_act_matches_numpy(act, bits, group, M):
+    """y = W_down h with h handed over in the activation type: numpy decodes the
+    bits (binary16 view, or bfloat16 as the upper half of a binary32) and
+    multiplies by the dequantized matrix rebuilt from codes/scale/zero.  The
+    bf16 case feeds bit patterns whose binary16 reading differs wildly, so a
+    down step that ignored the type would fail by orders of magnitude."""
+    cfg = _small_cfg(M=M, d=256, f=384, g=group, act=act)
+    L = wl.layer(cfg, 7)
+    qd = orc.quantize(L.W_down, bits, group)
+    rng = np.random.default_rng(13)
+    h = wl.to_act_bits(rng.standard_normal((M, cfg.f)) * 0.3, act)
+    y = orc.down_act(qd, h, bf16=(act == "bf16"))
+    ref = _numpy_act(h, act == "bf16") @ _numpy_dequant(qd).T
+    assert orc.max_rel_err(y, ref) < 1e-12
+    # the other reading of the same bits gives a different answer
+    other = _numpy_act(h, act != "bf16") @ _numpy_dequant(qd).T
+    assert orc.max_rel_err(other, ref) > 1e-2
+
+
+@pytest.mark.parametrize("act", ["f16", "bf16"])
+def test_lora_a_matches_numpy_both_types(act):
+    """t = A x over both activation types, against numpy's decoders."""
+    cfg = _small_cfg(M=4, r=16, act=act)
+    L = wl.layer(cfg, 8)
+    t = orc.lora_a(L.A_up, L.x, bf16=(act == "bf16"))
+    ref = _numpy_act(L.x, act == "bf16") @ _numpy_act(L.A_up, act == "bf16").T
+    assert orc.max_rel_err(t, ref) < 1e-13
+    other = _numpy_act(L.x, act != "bf16") @ _numpy_act(L.A_up, act != "bf16").T
+    assert not np.allclose(other, ref, rtol=1e-3, atol=0)
+
+
+@pytest.mark.parametrize("lora_scale", [0.5, 2.0])
+def test_moe_forward_passes_lora_scale(lora_scale):
+    """Every expert's adapters are scaled by lora_scale (Eq. (1)): the routed
+    sum against numpy brute force at scales other than 1."""
+    cfg = _small_cfg(M=1, d=128, f=192, g=64, r=8)
+    ex = _experts(3, cfg, seed=2)
+    lays = [wl.layer(cfg, e, 2) for e in range(3)]
+    x = wl.activations(cfg, 4, 2, M=2)
+    idx = np.array([[1, 2], [0, 1]], np.int32)
+    w = np.array([[0.375, 0.625], [0.75, 0.25]], np.float32)
+    y = orc.moe_forward(ex, idx, w, x, lora_scale=lora_scale)
+    y1 = orc.moe_forward(ex, idx, w, x, lora_scale=1.0)
+    for m in range(2):
+        ref = 0.0
+        for e, ww in zip(idx[m], w[m]):
+            L = lays[e]
+            one = wl.Layer(cfg, e, L.W_gate, L.W_up, L.W_down, L.A_gate, L.B_gate, L.A_up, L.B_up,
+                           x[m:m + 1])
+            ref = ref + float(ww) * _numpy_forward(cfg, one, *ex[e][:3], lora_scale=lora_scale)[0][0]
+        assert orc.max_rel_err(y[m], ref) < 1e-12
+    assert not np.array_equal(y, y1)
