@@ -645,6 +645,53 @@ def prefill_main(cfg: wl.Config, args):
 
 
 # --------------------------------------------------------------------- main
+# --------------------------------------------------------------------- HBM read rate
+PROBE_BLOCKS = (256, 512, 1024, 2048, 4096, 8192)
+
+
+def stream_probe_main(args):
+    """The read rate this GPU sustains: one read-only pass over a buffer far
+    larger than the 256 MB Infinity Cache, 128-bit loads, no arithmetic.
+    Context for the decode roofline, not its denominator (that stays the
+    8 TB/s peak)."""
+    import torch
+    import paper_2606_04238_amd as q
+    n = args.stream_probe_mib << 20
+    buf = torch.empty(n // 4, dtype=torch.int32, device="cuda").fill_(0x01020304)
+    torch.cuda.synchronize()
+    res = {}
+    for nt in (True, False):
+        for blocks in PROBE_BLOCKS:
+            out = torch.empty(4 * blocks, dtype=torch.int32, device="cuda")
+            ms, _ = time_passes(lambda: q.probe_stream_read(buf, blocks, nt, out),
+                                max(5, args.steps // 4), 3, 0.25)
+            med = statistics.median(ms)
+            res["%s_%d" % ("nt" if nt else "plain", blocks)] = round(n / (med * 1e-3) / 1e9, 1)
+            if torch.any(out != 0):         # every word XORs an even number of equal words
+                raise RuntimeError("stream probe read unexpected data")
+    best = max(res, key=res.get)
+    line = {"stream_probe": {"mib": args.stream_probe_mib, "gbs": res, "best": best,
+                             "best_gbs": res[best], "frac_of_hbm_peak": round(res[best] / HBM_PEAK_GBS, 4),
+                             "threads_per_block": 256, "loads_in_flight_per_thread": 8}}
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def stream_calibration(mib: int):
+    """One non-temporal and one plain pass of the streaming probe over `mib`
+    MiB (reference dispatches of known read size for the byte counters)."""
+    import torch
+    import paper_2606_04238_amd as q
+    n = mib << 20
+    buf = torch.empty(n // 4, dtype=torch.int32, device="cuda").fill_(7)
+    torch.cuda.synchronize()
+    for nt in (True, False):
+        q.probe_stream_read(buf, 1024, nt)
+        torch.cuda.synchronize()
+    log("stream calibration: %d bytes read with non-temporal loads, then %d with plain loads" % (n, n))
+    del buf
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -659,6 +706,15 @@ def main(argv=None):
                     help="untimed warmup lasts at least this long (and at least --warmup steps)")
     ap.add_argument("--no-precision-comparison", action="store_true",
                     help="skip the uniform-W4 / uniform-W2 / W4/W2-GateUp comparison (Sec. 5.2)")
+    ap.add_argument("--stream-probe", action="store_true",
+                    help="only measure the HBM read rate this GPU sustains: the read-only "
+                         "streaming probe over --stream-probe-mib MiB at several grid sizes, with "
+                         "non-temporal and plain 128-bit loads; prints one JSON line")
+    ap.add_argument("--stream-probe-mib", type=int, default=4096)
+    ap.add_argument("--calibrate-stream-mib", type=int, default=0,
+                    help="after timing, run the read-only streaming probe once over this many MiB "
+                         "with non-temporal loads and once with plain loads, as reference "
+                         "dispatches for HBM byte counters")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="after timing, run one copy-like elementwise kernel over this many MiB "
                          "(read N, write N) as the reference dispatch for HBM byte counters")
@@ -676,6 +732,8 @@ def main(argv=None):
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         return 2
+    if args.stream_probe:
+        return stream_probe_main(args)
     if args.config in wl.MOE:
         return moe_main(wl.MOE[args.config], args)
     cfg = wl.CONFIGS[args.config]
@@ -797,6 +855,8 @@ def main(argv=None):
             "traffic": None if traffic is None else int(traffic),
         },
     }
+    if args.calibrate_stream_mib > 0:
+        stream_calibration(args.calibrate_stream_mib)
     if args.calibrate_copy_mib > 0:
         n = args.calibrate_copy_mib << 20
         src = torch.ones(n // 2, dtype=torch.float16, device="cuda")

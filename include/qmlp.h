@@ -345,6 +345,18 @@ qmlp_status qmlp_dequant(const qmlp_qweight *w, uint16_t *w_f16, qmlp_stream str
  * stream order, 0 if the call would be rejected.  Host-only, enqueues nothing. */
 int qmlp_forward_launches(const qmlp_mlp *mlp, int M, qmlp_dtype dtype);
 
+/* Measurement hook (not part of the MLP): read `bytes` of device memory at
+ * `buf` once with 128-bit loads -- the non-temporal form the weight stream
+ * uses when `nontemporal` is nonzero, plain loads otherwise -- and write one
+ * XOR word per wave to out[0 .. 4*blocks).  Decode is bound by the rate of
+ * loading weights (Sec. 1, Sec. 3.3); this kernel does nothing but load, so
+ * its duration is the HBM read rate this GPU sustains, and its byte
+ * counters against the known size calibrate the counters of the decode
+ * kernels.  One launch of `blocks` 256-thread workgroups.  bytes % 16 == 0,
+ * 1 <= blocks <= 65536, buf 16-byte aligned, out 4-byte aligned. */
+qmlp_status qmlp_probe_stream_read(const void *buf, size_t bytes, uint32_t *out, int blocks,
+                                   int nontemporal, qmlp_stream stream);
+
 /* A static, human-readable name of a status code. */
 const char *qmlp_status_string(qmlp_status s);
 

@@ -87,6 +87,7 @@ def _lib():
             "qmlp_forward_moe": (I, [pm, I, P, I, I, P, P, I, P, P, Z, P]),
             "qmlp_forward_batch": (I, [pm, I, P, I, I, P, P, Z, P]),
             "qmlp_status_string": (ctypes.c_char_p, [I]),
+            "qmlp_probe_stream_read": (I, [P, Z, P, I, I, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(lib, name)
@@ -461,3 +462,15 @@ def forward_stack(stack: Stack, x: torch.Tensor, y: torch.Tensor | None = None,
     _check(_lib().qmlp_forward_stack(stack.c(), len(stack), _ptr(x), M, _dtype_code(x), _ptr(y),
                                      _ptr(x_out), _ptr(ws), ws.numel(), _stream()), "forward_stack")
     return y
+
+
+def probe_stream_read(buf: torch.Tensor, blocks: int, nontemporal: bool = True,
+                      out: torch.Tensor | None = None) -> torch.Tensor:
+    """Read all of `buf` once with 128-bit loads (measurement hook; see
+    qmlp_probe_stream_read).  Returns the per-wave XOR words."""
+    if out is None:
+        out = torch.empty(4 * blocks, dtype=torch.int32, device=buf.device)
+    _check(_lib().qmlp_probe_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(out),
+                                         blocks, int(bool(nontemporal)), _stream()),
+           "qmlp_probe_stream_read")
+    return out

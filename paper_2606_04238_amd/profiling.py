@@ -4,10 +4,18 @@ figure that bench.py reports from them.
 ``summarize`` turns the CSV output of three rocprofv3 runs of the same
 command -- ``--kernel-trace --stats``, ``--pmc FETCH_SIZE`` and
 ``--pmc WRITE_SIZE`` -- into a short markdown summary.  The byte counters
-are calibrated against a copy-like elementwise dispatch of known size that
-bench.py launches with ``--calibrate-copy-mib N`` (it reads N MiB and writes
-N MiB): the factor known bytes / counted bytes of that dispatch scales the
-counters of the kernel under study.
+are calibrated against reference dispatches of known size that bench.py
+launches after its timing:
+
+* ``--calibrate-stream-mib S``: the read-only streaming probe reads S MiB
+  with the same non-temporal 128-bit loads as the weight stream, then S MiB
+  with plain loads;
+* ``--calibrate-copy-mib N``: a copy-like elementwise dispatch reads N MiB
+  and writes N MiB.
+
+FETCH_SIZE is scaled by known / counted bytes of the non-temporal probe
+(the load kind of the weight stream) when it ran, else of the copy;
+WRITE_SIZE by those of the copy.  Every factor found is listed.
 
 The summary records a digest of the HIP sources; ``read_traffic`` returns
 the traffic figure only while the sources still hash to that digest, so a
@@ -60,29 +68,51 @@ def _counter_means(pmc_dir):
     return name, out
 
 
-def _copy_dispatch(per_kernel, counter, copy_kib):
-    """Counted KiB of the calibration dispatch: the elementwise dispatch whose
-    counter lies closest to the known size (the fill that precedes it reads
-    almost nothing, so the pick is unambiguous)."""
+def _closest(per_kernel, substr, known_kib):
+    """Counted KiB of the reference dispatch whose kernel name contains
+    `substr` and whose counter lies closest to the known size (fills and
+    other small dispatches of the same name read almost nothing, so the pick
+    is unambiguous); None if no such dispatch ran."""
     best = None
     for k, vals in per_kernel.items():
-        if "elementwise" not in k:
+        if substr not in k:
             continue
         for v in vals:
-            if best is None or abs(v - copy_kib) < abs(best - copy_kib):
+            if best is None or abs(v - known_kib) < abs(best - known_kib):
                 best = v
-    if best is None or best <= 0:
-        raise ValueError("no calibration dispatch found for %s" % counter)
-    return best
+    return best if best and best > 0 else None
 
 
-def summarize(kt_dir, pf_dir, pw_dir, kernel, copy_mib, out_md, commands):
+NT_PROBE, PLAIN_PROBE, COPY = "stream_read_kernel<true>", "stream_read_kernel<false>", "elementwise"
+
+
+def _factors(per_kernel, counter, copy_kib, stream_kib):
+    """{reference: (counted KiB, known KiB, factor)} for every reference
+    dispatch of this run that applies to the counter."""
+    out = {}
+    refs = [(COPY, copy_kib)]
+    if counter.startswith("FETCH") and stream_kib:
+        refs = [(NT_PROBE, stream_kib), (PLAIN_PROBE, stream_kib)] + refs
+    for name, known in refs:
+        if not known:
+            continue
+        c = _closest(per_kernel, name, known)
+        if c is not None:
+            out[name] = (c, known, known / c)
+    return out
+
+
+def summarize(kt_dir, pf_dir, pw_dir, kernel, copy_mib, out_md, commands, stream_mib=0,
+              extra=None):
+    """Write the summary; `extra` is a list of (title, markdown lines) that
+    other counter passes contribute (they do not enter the traffic figure)."""
     stats = list(csv.DictReader(open(_one(os.path.join(kt_dir, "*kernel_stats.csv")))))
     krow = [r for r in stats if kernel in r["Name"]]
     if len(krow) != 1:
         raise ValueError("kernel %r matches %d rows of the stats" % (kernel, len(krow)))
     krow = krow[0]
     copy_kib = copy_mib * 1024.0
+    stream_kib = stream_mib * 1024.0
     lines = ["# %s -- rocprofv3 summary" % kernel, ""]
     lines += ["Commands (run from the repository root on one MI355X; `R` is that root):", ""]
     lines += ["    " + c for c in commands]
@@ -94,21 +124,30 @@ def summarize(kt_dir, pf_dir, pw_dir, kernel, copy_mib, out_md, commands):
             r["Name"][:90], r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
             float(r["MaxNs"]) / 1e3, r["Percentage"]))
     total = 0.0
+    cal = ["", "## Calibration dispatches (known bytes / counted bytes)", "",
+           "| counter | reference dispatch | counted KiB | known KiB | factor |", "|---|---|---|---|---|"]
     lines += ["", "## HBM byte counters (--pmc, one counter per run)", "",
-              "| counter | kernel KiB/dispatch (mean) | dispatches | copy dispatch KiB | known KiB "
-              "| factor | kernel bytes/dispatch |", "|---|---|---|---|---|---|---|"]
+              "| counter | kernel KiB/dispatch (mean) | dispatches | reference | factor "
+              "| kernel bytes/dispatch |", "|---|---|---|---|---|---|"]
     for d in (pf_dir, pw_dir):
         counter, per = _counter_means(d)
         vals = [v for k, vs in per.items() if kernel in k for v in vs]
         if not vals:
             raise ValueError("kernel %r not in %s" % (kernel, d))
-        counted = _copy_dispatch(per, counter, copy_kib)
-        factor = copy_kib / counted
+        facs = _factors(per, counter, copy_kib, stream_kib)
+        if not facs:
+            raise ValueError("no calibration dispatch found for %s" % counter)
+        for name, (c, known, fac) in facs.items():
+            cal.append("| %s | `%s` | %.1f | %.0f | %.4f |" % (counter, name, c, known, fac))
+        ref = NT_PROBE if NT_PROBE in facs else COPY
+        factor = facs[ref][2]
         kib = statistics.mean(vals)
         b = kib * 1024.0 * factor
         total += b
-        lines.append("| %s | %.1f | %d | %.1f | %.0f | %.4f | %.0f |" % (
-            counter, kib, len(vals), counted, copy_kib, factor, b))
+        lines.append("| %s | %.1f | %d | `%s` | %.4f | %.0f |" % (counter, kib, len(vals), ref, factor, b))
+    lines += cal
+    for title, body in (extra or []):
+        lines += ["", "## " + title, ""] + list(body)
     lines += ["", "traffic_bytes_per_launch: %.0f" % total,
               "kernel_avg_us: %.3f" % (float(krow["AverageNs"]) / 1e3),
               "kernel: %s" % kernel,
@@ -116,6 +155,21 @@ def summarize(kt_dir, pf_dir, pw_dir, kernel, copy_mib, out_md, commands):
     with open(out_md, "w") as fh:
         fh.write("\n".join(lines))
     return total
+
+
+def counter_table(pmc_dir, kernels):
+    """Markdown rows of every counter of one --pmc run, mean per dispatch, for
+    each kernel whose name contains one of `kernels`."""
+    rows = list(csv.DictReader(open(_one(os.path.join(pmc_dir, "*counter_collection.csv")))))
+    acc = {}
+    for r in rows:
+        for kn in kernels:
+            if kn in r["Kernel_Name"]:
+                acc.setdefault((kn, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
+    out = ["| kernel | counter | mean per dispatch | dispatches |", "|---|---|---|---|"]
+    for (kn, cn), vs in sorted(acc.items()):
+        out.append("| `%s` | %s | %.6g | %d |" % (kn, cn, statistics.mean(vs), len(vs)))
+    return out
 
 
 def read_traffic(profile_md, kernel):
@@ -141,5 +195,8 @@ if __name__ == "__main__":
     if len(a) < 7:
         print(__doc__)
         sys.exit(2)
-    t = summarize(a[0], a[1], a[2], a[3], int(a[4]), a[5], a[6:])
+    stream = 0
+    if a[0].startswith("--stream-mib="):
+        stream = int(a.pop(0).split("=", 1)[1])
+    t = summarize(a[0], a[1], a[2], a[3], int(a[4]), a[5], a[6:], stream_mib=stream)
     print("traffic bytes per launch: %.0f" % t)

@@ -378,3 +378,17 @@ def test_moe_validation(q, lib):
     assert fm(big, 41) == SHAPE
     odd = _stack_arr(q, _mlp(q), _mlp(q, d=320, f=448))
     assert fm(odd, 2, k=1) == SHAPE
+
+
+def test_stream_probe_validation(lib):
+    P = ctypes.c_void_p
+    f = lib.qmlp_probe_stream_read
+    assert f(None, 1 << 20, P(FAKE), 256, 1, None) == NULL
+    assert f(P(FAKE), 1 << 20, None, 256, 1, None) == NULL
+    assert f(P(FAKE), 0, P(FAKE), 256, 1, None) == SHAPE
+    assert f(P(FAKE), (1 << 20) + 8, P(FAKE), 256, 1, None) == SHAPE      # not whole 16-byte units
+    assert f(P(FAKE), 1 << 20, P(FAKE), 0, 1, None) == SHAPE
+    assert f(P(FAKE), 1 << 20, P(FAKE), 65537, 0, None) == SHAPE
+    assert f(P(FAKE + 8), 1 << 20, P(FAKE), 256, 1, None) == ALIGN
+    assert f(P(FAKE), 1 << 20, P(FAKE + 2), 256, 1, None) == ALIGN
+
