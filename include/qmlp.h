@@ -192,6 +192,28 @@ qmlp_status qmlp_forward(const qmlp_mlp *mlp, const void *x, int M, qmlp_dtype d
                          void *y, void *ws, size_t ws_bytes, qmlp_stream stream);
 
 /*
+ * qmlp_forward without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The block's workspace is a fixed array
+ * of qmlp_noalloc_scratch_bytes() (1 MiB) in this library's device memory,
+ * one per GPU, held until the process ends; the call allocates and frees
+ * nothing.  Binary16 decode only (1 <= M <= 16): QMLP_ERR_UNSUPPORTED for
+ * bfloat16, QMLP_ERR_WORKSPACE when qmlp_workspace_bytes(mlp, M, dtype)
+ * exceeds the array (the Qwen3-4B, Qwen3-8B and 14B-class blocks fit up to
+ * M = 16; d = 8192, f = 32768 fits up to M = 7).  Each call first clears the part of the array
+ * the block uses (one small fill kernel, then the kernels of qmlp_forward,
+ * on `stream`), so it never depends on an earlier call's contents.  All
+ * calls on one GPU share its array: calls that overlap in time on the same
+ * GPU (other streams, other host threads) race.  Other errors as for
+ * qmlp_forward; on any error nothing is enqueued.
+ */
+qmlp_status qmlp_forward_noalloc(const qmlp_mlp *mlp, const void *x, int M, qmlp_dtype dtype,
+                                 void *y, qmlp_stream stream);
+
+/* Size of the per-GPU array behind qmlp_forward_noalloc.  Host-only. */
+size_t qmlp_noalloc_scratch_bytes(void);
+
+/*
  * A stack of L blocks of one shape on a residual stream, as the MLP
  * sub-blocks of an L-layer decoder with the attention sub-blocks left out
  * (Sec. 3.3: each layer carries one gated MLP):

@@ -88,6 +88,8 @@ def _lib():
             "qmlp_forward_batch": (I, [pm, I, P, I, I, P, P, Z, P]),
             "qmlp_status_string": (ctypes.c_char_p, [I]),
             "qmlp_probe_stream_read": (I, [P, Z, P, I, I, P]),
+            "qmlp_forward_noalloc": (I, [pm, P, I, I, P, P]),
+            "qmlp_noalloc_scratch_bytes": (Z, []),
         }
         for name, (res, args) in sig.items():
             fn = getattr(lib, name)
@@ -270,6 +272,22 @@ def forward(mlp: MLP, x: torch.Tensor, y: torch.Tensor | None = None,
     _check(_lib().qmlp_forward(ctypes.byref(mlp.c()), _ptr(x), M, _dtype_code(x), _ptr(y),
                                _ptr(ws), ws.numel(), _stream()), "forward")
     return y
+
+
+def forward_noalloc(mlp: MLP, x: torch.Tensor, y: torch.Tensor | None = None) -> torch.Tensor:
+    """The whole block x -> y with the library's own per-GPU scratch array as
+    workspace (qmlp_forward_noalloc): nothing is allocated by the call."""
+    M = x.shape[0]
+    if y is None:
+        y = torch.empty((M, mlp.d), dtype=x.dtype, device=x.device)
+    c = mlp.c()
+    _check(_lib().qmlp_forward_noalloc(ctypes.byref(c), _ptr(x), M, _dtype_code(x), _ptr(y), _stream()),
+           "qmlp_forward_noalloc")
+    return y
+
+
+def noalloc_scratch_bytes() -> int:
+    return int(_lib().qmlp_noalloc_scratch_bytes())
 
 
 def unpack(w: QWeight):

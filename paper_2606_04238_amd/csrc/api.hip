@@ -357,6 +357,24 @@ qmlp_status run_layers_batched(const qmlp_mlp* layers, int L, const char* xb, in
 
 }  // namespace
 
+namespace qmlp {
+
+// Everything qmlp_forward checks before it looks at the workspace.
+qmlp_status forward_check(const qmlp_mlp* mlp, const void* x, int M, qmlp_dtype dtype, const void* y) {
+    qmlp_status s = check_mlp(mlp, M, dtype);
+    if (s != QMLP_OK)
+        return s;
+    if (M == 0)
+        return QMLP_OK;
+    if (!x || !y)
+        return QMLP_ERR_NULL;
+    if (!aligned16(x) || !aligned16(y))
+        return QMLP_ERR_ALIGN;
+    return QMLP_OK;
+}
+
+}  // namespace qmlp
+
 extern "C" {
 
 size_t qmlp_codes_bytes(int bits, int n_out, int k_in) {
@@ -450,15 +468,9 @@ qmlp_status qmlp_down_w4(const qmlp_qweight* down, const void* h, int M, qmlp_dt
 
 qmlp_status qmlp_forward(const qmlp_mlp* mlp, const void* x, int M, qmlp_dtype dtype, void* y,
                          void* ws, size_t ws_bytes, qmlp_stream stream) {
-    qmlp_status s = check_mlp(mlp, M, dtype);
-    if (s != QMLP_OK)
+    qmlp_status s = qmlp::forward_check(mlp, x, M, dtype, y);
+    if (s != QMLP_OK || M == 0)
         return s;
-    if (M == 0)
-        return QMLP_OK;
-    if (!x || !y)
-        return QMLP_ERR_NULL;
-    if (!aligned16(x) || !aligned16(y))
-        return QMLP_ERR_ALIGN;
     if (!ws || ws_bytes < qmlp_workspace_bytes(mlp, M, dtype))
         return QMLP_ERR_WORKSPACE;
     if (!aligned16(ws))

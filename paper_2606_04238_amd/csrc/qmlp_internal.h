@@ -5,7 +5,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "qmlp.h"
+
 namespace qmlp {
+
+// The argument checks of qmlp_forward that precede its workspace checks
+// (descriptor, M, dtype, x and y); QMLP_OK for M == 0.
+qmlp_status forward_check(const qmlp_mlp* mlp, const void* x, int M, qmlp_dtype dtype, const void* y);
 
 // Codes per unit of a row's code stream: 32 at 4 bits and 64 at 2 bits (one
 // 16-byte load); at 3 bits 64 (16 bytes of the 2-bit plane and 8 bytes of

@@ -392,3 +392,22 @@ def test_stream_probe_validation(lib):
     assert f(P(FAKE + 8), 1 << 20, P(FAKE), 256, 1, None) == ALIGN
     assert f(P(FAKE), 1 << 20, P(FAKE + 2), 256, 1, None) == ALIGN
 
+
+def test_noalloc_validation(q, lib):
+    """The no-allocation entry checks as qmlp_forward does, then rejects
+    blocks whose workspace exceeds its array, before any HIP call."""
+    assert lib.qmlp_noalloc_scratch_bytes() == 1 << 20
+    m = _mlp(q)
+    P = ctypes.c_void_p
+    f = lib.qmlp_forward_noalloc
+    assert f(None, P(FAKE), 1, 0, P(FAKE), None) == NULL
+    assert f(ctypes.byref(m), None, 1, 0, P(FAKE), None) == NULL
+    assert f(ctypes.byref(m), P(FAKE + 4), 1, 0, P(FAKE), None) == ALIGN
+    assert f(ctypes.byref(m), P(FAKE), 0, 0, P(FAKE), None) == OK           # M = 0: nothing to do
+    assert f(ctypes.byref(m), P(FAKE), 17, 0, P(FAKE), None) != OK
+    big = q.MlpC(_qw(q, 2, 32768, 8192, 128), _qw(q, 2, 32768, 8192, 128), _qw(q, 4, 8192, 32768, 128),
+                 FAKE, FAKE, FAKE, FAKE, 32, 1.0)
+    assert lib.qmlp_workspace_bytes(ctypes.byref(big), 7, 0) <= 1 << 20
+    assert lib.qmlp_workspace_bytes(ctypes.byref(big), 8, 0) > 1 << 20
+    assert f(ctypes.byref(big), P(FAKE), 8, 0, P(FAKE), None) == WS
+    assert f(ctypes.byref(big), P(FAKE), 8, 1, P(FAKE), None) == UNSUP     # bfloat16
