@@ -5,18 +5,20 @@ A step is one pass over the 36 independently seeded MLP blocks of the
 Qwen3-4B-shaped workload (d=2560, f=9728, 2-bit gate/up and 4-bit down at
 group 128, LoRA rank 16, M=1 token, every block with its own weights and
 its own input x ~ N(0,1) in binary16), run back to back through
-qmlp_forward_layers (one persistent launch at this shape).  Inputs are
+qmlp_forward_layers (three streamed launches at this shape).  Inputs are
 packed and resident in HBM before the timed region.  Prints one JSON line:
 
   value    = achieved HBM GB/s = L * B(M) / t_step, where B(M) are the
              algorithmic bytes of one MLP step (packed codes + fp16
              scale/zero + LoRA factors + x in + y out; the intermediate h
              excluded, as the fused gate-activation-down keeps it on-chip);
-  roofline = the dominant kernel's algorithmic bytes per launch over its
-             average launch duration (HIP events on the launch stream over
-             the timed region); traffic = HBM bytes per launch from the
-             rocprofv3 byte counters summarized under profiles/, reported
-             only while the HIP sources match the ones profiled;
+  roofline = the step's algorithmic bytes over its duration (HIP events
+             on the launch stream around the K back-to-back steps; a step is
+             one qmlp_forward_layers call: the LoRA-A launch, then the
+             gate/up and down launches over every block); traffic = HBM bytes
+             of those launches from the rocprofv3 byte counters summarized
+             under profiles/, reported only while the HIP sources match the
+             ones profiled;
   cpu_baseline = the fp64 oracle timed on a bounded sample of the same
              blocks on this host (reported baseline only).
 
@@ -60,6 +62,8 @@ import workloads as wl  # noqa: E402
 from paper_2606_04238_amd.profiling import read_traffic  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
+# the launches of one streamed step, as named in the kernel trace
+STEP_KERNELS = "lora_a_kernel|gu_stream_kernel|dn_stream_kernel"
 METRIC = BASE_METRIC = ("achieved HBM GB/s (% of MI355X peak) and µs per W4/W2-GateUp MLP "
                         "decode step")
 
@@ -195,8 +199,8 @@ def precision_comparison(stack: Stack, seed: int, steps: int, min_warm_s: float,
     """us per MLP step of each width variant (graph replay of one pass over
     the blocks), its achieved GB/s, the oracle parity of block 0 and block
     L-1, and the MLP-level Gain / Capture of the two W4/W2-GateUp variants;
-    beside them the Gain of the persistent W4/W2-GateUp launch (mix_us) over
-    uniform W4 on the batched kernels."""
+    beside them the Gain of the streamed W4/W2-GateUp path (mix_us, the
+    headline) over uniform W4 on the batched kernels."""
     import torch
     import oracle as orc
     import paper_2606_04238_amd as q
@@ -243,7 +247,7 @@ def precision_comparison(stack: Stack, seed: int, steps: int, min_warm_s: float,
             # the same two figures if every variant moved its bytes at one bandwidth
             "bytes_model_gain_pct": round((b4 / bm - 1) * 100, 1),
             "bytes_model_capture_pct": round((1 / bm - 1 / b4) / (1 / b2 - 1 / b4) * 100, 1)}
-    out["persistent_w4w2_gateup_lora"] = {
+    out["streamed_w4w2_gateup_lora"] = {
         "us_per_mlp_step": round(mix_us, 3),
         "gain_pct_over_batched_w4": round((t4 / mix_us - 1) * 100, 1),
         "capture_pct_batched_w2_w4": round((1 / mix_us - 1 / t4) / (1 / t2 - 1 / t4) * 100, 1)}
@@ -395,6 +399,30 @@ def time_passes(fn, steps: int, warmup: int, min_warm_s: float = 0.25):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     return [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)], wall
+
+
+def time_block(fn, steps: int, warmup: int, min_warm_s: float = 0.25):
+    """Milliseconds per pass over `steps` passes launched back to back, with
+    one event before the first and one after the last (after the same warmup
+    as time_passes): nothing else is enqueued between the passes, so the
+    figure holds only the GPU's own gaps between them."""
+    import torch
+    t_end = time.perf_counter() + min_warm_s
+    done = 0
+    while done < warmup or time.perf_counter() < t_end:
+        fn()
+        done += 1
+        if done % 8 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(steps):
+        fn()
+    e1.record(st)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
 
 
 # --------------------------------------------------------------------- cpu baseline
@@ -744,24 +772,23 @@ def main(argv=None):
     B = cfg.alg_bytes()
     dt = stack.Y.dtype
     launches = q.layers_launches(stack.lay, cfg.M, dt)
-    chunks = (L + 39) // 40
-    persistent = launches == chunks                     # one persistent launch per 40 blocks
-    batched = not persistent and launches == chunks * (3 if cfg.r else 2)
+    path = q.layers_path(stack.lay, cfg.M, dt)
 
     # the timed step: every block on its own input, back to back
     # timed in both launch modes; `value` is the one --mode names, the other is
     # reported beside it
-    eager_ms, _ = time_passes(lambda: run_blocks_once(stack), args.steps, args.warmup, args.min_warm_s)
+    # the K timed steps back to back, bracketed by two events and a
+    # synchronize on both sides; per-step events (a second pass) give the
+    # spread of single steps
+    eager_step = time_block(lambda: run_blocks_once(stack), args.steps, args.warmup, args.min_warm_s)
+    eager_ms, _ = time_passes(lambda: run_blocks_once(stack), args.steps, 1, 0.0)
     g = capture(lambda: run_blocks_once(stack))
-    graph_ms, wall = time_passes(g.replay, args.steps, args.warmup, args.min_warm_s)
+    graph_step = time_block(g.replay, args.steps, args.warmup, args.min_warm_s)
+    graph_ms, wall = time_passes(g.replay, args.steps, 1, 0.0)
     head = graph_ms if args.mode == "graph" else eager_ms
-    t_step = sum(head) / len(head)          # the K timed steps, back to back
+    t_step = graph_step if args.mode == "graph" else eager_step
     gbs = L * B / (t_step * 1e-3) / 1e9
     us_layer = t_step * 1e3 / L
-    if persistent:
-        err_bits = q.layers_errors(stack.lws)
-        if err_bits:
-            raise RuntimeError("layers kernel reported error bits %#x" % err_bits)
     err = parity_blocks(stack, args.seed, sample=(0, L // 2, L - 1))
 
     # context: the same blocks as a decoder stack on the residual stream, and
@@ -791,26 +818,17 @@ def main(argv=None):
                 stack, args.seed, max(5, args.steps // 2), args.min_warm_s,
                 context["precision_comparison"]["mlp_us"])
 
-    traffic = None
-    if persistent:
-        # the timed region holds K steps of `launches` back-to-back launches
-        # of the layers kernel on the replay stream, so its events give the
-        # average launch duration (inter-launch gaps included)
-        dom_name = "layers_kernel"
-        dom_us = t_step * 1e3 / launches
-        dom_b = L * B / launches
-        kernel_us = {"layers_kernel_avg_launch": round(dom_us, 3), "launches_per_step": launches}
-        traffic = read_traffic(os.path.join(ROOT, "profiles", "layers_kernel_%s.md" % cfg.name),
-                               dom_name)
-    elif batched:
-        # the batched path's launches (LoRA-A, gate/up, down of up to 40
-        # blocks each) are internal to one call: the step is the unit timed
-        # here, the per-kernel split comes from the kernel trace
-        dom_name = "batched step (LoRA-A, gate/up and down launches of qmlp_forward_batch)"
-        dom_us, dom_b = t_step * 1e3, L * B
-        kernel_us = {"batched_step": round(dom_us, 3), "launches_per_step": launches}
-    else:
-        raise RuntimeError("binary16 decode runs persistently or batched; got %d launches" % launches)
+    # The step (one qmlp_forward_layers call) is the unit: its launches --
+    # LoRA-A, then gate/up and down over every block of a batch of up to 40 --
+    # are internal to the call, so the timed region's events give the step;
+    # the per-kernel split is in the committed kernel trace.
+    if path not in ("streamed", "batched"):
+        raise RuntimeError("binary16 decode streams or runs batched; got path %s" % path)
+    dom_name = ("%s step (LoRA-A, gate/up and down launches of qmlp_forward_layers)" % path)
+    dom_us, dom_b = t_step * 1e3, L * B
+    kernel_us = {"step": round(dom_us, 3), "launches_per_step": launches}
+    traffic = read_traffic(os.path.join(ROOT, "profiles", "layers_%s_%s.md" % (path, cfg.name)),
+                           STEP_KERNELS) if path == "streamed" else None
     achieved = dom_b / (dom_us * 1e-6) / 1e9
 
     out = {
@@ -834,11 +852,11 @@ def main(argv=None):
             "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
             "alg_bytes_per_mlp_step": B,
             "mode": "hip_graph" if args.mode == "graph" else "eager",
-            "path": "persistent layers kernel" if persistent else
-                    "batched stand-alone kernels" if batched else "per-block forward",
-            "eager_us_per_mlp_step": round(sum(eager_ms) / len(eager_ms) * 1e3 / L, 3),
-            "graph_us_per_mlp_step": round(sum(graph_ms) / len(graph_ms) * 1e3 / L, 3),
-            "median_ms_per_step": round(statistics.median(head), 4),
+            "path": {"streamed": "streamed launches (LoRA-A, gate/up, down over every block)",
+                     "batched": "batched stand-alone kernels"}[path],
+            "eager_us_per_mlp_step": round(eager_step * 1e3 / L, 3),
+            "graph_us_per_mlp_step": round(graph_step * 1e3 / L, 3),
+            "median_ms_per_step_with_per_step_events": round(statistics.median(head), 4),
             "p10_p90_ms_per_step": [round(float(np.percentile(head, 10)), 4),
                                     round(float(np.percentile(head, 90)), 4)],
             "kernel_us": kernel_us,

@@ -262,21 +262,20 @@ int qmlp_stack_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
  * rank); x [L][M][d] and y [L][M][d] are row-major in the activation type
  * (block l at x + l*M*d, y + l*M*d).
  *
- * At M = 1 in binary16 for shapes with f % 256 == 0, d % 512 == 0,
- * d <= 4096, (d/g) % 4 == 0 and the instances of the persistent stack on a
- * GPU with 8 XCDs of 32 compute units, the blocks run as ONE persistent
- * launch per 40 blocks, pipelined: the gate/up rows of block i, the down
- * rows of block i-2 and the output sum of block i-3 run together, so the
- * hand-offs inside a block overlap the weight stream of the next.  Every
- * other binary16 shape runs as qmlp_forward_batch does; bfloat16 runs
+ * Binary16 blocks run in batches of up to 40.  At M = 1 in the
+ * W4/W2-GateUp form (2-bit gate/up, 4-bit down, groups 64/128, rank 0, 8,
+ * 16 or 32) with d % 512 == 0, d <= 4096, f % 128 == 0, f <= 12288, a batch
+ * STREAMS: the LoRA-A products of every block (one launch), then one
+ * persistent gate/up launch and one persistent down launch, each workgroup
+ * owning a contiguous range of the batch's rows flattened over blocks, so
+ * no workgroup waits for another and h of every block passes through the
+ * workspace between the two launches.  Every other binary16 batch runs the
+ * stand-alone kernels as qmlp_forward_batch does; bfloat16 runs
  * qmlp_forward once per block.
  *
- * ws/ws_bytes: at least qmlp_layers_workspace_bytes(layers, L, M, dtype),
- * zero before the first call, with the rules of qmlp_workspace_bytes.  On
- * the persistent path it starts with a 1024-byte control block: word 0 the
- * step counter, word 64 sticky error bits (1/2/4 = a wait for the LoRA-A
- * products / h / the cross-XCD partials gave up, 8 = a workgroup found no
- * place); results are then invalid.  Errors as for qmlp_forward.
+ * ws/ws_bytes: at least qmlp_layers_workspace_bytes(layers, L, M, dtype)
+ * (binary16: that of qmlp_forward_batch).  No state is kept between calls.
+ * Errors as for qmlp_forward.
  */
 size_t qmlp_layers_workspace_bytes(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
 
@@ -284,10 +283,14 @@ qmlp_status qmlp_forward_layers(const qmlp_mlp *layers, int L, const void *x, in
                                 qmlp_dtype dtype, void *y, void *ws, size_t ws_bytes,
                                 qmlp_stream stream);
 
-/* Launches qmlp_forward_layers makes: the number of persistent launches, the
- * launches of the batched path (3 per 40 blocks, 2 without adapters), or
- * the per-block launches of qmlp_forward; 0 if the call would be rejected.
- * Host-only. */
+/* Which path qmlp_forward_layers takes for these blocks: 1 = streamed, 2 =
+ * the batched stand-alone kernels, 3 = qmlp_forward per block (bfloat16);
+ * 0 if the call would be rejected.  Host-only. */
+int qmlp_layers_path(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
+
+/* Launches qmlp_forward_layers makes: 3 per batch of up to 40 blocks (2
+ * without adapters) on the streamed and batched paths, or the per-block
+ * launches of qmlp_forward; 0 if the call would be rejected.  Host-only. */
 int qmlp_layers_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
 
 /*

@@ -89,6 +89,7 @@ def _lib():
             "qmlp_status_string": (ctypes.c_char_p, [I]),
             "qmlp_probe_stream_read": (I, [P, Z, P, I, I, P]),
             "qmlp_forward_noalloc": (I, [pm, P, I, I, P, P]),
+            "qmlp_layers_path": (I, [pm, I, I, I]),
             "qmlp_noalloc_scratch_bytes": (Z, []),
         }
         for name, (res, args) in sig.items():
@@ -335,9 +336,18 @@ def layers_workspace_bytes(layers: Layers, M: int, dtype=torch.float16) -> int:
     return int(_lib().qmlp_layers_workspace_bytes(layers.c(), len(layers), M, code))
 
 
+LAYERS_PATHS = {0: "rejected", 1: "streamed", 2: "batched", 3: "per-block"}
+
+
+def layers_path(layers: Layers, M: int, dtype=torch.float16) -> str:
+    """The path qmlp_forward_layers takes (qmlp_layers_path)."""
+    code = F16 if dtype == torch.float16 else BF16
+    return LAYERS_PATHS[int(_lib().qmlp_layers_path(layers.c(), len(layers), M, code))]
+
+
 def layers_launches(layers: Layers, M: int, dtype=torch.float16) -> int:
-    """Launches forward_layers makes (persistent launches, the batched path's
-    launches, or one forward per block)."""
+    """Launches forward_layers makes (three per batch of up to 40 blocks on
+    the streamed and batched paths, or those of one forward per block)."""
     code = F16 if dtype == torch.float16 else BF16
     return int(_lib().qmlp_layers_launches(layers.c(), len(layers), M, code))
 
@@ -346,13 +356,6 @@ def layers_workspace(layers: Layers, M: int, dtype=torch.float16, device="cuda")
     """A zeroed workspace for forward_layers."""
     n = layers_workspace_bytes(layers, M, dtype)
     return torch.zeros(max(n, 1024), dtype=torch.uint8, device=device)
-
-
-def layers_errors(ws: torch.Tensor) -> int:
-    """Sticky error bits of the persistent launch of forward_layers (syncs): 1/2/4 =
-    a wait for the LoRA-A products / h / the cross-XCD partials gave up, 8 = a
-    workgroup had no place."""
-    return int(ws[256:260].view(torch.int32).item())
 
 
 def forward_layers(layers: Layers, x: torch.Tensor, y: torch.Tensor | None = None,

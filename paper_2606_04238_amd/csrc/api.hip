@@ -299,19 +299,28 @@ StackLayerDesc stack_desc(const qmlp_mlp& m) {
     return s;
 }
 
-bool layers_persistent(const qmlp_mlp* layers, int M, qmlp_dtype dtype) {
+// Independent blocks at one token in the W4/W2-GateUp form stream: every
+// batch of up to kBatchMax blocks is the LoRA-A launch, one persistent
+// gate/up launch and one persistent down launch (decode_stream.hip).
+bool layers_streamed(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
     const qmlp_mlp& a = layers[0];
-    return dtype == QMLP_F16 && standard_mlp(&a) && a.down.group == a.gate.group &&
-           layers_supported(M, a.gate.k_in, a.gate.n_out, a.gate.group, a.rank);
+    if (dtype != QMLP_F16 || !standard_mlp(&a))
+        return false;
+    const int full = L / kBatchMax, rest = L % kBatchMax;
+    const auto ok = [&](int nb) {
+        return stream_supported(M, a.gate.k_in, a.gate.n_out, a.gate.group, a.gate.bits, a.down.group,
+                                a.down.bits, a.rank, nb);
+    };
+    return (full == 0 || ok(kBatchMax)) && (rest == 0 || ok(rest));
 }
 
-// Independent blocks that do not take the persistent launch run in batches
-// of up to kBatchMax blocks on the stand-alone kernels: LoRA-A of every
-// block of the batch, then gate/up of every block, then down of every block
-// (three launches per batch, two without adapters).  Binary16 decode only;
-// bfloat16 runs qmlp_forward per block.
-bool layers_batched(const qmlp_mlp* layers, int M, qmlp_dtype dtype) {
-    return dtype == QMLP_F16 && !layers_persistent(layers, M, dtype);
+// Independent blocks that do not stream run in batches of up to kBatchMax
+// blocks on the stand-alone kernels: LoRA-A of every block of the batch,
+// then gate/up of every block, then down of every block (three launches per
+// batch, two without adapters).  Binary16 decode only; bfloat16 runs
+// qmlp_forward per block.
+bool layers_batched(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    return dtype == QMLP_F16 && !layers_streamed(layers, L, M, dtype);
 }
 
 size_t batch_t_bytes(const qmlp_mlp* a, int nb, int M) {
@@ -323,7 +332,7 @@ size_t batch_h_bytes(const qmlp_mlp* a, int nb, int M) {
 int batch_size(int L) { return L < kBatchMax ? L : kBatchMax; }
 
 qmlp_status run_layers_batched(const qmlp_mlp* layers, int L, const char* xb, int M, char* yb,
-                               void* ws, hipStream_t st) {
+                               void* ws, hipStream_t st, bool streamed = false) {
     const qmlp_mlp& a = layers[0];
     const int d = a.gate.k_in;
     const size_t step = (size_t)M * d * 2;
@@ -346,9 +355,9 @@ qmlp_status run_layers_batched(const qmlp_mlp* layers, int L, const char* xb, in
         b.y = reinterpret_cast<uint16_t*>(yb + l0 * step);
         hipError_t e = b.r > 0 ? launch_lora_a_batch(b, n, st) : hipSuccess;
         if (e == hipSuccess)
-            e = launch_gateup_batch(b, n, st);
+            e = streamed ? launch_gateup_stream(b, n, st) : launch_gateup_batch(b, n, st);
         if (e == hipSuccess)
-            e = launch_down_batch(b, n, st);
+            e = streamed ? launch_down_stream(b, n, st) : launch_down_batch(b, n, st);
         if (e != hipSuccess)
             return QMLP_ERR_HIP;
     }
@@ -617,19 +626,25 @@ qmlp_status qmlp_forward_stack(const qmlp_mlp* layers, int L, const void* x, int
 size_t qmlp_layers_workspace_bytes(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
     if (check_layers(layers, L, M, dtype) != QMLP_OK || M == 0)
         return 0;
-    if (layers_persistent(layers, M, dtype))
-        return layers_ws_bytes(layers[0].gate.k_in, layers[0].gate.n_out, layers[0].rank);
-    if (layers_batched(layers, M, dtype))
+    if (dtype == QMLP_F16)              // streamed or batched
         return qmlp_batch_workspace_bytes(layers, L, M, dtype);
     return qmlp_workspace_bytes(&layers[0], M, dtype);
+}
+
+int qmlp_layers_path(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    if (check_layers(layers, L, M, dtype) != QMLP_OK || M == 0)
+        return 0;
+    if (layers_streamed(layers, L, M, dtype))
+        return 1;
+    if (layers_batched(layers, L, M, dtype))
+        return 2;
+    return 3;
 }
 
 int qmlp_layers_launches(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
     if (check_layers(layers, L, M, dtype) != QMLP_OK || M == 0)
         return 0;
-    if (layers_persistent(layers, M, dtype))
-        return (L + layers_max_layers() - 1) / layers_max_layers();
-    if (layers_batched(layers, M, dtype))
+    if (dtype == QMLP_F16)              // streamed or batched: three launches per batch
         return (L + kBatchMax - 1) / kBatchMax * (layers[0].rank > 0 ? 3 : 2);
     int n = 0;
     for (int i = 0; i < L; ++i) n += qmlp_forward_launches(&layers[i], M, dtype);
@@ -656,22 +671,8 @@ qmlp_status qmlp_forward_layers(const qmlp_mlp* layers, int L, const void* x, in
     const char* xb = static_cast<const char*>(x);
     char* yb = static_cast<char*>(y);
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if (layers_persistent(layers, M, dtype)) {
-        StackLayerDesc desc[64];
-        const int per = layers_max_layers();
-        for (int l0 = 0; l0 < L; l0 += per) {
-            const int n = L - l0 < per ? L - l0 : per;
-            for (int i = 0; i < n; ++i) desc[i] = stack_desc(layers[l0 + i]);
-            hipError_t e = launch_layers(desc, n, d, layers[0].gate.n_out, layers[0].gate.group, layers[0].rank,
-                                         reinterpret_cast<const uint16_t*>(xb + l0 * step),
-                                         reinterpret_cast<uint16_t*>(yb + l0 * step), ws, st);
-            if (e != hipSuccess)
-                return QMLP_ERR_HIP;
-        }
-        return QMLP_OK;
-    }
-    if (layers_batched(layers, M, dtype))
-        return run_layers_batched(layers, L, xb, M, yb, ws, st);
+    if (dtype == QMLP_F16)
+        return run_layers_batched(layers, L, xb, M, yb, ws, st, layers_streamed(layers, L, M, dtype));
     for (int i = 0; i < L; ++i) {
         s = qmlp_forward(&layers[i], xb + i * step, M, dtype, yb + i * step, ws, ws_bytes, stream);
         if (s != QMLP_OK)

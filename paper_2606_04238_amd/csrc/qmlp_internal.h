@@ -118,6 +118,14 @@ struct BatchArgs {
     int xdiv;
 };
 hipError_t launch_lora_a_batch(const BatchArgs& b, int nb, hipStream_t st);
+// The streamed path of a batch at one token (decode_stream.hip): one
+// persistent gate/up launch and one persistent down launch over all blocks of
+// the batch, after launch_lora_a_batch.  Binary16, 2-bit gate/up and 4-bit
+// down at groups 64/128, rank 0/8/16/32, d % 512 == 0, d <= 4096,
+// f % 128 == 0, f <= 12288 (plus the LDS and span limits it checks).
+bool stream_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r, int nb);
+hipError_t launch_gateup_stream(const BatchArgs& b, int nb, hipStream_t st);
+hipError_t launch_down_stream(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_gateup_batch(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_down_batch(const BatchArgs& b, int nb, hipStream_t st);
 // y[m] = sum_j w[m k + j] * yi[m k + j] over the k routed experts of token m
@@ -131,14 +139,5 @@ hipError_t launch_stack(const StackLayerDesc* layers, int L, int d, int f, int g
 hipError_t launch_residual(const uint16_t* x, const uint16_t* y, uint16_t* out, int n, bool bf16,
                            hipStream_t st);
 hipError_t launch_rmsnorm(const uint16_t* x, uint16_t* u, int M, int d, hipStream_t st);
-
-// decode_layers.hip: L independent blocks of one shape (M = 1, binary16) in one
-// persistent launch, block l on x[l] -> y[l].  ws: the layers area
-// (layers_ws_bytes, zero before the first call; 1024-byte control block first).
-bool layers_supported(int M, int d, int f, int g, int r);
-size_t layers_ws_bytes(int d, int f, int r);
-int layers_max_layers();
-hipError_t launch_layers(const StackLayerDesc* layers, int L, int d, int f, int g, int r, const uint16_t* x,
-                         uint16_t* y, void* ws, hipStream_t st);
 
 }  // namespace qmlp

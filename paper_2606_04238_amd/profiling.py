@@ -21,9 +21,12 @@ The summary records a digest of the HIP sources; ``read_traffic`` returns
 the traffic figure only while the sources still hash to that digest, so a
 figure taken on an older kernel is never reported for a newer one.
 
-Usage (on the CPU, after the three runs):
-    python3 -m paper_2606_04238_amd.profiling KT_DIR PF_DIR PW_DIR KERNEL_SUBSTR \
-        COPY_MIB OUT.md "COMMAND ..." ["COMMAND ..." ...]
+Usage (on the CPU, after the runs):
+    python3 -m paper_2606_04238_amd.profiling [--stream-mib=S] [--pmc-dir=DIR ...] \
+        KT_DIR PF_DIR PW_DIR KERNEL_SUBSTR[|KERNEL_SUBSTR...] COPY_MIB OUT.md \
+        "COMMAND ..." ["COMMAND ..." ...]
+Each --pmc-dir adds a table of every counter of that --pmc run for the
+kernels named.
 """
 from __future__ import annotations
 
@@ -107,10 +110,16 @@ def summarize(kt_dir, pf_dir, pw_dir, kernel, copy_mib, out_md, commands, stream
     """Write the summary; `extra` is a list of (title, markdown lines) that
     other counter passes contribute (they do not enter the traffic figure)."""
     stats = list(csv.DictReader(open(_one(os.path.join(kt_dir, "*kernel_stats.csv")))))
-    krow = [r for r in stats if kernel in r["Name"]]
-    if len(krow) != 1:
-        raise ValueError("kernel %r matches %d rows of the stats" % (kernel, len(krow)))
-    krow = krow[0]
+    # `kernel` may name several launches of one step, joined by "|": the
+    # step's duration and bytes are the sums of their per-dispatch means
+    parts = kernel.split("|")
+    krows = []
+    for part in parts:
+        rows = [r for r in stats if part in r["Name"]]
+        if len(rows) != 1:
+            raise ValueError("kernel %r matches %d rows of the stats" % (part, len(rows)))
+        krows.append(rows[0])
+    avg_us = sum(float(r["AverageNs"]) for r in krows) / 1e3
     copy_kib = copy_mib * 1024.0
     stream_kib = stream_mib * 1024.0
     lines = ["# %s -- rocprofv3 summary" % kernel, ""]
@@ -127,13 +136,18 @@ def summarize(kt_dir, pf_dir, pw_dir, kernel, copy_mib, out_md, commands, stream
     cal = ["", "## Calibration dispatches (known bytes / counted bytes)", "",
            "| counter | reference dispatch | counted KiB | known KiB | factor |", "|---|---|---|---|---|"]
     lines += ["", "## HBM byte counters (--pmc, one counter per run)", "",
-              "| counter | kernel KiB/dispatch (mean) | dispatches | reference | factor "
-              "| kernel bytes/dispatch |", "|---|---|---|---|---|---|"]
+              "| counter | KiB per step (sum of the kernels' means) | dispatches | reference | factor "
+              "| bytes per step |", "|---|---|---|---|---|---|"]
     for d in (pf_dir, pw_dir):
         counter, per = _counter_means(d)
-        vals = [v for k, vs in per.items() if kernel in k for v in vs]
-        if not vals:
-            raise ValueError("kernel %r not in %s" % (kernel, d))
+        kib = 0.0
+        nd = 0
+        for part in parts:
+            vals = [v for k, vs in per.items() if part in k for v in vs]
+            if not vals:
+                raise ValueError("kernel %r not in %s" % (part, d))
+            kib += statistics.mean(vals)
+            nd += len(vals)
         facs = _factors(per, counter, copy_kib, stream_kib)
         if not facs:
             raise ValueError("no calibration dispatch found for %s" % counter)
@@ -141,15 +155,14 @@ def summarize(kt_dir, pf_dir, pw_dir, kernel, copy_mib, out_md, commands, stream
             cal.append("| %s | `%s` | %.1f | %.0f | %.4f |" % (counter, name, c, known, fac))
         ref = NT_PROBE if NT_PROBE in facs else COPY
         factor = facs[ref][2]
-        kib = statistics.mean(vals)
         b = kib * 1024.0 * factor
         total += b
-        lines.append("| %s | %.1f | %d | `%s` | %.4f | %.0f |" % (counter, kib, len(vals), ref, factor, b))
+        lines.append("| %s | %.1f | %d | `%s` | %.4f | %.0f |" % (counter, kib, nd, ref, factor, b))
     lines += cal
     for title, body in (extra or []):
         lines += ["", "## " + title, ""] + list(body)
     lines += ["", "traffic_bytes_per_launch: %.0f" % total,
-              "kernel_avg_us: %.3f" % (float(krow["AverageNs"]) / 1e3),
+              "kernel_avg_us: %.3f" % avg_us,
               "kernel: %s" % kernel,
               "source_digest: %s" % source_digest(), ""]
     with open(out_md, "w") as fh:
@@ -192,11 +205,22 @@ def read_traffic(profile_md, kernel):
 
 if __name__ == "__main__":
     a = sys.argv[1:]
-    if len(a) < 7:
+    stream = 0
+    extra_dirs = []
+    rest = []
+    for v in a:
+        if v.startswith("--stream-mib="):
+            stream = int(v.split("=", 1)[1])
+        elif v.startswith("--pmc-dir="):
+            extra_dirs.append(v.split("=", 1)[1])
+        else:
+            rest.append(v)
+    if len(rest) < 7:
         print(__doc__)
         sys.exit(2)
-    stream = 0
-    if a[0].startswith("--stream-mib="):
-        stream = int(a.pop(0).split("=", 1)[1])
-    t = summarize(a[0], a[1], a[2], a[3], int(a[4]), a[5], a[6:], stream_mib=stream)
+    kern = rest[3]
+    extra = [("Counters (--pmc %s)" % os.path.basename(d.rstrip("/")), counter_table(d, kern.split("|")))
+             for d in extra_dirs]
+    t = summarize(rest[0], rest[1], rest[2], kern, int(rest[4]), rest[5], rest[6:], stream_mib=stream,
+                  extra=extra)
     print("traffic bytes per launch: %.0f" % t)

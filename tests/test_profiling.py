@@ -28,3 +28,40 @@ def test_read_traffic_stale_sources(tmp_path):
 def test_digest_is_stable():
     assert profiling.source_digest() == profiling.source_digest()
     assert len(profiling.source_digest()) == 16
+
+
+def _csv(path, header, rows):
+    import csv
+    with open(path, "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(header)
+        w.writerows(rows)
+
+
+def test_summary_sums_a_steps_kernels_and_uses_the_nontemporal_calibration(tmp_path):
+    """A step of two kernels: the duration and bytes are the sums of the
+    kernels' means; FETCH_SIZE is scaled by the non-temporal probe's factor
+    (known / counted), WRITE_SIZE by the copy's."""
+    kt, pf, pw = (tmp_path / n for n in ("kt", "pf", "pw"))
+    for d in (kt, pf, pw):
+        d.mkdir()
+    _csv(kt / "x_kernel_stats.csv", ["Name", "Calls", "AverageNs", "MinNs", "MaxNs", "Percentage"],
+         [["void a_kernel<1>()", 10, 1000.0, 900, 1100, 50], ["void b_kernel<2>()", 10, 3000.0, 2900, 3100, 50]])
+    hdr = ["Kernel_Name", "Counter_Name", "Counter_Value"]
+    _csv(pf / "x_counter_collection.csv", hdr,
+         [["void a_kernel<1>()", "FETCH_SIZE", 100.0], ["void b_kernel<2>()", "FETCH_SIZE", 300.0],
+          ["void a_kernel<1>()", "FETCH_SIZE", 100.0], ["void b_kernel<2>()", "FETCH_SIZE", 300.0],
+          ["void stream_read_kernel<true>(x)", "FETCH_SIZE", 512.0],
+          ["void stream_read_kernel<false>(x)", "FETCH_SIZE", 600.0],
+          ["void at::native::vectorized_elementwise_kernel<8>", "FETCH_SIZE", 64.0]])
+    _csv(pw / "x_counter_collection.csv", hdr,
+         [["void a_kernel<1>()", "WRITE_SIZE", 10.0], ["void b_kernel<2>()", "WRITE_SIZE", 20.0],
+          ["void at::native::vectorized_elementwise_kernel<8>", "WRITE_SIZE", 128.0]])
+    out = tmp_path / "s.md"
+    total = profiling.summarize(str(kt), str(pf), str(pw), "a_kernel|b_kernel", 128 / 1024, str(out),
+                                ["cmd"], stream_mib=1)
+    # fetch: (100 + 300) KiB * (1024 / 512); write: (10 + 20) KiB * (128 / 128)
+    assert total == (400 * 2 + 30) * 1024
+    text = out.read_text()
+    assert "kernel_avg_us: 4.000" in text and "kernel: a_kernel|b_kernel" in text
+    assert profiling.read_traffic(str(out), "a_kernel|b_kernel") == total
