@@ -69,9 +69,9 @@ struct Walk {
         l = item0 * rpi / per;
         n = item0 * rpi - l * per;
     }
-    __device__ __forceinline__ void next(int stride_rows, int per) {
+    __device__ __forceinline__ void next(int stride_rows, int per) {    // stride_rows < per
         n += stride_rows;
-        while (n >= per) {
+        if (n >= per) {
             n -= per;
             ++l;
         }
@@ -148,18 +148,26 @@ struct GuBuf {
 };
 
 // Loads of step c of the item whose first row is row n of block l (lane:
-// row n + lane/8).  Always issued, from valid addresses.
+// row n + lane/8).  Always issued, from valid addresses: a prefetch past a
+// wave's last step (dummy) reads the batch's x instead, which the staging
+// has just brought into the caches (every offset below stays inside the
+// first 2d bytes of x).
 template <int JC, int NCH, int R, int GSH>
-__device__ __forceinline__ void gu_load(GuBuf<JC>& q, int l, int n, int c, int lane) {
+__device__ __forceinline__ void gu_load(GuBuf<JC>& q, int l, int n, int c, bool dummy, const uint16_t* x,
+                                        int lane) {
     constexpr int UG = 8 * JC * NCH;
     constexpr int NG = UG >> GSH;                        // groups per row (64 << GSH codes each)
     KBatch* kb = kbatch();
-    const int row = n + (lane >> 3), s = lane & 7;
-    const uint4* cg = reinterpret_cast<const uint4*>(kb->lay[l].cg) + row * UG + s + 8 * JC * c;
-    const uint4* cu = reinterpret_cast<const uint4*>(kb->lay[l].cu) + row * UG + s + 8 * JC * c;
+    const int row = (dummy ? 0 : n) + (lane >> 3), s = lane & 7;
+    const void* pcg = dummy ? (const void*)x : (const void*)kb->lay[l].cg;
+    const void* pcu = dummy ? (const void*)x : (const void*)kb->lay[l].cu;
+    const void* pmg = dummy ? (const void*)x : (const void*)kb->lay[l].mg;
+    const void* pmu = dummy ? (const void*)x : (const void*)kb->lay[l].mu;
+    const uint4* cg = reinterpret_cast<const uint4*>(pcg) + row * UG + s + 8 * JC * c;
+    const uint4* cu = reinterpret_cast<const uint4*>(pcu) + row * UG + s + 8 * JC * c;
     // unit s + 8 i lies in group (s >> GSH) + (8 >> GSH) i
-    const uint32_t* mg = kb->lay[l].mg + row * NG + (s >> GSH) + (8 >> GSH) * JC * c;
-    const uint32_t* mu = kb->lay[l].mu + row * NG + (s >> GSH) + (8 >> GSH) * JC * c;
+    const uint32_t* mg = reinterpret_cast<const uint32_t*>(pmg) + row * NG + (s >> GSH) + (8 >> GSH) * JC * c;
+    const uint32_t* mu = reinterpret_cast<const uint32_t*>(pmu) + row * NG + (s >> GSH) + (8 >> GSH) * JC * c;
 #pragma unroll
     for (int j = 0; j < JC; ++j) {
         q.qg[j] = load_stream(cg + 8 * j);
@@ -167,8 +175,8 @@ __device__ __forceinline__ void gu_load(GuBuf<JC>& q, int l, int n, int c, int l
         q.mg[j] = load_stream(mg + (8 >> GSH) * j);
         q.mu[j] = load_stream(mu + (8 >> GSH) * j);
     }
-    const uint16_t* Bg = kb->lay[l].Bg;
-    const uint16_t* Bu = kb->lay[l].Bu;
+    const uint16_t* Bg = dummy ? x : kb->lay[l].Bg;
+    const uint16_t* Bu = dummy ? x : kb->lay[l].Bu;
     if constexpr (R == 8) {
         q.bg[0] = Bg[row * R + s];
         q.bu[0] = Bu[row * R + s];
@@ -226,10 +234,13 @@ __device__ __forceinline__ void gu_dot(GuBuf<JC>& q, const uint4* xl, const floa
     }
 }
 
-// LoRA-B, the row reduction over 8 lanes, SiLU(G) * U and the store of h.
+// LoRA-B, the row reduction over 8 lanes and SiLU(G) * U into the LDS copy
+// of the range's h (hs: this item's 8 values).  The loop stores nothing to
+// memory: a store counts in the same in-order counter as the loads, so a
+// store inside the loop makes the next prefetch wait for every earlier load.
 template <int JC, int R>
-__device__ __forceinline__ void gu_finish(GuBuf<JC>& q, const BatchArgs& b, const float* ts, int l, int n,
-                                          int lane, float G, float Uv) {
+__device__ __forceinline__ void gu_finish(GuBuf<JC>& q, const float* ts, int l, uint16_t* hs, int lane,
+                                          float G, float Uv) {
     const int s = lane & 7;
     if constexpr (R > 0) {
         constexpr int CPL = R / 8;               // ranks per lane
@@ -250,7 +261,7 @@ __device__ __forceinline__ void gu_finish(GuBuf<JC>& q, const BatchArgs& b, cons
     G = group_sum<8>(G);
     Uv = group_sum<8>(Uv);
     if (s == 0)
-        b.h[(long)l * b.f + n + (lane >> 3)] = (uint16_t)f2h(G / (1.0f + __expf(-G)) * Uv);
+        hs[lane >> 3] = (uint16_t)f2h(G / (1.0f + __expf(-G)) * Uv);
 }
 
 template <int JC, int NCH, int R, int GSH, int NW>
@@ -262,6 +273,7 @@ __global__ void __launch_bounds__(NW * 64) gu_stream_kernel(BatchArgs b, int nb,
     uint4* xs = smem;                                                   // [span][8][UG]
     float2* cx = reinterpret_cast<float2*>(smem + span * 8 * UG);       // [span][UG]
     float* ts = reinterpret_cast<float*>(cx + span * UG);               // [span][2R]
+    uint16_t* hout = reinterpret_cast<uint16_t*>(ts + span * 2 * R);    // [8 (i1 - i0)]
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
@@ -294,7 +306,7 @@ __global__ void __launch_bounds__(NW * 64) gu_stream_kernel(BatchArgs b, int nb,
     if (nsteps > 0) {
         ld.start(first, 8, f);
         cp = ld;
-        gu_load<JC, NCH, R, GSH>(A, ld.l, ld.n, 0, lane);
+        gu_load<JC, NCH, R, GSH>(A, ld.l, ld.n, 0, false, b.x, lane);
     }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -309,44 +321,52 @@ __global__ void __launch_bounds__(NW * 64) gu_stream_kernel(BatchArgs b, int nb,
             ts[k] = b.t[(long)l0 * 2 * R + k];
     }
     __syncthreads();
-    if (nsteps == 0)
-        return;
 
     // step bookkeeping: load position advances after each issued load while
     // steps remain (the last step's prefetch repeats the last load)
     int left = nsteps - 1;            // loads still to issue after the first
-    auto advance_load = [&]() {
+    auto advance_load = [&]() {       // false: the next load is a dummy
         if (left > 0) {
             --left;
             if (++ldc == NCH) {
                 ldc = 0;
                 ld.next(8 * NW, f);
             }
+            return true;
         }
+        return false;
     };
     float G = 0.0f, Uv = 0.0f;
+    int ci = first - i0;                 // the computed item's index inside the range
     auto run = [&](GuBuf<JC>& q, int c) {
         const int bb = cp.l - l0;
         const int s = lane & 7;
         gu_dot<JC, NCH>(q, xs + bb * 8 * UG + s, cx + bb * UG + s, c, G, Uv);
         if (c == NCH - 1) {
-            gu_finish<JC, R>(q, b, ts + bb * 2 * R, cp.l, cp.n, lane, G, Uv);
+            gu_finish<JC, R>(q, ts + bb * 2 * R, cp.l, hout + 8 * ci, lane, G, Uv);
             G = Uv = 0.0f;
             cp.next(8 * NW, f);
+            ci += NW;
         }
     };
-    for (int st = 0;; st += 2) {
-        advance_load();
-        gu_load<JC, NCH, R, GSH>(B, ld.l, ld.n, NCH - 1, lane);
+    // one back edge and no exit in the middle: both halves always issue
+    // their loads, the second half skips its arithmetic past the last step
+    for (int st = 0; st < nsteps; st += 2) {
+        bool real = advance_load();
+        gu_load<JC, NCH, R, GSH>(B, ld.l, ld.n, NCH - 1, !real, b.x, lane);
         run(A, 0);
-        if (st + 1 >= nsteps)
-            break;
-        advance_load();
-        gu_load<JC, NCH, R, GSH>(A, ld.l, ld.n, 0, lane);
-        run(B, NCH - 1);
-        if (st + 2 >= nsteps)
-            break;
+        real = advance_load();
+        gu_load<JC, NCH, R, GSH>(A, ld.l, ld.n, 0, !real, b.x, lane);
+        if (st + 1 < nsteps)
+            run(B, NCH - 1);
     }
+    // the range's h: 8 (i1 - i0) contiguous values of the batch's flattened
+    // [nb][f], written as 16-byte words (one item per thread and round)
+    __syncthreads();
+    uint4* hdst = reinterpret_cast<uint4*>(b.h) + i0;
+    const uint4* hsrc = reinterpret_cast<const uint4*>(hout);
+    for (int k = tid; k < i1 - i0; k += NT)
+        hdst[k] = hsrc[k];
 }
 
 // ---------------------------------------------------------------- down
@@ -384,11 +404,16 @@ struct DnBuf {
     uint32_t m[JD];
 };
 
+// Loads of row o of block l; a dummy prefetch (past a wave's last row)
+// reads the batch's h instead (offsets below f/2 bytes), which the staging
+// has just brought into the caches.
 template <int JD>
-__device__ __forceinline__ void dn_load(DnBuf<JD>& q, int l, int o, int U, int ng, int gsh, int lane) {
+__device__ __forceinline__ void dn_load(DnBuf<JD>& q, int l, int o, int U, int ng, int gsh, bool dummy,
+                                        const uint16_t* h, int lane) {
     KBatch* kb = kbatch();
-    const uint4* cd = reinterpret_cast<const uint4*>(kb->lay[l].cd) + (long)o * U;
-    const uint32_t* md = kb->lay[l].md + (long)o * ng;
+    const uint4* cd = dummy ? reinterpret_cast<const uint4*>(h)
+                            : reinterpret_cast<const uint4*>(kb->lay[l].cd) + (long)o * U;
+    const uint32_t* md = dummy ? reinterpret_cast<const uint32_t*>(h) : kb->lay[l].md + (long)o * ng;
 #pragma unroll
     for (int j = 0; j < JD; ++j) {
         const int u = lane + 64 * j;
@@ -437,6 +462,7 @@ __global__ void __launch_bounds__(NW * 64) dn_stream_kernel(BatchArgs b, int nb,
     extern __shared__ uint4 smem[];
     uint4* hs = smem;                                                   // [span][4][UD]
     float2* cx = reinterpret_cast<float2*>(smem + span * 4 * UD);       // [span][UD]
+    uint16_t* yout = reinterpret_cast<uint16_t*>(cx + span * UD);       // [r1 - r0]
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
@@ -464,19 +490,21 @@ __global__ void __launch_bounds__(NW * 64) dn_stream_kernel(BatchArgs b, int nb,
     Walk ld, cp;
     DnBuf<JD> A, B, C;
     int left = nk - 1;
-    auto advance_load = [&]() {
+    auto advance_load = [&]() {       // false: the next load is a dummy
         if (left > 0) {
             --left;
             ld.next(NW, d);
+            return true;
         }
+        return false;
     };
     if (nk > 0) {
         ld.start(first, 1, d);
         cp = ld;
-        dn_load<JD>(A, ld.l, ld.n, U, ng, gsh, lane);
+        dn_load<JD>(A, ld.l, ld.n, U, ng, gsh, false, b.h, lane);
         if constexpr (NBUF == 3) {
-            advance_load();
-            dn_load<JD>(B, ld.l, ld.n, U, ng, gsh, lane);
+            const bool real = advance_load();
+            dn_load<JD>(B, ld.l, ld.n, U, ng, gsh, !real, b.h, lane);
         }
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -490,48 +518,46 @@ __global__ void __launch_bounds__(NW * 64) dn_stream_kernel(BatchArgs b, int nb,
         dn_stage_word<UD>(hs + bb * 4 * UD, cx + bb * UD, wi, idx < words, v);
     }
     __syncthreads();
-    if (nk == 0)
-        return;
 
+    // the loop stores its rows into LDS only (see gu_finish)
+    int ci = first - r0;
     auto run = [&](DnBuf<JD>& q) {
         const int bb = cp.l - l0;
         const float v = group_sum<64>(dn_dot<JD>(q, hs + bb * 4 * UD + lane, cx + bb * UD + lane));
         if (lane == 0)
-            b.y[(long)cp.l * d + cp.n] = (uint16_t)f2h(v);
+            yout[ci] = (uint16_t)f2h(v);
         cp.next(NW, d);
+        ci += NW;
     };
     if constexpr (NBUF == 2) {
-        for (int st = 0;; st += 2) {
-            advance_load();
-            dn_load<JD>(B, ld.l, ld.n, U, ng, gsh, lane);
+        for (int st = 0; st < nk; st += 2) {
+            bool real = advance_load();
+            dn_load<JD>(B, ld.l, ld.n, U, ng, gsh, !real, b.h, lane);
             run(A);
-            if (st + 1 >= nk)
-                break;
-            advance_load();
-            dn_load<JD>(A, ld.l, ld.n, U, ng, gsh, lane);
-            run(B);
-            if (st + 2 >= nk)
-                break;
+            real = advance_load();
+            dn_load<JD>(A, ld.l, ld.n, U, ng, gsh, !real, b.h, lane);
+            if (st + 1 < nk)
+                run(B);
         }
     } else {
-        for (int st = 0;; st += 3) {
-            advance_load();
-            dn_load<JD>(C, ld.l, ld.n, U, ng, gsh, lane);
+        for (int st = 0; st < nk; st += 3) {
+            bool real = advance_load();
+            dn_load<JD>(C, ld.l, ld.n, U, ng, gsh, !real, b.h, lane);
             run(A);
-            if (st + 1 >= nk)
-                break;
-            advance_load();
-            dn_load<JD>(A, ld.l, ld.n, U, ng, gsh, lane);
-            run(B);
-            if (st + 2 >= nk)
-                break;
-            advance_load();
-            dn_load<JD>(B, ld.l, ld.n, U, ng, gsh, lane);
-            run(C);
-            if (st + 3 >= nk)
-                break;
+            real = advance_load();
+            dn_load<JD>(A, ld.l, ld.n, U, ng, gsh, !real, b.h, lane);
+            if (st + 1 < nk)
+                run(B);
+            real = advance_load();
+            dn_load<JD>(B, ld.l, ld.n, U, ng, gsh, !real, b.h, lane);
+            if (st + 2 < nk)
+                run(C);
         }
     }
+    // the range's y: r1 - r0 contiguous values of the batch's flattened [nb][d]
+    __syncthreads();
+    for (int k = tid; k < r1 - r0; k += NT)
+        b.y[r0 + k] = yout[k];
 }
 
 // ---------------------------------------------------------------- host side
@@ -581,8 +607,14 @@ int gu_steps(int UG, int& jc) {             // NCH, or 0 if the width is not bui
 
 int dn_slots(int f) { return (f / 32 + 63) / 64; }
 
-size_t gu_lds(int span, int UG, int r) { return (size_t)span * (UG * 8 * 16 + UG * 8 + 2 * r * 4); }
-size_t dn_lds(int span, int UD) { return (size_t)span * UD * (4 * 16 + 8); }
+size_t gu_lds(int span, int UG, int r, int nb, int f, int G) {
+    const size_t items = ((size_t)nb * f / 8 + G - 1) / G;          // most items of one range
+    return (size_t)span * (UG * 8 * 16 + UG * 8 + 2 * r * 4) + items * 16;
+}
+size_t dn_lds(int span, int UD, int nb, int d, int G) {
+    const size_t rows = ((size_t)nb * d + G - 1) / G;
+    return (size_t)span * UD * (4 * 16 + 8) + (rows * 2 + 15) / 16 * 16;
+}
 int gu_span(int nb, int f, int G) { return max_span((long)nb * f / 8, f / 8, G); }
 int dn_span(int nb, int d, int G) { return max_span((long)nb * d, d, G); }
 // One workgroup per compute unit, fewer when the batch has fewer items.
@@ -612,7 +644,8 @@ bool stream_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r
     const int sg = gu_span(nb, f, gu_grid(nb, f)), sd = dn_span(nb, d, dn_grid(nb, d));
     if (sg > kStreamSpan || sd > kStreamSpan)
         return false;
-    return gu_lds(sg, d / 64, r) <= 64 * 1024 && dn_lds(sd, 64 * dn_slots(f)) <= 64 * 1024;
+    return gu_lds(sg, d / 64, r, nb, f, gu_grid(nb, f)) <= 64 * 1024 &&
+           dn_lds(sd, 64 * dn_slots(f), nb, d, dn_grid(nb, d)) <= 64 * 1024;
 }
 
 #define QMLP_GUS(JC_, NCH_, R_)                                                           \
@@ -634,7 +667,7 @@ hipError_t launch_gateup_stream(const BatchArgs& b, int nb, hipStream_t st) {
     int jc = 0;
     const int nch = gu_steps(b.d / 64, jc);
     const int span = gu_span(nb, b.f, G);
-    const size_t lds = gu_lds(span, b.d / 64, r);
+    const size_t lds = gu_lds(span, b.d / 64, r, nb, b.f, G);
     QMLP_GUS_R(1, 1) QMLP_GUS_R(2, 1) QMLP_GUS_R(3, 1) QMLP_GUS_R(4, 1) QMLP_GUS_R(5, 1)
     QMLP_GUS_R(3, 2) QMLP_GUS_R(4, 2) QMLP_GUS_R(5, 2)
     return hipErrorInvalidValue;
@@ -652,7 +685,7 @@ hipError_t launch_down_stream(const BatchArgs& b, int nb, hipStream_t st) {
     const int G = dn_grid(nb, b.d);
     const int jd = dn_slots(b.f);
     const int span = dn_span(nb, b.d, G);
-    const size_t lds = dn_lds(span, 64 * jd);
+    const size_t lds = dn_lds(span, 64 * jd, nb, b.d, G);
     QMLP_DNS(1) QMLP_DNS(2) QMLP_DNS(3) QMLP_DNS(4) QMLP_DNS(5) QMLP_DNS(6)
     return hipErrorInvalidValue;
 }
