@@ -63,7 +63,9 @@ from paper_2606_04238_amd.profiling import read_traffic  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
 # the launches of one streamed step, as named in the kernel trace
-STEP_KERNELS = "lora_a_kernel|gu_stream_kernel|dn_stream_kernel"
+# the kernels of one step of qmlp_forward_layers on each path (profile summaries)
+STEP_KERNELS = {"streamed": "lora_a_kernel|gu_stream_kernel|dn_stream_kernel",
+                "mfma": "lora_a_kernel|mf_gu_kernel|mf_dn_kernel"}
 METRIC = BASE_METRIC = ("achieved HBM GB/s (% of MI355X peak) and µs per W4/W2-GateUp MLP "
                         "decode step")
 
@@ -822,13 +824,14 @@ def main(argv=None):
     # LoRA-A, then gate/up and down over every block of a batch of up to 40 --
     # are internal to the call, so the timed region's events give the step;
     # the per-kernel split is in the committed kernel trace.
-    if path not in ("streamed", "batched"):
-        raise RuntimeError("binary16 decode streams or runs batched; got path %s" % path)
+    if path not in ("streamed", "mfma", "batched"):
+        raise RuntimeError("binary16 decode streams, runs on the matrix cores or runs batched; got path %s"
+                           % path)
     dom_name = ("%s step (LoRA-A, gate/up and down launches of qmlp_forward_layers)" % path)
     dom_us, dom_b = t_step * 1e3, L * B
     kernel_us = {"step": round(dom_us, 3), "launches_per_step": launches}
     traffic = read_traffic(os.path.join(ROOT, "profiles", "layers_%s_%s.md" % (path, cfg.name)),
-                           STEP_KERNELS) if path == "streamed" else None
+                           STEP_KERNELS[path]) if path in STEP_KERNELS else None
     achieved = dom_b / (dom_us * 1e-6) / 1e9
 
     out = {
@@ -853,6 +856,7 @@ def main(argv=None):
             "alg_bytes_per_mlp_step": B,
             "mode": "hip_graph" if args.mode == "graph" else "eager",
             "path": {"streamed": "streamed launches (LoRA-A, gate/up, down over every block)",
+                     "mfma": "matrix-core launches (LoRA-A, gate/up, down over every block)",
                      "batched": "batched stand-alone kernels"}[path],
             "eager_us_per_mlp_step": round(eager_step * 1e3 / L, 3),
             "graph_us_per_mlp_step": round(graph_step * 1e3 / L, 3),

@@ -269,7 +269,12 @@ int qmlp_stack_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
  * persistent gate/up launch and one persistent down launch, each workgroup
  * owning a contiguous range of the batch's rows flattened over blocks, so
  * no workgroup waits for another and h of every block passes through the
- * workspace between the two launches.  Every other binary16 batch runs the
+ * workspace between the two launches.  At 3 <= M <= 16 in the same form
+ * (d % (4 g) == 0, f % (2 g_down) == 0, and the workspace-free limits
+ * qmlp_layers_path reports) a batch runs on the MATRIX CORES: the LoRA-A
+ * launch, then one persistent gate/up launch and one persistent down
+ * launch that multiply every unpacked weight into all M tokens with
+ * v_mfma_f32_16x16x32_f16.  Every other binary16 batch runs the
  * stand-alone kernels as qmlp_forward_batch does; bfloat16 runs
  * qmlp_forward once per block.
  *
@@ -284,12 +289,13 @@ qmlp_status qmlp_forward_layers(const qmlp_mlp *layers, int L, const void *x, in
                                 qmlp_stream stream);
 
 /* Which path qmlp_forward_layers takes for these blocks: 1 = streamed, 2 =
- * the batched stand-alone kernels, 3 = qmlp_forward per block (bfloat16);
- * 0 if the call would be rejected.  Host-only. */
+ * the batched stand-alone kernels, 3 = qmlp_forward per block (bfloat16),
+ * 4 = matrix cores; 0 if the call would be rejected.  Host-only (it queries
+ * the current device's compute-unit count). */
 int qmlp_layers_path(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
 
 /* Launches qmlp_forward_layers makes: 3 per batch of up to 40 blocks (2
- * without adapters) on the streamed and batched paths, or the per-block
+ * without adapters) on the streamed, matrix-core and batched paths, or the per-block
  * launches of qmlp_forward; 0 if the call would be rejected.  Host-only. */
 int qmlp_layers_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
 

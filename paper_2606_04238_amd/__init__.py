@@ -336,7 +336,7 @@ def layers_workspace_bytes(layers: Layers, M: int, dtype=torch.float16) -> int:
     return int(_lib().qmlp_layers_workspace_bytes(layers.c(), len(layers), M, code))
 
 
-LAYERS_PATHS = {0: "rejected", 1: "streamed", 2: "batched", 3: "per-block"}
+LAYERS_PATHS = {0: "rejected", 1: "streamed", 2: "batched", 3: "per-block", 4: "mfma"}
 
 
 def layers_path(layers: Layers, M: int, dtype=torch.float16) -> str:

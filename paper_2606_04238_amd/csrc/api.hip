@@ -314,13 +314,36 @@ bool layers_streamed(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
     return (full == 0 || ok(kBatchMax)) && (rest == 0 || ok(rest));
 }
 
-// Independent blocks that do not stream run in batches of up to kBatchMax
-// blocks on the stand-alone kernels: LoRA-A of every block of the batch,
-// then gate/up of every block, then down of every block (three launches per
-// batch, two without adapters).  Binary16 decode only; bfloat16 runs
-// qmlp_forward per block.
+// Independent blocks at 3..16 tokens in the W4/W2-GateUp form run on the
+// matrix cores: every batch is the LoRA-A launch, one persistent gate/up
+// launch and one persistent down launch (decode_mfma.hip).
+bool layers_mfma(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    const qmlp_mlp& a = layers[0];
+    if (dtype != QMLP_F16 || !standard_mlp(&a))
+        return false;
+    const int full = L / kBatchMax, rest = L % kBatchMax;
+    const auto ok = [&](int nb) {
+        return mfma_supported(M, a.gate.k_in, a.gate.n_out, a.gate.group, a.gate.bits, a.down.group,
+                              a.down.bits, a.rank, nb);
+    };
+    return (full == 0 || ok(kBatchMax)) && (rest == 0 || ok(rest));
+}
+
+// Independent blocks that neither stream nor take the matrix cores run in
+// batches of up to kBatchMax blocks on the stand-alone kernels: LoRA-A of
+// every block of the batch, then gate/up of every block, then down of every
+// block (three launches per batch, two without adapters).  Binary16 decode
+// only; bfloat16 runs qmlp_forward per block.
 bool layers_batched(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
-    return dtype == QMLP_F16 && !layers_streamed(layers, L, M, dtype);
+    return dtype == QMLP_F16 && !layers_streamed(layers, L, M, dtype) && !layers_mfma(layers, L, M, dtype);
+}
+
+enum class BatchPath { kBatched, kStreamed, kMfma };
+
+BatchPath batch_path(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    return layers_streamed(layers, L, M, dtype) ? BatchPath::kStreamed
+           : layers_mfma(layers, L, M, dtype)   ? BatchPath::kMfma
+                                                : BatchPath::kBatched;
 }
 
 size_t batch_t_bytes(const qmlp_mlp* a, int nb, int M) {
@@ -332,7 +355,7 @@ size_t batch_h_bytes(const qmlp_mlp* a, int nb, int M) {
 int batch_size(int L) { return L < kBatchMax ? L : kBatchMax; }
 
 qmlp_status run_layers_batched(const qmlp_mlp* layers, int L, const char* xb, int M, char* yb,
-                               void* ws, hipStream_t st, bool streamed = false) {
+                               void* ws, hipStream_t st, BatchPath path) {
     const qmlp_mlp& a = layers[0];
     const int d = a.gate.k_in;
     const size_t step = (size_t)M * d * 2;
@@ -355,9 +378,13 @@ qmlp_status run_layers_batched(const qmlp_mlp* layers, int L, const char* xb, in
         b.y = reinterpret_cast<uint16_t*>(yb + l0 * step);
         hipError_t e = b.r > 0 ? launch_lora_a_batch(b, n, st) : hipSuccess;
         if (e == hipSuccess)
-            e = streamed ? launch_gateup_stream(b, n, st) : launch_gateup_batch(b, n, st);
+            e = path == BatchPath::kStreamed ? launch_gateup_stream(b, n, st)
+                : path == BatchPath::kMfma   ? launch_gateup_mfma(b, n, st)
+                                             : launch_gateup_batch(b, n, st);
         if (e == hipSuccess)
-            e = streamed ? launch_down_stream(b, n, st) : launch_down_batch(b, n, st);
+            e = path == BatchPath::kStreamed ? launch_down_stream(b, n, st)
+                : path == BatchPath::kMfma   ? launch_down_mfma(b, n, st)
+                                             : launch_down_batch(b, n, st);
         if (e != hipSuccess)
             return QMLP_ERR_HIP;
     }
@@ -626,7 +653,7 @@ qmlp_status qmlp_forward_stack(const qmlp_mlp* layers, int L, const void* x, int
 size_t qmlp_layers_workspace_bytes(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
     if (check_layers(layers, L, M, dtype) != QMLP_OK || M == 0)
         return 0;
-    if (dtype == QMLP_F16)              // streamed or batched
+    if (dtype == QMLP_F16)              // streamed, matrix-core or batched
         return qmlp_batch_workspace_bytes(layers, L, M, dtype);
     return qmlp_workspace_bytes(&layers[0], M, dtype);
 }
@@ -636,6 +663,8 @@ int qmlp_layers_path(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
         return 0;
     if (layers_streamed(layers, L, M, dtype))
         return 1;
+    if (layers_mfma(layers, L, M, dtype))
+        return 4;
     if (layers_batched(layers, L, M, dtype))
         return 2;
     return 3;
@@ -644,7 +673,7 @@ int qmlp_layers_path(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
 int qmlp_layers_launches(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
     if (check_layers(layers, L, M, dtype) != QMLP_OK || M == 0)
         return 0;
-    if (dtype == QMLP_F16)              // streamed or batched: three launches per batch
+    if (dtype == QMLP_F16)              // streamed, matrix-core or batched: three launches per batch
         return (L + kBatchMax - 1) / kBatchMax * (layers[0].rank > 0 ? 3 : 2);
     int n = 0;
     for (int i = 0; i < L; ++i) n += qmlp_forward_launches(&layers[i], M, dtype);
@@ -672,7 +701,7 @@ qmlp_status qmlp_forward_layers(const qmlp_mlp* layers, int L, const void* x, in
     char* yb = static_cast<char*>(y);
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (dtype == QMLP_F16)
-        return run_layers_batched(layers, L, xb, M, yb, ws, st, layers_streamed(layers, L, M, dtype));
+        return run_layers_batched(layers, L, xb, M, yb, ws, st, batch_path(layers, L, M, dtype));
     for (int i = 0; i < L; ++i) {
         s = qmlp_forward(&layers[i], xb + i * step, M, dtype, yb + i * step, ws, ws_bytes, stream);
         if (s != QMLP_OK)
@@ -705,7 +734,7 @@ qmlp_status qmlp_forward_batch(const qmlp_mlp* layers, int L, const void* x, int
     if (!aligned16(ws))
         return QMLP_ERR_ALIGN;
     return run_layers_batched(layers, L, static_cast<const char*>(x), M, static_cast<char*>(y), ws,
-                              static_cast<hipStream_t>(stream));
+                              static_cast<hipStream_t>(stream), BatchPath::kBatched);
 }
 
 qmlp_status qmlp_linear_batch(const qmlp_qweight* w, int L, const void* x, int M, qmlp_dtype dtype,

@@ -30,6 +30,37 @@ namespace qmlp {
 constexpr int GU_UNIT_BYTES = 8 * 16 + 8;   // LDS bytes per (token, 2-bit unit): x' + (C, X)
 constexpr int DN_UNIT_BYTES = 4 * 16 + 8;   // LDS bytes per (token, 4-bit unit): h' + (C, X)
 
+// One-shift forms (the streamed and MFMA kernels): code fields are read where
+// they sit in the word, so a word needs one shift.
+// 2-bit code pairs of one word, one shift: pair p = (code p, code 8 + p) at
+// fraction positions 2 kp, kp = {0, 1, 2, 3, 4, 2, 3, 4}.
+__device__ __forceinline__ void extract_w2_s1(uint32_t w, uint32_t e[8], uint32_t mv) {
+    const uint32_t r = w >> 6;          // codes 5, 6, 7 -> bits 4-9
+    e[0] = magic(w, 0x00030003u, mv);
+    e[1] = magic(w, 0x000C000Cu, mv);
+    e[2] = magic(w, 0x00300030u, mv);
+    e[3] = magic(w, 0x00C000C0u, mv);
+    e[4] = magic(w, 0x03000300u, mv);
+    e[5] = magic(r, 0x00300030u, mv);
+    e[6] = magic(r, 0x00C000C0u, mv);
+    e[7] = magic(r, 0x03000300u, mv);
+}
+__device__ __forceinline__ float w2_s1_scale(int p) {
+    const int k = (0x43243210 >> (4 * p)) & 15;
+    return __builtin_bit_cast(float, (uint32_t)(127 - 2 * k) << 23);
+}
+
+// 4-bit code pairs of one word, one shift: pair p = (code p, code 4 + p) at
+// fraction positions {0, 4, 0, 4}.
+__device__ __forceinline__ void extract_w4_s1(uint32_t w, uint32_t e[4], uint32_t mv) {
+    const uint32_t r = w >> 8;          // codes 2, 3 -> bits 0-7
+    e[0] = magic(w, 0x000F000Fu, mv);
+    e[1] = magic(w, 0x00F000F0u, mv);
+    e[2] = magic(r, 0x000F000Fu, mv);
+    e[3] = magic(r, 0x00F000F0u, mv);
+}
+__device__ __forceinline__ float w4_s1_scale(int p) { return (p & 1) ? 1.0f / 16 : 1.0f; }
+
 // --------------------------------------------------------------- staging
 // The activation (x for gate/up, h for down) is staged in LDS pre-scaled per
 // fraction position.  Staging is split into a load phase (registers) and a

@@ -1,0 +1,723 @@
+// Decode at several tokens (3 <= M <= 16, binary16) on the matrix cores,
+// gfx950: a batch of independent blocks as two persistent launches after the
+// LoRA-A products,
+//
+//   gate/up launch:  h_l = SiLU(W2gate x_l + s B_g t_g) * (W2up x_l + s B_u t_u)
+//                    (Sec. 3.1 Eq. (1), Sec. 3.3, Sec. 4.2);
+//   down launch:     y_l = W4down h_l (Sec. 3.3).
+//
+// With M tokens a weight feeds M multiply-adds; on the vector ALU that is
+// M/2 dot2 operations per weight on top of its dequantization, more than the
+// weight stream allows from a few tokens on.  Here every weight is unpacked
+// once and multiplied into all tokens at once by v_mfma_f32_16x16x32_f16:
+// the activation is the A operand (tokens as the 16 rows, padded), the codes
+// the B operand (16 weight rows), D[token][weight row] in fp32.  A lane of a
+// 16x16x32 step holds row (lane & 15) of each operand and K elements
+// 8 (lane >> 4) .. + 7, and receives D rows 4 (lane >> 4) + v, column
+// (lane & 15): the D values of a lane belong to its own weight row.
+//
+// Every MFMA step stays inside one quantization group, so the group's scale
+// and zero apply exactly afterwards: lane quarter q = lane >> 4 covers a
+// fixed set of 16-code (2-bit) or 8-code (4-bit) words of each group.  The
+// codes enter as in the other decode kernels: a field OR-ed into binary16
+// 1024.0 reads 1024 + c 2^j, the activation is staged pre-scaled by 2^-j in
+// the same pair order per word, and each group's accumulator starts at
+// -(C + z X) (C = 1024 sum x', X = sum x per token and group), so the group
+// adds s * acc.  The LoRA-B term is one more MFMA per item: lora_scale * t
+// (binary16, zero past the rank) times the item's B rows.
+//
+// Loads.  Every code load is 16 bytes per lane, 64 contiguous bytes per
+// weight row and instruction.  Where one load spans several groups, the
+// words are redistributed between lane quarters with v_permlane32_swap /
+// v_permlane16_swap so that each quarter ends up with words of every group.
+//
+// Work split.  Each workgroup owns a contiguous range of the batch's
+// 16-row items (flattened over blocks).
+//   gate/up: the whole x' of the block an item belongs to sits in LDS (MT
+//     token rows, MT = 4, 8 or 16 >= M; A rows past MT re-read token
+//     row & (MT - 1), their results are never stored); a range touching two
+//     blocks stages them one after the other.  Waves take the range's items
+//     in turn and stream each item's codes in steps of four groups with two
+//     register sets.
+//   down: h' of a block is too large for LDS at these widths, so the K
+//     dimension (f) is walked in steps of two groups: every wave keeps the
+//     accumulators of its few items for the whole walk, and h' is staged in
+//     chunks of several steps into two LDS buffers that all waves share (one
+//     barrier per chunk).
+#include "decode_common.h"
+#include "decode_launch.h"
+
+namespace qmlp {
+
+namespace {
+
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef const BatchArgs __attribute__((address_space(4))) KBatchM;
+__device__ __forceinline__ KBatchM* kbm() { return (KBatchM*)__builtin_amdgcn_kernarg_segment_ptr(); }
+
+__device__ __forceinline__ f32x4_t mfma16(const uint4& a, const uint4& b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a),
+                                                  __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
+}
+
+// Lanes 32-63 of a trade places with lanes 0-31 of b.
+__device__ __forceinline__ void swap32(uint32_t& a, uint32_t& b) {
+    const auto r = __builtin_amdgcn_permlane32_swap(a, b, false, false);
+    a = r[0];
+    b = r[1];
+}
+// Lanes 16-31 and 48-63 of a trade places with lanes 0-15 and 32-47 of b.
+__device__ __forceinline__ void swap16(uint32_t& a, uint32_t& b) {
+    const auto r = __builtin_amdgcn_permlane16_swap(a, b, false, false);
+    a = r[0];
+    b = r[1];
+}
+
+// LDS barrier that leaves vector-memory loads in flight: this wave's LDS
+// accesses complete, then the workgroup meets.
+__device__ __forceinline__ void lds_barrier() {
+    __asm__ volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Weight loads go through buffer resources: a resource of zero bytes turns
+// a load into one that returns zeros without touching memory, so a prefetch
+// that has nothing to fetch issues the same instructions as one that has
+// (the compiler then keeps the next step's loads in flight across a step),
+// and every load is bounds-checked against its array.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+__device__ __forceinline__ Rsrc rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+constexpr int kAuxNt = 2;      // non-temporal: codes are read once
+template <int AUX>
+__device__ __forceinline__ uint4 bload16(Rsrc r, uint32_t voff, uint32_t soff) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, AUX);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ uint2 bload8(Rsrc r, uint32_t voff, uint32_t soff) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+    return make_uint2(v[0], v[1]);
+}
+
+constexpr int kMfWaves = 12;   // waves per workgroup (one workgroup per compute unit)
+constexpr int kSteps = 4;      // gate/up: groups per streamed step
+
+// First word, within a group, of the words that lane quarter q multiplies:
+// 2-bit g = 64 (one word each): q; 2-bit g = 128 and 4-bit g = 64 (two words
+// each, after the 32-lane swap): 4 (q & 1) + 2 (q >> 1); 4-bit g = 128 (four
+// words, loaded in place): 4 q.
+template <int QW>
+__device__ __forceinline__ int quarter_word(int q) {
+    if constexpr (QW == 1) return q;
+    else if constexpr (QW == 2) return 4 * (q & 1) + 2 * (q >> 1);
+    else return 4 * q;
+}
+
+// ---------------------------------------------------------------- staging
+// Staging word W (16 values) of token j of an activation into x' halves
+// (pairs (x[p], x[8 + p]), pre-scaled; layout [W][half][MT]) and the
+// (-C, -X) of its group (GW words per group on GW consecutive lanes; every
+// lane of the wave calls this).
+template <int MT, int GW>
+__device__ __forceinline__ void mf_stage_word(uint4* xs, float2* cx, int W, int j, bool live, const uint4& lo16,
+                                              const uint4& hi16) {
+    const uint32_t xl[4] = {lo16.x, lo16.y, lo16.z, lo16.w};
+    const uint32_t xh[4] = {hi16.x, hi16.y, hi16.z, hi16.w};
+    uint32_t pr[8];
+    float csum = 0.0f, xsum = 0.0f;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+        const uint32_t a16 = (xl[p >> 1] >> (16 * (p & 1))) & 0xFFFFu;     // x[p]
+        const uint32_t b16 = (xh[p >> 1] >> (16 * (p & 1))) & 0xFFFFu;     // x[8 + p]
+        const float sc = w2_s1_scale(p);
+        const uint32_t ha = f2h(h2f(a16) * sc), hb = f2h(h2f(b16) * sc);
+        pr[p] = ha | (hb << 16);
+        csum += h2f(ha) + h2f(hb);
+        xsum += h2f(a16) + h2f(b16);
+    }
+    csum = group_sum<GW>(csum);
+    xsum = group_sum<GW>(xsum);
+    if (live) {
+        xs[(W * 2) * MT + j] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
+        xs[(W * 2 + 1) * MT + j] = make_uint4(pr[4], pr[5], pr[6], pr[7]);
+        if (W % GW == 0)
+            cx[(W / GW) * MT + j] = make_float2(-1024.0f * csum, -xsum);
+    }
+}
+
+// 4-bit words: 8 values of token j (one 16-byte load) as pairs (h[p], h[4 + p])
+// pre-scaled for the positions {0, 4, 0, 4}; layout [W][MT]; GW words per group.
+template <int MT, int GW>
+__device__ __forceinline__ void mf_stage_word4(uint4* hs, float2* cx, int W, int j, bool live, const uint4& v) {
+    const uint32_t hl[4] = {v.x, v.y, v.z, v.w};
+    uint32_t pr[4];
+    float csum = 0.0f, xsum = 0.0f;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const uint32_t a16 = (hl[p >> 1] >> (16 * (p & 1))) & 0xFFFFu;
+        const uint32_t b16 = (hl[2 + (p >> 1)] >> (16 * (p & 1))) & 0xFFFFu;
+        const float sc = w4_s1_scale(p);
+        const uint32_t ha = f2h(h2f(a16) * sc), hb = f2h(h2f(b16) * sc);
+        pr[p] = ha | (hb << 16);
+        csum += h2f(ha) + h2f(hb);
+        xsum += h2f(a16) + h2f(b16);
+    }
+    csum = group_sum<GW>(csum);
+    xsum = group_sum<GW>(xsum);
+    if (live) {
+        hs[W * MT + j] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
+        if (W % GW == 0)
+            cx[(W / GW) * MT + j] = make_float2(-1024.0f * csum, -xsum);
+    }
+}
+
+// ---------------------------------------------------------------- gate/up
+// One step (four groups) of an item: NL = G / 64 loads per matrix.
+template <int G>
+struct MfGuBuf {
+    static constexpr int NL = G / 64;
+    uint4 cg[NL], cu[NL];
+    uint4 mg, mu;            // the row's (scale | zero) words of the four groups
+    uint4 bg, bu;            // LoRA-B ranks 8 q .. 8 q + 7 of the row (last step of an item)
+};
+
+// Step c of the item whose first row is row n of block l.  Lane: row
+// n + (lane & 15); load i covers bytes [64 i + 16 q, + 16) of the step's
+// 64 NL bytes of the row.  A prefetch past a wave's last step (dummy), and
+// the LoRA-B rows on every step but an item's last, load from empty
+// resources.  The (scale | zero) words are plain loads: a row's 128-byte
+// line of them serves several steps.
+template <int G>
+__device__ __forceinline__ void mf_gu_load(MfGuBuf<G>& q, int l, int n, int c, int nsb, int d, int f, int r,
+                                           bool dummy, int lane) {
+    constexpr int NL = G / 64;
+    KBatchM* kb = kbm();
+    const int qt = lane >> 4, lr = lane & 15;
+    const int ng = d / G, rw = d / 16;
+    const uint32_t cbytes = dummy ? 0u : (uint32_t)f * (uint32_t)(d / 4);
+    const uint32_t mbytes = dummy ? 0u : (uint32_t)f * (uint32_t)ng * 4u;
+    const Rsrc rg = rsrc(kb->lay[l].cg, cbytes), ru = rsrc(kb->lay[l].cu, cbytes);
+    const Rsrc sg = rsrc(kb->lay[l].mg, mbytes), su = rsrc(kb->lay[l].mu, mbytes);
+    const uint32_t cv = (uint32_t)(lr * rw + 4 * qt) * 4u;
+    const uint32_t cs = (uint32_t)(n * rw + c * kSteps * (G / 16)) * 4u;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+        q.cg[i] = bload16<kAuxNt>(rg, cv + 64 * i, cs);
+        q.cu[i] = bload16<kAuxNt>(ru, cv + 64 * i, cs);
+    }
+    const uint32_t mv = (uint32_t)(lr * ng) * 4u, ms = (uint32_t)(n * ng + c * kSteps) * 4u;
+    q.mg = bload16<0>(sg, mv, ms);
+    q.mu = bload16<0>(su, mv, ms);
+    const bool lora = !dummy && c == nsb - 1 && r > 0;
+    const uint32_t bbytes = lora ? (uint32_t)f * (uint32_t)r * 2u : 0u;
+    const Rsrc bg = rsrc(kb->lay[l].Bg, bbytes), bu = rsrc(kb->lay[l].Bu, bbytes);
+    const uint32_t bv = (uint32_t)(lr * r + (8 * qt < r ? 8 * qt : 0)) * 2u, bs = (uint32_t)(n * r) * 2u;
+    q.bg = bload16<0>(bg, bv, bs);
+    q.bu = bload16<0>(bu, bv, bs);
+}
+
+// Words of group i (0..3) of the step for this lane, after redistribution.
+template <int G>
+__device__ __forceinline__ void mf_gu_words(uint4 (&v)[G / 64], uint32_t (&w)[4][G / 64]) {
+    if constexpr (G == 64) {
+        // one load holds four groups: lane quarter q has group q; transpose
+        uint32_t a = v[0].x, b = v[0].y, c = v[0].z, e = v[0].w;
+        swap32(a, c);
+        swap32(b, e);
+        swap16(a, b);
+        swap16(c, e);
+        w[0][0] = a; w[1][0] = b; w[2][0] = c; w[3][0] = e;
+    } else {
+        // load i holds groups 2i, 2i + 1: lane quarter q has group 2i + (q >> 1)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            uint32_t a = v[i].x, b = v[i].y, c = v[i].z, e = v[i].w;
+            swap32(a, c);
+            swap32(b, e);
+            w[2 * i][0] = a; w[2 * i][1] = b;
+            w[2 * i + 1][0] = c; w[2 * i + 1][1] = e;
+        }
+    }
+}
+
+template <int G, int MT>
+__device__ __forceinline__ void mf_gu_step(MfGuBuf<G>& q, const uint4* xsb, const float2* cxb, int c, int lane,
+                                           f32x4_t& G4, f32x4_t& U4) {
+    constexpr int QW = G / 64, WPG = G / 16;
+    const uint32_t mv = magic_vgpr();
+    const int qt = lane >> 4;
+#pragma unroll
+    for (int i = 0; i < G / 64; ++i) {
+        pin4(q.cg[i]);
+        pin4(q.cu[i]);
+    }
+    uint32_t wg[4][QW], wu[4][QW];
+    mf_gu_words<G>(q.cg, wg);
+    mf_gu_words<G>(q.cu, wu);
+    const uint32_t mgw[4] = {q.mg.x, q.mg.y, q.mg.z, q.mg.w};
+    const uint32_t muw[4] = {q.mu.x, q.mu.y, q.mu.z, q.mu.w};
+#pragma unroll
+    for (int i = 0; i < kSteps; ++i) {
+        const int t = c * kSteps + i;
+        // (-C, -X) of the tokens of this lane's D rows, 4 (q & (MT/4 - 1)) .. + 3
+        const float2* cl = cxb + t * MT + 4 * (qt & (MT / 4 - 1));
+        const float2 k0 = cl[0], k1 = cl[1], k2 = cl[2], k3 = cl[3];
+        const float zg = h2f(mgw[i] >> 16), zu = h2f(muw[i] >> 16);
+        f32x4_t ag = {zg * k0.y + k0.x, zg * k1.y + k1.x, zg * k2.y + k2.x, zg * k3.y + k3.x};
+        f32x4_t au = {zu * k0.y + k0.x, zu * k1.y + k1.x, zu * k2.y + k2.x, zu * k3.y + k3.x};
+#pragma unroll
+        for (int w = 0; w < QW; ++w) {
+            uint32_t eg[8], eu[8];
+            extract_w2_s1(wg[i][w], eg, mv);
+            extract_w2_s1(wu[i][w], eu, mv);
+            const int W = t * WPG + w;                         // plus the lane's quarter offset (in xsb)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const uint4 a = xsb[(W * 2 + h) * MT];
+                ag = mfma16(a, make_uint4(eg[4 * h], eg[4 * h + 1], eg[4 * h + 2], eg[4 * h + 3]), ag);
+                au = mfma16(a, make_uint4(eu[4 * h], eu[4 * h + 1], eu[4 * h + 2], eu[4 * h + 3]), au);
+            }
+        }
+        G4 += h2f(mgw[i] & 0xFFFFu) * ag;
+        U4 += h2f(muw[i] & 0xFFFFu) * au;
+    }
+}
+
+template <int G, int MT, int NW>
+__global__ void __launch_bounds__(NW * 64) mf_gu_kernel(BatchArgs b, int nb) {
+    constexpr int NT = NW * 64, GW = G / 16, QW = G / 64;
+    const int d = b.d, f = b.f, r = b.r, M = b.M;
+    const int nsb = d / (G * kSteps);                     // steps per item
+    const int NWd = d / 16;                               // 16-code words per row
+    extern __shared__ uint4 smem[];
+    uint4* xs = smem;                                                    // [NWd][2][MT]
+    float2* cx = reinterpret_cast<float2*>(smem + NWd * 2 * MT);          // [d/G][MT]
+    uint16_t* tsg = reinterpret_cast<uint16_t*>(cx + (d / G) * MT);       // [MT][32] lora_scale t_g
+    uint16_t* tsu = tsg + MT * 32;                                       // [MT][32] lora_scale t_u
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int ipb = f / 16;                               // items per block
+    const int qt = lane >> 4, jj = (lane & 15) & (MT - 1);
+
+    const int nit = nb * ipb;
+    const int i0 = (int)((long)blockIdx.x * nit / gridDim.x), i1 = (int)((long)(blockIdx.x + 1) * nit / gridDim.x);
+    for (int seg = i0; seg < i1;) {
+        const int l = seg / ipb;
+        const int send = (l + 1) * ipb < i1 ? (l + 1) * ipb : i1;
+        // ---- stage x' of block l, its (-C, -X) and lora_scale * t
+        __syncthreads();                                  // the previous segment is done with LDS
+        {
+            const uint16_t* xl = b.x + (long)l * M * d;
+            const int words = MT * NWd;
+            for (int idx = tid; idx < ((words + 63) & ~63); idx += NT) {
+                const bool live = idx < words;
+                const int j = live ? idx / NWd : 0, W = live ? idx - j * NWd : 0;
+                const bool data = live && j < M;
+                const uint4* src = reinterpret_cast<const uint4*>(xl + (long)(data ? j : 0) * d) + 2 * W;
+                uint4 lo = src[0], hi = src[1];
+                if (!data)
+                    lo = hi = make_uint4(0u, 0u, 0u, 0u);
+                mf_stage_word<MT, GW>(xs, cx, W, j, live, lo, hi);
+            }
+            const float ls = kbm()->lay[l].lora_scale;
+            for (int k = tid; k < MT * 32; k += NT) {
+                const int j = k >> 5, c = k & 31;
+                const bool ok = j < M && c < r;
+                const float* tl = b.t + ((long)l * M + (ok ? j : 0)) * 2 * r;
+                tsg[k] = (uint16_t)f2h(ok ? ls * tl[c] : 0.0f);
+                tsu[k] = (uint16_t)f2h(ok ? ls * tl[r + c] : 0.0f);
+            }
+        }
+        __syncthreads();
+        // ---- this wave's items of the segment, nsb steps each, two register sets
+        const int first = seg + wave;
+        const int nk = first < send ? (send - first + NW - 1) / NW : 0;
+        const int nsteps = nk * nsb;
+        if (nsteps > 0) {
+            const uint4* xsb = xs + quarter_word<QW>(qt) * 2 * MT + jj;     // this lane's A base
+            int ld_item = first, ld_c = 0, left = nsteps - 1;
+            int cp_item = first, cp_c = 0;
+            auto advance = [&]() {
+                if (left > 0) {
+                    --left;
+                    if (++ld_c == nsb) {
+                        ld_c = 0;
+                        ld_item += NW;
+                    }
+                    return true;
+                }
+                return false;
+            };
+            MfGuBuf<G> A, B;
+            mf_gu_load<G>(A, l, (ld_item - l * ipb) * 16, ld_c, nsb, d, f, r, false, lane);
+            f32x4_t Gt = {0.f, 0.f, 0.f, 0.f}, Ut = {0.f, 0.f, 0.f, 0.f};
+            auto run = [&](MfGuBuf<G>& q) {
+                mf_gu_step<G, MT>(q, xsb, cx, cp_c, lane, Gt, Ut);
+                if (cp_c == nsb - 1) {
+                    if (r > 0) {
+                        // LoRA-B: lora_scale * t (A rows = tokens) times the item's B rows
+                        const uint4 ag = *reinterpret_cast<const uint4*>(tsg + jj * 32 + 8 * qt);
+                        const uint4 au = *reinterpret_cast<const uint4*>(tsu + jj * 32 + 8 * qt);
+                        Gt = mfma16(ag, q.bg, Gt);
+                        Ut = mfma16(au, q.bu, Ut);
+                    }
+                    const int n = (cp_item - l * ipb) * 16 + (lane & 15);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int tok = 4 * qt + v;
+                        const float gv = Gt[v], uv = Ut[v];
+                        if (tok < M)
+                            b.h[((long)l * M + tok) * f + n] = (uint16_t)f2h(gv / (1.0f + __expf(-gv)) * uv);
+                    }
+                    Gt = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                    Ut = f32x4_t{0.f, 0.f, 0.f, 0.f};
+                    cp_c = 0;
+                    cp_item += NW;
+                } else {
+                    ++cp_c;
+                }
+            };
+            for (int st = 0; st < nsteps; st += 2) {
+                bool real = advance();
+                mf_gu_load<G>(B, l, (ld_item - l * ipb) * 16, ld_c, nsb, d, f, r, !real, lane);
+                run(A);
+                real = advance();
+                mf_gu_load<G>(A, l, (ld_item - l * ipb) * 16, ld_c, nsb, d, f, r, !real, lane);
+                if (st + 1 < nsteps)
+                    run(B);
+            }
+        }
+        seg = send;
+    }
+}
+
+// ---------------------------------------------------------------- down
+constexpr int kDnSteps = 2;    // down: groups per streamed step
+
+// One step (two groups) of TPW items: NL = G / 64 loads per item.
+template <int G, int TPW>
+struct MfDnBuf {
+    static constexpr int NL = G / 64;
+    uint4 c[TPW][NL];
+    uint2 m[TPW];            // the row's (scale | zero) words of the two groups
+};
+
+// Step k of the wave's items: item tt has its first row at row0 + tt * srow.
+// Load i of an item covers bytes [64 i + 16 q, + 16) of the step's 64 NL
+// bytes of the row.  Items at or past ntile, and a prefetch past the last
+// step, load from empty resources.
+template <int G, int TPW>
+__device__ __forceinline__ void mf_dn_load(MfDnBuf<G, TPW>& q, int l, int row0, int srow, int ntile, int k, int d,
+                                           int f, bool dummy, int lane) {
+    constexpr int NL = G / 64;
+    KBatchM* kb = kbm();
+    const int qt = lane >> 4, lr = lane & 15, ng = f / G, rw = f / 8;
+    const uint32_t cv = (uint32_t)(lr * rw + 4 * qt) * 4u, mv = (uint32_t)(lr * ng) * 4u;
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+        const bool real = !dummy && tt < ntile;
+        const Rsrc rc = rsrc(kb->lay[l].cd, real ? (uint32_t)d * (uint32_t)(f / 2) : 0u);
+        const Rsrc rm = rsrc(kb->lay[l].md, real ? (uint32_t)d * (uint32_t)ng * 4u : 0u);
+        const int row = row0 + tt * srow;
+        const uint32_t cs = (uint32_t)(row * rw + k * kDnSteps * (G / 8)) * 4u;
+#pragma unroll
+        for (int i = 0; i < NL; ++i) q.c[tt][i] = bload16<kAuxNt>(rc, cv + 64 * i, cs);
+        q.m[tt] = bload8(rm, mv, (uint32_t)(row * ng + k * kDnSteps) * 4u);
+    }
+}
+
+// Word ww (0 .. G/32 - 1) of group i (0, 1) of the step for this lane, from
+// the item's loads after mf_dn_arrange.
+template <int G>
+__device__ __forceinline__ uint32_t mf_dn_word(const uint4 (&v)[G / 64], int i, int ww) {
+    const uint4& s = G == 128 ? v[i] : v[0];
+    const int c = G == 128 ? ww : 2 * i + ww;
+    return c == 0 ? s.x : c == 1 ? s.y : c == 2 ? s.z : s.w;
+}
+// g = 128: load i is group i, lane quarter q has its words 4q .. 4q + 3.
+// g = 64: the load holds groups 0 and 1 (lane quarter q has group q >> 1);
+// after the swaps (x, y) are group 0's words of the quarter, (z, w) group 1's.
+template <int G>
+__device__ __forceinline__ void mf_dn_arrange(uint4 (&v)[G / 64]) {
+    if constexpr (G == 64) {
+        swap32(v[0].x, v[0].z);
+        swap32(v[0].y, v[0].w);
+    }
+}
+
+template <int G, int MT, int TPW>
+__device__ __forceinline__ void mf_dn_step(MfDnBuf<G, TPW>& q, const uint4* hsb, const float2* cxb, int ntile,
+                                           int lane, f32x4_t (&Y)[TPW]) {
+    constexpr int QW = G / 32, WPG = G / 8;
+    const uint32_t mv = magic_vgpr();
+    const int qt = lane >> 4;
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+        if (tt < ntile) {
+#pragma unroll
+            for (int i = 0; i < G / 64; ++i) pin4(q.c[tt][i]);
+            mf_dn_arrange<G>(q.c[tt]);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < kDnSteps; ++i) {
+        const float2* cl = cxb + i * MT + 4 * (qt & (MT / 4 - 1));
+        const float2 k0 = cl[0], k1 = cl[1], k2 = cl[2], k3 = cl[3];
+#pragma unroll
+        for (int tt = 0; tt < TPW; ++tt) {
+            if (tt < ntile) {
+                const uint32_t mw = i == 0 ? q.m[tt].x : q.m[tt].y;
+                const float z = h2f(mw >> 16);
+                f32x4_t acc = {z * k0.y + k0.x, z * k1.y + k1.x, z * k2.y + k2.x, z * k3.y + k3.x};
+#pragma unroll
+                for (int ww = 0; ww < QW; ++ww) {
+                    uint32_t e[4];
+                    extract_w4_s1(mf_dn_word<G>(q.c[tt], i, ww), e, mv);
+                    acc = mfma16(hsb[(i * WPG + ww) * MT], make_uint4(e[0], e[1], e[2], e[3]), acc);
+                }
+                Y[tt] += h2f(mw & 0xFFFFu) * acc;
+            }
+        }
+    }
+}
+
+// h' staging: each thread holds SPT 16-byte words of a chunk between
+// issuing their loads and writing them to LDS.
+template <int SPT>
+struct MfStage {
+    uint4 v[SPT];
+};
+
+// ck: codes of f per staged chunk (a multiple of 2 G, with MT ck / 8 <= SPT NT).
+template <int G, int MT, int TPW, int NW, int SPT>
+__global__ void __launch_bounds__(NW * 64) mf_dn_kernel(BatchArgs b, int nb, int ck) {
+    constexpr int NT = NW * 64, GW = G / 8, QW = G / 32;
+    const int d = b.d, f = b.f, M = b.M;
+    const int nsteps = f / (G * kDnSteps);
+    const int sc = ck / (G * kDnSteps);                   // steps per chunk
+    const int nchunk = (nsteps + sc - 1) / sc;
+    const int ckw = ck / 8, ckg = ck / G;                 // words and groups per chunk row
+    extern __shared__ uint4 smem[];
+    uint4* hs = smem;                                                     // [2][ckw][MT]
+    float2* cx = reinterpret_cast<float2*>(smem + 2 * ckw * MT);          // [2][ckg][MT]
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int ipb = d / 16;
+    const int qt = lane >> 4, jj = (lane & 15) & (MT - 1);
+    const int qoff = quarter_word<QW>(qt) * MT + jj;
+
+    const int nit = nb * ipb;
+    const int i0 = (int)((long)blockIdx.x * nit / gridDim.x), i1 = (int)((long)(blockIdx.x + 1) * nit / gridDim.x);
+    MfStage<SPT> sb;
+    // this thread's staging words of a chunk: word sW of token sj (sj >= MT:
+    // past the chunk)
+    int sj[SPT], sW[SPT];
+#pragma unroll
+    for (int s = 0; s < SPT; ++s) {
+        const int idx = tid + s * NT;
+        sj[s] = idx / ckw;
+        sW[s] = idx - sj[s] * ckw;
+    }
+    for (int seg = i0; seg < i1;) {
+        const int l = seg / ipb;
+        const int send = (l + 1) * ipb < i1 ? (l + 1) * ipb : i1;
+        const int first = seg + wave;
+        const int ntile = first < send ? (send - first + NW - 1) / NW : 0;     // <= TPW (host)
+        const uint16_t* hl = b.h + (long)l * M * f;
+        // h' of chunk c: thread word s is word sW[s] of token sj[s]; padding
+        // tokens and words past a short last chunk load from outside the
+        // resource (zeros) and are dropped
+        const Rsrc rh = rsrc(b.h + (long)l * M * f, (uint32_t)M * (uint32_t)f * 2u);
+        auto chunk_words = [&](int c) { return ((c + 1) * ck <= f ? ck : f - c * ck) / 8; };
+        auto stage_issue = [&](int c) {
+            const int cw = chunk_words(c);
+#pragma unroll
+            for (int s = 0; s < SPT; ++s) {
+                const bool data = sj[s] < M && sW[s] < cw;
+                const uint32_t vo = data ? (uint32_t)(sj[s] * f + 8 * sW[s]) * 2u : 0x80000000u;
+                sb.v[s] = bload16<0>(rh, vo, (uint32_t)(c * ck) * 2u);
+            }
+        };
+        auto stage_commit = [&](int c) {
+            uint4* hb = hs + (c & 1) * ckw * MT;
+            float2* cb = cx + (c & 1) * ckg * MT;
+            const int cw = chunk_words(c);
+#pragma unroll
+            for (int s = 0; s < SPT; ++s)
+                if (s * NT < MT * ckw)                    // uniform: the workgroup's last words
+                    mf_stage_word4<MT, GW>(hb, cb, sW[s], sj[s], sj[s] < MT && sW[s] < cw, sb.v[s]);
+        };
+        lds_barrier();                                     // the previous segment is done with LDS
+        stage_issue(0);
+        stage_commit(0);
+        f32x4_t Y[TPW];
+#pragma unroll
+        for (int tt = 0; tt < TPW; ++tt) Y[tt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        const int row0 = (first - l * ipb) * 16;
+        MfDnBuf<G, TPW> A, B;
+        mf_dn_load<G, TPW>(A, l, row0, 16 * NW, ntile, 0, d, f, false, lane);
+        int kin = 0, cbuf = 0, cnext = 1;
+        auto body = [&](MfDnBuf<G, TPW>& cur, MfDnBuf<G, TPW>& nxt, int k) {
+            // at a chunk's first step: chunk cnext - 1 is in LDS (every wave
+            // waited for its own writes) and chunk cnext - 2 is consumed, so
+            // chunk cnext is loaded now (after the next step's prefetch) and
+            // written after this step's work
+            const bool stg = kin == 0 && cnext < nchunk;
+            if (kin == 0)
+                lds_barrier();
+            const bool more = k + 1 < nsteps;
+            mf_dn_load<G, TPW>(nxt, l, row0, 16 * NW, ntile, more ? k + 1 : k, d, f, !more, lane);
+            if (stg)
+                stage_issue(cnext);
+            mf_dn_step<G, MT, TPW>(cur, hs + cbuf * ckw * MT + kin * kDnSteps * (G / 8) * MT + qoff,
+                                   cx + cbuf * ckg * MT + kin * kDnSteps * MT, ntile, lane, Y);
+            if (stg)
+                stage_commit(cnext);
+            if (kin == 0)
+                ++cnext;
+            if (++kin == sc) {
+                kin = 0;
+                cbuf ^= 1;
+            }
+        };
+        for (int k = 0; k < nsteps; k += 2) {
+            body(A, B, k);
+            if (k + 1 < nsteps)
+                body(B, A, k + 1);
+        }
+        // y of the wave's items: D[token 4 q + v][row lane & 15]
+#pragma unroll
+        for (int tt = 0; tt < TPW; ++tt) {
+            if (tt < ntile) {
+                const int o = row0 + tt * 16 * NW + (lane & 15);
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int tok = 4 * qt + v;
+                    if (tok < M)
+                        b.y[((long)l * M + tok) * d + o] = (uint16_t)f2h(Y[tt][v]);
+                }
+            }
+        }
+        seg = send;
+    }
+}
+
+int mf_cu_count() {
+    static int cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 0;
+    if (cache[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
+
+constexpr size_t kMfLds = 160 * 1024;
+
+int mf_mt(int M) { return M <= 4 ? 4 : M <= 8 ? 8 : 16; }
+
+size_t mf_gu_lds(int d, int g, int MT) {
+    return (size_t)(d / 16) * 2 * MT * 16 + (size_t)(d / g) * MT * 8 + 2 * MT * 32 * 2;
+}
+size_t mf_dn_lds(int ck, int g, int MT) { return (size_t)2 * (ck / 8) * MT * 16 + (size_t)2 * (ck / g) * MT * 8; }
+// Items per wave a down kernel is built for: the fewest of the built
+// counts (1 or 3 at g = 128, 2 or 5 at g = 64) covering tpw.
+int mf_dn_tpw_built(int g, int tpw) { return g == 128 ? (tpw <= 1 ? 1 : 3) : (tpw <= 2 ? 2 : 5); }
+// Staged h' words per thread and chunk (registers left beside TPW items).
+constexpr int mf_dn_spt(int tpw_built) { return tpw_built >= 5 ? 2 : 4; }
+// Codes per staged h' chunk: the largest multiple of 2 g whose MT tokens fit
+// the staging registers of the workgroup and whose two buffers fit in LDS,
+// no larger than f rounded up to a step.
+int mf_dn_chunk(int f, int g, int MT, int spt) {
+    const int step = kDnSteps * g;
+    int ck = spt * kMfWaves * 64 * 8 / MT / step * step;
+    while (ck > step && mf_dn_lds(ck, g, MT) > kMfLds) ck -= step;
+    const int fr = (f + step - 1) / step * step;
+    return ck < fr ? ck : fr;
+}
+int mf_grid(long items) {
+    const long c = mf_cu_count();
+    return (int)(items < c ? items : c);
+}
+// Most items any wave of the down launch holds.
+int mf_dn_tiles(int nb, int d) {
+    const long nit = (long)nb * (d / 16);
+    const long grid = mf_grid(nit);
+    if (grid <= 0)
+        return 1 << 30;
+    const long per = (nit + grid - 1) / grid;
+    return (int)((per + kMfWaves - 1) / kMfWaves);
+}
+// Items per wave the down kernel is built for (register budget of two-group
+// steps at 12 waves).
+int mf_dn_tpw_max(int g) { return g == 64 ? 5 : 3; }
+
+}  // namespace
+
+bool mfma_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r, int nb) {
+    if (M < 3 || M > 16 || bg != 2 || bd != 4 || (gg != 64 && gg != 128) || (gd != 64 && gd != 128))
+        return false;
+    if (r != 0 && r != 8 && r != 16 && r != 32)
+        return false;
+    if (nb < 1 || nb > kBatchMax || d % (4 * gg) != 0 || f % (2 * gd) != 0 || d % 16 != 0 || f % 16 != 0)
+        return false;
+    if (mf_cu_count() <= 0)
+        return false;
+    const int MT = mf_mt(M);
+    const int tpw = mf_dn_tiles(nb, d);
+    if (tpw > mf_dn_tpw_max(gd))
+        return false;
+    const int ck = mf_dn_chunk(f, gd, MT, mf_dn_spt(mf_dn_tpw_built(gd, tpw)));
+    return mf_gu_lds(d, gg, MT) <= kMfLds && mf_dn_lds(ck, gd, MT) <= kMfLds;
+}
+
+#define QMLP_MFGU(G_, MT_)                                                                \
+    if (b.gg == G_ && MT == MT_) {                                                        \
+        auto k = mf_gu_kernel<G_, MT_, kMfWaves>;                                         \
+        hipError_t e = set_lds(k, lds);                                                   \
+        if (e != hipSuccess) return e;                                                    \
+        k<<<grid, kMfWaves * 64, lds, st>>>(b, nb);                                       \
+        return hipGetLastError();                                                         \
+    }
+
+hipError_t launch_gateup_mfma(const BatchArgs& b, int nb, hipStream_t st) {
+    if (!mfma_supported(b.M, b.d, b.f, b.gg, b.bg, b.gd, b.bd, b.r, nb))
+        return hipErrorInvalidValue;
+    const int MT = mf_mt(b.M);
+    const int grid = mf_grid((long)nb * (b.f / 16));
+    const size_t lds = mf_gu_lds(b.d, b.gg, MT);
+    QMLP_MFGU(64, 4) QMLP_MFGU(64, 8) QMLP_MFGU(64, 16)
+    QMLP_MFGU(128, 4) QMLP_MFGU(128, 8) QMLP_MFGU(128, 16)
+    return hipErrorInvalidValue;
+}
+
+#define QMLP_MFDN(G_, MT_, TPW_)                                                          \
+    if (b.gd == G_ && MT == MT_ && tpwb == TPW_) {                                        \
+        auto k = mf_dn_kernel<G_, MT_, TPW_, kMfWaves, mf_dn_spt(TPW_)>;                  \
+        hipError_t e = set_lds(k, lds);                                                   \
+        if (e != hipSuccess) return e;                                                    \
+        k<<<grid, kMfWaves * 64, lds, st>>>(b, nb, ck);                                   \
+        return hipGetLastError();                                                         \
+    }
+
+hipError_t launch_down_mfma(const BatchArgs& b, int nb, hipStream_t st) {
+    if (!mfma_supported(b.M, b.d, b.f, b.gg, b.bg, b.gd, b.bd, b.r, nb))
+        return hipErrorInvalidValue;
+    const int MT = mf_mt(b.M);
+    const int grid = mf_grid((long)nb * (b.d / 16));
+    const int tpwb = mf_dn_tpw_built(b.gd, mf_dn_tiles(nb, b.d));
+    const int ck = mf_dn_chunk(b.f, b.gd, MT, mf_dn_spt(tpwb));
+    const size_t lds = mf_dn_lds(ck, b.gd, MT);
+    QMLP_MFDN(64, 4, 2) QMLP_MFDN(64, 4, 5) QMLP_MFDN(64, 8, 2) QMLP_MFDN(64, 8, 5)
+    QMLP_MFDN(64, 16, 2) QMLP_MFDN(64, 16, 5)
+    QMLP_MFDN(128, 4, 1) QMLP_MFDN(128, 4, 3) QMLP_MFDN(128, 8, 1) QMLP_MFDN(128, 8, 3)
+    QMLP_MFDN(128, 16, 1) QMLP_MFDN(128, 16, 3)
+    return hipErrorInvalidValue;
+}
+
+}  // namespace qmlp

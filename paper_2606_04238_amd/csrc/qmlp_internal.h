@@ -126,6 +126,14 @@ hipError_t launch_lora_a_batch(const BatchArgs& b, int nb, hipStream_t st);
 bool stream_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r, int nb);
 hipError_t launch_gateup_stream(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_down_stream(const BatchArgs& b, int nb, hipStream_t st);
+// The matrix-core path of a batch at 3..16 tokens (decode_mfma.hip): one
+// persistent gate/up launch and one persistent down launch over all blocks
+// of the batch, after launch_lora_a_batch.  Binary16, 2-bit gate/up and
+// 4-bit down at groups 64/128, rank 0/8/16/32, d % (4 g) == 0,
+// f % (2 g_down) == 0 (plus the LDS and items-per-wave limits it checks).
+bool mfma_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r, int nb);
+hipError_t launch_gateup_mfma(const BatchArgs& b, int nb, hipStream_t st);
+hipError_t launch_down_mfma(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_gateup_batch(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_down_batch(const BatchArgs& b, int nb, hipStream_t st);
 // y[m] = sum_j w[m k + j] * yi[m k + j] over the k routed experts of token m

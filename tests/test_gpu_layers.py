@@ -189,14 +189,16 @@ def test_layers_qwen3_8b_match_oracle(q):
     _check(layers, y)
 
 
-@pytest.mark.parametrize("M,L", [(4, 3), (13, 5), (2, 41)])
-def test_layers_batched_shapes_match_oracle(q, M, L):
-    """Shapes outside the streamed path (M > 1) run in batches of up to
-    40 blocks on the stand-alone kernels (LoRA-A, gate/up and down of every
-    block of a batch); 41 blocks take two batches that reuse t and h."""
-    small = wl.Config("layers_m%d" % M, M=M, d=512, f=1536, g=64, r=8, L=L)
-    _announce("layers batched", small.name, "L", L)
+@pytest.mark.parametrize("M,L,d", [(2, 3, 512), (2, 41, 512), (4, 3, 640), (13, 5, 640)])
+def test_layers_batched_shapes_match_oracle(q, M, L, d):
+    """Shapes outside the streamed and matrix-core paths (M = 2, or d not a
+    multiple of four groups) run in batches of up to 40 blocks on the
+    stand-alone kernels (LoRA-A, gate/up and down of every block of a
+    batch); 41 blocks take two batches that reuse t and h."""
+    small = wl.Config("layers_m%d" % M, M=M, d=d, f=1536, g=64, r=8, L=L)
+    _announce("layers batched", small.name, "d", d, "L", L)
     layers, mlps, ls, x = _blocks(q, small, L)
+    assert q.layers_path(ls, M) == "batched"
     assert q.layers_launches(ls, M) == 3 * ((L + 39) // 40)
     y = q.forward_layers(ls, x)
     torch.cuda.synchronize()
@@ -268,3 +270,63 @@ def test_layers_streamed_shapes_match_oracle(q, d, f, g, r, L):
     y = q.forward_layers(ls, x)
     torch.cuda.synchronize()
     _check(layers, y, rank=r > 0, which=None if L <= 9 else (0, 1, L // 2, L - 2, L - 1))
+
+
+@pytest.mark.parametrize("M,d,f,g,r,L", [
+    (3, 512, 1536, 64, 8, 1),       # the fewest tokens, one block: fewer items than compute units
+    (4, 512, 1280, 128, 16, 3),     # MT = 4, f a multiple of 2 g but not of the h' chunk
+    (5, 768, 1536, 64, 0, 9),       # MT = 8, no adapter
+    (8, 1024, 2048, 128, 32, 40),   # a full batch: ranges straddle blocks
+    (9, 512, 1536, 64, 16, 41),     # MT = 16, two batches
+    (16, 2048, 3072, 64, 8, 6),     # all sixteen token rows
+])
+def test_layers_mfma_shapes_match_oracle(q, M, d, f, g, r, L):
+    """3 <= M <= 16 runs on the matrix cores (LoRA-A, then one gate/up and
+    one down launch per batch): token counts on both sides of each padded
+    tile height (4, 8, 16), groups 64 and 128, ranks 0 to 32, batches from
+    one block to two batches.  Every block against the oracle (sampled for
+    long batches) and against the stand-alone kernels on the same input."""
+    cfg = wl.Config("mfma_m%d_%d_%d" % (M, d, f), M=M, d=d, f=f, g=g, r=r, L=L)
+    _announce("layers mfma", cfg.name, "g", g, "r", r, "L", L)
+    layers, mlps, ls, x = _blocks(q, cfg, L, rank=r > 0)
+    assert q.layers_path(ls, M) == "mfma"
+    assert q.layers_launches(ls, M) == (3 if r > 0 else 2) * ((L + 39) // 40)
+    ws = q.layers_workspace(ls, M)
+    y = q.forward_layers(ls, x, ws=ws)
+    yb = q.forward_batch(ls, x)
+    torch.cuda.synchronize()
+    errs = _check(layers, y, rank=r > 0, which=None if L <= 9 else (0, 1, L // 2, L - 2, L - 1))
+    print("max-rel errors:", {k: "%.2e" % v for k, v in errs.items()})
+    assert orc.max_rel_err(values_of(y), values_of(yb)) <= Y_TOL
+    assert np.isfinite(values_of(y)).all()
+    # a second call on the same workspace repeats the bits
+    y2 = q.forward_layers(ls, x, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
+
+
+@pytest.mark.parametrize("name", ["qwen3_8b_m4", "qwen3_8b_m16", "dense14b_m8"])
+def test_layers_mfma_full_depth_sampled(q, name):
+    """The benchmark's several-token workloads in its launch configuration:
+    every block of the model (36 or 40, each with its own weights and input)
+    in one qmlp_forward_layers call on the matrix cores; the first, middle
+    and last blocks against the oracle, every block against the stand-alone
+    kernels on its input."""
+    import concurrent.futures
+    cfg = wl.CONFIGS[name]
+    _announce("layers mfma full depth", cfg.name, "M", cfg.M, "L", cfg.L)
+    with concurrent.futures.ThreadPoolExecutor(max_workers=8) as ex:
+        layers = list(ex.map(lambda i: wl.layer(cfg, i, 0), range(cfg.L)))
+    mlps = [gpu_mlp(lay) for lay in layers]
+    x = torch.stack([act_tensor(lay.x) for lay in layers])
+    ls = q.Layers(mlps)
+    assert q.layers_path(ls, cfg.M) == "mfma" and q.layers_launches(ls, cfg.M) == 3
+    ws = q.layers_workspace(ls, cfg.M)
+    y = q.forward_layers(ls, x, ws=ws)
+    yb = q.forward_batch(ls, x)
+    torch.cuda.synchronize()
+    errs = _check(layers, y, which=(0, cfg.L // 2, cfg.L - 1))
+    print("max-rel errors:", {k: "%.2e" % v for k, v in errs.items()})
+    worst = max(orc.max_rel_err(values_of(y[i]), values_of(yb[i])) for i in range(cfg.L))
+    print("max-rel vs stand-alone kernels: %.2e" % worst)
+    assert worst <= Y_TOL
