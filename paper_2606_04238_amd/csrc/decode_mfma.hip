@@ -101,7 +101,6 @@ __device__ __forceinline__ uint2 bload8(Rsrc r, uint32_t voff, uint32_t soff) {
 }
 
 constexpr int kMfWaves = 12;   // waves per workgroup (one workgroup per compute unit)
-constexpr int kSteps = 4;      // gate/up: groups per streamed step
 
 // First word, within a group, of the words that lane quarter q multiplies:
 // 2-bit g = 64 (one word each): q; 2-bit g = 128 and 4-bit g = 64 (two words
@@ -173,25 +172,31 @@ __device__ __forceinline__ void mf_stage_word4(uint4* hs, float2* cx, int W, int
 }
 
 // ---------------------------------------------------------------- gate/up
-// One step (four groups) of an item: NL = G / 64 loads per matrix.
+// One step of an item: 128 bytes of each of its 16 rows per matrix (512
+// codes, GSU = 512 / G groups) in two loads, and the rows' (scale | zero)
+// words of those groups (MW = GSU / 4 loads).
 template <int G>
 struct MfGuBuf {
-    static constexpr int NL = G / 64;
-    uint4 cg[NL], cu[NL];
-    uint4 mg, mu;            // the row's (scale | zero) words of the four groups
+    static constexpr int GSU = 512 / G, MW = GSU / 4;
+    uint4 cg[2], cu[2];
+    uint4 mg[MW], mu[MW];
     uint4 bg, bu;            // LoRA-B ranks 8 q .. 8 q + 7 of the row (last step of an item)
 };
 
+__device__ __forceinline__ uint32_t word_of(const uint4& v, int i) {
+    return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+}
+
 // Step c of the item whose first row is row n of block l.  Lane: row
-// n + (lane & 15); load i covers bytes [64 i + 16 q, + 16) of the step's
-// 64 NL bytes of the row.  A prefetch past a wave's last step (dummy), and
-// the LoRA-B rows on every step but an item's last, load from empty
-// resources.  The (scale | zero) words are plain loads: a row's 128-byte
-// line of them serves several steps.
+// n + (lane & 15); load i covers bytes [64 i + 16 q, + 16) of the row's 128
+// bytes of the step, so the two loads of a matrix fetch whole lines.  A
+// prefetch past a wave's last step (dummy), and the LoRA-B rows on every
+// step but an item's last, load from empty resources.  The (scale | zero)
+// words are plain loads: a row's line of them serves several steps.
 template <int G>
 __device__ __forceinline__ void mf_gu_load(MfGuBuf<G>& q, int l, int n, int c, int nsb, int d, int f, int r,
                                            bool dummy, int lane) {
-    constexpr int NL = G / 64;
+    constexpr int GSU = 512 / G, MW = GSU / 4;
     KBatchM* kb = kbm();
     const int qt = lane >> 4, lr = lane & 15;
     const int ng = d / G, rw = d / 16;
@@ -200,15 +205,18 @@ __device__ __forceinline__ void mf_gu_load(MfGuBuf<G>& q, int l, int n, int c, i
     const Rsrc rg = rsrc(kb->lay[l].cg, cbytes), ru = rsrc(kb->lay[l].cu, cbytes);
     const Rsrc sg = rsrc(kb->lay[l].mg, mbytes), su = rsrc(kb->lay[l].mu, mbytes);
     const uint32_t cv = (uint32_t)(lr * rw + 4 * qt) * 4u;
-    const uint32_t cs = (uint32_t)(n * rw + c * kSteps * (G / 16)) * 4u;
+    const uint32_t cs = (uint32_t)(n * rw + c * 32) * 4u;
 #pragma unroll
-    for (int i = 0; i < NL; ++i) {
+    for (int i = 0; i < 2; ++i) {
         q.cg[i] = bload16<kAuxNt>(rg, cv + 64 * i, cs);
         q.cu[i] = bload16<kAuxNt>(ru, cv + 64 * i, cs);
     }
-    const uint32_t mv = (uint32_t)(lr * ng) * 4u, ms = (uint32_t)(n * ng + c * kSteps) * 4u;
-    q.mg = bload16<0>(sg, mv, ms);
-    q.mu = bload16<0>(su, mv, ms);
+    const uint32_t mv = (uint32_t)(lr * ng) * 4u, ms = (uint32_t)(n * ng + c * GSU) * 4u;
+#pragma unroll
+    for (int i = 0; i < MW; ++i) {
+        q.mg[i] = bload16<0>(sg, mv + 16 * i, ms);
+        q.mu[i] = bload16<0>(su, mv + 16 * i, ms);
+    }
     const bool lora = !dummy && c == nsb - 1 && r > 0;
     const uint32_t bbytes = lora ? (uint32_t)f * (uint32_t)r * 2u : 0u;
     const Rsrc bg = rsrc(kb->lay[l].Bg, bbytes), bu = rsrc(kb->lay[l].Bu, bbytes);
@@ -217,24 +225,23 @@ __device__ __forceinline__ void mf_gu_load(MfGuBuf<G>& q, int l, int n, int c, i
     q.bu = bload16<0>(bu, bv, bs);
 }
 
-// Words of group i (0..3) of the step for this lane, after redistribution.
+// Words of group i (0 .. GSU - 1) of the step for this lane (QW = G / 64
+// each), after redistribution between lane quarters.
 template <int G>
-__device__ __forceinline__ void mf_gu_words(uint4 (&v)[G / 64], uint32_t (&w)[4][G / 64]) {
-    if constexpr (G == 64) {
-        // one load holds four groups: lane quarter q has group q; transpose
-        uint32_t a = v[0].x, b = v[0].y, c = v[0].z, e = v[0].w;
+__device__ __forceinline__ void mf_gu_words(uint4 (&v)[2], uint32_t (&w)[512 / G][G / 64]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        uint32_t a = v[i].x, b = v[i].y, c = v[i].z, e = v[i].w;
         swap32(a, c);
         swap32(b, e);
-        swap16(a, b);
-        swap16(c, e);
-        w[0][0] = a; w[1][0] = b; w[2][0] = c; w[3][0] = e;
-    } else {
-        // load i holds groups 2i, 2i + 1: lane quarter q has group 2i + (q >> 1)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            uint32_t a = v[i].x, b = v[i].y, c = v[i].z, e = v[i].w;
-            swap32(a, c);
-            swap32(b, e);
+        if constexpr (G == 64) {
+            // load i holds groups 4i .. 4i + 3, lane quarter q has group 4i + q:
+            // a 4 x 4 transpose between quarters
+            swap16(a, b);
+            swap16(c, e);
+            w[4 * i][0] = a; w[4 * i + 1][0] = b; w[4 * i + 2][0] = c; w[4 * i + 3][0] = e;
+        } else {
+            // load i holds groups 2i, 2i + 1, lane quarter q has group 2i + (q >> 1)
             w[2 * i][0] = a; w[2 * i][1] = b;
             w[2 * i + 1][0] = c; w[2 * i + 1][1] = e;
         }
@@ -244,26 +251,25 @@ __device__ __forceinline__ void mf_gu_words(uint4 (&v)[G / 64], uint32_t (&w)[4]
 template <int G, int MT>
 __device__ __forceinline__ void mf_gu_step(MfGuBuf<G>& q, const uint4* xsb, const float2* cxb, int c, int lane,
                                            f32x4_t& G4, f32x4_t& U4) {
-    constexpr int QW = G / 64, WPG = G / 16;
+    constexpr int QW = G / 64, WPG = G / 16, GSU = 512 / G;
     const uint32_t mv = magic_vgpr();
     const int qt = lane >> 4;
 #pragma unroll
-    for (int i = 0; i < G / 64; ++i) {
+    for (int i = 0; i < 2; ++i) {
         pin4(q.cg[i]);
         pin4(q.cu[i]);
     }
-    uint32_t wg[4][QW], wu[4][QW];
+    uint32_t wg[GSU][QW], wu[GSU][QW];
     mf_gu_words<G>(q.cg, wg);
     mf_gu_words<G>(q.cu, wu);
-    const uint32_t mgw[4] = {q.mg.x, q.mg.y, q.mg.z, q.mg.w};
-    const uint32_t muw[4] = {q.mu.x, q.mu.y, q.mu.z, q.mu.w};
 #pragma unroll
-    for (int i = 0; i < kSteps; ++i) {
-        const int t = c * kSteps + i;
+    for (int i = 0; i < GSU; ++i) {
+        const int t = c * GSU + i;
+        const uint32_t mgi = word_of(q.mg[i / 4], i % 4), mui = word_of(q.mu[i / 4], i % 4);
         // (-C, -X) of the tokens of this lane's D rows, 4 (q & (MT/4 - 1)) .. + 3
         const float2* cl = cxb + t * MT + 4 * (qt & (MT / 4 - 1));
         const float2 k0 = cl[0], k1 = cl[1], k2 = cl[2], k3 = cl[3];
-        const float zg = h2f(mgw[i] >> 16), zu = h2f(muw[i] >> 16);
+        const float zg = h2f(mgi >> 16), zu = h2f(mui >> 16);
         f32x4_t ag = {zg * k0.y + k0.x, zg * k1.y + k1.x, zg * k2.y + k2.x, zg * k3.y + k3.x};
         f32x4_t au = {zu * k0.y + k0.x, zu * k1.y + k1.x, zu * k2.y + k2.x, zu * k3.y + k3.x};
 #pragma unroll
@@ -279,8 +285,8 @@ __device__ __forceinline__ void mf_gu_step(MfGuBuf<G>& q, const uint4* xsb, cons
                 au = mfma16(a, make_uint4(eu[4 * h], eu[4 * h + 1], eu[4 * h + 2], eu[4 * h + 3]), au);
             }
         }
-        G4 += h2f(mgw[i] & 0xFFFFu) * ag;
-        U4 += h2f(muw[i] & 0xFFFFu) * au;
+        G4 += h2f(mgi & 0xFFFFu) * ag;
+        U4 += h2f(mui & 0xFFFFu) * au;
     }
 }
 
@@ -288,7 +294,7 @@ template <int G, int MT, int NW>
 __global__ void __launch_bounds__(NW * 64) mf_gu_kernel(BatchArgs b, int nb) {
     constexpr int NT = NW * 64, GW = G / 16, QW = G / 64;
     const int d = b.d, f = b.f, r = b.r, M = b.M;
-    const int nsb = d / (G * kSteps);                     // steps per item
+    const int nsb = d / 512;                              // steps per item
     const int NWd = d / 16;                               // 16-code words per row
     extern __shared__ uint4 smem[];
     uint4* xs = smem;                                                    // [NWd][2][MT]
@@ -393,24 +399,35 @@ __global__ void __launch_bounds__(NW * 64) mf_gu_kernel(BatchArgs b, int nb) {
 }
 
 // ---------------------------------------------------------------- down
-constexpr int kDnSteps = 2;    // down: groups per streamed step
-
-// One step (two groups) of TPW items: NL = G / 64 loads per item.
+// One step of TPW items: 128 bytes of each row (256 codes, GSD = 256 / G
+// groups) in two loads per item, and the rows' (scale | zero) words of those
+// groups.
+template <int G>
+struct MfDnMeta;
+template <>
+struct MfDnMeta<128> {
+    typedef uint2 type;       // two groups
+};
+template <>
+struct MfDnMeta<64> {
+    typedef uint4 type;       // four groups
+};
 template <int G, int TPW>
 struct MfDnBuf {
-    static constexpr int NL = G / 64;
-    uint4 c[TPW][NL];
-    uint2 m[TPW];            // the row's (scale | zero) words of the two groups
+    uint4 c[TPW][2];
+    typename MfDnMeta<G>::type m[TPW];
 };
 
+__device__ __forceinline__ uint32_t word_of(const uint2& v, int i) { return i == 0 ? v.x : v.y; }
+
 // Step k of the wave's items: item tt has its first row at row0 + tt * srow.
-// Load i of an item covers bytes [64 i + 16 q, + 16) of the step's 64 NL
-// bytes of the row.  Items at or past ntile, and a prefetch past the last
-// step, load from empty resources.
+// Load i of an item covers bytes [64 i + 16 q, + 16) of the row's 128 bytes
+// of the step.  Items at or past ntile, and a prefetch past the last step,
+// load from empty resources.
 template <int G, int TPW>
 __device__ __forceinline__ void mf_dn_load(MfDnBuf<G, TPW>& q, int l, int row0, int srow, int ntile, int k, int d,
                                            int f, bool dummy, int lane) {
-    constexpr int NL = G / 64;
+    constexpr int GSD = 256 / G;
     KBatchM* kb = kbm();
     const int qt = lane >> 4, lr = lane & 15, ng = f / G, rw = f / 8;
     const uint32_t cv = (uint32_t)(lr * rw + 4 * qt) * 4u, mv = (uint32_t)(lr * ng) * 4u;
@@ -420,54 +437,62 @@ __device__ __forceinline__ void mf_dn_load(MfDnBuf<G, TPW>& q, int l, int row0, 
         const Rsrc rc = rsrc(kb->lay[l].cd, real ? (uint32_t)d * (uint32_t)(f / 2) : 0u);
         const Rsrc rm = rsrc(kb->lay[l].md, real ? (uint32_t)d * (uint32_t)ng * 4u : 0u);
         const int row = row0 + tt * srow;
-        const uint32_t cs = (uint32_t)(row * rw + k * kDnSteps * (G / 8)) * 4u;
+        const uint32_t cs = (uint32_t)(row * rw + k * 32) * 4u, ms = (uint32_t)(row * ng + k * GSD) * 4u;
 #pragma unroll
-        for (int i = 0; i < NL; ++i) q.c[tt][i] = bload16<kAuxNt>(rc, cv + 64 * i, cs);
-        q.m[tt] = bload8(rm, mv, (uint32_t)(row * ng + k * kDnSteps) * 4u);
+        for (int i = 0; i < 2; ++i) q.c[tt][i] = bload16<kAuxNt>(rc, cv + 64 * i, cs);
+        if constexpr (G == 128)
+            q.m[tt] = bload8(rm, mv, ms);
+        else
+            q.m[tt] = bload16<0>(rm, mv, ms);
     }
 }
 
-// Word ww (0 .. G/32 - 1) of group i (0, 1) of the step for this lane, from
-// the item's loads after mf_dn_arrange.
+// Word ww (0 .. G/32 - 1) of group i (0 .. GSD - 1) of the step for this
+// lane, from the item's loads after mf_dn_arrange.
+//   g = 128: load i is group i, lane quarter q has its words 4q .. 4q + 3.
+//   g = 64: load i holds groups 2i, 2i + 1 (lane quarter q has group
+//   2i + (q >> 1)); after the swaps (x, y) are group 2i's words of the
+//   quarter, (z, w) group 2i + 1's.
 template <int G>
-__device__ __forceinline__ uint32_t mf_dn_word(const uint4 (&v)[G / 64], int i, int ww) {
-    const uint4& s = G == 128 ? v[i] : v[0];
-    const int c = G == 128 ? ww : 2 * i + ww;
-    return c == 0 ? s.x : c == 1 ? s.y : c == 2 ? s.z : s.w;
+__device__ __forceinline__ uint32_t mf_dn_word(const uint4 (&v)[2], int i, int ww) {
+    if constexpr (G == 128)
+        return word_of(v[i], ww);
+    else
+        return word_of(v[i >> 1], 2 * (i & 1) + ww);
 }
-// g = 128: load i is group i, lane quarter q has its words 4q .. 4q + 3.
-// g = 64: the load holds groups 0 and 1 (lane quarter q has group q >> 1);
-// after the swaps (x, y) are group 0's words of the quarter, (z, w) group 1's.
 template <int G>
-__device__ __forceinline__ void mf_dn_arrange(uint4 (&v)[G / 64]) {
+__device__ __forceinline__ void mf_dn_arrange(uint4 (&v)[2]) {
     if constexpr (G == 64) {
-        swap32(v[0].x, v[0].z);
-        swap32(v[0].y, v[0].w);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            swap32(v[i].x, v[i].z);
+            swap32(v[i].y, v[i].w);
+        }
     }
 }
 
 template <int G, int MT, int TPW>
 __device__ __forceinline__ void mf_dn_step(MfDnBuf<G, TPW>& q, const uint4* hsb, const float2* cxb, int ntile,
                                            int lane, f32x4_t (&Y)[TPW]) {
-    constexpr int QW = G / 32, WPG = G / 8;
+    constexpr int QW = G / 32, WPG = G / 8, GSD = 256 / G;
     const uint32_t mv = magic_vgpr();
     const int qt = lane >> 4;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
         if (tt < ntile) {
-#pragma unroll
-            for (int i = 0; i < G / 64; ++i) pin4(q.c[tt][i]);
+            pin4(q.c[tt][0]);
+            pin4(q.c[tt][1]);
             mf_dn_arrange<G>(q.c[tt]);
         }
     }
 #pragma unroll
-    for (int i = 0; i < kDnSteps; ++i) {
+    for (int i = 0; i < GSD; ++i) {
         const float2* cl = cxb + i * MT + 4 * (qt & (MT / 4 - 1));
         const float2 k0 = cl[0], k1 = cl[1], k2 = cl[2], k3 = cl[3];
 #pragma unroll
         for (int tt = 0; tt < TPW; ++tt) {
             if (tt < ntile) {
-                const uint32_t mw = i == 0 ? q.m[tt].x : q.m[tt].y;
+                const uint32_t mw = word_of(q.m[tt], i);
                 const float z = h2f(mw >> 16);
                 f32x4_t acc = {z * k0.y + k0.x, z * k1.y + k1.x, z * k2.y + k2.x, z * k3.y + k3.x};
 #pragma unroll
@@ -489,13 +514,13 @@ struct MfStage {
     uint4 v[SPT];
 };
 
-// ck: codes of f per staged chunk (a multiple of 2 G, with MT ck / 8 <= SPT NT).
+// ck: codes of f per staged chunk (a multiple of 256, with MT ck / 8 <= SPT NT).
 template <int G, int MT, int TPW, int NW, int SPT>
 __global__ void __launch_bounds__(NW * 64) mf_dn_kernel(BatchArgs b, int nb, int ck) {
     constexpr int NT = NW * 64, GW = G / 8, QW = G / 32;
     const int d = b.d, f = b.f, M = b.M;
-    const int nsteps = f / (G * kDnSteps);
-    const int sc = ck / (G * kDnSteps);                   // steps per chunk
+    const int nsteps = f / 256;
+    const int sc = ck / 256;                              // steps per chunk
     const int nchunk = (nsteps + sc - 1) / sc;
     const int ckw = ck / 8, ckg = ck / G;                 // words and groups per chunk row
     extern __shared__ uint4 smem[];
@@ -519,12 +544,15 @@ __global__ void __launch_bounds__(NW * 64) mf_dn_kernel(BatchArgs b, int nb, int
         sj[s] = idx / ckw;
         sW[s] = idx - sj[s] * ckw;
     }
+    // Segments: the range's items of one block, in rounds of at most TPW
+    // items per wave, each round a full walk over f.
     for (int seg = i0; seg < i1;) {
         const int l = seg / ipb;
-        const int send = (l + 1) * ipb < i1 ? (l + 1) * ipb : i1;
+        const int bend = (l + 1) * ipb < i1 ? (l + 1) * ipb : i1;
+        const int rounds = (bend - seg + TPW * NW - 1) / (TPW * NW);
+        const int send = seg + (bend - seg + rounds - 1) / rounds;
         const int first = seg + wave;
-        const int ntile = first < send ? (send - first + NW - 1) / NW : 0;     // <= TPW (host)
-        const uint16_t* hl = b.h + (long)l * M * f;
+        const int ntile = first < send ? (send - first + NW - 1) / NW : 0;     // <= TPW
         // h' of chunk c: thread word s is word sW[s] of token sj[s]; padding
         // tokens and words past a short last chunk load from outside the
         // resource (zeros) and are dropped
@@ -548,7 +576,7 @@ __global__ void __launch_bounds__(NW * 64) mf_dn_kernel(BatchArgs b, int nb, int
                 if (s * NT < MT * ckw)                    // uniform: the workgroup's last words
                     mf_stage_word4<MT, GW>(hb, cb, sW[s], sj[s], sj[s] < MT && sW[s] < cw, sb.v[s]);
         };
-        lds_barrier();                                     // the previous segment is done with LDS
+        lds_barrier();                                     // the previous round is done with LDS
         stage_issue(0);
         stage_commit(0);
         f32x4_t Y[TPW];
@@ -570,8 +598,8 @@ __global__ void __launch_bounds__(NW * 64) mf_dn_kernel(BatchArgs b, int nb, int
             mf_dn_load<G, TPW>(nxt, l, row0, 16 * NW, ntile, more ? k + 1 : k, d, f, !more, lane);
             if (stg)
                 stage_issue(cnext);
-            mf_dn_step<G, MT, TPW>(cur, hs + cbuf * ckw * MT + kin * kDnSteps * (G / 8) * MT + qoff,
-                                   cx + cbuf * ckg * MT + kin * kDnSteps * MT, ntile, lane, Y);
+            mf_dn_step<G, MT, TPW>(cur, hs + cbuf * ckw * MT + kin * 32 * MT + qoff,
+                                   cx + cbuf * ckg * MT + kin * (256 / G) * MT, ntile, lane, Y);
             if (stg)
                 stage_commit(cnext);
             if (kin == 0)
@@ -625,37 +653,23 @@ size_t mf_gu_lds(int d, int g, int MT) {
     return (size_t)(d / 16) * 2 * MT * 16 + (size_t)(d / g) * MT * 8 + 2 * MT * 32 * 2;
 }
 size_t mf_dn_lds(int ck, int g, int MT) { return (size_t)2 * (ck / 8) * MT * 16 + (size_t)2 * (ck / g) * MT * 8; }
-// Items per wave a down kernel is built for: the fewest of the built
-// counts (1 or 3 at g = 128, 2 or 5 at g = 64) covering tpw.
-int mf_dn_tpw_built(int g, int tpw) { return g == 128 ? (tpw <= 1 ? 1 : 3) : (tpw <= 2 ? 2 : 5); }
-// Staged h' words per thread and chunk (registers left beside TPW items).
-constexpr int mf_dn_spt(int tpw_built) { return tpw_built >= 5 ? 2 : 4; }
-// Codes per staged h' chunk: the largest multiple of 2 g whose MT tokens fit
+constexpr int kDnTpw = 3;        // down: items per wave and round
+// down: staged h' words per thread and chunk (registers left beside the
+// items' loads: those of g = 64 carry twice the (scale | zero) words)
+constexpr int mf_stage_words(int g) { return g == 64 ? 2 : 4; }
+// Codes per staged h' chunk: the largest multiple of 256 whose MT tokens fit
 // the staging registers of the workgroup and whose two buffers fit in LDS,
 // no larger than f rounded up to a step.
-int mf_dn_chunk(int f, int g, int MT, int spt) {
-    const int step = kDnSteps * g;
-    int ck = spt * kMfWaves * 64 * 8 / MT / step * step;
-    while (ck > step && mf_dn_lds(ck, g, MT) > kMfLds) ck -= step;
-    const int fr = (f + step - 1) / step * step;
+int mf_dn_chunk(int f, int g, int MT) {
+    int ck = mf_stage_words(g) * kMfWaves * 64 * 8 / MT / 256 * 256;
+    while (ck > 256 && mf_dn_lds(ck, g, MT) > kMfLds) ck -= 256;
+    const int fr = (f + 255) / 256 * 256;
     return ck < fr ? ck : fr;
 }
 int mf_grid(long items) {
     const long c = mf_cu_count();
     return (int)(items < c ? items : c);
 }
-// Most items any wave of the down launch holds.
-int mf_dn_tiles(int nb, int d) {
-    const long nit = (long)nb * (d / 16);
-    const long grid = mf_grid(nit);
-    if (grid <= 0)
-        return 1 << 30;
-    const long per = (nit + grid - 1) / grid;
-    return (int)((per + kMfWaves - 1) / kMfWaves);
-}
-// Items per wave the down kernel is built for (register budget of two-group
-// steps at 12 waves).
-int mf_dn_tpw_max(int g) { return g == 64 ? 5 : 3; }
 
 }  // namespace
 
@@ -664,16 +678,12 @@ bool mfma_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r, 
         return false;
     if (r != 0 && r != 8 && r != 16 && r != 32)
         return false;
-    if (nb < 1 || nb > kBatchMax || d % (4 * gg) != 0 || f % (2 * gd) != 0 || d % 16 != 0 || f % 16 != 0)
+    if (nb < 1 || nb > kBatchMax || d % 512 != 0 || f % 256 != 0)
         return false;
     if (mf_cu_count() <= 0)
         return false;
     const int MT = mf_mt(M);
-    const int tpw = mf_dn_tiles(nb, d);
-    if (tpw > mf_dn_tpw_max(gd))
-        return false;
-    const int ck = mf_dn_chunk(f, gd, MT, mf_dn_spt(mf_dn_tpw_built(gd, tpw)));
-    return mf_gu_lds(d, gg, MT) <= kMfLds && mf_dn_lds(ck, gd, MT) <= kMfLds;
+    return mf_gu_lds(d, gg, MT) <= kMfLds && mf_dn_lds(mf_dn_chunk(f, gd, MT), gd, MT) <= kMfLds;
 }
 
 #define QMLP_MFGU(G_, MT_)                                                                \
@@ -696,9 +706,9 @@ hipError_t launch_gateup_mfma(const BatchArgs& b, int nb, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
-#define QMLP_MFDN(G_, MT_, TPW_)                                                          \
-    if (b.gd == G_ && MT == MT_ && tpwb == TPW_) {                                        \
-        auto k = mf_dn_kernel<G_, MT_, TPW_, kMfWaves, mf_dn_spt(TPW_)>;                  \
+#define QMLP_MFDN(G_, MT_)                                                                \
+    if (b.gd == G_ && MT == MT_) {                                                        \
+        auto k = mf_dn_kernel<G_, MT_, kDnTpw, kMfWaves, mf_stage_words(G_)>;             \
         hipError_t e = set_lds(k, lds);                                                   \
         if (e != hipSuccess) return e;                                                    \
         k<<<grid, kMfWaves * 64, lds, st>>>(b, nb, ck);                                   \
@@ -710,13 +720,10 @@ hipError_t launch_down_mfma(const BatchArgs& b, int nb, hipStream_t st) {
         return hipErrorInvalidValue;
     const int MT = mf_mt(b.M);
     const int grid = mf_grid((long)nb * (b.d / 16));
-    const int tpwb = mf_dn_tpw_built(b.gd, mf_dn_tiles(nb, b.d));
-    const int ck = mf_dn_chunk(b.f, b.gd, MT, mf_dn_spt(tpwb));
+    const int ck = mf_dn_chunk(b.f, b.gd, MT);
     const size_t lds = mf_dn_lds(ck, b.gd, MT);
-    QMLP_MFDN(64, 4, 2) QMLP_MFDN(64, 4, 5) QMLP_MFDN(64, 8, 2) QMLP_MFDN(64, 8, 5)
-    QMLP_MFDN(64, 16, 2) QMLP_MFDN(64, 16, 5)
-    QMLP_MFDN(128, 4, 1) QMLP_MFDN(128, 4, 3) QMLP_MFDN(128, 8, 1) QMLP_MFDN(128, 8, 3)
-    QMLP_MFDN(128, 16, 1) QMLP_MFDN(128, 16, 3)
+    QMLP_MFDN(64, 4) QMLP_MFDN(64, 8) QMLP_MFDN(64, 16)
+    QMLP_MFDN(128, 4) QMLP_MFDN(128, 8) QMLP_MFDN(128, 16)
     return hipErrorInvalidValue;
 }
 
