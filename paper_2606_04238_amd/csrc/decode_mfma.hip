@@ -102,15 +102,63 @@ __device__ __forceinline__ uint2 bload8(Rsrc r, uint32_t voff, uint32_t soff) {
 
 constexpr int kMfWaves = 12;   // waves per workgroup (one workgroup per compute unit)
 
-// First word, within a group, of the words that lane quarter q multiplies:
-// 2-bit g = 64 (one word each): q; 2-bit g = 128 and 4-bit g = 64 (two words
-// each, after the 32-lane swap): 4 (q & 1) + 2 (q >> 1); 4-bit g = 128 (four
-// words, loaded in place): 4 q.
+// Whole-line loads.  A step reads 128 bytes (eight 16-byte units) of each of
+// 16 weight rows; each load instruction covers 8 rows whole (lane L: row
+// 8 h + (L & 7) for load h, unit u(L) from lane bits 5..3), so every 128-byte
+// line is fetched by one instruction.  The matrix cores want lane l = 16 q + j
+// to hold row j, so the units are then moved between lanes in registers: with
+// the row bit h exchanged for lane bit 3 (E3, a row rotation by 8 under a
+// bank mask), the 4-byte words of a unit u = (u2 u1 u0), w = (w1 w0) sit at
+// register (u2 after E3) and component (w1 w0); E4 exchanges lane bit 4 with
+// component bit w1 (v_permlane16_swap) and E5 lane bit 5 with w0
+// (v_permlane32_swap).  Which unit bit each lane bit carries is chosen per
+// layout so that a quarter's words of one group end up in the same register
+// positions for every group (QW words per quarter and group):
+//   2-bit g = 128, 4-bit g = 64 (E3, E4): lane bits 5, 4, 3 = u0, u1, u2;
+//     quarter q holds words 2q, 2q + 1 of a group;
+//   2-bit g = 64 (E3, E4, E5): same units; quarter q holds word
+//     2 (q & 1) + (q >> 1) of each group;
+//   4-bit g = 128 (E3): lane bits 5, 4, 3 = u1, u0, u2; quarter q holds
+//     words 4q .. 4q + 3.
 template <int QW>
 __device__ __forceinline__ int quarter_word(int q) {
-    if constexpr (QW == 1) return q;
-    else if constexpr (QW == 2) return 4 * (q & 1) + 2 * (q >> 1);
+    if constexpr (QW == 1) return 2 * (q & 1) + (q >> 1);
+    else if constexpr (QW == 2) return 2 * q;
     else return 4 * q;
+}
+// 16-byte unit of the step's 128 bytes that lane L loads.
+template <bool DN128>
+__device__ __forceinline__ int lane_unit(int L) {
+    const int b5 = (L >> 5) & 1, b4 = (L >> 4) & 1, b3 = (L >> 3) & 1;
+    return DN128 ? 4 * b3 + 2 * b5 + b4 : 4 * b3 + 2 * b4 + b5;
+}
+constexpr int kDppRowRor8 = 0x128;
+// E3 on one component: a (h = 0) and b (h = 1) become the S3 = 0 and S3 = 1
+// halves, rows 8..15 taken from lane l ^ 8.
+__device__ __forceinline__ void e3(uint32_t& a, uint32_t& b) {
+    const int na = __builtin_amdgcn_update_dpp((int)a, (int)b, kDppRowRor8, 0xF, 0xC, false);
+    const int nb = __builtin_amdgcn_update_dpp((int)b, (int)a, kDppRowRor8, 0xF, 0x3, false);
+    a = (uint32_t)na;
+    b = (uint32_t)nb;
+}
+// The exchanges of a step's two loads: E3 always, E4 and E5 as asked.
+template <bool E4, bool E5>
+__device__ __forceinline__ void arrange(uint4 (&v)[2]) {
+    e3(v[0].x, v[1].x);
+    e3(v[0].y, v[1].y);
+    e3(v[0].z, v[1].z);
+    e3(v[0].w, v[1].w);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        if constexpr (E4) {
+            swap16(v[i].x, v[i].z);
+            swap16(v[i].y, v[i].w);
+        }
+        if constexpr (E5) {
+            swap32(v[i].x, v[i].y);
+            swap32(v[i].z, v[i].w);
+        }
+    }
 }
 
 // ---------------------------------------------------------------- staging
@@ -187,12 +235,12 @@ __device__ __forceinline__ uint32_t word_of(const uint4& v, int i) {
     return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
 }
 
-// Step c of the item whose first row is row n of block l.  Lane: row
-// n + (lane & 15); load i covers bytes [64 i + 16 q, + 16) of the row's 128
-// bytes of the step, so the two loads of a matrix fetch whole lines.  A
-// prefetch past a wave's last step (dummy), and the LoRA-B rows on every
-// step but an item's last, load from empty resources.  The (scale | zero)
-// words are plain loads: a row's line of them serves several steps.
+// Step c of the item whose first row is row n of block l: the two
+// whole-line loads per matrix (rows n + 8 i + (lane & 7)), and for lane row
+// n + (lane & 15) its (scale | zero) words and LoRA-B ranks.  A prefetch
+// past a wave's last step (dummy), and the LoRA-B rows on every step but an
+// item's last, load from empty resources.  The (scale | zero) words are
+// plain loads: a row's line of them serves several steps.
 template <int G>
 __device__ __forceinline__ void mf_gu_load(MfGuBuf<G>& q, int l, int n, int c, int nsb, int d, int f, int r,
                                            bool dummy, int lane) {
@@ -204,12 +252,12 @@ __device__ __forceinline__ void mf_gu_load(MfGuBuf<G>& q, int l, int n, int c, i
     const uint32_t mbytes = dummy ? 0u : (uint32_t)f * (uint32_t)ng * 4u;
     const Rsrc rg = rsrc(kb->lay[l].cg, cbytes), ru = rsrc(kb->lay[l].cu, cbytes);
     const Rsrc sg = rsrc(kb->lay[l].mg, mbytes), su = rsrc(kb->lay[l].mu, mbytes);
-    const uint32_t cv = (uint32_t)(lr * rw + 4 * qt) * 4u;
+    const uint32_t cv = (uint32_t)((lane & 7) * rw) * 4u + 16u * (uint32_t)lane_unit<false>(lane);
     const uint32_t cs = (uint32_t)(n * rw + c * 32) * 4u;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-        q.cg[i] = bload16<kAuxNt>(rg, cv + 64 * i, cs);
-        q.cu[i] = bload16<kAuxNt>(ru, cv + 64 * i, cs);
+        q.cg[i] = bload16<kAuxNt>(rg, cv + (uint32_t)(8 * i * rw) * 4u, cs);
+        q.cu[i] = bload16<kAuxNt>(ru, cv + (uint32_t)(8 * i * rw) * 4u, cs);
     }
     const uint32_t mv = (uint32_t)(lr * ng) * 4u, ms = (uint32_t)(n * ng + c * GSU) * 4u;
 #pragma unroll
@@ -226,24 +274,17 @@ __device__ __forceinline__ void mf_gu_load(MfGuBuf<G>& q, int l, int n, int c, i
 }
 
 // Words of group i (0 .. GSU - 1) of the step for this lane (QW = G / 64
-// each), after redistribution between lane quarters.
+// each) from the arranged loads.
 template <int G>
 __device__ __forceinline__ void mf_gu_words(uint4 (&v)[2], uint32_t (&w)[512 / G][G / 64]) {
+    arrange<true, G == 64>(v);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        uint32_t a = v[i].x, b = v[i].y, c = v[i].z, e = v[i].w;
-        swap32(a, c);
-        swap32(b, e);
-        if constexpr (G == 64) {
-            // load i holds groups 4i .. 4i + 3, lane quarter q has group 4i + q:
-            // a 4 x 4 transpose between quarters
-            swap16(a, b);
-            swap16(c, e);
-            w[4 * i][0] = a; w[4 * i + 1][0] = b; w[4 * i + 2][0] = c; w[4 * i + 3][0] = e;
-        } else {
-            // load i holds groups 2i, 2i + 1, lane quarter q has group 2i + (q >> 1)
-            w[2 * i][0] = a; w[2 * i][1] = b;
-            w[2 * i + 1][0] = c; w[2 * i + 1][1] = e;
+    for (int g = 0; g < 512 / G; ++g) {
+        if constexpr (G == 64)
+            w[g][0] = word_of(v[g >> 2], g & 3);
+        else {
+            w[g][0] = word_of(v[g >> 1], 2 * (g & 1));
+            w[g][1] = word_of(v[g >> 1], 2 * (g & 1) + 1);
         }
     }
 }
@@ -420,17 +461,18 @@ struct MfDnBuf {
 
 __device__ __forceinline__ uint32_t word_of(const uint2& v, int i) { return i == 0 ? v.x : v.y; }
 
-// Step k of the wave's items: item tt has its first row at row0 + tt * srow.
-// Load i of an item covers bytes [64 i + 16 q, + 16) of the row's 128 bytes
-// of the step.  Items at or past ntile, and a prefetch past the last step,
-// load from empty resources.
+// Step k of the wave's items: item tt has its first row at row0 + tt * srow;
+// its two whole-line loads cover rows + 8 i + (lane & 7), its (scale | zero)
+// words are lane row + (lane & 15)'s.  Items at or past ntile, and a
+// prefetch past the last step, load from empty resources.
 template <int G, int TPW>
 __device__ __forceinline__ void mf_dn_load(MfDnBuf<G, TPW>& q, int l, int row0, int srow, int ntile, int k, int d,
                                            int f, bool dummy, int lane) {
     constexpr int GSD = 256 / G;
     KBatchM* kb = kbm();
-    const int qt = lane >> 4, lr = lane & 15, ng = f / G, rw = f / 8;
-    const uint32_t cv = (uint32_t)(lr * rw + 4 * qt) * 4u, mv = (uint32_t)(lr * ng) * 4u;
+    const int lr = lane & 15, ng = f / G, rw = f / 8;
+    const uint32_t cv = (uint32_t)((lane & 7) * rw) * 4u + 16u * (uint32_t)lane_unit<G == 128>(lane);
+    const uint32_t mv = (uint32_t)(lr * ng) * 4u;
 #pragma unroll
     for (int tt = 0; tt < TPW; ++tt) {
         const bool real = !dummy && tt < ntile;
@@ -439,7 +481,7 @@ __device__ __forceinline__ void mf_dn_load(MfDnBuf<G, TPW>& q, int l, int row0, 
         const int row = row0 + tt * srow;
         const uint32_t cs = (uint32_t)(row * rw + k * 32) * 4u, ms = (uint32_t)(row * ng + k * GSD) * 4u;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) q.c[tt][i] = bload16<kAuxNt>(rc, cv + 64 * i, cs);
+        for (int i = 0; i < 2; ++i) q.c[tt][i] = bload16<kAuxNt>(rc, cv + (uint32_t)(8 * i * rw) * 4u, cs);
         if constexpr (G == 128)
             q.m[tt] = bload8(rm, mv, ms);
         else
@@ -448,11 +490,8 @@ __device__ __forceinline__ void mf_dn_load(MfDnBuf<G, TPW>& q, int l, int row0, 
 }
 
 // Word ww (0 .. G/32 - 1) of group i (0 .. GSD - 1) of the step for this
-// lane, from the item's loads after mf_dn_arrange.
-//   g = 128: load i is group i, lane quarter q has its words 4q .. 4q + 3.
-//   g = 64: load i holds groups 2i, 2i + 1 (lane quarter q has group
-//   2i + (q >> 1)); after the swaps (x, y) are group 2i's words of the
-//   quarter, (z, w) group 2i + 1's.
+// lane, from the item's loads after mf_dn_arrange: g = 128, register i,
+// components ww; g = 64, register i >> 1, components 2 (i & 1) + ww.
 template <int G>
 __device__ __forceinline__ uint32_t mf_dn_word(const uint4 (&v)[2], int i, int ww) {
     if constexpr (G == 128)
@@ -462,13 +501,7 @@ __device__ __forceinline__ uint32_t mf_dn_word(const uint4 (&v)[2], int i, int w
 }
 template <int G>
 __device__ __forceinline__ void mf_dn_arrange(uint4 (&v)[2]) {
-    if constexpr (G == 64) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            swap32(v[i].x, v[i].z);
-            swap32(v[i].y, v[i].w);
-        }
-    }
+    arrange<G == 64, false>(v);
 }
 
 template <int G, int MT, int TPW>
