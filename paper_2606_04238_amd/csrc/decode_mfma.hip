@@ -163,7 +163,9 @@ __device__ __forceinline__ void arrange(uint4 (&v)[2]) {
 
 // ---------------------------------------------------------------- staging
 // Staging word W (16 values) of token j of an activation into x' halves
-// (pairs (x[p], x[8 + p]), pre-scaled; layout [W][half][MT]) and the
+// (pairs (x[p], x[8 + p]), pre-scaled; layout [W][half][MT] with one pad
+// entry per word, so that the lanes writing consecutive words hit distinct
+// LDS banks) and the
 // (-C, -X) of its group (GW words per group on GW consecutive lanes; every
 // lane of the wave calls this).
 template <int MT, int GW>
@@ -186,15 +188,17 @@ __device__ __forceinline__ void mf_stage_word(uint4* xs, float2* cx, int W, int 
     csum = group_sum<GW>(csum);
     xsum = group_sum<GW>(xsum);
     if (live) {
-        xs[(W * 2) * MT + j] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
-        xs[(W * 2 + 1) * MT + j] = make_uint4(pr[4], pr[5], pr[6], pr[7]);
+        xs[W * (2 * MT + 1) + j] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
+        xs[W * (2 * MT + 1) + MT + j] = make_uint4(pr[4], pr[5], pr[6], pr[7]);
         if (W % GW == 0)
             cx[(W / GW) * MT + j] = make_float2(-1024.0f * csum, -xsum);
     }
 }
 
 // 4-bit words: 8 values of token j (one 16-byte load) as pairs (h[p], h[4 + p])
-// pre-scaled for the positions {0, 4, 0, 4}; layout [W][MT]; GW words per group.
+// pre-scaled for the positions {0, 4, 0, 4}; layout [W][MT + 1] (the pad makes
+// the 16 lanes that write consecutive words of one token hit distinct LDS
+// banks); GW words per group.
 template <int MT, int GW>
 __device__ __forceinline__ void mf_stage_word4(uint4* hs, float2* cx, int W, int j, bool live, const uint4& v) {
     const uint32_t hl[4] = {v.x, v.y, v.z, v.w};
@@ -213,7 +217,7 @@ __device__ __forceinline__ void mf_stage_word4(uint4* hs, float2* cx, int W, int
     csum = group_sum<GW>(csum);
     xsum = group_sum<GW>(xsum);
     if (live) {
-        hs[W * MT + j] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
+        hs[W * (MT + 1) + j] = make_uint4(pr[0], pr[1], pr[2], pr[3]);
         if (W % GW == 0)
             cx[(W / GW) * MT + j] = make_float2(-1024.0f * csum, -xsum);
     }
@@ -321,7 +325,7 @@ __device__ __forceinline__ void mf_gu_step(MfGuBuf<G>& q, const uint4* xsb, cons
             const int W = t * WPG + w;                         // plus the lane's quarter offset (in xsb)
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const uint4 a = xsb[(W * 2 + h) * MT];
+                const uint4 a = xsb[W * (2 * MT + 1) + h * MT];
                 ag = mfma16(a, make_uint4(eg[4 * h], eg[4 * h + 1], eg[4 * h + 2], eg[4 * h + 3]), ag);
                 au = mfma16(a, make_uint4(eu[4 * h], eu[4 * h + 1], eu[4 * h + 2], eu[4 * h + 3]), au);
             }
@@ -338,8 +342,8 @@ __global__ void __launch_bounds__(NW * 64) mf_gu_kernel(BatchArgs b, int nb) {
     const int nsb = d / 512;                              // steps per item
     const int NWd = d / 16;                               // 16-code words per row
     extern __shared__ uint4 smem[];
-    uint4* xs = smem;                                                    // [NWd][2][MT]
-    float2* cx = reinterpret_cast<float2*>(smem + NWd * 2 * MT);          // [d/G][MT]
+    uint4* xs = smem;                                                    // [NWd][2 MT + 1]
+    float2* cx = reinterpret_cast<float2*>(smem + NWd * (2 * MT + 1));    // [d/G][MT]
     uint16_t* tsg = reinterpret_cast<uint16_t*>(cx + (d / G) * MT);       // [MT][32] lora_scale t_g
     uint16_t* tsu = tsg + MT * 32;                                       // [MT][32] lora_scale t_u
     const int tid = threadIdx.x, lane = tid & 63;
@@ -382,7 +386,7 @@ __global__ void __launch_bounds__(NW * 64) mf_gu_kernel(BatchArgs b, int nb) {
         const int nk = first < send ? (send - first + NW - 1) / NW : 0;
         const int nsteps = nk * nsb;
         if (nsteps > 0) {
-            const uint4* xsb = xs + quarter_word<QW>(qt) * 2 * MT + jj;     // this lane's A base
+            const uint4* xsb = xs + quarter_word<QW>(qt) * (2 * MT + 1) + jj;   // this lane's A base
             int ld_item = first, ld_c = 0, left = nsteps - 1;
             int cp_item = first, cp_c = 0;
             auto advance = [&]() {
@@ -532,7 +536,7 @@ __device__ __forceinline__ void mf_dn_step(MfDnBuf<G, TPW>& q, const uint4* hsb,
                 for (int ww = 0; ww < QW; ++ww) {
                     uint32_t e[4];
                     extract_w4_s1(mf_dn_word<G>(q.c[tt], i, ww), e, mv);
-                    acc = mfma16(hsb[(i * WPG + ww) * MT], make_uint4(e[0], e[1], e[2], e[3]), acc);
+                    acc = mfma16(hsb[(i * WPG + ww) * (MT + 1)], make_uint4(e[0], e[1], e[2], e[3]), acc);
                 }
                 Y[tt] += h2f(mw & 0xFFFFu) * acc;
             }
@@ -557,13 +561,13 @@ __global__ void __launch_bounds__(NW * 64) mf_dn_kernel(BatchArgs b, int nb, int
     const int nchunk = (nsteps + sc - 1) / sc;
     const int ckw = ck / 8, ckg = ck / G;                 // words and groups per chunk row
     extern __shared__ uint4 smem[];
-    uint4* hs = smem;                                                     // [2][ckw][MT]
-    float2* cx = reinterpret_cast<float2*>(smem + 2 * ckw * MT);          // [2][ckg][MT]
+    uint4* hs = smem;                                                     // [2][ckw][MT + 1]
+    float2* cx = reinterpret_cast<float2*>(smem + 2 * ckw * (MT + 1));    // [2][ckg][MT]
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int ipb = d / 16;
     const int qt = lane >> 4, jj = (lane & 15) & (MT - 1);
-    const int qoff = quarter_word<QW>(qt) * MT + jj;
+    const int qoff = quarter_word<QW>(qt) * (MT + 1) + jj;
 
     const int nit = nb * ipb;
     const int i0 = (int)((long)blockIdx.x * nit / gridDim.x), i1 = (int)((long)(blockIdx.x + 1) * nit / gridDim.x);
@@ -601,7 +605,7 @@ __global__ void __launch_bounds__(NW * 64) mf_dn_kernel(BatchArgs b, int nb, int
             }
         };
         auto stage_commit = [&](int c) {
-            uint4* hb = hs + (c & 1) * ckw * MT;
+            uint4* hb = hs + (c & 1) * ckw * (MT + 1);
             float2* cb = cx + (c & 1) * ckg * MT;
             const int cw = chunk_words(c);
 #pragma unroll
@@ -631,7 +635,7 @@ __global__ void __launch_bounds__(NW * 64) mf_dn_kernel(BatchArgs b, int nb, int
             mf_dn_load<G, TPW>(nxt, l, row0, 16 * NW, ntile, more ? k + 1 : k, d, f, !more, lane);
             if (stg)
                 stage_issue(cnext);
-            mf_dn_step<G, MT, TPW>(cur, hs + cbuf * ckw * MT + kin * 32 * MT + qoff,
+            mf_dn_step<G, MT, TPW>(cur, hs + cbuf * ckw * (MT + 1) + kin * 32 * (MT + 1) + qoff,
                                    cx + cbuf * ckg * MT + kin * (256 / G) * MT, ntile, lane, Y);
             if (stg)
                 stage_commit(cnext);
@@ -683,9 +687,11 @@ constexpr size_t kMfLds = 160 * 1024;
 int mf_mt(int M) { return M <= 4 ? 4 : M <= 8 ? 8 : 16; }
 
 size_t mf_gu_lds(int d, int g, int MT) {
-    return (size_t)(d / 16) * 2 * MT * 16 + (size_t)(d / g) * MT * 8 + 2 * MT * 32 * 2;
+    return (size_t)(d / 16) * (2 * MT + 1) * 16 + (size_t)(d / g) * MT * 8 + 2 * MT * 32 * 2;
 }
-size_t mf_dn_lds(int ck, int g, int MT) { return (size_t)2 * (ck / 8) * MT * 16 + (size_t)2 * (ck / g) * MT * 8; }
+size_t mf_dn_lds(int ck, int g, int MT) {
+    return (size_t)2 * (ck / 8) * (MT + 1) * 16 + (size_t)2 * (ck / g) * MT * 8;
+}
 constexpr int kDnTpw = 3;        // down: items per wave and round
 // down: staged h' words per thread and chunk (registers left beside the
 // items' loads: those of g = 64 carry twice the (scale | zero) words)
