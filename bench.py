@@ -517,7 +517,7 @@ def moe_main(mc: wl.MoeConfig, args):
     import oracle as orc
     import paper_2606_04238_amd as q
     cfg = mc.block
-    L, E, k, M = 24, mc.experts, mc.topk, cfg.M
+    L, E, k, M = cfg.L, mc.experts, mc.topk, cfg.M
     routes = [wl.routing(M, E, k, l, args.seed) for l in range(L)]
     widths = {"w4_uniform": (4, 4, False), "w2_uniform": (2, 2, False),
               "w4w2_gateup_lora": (2, 4, True)}

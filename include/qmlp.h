@@ -249,6 +249,14 @@ qmlp_status qmlp_forward_stack(const qmlp_mlp *layers, int L, const void *x, int
                                qmlp_dtype dtype, void *y, void *x_out, void *ws, size_t ws_bytes,
                                qmlp_stream stream);
 
+/* Byte offset, within a qmlp_forward_stack workspace, of the persistent
+ * launch's sticky error word (a uint32: 1/2/4 = a wait for the activation /
+ * h / the cross-XCD partials gave up, 8 = a workgroup had no place; the
+ * word is cleared by the caller when it zeroes the workspace and never by
+ * the library); 0 if these blocks do not run persistently or the call would
+ * be rejected.  Host-only. */
+size_t qmlp_stack_error_offset(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
+
 /* Launches qmlp_forward_stack makes: the number of persistent launches when
  * the stack runs persistently, else the per-layer kernels plus the norm and
  * residual-add kernels; 0 if the call would be rejected.  Host-only. */
@@ -356,6 +364,18 @@ size_t qmlp_moe_workspace_bytes(const qmlp_mlp *experts, int E, int M, int k, qm
 qmlp_status qmlp_forward_moe(const qmlp_mlp *experts, int E, const void *x, int M,
                              qmlp_dtype dtype, const int32_t *topk_idx, const float *topk_w, int k,
                              void *y, void *ws, size_t ws_bytes, qmlp_stream stream);
+
+/* Launch shape of qmlp_forward_moe's weight launches at one token over
+ * `instances` routed expert instances (M k) of a [d][f] expert, on a device
+ * with `cus` compute units: the lanes per row of the gate/up launch
+ * (gu_bits 2 or 4) and of the down launch (dn_bits 2 or 4).  A few
+ * instances leave the chip with fewer than two workgroups per compute unit
+ * at the usual choice, so the lanes per row double (more, shorter rows per
+ * workgroup) until it has them.  Returns 1 when down takes the pipelined
+ * kernel, 0 the plain one, -1 for arguments outside d, f > 0 and multiples
+ * of 64, 1 <= instances <= 40, cus >= 1, non-null outputs.  Host-only. */
+int qmlp_moe_lanes(int d, int f, int gu_bits, int dn_bits, int instances, int cus,
+                   int *gu_lanes, int *dn_lanes);
 
 /* ---------------------------------------------- inspection (not timed) */
 

@@ -78,6 +78,8 @@ def _lib():
             "qmlp_stack_workspace_bytes": (Z, [pm, I, I, I]),
             "qmlp_forward_stack": (I, [pm, I, P, I, I, P, P, P, Z, P]),
             "qmlp_stack_launches": (I, [pm, I, I, I]),
+            "qmlp_stack_error_offset": (Z, [pm, I, I, I]),
+            "qmlp_moe_lanes": (I, [I, I, I, I, I, I, ctypes.POINTER(I), ctypes.POINTER(I)]),
             "qmlp_layers_workspace_bytes": (Z, [pm, I, I, I]),
             "qmlp_forward_layers": (I, [pm, I, P, I, I, P, P, Z, P]),
             "qmlp_layers_launches": (I, [pm, I, I, I]),
@@ -419,6 +421,17 @@ def moe_workspace_bytes(experts: Layers, M: int, k: int, dtype=torch.float16) ->
     return int(_lib().qmlp_moe_workspace_bytes(experts.c(), len(experts), M, k, code))
 
 
+def moe_lanes(d: int, f: int, gu_bits: int, dn_bits: int, instances: int, cus: int):
+    """(gate/up lanes per row, down lanes per row, down pipelined) of
+    qmlp_forward_moe's launches over `instances` routed expert instances on
+    `cus` compute units (qmlp_moe_lanes; host-only)."""
+    g, dn = ctypes.c_int(0), ctypes.c_int(0)
+    r = int(_lib().qmlp_moe_lanes(d, f, gu_bits, dn_bits, instances, cus, ctypes.byref(g), ctypes.byref(dn)))
+    if r < 0:
+        raise ValueError("qmlp_moe_lanes rejected its arguments")
+    return g.value, dn.value, bool(r)
+
+
 def forward_moe(experts: Layers, x: torch.Tensor, topk_idx: torch.Tensor, topk_w: torch.Tensor,
                 y: torch.Tensor | None = None, ws: torch.Tensor | None = None) -> torch.Tensor:
     """y [M][d] = sum_j topk_w[m][j] * expert_{topk_idx[m][j]}(x[m]); topk_idx int32
@@ -458,16 +471,11 @@ def stack_workspace(stack: Stack, M: int, dtype=torch.float16, device="cuda") ->
 def stack_errors(stack: Stack, ws: torch.Tensor, M: int = 1, dtype=torch.float16) -> int:
     """Sticky error bits of the persistent stack launch (syncs): 1/2/4 = a wait for
     the activation / h / the cross-XCD partials gave up, 8 = a workgroup had no place."""
-    base = stack_workspace_bytes(stack, M, dtype) - _stack_area_bytes(stack)
-    return int(ws[base + 256: base + 260].view(torch.int32).item())
-
-
-def _stack_area_bytes(stack: Stack) -> int:
-    m = stack.mlps[0]
-    d, f, r = m.d, m.f, m.rank
-    xw = d + d // 4 + 2 * (2 * r + 1) * 32
-    rnd = lambda v: (v + 255) // 256 * 256  # noqa: E731
-    return 1024 + rnd(8 * xw * 4) + rnd(f * 4) + 2 * 8 * d * 8
+    code = F16 if dtype == torch.float16 else BF16
+    off = int(_lib().qmlp_stack_error_offset(stack.c(), len(stack), M, code))
+    if off == 0:
+        return 0
+    return int(ws[off: off + 4].view(torch.int32).item())
 
 
 def forward_stack(stack: Stack, x: torch.Tensor, y: torch.Tensor | None = None,

@@ -579,6 +579,13 @@ size_t qmlp_stack_workspace_bytes(const qmlp_mlp* layers, int L, int M, qmlp_dty
     return n;
 }
 
+size_t qmlp_stack_error_offset(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
+    if (check_stack(layers, L, M, dtype) != QMLP_OK || M == 0 || !stack_persistent(layers, M, dtype))
+        return 0;
+    return stack_layer_ws(layers, M, dtype) + 3 * round256((size_t)M * layers[0].gate.k_in * 2) +
+           stack_error_word_offset();
+}
+
 int qmlp_stack_launches(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
     if (check_stack(layers, L, M, dtype) != QMLP_OK || M == 0)
         return 0;

@@ -30,6 +30,23 @@ hipError_t launch_down_batch(const BatchArgs& b, int nb, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
+}  // namespace qmlp
+
+extern "C" int qmlp_moe_lanes(int d, int f, int gu_bits, int dn_bits, int instances, int cus,
+                              int* gu_lanes, int* dn_lanes) {
+    using namespace qmlp;
+    if (d <= 0 || f <= 0 || instances < 1 || instances > kBatchMax || cus < 1 || !gu_lanes || !dn_lanes ||
+        (gu_bits != 2 && gu_bits != 4) || (dn_bits != 2 && dn_bits != 4) || d % 64 != 0 || f % 64 != 0)
+        return -1;
+    *gu_lanes = routed_gateup_lanes(d / codes_per_unit(gu_bits), f, instances, gu_bits, cus);
+    const int Ud = f / codes_per_unit(dn_bits);
+    const bool pipe = down_pipe_fits_shape(d, f, 1, instances, dn_bits);
+    *dn_lanes = pipe ? routed_pipe_lanes(Ud, d, instances, cus) : instances > 1 ? lanes_fewest(Ud) : lanes_for(Ud, dn_bits);
+    return pipe ? 1 : 0;
+}
+
+namespace qmlp {
+
 // One thread per output element: the routing-weighted sum of the k expert
 // outputs of its token (Sec. 5 names the routed experts of the MoE decoder;
 // the weights come with the routing).

@@ -46,17 +46,12 @@ hipError_t launch_gateup_batch(const BatchArgs& b, int nb, hipStream_t st) {
     if (nb < 1 || nb > kBatchMax)
         return hipErrorInvalidValue;
     const int U = b.d / codes_per_unit(b.bg);
-    int S = lanes_for(U, b.bg);
     // A routed launch over a few expert instances (one token, top-k) leaves
     // the chip with fewer than two workgroups per CU at lanes_for's choice:
-    // double the lanes per row (more, shorter rows per workgroup) until it
-    // has them.  GPT-OSS-20B-class experts, 2-bit gate/up, top-4: 8 -> 16
-    // lanes, 360 -> 720 workgroups, 31.3 -> 27.7 us per MoE layer.
-    if (b.route) {
-        const auto blocks = [&](int s) { return (long)((b.f + 256 / s - 1) / (256 / s)) * nb; };
-        while (S < 64 && 2 * S <= U && blocks(S) < 2L * 256)
-            S *= 2;
-    }
+    // routed_gateup_lanes doubles the lanes per row until it has them.
+    // GPT-OSS-20B-class experts, 2-bit gate/up, top-4: 8 -> 16 lanes,
+    // 360 -> 720 workgroups, 31.3 -> 27.7 us per MoE layer.
+    const int S = b.route ? routed_gateup_lanes(U, b.f, nb, b.bg, device_cu_count()) : lanes_for(U, b.bg);
     if (b.bg == 4)
         return launch_gateup_bits<4, false, 256>(b, nb, S, st);
     if (b.bg == 3)

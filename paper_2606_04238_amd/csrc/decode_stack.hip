@@ -582,6 +582,8 @@ size_t stack_ws_bytes(int d, int f, int r) {
 
 int stack_max_layers() { return kStackMaxLayers; }
 
+size_t stack_error_word_offset() { return (size_t)C_ERR * sizeof(unsigned); }
+
 hipError_t launch_rmsnorm(const uint16_t* x, uint16_t* u, int M, int d, hipStream_t st) {
     if (M <= 0)
         return hipSuccess;

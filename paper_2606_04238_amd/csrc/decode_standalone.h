@@ -297,6 +297,48 @@ inline int pipe_lanes(int U) {
     return 0;
 }
 
+// Compute units of the current device (an immutable property, cached per
+// device); 0 without one.
+inline int device_cu_count() {
+    static int cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 0;
+    if (cache[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
+
+// Lanes per row of a routed launch (a few expert instances of one token):
+// the launch's usual choice doubled (more, shorter rows per workgroup) while
+// it has fewer than two workgroups per compute unit, up to 64 lanes and one
+// 16-byte unit per lane.  blocks(S) = the launch's workgroups at S lanes.
+template <typename Blocks>
+inline int routed_lanes(int S, int U, int cus, Blocks blocks) {
+    while (S < 64 && 2 * S <= U && blocks(S) < 2L * cus)
+        S *= 2;
+    return S;
+}
+// Gate/up over nb instances of f rows (256-thread workgroups, 256 / S rows each).
+inline int routed_gateup_lanes(int U, int f, int nb, int bits, int cus) {
+    return routed_lanes(lanes_for(U, bits), U, cus,
+                        [&](int s) { return (long)((f + 256 / s - 1) / (256 / s)) * nb; });
+}
+// The pipelined down kernel over nb instances of d rows (0: it does not take U).
+inline int routed_pipe_lanes(int U, int d, int nb, int cus) {
+    const int S = pipe_lanes(U);
+    if (S == 0)
+        return 0;
+    return routed_lanes(S, U, cus, [&](int s) {
+        const int rpb = 4 * kPipeItems * (64 / s);
+        return (long)((d + rpb - 1) / rpb) * nb;
+    });
+}
+
 #define QMLP_PIPE_CASE(S_, J_)                                                            \
     if (S == S_ && JJ == J_) {                                                            \
         auto k = down_pipe_kernel<S_, J_, B, kPipeItems>;                                 \
@@ -311,17 +353,7 @@ inline int pipe_lanes(int U) {
 template <int B>
 hipError_t launch_down_pipe(const BatchArgs& args, int nb, hipStream_t st) {
     const int U = args.f / codes_per_unit(B);
-    int S = pipe_lanes(U);
-    // Routed launches over a few expert instances: double the lanes per row
-    // while the grid has fewer than two workgroups per CU (as for gate/up).
-    if (args.route && S) {
-        const auto blocks = [&](int s) {
-            const int rpb = 4 * kPipeItems * (64 / s);
-            return (long)((args.d + rpb - 1) / rpb) * nb;
-        };
-        while (S < 64 && 2 * S <= U && blocks(S) < 2L * 256)
-            S *= 2;
-    }
+    const int S = args.route ? routed_pipe_lanes(U, args.d, nb, device_cu_count()) : pipe_lanes(U);
     const int JJ = S ? (U + S - 1) / S : 0;
     const size_t lds = (size_t)U * (B == 2 ? GU_UNIT_BYTES : DN_UNIT_BYTES);
     const int rows_per_block = 4 * kPipeItems * (64 / (S ? S : 64));
@@ -334,11 +366,14 @@ hipError_t launch_down_pipe(const BatchArgs& args, int nb, hipStream_t st) {
 // workgroups of 4 * kPipeItems items (an LM head).
 constexpr int kPipeSingleMinRows = 16384;
 
+inline bool down_pipe_fits_shape(int d, int f, int M, int nb, int bits) {
+    const int U = f / codes_per_unit(bits);
+    return (nb > 1 || d >= kPipeSingleMinRows) && M == 1 && pipe_lanes(U) != 0 &&
+           (size_t)U * (bits == 2 ? GU_UNIT_BYTES : DN_UNIT_BYTES) <= (size_t)kLdsBudget;
+}
 template <int B>
 bool down_pipe_fits(const BatchArgs& args, int nb) {
-    const int U = args.f / codes_per_unit(B);
-    return (nb > 1 || args.d >= kPipeSingleMinRows) && args.M == 1 && pipe_lanes(U) != 0 &&
-           (size_t)U * (B == 2 ? GU_UNIT_BYTES : DN_UNIT_BYTES) <= (size_t)kLdsBudget;
+    return down_pipe_fits_shape(args.d, args.f, args.M, nb, B);
 }
 
 #define QMLP_DN_CASE(MT_, S_, J_)                                                         \

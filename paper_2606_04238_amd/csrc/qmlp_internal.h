@@ -142,6 +142,8 @@ hipError_t launch_moe_combine(const uint16_t* yi, const float* w, int M, int k, 
                               hipStream_t st);
 size_t stack_ws_bytes(int d, int f, int r);
 int stack_max_layers();
+// Byte offset of the persistent stack launch's sticky error word in its area.
+size_t stack_error_word_offset();
 hipError_t launch_stack(const StackLayerDesc* layers, int L, int d, int f, int g, int r,
                         const uint16_t* x0, uint16_t* y, uint16_t* x_last, void* ws, hipStream_t st);
 hipError_t launch_residual(const uint16_t* x, const uint16_t* y, uint16_t* out, int n, bool bf16,

@@ -188,6 +188,12 @@ def test_stack_validation(q, lib):
     assert fs(odd, 2) == SHAPE
     assert lib.qmlp_stack_workspace_bytes(odd, 2, 1, 0) == 0
     assert lib.qmlp_stack_launches(odd, 2, 1, 0) == 0
+    assert lib.qmlp_stack_error_offset(odd, 2, 1, 0) == 0
+    # without a GPU the blocks never run persistently: no error word; with
+    # one, the word lies inside the workspace past the per-layer part
+    off = lib.qmlp_stack_error_offset(arr, 2, 1, 0)
+    assert off == 0 or (lib.qmlp_workspace_bytes(ctypes.byref(m), 1, 0) < off
+                        <= lib.qmlp_stack_workspace_bytes(arr, 2, 1, 0) - 4)
     # an invalid block anywhere in the stack is reported
     bad = _stack_arr(q, m, _mlp(q, rank=7))
     assert fs(bad, 2) == UNSUP
@@ -411,3 +417,31 @@ def test_noalloc_validation(q, lib):
     assert lib.qmlp_workspace_bytes(ctypes.byref(big), 8, 0) > 1 << 20
     assert f(ctypes.byref(big), P(FAKE), 8, 0, P(FAKE), None) == WS
     assert f(ctypes.byref(big), P(FAKE), 8, 1, P(FAKE), None) == UNSUP     # bfloat16
+
+
+@pytest.mark.parametrize("d,f,gu_bits,dn_bits,inst,cus,want", [
+    # GPT-OSS-20B-class experts, top-4, one token, 256 compute units:
+    # W4/W2-GateUp gate/up 8 -> 16 lanes, W4 down 16 -> 64 (pipelined)
+    (2880, 2880, 2, 4, 4, 256, (16, 64, True)),
+    (2880, 2880, 2, 2, 4, 256, (16, 32, True)),        # uniform W2 down 8 -> 32
+    (2880, 2880, 4, 4, 4, 256, (16, 64, True)),        # uniform W4 gate/up keeps 16
+    # one instance: down runs the plain kernel (the pipelined one wants a batch)
+    (1024, 768, 2, 4, 1, 256, (16, 8, False)),
+    (1024, 768, 2, 4, 2, 256, (16, 16, True)),
+    (2048, 768, 2, 4, 2, 256, (32, 16, True)),         # one 16-byte unit per lane
+    # the rule counts the device's compute units, not a fixed 256
+    (2880, 2880, 2, 4, 4, 80, (8, 16, True)),
+    # enough instances to fill the chip: no doubling
+    (2880, 2880, 2, 4, 40, 256, (8, 16, True)),
+])
+def test_moe_lane_choice(q, d, f, gu_bits, dn_bits, inst, cus, want):
+    """The lanes per row of qmlp_forward_moe's launches (host-only query)."""
+    assert q.moe_lanes(d, f, gu_bits, dn_bits, inst, cus) == want
+
+
+def test_moe_lane_choice_rejects(q, lib):
+    g, dn = ctypes.c_int(0), ctypes.c_int(0)
+    for args in [(2880, 2880, 3, 4, 4, 256), (2880, 2880, 2, 4, 0, 256), (2880, 2880, 2, 4, 41, 256),
+                 (2880, 2880, 2, 4, 4, 0), (2890, 2880, 2, 4, 4, 256)]:
+        assert lib.qmlp_moe_lanes(*args, ctypes.byref(g), ctypes.byref(dn)) == -1
+    assert lib.qmlp_moe_lanes(2880, 2880, 2, 4, 4, 256, None, ctypes.byref(dn)) == -1

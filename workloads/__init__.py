@@ -211,7 +211,7 @@ class MoeConfig:
 
 
 MOE = {"gptoss20b_moe": MoeConfig("gptoss20b_moe", experts=32, topk=4,
-                                  block=Config("gptoss20b_expert", M=1, d=2880, f=2880, g=64, r=16, L=8))}
+                                  block=Config("gptoss20b_expert", M=1, d=2880, f=2880, g=64, r=16, L=24))}
 
 TID_ROUTE = 15
 
