@@ -127,7 +127,9 @@ size_t qmlp_meta_bytes(int n_out, int k_in, int group);
  * sticky error bits: 1 = t wait timed out, 2 = h wait timed out), then t
  * (fp32), h (activation type [M][f]), on the prefill path lora_scale * t in
  * bfloat16, and on the decode path the one-kernel layer's tagged hand-off
- * words (one [4][64] block of 64-bit words per compute unit, [4][f] 32-bit).  The workspace must be ZERO before
+ * words (one [4][64] block of 64-bit words per compute unit, [4][f] 32-bit),
+ * and on the prefill path, when the down projection splits f into slices
+ * to fill the chip, the slices' fp32 partial sums [S][M][d].  The workspace must be ZERO before
  * its first call, and zeroed again before it serves a block of another shape
  * or after an error bit appeared (the results of that call are invalid).
  * One workspace serves one call at a time: calls that overlap in time on the
@@ -393,7 +395,11 @@ qmlp_status qmlp_dequant(const qmlp_qweight *w, uint16_t *w_f16, qmlp_stream str
 /* Number of kernel launches qmlp_forward makes for this block at M tokens:
  * 1 when the whole layer runs as one fused kernel (the decode shapes it
  * covers), 2 or 3 when it runs as the LoRA-A, gate/up and down kernels in
- * stream order, 0 if the call would be rejected.  Host-only, enqueues nothing. */
+ * stream order; a bfloat16 prefill chunk makes LoRA-A and its reduction
+ * (with an adapter), gate/up, down, and, when down splits f into slices to
+ * fill the chip (f a multiple of 128 and fewer than 512 token x row tiles),
+ * the slices' reduction; 0 if the call would be rejected.  Host-only,
+ * enqueues nothing. */
 int qmlp_forward_launches(const qmlp_mlp *mlp, int M, qmlp_dtype dtype);
 
 /* Measurement hook (not part of the MLP): read `bytes` of device memory at

@@ -105,6 +105,7 @@ struct Workspace {
     uint16_t* T;
     unsigned long long* t64;
     uint32_t* h32;
+    float* part;                // prefill down partial sums (bfloat16 chunks), else null
 };
 
 size_t ws_t_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
@@ -119,16 +120,26 @@ size_t ws_t64_bytes() { return (size_t)fused_grid() * 256 * 8; }
 size_t ws_tag_bytes(const qmlp_mlp* mlp, qmlp_dtype dtype) {
     return dtype == QMLP_F16 ? ws_t64_bytes() + round256((size_t)4 * mlp->gate.n_out * 4) : 0;
 }
+size_t ws_part_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
+    return dtype == QMLP_BF16 ? round256(prefill_down_part_bytes(M, mlp->gate.k_in, mlp->gate.n_out)) : 0;
+}
+// Everything qmlp_forward carves from its workspace.
+size_t ws_total_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
+    return kCtlBytes + ws_t_bytes(mlp, M, dtype) + ws_h_bytes(mlp, M) + ws_T_bytes(mlp, M, dtype) +
+           ws_tag_bytes(mlp, dtype) + ws_part_bytes(mlp, M, dtype);
+}
 
 Workspace carve(const qmlp_mlp* mlp, int M, qmlp_dtype dtype, void* ws) {
     char* base = static_cast<char*>(ws);
     const size_t tb = ws_t_bytes(mlp, M, dtype), hb = ws_h_bytes(mlp, M);
     char* tag = base + kCtlBytes + tb + hb + ws_T_bytes(mlp, M, dtype);
+    char* part = tag + ws_tag_bytes(mlp, dtype);
     return {reinterpret_cast<unsigned*>(base), reinterpret_cast<float*>(base + kCtlBytes),
             reinterpret_cast<uint16_t*>(base + kCtlBytes + tb),
             reinterpret_cast<uint16_t*>(base + kCtlBytes + tb + hb),
             reinterpret_cast<unsigned long long*>(tag),
-            reinterpret_cast<uint32_t*>(tag + (dtype == QMLP_F16 ? ws_t64_bytes() : 0))};
+            reinterpret_cast<uint32_t*>(tag + (dtype == QMLP_F16 ? ws_t64_bytes() : 0)),
+            ws_part_bytes(mlp, M, dtype) ? reinterpret_cast<float*>(part) : nullptr};
 }
 
 // The prefill-chunk gate/up half: LoRA-A (split K + reduction), then the
@@ -151,12 +162,12 @@ qmlp_status run_prefill_gateup(const qmlp_mlp* mlp, const void* x, int M, uint16
         static_cast<const uint16_t*>(mlp->B_up), h, M, d, f, mlp->gate.group, r, st));
 }
 
-qmlp_status run_prefill_down(const qmlp_qweight* down, const void* h, int M, void* y,
+qmlp_status run_prefill_down(const qmlp_qweight* down, const void* h, int M, void* y, float* part,
                              hipStream_t st) {
     return from_hip(launch_prefill_down(static_cast<const uint32_t*>(down->codes),
                                         static_cast<const uint32_t*>(down->meta),
                                         static_cast<const uint16_t*>(h), static_cast<uint16_t*>(y),
-                                        M, down->n_out, down->k_in, down->group, st));
+                                        M, down->n_out, down->k_in, down->group, part, st));
 }
 
 GateUpArgs gateup_args(const qmlp_mlp* mlp, const void* x, int M, uint16_t* h, const float* t) {
@@ -279,8 +290,7 @@ bool stack_persistent(const qmlp_mlp* layers, int M, qmlp_dtype dtype) {
 }
 
 size_t stack_layer_ws(const qmlp_mlp* layers, int M, qmlp_dtype dtype) {
-    return round256(kCtlBytes + ws_t_bytes(layers, M, dtype) + ws_h_bytes(layers, M) +
-                    ws_T_bytes(layers, M, dtype) + ws_tag_bytes(layers, dtype));
+    return round256(ws_total_bytes(layers, M, dtype));
 }
 
 StackLayerDesc stack_desc(const qmlp_mlp& m) {
@@ -433,8 +443,7 @@ size_t qmlp_workspace_bytes(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
         return 0;
     if (M == 0)
         return 0;
-    return kCtlBytes + ws_t_bytes(mlp, M, dtype) + ws_h_bytes(mlp, M) + ws_T_bytes(mlp, M, dtype) +
-           ws_tag_bytes(mlp, dtype);
+    return ws_total_bytes(mlp, M, dtype);
 }
 
 qmlp_status qmlp_pack_w2(const float* W, int n_out, int k_in, int group, qmlp_qweight* out,
@@ -498,7 +507,7 @@ qmlp_status qmlp_down_w4(const qmlp_qweight* down, const void* h, int M, qmlp_dt
     if (!aligned16(h) || !aligned16(y))
         return QMLP_ERR_ALIGN;
     if (dtype == QMLP_BF16)
-        return run_prefill_down(down, h, M, y, static_cast<hipStream_t>(stream));
+        return run_prefill_down(down, h, M, y, nullptr, static_cast<hipStream_t>(stream));
     return from_hip(launch_down(down_args(down, h, M, y), static_cast<hipStream_t>(stream)));
 }
 
@@ -517,7 +526,7 @@ qmlp_status qmlp_forward(const qmlp_mlp* mlp, const void* x, int M, qmlp_dtype d
         s = run_prefill_gateup(mlp, x, M, w.h, w, st);
         if (s != QMLP_OK)
             return s;
-        return run_prefill_down(&mlp->down, w.h, M, y, st);
+        return run_prefill_down(&mlp->down, w.h, M, y, w.part, st);
     }
     if (standard_mlp(mlp) &&
         fused_supported(M, mlp->gate.k_in, mlp->gate.n_out, mlp->gate.group, mlp->rank))
@@ -563,7 +572,8 @@ int qmlp_forward_launches(const qmlp_mlp* mlp, int M, qmlp_dtype dtype) {
     if (check_mlp(mlp, M, dtype) != QMLP_OK || M == 0)
         return 0;
     if (dtype == QMLP_BF16)
-        return mlp->rank > 0 ? 4 : 2;
+        return (mlp->rank > 0 ? 4 : 2) +
+               (prefill_down_slices(M, mlp->gate.k_in, mlp->gate.n_out) > 1 ? 1 : 0);
     if (standard_mlp(mlp) &&
         fused_supported(M, mlp->gate.k_in, mlp->gate.n_out, mlp->gate.group, mlp->rank))
         return 1;

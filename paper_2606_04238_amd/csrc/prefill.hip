@@ -21,6 +21,7 @@
 // k + 1 are in flight while step k runs on the matrix cores.
 #include "qmlp_device.h"
 #include "qmlp_internal.h"
+#include "decode_launch.h"
 
 namespace qmlp {
 namespace {
@@ -51,51 +52,54 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
-__device__ __forceinline__ float bf2f(uint32_t bits16) {
-    return __builtin_bit_cast(float, bits16 << 16);
-}
-
 __device__ __forceinline__ f32x16_t mfma(const uint4& a, const uint4& b, const f32x16_t& c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                    __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
 
 // ------------------------------------------------------------ activation tile
-// 128 rows x 64 bf16 = 1024 chunks, 4 per thread; chunk id = tid + 256 i.
+// BM rows x 64 bf16 = 8 BM chunks, 4 per thread (BM = NT / 2); chunk id =
+// tid + NT i.
 struct ActRegs {
     uint4 v[4];
 };
 
+template <int NT = PF_NT>
 __device__ __forceinline__ void act_load(ActRegs& ar, const uint16_t* A, int K, int m0, int k0,
                                          int tid) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int id = tid + PF_NT * i, row = id >> 3, c = id & 7;
+        const int id = tid + NT * i, row = id >> 3, c = id & 7;
         ar.v[i] = ld16(A + (long)(m0 + row) * K + k0 + c * 8);
     }
 }
 
+template <int NT = PF_NT>
 __device__ __forceinline__ void act_store(uint4* lds, const ActRegs& ar, int tid) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int id = tid + PF_NT * i;
+        const int id = tid + NT * i;
         st16(&lds[swz(id >> 3, id & 7)], ar.v[i]);
     }
 }
 
 // --------------------------------------------------------- quantized weights
-// Thread t owns tile row t >> 1 and half t & 1 (32 codes) of a 128-row tile.
-template <int BITS>
+// Thread t owns tile row t / P and part t % P (CPT = 64 / P codes) of a
+// 128-row tile: P = 2 at 256 threads, 4 at 512.
+template <int BITS, int CPT>
 struct QRegs {
-    uint32_t w[BITS];           // 32 codes: 2 words at 2 bits, 4 words at 4 bits
-    uint32_t meta;              // scale | zero << 16 of the row's group
+    uint32_t w[BITS * CPT / 32];   // CPT codes
+    uint32_t meta;                 // scale | zero << 16 of the row's group
 };
 
-template <int BITS>
-__device__ __forceinline__ void q_load(QRegs<BITS>& qr, const uint32_t* codes_row,
-                                       const uint32_t* meta_row, int k0, int g, int half) {
-    const uint32_t* p = codes_row + (k0 + half * 32) * BITS / 32;
-    if constexpr (BITS == 2) {
+template <int BITS, int CPT>
+__device__ __forceinline__ void q_load(QRegs<BITS, CPT>& qr, const uint32_t* codes_row,
+                                       const uint32_t* meta_row, int k0, int g, int part) {
+    constexpr int NW = BITS * CPT / 32;
+    const uint32_t* p = codes_row + (k0 + part * CPT) * BITS / 32;
+    if constexpr (NW == 1) {
+        qr.w[0] = *p;
+    } else if constexpr (NW == 2) {
         const uint2 v = *reinterpret_cast<const uint2*>(p);
         qr.w[0] = v.x;
         qr.w[1] = v.y;
@@ -109,16 +113,17 @@ __device__ __forceinline__ void q_load(QRegs<BITS>& qr, const uint32_t* codes_ro
     qr.meta = meta_row[k0 / g];
 }
 
-// Dequantize 32 codes to bfloat16 scale * (q - zero) (one rounding: the fp32
+// Dequantize CPT codes to bfloat16 scale * (q - zero) (one rounding: the fp32
 // value is exact, since scale has 11 significant bits and |q - zero| < 16)
-// and store them as chunks half*4 .. half*4+3 of the tile row.
-template <int BITS>
-__device__ __forceinline__ void q_store(uint4* lds, const QRegs<BITS>& qr, int row, int half) {
+// and store them as chunks part * CPT/8 .. of the tile row.
+template <int BITS, int CPT>
+__device__ __forceinline__ void q_store(uint4* lds, const QRegs<BITS, CPT>& qr, int row, int part) {
     const float s = h2f(qr.meta & 0xFFFFu);
     const float nsz = -s * h2f(qr.meta >> 16);
+    constexpr int C0 = CPT / 8;                     // chunks per thread
     if constexpr (BITS == 2) {
 #pragma unroll
-        for (int wi = 0; wi < 2; ++wi) {
+        for (int wi = 0; wi < CPT / 16; ++wi) {
             // byte b of m[i] holds code 4b + i of the word
             uint32_t m[4];
 #pragma unroll
@@ -133,12 +138,12 @@ __device__ __forceinline__ void q_store(uint4* lds, const QRegs<BITS>& qr, int r
                                            pack_bf16(v[8 * j + 2], v[8 * j + 3]),
                                            pack_bf16(v[8 * j + 4], v[8 * j + 5]),
                                            pack_bf16(v[8 * j + 6], v[8 * j + 7]));
-                st16(&lds[swz(row, half * 4 + wi * 2 + j)], o);
+                st16(&lds[swz(row, part * C0 + wi * 2 + j)], o);
             }
         }
     } else {
 #pragma unroll
-        for (int wi = 0; wi < 4; ++wi) {
+        for (int wi = 0; wi < CPT / 8; ++wi) {
             // byte b of m0 holds code 2b, of m1 code 2b + 1
             const uint32_t m0 = qr.w[wi] & 0x0F0F0F0Fu, m1 = (qr.w[wi] >> 4) & 0x0F0F0F0Fu;
             float v[8];
@@ -147,7 +152,7 @@ __device__ __forceinline__ void q_store(uint4* lds, const QRegs<BITS>& qr, int r
                 v[2 * b] = __builtin_fmaf((float)((m0 >> (8 * b)) & 0xFFu), s, nsz);
                 v[2 * b + 1] = __builtin_fmaf((float)((m1 >> (8 * b)) & 0xFFu), s, nsz);
             }
-            st16(&lds[swz(row, half * 4 + wi)],
+            st16(&lds[swz(row, part * C0 + wi)],
                  make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]), pack_bf16(v[4], v[5]),
                             pack_bf16(v[6], v[7])));
         }
@@ -191,20 +196,22 @@ struct PfGateUpArgs {
     int M, d, f, g, r;
 };
 
-// Block tile: 128 tokens x 64 columns of h; the 128 weight rows are
+// Block tile: BM tokens x 64 columns of h; the 128 weight rows are
 // gate rows n0..n0+31, up n0..n0+31, gate n0+32.., up n0+32.., so wave
-// (wm, wn) holds G and U of the same 64 x 32 outputs.
-__global__ void __launch_bounds__(PF_NT) pf_gateup_kernel(PfGateUpArgs a) {
-    constexpr int BN = 128;
-    __shared__ uint4 lds[2][(PF_BM + BN) * 8];
+// (wm, wn) (BM/64 x 2 waves) holds G and U of the same 64 x 32 outputs.
+template <int BM, int NT>
+__global__ void __launch_bounds__(NT) pf_gateup_kernel(PfGateUpArgs a) {
+    constexpr int BN = 128, WMW = BM / 64, P = NT / 128, CPT = 64 / P;
+    static_assert(NT == 2 * BM, "4 activation chunks per thread");
+    extern __shared__ uint4 smem[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave & 1, wn = wave >> 1;
-    const int mtiles = a.M / PF_BM;
+    const int wm = wave % WMW, wn = wave / WMW;
+    const int mtiles = a.M / BM;
     const int mt0 = blockIdx.x % mtiles, nt0 = blockIdx.x / mtiles;
-    const int m0 = mt0 * PF_BM, n0 = nt0 * 64;
+    const int m0 = mt0 * BM, n0 = nt0 * 64;
 
-    const int trow = tid >> 1, half = tid & 1;
+    const int trow = tid / P, part = tid % P;
     const int mat = (trow >> 5) & 1;
     const int wrow = n0 + (trow >> 6) * 32 + (trow & 31);
     const int wpr = a.d / 16, ng = a.d / a.g;
@@ -218,20 +225,20 @@ __global__ void __launch_bounds__(PF_NT) pf_gateup_kernel(PfGateUpArgs a) {
         for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
 
     ActRegs ar;
-    QRegs<2> qr;
-    act_load(ar, a.x, a.d, m0, 0, tid);
-    q_load<2>(qr, crow, mrow, 0, a.g, half);
+    QRegs<2, CPT> qr;
+    act_load<NT>(ar, a.x, a.d, m0, 0, tid);
+    q_load<2, CPT>(qr, crow, mrow, 0, a.g, part);
     const int nk = a.d / PF_BK;
     for (int kt = 0; kt < nk; ++kt) {
-        uint4* xs = lds[kt & 1];
-        uint4* ws = xs + PF_BM * 8;
-        act_store(xs, ar, tid);
-        q_store<2>(ws, qr, trow, half);
+        uint4* xs = smem + (kt & 1) * (BM + BN) * 8;
+        uint4* ws = xs + BM * 8;
+        act_store<NT>(xs, ar, tid);
+        q_store<2, CPT>(ws, qr, trow, part);
         __syncthreads();
         {   // the next step's tiles (the last step re-reads its own: no branch)
             const int k1 = (kt + 1 < nk ? kt + 1 : kt) * PF_BK;
-            act_load(ar, a.x, a.d, m0, k1, tid);
-            q_load<2>(qr, crow, mrow, k1, a.g, half);
+            act_load<NT>(ar, a.x, a.d, m0, k1, tid);
+            q_load<2, CPT>(qr, crow, mrow, k1, a.g, part);
         }
         mfma_step<2, 2>(xs, ws, acc, wm, wn, lane);
     }
@@ -275,21 +282,26 @@ __global__ void __launch_bounds__(PF_NT) pf_gateup_kernel(PfGateUpArgs a) {
 struct PfDownArgs {
     const uint32_t *cd, *md;     // down codes [d][f/8], meta [d][f/g]
     const uint16_t* h;           // [M][f] bf16
-    uint16_t* y;                 // [M][d] bf16
-    int M, d, f, g;
+    uint16_t* y;                 // [M][d] bf16 (S == 1)
+    float* part;                 // [S][M][d] fp32 partial sums (S > 1)
+    int M, d, f, g, S;           // S: slices of f (split K), f / S a multiple of 64
 };
 
-__global__ void __launch_bounds__(PF_NT) pf_down_kernel(PfDownArgs a) {
-    constexpr int BN = 128;
-    __shared__ uint4 lds[2][(PF_BM + BN) * 8];
+template <int BM, int NT>
+__global__ void __launch_bounds__(NT) pf_down_kernel(PfDownArgs a) {
+    constexpr int BN = 128, WMW = BM / 64, P = NT / 128, CPT = 64 / P;
+    static_assert(NT == 2 * BM, "4 activation chunks per thread");
+    extern __shared__ uint4 smem[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave & 1, wn = wave >> 1;
-    const int mtiles = a.M / PF_BM;
-    const int mt0 = blockIdx.x % mtiles, nt0 = blockIdx.x / mtiles;
-    const int m0 = mt0 * PF_BM, n0 = nt0 * BN;
+    const int wm = wave % WMW, wn = wave / WMW;
+    const int mtiles = a.M / BM, ntiles = a.d / BN;
+    const int sl = blockIdx.x / (mtiles * ntiles), tile = blockIdx.x - sl * mtiles * ntiles;
+    const int mt0 = tile % mtiles, nt0 = tile / mtiles;
+    const int m0 = mt0 * BM, n0 = nt0 * BN;
+    const int kper = a.f / a.S, kbeg = sl * kper;     // this block's slice of f
 
-    const int trow = tid >> 1, half = tid & 1;
+    const int trow = tid / P, part = tid % P;
     const int wpr = a.f / 8, ng = a.f / a.g;
     const uint32_t* crow = a.cd + (long)(n0 + trow) * wpr;
     const uint32_t* mrow = a.md + (long)(n0 + trow) * ng;
@@ -301,24 +313,25 @@ __global__ void __launch_bounds__(PF_NT) pf_down_kernel(PfDownArgs a) {
         for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
 
     ActRegs ar;
-    QRegs<4> qr;
-    act_load(ar, a.h, a.f, m0, 0, tid);
-    q_load<4>(qr, crow, mrow, 0, a.g, half);
-    const int nk = a.f / PF_BK;
+    QRegs<4, CPT> qr;
+    act_load<NT>(ar, a.h, a.f, m0, kbeg, tid);
+    q_load<4, CPT>(qr, crow, mrow, kbeg, a.g, part);
+    const int nk = kper / PF_BK;
     for (int kt = 0; kt < nk; ++kt) {
-        uint4* xs = lds[kt & 1];
-        uint4* ws = xs + PF_BM * 8;
-        act_store(xs, ar, tid);
-        q_store<4>(ws, qr, trow, half);
+        uint4* xs = smem + (kt & 1) * (BM + BN) * 8;
+        uint4* ws = xs + BM * 8;
+        act_store<NT>(xs, ar, tid);
+        q_store<4, CPT>(ws, qr, trow, part);
         __syncthreads();
         {
-            const int k1 = (kt + 1 < nk ? kt + 1 : kt) * PF_BK;
-            act_load(ar, a.h, a.f, m0, k1, tid);
-            q_load<4>(qr, crow, mrow, k1, a.g, half);
+            const int k1 = kbeg + (kt + 1 < nk ? kt + 1 : kt) * PF_BK;
+            act_load<NT>(ar, a.h, a.f, m0, k1, tid);
+            q_load<4, CPT>(qr, crow, mrow, k1, a.g, part);
         }
         mfma_step<2, 2>(xs, ws, acc, wm, wn, lane);
     }
 
+    float* out = a.S > 1 ? a.part + (long)sl * a.M * a.d : nullptr;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
         const int col = n0 + wn * 64 + j * 32 + (lane & 31);
@@ -327,10 +340,25 @@ __global__ void __launch_bounds__(PF_NT) pf_down_kernel(PfDownArgs a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int m = m0 + wm * 64 + i * 32 + acc_row(v, lane);
-                const bf16x2_t p = {(__bf16)acc[i][j][v], (__bf16)0.0f};
-                a.y[(long)m * a.d + col] = (uint16_t)(__builtin_bit_cast(uint32_t, p) & 0xFFFFu);
+                if (out) {
+                    out[(long)m * a.d + col] = acc[i][j][v];
+                } else {
+                    const bf16x2_t p = {(__bf16)acc[i][j][v], (__bf16)0.0f};
+                    a.y[(long)m * a.d + col] = (uint16_t)(__builtin_bit_cast(uint32_t, p) & 0xFFFFu);
+                }
             }
     }
+}
+
+// y[i] = bf16(sum of the S partials, in slice order).
+__global__ void pf_down_reduce_kernel(const float* part, uint16_t* y, long n, int S) {
+    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n)
+        return;
+    float s = 0.0f;
+    for (int k = 0; k < S; ++k) s += part[(long)k * n + i];
+    const bf16x2_t p = {(__bf16)s, (__bf16)0.0f};
+    y[i] = (uint16_t)(__builtin_bit_cast(uint32_t, p) & 0xFFFFu);
 }
 
 struct PfLoraArgs {
@@ -453,19 +481,58 @@ hipError_t launch_prefill_lora(const uint16_t* Ag, const uint16_t* Au, const uin
     return hipGetLastError();
 }
 
+// Token tile of the gate/up and down kernels: 256 tokens (8 waves; every
+// dequantized weight serves 256 tokens) where M allows, else 128 (4 waves).
+int prefill_bm(int M) { return M % 256 == 0 ? 256 : 128; }
 hipError_t launch_prefill_gateup(const uint32_t* cg, const uint32_t* mg, const uint32_t* cu,
                                  const uint32_t* mu, const uint16_t* x, const uint16_t* T,
                                  const uint16_t* Bg, const uint16_t* Bu, uint16_t* h, int M, int d,
                                  int f, int g, int r, hipStream_t st) {
     PfGateUpArgs a{cg, mg, cu, mu, x, T, Bg, Bu, h, M, d, f, g, r};
-    pf_gateup_kernel<<<(M / PF_BM) * (f / 64), PF_NT, 0, st>>>(a);
-    return hipGetLastError();
+    const int BM = prefill_bm(M);
+    const size_t lds = (size_t)2 * (BM + 128) * 8 * 16;
+    auto run = [&](auto k) {
+        hipError_t e = set_lds(k, lds);
+        if (e != hipSuccess)
+            return e;
+        k<<<(M / BM) * (f / 64), 2 * BM, lds, st>>>(a);
+        return hipGetLastError();
+    };
+    return BM == 256 ? run(pf_gateup_kernel<256, 512>) : run(pf_gateup_kernel<128, 256>);
+}
+
+int prefill_down_slices(int M, int d, int f) {
+    // Enough (token tile x row tile x slice) blocks for two rounds over the
+    // compute units; slices of f stay whole 64-wide steps.
+    const long tiles = (long)(M / prefill_bm(M)) * (d / 128);
+    int S = 1;
+    while (S < 8 && tiles * S < 512 && f % (2 * S * PF_BK) == 0) S *= 2;
+    return S;
+}
+
+size_t prefill_down_part_bytes(int M, int d, int f) {
+    const int S = prefill_down_slices(M, d, f);
+    return S > 1 ? (size_t)S * M * d * 4 : 0;
 }
 
 hipError_t launch_prefill_down(const uint32_t* cd, const uint32_t* md, const uint16_t* h,
-                               uint16_t* y, int M, int d, int f, int g, hipStream_t st) {
-    PfDownArgs a{cd, md, h, y, M, d, f, g};
-    pf_down_kernel<<<(M / PF_BM) * (d / 128), PF_NT, 0, st>>>(a);
+                               uint16_t* y, int M, int d, int f, int g, float* part, hipStream_t st) {
+    const int S = part ? prefill_down_slices(M, d, f) : 1;
+    PfDownArgs a{cd, md, h, y, part, M, d, f, g, S};
+    const int BM = prefill_bm(M);
+    const size_t lds = (size_t)2 * (BM + 128) * 8 * 16;
+    auto run = [&](auto k) {
+        hipError_t e = set_lds(k, lds);
+        if (e != hipSuccess)
+            return e;
+        k<<<(M / BM) * (d / 128) * S, 2 * BM, lds, st>>>(a);
+        return hipGetLastError();
+    };
+    hipError_t e = BM == 256 ? run(pf_down_kernel<256, 512>) : run(pf_down_kernel<128, 256>);
+    if (e != hipSuccess || S == 1)
+        return e;
+    const long n = (long)M * d;
+    pf_down_reduce_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(part, y, n, S);
     return hipGetLastError();
 }
 

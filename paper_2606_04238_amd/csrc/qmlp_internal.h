@@ -80,8 +80,13 @@ hipError_t launch_prefill_gateup(const uint32_t* cg, const uint32_t* mg, const u
                                  const uint32_t* mu, const uint16_t* x, const uint16_t* T,
                                  const uint16_t* Bg, const uint16_t* Bu, uint16_t* h, int M, int d,
                                  int f, int g, int r, hipStream_t st);
+// Down over the chunk; with part (fp32 scratch of prefill_down_part_bytes)
+// f is split into slices whose partial sums a second launch adds in slice
+// order, else one launch writes y.
+int prefill_down_slices(int M, int d, int f);
+size_t prefill_down_part_bytes(int M, int d, int f);
 hipError_t launch_prefill_down(const uint32_t* cd, const uint32_t* md, const uint16_t* h,
-                               uint16_t* y, int M, int d, int f, int g, hipStream_t st);
+                               uint16_t* y, int M, int d, int f, int g, float* part, hipStream_t st);
 
 // A stack of decode blocks in one persistent launch per up to
 // stack_max_layers() layers (decode_stack.hip): M = 1, binary16, block l

@@ -115,12 +115,16 @@ def test_prefill_validation(q, lib):
     assert _fwd(lib, m, M=128, dtype=0) == UNSUP    # binary16 decode stops at 16 tokens
     assert _fwd(lib, _mlp(q, d=320, f=448), M=128, dtype=1) == UNSUP
     assert _fwd(lib, m, M=0, dtype=1) == OK
-    assert lib.qmlp_forward_launches(ctypes.byref(m), 256, 1) == 4
-    assert lib.qmlp_forward_launches(ctypes.byref(_mlp(q, rank=0)), 256, 1) == 2
+    # LoRA-A, its reduction, gate/up, down over slices of f, the slices' sum
+    assert lib.qmlp_forward_launches(ctypes.byref(m), 256, 1) == 5
+    assert lib.qmlp_forward_launches(ctypes.byref(_mlp(q, rank=0)), 256, 1) == 3
+    # f = 448 is not a multiple of 128: down runs unsplit
+    assert lib.qmlp_forward_launches(ctypes.byref(_mlp(q, d=256, f=448)), 256, 1) == 4
     assert lib.qmlp_forward_launches(ctypes.byref(m), 100, 1) == 0
     big = _mlp(q, d=6144, f=16384, g=128, rank=32)
     n = lib.qmlp_workspace_bytes(ctypes.byref(big), 512, 1)
-    assert n >= 1024 + 512 * 16384 * 2 + 512 * 64 * 2 + 512 * 64 * 4
+    # h, T, t and the down slices' fp32 partial sums (4 slices of 512 x 6144)
+    assert n >= 1024 + 512 * 16384 * 2 + 512 * 64 * 2 + 512 * 64 * 4 + 4 * 512 * 6144 * 4
     w = _qw(q, bits=4, n=256, k=512)
     assert lib.qmlp_down_w4(ctypes.byref(w), ctypes.c_void_p(FAKE), 100, 1,
                             ctypes.c_void_p(FAKE), None) == UNSUP
