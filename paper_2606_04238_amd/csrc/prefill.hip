@@ -196,20 +196,22 @@ struct PfGateUpArgs {
     int M, d, f, g, r;
 };
 
-// Block tile: BM tokens x 64 columns of h; the 128 weight rows are
-// gate rows n0..n0+31, up n0..n0+31, gate n0+32.., up n0+32.., so wave
-// (wm, wn) (BM/64 x 2 waves) holds G and U of the same 64 x 32 outputs.
-template <int BM, int NT>
+// Block tile: BM tokens x HC columns of h.  The 2 HC weight rows come in
+// groups of 64: gate rows c..c+31 then up rows c..c+31 of the group's 32
+// columns c, so a wave tile of 32 WM tokens x one group holds G and U of the
+// same outputs.  Waves: BM / (32 WM) along tokens x HC / 32 along columns.
+template <int BM, int HC, int NT, int WM>
 __global__ void __launch_bounds__(NT) pf_gateup_kernel(PfGateUpArgs a) {
-    constexpr int BN = 128, WMW = BM / 64, P = NT / 128, CPT = 64 / P;
+    constexpr int BN = 2 * HC, WMW = BM / (32 * WM), P = NT / BN, CPT = 64 / P;
     static_assert(NT == 2 * BM, "4 activation chunks per thread");
+    static_assert(WMW * (HC / 32) == NT / 64, "one wave tile per wave");
     extern __shared__ uint4 smem[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave % WMW, wn = wave / WMW;
     const int mtiles = a.M / BM;
     const int mt0 = blockIdx.x % mtiles, nt0 = blockIdx.x / mtiles;
-    const int m0 = mt0 * BM, n0 = nt0 * 64;
+    const int m0 = mt0 * BM, n0 = nt0 * HC;
 
     const int trow = tid / P, part = tid % P;
     const int mat = (trow >> 5) & 1;
@@ -218,9 +220,9 @@ __global__ void __launch_bounds__(NT) pf_gateup_kernel(PfGateUpArgs a) {
     const uint32_t* crow = (mat ? a.cu : a.cg) + (long)wrow * wpr;
     const uint32_t* mrow = (mat ? a.mu : a.mg) + (long)wrow * ng;
 
-    f32x16_t acc[2][2];
+    f32x16_t acc[WM][2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < WM; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
 
@@ -240,7 +242,7 @@ __global__ void __launch_bounds__(NT) pf_gateup_kernel(PfGateUpArgs a) {
             act_load<NT>(ar, a.x, a.d, m0, k1, tid);
             q_load<2, CPT>(qr, crow, mrow, k1, a.g, part);
         }
-        mfma_step<2, 2>(xs, ws, acc, wm, wn, lane);
+        mfma_step<WM, 2>(xs, ws, acc, wm, wn, lane);
     }
 
     // LoRA: G += T_g B_g^T, U += T_u B_u^T over k < r (zero-padded to 16).
@@ -255,8 +257,8 @@ __global__ void __launch_bounds__(NT) pf_gateup_kernel(PfGateUpArgs a) {
                 const uint16_t* Bm = j ? a.Bu : a.Bg;
                 const uint4 b = in ? ld16(Bm + (long)ncol * a.r + kk) : make_uint4(0, 0, 0, 0);
 #pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    const int m = m0 + wm * 64 + i * 32 + r;
+                for (int i = 0; i < WM; ++i) {
+                    const int m = m0 + wm * 32 * WM + i * 32 + r;
                     const uint4 t = in ? ld16(a.T + (long)m * 2 * a.r + j * a.r + kk)
                                        : make_uint4(0, 0, 0, 0);
                     acc[i][j] = mfma(t, b, acc[i][j]);
@@ -268,10 +270,10 @@ __global__ void __launch_bounds__(NT) pf_gateup_kernel(PfGateUpArgs a) {
     // SiLU(G) * U -> h (bf16)
     const int col = n0 + wn * 32 + (lane & 31);
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < WM; ++i)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-            const int m = m0 + wm * 64 + i * 32 + acc_row(v, lane);
+            const int m = m0 + wm * 32 * WM + i * 32 + acc_row(v, lane);
             const float G = acc[i][0][v], U = acc[i][1][v];
             const float hv = G / (1.0f + __expf(-G)) * U;
             const bf16x2_t p = {(__bf16)hv, (__bf16)0.0f};
@@ -490,15 +492,21 @@ hipError_t launch_prefill_gateup(const uint32_t* cg, const uint32_t* mg, const u
                                  int f, int g, int r, hipStream_t st) {
     PfGateUpArgs a{cg, mg, cu, mu, x, T, Bg, Bu, h, M, d, f, g, r};
     const int BM = prefill_bm(M);
-    const size_t lds = (size_t)2 * (BM + 128) * 8 * 16;
+    // 256 tokens x 128 columns of h (wave tiles of 128 tokens x 32 columns,
+    // half the LDS reads and two thirds of the LDS writes per MFMA of the
+    // 64-column tile) where f allows
+    const int HC = BM == 256 && f % 128 == 0 ? 128 : 64;
+    const size_t lds = (size_t)2 * (BM + 2 * HC) * 8 * 16;
     auto run = [&](auto k) {
         hipError_t e = set_lds(k, lds);
         if (e != hipSuccess)
             return e;
-        k<<<(M / BM) * (f / 64), 2 * BM, lds, st>>>(a);
+        k<<<(M / BM) * (f / HC), 2 * BM, lds, st>>>(a);
         return hipGetLastError();
     };
-    return BM == 256 ? run(pf_gateup_kernel<256, 512>) : run(pf_gateup_kernel<128, 256>);
+    if (HC == 128)
+        return run(pf_gateup_kernel<256, 128, 512, 4>);
+    return BM == 256 ? run(pf_gateup_kernel<256, 64, 512, 2>) : run(pf_gateup_kernel<128, 64, 256, 2>);
 }
 
 int prefill_down_slices(int M, int d, int f) {

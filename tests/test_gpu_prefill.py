@@ -60,6 +60,10 @@ PREFILL_CASES = {
                                   act="bf16"),
     "pf_m384_r32_g128_out": wl.Config("pf_m384_r32_g128_out", M=384, d=768, f=1024, g=128, r=32,
                                       L=1, act="bf16", outliers=True),
+    # 256-token tiles with 128 columns of h per block (f % 128 == 0), two
+    # token tiles, down over slices of f
+    "pf_m512_r16_g128_wide": wl.Config("pf_m512_r16_g128_wide", M=512, d=512, f=768, g=128, r=16,
+                                       L=1, act="bf16"),
 }
 
 
