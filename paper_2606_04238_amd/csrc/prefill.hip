@@ -11,14 +11,16 @@
 //   pf_gateup  : G, U tiles + the rank-r LoRA products + SiLU(G) * U -> h,
 //   pf_down    : y = dequant4(W_down) h.
 //
-// Tile engine shared by the three GEMM kernels: a block of 256 threads
-// (4 waves in a 2 x 2 grid) owns a 128-token x BN-weight-row tile and walks
-// the input dimension in steps of 64.  Each step stages the activation tile
-// (128 x 64 bf16) and the dequantized weight tile (BN x 64 bf16) in LDS,
-// rows of eight 16-byte chunks with chunk c of row r stored at c ^ (r & 7),
-// so the 16-byte fragment reads of an MFMA (32 rows, one chunk) hit 32
-// distinct banks per 8 lanes.  Two LDS buffers; the global loads of step
-// k + 1 are in flight while step k runs on the matrix cores.
+// Tile engine shared by the three GEMM kernels: a block of NT threads owns
+// a BM-token x BN-weight-row tile (BM = 128 on 4 waves, or 256 on 8 waves
+// where M allows) and walks the input dimension in steps of 64.  Each step
+// stages the activation tile (BM x 64 bf16) and the dequantized weight tile
+// (BN x 64 bf16) in LDS, rows of eight 16-byte chunks with chunk c of row r
+// stored at c ^ ((r >> 1) & 7): the 16-byte fragment reads of an MFMA (32
+// rows, one chunk) and the row-wise tile writes cover every LDS bank once
+// per 16 lanes (two rows share a 256-byte bank line).  Two LDS buffers; the
+// global loads of step k + 1 are in flight while step k runs on the matrix
+// cores.
 #include "qmlp_device.h"
 #include "qmlp_internal.h"
 #include "decode_launch.h"
@@ -34,7 +36,7 @@ constexpr int PF_BM = 128;     // tokens per block tile
 constexpr int PF_BK = 64;      // input elements per step
 constexpr int PF_NT = 256;     // threads per block
 
-__device__ __forceinline__ int swz(int r, int c) { return r * 8 + (c ^ (r & 7)); }
+__device__ __forceinline__ int swz(int r, int c) { return r * 8 + (c ^ ((r >> 1) & 7)); }
 
 // 16-byte global load / LDS store through a plain vector type (HIP's uint4
 // copies are lowered to memcpy, which keeps a register tile in scratch).
@@ -226,23 +228,35 @@ __global__ void __launch_bounds__(NT) pf_gateup_kernel(PfGateUpArgs a) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
 
+    // Step k's tiles are staged during step k - 1's matrix-core work: the
+    // MFMAs of a step are issued, then the same wave dequantizes and stores
+    // the next step's tiles into the other buffer while they run.  One
+    // barrier per step: step k's tiles are complete, and every wave is done
+    // reading the buffer step k + 1 will overwrite.
     ActRegs ar;
     QRegs<2, CPT> qr;
+    const int nk = a.d / PF_BK;
     act_load<NT>(ar, a.x, a.d, m0, 0, tid);
     q_load<2, CPT>(qr, crow, mrow, 0, a.g, part);
-    const int nk = a.d / PF_BK;
+    act_store<NT>(smem, ar, tid);
+    q_store<2, CPT>(smem + BM * 8, qr, trow, part);
+    {
+        const int k1 = (nk > 1 ? 1 : 0) * PF_BK;
+        act_load<NT>(ar, a.x, a.d, m0, k1, tid);
+        q_load<2, CPT>(qr, crow, mrow, k1, a.g, part);
+    }
     for (int kt = 0; kt < nk; ++kt) {
-        uint4* xs = smem + (kt & 1) * (BM + BN) * 8;
-        uint4* ws = xs + BM * 8;
-        act_store<NT>(xs, ar, tid);
-        q_store<2, CPT>(ws, qr, trow, part);
         __syncthreads();
-        {   // the next step's tiles (the last step re-reads its own: no branch)
-            const int k1 = (kt + 1 < nk ? kt + 1 : kt) * PF_BK;
-            act_load<NT>(ar, a.x, a.d, m0, k1, tid);
-            q_load<2, CPT>(qr, crow, mrow, k1, a.g, part);
-        }
-        mfma_step<WM, 2>(xs, ws, acc, wm, wn, lane);
+        uint4* xs = smem + (kt & 1) * (BM + BN) * 8;
+        mfma_step<WM, 2>(xs, xs + BM * 8, acc, wm, wn, lane);
+        // the next step's tiles (past the last step: a copy of the last
+        // step's, never read), then the loads of the one after
+        uint4* xn = smem + ((kt + 1) & 1) * (BM + BN) * 8;
+        act_store<NT>(xn, ar, tid);
+        q_store<2, CPT>(xn + BM * 8, qr, trow, part);
+        const int k2 = (kt + 2 < nk ? kt + 2 : nk - 1) * PF_BK;
+        act_load<NT>(ar, a.x, a.d, m0, k2, tid);
+        q_load<2, CPT>(qr, crow, mrow, k2, a.g, part);
     }
 
     // LoRA: G += T_g B_g^T, U += T_u B_u^T over k < r (zero-padded to 16).
@@ -314,23 +328,29 @@ __global__ void __launch_bounds__(NT) pf_down_kernel(PfDownArgs a) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
 
+    // staged one step ahead, as in the gate/up kernel
     ActRegs ar;
     QRegs<4, CPT> qr;
+    const int nk = kper / PF_BK;
     act_load<NT>(ar, a.h, a.f, m0, kbeg, tid);
     q_load<4, CPT>(qr, crow, mrow, kbeg, a.g, part);
-    const int nk = kper / PF_BK;
+    act_store<NT>(smem, ar, tid);
+    q_store<4, CPT>(smem + BM * 8, qr, trow, part);
+    {
+        const int k1 = kbeg + (nk > 1 ? 1 : 0) * PF_BK;
+        act_load<NT>(ar, a.h, a.f, m0, k1, tid);
+        q_load<4, CPT>(qr, crow, mrow, k1, a.g, part);
+    }
     for (int kt = 0; kt < nk; ++kt) {
-        uint4* xs = smem + (kt & 1) * (BM + BN) * 8;
-        uint4* ws = xs + BM * 8;
-        act_store<NT>(xs, ar, tid);
-        q_store<4, CPT>(ws, qr, trow, part);
         __syncthreads();
-        {
-            const int k1 = kbeg + (kt + 1 < nk ? kt + 1 : kt) * PF_BK;
-            act_load<NT>(ar, a.h, a.f, m0, k1, tid);
-            q_load<4, CPT>(qr, crow, mrow, k1, a.g, part);
-        }
-        mfma_step<2, 2>(xs, ws, acc, wm, wn, lane);
+        uint4* xs = smem + (kt & 1) * (BM + BN) * 8;
+        mfma_step<2, 2>(xs, xs + BM * 8, acc, wm, wn, lane);
+        uint4* xn = smem + ((kt + 1) & 1) * (BM + BN) * 8;
+        act_store<NT>(xn, ar, tid);
+        q_store<4, CPT>(xn + BM * 8, qr, trow, part);
+        const int k2 = kbeg + (kt + 2 < nk ? kt + 2 : nk - 1) * PF_BK;
+        act_load<NT>(ar, a.h, a.f, m0, k2, tid);
+        q_load<4, CPT>(qr, crow, mrow, k2, a.g, part);
     }
 
     float* out = a.S > 1 ? a.part + (long)sl * a.M * a.d : nullptr;
