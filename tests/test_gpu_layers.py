@@ -274,8 +274,8 @@ def test_layers_streamed_shapes_match_oracle(q, d, f, g, r, L):
 
 @pytest.mark.parametrize("M,d,f,g,r,L", [
     (3, 512, 1536, 64, 8, 1),       # the fewest tokens, one block: fewer items than compute units
-    (4, 512, 1280, 128, 16, 3),     # MT = 4, f a multiple of 2 g but not of the h' chunk
-    (5, 768, 1536, 64, 0, 9),       # MT = 8, no adapter
+    (4, 512, 6400, 128, 16, 3),     # MT = 4: f over two h' chunks of 6144 codes, the second short
+    (5, 1536, 2560, 64, 0, 9),      # MT = 8, no adapter: h' chunks of 1536 codes, the last short
     (8, 1024, 2048, 128, 32, 40),   # a full batch: ranges straddle blocks
     (9, 512, 1536, 64, 16, 41),     # MT = 16, two batches
     (16, 2048, 3072, 64, 8, 6),     # all sixteen token rows
