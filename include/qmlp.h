@@ -280,16 +280,18 @@ int qmlp_stack_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
  * owning a contiguous range of the batch's rows flattened over blocks, so
  * no workgroup waits for another and h of every block passes through the
  * workspace between the two launches.  At 3 <= M <= 16 in the same form
- * (d % (4 g) == 0, f % (2 g_down) == 0, and the workspace-free limits
- * qmlp_layers_path reports) a batch runs on the MATRIX CORES: the LoRA-A
- * launch, then one persistent gate/up launch and one persistent down
+ * (d % 512 == 0, f % 256 == 0, and the LDS limits qmlp_layers_path
+ * reports) a batch runs on the MATRIX CORES: the LoRA-A launch (fp32
+ * partial sums over four slices of d, added in slice order by the next
+ * launch), then one persistent gate/up launch and one persistent down
  * launch that multiply every unpacked weight into all M tokens with
  * v_mfma_f32_16x16x32_f16.  Every other binary16 batch runs the
  * stand-alone kernels as qmlp_forward_batch does; bfloat16 runs
  * qmlp_forward once per block.
  *
  * ws/ws_bytes: at least qmlp_layers_workspace_bytes(layers, L, M, dtype)
- * (binary16: that of qmlp_forward_batch).  No state is kept between calls.
+ * (binary16: that of qmlp_forward_batch, with four times its t area on the
+ * matrix cores).  No state is kept between calls.
  * Errors as for qmlp_forward.
  */
 size_t qmlp_layers_workspace_bytes(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);

@@ -356,8 +356,10 @@ BatchPath batch_path(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
                                                 : BatchPath::kBatched;
 }
 
-size_t batch_t_bytes(const qmlp_mlp* a, int nb, int M) {
-    return round256((size_t)nb * M * 2 * a->rank * 4);
+// t of a batch: [nb][M][2r] fp32, or kLoraSlices such arrays of partial
+// sums on the matrix-core path.
+size_t batch_t_bytes(const qmlp_mlp* a, int nb, int M, int slices = 1) {
+    return round256((size_t)slices * nb * M * 2 * a->rank * 4);
 }
 size_t batch_h_bytes(const qmlp_mlp* a, int nb, int M) {
     return round256((size_t)nb * M * a->gate.n_out * 2);
@@ -370,9 +372,10 @@ qmlp_status run_layers_batched(const qmlp_mlp* layers, int L, const char* xb, in
     const int d = a.gate.k_in;
     const size_t step = (size_t)M * d * 2;
     char* base = static_cast<char*>(ws);
+    const int ts = path == BatchPath::kMfma ? kLoraSlices : 1;
     BatchArgs b{};
     b.t = reinterpret_cast<float*>(base + kCtlBytes);
-    b.h = reinterpret_cast<uint16_t*>(base + kCtlBytes + batch_t_bytes(&a, batch_size(L), M));
+    b.h = reinterpret_cast<uint16_t*>(base + kCtlBytes + batch_t_bytes(&a, batch_size(L), M, ts));
     b.M = M;
     b.d = d;
     b.f = a.gate.n_out;
@@ -386,7 +389,9 @@ qmlp_status run_layers_batched(const qmlp_mlp* layers, int L, const char* xb, in
         for (int i = 0; i < n; ++i) b.lay[i] = stack_desc(layers[l0 + i]);
         b.x = reinterpret_cast<const uint16_t*>(xb + l0 * step);
         b.y = reinterpret_cast<uint16_t*>(yb + l0 * step);
-        hipError_t e = b.r > 0 ? launch_lora_a_batch(b, n, st) : hipSuccess;
+        hipError_t e = b.r == 0                  ? hipSuccess
+                       : path == BatchPath::kMfma ? launch_lora_a_mfma(b, n, st)
+                                                  : launch_lora_a_batch(b, n, st);
         if (e == hipSuccess)
             e = path == BatchPath::kStreamed ? launch_gateup_stream(b, n, st)
                 : path == BatchPath::kMfma   ? launch_gateup_mfma(b, n, st)
@@ -671,7 +676,9 @@ size_t qmlp_layers_workspace_bytes(const qmlp_mlp* layers, int L, int M, qmlp_dt
     if (check_layers(layers, L, M, dtype) != QMLP_OK || M == 0)
         return 0;
     if (dtype == QMLP_F16)              // streamed, matrix-core or batched
-        return qmlp_batch_workspace_bytes(layers, L, M, dtype);
+        return kCtlBytes +
+               batch_t_bytes(layers, batch_size(L), M, layers_mfma(layers, L, M, dtype) ? kLoraSlices : 1) +
+               batch_h_bytes(layers, batch_size(L), M);
     return qmlp_workspace_bytes(&layers[0], M, dtype);
 }
 

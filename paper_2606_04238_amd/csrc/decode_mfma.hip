@@ -26,10 +26,11 @@
 // adds s * acc.  The LoRA-B term is one more MFMA per item: lora_scale * t
 // (binary16, zero past the rank) times the item's B rows.
 //
-// Loads.  Every code load is 16 bytes per lane, 64 contiguous bytes per
-// weight row and instruction.  Where one load spans several groups, the
-// words are redistributed between lane quarters with v_permlane32_swap /
-// v_permlane16_swap so that each quarter ends up with words of every group.
+// Loads.  Every code load is 16 bytes per lane and fetches eight weight
+// rows' 128-byte lines whole; the words then move between lanes in
+// registers (a row rotation, v_permlane16_swap, v_permlane32_swap) so that
+// lane 16 q + j holds row j and each quarter q words of every group (see
+// "Whole-line loads" below).
 //
 // Work split.  Each workgroup owns a contiguous range of the batch's
 // 16-row items (flattened over blocks).
@@ -335,6 +336,57 @@ __device__ __forceinline__ void mf_gu_step(MfGuBuf<G>& q, const uint4* xsb, cons
     }
 }
 
+// ---------------------------------------------------------------- LoRA-A
+// t = [A_g; A_u] x of every block of the batch (Sec. 3.1 Eq. (1), Sec. 4.2),
+// also on the matrix cores: workgroup (tile, slice) of block l multiplies 16
+// rows of [A_g; A_u] (rows past r are those of A_u) by the block's tokens
+// over slice s of d (the tokens as the A operand, padded with token 0 whose
+// results are dropped).  Its four waves take a quarter of the slice each
+// and add their sums in wave order through LDS; the fp32 partial goes to
+// t[s][l][token][row] and the gate/up launch adds the kLoraSlices partials
+// in slice order.  Every wave streams 16 rows x 64 bytes per load from
+// independent addresses, so nothing here waits on another workgroup.
+__global__ void __launch_bounds__(256) mf_lora_kernel(BatchArgs b, int nb) {
+    __shared__ float red[4][4][64];                       // [wave][v][lane]
+    const int l = blockIdx.y;
+    const int tile = blockIdx.x / kLoraSlices, s = blockIdx.x - tile * kLoraSlices;
+    const int d = b.d, r = b.r, M = b.M;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, q = lane >> 4;
+    const int c = tile * 16 + (lane & 15);                // this lane's row of [A_g; A_u]
+    const int kc = d / (4 * kLoraSlices);                 // K of one wave, a multiple of 32
+    const int nst = kc / 32;
+    const int k0 = (s * 4 + wave) * kc + 8 * q;
+    const uint16_t* ar = c < r ? kbm()->lay[l].Ag + (long)c * d : kbm()->lay[l].Au + (long)(c - r) * d;
+    const int j = (lane & 15) < M ? (lane & 15) : 0;
+    const uint16_t* xr = b.x + ((long)l * M + j) * d;
+    f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int i = 0; i < nst; i += 4) {
+        uint4 av[4], xv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int k = k0 + 32 * (i + u < nst ? i + u : nst - 1);
+            av[u] = *reinterpret_cast<const uint4*>(ar + k);
+            xv[u] = *reinterpret_cast<const uint4*>(xr + k);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (i + u < nst)
+                acc = mfma16(xv[u], av[u], acc);
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v) red[wave][v][lane] = acc[v];
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const float sum = ((red[0][v][lane] + red[1][v][lane]) + red[2][v][lane]) + red[3][v][lane];
+            const int tok = 4 * q + v;                    // D row of this lane and v
+            if (tok < M)
+                b.t[(((long)s * nb + l) * M + tok) * 2 * r + c] = sum;
+        }
+    }
+}
+
 template <int G, int MT, int NW>
 __global__ void __launch_bounds__(NW * 64) mf_gu_kernel(BatchArgs b, int nb) {
     constexpr int NT = NW * 64, GW = G / 16, QW = G / 64;
@@ -375,9 +427,19 @@ __global__ void __launch_bounds__(NW * 64) mf_gu_kernel(BatchArgs b, int nb) {
             for (int k = tid; k < MT * 32; k += NT) {
                 const int j = k >> 5, c = k & 31;
                 const bool ok = j < M && c < r;
+                // the LoRA-A partials of the kLoraSlices slices of d, added in order
                 const float* tl = b.t + ((long)l * M + (ok ? j : 0)) * 2 * r;
-                tsg[k] = (uint16_t)f2h(ok ? ls * tl[c] : 0.0f);
-                tsu[k] = (uint16_t)f2h(ok ? ls * tl[r + c] : 0.0f);
+                const long ps = (long)nb * M * 2 * r;
+                float vg = 0.0f, vu = 0.0f;
+                if (ok) {
+#pragma unroll
+                    for (int sl = 0; sl < kLoraSlices; ++sl) {
+                        vg += tl[sl * ps + c];
+                        vu += tl[sl * ps + r + c];
+                    }
+                }
+                tsg[k] = (uint16_t)f2h(ls * vg);
+                tsu[k] = (uint16_t)f2h(ls * vu);
             }
         }
         __syncthreads();
@@ -723,6 +785,13 @@ bool mfma_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r, 
         return false;
     const int MT = mf_mt(M);
     return mf_gu_lds(d, gg, MT) <= kMfLds && mf_dn_lds(mf_dn_chunk(f, gd, MT), gd, MT) <= kMfLds;
+}
+
+hipError_t launch_lora_a_mfma(const BatchArgs& b, int nb, hipStream_t st) {
+    if (!mfma_supported(b.M, b.d, b.f, b.gg, b.bg, b.gd, b.bd, b.r, nb) || b.r == 0)
+        return hipErrorInvalidValue;
+    mf_lora_kernel<<<dim3((unsigned)(2 * b.r / 16 * kLoraSlices), (unsigned)nb), 256, 0, st>>>(b, nb);
+    return hipGetLastError();
 }
 
 #define QMLP_MFGU(G_, MT_)                                                                \

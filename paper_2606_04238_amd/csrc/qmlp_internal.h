@@ -133,10 +133,15 @@ hipError_t launch_gateup_stream(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_down_stream(const BatchArgs& b, int nb, hipStream_t st);
 // The matrix-core path of a batch at 3..16 tokens (decode_mfma.hip): one
 // persistent gate/up launch and one persistent down launch over all blocks
-// of the batch, after launch_lora_a_batch.  Binary16, 2-bit gate/up and
-// 4-bit down at groups 64/128, rank 0/8/16/32, d % (4 g) == 0,
-// f % (2 g_down) == 0 (plus the LDS and items-per-wave limits it checks).
+// of the batch, after launch_lora_a_mfma.  Binary16, 2-bit gate/up and
+// 4-bit down at groups 64/128, rank 0/8/16/32, d % 512 == 0,
+// f % 256 == 0 (plus the LDS limits it checks).
 bool mfma_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r, int nb);
+// Its LoRA-A products t = [A_g; A_u] x (r > 0) as fp32 partial sums over
+// kLoraSlices slices of d, t [kLoraSlices][nb][M][2r]; the gate/up launch
+// adds them in slice order.
+constexpr int kLoraSlices = 4;
+hipError_t launch_lora_a_mfma(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_gateup_mfma(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_down_mfma(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_gateup_batch(const BatchArgs& b, int nb, hipStream_t st);

@@ -62,13 +62,48 @@ def _one(path_glob):
 
 
 def _counter_means(pmc_dir):
-    """{kernel name: [values per dispatch]} of the one counter in a --pmc run."""
+    """{kernel name: [values per dispatch]} of the one counter in a --pmc run,
+    and the run's rows."""
     rows = list(csv.DictReader(open(_one(os.path.join(pmc_dir, "*counter_collection.csv")))))
     name = rows[0]["Counter_Name"] if rows else "?"
     out = {}
     for r in rows:
         out.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
-    return name, out
+    return name, out, rows
+
+
+def step_dispatches(rows, parts, name_key):
+    """Dispatch ids of the step's launches, one list per part: every run of
+    consecutive dispatches (in dispatch order) whose kernel names contain
+    parts[0], parts[1], ... in turn.  A command may launch the same kernel
+    outside the step (one block per call, other precisions); those
+    dispatches do not follow the step's order and are left out.  None when
+    the rows carry no dispatch ids or no such run exists."""
+    if not rows or "Dispatch_Id" not in rows[0]:
+        return None
+    seq = sorted({int(r["Dispatch_Id"]): r[name_key] for r in rows}.items())
+    out = [[] for _ in parts]
+    i = 0
+    while i + len(parts) <= len(seq):
+        if all(parts[j] in seq[i + j][1] for j in range(len(parts))):
+            for j in range(len(parts)):
+                out[j].append(seq[i + j][0])
+            i += len(parts)
+        else:
+            i += 1
+    return out if out[0] else None
+
+
+def _part_values(rows, per, parts):
+    """Per part: the counter values of the step's dispatches (by dispatch
+    order when the rows allow it, else every dispatch of that name)."""
+    ids = step_dispatches(rows, parts, "Kernel_Name")
+    if ids is None:
+        return [[v for k, vs in per.items() if part in k for v in vs] for part in parts]
+    by_id = {}
+    for r in rows:
+        by_id.setdefault(int(r["Dispatch_Id"]), []).append(float(r["Counter_Value"]))
+    return [[v for i in idl for v in by_id[i]] for idl in ids]
 
 
 def _closest(per_kernel, substr, known_kib):
@@ -118,20 +153,36 @@ def summarize(kt_dir, pf_dir, pw_dir, kernel, copy_mib, out_md, commands, stream
         rows = [r for r in stats if part in r["Name"]]
         if len(rows) != 1:
             raise ValueError("kernel %r matches %d rows of the stats" % (part, len(rows)))
-        krows.append(rows[0])
+        krows.append(dict(rows[0]))
+    # with the per-dispatch trace, the step's own dispatches give the figures
+    traces = glob.glob(os.path.join(kt_dir, "*kernel_trace.csv"))
+    if len(traces) == 1:
+        trows = list(csv.DictReader(open(traces[0])))
+        ids = step_dispatches(trows, parts, "Kernel_Name")
+        if ids is not None:
+            dur = {int(r["Dispatch_Id"]): int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+                   for r in trows}
+            for kr, idl in zip(krows, ids):
+                ns = [dur[i] for i in idl]
+                kr.update(Calls=len(ns), AverageNs=statistics.mean(ns), MinNs=min(ns), MaxNs=max(ns))
     avg_us = sum(float(r["AverageNs"]) for r in krows) / 1e3
     copy_kib = copy_mib * 1024.0
     stream_kib = stream_mib * 1024.0
     lines = ["# %s -- rocprofv3 summary" % kernel, ""]
     lines += ["Commands (run from the repository root on one MI355X; `R` is that root):", ""]
     lines += ["    " + c for c in commands]
-    lines += ["", "## Kernel trace (--kernel-trace --stats), top dispatches", "",
-              "| kernel | calls | avg us | min us | max us | share % |",
-              "|---|---|---|---|---|---|"]
-    for r in stats[:6]:
-        lines.append("| `%s` | %s | %.3f | %.3f | %.3f | %s |" % (
+    def trace_rows(rs):
+        return ["| `%s` | %s | %.3f | %.3f | %.3f | %s |" % (
             r["Name"][:90], r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
-            float(r["MaxNs"]) / 1e3, r["Percentage"]))
+            float(r["MaxNs"]) / 1e3, r["Percentage"]) for r in rs]
+    head = ["| kernel | calls | avg us | min us | max us | share % |", "|---|---|---|---|---|---|"]
+    lines += ["", "## Kernel trace (--kernel-trace --stats), the launches of one step", "",
+              "Dispatches taken in the step's launch order; the share is that of every "
+              "dispatch of the kernel in the run.", ""]
+    lines += head + trace_rows(krows)
+    lines += ["", "Sum of their average durations: %.3f us." % avg_us]
+    lines += ["", "## Kernel trace, the run's top dispatches (all kernels of the command)", ""]
+    lines += head + trace_rows(stats[:6])
     total = 0.0
     cal = ["", "## Calibration dispatches (known bytes / counted bytes)", "",
            "| counter | reference dispatch | counted KiB | known KiB | factor |", "|---|---|---|---|---|"]
@@ -139,11 +190,10 @@ def summarize(kt_dir, pf_dir, pw_dir, kernel, copy_mib, out_md, commands, stream
               "| counter | KiB per step (sum of the kernels' means) | dispatches | reference | factor "
               "| bytes per step |", "|---|---|---|---|---|---|"]
     for d in (pf_dir, pw_dir):
-        counter, per = _counter_means(d)
+        counter, per, crows = _counter_means(d)
         kib = 0.0
         nd = 0
-        for part in parts:
-            vals = [v for k, vs in per.items() if part in k for v in vs]
+        for part, vals in zip(parts, _part_values(crows, per, parts)):
             if not vals:
                 raise ValueError("kernel %r not in %s" % (part, d))
             kib += statistics.mean(vals)
@@ -172,12 +222,15 @@ def summarize(kt_dir, pf_dir, pw_dir, kernel, copy_mib, out_md, commands, stream
 
 def counter_table(pmc_dir, kernels):
     """Markdown rows of every counter of one --pmc run, mean per dispatch, for
-    each kernel whose name contains one of `kernels`."""
+    each kernel whose name contains one of `kernels` (the step's dispatches
+    when the rows carry dispatch ids)."""
     rows = list(csv.DictReader(open(_one(os.path.join(pmc_dir, "*counter_collection.csv")))))
+    ids = step_dispatches(rows, kernels, "Kernel_Name")
+    keep = None if ids is None else {i: kn for kn, idl in zip(kernels, ids) for i in idl}
     acc = {}
     for r in rows:
         for kn in kernels:
-            if kn in r["Kernel_Name"]:
+            if kn in r["Kernel_Name"] and (keep is None or keep.get(int(r["Dispatch_Id"])) == kn):
                 acc.setdefault((kn, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
     out = ["| kernel | counter | mean per dispatch | dispatches |", "|---|---|---|---|"]
     for (kn, cn), vs in sorted(acc.items()):

@@ -284,13 +284,17 @@ def test_layers_mfma_shapes_match_oracle(q, M, d, f, g, r, L):
     """3 <= M <= 16 runs on the matrix cores (LoRA-A, then one gate/up and
     one down launch per batch): token counts on both sides of each padded
     tile height (4, 8, 16), groups 64 and 128, ranks 0 to 32, batches from
-    one block to two batches.  Every block against the oracle (sampled for
+    one block to two batches; d from 512 to 2048 gives each LoRA-A wave 1 to
+    4 steps of 32 (a partial group of four at 1536).  Every block against the oracle (sampled for
     long batches) and against the stand-alone kernels on the same input."""
     cfg = wl.Config("mfma_m%d_%d_%d" % (M, d, f), M=M, d=d, f=f, g=g, r=r, L=L)
     _announce("layers mfma", cfg.name, "g", g, "r", r, "L", L)
     layers, mlps, ls, x = _blocks(q, cfg, L, rank=r > 0)
     assert q.layers_path(ls, M) == "mfma"
     assert q.layers_launches(ls, M) == (3 if r > 0 else 2) * ((L + 39) // 40)
+    # control block, four slices of LoRA-A partial sums t, then h of a batch
+    nb, r256 = min(L, 40), (lambda v: (v + 255) // 256 * 256)
+    assert q.layers_workspace_bytes(ls, M) == 1024 + r256(4 * nb * M * 2 * r * 4) + r256(nb * M * f * 2)
     ws = q.layers_workspace(ls, M)
     y = q.forward_layers(ls, x, ws=ws)
     yb = q.forward_batch(ls, x)
