@@ -49,7 +49,11 @@ namespace qmlp {
 
 // One thread per output element: the routing-weighted sum of the k expert
 // outputs of its token (Sec. 5 names the routed experts of the MoE decoder;
-// the weights come with the routing).
+// the weights come with the routing).  KM >= k: every load of a thread is
+// issued before the first add (the slots past k re-read slot k - 1 and are
+// dropped), so the kernel makes one trip to memory; the sum runs over
+// j = 0 .. k - 1 in order.
+template <int KM>
 __global__ void __launch_bounds__(256)
 moe_combine_kernel(const uint16_t* __restrict__ yi, const float* __restrict__ w, int M, int k,
                    int d, uint16_t* __restrict__ y) {
@@ -57,16 +61,32 @@ moe_combine_kernel(const uint16_t* __restrict__ yi, const float* __restrict__ w,
     if (i >= (long)M * d)
         return;
     const long m = i / d, c = i - m * d;
+    float wv[KM];
+    uint32_t yv[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+        const int jj = j < k ? j : k - 1;
+        wv[j] = w[m * k + jj];
+        yv[j] = yi[(m * k + jj) * d + c];
+    }
     float acc = 0.0f;
-    for (int j = 0; j < k; ++j)
-        acc += w[m * k + j] * h2f(yi[(m * k + j) * d + c]);
+#pragma unroll
+    for (int j = 0; j < KM; ++j)
+        if (j < k)
+            acc += wv[j] * h2f(yv[j]);
     y[i] = (uint16_t)f2h(acc);
 }
 
 hipError_t launch_moe_combine(const uint16_t* yi, const float* w, int M, int k, int d, uint16_t* y,
                               hipStream_t st) {
     const long n = (long)M * d;
-    moe_combine_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(yi, w, M, k, d, y);
+    const unsigned grid = (unsigned)((n + 255) / 256);
+    if (k <= 4)
+        moe_combine_kernel<4><<<grid, 256, 0, st>>>(yi, w, M, k, d, y);
+    else if (k <= 8)
+        moe_combine_kernel<8><<<grid, 256, 0, st>>>(yi, w, M, k, d, y);
+    else
+        moe_combine_kernel<kBatchMax><<<grid, 256, 0, st>>>(yi, w, M, k, d, y);
     return hipGetLastError();
 }
 
