@@ -606,6 +606,7 @@ def moe_main(mc: wl.MoeConfig, args):
                      "achieved": mix["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": mix["frac_of_hbm_peak"], "traffic": None},
     }
+    calibrations(args)
     print(json.dumps(out), flush=True)
     return 0
 
@@ -674,6 +675,7 @@ def prefill_main(cfg: wl.Config, args):
             "traffic": None,
         },
     }
+    calibrations(args)
     print(json.dumps(out), flush=True)
     return 0
 
@@ -724,6 +726,23 @@ def stream_calibration(mib: int):
         torch.cuda.synchronize()
     log("stream calibration: %d bytes read with non-temporal loads, then %d with plain loads" % (n, n))
     del buf
+
+
+def calibrations(args):
+    """The reference dispatches of known size that the byte counters are
+    scaled by (after the timing, so they never enter it)."""
+    import torch
+    if args.calibrate_stream_mib > 0:
+        stream_calibration(args.calibrate_stream_mib)
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib << 20
+        src = torch.ones(n // 2, dtype=torch.float16, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        log("copy calibration: %d bytes read, %d bytes written" % (n, n))
+        del src, dst
 
 
 def main(argv=None):
@@ -881,17 +900,7 @@ def main(argv=None):
             "traffic": None if traffic is None else int(traffic),
         },
     }
-    if args.calibrate_stream_mib > 0:
-        stream_calibration(args.calibrate_stream_mib)
-    if args.calibrate_copy_mib > 0:
-        n = args.calibrate_copy_mib << 20
-        src = torch.ones(n // 2, dtype=torch.float16, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        torch.neg(src, out=dst)
-        torch.cuda.synchronize()
-        log("copy calibration: %d bytes read, %d bytes written" % (n, n))
-        del src, dst
+    calibrations(args)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, args.seed)
     print(json.dumps(out), flush=True)

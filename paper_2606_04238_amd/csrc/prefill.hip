@@ -9,7 +9,10 @@
 //   pf_lora_a  : partial t over a slice of the input dimension (split K),
 //   pf_lora_t  : t = lora_scale * sum of the partials, rounded to bfloat16,
 //   pf_gateup  : G, U tiles + the rank-r LoRA products + SiLU(G) * U -> h,
-//   pf_down    : y = dequant4(W_down) h.
+//   pf_down    : y = dequant4(W_down) h, split over S slices of f when the
+//                token x row tiles alone would not fill the chip (fp32
+//                partials [S][M][d]),
+//   pf_down_reduce (S > 1): y = the partials' sum in slice order.
 //
 // Tile engine shared by the three GEMM kernels: a block of NT threads owns
 // a BM-token x BN-weight-row tile (BM = 128 on 4 waves, or 256 on 8 waves
@@ -18,9 +21,10 @@
 // (BN x 64 bf16) in LDS, rows of eight 16-byte chunks with chunk c of row r
 // stored at c ^ ((r >> 1) & 7): the 16-byte fragment reads of an MFMA (32
 // rows, one chunk) and the row-wise tile writes cover every LDS bank once
-// per 16 lanes (two rows share a 256-byte bank line).  Two LDS buffers; the
-// global loads of step k + 1 are in flight while step k runs on the matrix
-// cores.
+// per 16 lanes (two rows share a 256-byte bank line).  Two LDS buffers and
+// one set of staging registers: while step k runs on the matrix cores the
+// registers hold step k + 1, which then goes to the other buffer, and the
+// global loads of step k + 2 are issued (one barrier per step).
 #include "qmlp_device.h"
 #include "qmlp_internal.h"
 #include "decode_launch.h"
