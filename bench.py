@@ -65,7 +65,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
 # the launches of one streamed step, as named in the kernel trace
 # the kernels of one step of qmlp_forward_layers on each path (profile summaries)
 STEP_KERNELS = {"streamed": "lora_a_kernel|gu_stream_kernel|dn_stream_kernel",
-                "mfma": "lora_a_kernel|mf_gu_kernel|mf_dn_kernel"}
+                "mfma": "mf_lora_kernel|mf_gu_kernel|mf_dn_kernel"}
 METRIC = BASE_METRIC = ("achieved HBM GB/s (% of MI355X peak) and µs per W4/W2-GateUp MLP "
                         "decode step")
 
