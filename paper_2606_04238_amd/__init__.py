@@ -23,7 +23,9 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libqmlp.so")
+# QMLP_LIB_PATH: another build of the same sources (the host-sanitized one
+# of build.py --host-sanitize); by default the library next to this file
+LIB_PATH = os.environ.get("QMLP_LIB_PATH") or os.path.join(_HERE, "libqmlp.so")
 
 F16, BF16 = 0, 1
 _STATUS = {0: "QMLP_OK", 1: "QMLP_ERR_NULL", 2: "QMLP_ERR_SHAPE", 3: "QMLP_ERR_ALIGN",

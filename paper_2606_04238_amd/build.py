@@ -4,6 +4,15 @@ Each ``csrc/*.hip`` is compiled to an object in parallel with hipcc, then
 linked into a shared library next to this file.  Packed-fp32 VALU forms are
 disabled (``-packed-fp32-ops``); the compiler still emits ordinary fp32 and
 the packed fp16 / dot2 instructions the kernels ask for.
+
+``--host-sanitize`` builds ``_build_san/libqmlp_san.so`` instead: the host
+code (argument validation, sizes, dispatch) under AddressSanitizer and
+UndefinedBehaviorSanitizer, the device code as usual.  Run the CPU ABI tests
+against it with clang's ASan runtime preloaded:
+    QMLP_LIB_PATH=paper_2606_04238_amd/_build_san/libqmlp_san.so \
+    LD_PRELOAD=$(ls /opt/rocm/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so) \
+    ASAN_OPTIONS=detect_leaks=0 UBSAN_OPTIONS=halt_on_error=1 \
+    python -m pytest -s tests/test_abi.py tests/test_bench_cli.py
 """
 import concurrent.futures
 import glob
@@ -24,28 +33,37 @@ COMMON = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
           "-Wall", "-Wno-unused-result", "-I", os.path.join(_HERE, "..", "include")]
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + COMMON + ["-c", src, "-o", obj]
+# host-only sanitizers (each -fsanitize= right after -Xarch_host: the device
+# code is built as usual)
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+
+
+def _compile(src: str, build_dir: str = BUILD, extra=()) -> str:
+    obj = os.path.join(build_dir, os.path.basename(src) + ".o")
+    cmd = [HIPCC] + COMMON + list(extra) + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed on %s:\n%s" % (src, r.stderr[-8000:]))
     return obj
 
 
-def build(jobs: int = 8) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+def build(jobs: int = 8, host_sanitize: bool = False) -> str:
+    build_dir = os.path.join(_HERE, "_build_san") if host_sanitize else BUILD
+    lib = os.path.join(build_dir, "libqmlp_san.so") if host_sanitize else LIB
+    extra = SANITIZE if host_sanitize else []
+    os.makedirs(build_dir, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     with concurrent.futures.ThreadPoolExecutor(max_workers=min(jobs, len(srcs))) as ex:
-        objs = list(ex.map(_compile, srcs))
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
+        objs = list(ex.map(lambda s: _compile(s, build_dir, extra), srcs))
+    tmp = lib + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC"] + extra + ["-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n%s" % r.stderr[-8000:])
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(), file=sys.stderr)
+    print(build(host_sanitize="--host-sanitize" in sys.argv[1:]), file=sys.stderr)

@@ -1,6 +1,7 @@
 // C ABI of libqmlp: argument validation, workspace layout and kernel dispatch.
 // Every check runs before the first launch, so a rejected call enqueues
 // nothing and writes nothing.
+#include <cstring>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -864,7 +865,11 @@ qmlp_status qmlp_forward_moe(const qmlp_mlp* experts, int E, const void* x, int 
 }
 
 const char* qmlp_status_string(qmlp_status s) {
-    switch (s) {
+    // a C caller may pass any int: read its bytes as an int, since loading a
+    // value outside the enumerators' range as the enum type is undefined here
+    int v = 0;
+    std::memcpy(&v, &s, sizeof v);
+    switch (v) {
     case QMLP_OK: return "ok";
     case QMLP_ERR_NULL: return "null pointer";
     case QMLP_ERR_SHAPE: return "invalid shape";
