@@ -360,16 +360,17 @@ __global__ void __launch_bounds__(256) mf_lora_kernel(BatchArgs b, int nb) {
     const int j = (lane & 15) < M ? (lane & 15) : 0;
     const uint16_t* xr = b.x + ((long)l * M + j) * d;
     f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (int i = 0; i < nst; i += 4) {
-        uint4 av[4], xv[4];
+    constexpr int KC = 4;                                 // steps whose loads go out together
+    for (int i = 0; i < nst; i += KC) {
+        uint4 av[KC], xv[KC];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < KC; ++u) {
             const int k = k0 + 32 * (i + u < nst ? i + u : nst - 1);
             av[u] = *reinterpret_cast<const uint4*>(ar + k);
             xv[u] = *reinterpret_cast<const uint4*>(xr + k);
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < KC; ++u)
             if (i + u < nst)
                 acc = mfma16(xv[u], av[u], acc);
     }
@@ -754,7 +755,12 @@ size_t mf_gu_lds(int d, int g, int MT) {
 size_t mf_dn_lds(int ck, int g, int MT) {
     return (size_t)2 * (ck / 8) * (MT + 1) * 16 + (size_t)2 * (ck / g) * MT * 8;
 }
-constexpr int kDnTpw = 3;        // down: items per wave and round
+// down: items per wave and round, and waves per workgroup, by token tile (at
+// MT = 8 two items per wave measured 3 % faster on the 14B-class blocks than
+// three; other choices, such as 8 waves of 4 items at MT = 4, stayed within
+// the run-to-run spread)
+constexpr int dn_tpw(int MT) { return MT == 8 ? 2 : 3; }
+constexpr int dn_waves(int MT) { return kMfWaves; }
 // down: staged h' words per thread and chunk (registers left beside the
 // items' loads: those of g = 64 carry twice the (scale | zero) words)
 constexpr int mf_stage_words(int g) { return g == 64 ? 2 : 4; }
@@ -762,7 +768,7 @@ constexpr int mf_stage_words(int g) { return g == 64 ? 2 : 4; }
 // the staging registers of the workgroup and whose two buffers fit in LDS,
 // no larger than f rounded up to a step.
 int mf_dn_chunk(int f, int g, int MT) {
-    int ck = mf_stage_words(g) * kMfWaves * 64 * 8 / MT / 256 * 256;
+    int ck = mf_stage_words(g) * dn_waves(MT) * 64 * 8 / MT / 256 * 256;
     while (ck > 256 && mf_dn_lds(ck, g, MT) > kMfLds) ck -= 256;
     const int fr = (f + 255) / 256 * 256;
     return ck < fr ? ck : fr;
@@ -816,10 +822,10 @@ hipError_t launch_gateup_mfma(const BatchArgs& b, int nb, hipStream_t st) {
 
 #define QMLP_MFDN(G_, MT_)                                                                \
     if (b.gd == G_ && MT == MT_) {                                                        \
-        auto k = mf_dn_kernel<G_, MT_, kDnTpw, kMfWaves, mf_stage_words(G_)>;             \
+        auto k = mf_dn_kernel<G_, MT_, dn_tpw(MT_), dn_waves(MT_), mf_stage_words(G_)>;   \
         hipError_t e = set_lds(k, lds);                                                   \
         if (e != hipSuccess) return e;                                                    \
-        k<<<grid, kMfWaves * 64, lds, st>>>(b, nb, ck);                                   \
+        k<<<grid, dn_waves(MT_) * 64, lds, st>>>(b, nb, ck);                              \
         return hipGetLastError();                                                         \
     }
 
