@@ -264,8 +264,9 @@ def decoder_model(stack: Stack, seed: int, steps: int, min_warm_s: float, mlp_us
     (one [q + 2 kv][d] matrix) and the o projection (qmlp_linear_batch over
     the layers; 4-bit, or 2-bit for W2), the MLP (mlp_us: the precision
     comparison's pass), and the read of a BF16 KV cache of ctx positions (a
-    streaming read of those bytes stands in for attention, which is not
-    built); per token the LM head at the linears' width.  The weight part of
+    read-only pass of this library's streaming kernel over that many bytes
+    stands in for attention, which is not built); per token the LM head at
+    the linears' width.  The weight part of
     a token is timed as one graph per width; the per-operator times are
     reported beside it."""
     import torch
@@ -315,14 +316,17 @@ def decoder_model(stack: Stack, seed: int, steps: int, min_warm_s: float, mlp_us
         gr = capture(lambda: q.linear_batch([lm[b]], xl, y=yl))
         ms, _ = time_passes(gr.replay, steps, 2, min_warm_s)
         us[(b, "lm_head")] = sum(ms) / len(ms) * 1e3
-    # the KV stand-in: one reduction over the BF16 bytes, timed eagerly (a
-    # reduction over many blocks is kept out of HIP graphs)
-    kv = torch.ones(L * dims.kv_bytes_per_layer() // 2, dtype=torch.bfloat16, device="cuda")
-    ms, _ = time_passes(lambda: kv.sum(dtype=torch.float32), steps, 2, min_warm_s)
+    # the KV stand-in: one read-only pass over the BF16 bytes (pairs of 1.0)
+    # with the streaming probe's 128-bit non-temporal loads, timed eagerly;
+    # every wave reads an even number of equal words, so their XORs are zero
+    kv = torch.full((L * dims.kv_bytes_per_layer() // 4,), 0x3F803F80, dtype=torch.int32, device="cuda")
+    kvo = torch.empty(4 * 256, dtype=torch.int32, device="cuda")
+    ms, _ = time_passes(lambda: q.probe_stream_read(kv, 256, True, kvo), steps, 2, min_warm_s)
     kv_us = sum(ms) / len(ms) * 1e3
-    if float(kv.sum(dtype=torch.float32)) != float(kv.numel()):
-        raise RuntimeError("KV read stand-in summed wrong")
-    del kv
+    torch.cuda.synchronize()
+    if torch.any(kvo != 0):
+        raise RuntimeError("KV read stand-in read unexpected data")
+    del kv, kvo
     widths = {"w4_uniform": 4, "w2_uniform": 2, "w4w2_gateup_lora": 4}
     out = {"dims": dataclasses.asdict(dims),
            "ops_us_per_token": {"qkv_4bit": round(us[(4, "qkv")], 2), "o_4bit": round(us[(4, "o")], 2),
