@@ -93,8 +93,9 @@ typedef struct {
 /* One W4/W2-GateUp MLP block with its Recover-LoRA adapters (Sec. 3.3, 4.2).
  * gate/up at 2 bits and down at 4 bits, groups of 64 or 128, is the block
  * every path takes.  The binary16 decode path (qmlp_forward,
- * qmlp_forward_layers, qmlp_forward_batch; not the one-kernel layer nor the
- * persistent launches, which take only that form) also runs the comparison
+ * qmlp_forward_layers, qmlp_forward_batch; not the one-kernel layer, the
+ * streamed and matrix-core launches nor the persistent stack, which take
+ * only that form) also runs the comparison
  * points of the throughput analysis (Sec. 5.2) and the paper's INT2 grouping
  * (Sec. 3.3, Sec. 4.1): gate/up at 4 bits (uniform W4), down at 2 bits
  * (uniform W2, groups of 64 or 128), and group 32 for gate/up (any width)
