@@ -35,6 +35,7 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int PF_BM = 128;     // tokens per block tile
 constexpr int PF_BK = 64;      // input elements per step
@@ -376,15 +377,22 @@ __global__ void __launch_bounds__(NT) pf_down_kernel(PfDownArgs a) {
     }
 }
 
-// y[i] = bf16(sum of the S partials, in slice order).
+// y[i] = bf16(sum of the S <= kDownSlicesMax partials, in slice order), four
+// outputs per thread with 16-byte loads (n % 4 == 0).
+constexpr int kDownSlicesMax = 8;
 __global__ void pf_down_reduce_kernel(const float* part, uint16_t* y, long n, int S) {
-    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    const long i = ((long)blockIdx.x * blockDim.x + threadIdx.x) * 4;
     if (i >= n)
         return;
-    float s = 0.0f;
-    for (int k = 0; k < S; ++k) s += part[(long)k * n + i];
-    const bf16x2_t p = {(__bf16)s, (__bf16)0.0f};
-    y[i] = (uint16_t)(__builtin_bit_cast(uint32_t, p) & 0xFFFFu);
+    float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
+    for (int k = 0; k < S; ++k) {
+        const f32x4_t v = *reinterpret_cast<const f32x4_t*>(part + (long)k * n + i);
+        s0 += v[0];
+        s1 += v[1];
+        s2 += v[2];
+        s3 += v[3];
+    }
+    *reinterpret_cast<uint2*>(y + i) = make_uint2(pack_bf16(s0, s1), pack_bf16(s2, s3));
 }
 
 struct PfLoraArgs {
@@ -464,15 +472,25 @@ __global__ void __launch_bounds__(PF_NT) pf_lora_a_kernel(PfLoraArgs a) {
     }
 }
 
-// T[m][c] = bf16(lora_scale * sum over slices, in slice order).
+// T[m][c] = bf16(lora_scale * sum over the S <= kLoraSplitsMax slices, in
+// slice order).
+constexpr int kLoraSplitsMax = 24;
 __global__ void pf_lora_t_kernel(const float* part, uint16_t* T, int M, int r, int S,
                                  float lora_scale) {
     const long n = (long)M * 2 * r;
     const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n)
         return;
+    // every load first (slots past S re-read slice S - 1 and are dropped),
+    // then the sum in slice order
+    float v[kLoraSplitsMax];
+#pragma unroll
+    for (int k = 0; k < kLoraSplitsMax; ++k) v[k] = part[(long)(k < S ? k : S - 1) * n + i];
     float s = 0.0f;
-    for (int k = 0; k < S; ++k) s += part[(long)k * n + i];
+#pragma unroll
+    for (int k = 0; k < kLoraSplitsMax; ++k)
+        if (k < S)
+            s += v[k];
     const bf16x2_t p = {(__bf16)(lora_scale * s), (__bf16)0.0f};
     T[i] = (uint16_t)(__builtin_bit_cast(uint32_t, p) & 0xFFFFu);
 }
@@ -487,7 +505,7 @@ bool prefill_supported(int M, int d, int f, int g, int r) {
 
 int prefill_splits(int d) {
     const int nk = d / PF_BK;
-    for (int s = nk < 24 ? nk : 24; s > 1; --s)
+    for (int s = nk < kLoraSplitsMax ? nk : kLoraSplitsMax; s > 1; --s)
         if (nk % s == 0 && nk / s >= 2)
             return s;
     return 1;
@@ -538,7 +556,7 @@ int prefill_down_slices(int M, int d, int f) {
     // compute units; slices of f stay whole 64-wide steps.
     const long tiles = (long)(M / prefill_bm(M)) * (d / 128);
     int S = 1;
-    while (S < 8 && tiles * S < 512 && f % (2 * S * PF_BK) == 0) S *= 2;
+    while (S < kDownSlicesMax && tiles * S < 512 && f % (2 * S * PF_BK) == 0) S *= 2;
     return S;
 }
 
@@ -563,8 +581,8 @@ hipError_t launch_prefill_down(const uint32_t* cd, const uint32_t* md, const uin
     hipError_t e = BM == 256 ? run(pf_down_kernel<256, 512>) : run(pf_down_kernel<128, 256>);
     if (e != hipSuccess || S == 1)
         return e;
-    const long n = (long)M * d;
-    pf_down_reduce_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(part, y, n, S);
+    const long n = (long)M * d;                          // d % 128 == 0
+    pf_down_reduce_kernel<<<(unsigned)((n / 4 + 255) / 256), 256, 0, st>>>(part, y, n, S);
     return hipGetLastError();
 }
 
