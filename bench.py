@@ -606,7 +606,7 @@ def moe_main(mc: wl.MoeConfig, args):
                    "widths": res,
                    "gain_pct": round((t4 / tm - 1) * 100, 1),
                    "capture_pct": round((1 / tm - 1 / t4) / (1 / t2 - 1 / t4) * 100, 1)},
-        "roofline": {"bound": "hbm", "kernel": "MoE layer step (LoRA-A, gate/up, down, combine)",
+        "roofline": {"bound": "hbm", "kernel": "MoE layer step (LoRA-A, gate/up, down with the routing-weighted sum)",
                      "achieved": mix["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": mix["frac_of_hbm_peak"], "traffic": None},
     }

@@ -359,8 +359,13 @@ qmlp_status qmlp_linear_batch(const qmlp_qweight *w, int L, const void *x, int M
  * arrays (routing runs on the GPU); ids outside [0, E) are a precondition
  * violation (the kernels clamp them, so nothing is read outside the
  * table).  1 <= k <= E, M <= 16, M*k <= 40.  Every (token, slot) pair runs
- * as one instance: an expert chosen by two tokens is read twice.  Three
- * launches over the M*k instances (LoRA-A, gate/up, down) and one combine.
+ * as one instance: an expert chosen by two tokens is read twice.  Launches
+ * over the M*k instances: LoRA-A (with adapters), gate/up, then down.  With
+ * k <= 4 (and h of the k instances within the down kernel's LDS staging)
+ * the down launch also forms y: one workgroup computes all k instances of
+ * its output rows and adds them in fp32, w[m][j] y_j from j = 0, rounding
+ * once to binary16.  Otherwise each instance's output is rounded to
+ * binary16 and a combine launch adds them in the same order.
  * ws/ws_bytes: at least qmlp_moe_workspace_bytes(...): t, h and the
  * per-instance outputs; no state is kept between calls.
  */

@@ -857,6 +857,12 @@ qmlp_status qmlp_forward_moe(const qmlp_mlp* experts, int E, const void* x, int 
     hipError_t e = b.r > 0 ? launch_lora_a_batch(b, n, st) : hipSuccess;
     if (e == hipSuccess)
         e = launch_gateup_batch(b, n, st);
+    if (down_combine_fits(b, n)) {
+        // each workgroup computes all k instances of its rows and adds them
+        if (e == hipSuccess)
+            e = launch_down_combine(b, n, topk_w, static_cast<uint16_t*>(y), st);
+        return from_hip(e);
+    }
     if (e == hipSuccess)
         e = launch_down_batch(b, n, st);
     if (e == hipSuccess)

@@ -90,6 +90,17 @@ hipError_t launch_moe_combine(const uint16_t* yi, const float* w, int M, int k, 
     return hipGetLastError();
 }
 
+bool down_combine_fits(const BatchArgs& b, int nb) {
+    return b.route && b.M == 1 && b.xdiv >= 1 && nb % b.xdiv == 0 && (b.bd == 4 || (b.bd == 2 && b.gd != 32)) &&
+           down_combine_fits_shape(b.d, b.f, b.xdiv, b.bd);
+}
+
+hipError_t launch_down_combine(const BatchArgs& b, int nb, const float* w, uint16_t* y, hipStream_t st) {
+    if (nb < 1 || nb > kBatchMax || !w || !y || !down_combine_fits(b, nb))
+        return hipErrorInvalidValue;
+    return b.bd == 4 ? launch_down_pipe_combine<4>(b, nb, w, y, st) : launch_down_pipe_combine<2>(b, nb, w, y, st);
+}
+
 // A single block as a batch of one.
 hipError_t launch_down(DownArgs a, hipStream_t st) {
     BatchArgs b{};

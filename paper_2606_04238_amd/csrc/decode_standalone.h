@@ -286,6 +286,82 @@ down_pipe_kernel(BatchArgs b) {
     }
 }
 
+// ---- the pipelined down kernel over routed instances with the combine of
+// the MoE layer folded in (k <= 4 instances per token, one token per
+// workgroup row of the grid).  The workgroup's waves are split into
+// G = 4 / k row groups of k waves; wave j of a group runs instance (token,
+// slot j) over the group's NI items, so all k instances of an output row are
+// computed in one workgroup.  The workgroup stages the h of its k instances
+// (k * 4U staging words, at most kPipeStageWords per thread), each wave puts
+// its fp32 rows into LDS, and after one barrier the sum over the slots in
+// order, w[m][j] y_j from j = 0, is rounded once to binary16 into y[m].
+// Waves past G * k (k = 3) only stage.
+template <int S, int JJ, int B, int NI>
+__global__ void __launch_bounds__(256)
+down_pipe_combine_kernel(BatchArgs b, const float* __restrict__ w, uint16_t* __restrict__ y) {
+    constexpr int CH = B == 2 ? 8 : 4;
+    constexpr int RPI = 64 / S;                      // rows per item
+    constexpr int RPW = NI * RPI;                    // rows per wave
+    const int k = b.xdiv, G = 4 / k, m = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int j = wave % k, grp = wave / k;
+    const bool active = grp < G;
+    const DownArgs a = batch_down_args(b, m * k + (active ? j : 0));
+    extern __shared__ uint4 smem[];
+    __shared__ float part[4][4 * RPW];
+    const int U = a.f / codes_per_unit(B);
+    uint4* hs = smem;
+    float2* cx = reinterpret_cast<float2*>(smem + k * U * CH);
+    const int rbase = blockIdx.x * G * RPW;          // first output row of the workgroup
+    const int row0 = rbase + (active ? grp : 0) * RPW + lane / S;
+    // staging word t: instance slot t / 4U, word t % 4U of its h (a word past
+    // the k instances is given an index past the end: it loads word 0 and
+    // its store is dropped)
+    const uint16_t* hb = b.h + (long)m * k * a.f;
+    using HW = typename std::conditional<B == 2, XWord, uint4>::type;
+    HW hv[kPipeStageWords];
+#pragma unroll
+    for (int i = 0; i < kPipeStageWords; ++i) {
+        const int t = tid + 256 * i, sl = min(t / (4 * U), k - 1), wl = t - sl * 4 * U;
+        if constexpr (B == 2)
+            hv[i] = stage_x_load<1>(hb + (long)sl * a.f, 1, a.f, 0, U, wl);
+        else
+            hv[i] = stage_h_load<1>(hb + (long)sl * a.f, 1, a.f, 0, U, wl);
+    }
+    __builtin_amdgcn_sched_barrier(0);              // keep the h loads ahead of the weights
+    PipeItem<JJ> buf[2];
+    pipe_load<S, JJ, B>(buf[0], a, U, row0, lane);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < kPipeStageWords; ++i) {
+        const int t = tid + 256 * i, sl = min(t / (4 * U), k - 1), wl = t - sl * 4 * U;
+        if constexpr (B == 2)
+            stage_x_store<1>(hs + sl * U * CH, cx + sl * U, U, U, 1, wl, hv[i]);
+        else
+            stage_h_store<1>(hs + sl * U * CH, cx + sl * U, U, U, 1, wl, hv[i]);
+    }
+    __syncthreads();
+    if (active) {
+        const uint4* hj = hs + j * U * CH;
+        const float2* cj = cx + j * U;
+#pragma unroll
+        for (int it = 0; it < NI; ++it) {
+            if (it + 1 < NI)
+                pipe_load<S, JJ, B>(buf[(it + 1) & 1], a, U, row0 + (it + 1) * RPI, lane);
+            const float v = group_sum<S>(pipe_dot<S, JJ, B>(buf[it & 1], hj, cj, U, lane));
+            if (lane % S == 0)
+                part[j][grp * RPW + it * RPI + lane / S] = v;
+        }
+    }
+    __syncthreads();
+    if (tid < G * RPW && rbase + tid < a.d) {
+        float acc = 0.0f;
+        for (int s = 0; s < k; ++s)
+            acc += w[m * k + s] * part[s][tid];
+        y[(long)m * a.d + rbase + tid] = (uint16_t)f2h(acc);
+    }
+}
+
 
 // The pipelined kernel serves M = 1 launches whose whole h fits the LDS
 // budget; S = the fewest lanes per row with at most kPipeMaxUnits units each.
@@ -359,6 +435,47 @@ hipError_t launch_down_pipe(const BatchArgs& args, int nb, hipStream_t st) {
     const int rows_per_block = 4 * kPipeItems * (64 / (S ? S : 64));
     const dim3 grid((args.d + rows_per_block - 1) / rows_per_block, (unsigned)nb);
     QMLP_PIPE_S(8) QMLP_PIPE_S(16) QMLP_PIPE_S(32) QMLP_PIPE_S(64)
+    return hipErrorInvalidValue;
+}
+
+#define QMLP_PIPE_CMB_CASE(S_, J_)                                                        \
+    if (S == S_ && JJ == J_) {                                                            \
+        auto kf = down_pipe_combine_kernel<S_, J_, B, kPipeItems>;                        \
+        hipError_t e = set_lds(kf, lds);                                                  \
+        if (e != hipSuccess) return e;                                                    \
+        kf<<<grid, 256, lds, st>>>(args, w, y);                                           \
+        return hipGetLastError();                                                         \
+    }
+#define QMLP_PIPE_CMB_S(S_) QMLP_PIPE_CMB_CASE(S_, 1) QMLP_PIPE_CMB_CASE(S_, 2)             \
+    QMLP_PIPE_CMB_CASE(S_, 3) QMLP_PIPE_CMB_CASE(S_, 4) QMLP_PIPE_CMB_CASE(S_, 5)         \
+    QMLP_PIPE_CMB_CASE(S_, 6)
+
+// Whether down_pipe_combine_kernel takes a routed batch of ntok * k
+// instances at one token each: k <= 4, h of the k instances within the
+// staging words and the LDS budget, and the lanes per row of the routed
+// pipelined launch.
+inline bool down_combine_fits_shape(int d, int f, int k, int bits) {
+    const int U = f / codes_per_unit(bits);
+    return k >= 1 && k <= 4 && d >= 1 && pipe_lanes(U) != 0 && k * 4 * U <= 256 * kPipeStageWords &&
+           (size_t)k * U * (bits == 2 ? GU_UNIT_BYTES : DN_UNIT_BYTES) <= (size_t)kLdsBudget;
+}
+
+// y [ntok][d] = sum_j w[m][j] * down(instance m k + j): args is the routed
+// batch (M = 1, xdiv = k), nb = ntok * k; the caller checks
+// down_combine_fits_shape first.
+template <int B>
+hipError_t launch_down_pipe_combine(const BatchArgs& args, int nb, const float* w, uint16_t* y,
+                                    hipStream_t st) {
+    const int k = args.xdiv;
+    const int U = args.f / codes_per_unit(B);
+    const int S = routed_pipe_lanes(U, args.d, nb, device_cu_count());
+    const int JJ = S ? (U + S - 1) / S : 0;
+    if (!S || k < 1 || k > 4 || nb % k != 0)
+        return hipErrorInvalidValue;
+    const size_t lds = (size_t)k * U * (B == 2 ? GU_UNIT_BYTES : DN_UNIT_BYTES);
+    const int rows_per_block = (4 / k) * kPipeItems * (64 / S);
+    const dim3 grid((args.d + rows_per_block - 1) / rows_per_block, (unsigned)(nb / k));
+    QMLP_PIPE_CMB_S(8) QMLP_PIPE_CMB_S(16) QMLP_PIPE_CMB_S(32) QMLP_PIPE_CMB_S(64)
     return hipErrorInvalidValue;
 }
 

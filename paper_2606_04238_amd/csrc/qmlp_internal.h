@@ -123,6 +123,13 @@ struct BatchArgs {
     int xdiv;
 };
 hipError_t launch_lora_a_batch(const BatchArgs& b, int nb, hipStream_t st);
+// Down over a routed batch (M = 1, k = xdiv instances per token) with the
+// routing-weighted combine folded in: y [nb/k][d] binary16, w [nb/k][k].
+// down_combine_fits says whether the folded kernel takes the shape (k <= 4,
+// the instances' h within its staging); otherwise launch_down_combine
+// returns hipErrorInvalidValue before launching anything.
+bool down_combine_fits(const BatchArgs& b, int nb);
+hipError_t launch_down_combine(const BatchArgs& b, int nb, const float* w, uint16_t* y, hipStream_t st);
 // The streamed path of a batch at one token (decode_stream.hip): one
 // persistent gate/up launch and one persistent down launch over all blocks of
 // the batch, after launch_lora_a_batch.  Binary16, 2-bit gate/up and 4-bit

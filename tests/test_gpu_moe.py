@@ -148,3 +148,28 @@ def test_moe_route_ids_outside_the_table_are_clamped(q):
     good = q.forward_moe(experts, x, torch.tensor([[2], [0]], dtype=torch.int32, device="cuda"), w)
     torch.cuda.synchronize()
     assert torch.equal(bad.view(torch.int16), good.view(torch.int16))
+
+
+
+@pytest.mark.parametrize("k", [3, 6])
+def test_moe_repeated_calls_on_one_workspace(q, k):
+    """Up to four slots per token the down launch also adds the slots (each
+    workgroup runs all k instances of its rows; at k = 3 one wave of four
+    only stages); past four a combine launch adds them.  Both forms, over
+    three calls with other inputs and routing on one workspace."""
+    cfg = wl.Config("moe_reuse", M=1, d=1024, f=768, g=64, r=8, L=1)
+    E, M = 8, 4
+    lays = [wl.layer(cfg, e) for e in range(E)]
+    experts = q.Layers([gpu_mlp(lay) for lay in lays])
+    oq = [oracle_q(lay) + (lay.A_gate, lay.B_gate, lay.A_up, lay.B_up) for lay in lays]
+    ws = torch.zeros(q.moe_workspace_bytes(experts, M, k), dtype=torch.uint8, device="cuda")
+    for call in range(3):
+        print("\n[case] moe k %d call %d" % (k, call), flush=True)
+        x = wl.activations(cfg, 40 + call, 0, M=M)
+        idx, w = wl.routing(M, E, k, call)
+        y = q.forward_moe(experts, act_tensor(x), torch.from_numpy(idx).cuda(),
+                          torch.from_numpy(w).cuda(), ws=ws)
+        torch.cuda.synchronize()
+        err = orc.max_rel_err(values_of(y), orc.moe_forward(oq, idx, w, x, lora_scale=cfg.lora_scale))
+        print("max-rel %.2e" % err)
+        assert err <= Y_TOL
