@@ -602,11 +602,11 @@ def moe_main(mc: wl.MoeConfig, args):
         "config": {"workload": "%s: %d MoE layers of %d experts (d=%d, f=%d, group %d, LoRA rank %d), "
                                "top-%d routing, M=%d, every layer on its own input and routing"
                                % (mc.name, L, E, cfg.d, cfg.f, cfg.g, cfg.r, k, M),
-                   "path": "qmlp_forward_moe (batched stand-alone kernels over the routed instances)",
+                   "path": "qmlp_forward_moe (two launches over the routed instances: gate/up with LoRA-A, down with the routing-weighted sum)",
                    "widths": res,
                    "gain_pct": round((t4 / tm - 1) * 100, 1),
                    "capture_pct": round((1 / tm - 1 / t4) / (1 / t2 - 1 / t4) * 100, 1)},
-        "roofline": {"bound": "hbm", "kernel": "MoE layer step (LoRA-A, gate/up, down with the routing-weighted sum)",
+        "roofline": {"bound": "hbm", "kernel": "MoE layer step (gate/up with LoRA-A, down with the routing-weighted sum)",
                      "achieved": mix["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": mix["frac_of_hbm_peak"], "traffic": None},
     }

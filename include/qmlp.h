@@ -359,15 +359,23 @@ qmlp_status qmlp_linear_batch(const qmlp_qweight *w, int L, const void *x, int M
  * arrays (routing runs on the GPU); ids outside [0, E) are a precondition
  * violation (the kernels clamp them, so nothing is read outside the
  * table).  1 <= k <= E, M <= 16, M*k <= 40.  Every (token, slot) pair runs
- * as one instance: an expert chosen by two tokens is read twice.  Launches
- * over the M*k instances: LoRA-A (with adapters), gate/up, then down.  With
+ * as one instance: an expert chosen by two tokens is read twice.  Two
+ * launches over the M*k instances: gate/up, whose first workgroups of each
+ * instance compute LoRA-A (with adapters) and hand t to the others as tagged
+ * words, then down.  With
  * k <= 4 (and h of the k instances within the down kernel's LDS staging)
  * the down launch also forms y: one workgroup computes all k instances of
  * its output rows and adds them in fp32, w[m][j] y_j from j = 0, rounding
  * once to binary16.  Otherwise each instance's output is rounded to
  * binary16 and a combine launch adds them in the same order.
- * ws/ws_bytes: at least qmlp_moe_workspace_bytes(...): t, h and the
- * per-instance outputs; no state is kept between calls.
+ * ws/ws_bytes: at least qmlp_moe_workspace_bytes(...): a 1024-byte control
+ * block (uint32 words on 128-byte lines: word 0 counts the calls and tags
+ * each call's t words, word 160 holds sticky error bits, 1 = a wait for t
+ * gave up), t as tagged 64-bit words [M*k][2r], h and the per-instance
+ * outputs.  The workspace must be ZERO before its first call, and zeroed
+ * again after a call failed or an error bit appeared (the results of that
+ * call are invalid).  One workspace serves one call at a time: calls that
+ * overlap in time on the same workspace race.
  */
 size_t qmlp_moe_workspace_bytes(const qmlp_mlp *experts, int E, int M, int k, qmlp_dtype dtype);
 

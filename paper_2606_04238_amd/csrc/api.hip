@@ -808,7 +808,8 @@ size_t qmlp_moe_workspace_bytes(const qmlp_mlp* experts, int E, int M, int k, qm
         dtype != QMLP_F16 || check_layers(experts, E, 1, dtype) != QMLP_OK)
         return 0;
     const int n = M * k;
-    return kCtlBytes + batch_t_bytes(experts, n, 1) + batch_h_bytes(experts, n, 1) +
+    // control block, t as tagged 64-bit words, h, the instances' outputs
+    return kCtlBytes + batch_t_bytes(experts, n, 1, 2) + batch_h_bytes(experts, n, 1) +
            round256((size_t)n * experts[0].gate.k_in * 2);
 }
 
@@ -841,9 +842,10 @@ qmlp_status qmlp_forward_moe(const qmlp_mlp* experts, int E, const void* x, int 
     b.nexp = E;
     b.xdiv = k;                                   // instance l runs token l / k
     b.x = static_cast<const uint16_t*>(x);
-    b.t = reinterpret_cast<float*>(base + kCtlBytes);
-    b.h = reinterpret_cast<uint16_t*>(base + kCtlBytes + batch_t_bytes(&a, n, 1));
-    b.y = reinterpret_cast<uint16_t*>(base + kCtlBytes + batch_t_bytes(&a, n, 1) +
+    unsigned* ctl = reinterpret_cast<unsigned*>(base);
+    auto* t64 = reinterpret_cast<unsigned long long*>(base + kCtlBytes);
+    b.h = reinterpret_cast<uint16_t*>(base + kCtlBytes + batch_t_bytes(&a, n, 1, 2));
+    b.y = reinterpret_cast<uint16_t*>(base + kCtlBytes + batch_t_bytes(&a, n, 1, 2) +
                                       batch_h_bytes(&a, n, 1));
     b.M = 1;
     b.d = d;
@@ -854,19 +856,21 @@ qmlp_status qmlp_forward_moe(const qmlp_mlp* experts, int E, const void* x, int 
     b.gd = a.down.group;
     b.bd = a.down.bits;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    hipError_t e = b.r > 0 ? launch_lora_a_batch(b, n, st) : hipSuccess;
-    if (e == hipSuccess)
-        e = launch_gateup_batch(b, n, st);
+    // LoRA-A runs in the gate/up launch (rank > 0 at one token per
+    // instance: always here); t is handed over as tagged words
+    if (b.r > 0 && !gateup_lora_fits(b, n))
+        return QMLP_ERR_UNSUPPORTED;
+    hipError_t e = b.r > 0 ? launch_gateup_lora_batch(b, n, t64, ctl, st) : launch_gateup_batch(b, n, st);
     if (down_combine_fits(b, n)) {
         // each workgroup computes all k instances of its rows and adds them
         if (e == hipSuccess)
-            e = launch_down_combine(b, n, topk_w, static_cast<uint16_t*>(y), st);
+            e = launch_down_combine(b, n, topk_w, static_cast<uint16_t*>(y), ctl, st);
         return from_hip(e);
     }
     if (e == hipSuccess)
         e = launch_down_batch(b, n, st);
     if (e == hipSuccess)
-        e = launch_moe_combine(b.y, topk_w, M, k, d, static_cast<uint16_t*>(y), st);
+        e = launch_moe_combine(b.y, topk_w, M, k, d, static_cast<uint16_t*>(y), ctl, st);
     return from_hip(e);
 }
 

@@ -262,14 +262,14 @@ __device__ __forceinline__ void stage_h(uint4* hs, float2* cx, int UC, const uin
 // SPLIT = group 32 at 2 bits (the paper's INT2 grouping, Sec. 3.3 and
 // Sec. 4.1): a unit spans two groups, so each carries two metadata words
 // and two (C, X) pairs (stage_x<MT, true>).
-template <int MT, int S, int MAXJ, int B = 2, bool SPLIT = false>
+template <int MT, int S, int MAXJ, int B = 2, bool SPLIT = false, bool TP = (MT == 1 && B == 2)>
 struct GuItem {
     static constexpr int NM = SPLIT ? 2 : 1;     // metadata words per unit
     uint4 qg[MAXJ], qu[MAXJ];
     uint2 hg[B == 3 ? MAXJ : 1], hu[B == 3 ? MAXJ : 1];   // 1-bit planes (3 bits)
     uint32_t mg[MAXJ][NM], mu[MAXJ][NM];
     uint32_t bg[4], bu[4];          // LoRA-B row slice, raw binary16
-    static constexpr bool TPRE = MT == 1 && B == 2;  // t prefetched with the weights
+    static constexpr bool TPRE = TP;  // t prefetched with the weights (one token, 2 bits)
     float tg[TPRE ? 4 : 1], tu[TPRE ? 4 : 1];        // the lane's slice of t
     float G[MT], U[MT];
     int row;
@@ -277,8 +277,8 @@ struct GuItem {
 };
 
 // Issue the loads of one gate/up item: S lanes per row, rows row0 + lane/S.
-template <int MT, int S, int MAXJ, int B, bool SPLIT>
-__device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ, B, SPLIT>& it, const GateUpArgs& a,
+template <int MT, int S, int MAXJ, int B, bool SPLIT, bool TP>
+__device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ, B, SPLIT, TP>& it, const GateUpArgs& a,
                                         int row0, bool active, int lane) {
     static_assert((B == 2 || B == 3 || B == 4) && (!SPLIT || B != 4), "gate/up at 2, 3 or 4 bits");
     constexpr int UI = codes_per_unit(B);
@@ -316,7 +316,7 @@ __device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ, B, SPLIT>& it, const
                 it.hu[i] = pu[uu];
             }
 #pragma unroll
-            for (int h = 0; h < GuItem<MT, S, MAXJ, B, SPLIT>::NM; ++h) {
+            for (int h = 0; h < GuItem<MT, S, MAXJ, B, SPLIT, TP>::NM; ++h) {
                 const int gi = SPLIT ? 2 * uu + h : uu / upg;
                 it.mg[i][h] = load_stream(mg + gi);
                 it.mu[i][h] = load_stream(mu + gi);
@@ -339,7 +339,7 @@ __device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ, B, SPLIT>& it, const
     // makes no second trip to memory; with rank 0 a readable dummy (x)
     // stands in.  (With it the 4-bit item measured slower, 8.1 -> 8.6 us per
     // uniform-W4 block, so that item reads t in the epilogue.)
-    if constexpr (GuItem<MT, S, MAXJ, B, SPLIT>::TPRE) {
+    if constexpr (GuItem<MT, S, MAXJ, B, SPLIT, TP>::TPRE) {
         const float* tp = a.r > 0 ? a.t : reinterpret_cast<const float*>(a.x);
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
@@ -354,11 +354,11 @@ __device__ __forceinline__ void gu_load(GuItem<MT, S, MAXJ, B, SPLIT>& it, const
 }
 
 // Dot products of the item's units that fall in the staged chunk [u0, u0+uc).
-template <int MT, int S, int MAXJ, int B, bool SPLIT>
-__device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ, B, SPLIT>& it, const uint4* xs,
+template <int MT, int S, int MAXJ, int B, bool SPLIT, bool TP>
+__device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ, B, SPLIT, TP>& it, const uint4* xs,
                                               const float2* cx, int UC, int d, int u0, int uc,
                                               int lane) {
-    constexpr int NM = GuItem<MT, S, MAXJ, B, SPLIT>::NM;
+    constexpr int NM = GuItem<MT, S, MAXJ, B, SPLIT, TP>::NM;
     constexpr int UI = codes_per_unit(B);
     const uint32_t mv = 0x64006400u;           // (the standalone kernels keep the literal)
     const int s = lane % S;
@@ -486,8 +486,8 @@ __device__ __forceinline__ void gu_accumulate(GuItem<MT, S, MAXJ, B, SPLIT>& it,
 
 // LoRA-B on the lane's rank slice, reduction over the S lanes of each row,
 // and the epilogue h = SiLU(G) * U (t: [M][2r] fp32, gate ranks then up).
-template <int MT, int S, int MAXJ, int B, bool SPLIT>
-__device__ __forceinline__ void gu_finish(GuItem<MT, S, MAXJ, B, SPLIT>& it, const GateUpArgs& a,
+template <int MT, int S, int MAXJ, int B, bool SPLIT, bool TP>
+__device__ __forceinline__ void gu_finish(GuItem<MT, S, MAXJ, B, SPLIT, TP>& it, const GateUpArgs& a,
                                           const float* t, uint16_t* h, int lane) {
     const int s = lane % S;
     if (a.r > 0) {
@@ -503,7 +503,7 @@ __device__ __forceinline__ void gu_finish(GuItem<MT, S, MAXJ, B, SPLIT>& it, con
                         uint32_t bgc = it.bg[c], buc = it.bu[c];
                         pin(bgc);
                         pin(buc);
-                        if constexpr (GuItem<MT, S, MAXJ, B, SPLIT>::TPRE) {
+                        if constexpr (GuItem<MT, S, MAXJ, B, SPLIT, TP>::TPRE) {
                             lg += h2f(bgc) * it.tg[c];
                             lu += h2f(buc) * it.tu[c];
                         } else {
@@ -1203,6 +1203,43 @@ __device__ __forceinline__ void lora_a_row(const uint16_t* Ag, const uint16_t* A
         if (lane == 0 && m < M)   // device-coherent: read by other compute units
             __hip_atomic_store(t + m * 2 * r + c, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+}
+
+// The call counter of a control block advances by one.  Called by one lane
+// of one workgroup of a launch that runs, in stream order, after every
+// reader of the counter in the call and before the next call's first one.
+__device__ __forceinline__ void advance_call_counter(unsigned* c) {
+    const unsigned e = __hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(c, e + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One row of [A_g; A_u] against one token: the dot over d (every load of
+// the row issued before the first multiply, as in lora_a_row), summed over
+// the wave; every lane returns the sum.
+template <int KA>
+__device__ __forceinline__ float lora_a_dot(const uint16_t* a, const uint16_t* x, int d, int lane) {
+    const int nch = d / 8;
+    float acc = 0.0f;
+    for (int base = 0; base < nch; base += 64 * KA) {
+        uint4 av[KA], xv[KA];
+#pragma unroll
+        for (int k = 0; k < KA; ++k) {
+            const int ch = base + lane + 64 * k;
+            const int cc = ch < nch ? ch : 0;
+            av[k] = *reinterpret_cast<const uint4*>(a + cc * 8);
+            xv[k] = *reinterpret_cast<const uint4*>(x + cc * 8);
+        }
+#pragma unroll
+        for (int k = 0; k < KA; ++k) {
+            if (base + lane + 64 * k < nch) {
+                acc = dot2(av[k].x, xv[k].x, acc);
+                acc = dot2(av[k].y, xv[k].y, acc);
+                acc = dot2(av[k].z, xv[k].z, acc);
+                acc = dot2(av[k].w, xv[k].w, acc);
+            }
+        }
+    }
+    return group_sum<64>(acc);
 }
 
 }  // namespace qmlp

@@ -56,8 +56,10 @@ namespace qmlp {
 template <int KM>
 __global__ void __launch_bounds__(256)
 moe_combine_kernel(const uint16_t* __restrict__ yi, const float* __restrict__ w, int M, int k,
-                   int d, uint16_t* __restrict__ y) {
+                   int d, uint16_t* __restrict__ y, unsigned* ctl) {
     const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i == 0 && ctl)
+        advance_call_counter(ctl + kMoeCtlEpoch);
     if (i >= (long)M * d)
         return;
     const long m = i / d, c = i - m * d;
@@ -78,15 +80,15 @@ moe_combine_kernel(const uint16_t* __restrict__ yi, const float* __restrict__ w,
 }
 
 hipError_t launch_moe_combine(const uint16_t* yi, const float* w, int M, int k, int d, uint16_t* y,
-                              hipStream_t st) {
+                              unsigned* ctl, hipStream_t st) {
     const long n = (long)M * d;
     const unsigned grid = (unsigned)((n + 255) / 256);
     if (k <= 4)
-        moe_combine_kernel<4><<<grid, 256, 0, st>>>(yi, w, M, k, d, y);
+        moe_combine_kernel<4><<<grid, 256, 0, st>>>(yi, w, M, k, d, y, ctl);
     else if (k <= 8)
-        moe_combine_kernel<8><<<grid, 256, 0, st>>>(yi, w, M, k, d, y);
+        moe_combine_kernel<8><<<grid, 256, 0, st>>>(yi, w, M, k, d, y, ctl);
     else
-        moe_combine_kernel<kBatchMax><<<grid, 256, 0, st>>>(yi, w, M, k, d, y);
+        moe_combine_kernel<kBatchMax><<<grid, 256, 0, st>>>(yi, w, M, k, d, y, ctl);
     return hipGetLastError();
 }
 
@@ -95,10 +97,12 @@ bool down_combine_fits(const BatchArgs& b, int nb) {
            down_combine_fits_shape(b.d, b.f, b.xdiv, b.bd);
 }
 
-hipError_t launch_down_combine(const BatchArgs& b, int nb, const float* w, uint16_t* y, hipStream_t st) {
+hipError_t launch_down_combine(const BatchArgs& b, int nb, const float* w, uint16_t* y, unsigned* ctl,
+                               hipStream_t st) {
     if (nb < 1 || nb > kBatchMax || !w || !y || !down_combine_fits(b, nb))
         return hipErrorInvalidValue;
-    return b.bd == 4 ? launch_down_pipe_combine<4>(b, nb, w, y, st) : launch_down_pipe_combine<2>(b, nb, w, y, st);
+    return b.bd == 4 ? launch_down_pipe_combine<4>(b, nb, w, y, ctl, st)
+                     : launch_down_pipe_combine<2>(b, nb, w, y, ctl, st);
 }
 
 // A single block as a batch of one.

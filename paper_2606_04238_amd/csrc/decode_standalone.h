@@ -85,6 +85,108 @@ gateup_kernel(BatchArgs b) {
     gu_finish(it, a, a.t, a.h, lane);
 }
 
+// ---- gate/up over routed instances at one token with the LoRA-A projection
+// in the same launch.  Workgroup column x < LB of instance l (LB = 2r/4
+// rounded up) computes four rows c of t_l = [A_g; A_u] x_l, one per wave,
+// and publishes each as a tagged word (fp32 bits | tag << 32, tag = the call
+// counter plus one, never 0) with a device-coherent store.  The other
+// columns run the gate/up item as gateup_kernel does; after their first
+// staging barrier the block's first 2r threads issue device-coherent loads
+// of t_l (they return behind the weights), and before the epilogue they
+// re-read any word that does not yet show this call's tag (bounded: after
+// kTagSpinLimit polls the word is taken as it is and error bit 1 is set).
+// The LoRA-A columns of an instance precede its gate/up columns in dispatch
+// order, so every wait is on a workgroup that is already resident.
+constexpr unsigned kTagSpinLimit = 1u << 18;
+
+template <int S, int MAXJ, int B, bool SPLIT>
+__global__ void __launch_bounds__(256)
+gateup_lora_kernel(BatchArgs b, unsigned long long* t64, unsigned* ctl, int LB) {
+    const int l = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const unsigned epoch = __hip_atomic_load(ctl + kMoeCtlEpoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned tag = epoch % 0xFFFFFFFFu + 1u;
+    unsigned long long* tl = t64 + (long)l * 2 * b.r;
+    if ((int)blockIdx.x < LB) {
+        const int c = blockIdx.x * 4 + wave;
+        if (c < 2 * b.r) {
+            const StackLayerDesc& w = b.lay[batch_expert(b, l)];
+            const uint16_t* arow = c < b.r ? w.Ag + (long)c * b.d : w.Au + (long)(c - b.r) * b.d;
+            const float v = lora_a_dot<12>(arow, batch_x(b, l), b.d, lane);
+            if (lane == 0)
+                __hip_atomic_store(tl + c, (unsigned long long)__float_as_uint(v) | ((unsigned long long)tag << 32),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        return;
+    }
+    GateUpArgs a = batch_gateup_args(b, l);
+    constexpr int CH = B == 2 ? 8 : B == 3 ? 16 : 4;
+    extern __shared__ uint4 smem[];
+    __shared__ float ts[64];
+    const int UC = a.uc;
+    uint4* xs = smem;
+    float2* cx = reinterpret_cast<float2*>(smem + UC * CH);
+    GuItem<1, S, MAXJ, B, SPLIT, false> it;
+    gu_load(it, a, ((blockIdx.x - LB) * 4 + wave) * (64 / S), true, lane);
+    const int U = a.d / codes_per_unit(B);
+    const bool poll = tid < 2 * a.r;
+    unsigned long long tv = 0;
+    for (int u0 = 0; u0 < U; u0 += UC) {
+        const int uc = min(UC, U - u0);
+        __syncthreads();
+        if constexpr (B == 2)
+            stage_x<1, SPLIT>(xs, cx, UC, a.x, 1, a.d, u0, uc, tid, 256);
+        else if constexpr (B == 3)
+            stage_x3<1, SPLIT>(xs, cx, UC, a.x, 1, a.d, u0, uc, tid, 256);
+        else
+            stage_h<1>(xs, cx, UC, a.x, 1, a.d, u0, uc, tid, 256);
+        __syncthreads();
+        if (u0 == 0 && poll)
+            tv = __hip_atomic_load(tl + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        gu_accumulate(it, xs, cx, UC, a.d, u0, uc, lane);
+    }
+    if (poll) {
+        for (unsigned n = 0; (unsigned)(tv >> 32) != tag && n < kTagSpinLimit; ++n) {
+            __builtin_amdgcn_s_sleep(2);
+            tv = __hip_atomic_load(tl + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if ((unsigned)(tv >> 32) != tag)
+            __hip_atomic_fetch_or(ctl + kMoeCtlErr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ts[tid] = __uint_as_float((uint32_t)tv);
+    }
+    __syncthreads();
+    gu_finish(it, a, ts, a.h, lane);
+}
+
+#define QMLP_GUL_CASE(S_, J_)                                                             \
+    if (S == S_ && mj == J_) {                                                            \
+        auto k = gateup_lora_kernel<S_, J_, B, SPLIT>;                                    \
+        hipError_t e = set_lds(k, lds);                                                   \
+        if (e != hipSuccess) return e;                                                    \
+        k<<<grid, 256, lds, st>>>(args, t64, ctl, LB);                                    \
+        return hipGetLastError();                                                         \
+    }
+#define QMLP_GUL_S(S_) QMLP_GUL_CASE(S_, 8) QMLP_GUL_CASE(S_, 16)
+
+// Routed instances at one token, rank 1..32: LB LoRA-A columns, then the
+// gate/up columns of launch_gateup_bits's shape at S lanes per row.
+template <int B, bool SPLIT>
+hipError_t launch_gateup_lora_bits(BatchArgs args, int nb, int S, unsigned long long* t64, unsigned* ctl,
+                                   hipStream_t st) {
+    if (args.M != 1 || args.r < 1 || 2 * args.r > 64 || !t64 || !ctl)
+        return hipErrorInvalidValue;
+    const int U = args.d / codes_per_unit(B);
+    const int J = (U + S - 1) / S;
+    const int mj = maxj_for(J);
+    const size_t unit_bytes = B == 4 ? DN_UNIT_BYTES : (B == 3 ? 16 : 8) * 16 + 8 * (SPLIT ? 2 : 1);
+    args.uc = units_per_chunk(U, S, unit_bytes, 1);
+    const size_t lds = (size_t)args.uc * unit_bytes;
+    const int LB = (2 * args.r + 3) / 4;
+    const int rows_per_block = 4 * (64 / S);
+    const dim3 grid((unsigned)(LB + (args.f + rows_per_block - 1) / rows_per_block), (unsigned)nb);
+    QMLP_GUL_S(8) QMLP_GUL_S(16) QMLP_GUL_S(32) QMLP_GUL_S(64)
+    return hipErrorInvalidValue;
+}
+
 #define QMLP_GU_CASE(MT_, S_, J_)                                                         \
     if (mt == MT_ && S == S_ && mj == J_) {                                               \
         auto k = gateup_kernel<MT_, S_, J_, B, SPLIT, NT>;                                \
@@ -298,7 +400,8 @@ down_pipe_kernel(BatchArgs b) {
 // Waves past G * k (k = 3) only stage.
 template <int S, int JJ, int B, int NI>
 __global__ void __launch_bounds__(256)
-down_pipe_combine_kernel(BatchArgs b, const float* __restrict__ w, uint16_t* __restrict__ y) {
+down_pipe_combine_kernel(BatchArgs b, const float* __restrict__ w, uint16_t* __restrict__ y,
+                         unsigned* ctl) {
     constexpr int CH = B == 2 ? 8 : 4;
     constexpr int RPI = 64 / S;                      // rows per item
     constexpr int RPW = NI * RPI;                    // rows per wave
@@ -306,6 +409,8 @@ down_pipe_combine_kernel(BatchArgs b, const float* __restrict__ w, uint16_t* __r
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int j = wave % k, grp = wave / k;
     const bool active = grp < G;
+    if (ctl && tid == 0 && blockIdx.x == 0 && blockIdx.y == 0)
+        advance_call_counter(ctl + kMoeCtlEpoch);
     const DownArgs a = batch_down_args(b, m * k + (active ? j : 0));
     extern __shared__ uint4 smem[];
     __shared__ float part[4][4 * RPW];
@@ -443,7 +548,7 @@ hipError_t launch_down_pipe(const BatchArgs& args, int nb, hipStream_t st) {
         auto kf = down_pipe_combine_kernel<S_, J_, B, kPipeItems>;                        \
         hipError_t e = set_lds(kf, lds);                                                  \
         if (e != hipSuccess) return e;                                                    \
-        kf<<<grid, 256, lds, st>>>(args, w, y);                                           \
+        kf<<<grid, 256, lds, st>>>(args, w, y, ctl);                                      \
         return hipGetLastError();                                                         \
     }
 #define QMLP_PIPE_CMB_S(S_) QMLP_PIPE_CMB_CASE(S_, 1) QMLP_PIPE_CMB_CASE(S_, 2)             \
@@ -465,7 +570,7 @@ inline bool down_combine_fits_shape(int d, int f, int k, int bits) {
 // down_combine_fits_shape first.
 template <int B>
 hipError_t launch_down_pipe_combine(const BatchArgs& args, int nb, const float* w, uint16_t* y,
-                                    hipStream_t st) {
+                                    unsigned* ctl, hipStream_t st) {
     const int k = args.xdiv;
     const int U = args.f / codes_per_unit(B);
     const int S = routed_pipe_lanes(U, args.d, nb, device_cu_count());
@@ -527,6 +632,16 @@ hipError_t launch_down_bits(BatchArgs args, int nb, int S, hipStream_t st) {
     extern template hipError_t launch_gateup_bits<4, false, 256>(BatchArgs, int, int, hipStream_t);  \
     extern template hipError_t launch_gateup_bits<3, false, 256>(BatchArgs, int, int, hipStream_t);  \
     extern template hipError_t launch_gateup_bits<3, true, 256>(BatchArgs, int, int, hipStream_t);   \
+    extern template hipError_t launch_gateup_lora_bits<2, false>(BatchArgs, int, int, unsigned long long*, \
+                                                                 unsigned*, hipStream_t);            \
+    extern template hipError_t launch_gateup_lora_bits<2, true>(BatchArgs, int, int, unsigned long long*,  \
+                                                                unsigned*, hipStream_t);             \
+    extern template hipError_t launch_gateup_lora_bits<3, false>(BatchArgs, int, int, unsigned long long*, \
+                                                                 unsigned*, hipStream_t);            \
+    extern template hipError_t launch_gateup_lora_bits<3, true>(BatchArgs, int, int, unsigned long long*,  \
+                                                                unsigned*, hipStream_t);             \
+    extern template hipError_t launch_gateup_lora_bits<4, false>(BatchArgs, int, int, unsigned long long*, \
+                                                                 unsigned*, hipStream_t);            \
     extern template hipError_t launch_down_bits<2, 256>(BatchArgs, int, int, hipStream_t);           \
     extern template hipError_t launch_down_bits<2, 1024>(BatchArgs, int, int, hipStream_t);          \
     extern template hipError_t launch_down_bits<4, 256>(BatchArgs, int, int, hipStream_t);           \

@@ -123,13 +123,28 @@ struct BatchArgs {
     int xdiv;
 };
 hipError_t launch_lora_a_batch(const BatchArgs& b, int nb, hipStream_t st);
+// The routed-expert layer's control words (uint32 indices into the
+// workspace's control block, each on its own 128-byte line): the call
+// counter, whose value plus one tags this call's LoRA-A words, and sticky
+// error bits (1 = a wait for t gave up).
+constexpr int kMoeCtlEpoch = 0, kMoeCtlErr = 160;
+// Gate/up over a routed batch at one token with the LoRA-A projection in the
+// same launch: the first workgroups of each instance compute t and publish
+// it as tagged 64-bit words (fp32 bits | tag << 32) in t64 [nb][2r]; the
+// gate/up workgroups read them for the LoRA-B term.  gateup_lora_fits says
+// whether it takes the shape (rank > 0, one token per instance).
+bool gateup_lora_fits(const BatchArgs& b, int nb);
+hipError_t launch_gateup_lora_batch(const BatchArgs& b, int nb, unsigned long long* t64, unsigned* ctl,
+                                    hipStream_t st);
 // Down over a routed batch (M = 1, k = xdiv instances per token) with the
 // routing-weighted combine folded in: y [nb/k][d] binary16, w [nb/k][k].
 // down_combine_fits says whether the folded kernel takes the shape (k <= 4,
 // the instances' h within its staging); otherwise launch_down_combine
 // returns hipErrorInvalidValue before launching anything.
 bool down_combine_fits(const BatchArgs& b, int nb);
-hipError_t launch_down_combine(const BatchArgs& b, int nb, const float* w, uint16_t* y, hipStream_t st);
+// ctl: the control block; its call counter advances once the sums are written.
+hipError_t launch_down_combine(const BatchArgs& b, int nb, const float* w, uint16_t* y, unsigned* ctl,
+                               hipStream_t st);
 // The streamed path of a batch at one token (decode_stream.hip): one
 // persistent gate/up launch and one persistent down launch over all blocks of
 // the batch, after launch_lora_a_batch.  Binary16, 2-bit gate/up and 4-bit
@@ -155,8 +170,10 @@ hipError_t launch_gateup_batch(const BatchArgs& b, int nb, hipStream_t st);
 hipError_t launch_down_batch(const BatchArgs& b, int nb, hipStream_t st);
 // y[m] = sum_j w[m k + j] * yi[m k + j] over the k routed experts of token m
 // (fp32 sum, one rounding to binary16); yi [M k][d], w [M k], y [M][d].
+// ctl (may be null): the routed layer's control block, whose call counter
+// advances.
 hipError_t launch_moe_combine(const uint16_t* yi, const float* w, int M, int k, int d, uint16_t* y,
-                              hipStream_t st);
+                              unsigned* ctl, hipStream_t st);
 size_t stack_ws_bytes(int d, int f, int r);
 int stack_max_layers();
 // Byte offset of the persistent stack launch's sticky error word in its area.

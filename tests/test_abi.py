@@ -382,7 +382,8 @@ def test_moe_validation(q, lib):
     assert fm(arr, E, w=FAKE + 2) == ALIGN
     need = lib.qmlp_moe_workspace_bytes(arr, E, 3, 2, 0)
     r256 = lambda v: (v + 255) // 256 * 256
-    assert need == 1024 + r256(6 * 16 * 4) + r256(6 * 512 * 2) + r256(6 * 256 * 2)
+    # control block, t as tagged 64-bit words, h, the instances' outputs
+    assert need == 1024 + r256(6 * 16 * 8) + r256(6 * 512 * 2) + r256(6 * 256 * 2)
     assert fm(arr, E, M=3, wsb=need - 1) == WS
     big = _stack_arr(q, *[_mlp(q) for _ in range(41)])
     assert fm(big, 41) == SHAPE

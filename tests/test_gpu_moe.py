@@ -156,7 +156,8 @@ def test_moe_repeated_calls_on_one_workspace(q, k):
     """Up to four slots per token the down launch also adds the slots (each
     workgroup runs all k instances of its rows; at k = 3 one wave of four
     only stages); past four a combine launch adds them.  Both forms, over
-    three calls with other inputs and routing on one workspace."""
+    three calls with other inputs and routing on one workspace (LoRA-A runs
+    in the gate/up launch: each call's t words carry a new tag)."""
     cfg = wl.Config("moe_reuse", M=1, d=1024, f=768, g=64, r=8, L=1)
     E, M = 8, 4
     lays = [wl.layer(cfg, e) for e in range(E)]
@@ -173,3 +174,7 @@ def test_moe_repeated_calls_on_one_workspace(q, k):
         err = orc.max_rel_err(values_of(y), orc.moe_forward(oq, idx, w, x, lora_scale=cfg.lora_scale))
         print("max-rel %.2e" % err)
         assert err <= Y_TOL
+    # the gate/up launch's waits for the LoRA-A words all ended with this
+    # call's tag, and the call counter advanced once per call
+    assert q.workspace_errors(ws) == 0
+    assert int(ws[0:4].view(torch.int32).item()) == 3
