@@ -856,11 +856,11 @@ qmlp_status qmlp_forward_moe(const qmlp_mlp* experts, int E, const void* x, int 
     b.gd = a.down.group;
     b.bd = a.down.bits;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    // LoRA-A runs in the gate/up launch (rank > 0 at one token per
-    // instance: always here); t is handed over as tagged words
-    if (b.r > 0 && !gateup_lora_fits(b, n))
+    // LoRA-A runs in the gate/up launch (one token per instance: always
+    // here); t is handed over as tagged words
+    if (!gateup_routed_fits(b, n))
         return QMLP_ERR_UNSUPPORTED;
-    hipError_t e = b.r > 0 ? launch_gateup_lora_batch(b, n, t64, ctl, st) : launch_gateup_batch(b, n, st);
+    hipError_t e = launch_gateup_routed_batch(b, n, t64, ctl, st);
     if (down_combine_fits(b, n)) {
         // each workgroup computes all k instances of its rows and adds them
         if (e == hipSuccess)

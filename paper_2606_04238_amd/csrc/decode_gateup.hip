@@ -64,25 +64,25 @@ hipError_t launch_gateup_batch(const BatchArgs& b, int nb, hipStream_t st) {
     return hipErrorInvalidValue;
 }
 
-bool gateup_lora_fits(const BatchArgs& b, int nb) {
-    return nb >= 1 && nb <= kBatchMax && b.M == 1 && b.r >= 1 && 2 * b.r <= 64 &&
+bool gateup_routed_fits(const BatchArgs& b, int nb) {
+    return nb >= 1 && nb <= kBatchMax && b.M == 1 && b.r >= 0 && 2 * b.r <= 64 &&
            (b.bg == 2 || b.bg == 3 || b.bg == 4);
 }
 
 // The lanes per row are those of launch_gateup_batch.
-hipError_t launch_gateup_lora_batch(const BatchArgs& b, int nb, unsigned long long* t64, unsigned* ctl,
+hipError_t launch_gateup_routed_batch(const BatchArgs& b, int nb, unsigned long long* t64, unsigned* ctl,
                                     hipStream_t st) {
-    if (!gateup_lora_fits(b, nb))
+    if (!gateup_routed_fits(b, nb))
         return hipErrorInvalidValue;
     const int U = b.d / codes_per_unit(b.bg);
     const int S = b.route ? routed_gateup_lanes(U, b.f, nb, b.bg, device_cu_count()) : lanes_for(U, b.bg);
     if (b.bg == 4)
-        return launch_gateup_lora_bits<4, false>(b, nb, S, t64, ctl, st);
+        return launch_gateup_routed_bits<4, false>(b, nb, S, t64, ctl, st);
     if (b.bg == 3)
-        return b.gg == 32 ? launch_gateup_lora_bits<3, true>(b, nb, S, t64, ctl, st)
-                          : launch_gateup_lora_bits<3, false>(b, nb, S, t64, ctl, st);
-    return b.gg == 32 ? launch_gateup_lora_bits<2, true>(b, nb, S, t64, ctl, st)
-                      : launch_gateup_lora_bits<2, false>(b, nb, S, t64, ctl, st);
+        return b.gg == 32 ? launch_gateup_routed_bits<3, true>(b, nb, S, t64, ctl, st)
+                          : launch_gateup_routed_bits<3, false>(b, nb, S, t64, ctl, st);
+    return b.gg == 32 ? launch_gateup_routed_bits<2, true>(b, nb, S, t64, ctl, st)
+                      : launch_gateup_routed_bits<2, false>(b, nb, S, t64, ctl, st);
 }
 
 // A single block as a batch of one.

@@ -6,7 +6,7 @@ namespace qmlp {
 
 template hipError_t launch_gateup_bits<2, true, 256>(BatchArgs, int, int, hipStream_t);
 
-template hipError_t launch_gateup_lora_bits<2, true>(BatchArgs, int, int, unsigned long long*, unsigned*,
+template hipError_t launch_gateup_routed_bits<2, true>(BatchArgs, int, int, unsigned long long*, unsigned*,
                                                      hipStream_t);
 
 }  // namespace qmlp

@@ -7,9 +7,9 @@ namespace qmlp {
 template hipError_t launch_gateup_bits<3, false, 256>(BatchArgs, int, int, hipStream_t);
 template hipError_t launch_gateup_bits<3, true, 256>(BatchArgs, int, int, hipStream_t);
 
-template hipError_t launch_gateup_lora_bits<3, false>(BatchArgs, int, int, unsigned long long*, unsigned*,
+template hipError_t launch_gateup_routed_bits<3, false>(BatchArgs, int, int, unsigned long long*, unsigned*,
                                                      hipStream_t);
-template hipError_t launch_gateup_lora_bits<3, true>(BatchArgs, int, int, unsigned long long*, unsigned*,
+template hipError_t launch_gateup_routed_bits<3, true>(BatchArgs, int, int, unsigned long long*, unsigned*,
                                                      hipStream_t);
 
 }  // namespace qmlp

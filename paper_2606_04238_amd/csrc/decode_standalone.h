@@ -85,23 +85,27 @@ gateup_kernel(BatchArgs b) {
     gu_finish(it, a, a.t, a.h, lane);
 }
 
-// ---- gate/up over routed instances at one token with the LoRA-A projection
-// in the same launch.  Workgroup column x < LB of instance l (LB = 2r/4
-// rounded up) computes four rows c of t_l = [A_g; A_u] x_l, one per wave,
-// and publishes each as a tagged word (fp32 bits | tag << 32, tag = the call
-// counter plus one, never 0) with a device-coherent store.  The other
-// columns run the gate/up item as gateup_kernel does; after their first
-// staging barrier the block's first 2r threads issue device-coherent loads
-// of t_l (they return behind the weights), and before the epilogue they
-// re-read any word that does not yet show this call's tag (bounded: after
-// kTagSpinLimit polls the word is taken as it is and error bit 1 is set).
-// The LoRA-A columns of an instance precede its gate/up columns in dispatch
-// order, so every wait is on a workgroup that is already resident.
+// ---- gate/up over routed instances at one token, with the LoRA-A
+// projection in the same launch.  With rank r > 0, workgroup column x < LB
+// of instance l (LB = 2r/4 rounded up) computes four rows c of
+// t_l = [A_g; A_u] x_l, one per wave, and publishes each as a tagged word
+// (fp32 bits | tag << 32, tag = the call counter plus one, never 0) with a
+// device-coherent store.  The other columns run the gate/up item: with
+// NXW > 0 (the activation fits one staging pass at NXW words per thread)
+// the activation loads go out BEFORE the weights, so its staging converts
+// while the weight stream is still in flight (loads retire in order);
+// otherwise the chunk loop of gateup_kernel.  After the staging barrier the
+// block's first 2r threads issue device-coherent loads of t_l, and before
+// the epilogue they re-read any word that does not yet show this call's tag
+// (bounded: after kTagSpinLimit polls the word is taken as it is and error
+// bit 1 is set).  The LoRA-A columns of an instance precede its gate/up
+// columns in dispatch order, so every wait is on a workgroup that is already
+// resident.
 constexpr unsigned kTagSpinLimit = 1u << 18;
 
-template <int S, int MAXJ, int B, bool SPLIT>
+template <int S, int MAXJ, int B, bool SPLIT, int NXW>
 __global__ void __launch_bounds__(256)
-gateup_lora_kernel(BatchArgs b, unsigned long long* t64, unsigned* ctl, int LB) {
+gateup_routed_kernel(BatchArgs b, unsigned long long* t64, unsigned* ctl, int LB) {
     const int l = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const unsigned epoch = __hip_atomic_load(ctl + kMoeCtlEpoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const unsigned tag = epoch % 0xFFFFFFFFu + 1u;
@@ -126,23 +130,53 @@ gateup_lora_kernel(BatchArgs b, unsigned long long* t64, unsigned* ctl, int LB) 
     uint4* xs = smem;
     float2* cx = reinterpret_cast<float2*>(smem + UC * CH);
     GuItem<1, S, MAXJ, B, SPLIT, false> it;
-    gu_load(it, a, ((blockIdx.x - LB) * 4 + wave) * (64 / S), true, lane);
+    const int row0 = ((blockIdx.x - LB) * 4 + wave) * (64 / S);
     const int U = a.d / codes_per_unit(B);
     const bool poll = tid < 2 * a.r;
     unsigned long long tv = 0;
-    for (int u0 = 0; u0 < U; u0 += UC) {
-        const int uc = min(UC, U - u0);
+    if constexpr (NXW > 0) {
+        // one pass (UC = U): words past 4U load word 0 and are dropped
+        using HW = typename std::conditional<B == 4, uint4, XWord>::type;
+        HW xw[NXW];
+#pragma unroll
+        for (int k = 0; k < NXW; ++k) {
+            if constexpr (B == 4)
+                xw[k] = stage_h_load<1>(a.x, 1, a.d, 0, U, tid + 256 * k);
+            else
+                xw[k] = stage_x_load<1>(a.x, 1, a.d, 0, U, tid + 256 * k);
+        }
+        __builtin_amdgcn_sched_barrier(0);          // keep the activation loads ahead of the weights
+        gu_load(it, a, row0, true, lane);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int k = 0; k < NXW; ++k) {
+            if constexpr (B == 2)
+                stage_x_store<1, SPLIT>(xs, cx, U, U, 1, tid + 256 * k, xw[k]);
+            else if constexpr (B == 3)
+                stage_x3_store<1, SPLIT>(xs, cx, U, U, 1, tid + 256 * k, xw[k]);
+            else
+                stage_h_store<1>(xs, cx, U, U, 1, tid + 256 * k, xw[k]);
+        }
         __syncthreads();
-        if constexpr (B == 2)
-            stage_x<1, SPLIT>(xs, cx, UC, a.x, 1, a.d, u0, uc, tid, 256);
-        else if constexpr (B == 3)
-            stage_x3<1, SPLIT>(xs, cx, UC, a.x, 1, a.d, u0, uc, tid, 256);
-        else
-            stage_h<1>(xs, cx, UC, a.x, 1, a.d, u0, uc, tid, 256);
-        __syncthreads();
-        if (u0 == 0 && poll)
+        if (poll)
             tv = __hip_atomic_load(tl + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        gu_accumulate(it, xs, cx, UC, a.d, u0, uc, lane);
+        gu_accumulate(it, xs, cx, U, a.d, 0, U, lane);
+    } else {
+        gu_load(it, a, row0, true, lane);
+        for (int u0 = 0; u0 < U; u0 += UC) {
+            const int uc = min(UC, U - u0);
+            __syncthreads();
+            if constexpr (B == 2)
+                stage_x<1, SPLIT>(xs, cx, UC, a.x, 1, a.d, u0, uc, tid, 256);
+            else if constexpr (B == 3)
+                stage_x3<1, SPLIT>(xs, cx, UC, a.x, 1, a.d, u0, uc, tid, 256);
+            else
+                stage_h<1>(xs, cx, UC, a.x, 1, a.d, u0, uc, tid, 256);
+            __syncthreads();
+            if (u0 == 0 && poll)
+                tv = __hip_atomic_load(tl + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            gu_accumulate(it, xs, cx, UC, a.d, u0, uc, lane);
+        }
     }
     if (poll) {
         for (unsigned n = 0; (unsigned)(tv >> 32) != tag && n < kTagSpinLimit; ++n) {
@@ -157,33 +191,37 @@ gateup_lora_kernel(BatchArgs b, unsigned long long* t64, unsigned* ctl, int LB) 
     gu_finish(it, a, ts, a.h, lane);
 }
 
-#define QMLP_GUL_CASE(S_, J_)                                                             \
-    if (S == S_ && mj == J_) {                                                            \
-        auto k = gateup_lora_kernel<S_, J_, B, SPLIT>;                                    \
+#define QMLP_GUR_CASE(S_, J_, X_)                                                         \
+    if (S == S_ && mj == J_ && nxw == X_) {                                               \
+        auto k = gateup_routed_kernel<S_, J_, B, SPLIT, X_>;                              \
         hipError_t e = set_lds(k, lds);                                                   \
         if (e != hipSuccess) return e;                                                    \
         k<<<grid, 256, lds, st>>>(args, t64, ctl, LB);                                    \
         return hipGetLastError();                                                         \
     }
-#define QMLP_GUL_S(S_) QMLP_GUL_CASE(S_, 8) QMLP_GUL_CASE(S_, 16)
+#define QMLP_GUR_S(S_) QMLP_GUR_CASE(S_, 8, 0) QMLP_GUR_CASE(S_, 16, 0) QMLP_GUR_CASE(S_, 8, 1) \
+    QMLP_GUR_CASE(S_, 16, 1) QMLP_GUR_CASE(S_, 8, 2) QMLP_GUR_CASE(S_, 16, 2)
 
-// Routed instances at one token, rank 1..32: LB LoRA-A columns, then the
-// gate/up columns of launch_gateup_bits's shape at S lanes per row.
+// Routed instances at one token, rank 0 or 8..32: LB LoRA-A columns (none
+// at rank 0), then the gate/up columns of launch_gateup_bits's shape at S
+// lanes per row; the activation is loaded ahead of the weights when one
+// staging pass of at most two words per thread holds it.
 template <int B, bool SPLIT>
-hipError_t launch_gateup_lora_bits(BatchArgs args, int nb, int S, unsigned long long* t64, unsigned* ctl,
-                                   hipStream_t st) {
-    if (args.M != 1 || args.r < 1 || 2 * args.r > 64 || !t64 || !ctl)
+hipError_t launch_gateup_routed_bits(BatchArgs args, int nb, int S, unsigned long long* t64, unsigned* ctl,
+                                     hipStream_t st) {
+    if (args.M != 1 || args.r < 0 || 2 * args.r > 64 || !t64 || !ctl)
         return hipErrorInvalidValue;
     const int U = args.d / codes_per_unit(B);
     const int J = (U + S - 1) / S;
     const int mj = maxj_for(J);
     const size_t unit_bytes = B == 4 ? DN_UNIT_BYTES : (B == 3 ? 16 : 8) * 16 + 8 * (SPLIT ? 2 : 1);
     args.uc = units_per_chunk(U, S, unit_bytes, 1);
+    const int nxw = args.uc >= U && 4 * U <= 256 * 2 ? (4 * U + 255) / 256 : 0;
     const size_t lds = (size_t)args.uc * unit_bytes;
     const int LB = (2 * args.r + 3) / 4;
     const int rows_per_block = 4 * (64 / S);
     const dim3 grid((unsigned)(LB + (args.f + rows_per_block - 1) / rows_per_block), (unsigned)nb);
-    QMLP_GUL_S(8) QMLP_GUL_S(16) QMLP_GUL_S(32) QMLP_GUL_S(64)
+    QMLP_GUR_S(8) QMLP_GUR_S(16) QMLP_GUR_S(32) QMLP_GUR_S(64)
     return hipErrorInvalidValue;
 }
 
@@ -632,15 +670,15 @@ hipError_t launch_down_bits(BatchArgs args, int nb, int S, hipStream_t st) {
     extern template hipError_t launch_gateup_bits<4, false, 256>(BatchArgs, int, int, hipStream_t);  \
     extern template hipError_t launch_gateup_bits<3, false, 256>(BatchArgs, int, int, hipStream_t);  \
     extern template hipError_t launch_gateup_bits<3, true, 256>(BatchArgs, int, int, hipStream_t);   \
-    extern template hipError_t launch_gateup_lora_bits<2, false>(BatchArgs, int, int, unsigned long long*, \
+    extern template hipError_t launch_gateup_routed_bits<2, false>(BatchArgs, int, int, unsigned long long*, \
                                                                  unsigned*, hipStream_t);            \
-    extern template hipError_t launch_gateup_lora_bits<2, true>(BatchArgs, int, int, unsigned long long*,  \
+    extern template hipError_t launch_gateup_routed_bits<2, true>(BatchArgs, int, int, unsigned long long*,  \
                                                                 unsigned*, hipStream_t);             \
-    extern template hipError_t launch_gateup_lora_bits<3, false>(BatchArgs, int, int, unsigned long long*, \
+    extern template hipError_t launch_gateup_routed_bits<3, false>(BatchArgs, int, int, unsigned long long*, \
                                                                  unsigned*, hipStream_t);            \
-    extern template hipError_t launch_gateup_lora_bits<3, true>(BatchArgs, int, int, unsigned long long*,  \
+    extern template hipError_t launch_gateup_routed_bits<3, true>(BatchArgs, int, int, unsigned long long*,  \
                                                                 unsigned*, hipStream_t);             \
-    extern template hipError_t launch_gateup_lora_bits<4, false>(BatchArgs, int, int, unsigned long long*, \
+    extern template hipError_t launch_gateup_routed_bits<4, false>(BatchArgs, int, int, unsigned long long*, \
                                                                  unsigned*, hipStream_t);            \
     extern template hipError_t launch_down_bits<2, 256>(BatchArgs, int, int, hipStream_t);           \
     extern template hipError_t launch_down_bits<2, 1024>(BatchArgs, int, int, hipStream_t);          \

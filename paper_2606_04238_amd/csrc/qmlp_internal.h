@@ -131,10 +131,10 @@ constexpr int kMoeCtlEpoch = 0, kMoeCtlErr = 160;
 // Gate/up over a routed batch at one token with the LoRA-A projection in the
 // same launch: the first workgroups of each instance compute t and publish
 // it as tagged 64-bit words (fp32 bits | tag << 32) in t64 [nb][2r]; the
-// gate/up workgroups read them for the LoRA-B term.  gateup_lora_fits says
+// gate/up workgroups read them for the LoRA-B term.  gateup_routed_fits says
 // whether it takes the shape (rank > 0, one token per instance).
-bool gateup_lora_fits(const BatchArgs& b, int nb);
-hipError_t launch_gateup_lora_batch(const BatchArgs& b, int nb, unsigned long long* t64, unsigned* ctl,
+bool gateup_routed_fits(const BatchArgs& b, int nb);
+hipError_t launch_gateup_routed_batch(const BatchArgs& b, int nb, unsigned long long* t64, unsigned* ctl,
                                     hipStream_t st);
 // Down over a routed batch (M = 1, k = xdiv instances per token) with the
 // routing-weighted combine folded in: y [nb/k][d] binary16, w [nb/k][k].

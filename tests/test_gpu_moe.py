@@ -178,3 +178,14 @@ def test_moe_repeated_calls_on_one_workspace(q, k):
     # call's tag, and the call counter advanced once per call
     assert q.workspace_errors(ws) == 0
     assert int(ws[0:4].view(torch.int32).item()) == 3
+
+
+def test_moe_wide_activation_takes_the_chunked_staging(q):
+    """Routed gate/up loads the activation ahead of the weights when one
+    staging pass of at most two words per thread holds it (d <= 8192 at
+    2 bits); a wider activation takes the chunk loop.  d = 8704 here."""
+    cfg = wl.Config("moe_wide_x", M=1, d=8704, f=256, g=64, r=8, L=1)
+    print("\n[case] moe d 8704 E 3 k 2 M 2", flush=True)
+    err = _run(q, cfg, 3, 2, 2, layer=5)
+    print("max-rel %.2e" % err)
+    assert err <= Y_TOL
