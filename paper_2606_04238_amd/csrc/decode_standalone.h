@@ -56,8 +56,11 @@ __device__ __forceinline__ GateUpArgs batch_gateup_args(const BatchArgs& b, int 
 // NT/64 waves per block, one gate/up item (64/S row pairs) per wave.  B and
 // SPLIT as for GuItem: the activation is staged in the layout of the code
 // width (eight 16-byte chunks per 64-code unit at 2 bits, four per 32-code
-// unit at 4 bits) with one or two (C, X) pairs per unit.
-template <int MT, int S, int MAXJ, int B, bool SPLIT, int NT>
+// unit at 4 bits) with one or two (C, X) pairs per unit.  NXW > 0 (one
+// token, the activation in one staging pass of NXW words per thread): the
+// activation loads go out before the weights, so the staging converts while
+// the weight stream is in flight (loads retire in order).
+template <int MT, int S, int MAXJ, int B, bool SPLIT, int NT, int NXW = 0>
 __global__ void __launch_bounds__(NT)
 gateup_kernel(BatchArgs b) {
     const GateUpArgs a = batch_gateup_args(b, blockIdx.y);
@@ -68,8 +71,37 @@ gateup_kernel(BatchArgs b) {
     float2* cx = reinterpret_cast<float2*>(smem + MT * UC * CH);
     const int tid = threadIdx.x, lane = tid & 63;
     GuItem<MT, S, MAXJ, B, SPLIT> it;
-    gu_load(it, a, (blockIdx.x * (blockDim.x >> 6) + (tid >> 6)) * (64 / S), true, lane);
+    const int row0 = (blockIdx.x * (NT >> 6) + (tid >> 6)) * (64 / S);
     const int U = a.d / codes_per_unit(B);
+    if constexpr (NXW > 0) {
+        static_assert(MT == 1, "one staging pass at one token");
+        using HW = typename std::conditional<B == 4, uint4, XWord>::type;
+        HW xw[NXW];
+#pragma unroll
+        for (int k = 0; k < NXW; ++k) {
+            if constexpr (B == 4)
+                xw[k] = stage_h_load<1>(a.x, 1, a.d, 0, U, tid + NT * k);
+            else
+                xw[k] = stage_x_load<1>(a.x, 1, a.d, 0, U, tid + NT * k);
+        }
+        __builtin_amdgcn_sched_barrier(0);          // keep the activation loads ahead of the weights
+        gu_load(it, a, row0, true, lane);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int k = 0; k < NXW; ++k) {
+            if constexpr (B == 2)
+                stage_x_store<1, SPLIT>(xs, cx, U, U, 1, tid + NT * k, xw[k]);
+            else if constexpr (B == 3)
+                stage_x3_store<1, SPLIT>(xs, cx, U, U, 1, tid + NT * k, xw[k]);
+            else
+                stage_h_store<1>(xs, cx, U, U, 1, tid + NT * k, xw[k]);
+        }
+        __syncthreads();
+        gu_accumulate(it, xs, cx, U, a.d, 0, U, lane);
+        gu_finish(it, a, a.t, a.h, lane);
+        return;
+    }
+    gu_load(it, a, row0, true, lane);
     for (int u0 = 0; u0 < U; u0 += UC) {
         const int uc = min(UC, U - u0);
         __syncthreads();
@@ -226,8 +258,16 @@ hipError_t launch_gateup_routed_bits(BatchArgs args, int nb, int S, unsigned lon
 }
 
 #define QMLP_GU_CASE(MT_, S_, J_)                                                         \
-    if (mt == MT_ && S == S_ && mj == J_) {                                               \
+    if (mt == MT_ && S == S_ && mj == J_ && (MT_ > 1 || nxw == 0)) {                      \
         auto k = gateup_kernel<MT_, S_, J_, B, SPLIT, NT>;                                \
+        hipError_t e = set_lds(k, lds);                                                   \
+        if (e != hipSuccess) return e;                                                    \
+        k<<<grid, NT, lds, st>>>(args);                                                   \
+        return hipGetLastError();                                                         \
+    }
+#define QMLP_GU_X(S_, J_, X_)                                                             \
+    if (mt == 1 && S == S_ && mj == J_ && nxw == X_) {                                    \
+        auto k = gateup_kernel<1, S_, J_, B, SPLIT, NT, X_>;                              \
         hipError_t e = set_lds(k, lds);                                                   \
         if (e != hipSuccess) return e;                                                    \
         k<<<grid, NT, lds, st>>>(args);                                                   \
@@ -235,6 +275,7 @@ hipError_t launch_gateup_routed_bits(BatchArgs args, int nb, int S, unsigned lon
     }
 #define QMLP_GU_S(MT_, S_) QMLP_GU_CASE(MT_, S_, 8) QMLP_GU_CASE(MT_, S_, 16)
 #define QMLP_GU_MT(MT_) QMLP_GU_S(MT_, 8) QMLP_GU_S(MT_, 16) QMLP_GU_S(MT_, 32) QMLP_GU_S(MT_, 64)
+#define QMLP_GU_XS(S_) QMLP_GU_X(S_, 8, 1) QMLP_GU_X(S_, 16, 1) QMLP_GU_X(S_, 8, 2) QMLP_GU_X(S_, 16, 2)
 
 // S lanes per row (8, 16, 32 or 64, at most 16 units per lane), chosen by
 // the dispatcher.
@@ -249,6 +290,10 @@ hipError_t launch_gateup_bits(BatchArgs args, int nb, int S, hipStream_t st) {
     const size_t lds = (size_t)mt * args.uc * unit_bytes;
     const int rows_per_block = (NT / 64) * (64 / S);
     const dim3 grid((args.f + rows_per_block - 1) / rows_per_block, (unsigned)nb);
+    // one token whose activation fits one staging pass of at most two words
+    // per thread: the activation-first form
+    const int nxw = mt == 1 && args.uc >= U && 4 * U <= 2 * NT ? (4 * U + NT - 1) / NT : 0;
+    QMLP_GU_XS(8) QMLP_GU_XS(16) QMLP_GU_XS(32) QMLP_GU_XS(64)
     QMLP_GU_MT(1) QMLP_GU_MT(2) QMLP_GU_MT(4) QMLP_GU_MT(8) QMLP_GU_MT(16)
     return hipErrorInvalidValue;
 }
