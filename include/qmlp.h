@@ -383,16 +383,18 @@ qmlp_status qmlp_forward_moe(const qmlp_mlp *experts, int E, const void *x, int 
                              qmlp_dtype dtype, const int32_t *topk_idx, const float *topk_w, int k,
                              void *y, void *ws, size_t ws_bytes, qmlp_stream stream);
 
-/* Launch shape of qmlp_forward_moe's weight launches at one token over
- * `instances` routed expert instances (M k) of a [d][f] expert, on a device
- * with `cus` compute units: the lanes per row of the gate/up launch
- * (gu_bits 2 or 4) and of the down launch (dn_bits 2 or 4).  A few
- * instances leave the chip with fewer than two workgroups per compute unit
- * at the usual choice, so the lanes per row double (more, shorter rows per
- * workgroup) until it has them.  Returns 1 when down takes the pipelined
- * kernel, 0 the plain one, -1 for arguments outside d, f > 0 and multiples
- * of 64, 1 <= instances <= 40, cus >= 1, non-null outputs.  Host-only. */
-int qmlp_moe_lanes(int d, int f, int gu_bits, int dn_bits, int instances, int cus,
+/* Launch shape of qmlp_forward_moe's weight launches for M tokens with k
+ * routed experts each (M k instances) of a [d][f] expert, on a device with
+ * `cus` compute units: the lanes per row of the gate/up launch (gu_bits 2 or
+ * 4) and of the down launch (dn_bits 2 or 4).  Gate/up: a few instances
+ * leave the chip with fewer than two workgroups per compute unit at the
+ * usual choice, so the lanes per row double (more, shorter rows per
+ * workgroup) until it has them.  Returns 2 when down also forms the routing
+ * sum (k <= 4; the fewest lanes with at most three 16-byte units each),
+ * 1 when it takes the pipelined kernel and a combine launch follows, 0 the
+ * plain kernel; -1 for arguments outside d, f > 0 and multiples of 64,
+ * M, k >= 1, M k <= 40, cus >= 1, non-null outputs.  Host-only. */
+int qmlp_moe_lanes(int d, int f, int gu_bits, int dn_bits, int M, int k, int cus,
                    int *gu_lanes, int *dn_lanes);
 
 /* ---------------------------------------------- inspection (not timed) */

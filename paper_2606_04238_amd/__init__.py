@@ -81,7 +81,7 @@ def _lib():
             "qmlp_forward_stack": (I, [pm, I, P, I, I, P, P, P, Z, P]),
             "qmlp_stack_launches": (I, [pm, I, I, I]),
             "qmlp_stack_error_offset": (Z, [pm, I, I, I]),
-            "qmlp_moe_lanes": (I, [I, I, I, I, I, I, ctypes.POINTER(I), ctypes.POINTER(I)]),
+            "qmlp_moe_lanes": (I, [I, I, I, I, I, I, I, ctypes.POINTER(I), ctypes.POINTER(I)]),
             "qmlp_layers_workspace_bytes": (Z, [pm, I, I, I]),
             "qmlp_forward_layers": (I, [pm, I, P, I, I, P, P, Z, P]),
             "qmlp_layers_launches": (I, [pm, I, I, I]),
@@ -423,15 +423,16 @@ def moe_workspace_bytes(experts: Layers, M: int, k: int, dtype=torch.float16) ->
     return int(_lib().qmlp_moe_workspace_bytes(experts.c(), len(experts), M, k, code))
 
 
-def moe_lanes(d: int, f: int, gu_bits: int, dn_bits: int, instances: int, cus: int):
-    """(gate/up lanes per row, down lanes per row, down pipelined) of
-    qmlp_forward_moe's launches over `instances` routed expert instances on
-    `cus` compute units (qmlp_moe_lanes; host-only)."""
+def moe_lanes(d: int, f: int, gu_bits: int, dn_bits: int, M: int, k: int, cus: int):
+    """(gate/up lanes per row, down lanes per row, down form) of
+    qmlp_forward_moe's launches for M tokens with k experts each on `cus`
+    compute units (qmlp_moe_lanes; host-only).  Down form: "sum" (the down
+    launch forms the routing sum), "pipe" or "plain" (a combine follows)."""
     g, dn = ctypes.c_int(0), ctypes.c_int(0)
-    r = int(_lib().qmlp_moe_lanes(d, f, gu_bits, dn_bits, instances, cus, ctypes.byref(g), ctypes.byref(dn)))
+    r = int(_lib().qmlp_moe_lanes(d, f, gu_bits, dn_bits, M, k, cus, ctypes.byref(g), ctypes.byref(dn)))
     if r < 0:
         raise ValueError("qmlp_moe_lanes rejected its arguments")
-    return g.value, dn.value, bool(r)
+    return g.value, dn.value, ("plain", "pipe", "sum")[r]
 
 
 def forward_moe(experts: Layers, x: torch.Tensor, topk_idx: torch.Tensor, topk_w: torch.Tensor,

@@ -32,14 +32,19 @@ hipError_t launch_down_batch(const BatchArgs& b, int nb, hipStream_t st) {
 
 }  // namespace qmlp
 
-extern "C" int qmlp_moe_lanes(int d, int f, int gu_bits, int dn_bits, int instances, int cus,
-                              int* gu_lanes, int* dn_lanes) {
+extern "C" int qmlp_moe_lanes(int d, int f, int gu_bits, int dn_bits, int M, int k, int cus, int* gu_lanes,
+                              int* dn_lanes) {
     using namespace qmlp;
-    if (d <= 0 || f <= 0 || instances < 1 || instances > kBatchMax || cus < 1 || !gu_lanes || !dn_lanes ||
+    const int instances = M * k;
+    if (d <= 0 || f <= 0 || M < 1 || k < 1 || instances > kBatchMax || cus < 1 || !gu_lanes || !dn_lanes ||
         (gu_bits != 2 && gu_bits != 4) || (dn_bits != 2 && dn_bits != 4) || d % 64 != 0 || f % 64 != 0)
         return -1;
     *gu_lanes = routed_gateup_lanes(d / codes_per_unit(gu_bits), f, instances, gu_bits, cus);
     const int Ud = f / codes_per_unit(dn_bits);
+    if (down_combine_fits_shape(d, f, k, dn_bits)) {
+        *dn_lanes = combine_lanes(Ud);
+        return 2;
+    }
     const bool pipe = down_pipe_fits_shape(d, f, 1, instances, dn_bits);
     *dn_lanes = pipe ? routed_pipe_lanes(Ud, d, instances, cus) : instances > 1 ? lanes_fewest(Ud) : lanes_for(Ud, dn_bits);
     return pipe ? 1 : 0;

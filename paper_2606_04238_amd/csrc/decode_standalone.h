@@ -638,6 +638,20 @@ hipError_t launch_down_pipe(const BatchArgs& args, int nb, hipStream_t st) {
     QMLP_PIPE_CMB_CASE(S_, 3) QMLP_PIPE_CMB_CASE(S_, 4) QMLP_PIPE_CMB_CASE(S_, 5)         \
     QMLP_PIPE_CMB_CASE(S_, 6)
 
+// Lanes per row of down_pipe_combine_kernel: the fewest with at most
+// kCombineUnits units per lane.  A workgroup stages the h of all k
+// instances of its token, so fewer, longer rows per lane spread that staging
+// over more rows: at GPT-OSS-20B-class experts (f = 2880, top-4) 3 units per
+// lane measured fastest at both down widths (4 bits: 32 lanes, 2 bits: 16),
+// ahead of 2 (20.2 against 21.2 us per W4/W2-GateUp layer; 18.8 against
+// 20.1 at uniform W2) and 6.
+constexpr int kCombineUnits = 3;
+inline int combine_lanes(int U) {
+    for (int S = 8; S <= 64; S *= 2)
+        if ((U + S - 1) / S <= kCombineUnits) return S;
+    return pipe_lanes(U);
+}
+
 // Whether down_pipe_combine_kernel takes a routed batch of ntok * k
 // instances at one token each: k <= 4, h of the k instances within the
 // staging words and the LDS budget, and the lanes per row of the routed
@@ -656,7 +670,7 @@ hipError_t launch_down_pipe_combine(const BatchArgs& args, int nb, const float* 
                                     unsigned* ctl, hipStream_t st) {
     const int k = args.xdiv;
     const int U = args.f / codes_per_unit(B);
-    const int S = routed_pipe_lanes(U, args.d, nb, device_cu_count());
+    const int S = combine_lanes(U);
     const int JJ = S ? (U + S - 1) / S : 0;
     if (!S || k < 1 || k > 4 || nb % k != 0)
         return hipErrorInvalidValue;

@@ -424,29 +424,36 @@ def test_noalloc_validation(q, lib):
     assert f(ctypes.byref(big), P(FAKE), 8, 1, P(FAKE), None) == UNSUP     # bfloat16
 
 
-@pytest.mark.parametrize("d,f,gu_bits,dn_bits,inst,cus,want", [
+@pytest.mark.parametrize("d,f,gu_bits,dn_bits,M,k,cus,want", [
     # GPT-OSS-20B-class experts, top-4, one token, 256 compute units:
-    # W4/W2-GateUp gate/up 8 -> 16 lanes, W4 down 16 -> 64 (pipelined)
-    (2880, 2880, 2, 4, 4, 256, (16, 64, True)),
-    (2880, 2880, 2, 2, 4, 256, (16, 32, True)),        # uniform W2 down 8 -> 32
-    (2880, 2880, 4, 4, 4, 256, (16, 64, True)),        # uniform W4 gate/up keeps 16
-    # one instance: down runs the plain kernel (the pipelined one wants a batch)
-    (1024, 768, 2, 4, 1, 256, (16, 8, False)),
-    (1024, 768, 2, 4, 2, 256, (16, 16, True)),
-    (2048, 768, 2, 4, 2, 256, (32, 16, True)),         # one 16-byte unit per lane
-    # the rule counts the device's compute units, not a fixed 256
-    (2880, 2880, 2, 4, 4, 80, (8, 16, True)),
+    # W4/W2-GateUp gate/up 8 -> 16 lanes; down forms the routing sum at the
+    # fewest lanes with at most three units each (W4: 90 units -> 32 lanes)
+    (2880, 2880, 2, 4, 1, 4, 256, (16, 32, "sum")),
+    (2880, 2880, 2, 2, 1, 4, 256, (16, 16, "sum")),    # uniform W2 down: 45 units -> 16
+    (2880, 2880, 4, 4, 1, 4, 256, (16, 32, "sum")),    # uniform W4 gate/up keeps 16
+    (1024, 768, 2, 4, 1, 1, 256, (16, 8, "sum")),
+    (1024, 768, 2, 4, 1, 2, 256, (16, 8, "sum")),
+    (2048, 768, 2, 4, 1, 2, 256, (32, 8, "sum")),      # gate/up: one 16-byte unit per lane
+    # the gate/up rule counts the device's compute units, not a fixed 256
+    (2880, 2880, 2, 4, 1, 4, 80, (8, 32, "sum")),
     # enough instances to fill the chip: no doubling
-    (2880, 2880, 2, 4, 40, 256, (8, 16, True)),
+    (2880, 2880, 2, 4, 10, 4, 256, (8, 32, "sum")),
+    # past four slots: the pipelined down kernel (its lanes double while the
+    # grid has fewer than two workgroups per CU) and a combine launch
+    (2880, 2880, 2, 4, 1, 5, 256, (16, 64, "pipe")),
+    (2880, 2880, 2, 4, 8, 5, 256, (8, 16, "pipe")),
+    # f past the folded kernel's staging at k = 4 (U = 128 units of 4 bits);
+    # 4096 gate/up rows at 8 lanes are already 512 workgroups: no doubling
+    (2880, 4096, 2, 4, 1, 4, 256, (8, 64, "pipe")),
 ])
-def test_moe_lane_choice(q, d, f, gu_bits, dn_bits, inst, cus, want):
+def test_moe_lane_choice(q, d, f, gu_bits, dn_bits, M, k, cus, want):
     """The lanes per row of qmlp_forward_moe's launches (host-only query)."""
-    assert q.moe_lanes(d, f, gu_bits, dn_bits, inst, cus) == want
+    assert q.moe_lanes(d, f, gu_bits, dn_bits, M, k, cus) == want
 
 
 def test_moe_lane_choice_rejects(q, lib):
     g, dn = ctypes.c_int(0), ctypes.c_int(0)
-    for args in [(2880, 2880, 3, 4, 4, 256), (2880, 2880, 2, 4, 0, 256), (2880, 2880, 2, 4, 41, 256),
-                 (2880, 2880, 2, 4, 4, 0), (2890, 2880, 2, 4, 4, 256)]:
+    for args in [(2880, 2880, 3, 4, 1, 4, 256), (2880, 2880, 2, 4, 0, 4, 256), (2880, 2880, 2, 4, 1, 0, 256),
+                 (2880, 2880, 2, 4, 9, 5, 256), (2880, 2880, 2, 4, 1, 4, 0), (2890, 2880, 2, 4, 1, 4, 256)]:
         assert lib.qmlp_moe_lanes(*args, ctypes.byref(g), ctypes.byref(dn)) == -1
-    assert lib.qmlp_moe_lanes(2880, 2880, 2, 4, 4, 256, None, ctypes.byref(dn)) == -1
+    assert lib.qmlp_moe_lanes(2880, 2880, 2, 4, 1, 4, 256, None, ctypes.byref(dn)) == -1

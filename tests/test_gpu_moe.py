@@ -61,11 +61,10 @@ def test_moe_gptoss20b_shape_matches_oracle(q):
 def test_moe_few_instances_take_more_lanes_per_row(q, d):
     """One token routed to one or two experts fills fewer than two workgroups
     per CU, so the gate/up launch doubles its lanes per row (16, then 32 at
-    d = 2048, one 16-byte unit per lane); with two instances (k = 2) down
-    takes the pipelined kernel and doubles its lanes too (8 -> 16 over
-    f = 768), with one (k = 1) it runs the plain kernel.  The picks are
-    pinned on the CPU (test_abi.test_moe_lane_choice); here the results of
-    both launch shapes match the oracle."""
+    d = 2048, one 16-byte unit per lane); down forms the routing sum at 8
+    lanes over f = 768 (k = 1: one wave per row group, four row groups;
+    k = 2: two).  The picks are pinned on the CPU
+    (test_abi.test_moe_lane_choice); here the results match the oracle."""
     cfg = wl.Config("moe_wide_tiny", M=1, d=d, f=768, g=64, r=8, L=1)
     for k in (1, 2):
         print("\n[case] moe d %d E 4 k %d M 1" % (d, k), flush=True)
