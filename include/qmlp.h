@@ -292,7 +292,13 @@ int qmlp_stack_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
  *
  * ws/ws_bytes: at least qmlp_layers_workspace_bytes(layers, L, M, dtype)
  * (binary16: that of qmlp_forward_batch, with four times its t area on the
- * matrix cores).  No state is kept between calls.
+ * matrix cores and twice on the streamed path).  On the streamed path with
+ * adapters the gate/up launch also computes LoRA-A and hands t over as
+ * tagged words: the control block's word 0 counts the calls and word 160
+ * holds sticky error bits (1 = a wait for t gave up), so the workspace must
+ * be ZERO before its first call and zeroed again before it serves other
+ * blocks' shape or after an error bit; one call at a time per workspace.
+ * The other paths keep no state between calls.
  * Errors as for qmlp_forward.
  */
 size_t qmlp_layers_workspace_bytes(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
@@ -307,9 +313,10 @@ qmlp_status qmlp_forward_layers(const qmlp_mlp *layers, int L, const void *x, in
  * the current device's compute-unit count). */
 int qmlp_layers_path(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
 
-/* Launches qmlp_forward_layers makes: 3 per batch of up to 40 blocks (2
- * without adapters) on the streamed, matrix-core and batched paths, or the per-block
- * launches of qmlp_forward; 0 if the call would be rejected.  Host-only. */
+/* Launches qmlp_forward_layers makes: per batch of up to 40 blocks 2 on the
+ * streamed path, 3 on the matrix-core and batched paths (2 without
+ * adapters), or the per-block launches of qmlp_forward; 0 if the call would
+ * be rejected.  Host-only. */
 int qmlp_layers_launches(const qmlp_mlp *layers, int L, int M, qmlp_dtype dtype);
 
 /*

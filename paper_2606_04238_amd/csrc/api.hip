@@ -373,7 +373,9 @@ qmlp_status run_layers_batched(const qmlp_mlp* layers, int L, const char* xb, in
     const int d = a.gate.k_in;
     const size_t step = (size_t)M * d * 2;
     char* base = static_cast<char*>(ws);
-    const int ts = path == BatchPath::kMfma ? kLoraSlices : 1;
+    // t: four fp32 partial sums per value on the matrix cores, one tagged
+    // 64-bit word on the streamed path, fp32 otherwise
+    const int ts = path == BatchPath::kMfma ? kLoraSlices : path == BatchPath::kStreamed ? 2 : 1;
     BatchArgs b{};
     b.t = reinterpret_cast<float*>(base + kCtlBytes);
     b.h = reinterpret_cast<uint16_t*>(base + kCtlBytes + batch_t_bytes(&a, batch_size(L), M, ts));
@@ -390,15 +392,17 @@ qmlp_status run_layers_batched(const qmlp_mlp* layers, int L, const char* xb, in
         for (int i = 0; i < n; ++i) b.lay[i] = stack_desc(layers[l0 + i]);
         b.x = reinterpret_cast<const uint16_t*>(xb + l0 * step);
         b.y = reinterpret_cast<uint16_t*>(yb + l0 * step);
-        hipError_t e = b.r == 0                  ? hipSuccess
-                       : path == BatchPath::kMfma ? launch_lora_a_mfma(b, n, st)
-                                                  : launch_lora_a_batch(b, n, st);
+        unsigned* ctl = reinterpret_cast<unsigned*>(base);
+        auto* t64 = reinterpret_cast<unsigned long long*>(b.t);
+        hipError_t e = b.r == 0 || path == BatchPath::kStreamed ? hipSuccess   // streamed: in gate/up
+                       : path == BatchPath::kMfma              ? launch_lora_a_mfma(b, n, st)
+                                                               : launch_lora_a_batch(b, n, st);
         if (e == hipSuccess)
-            e = path == BatchPath::kStreamed ? launch_gateup_stream(b, n, st)
+            e = path == BatchPath::kStreamed ? launch_gateup_stream(b, n, t64, ctl, st)
                 : path == BatchPath::kMfma   ? launch_gateup_mfma(b, n, st)
                                              : launch_gateup_batch(b, n, st);
         if (e == hipSuccess)
-            e = path == BatchPath::kStreamed ? launch_down_stream(b, n, st)
+            e = path == BatchPath::kStreamed ? launch_down_stream(b, n, ctl, st)
                 : path == BatchPath::kMfma   ? launch_down_mfma(b, n, st)
                                              : launch_down_batch(b, n, st);
         if (e != hipSuccess)
@@ -678,7 +682,8 @@ size_t qmlp_layers_workspace_bytes(const qmlp_mlp* layers, int L, int M, qmlp_dt
         return 0;
     if (dtype == QMLP_F16)              // streamed, matrix-core or batched
         return kCtlBytes +
-               batch_t_bytes(layers, batch_size(L), M, layers_mfma(layers, L, M, dtype) ? kLoraSlices : 1) +
+               batch_t_bytes(layers, batch_size(L), M,
+                             layers_mfma(layers, L, M, dtype) ? kLoraSlices : layers_streamed(layers, L, M, dtype) ? 2 : 1) +
                batch_h_bytes(layers, batch_size(L), M);
     return qmlp_workspace_bytes(&layers[0], M, dtype);
 }
@@ -698,8 +703,9 @@ int qmlp_layers_path(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
 int qmlp_layers_launches(const qmlp_mlp* layers, int L, int M, qmlp_dtype dtype) {
     if (check_layers(layers, L, M, dtype) != QMLP_OK || M == 0)
         return 0;
-    if (dtype == QMLP_F16)              // streamed, matrix-core or batched: three launches per batch
-        return (L + kBatchMax - 1) / kBatchMax * (layers[0].rank > 0 ? 3 : 2);
+    if (dtype == QMLP_F16)              // three launches per batch (two streamed or without adapters)
+        return (L + kBatchMax - 1) / kBatchMax *
+               (layers[0].rank > 0 && !layers_streamed(layers, L, M, dtype) ? 3 : 2);
     int n = 0;
     for (int i = 0; i < L; ++i) n += qmlp_forward_launches(&layers[i], M, dtype);
     return n;

@@ -47,6 +47,10 @@ namespace qmlp {
 namespace {
 
 constexpr int kStreamSpan = 3;          // blocks one workgroup's range may touch
+// Control words of the batch workspace (uint32 indices, each on its own
+// 128-byte line): the call counter that tags t, sticky error bits.
+constexpr int kStreamCtlEpoch = 0, kStreamCtlErr = 160;
+constexpr unsigned kStreamSpinLimit = 1u << 18;
 
 // The kernel's BatchArgs read in place from the kernel-argument segment, so
 // indexing the descriptor table with a (wave-uniform) block index compiles to
@@ -236,7 +240,8 @@ __device__ __forceinline__ void gu_finish(GuBuf<JC>& q, const float* ts, int l, 
 }
 
 template <int JC, int NCH, int R, int GSH, int NW>
-__global__ void __launch_bounds__(NW * 64) gu_stream_kernel(BatchArgs b, int nb, int span) {
+__global__ void __launch_bounds__(NW * 64) gu_stream_kernel(BatchArgs b, int nb, int span,
+                                                            unsigned long long* t64, unsigned* ctl) {
     static_assert(NCH == 1 || NCH == 2, "one or two steps per row");
     constexpr int NT = NW * 64, UG = 8 * JC * NCH;
     const int f = b.f;
@@ -247,6 +252,37 @@ __global__ void __launch_bounds__(NW * 64) gu_stream_kernel(BatchArgs b, int nb,
     uint16_t* hout = reinterpret_cast<uint16_t*>(ts + span * 2 * R);    // [8 (i1 - i0)]
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+    // LoRA-A: the workgroup's share [c0, c1) of the rows of the batch's
+    // [nb][2R] t (at most one per wave, the host checks), each computed by
+    // one wave whose loads go out first and whose product is published as a
+    // tagged word (fp32 | tag << 32, tag = the call counter plus one) after
+    // the staging; every workgroup then reads the t of its range's blocks,
+    // which other workgroups of this launch (all resident: one per compute
+    // unit) publish.
+    constexpr int KA = JC * NCH;                 // 8-element chunks of a row per lane (d / 512)
+    int c0 = 0, c1 = 0;
+    if constexpr (R > 0)
+        wg_share(nb * 2 * R, gridDim.x, blockIdx.x, c0, c1);
+    const int lc = c0 + wave;
+    const bool lw = R > 0 && lc < c1;
+    uint4 la[R > 0 ? KA : 1], lx[R > 0 ? KA : 1];
+    if constexpr (R > 0) {
+        if (lw) {
+            KBatch* kb = kbatch();
+            const int l = lc / (2 * R), row = lc - l * 2 * R;
+            const uint16_t* arow = row < R ? kb->lay[l].Ag + (long)row * b.d : kb->lay[l].Au + (long)(row - R) * b.d;
+            const uint16_t* xrow = b.x + (long)l * b.d;
+#pragma unroll
+            for (int k = 0; k < KA; ++k) {
+                la[k] = *reinterpret_cast<const uint4*>(arow + (lane + 64 * k) * 8);
+                lx[k] = *reinterpret_cast<const uint4*>(xrow + (lane + 64 * k) * 8);
+            }
+        }
+    }
+    unsigned epoch = 0;
+    if constexpr (R > 0)
+        epoch = __hip_atomic_load(ctl + kStreamCtlEpoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
     int i0, i1;
     wg_share(nb * (f / 8), gridDim.x, blockIdx.x, i0, i1);
@@ -288,8 +324,38 @@ __global__ void __launch_bounds__(NW * 64) gu_stream_kernel(BatchArgs b, int nb,
         gu_stage_word<UG>(xs + bb * 8 * UG, cx + bb * UG, wi, idx < words, xv[k]);
     }
     if constexpr (R > 0) {
-        for (int k = tid; k < nbk * 2 * R; k += NT)
-            ts[k] = b.t[(long)l0 * 2 * R + k];
+        const unsigned long long tag = epoch % 0xFFFFFFFFu + 1u;
+        if (lw) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int k = 0; k < KA; ++k) {
+                acc = dot2(la[k].x, lx[k].x, acc);
+                acc = dot2(la[k].y, lx[k].y, acc);
+                acc = dot2(la[k].z, lx[k].z, acc);
+                acc = dot2(la[k].w, lx[k].w, acc);
+            }
+            acc = group_sum<64>(acc);
+            if (lane == 0)
+                __hip_atomic_store(t64 + lc, (unsigned long long)__float_as_uint(acc) | (tag << 32),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    if constexpr (R > 0) {
+        // t of the range's blocks: re-read until a word shows this call's tag
+        // (bounded: after kStreamSpinLimit polls the word is taken as it is
+        // and error bit 1 is set)
+        const unsigned tag = epoch % 0xFFFFFFFFu + 1u;
+        for (int k = tid; k < nbk * 2 * R; k += NT) {
+            const unsigned long long* p = t64 + (long)l0 * 2 * R + k;
+            unsigned long long v = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (unsigned n = 0; (unsigned)(v >> 32) != tag && n < kStreamSpinLimit; ++n) {
+                __builtin_amdgcn_s_sleep(2);
+                v = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            if ((unsigned)(v >> 32) != tag)
+                __hip_atomic_fetch_or(ctl + kStreamCtlErr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            ts[k] = __uint_as_float((uint32_t)v);
+        }
     }
     __syncthreads();
 
@@ -426,7 +492,7 @@ __device__ __forceinline__ float dn_dot(DnBuf<JD>& q, const uint4* hl, const flo
 }
 
 template <int JD, int NW, int NBUF>
-__global__ void __launch_bounds__(NW * 64) dn_stream_kernel(BatchArgs b, int nb, int span) {
+__global__ void __launch_bounds__(NW * 64) dn_stream_kernel(BatchArgs b, int nb, int span, unsigned* ctl) {
     static_assert(NBUF == 2 || NBUF == 3, "two or three register sets");
     constexpr int NT = NW * 64, UD = 64 * JD;
     const int d = b.d, f = b.f, U = f / 32, gsh = b.gd == 128 ? 2 : 1, ng = f / b.gd;
@@ -436,6 +502,13 @@ __global__ void __launch_bounds__(NW * 64) dn_stream_kernel(BatchArgs b, int nb,
     uint16_t* yout = reinterpret_cast<uint16_t*>(cx + span * UD);       // [r1 - r0]
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+    // one lane of the first workgroup advances the call counter (with
+    // adapters): its load goes out first and the store comes at the end
+    const bool leader = ctl && b.r > 0 && tid == 0 && blockIdx.x == 0;
+    unsigned epoch = 0;
+    if (leader)
+        epoch = __hip_atomic_load(ctl + kStreamCtlEpoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 
     int r0, r1;
     wg_share(nb * d, gridDim.x, blockIdx.x, r0, r1);
@@ -529,6 +602,8 @@ __global__ void __launch_bounds__(NW * 64) dn_stream_kernel(BatchArgs b, int nb,
     __syncthreads();
     for (int k = tid; k < r1 - r0; k += NT)
         b.y[r0 + k] = yout[k];
+    if (leader)
+        __hip_atomic_store(ctl + kStreamCtlEpoch, epoch + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ---------------------------------------------------------------- host side
@@ -615,6 +690,10 @@ bool stream_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r
     const int sg = gu_span(nb, f, gu_grid(nb, f)), sd = dn_span(nb, d, dn_grid(nb, d));
     if (sg > kStreamSpan || sd > kStreamSpan)
         return false;
+    // the gate/up workgroups' LoRA-A shares: at most one row per wave
+    const int gw = gu_steps(d / 64, jc) == 1 ? gu_waves<1>() : gu_waves<2>();
+    if (((long)nb * 2 * r + gu_grid(nb, f) - 1) / gu_grid(nb, f) > gw)
+        return false;
     return gu_lds(sg, d / 64, r, nb, f, gu_grid(nb, f)) <= 64 * 1024 &&
            dn_lds(sd, 64 * dn_slots(f), nb, d, dn_grid(nb, d)) <= 64 * 1024;
 }
@@ -623,16 +702,17 @@ bool stream_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r
     if (jc == JC_ && nch == NCH_ && r == R_) {                                            \
         constexpr int NW = gu_waves<NCH_>();                                              \
         if (b.gg == 128)                                                                  \
-            gu_stream_kernel<JC_, NCH_, R_, 1, NW><<<G, NW * 64, lds, st>>>(b, nb, span); \
+            gu_stream_kernel<JC_, NCH_, R_, 1, NW><<<G, NW * 64, lds, st>>>(b, nb, span, t64, ctl); \
         else                                                                              \
-            gu_stream_kernel<JC_, NCH_, R_, 0, NW><<<G, NW * 64, lds, st>>>(b, nb, span); \
+            gu_stream_kernel<JC_, NCH_, R_, 0, NW><<<G, NW * 64, lds, st>>>(b, nb, span, t64, ctl); \
         return hipGetLastError();                                                         \
     }
 #define QMLP_GUS_R(JC_, NCH_) QMLP_GUS(JC_, NCH_, 0) QMLP_GUS(JC_, NCH_, 8) QMLP_GUS(JC_, NCH_, 16) \
     QMLP_GUS(JC_, NCH_, 32)
 
-hipError_t launch_gateup_stream(const BatchArgs& b, int nb, hipStream_t st) {
-    if (!stream_supported(b.M, b.d, b.f, b.gg, b.bg, b.gd, b.bd, b.r, nb))
+hipError_t launch_gateup_stream(const BatchArgs& b, int nb, unsigned long long* t64, unsigned* ctl,
+                                hipStream_t st) {
+    if (!stream_supported(b.M, b.d, b.f, b.gg, b.bg, b.gd, b.bd, b.r, nb) || (b.r > 0 && (!t64 || !ctl)))
         return hipErrorInvalidValue;
     const int G = gu_grid(nb, b.f), r = b.r;
     int jc = 0;
@@ -646,11 +726,11 @@ hipError_t launch_gateup_stream(const BatchArgs& b, int nb, hipStream_t st) {
 
 #define QMLP_DNS(JD_)                                                                     \
     if (jd == JD_) {                                                                      \
-        dn_stream_kernel<JD_, kDnWaves, kDnBufs><<<G, kDnWaves * 64, lds, st>>>(b, nb, span); \
+        dn_stream_kernel<JD_, kDnWaves, kDnBufs><<<G, kDnWaves * 64, lds, st>>>(b, nb, span, ctl); \
         return hipGetLastError();                                                         \
     }
 
-hipError_t launch_down_stream(const BatchArgs& b, int nb, hipStream_t st) {
+hipError_t launch_down_stream(const BatchArgs& b, int nb, unsigned* ctl, hipStream_t st) {
     if (!stream_supported(b.M, b.d, b.f, b.gg, b.bg, b.gd, b.bd, b.r, nb))
         return hipErrorInvalidValue;
     const int G = dn_grid(nb, b.d);

@@ -146,13 +146,19 @@ bool down_combine_fits(const BatchArgs& b, int nb);
 hipError_t launch_down_combine(const BatchArgs& b, int nb, const float* w, uint16_t* y, unsigned* ctl,
                                hipStream_t st);
 // The streamed path of a batch at one token (decode_stream.hip): one
-// persistent gate/up launch and one persistent down launch over all blocks of
-// the batch, after launch_lora_a_batch.  Binary16, 2-bit gate/up and 4-bit
+// persistent gate/up launch (with LoRA-A) and one persistent down launch
+// over all blocks of the batch.  Binary16, 2-bit gate/up and 4-bit
 // down at groups 64/128, rank 0/8/16/32, d % 512 == 0, d <= 4096,
 // f % 128 == 0, f <= 12288 (plus the LDS and span limits it checks).
 bool stream_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r, int nb);
-hipError_t launch_gateup_stream(const BatchArgs& b, int nb, hipStream_t st);
-hipError_t launch_down_stream(const BatchArgs& b, int nb, hipStream_t st);
+// With adapters the gate/up launch also computes LoRA-A (extra workgroups
+// after the streaming ones) and hands t over as tagged words in t64
+// [nb][2r] (fp32 | tag << 32); the tag is the call counter in ctl (word 0)
+// plus one, which the down launch advances; word 160 holds sticky error
+// bits (1 = a wait for t gave up).
+hipError_t launch_gateup_stream(const BatchArgs& b, int nb, unsigned long long* t64, unsigned* ctl,
+                                hipStream_t st);
+hipError_t launch_down_stream(const BatchArgs& b, int nb, unsigned* ctl, hipStream_t st);
 // The matrix-core path of a batch at 3..16 tokens (decode_mfma.hip): one
 // persistent gate/up launch and one persistent down launch over all blocks
 // of the batch, after launch_lora_a_mfma.  Binary16, 2-bit gate/up and
