@@ -1,17 +1,22 @@
 // Streamed decode path for a batch of independent blocks at one token
-// (binary16), gfx950: two persistent launches after the LoRA-A products.
+// (binary16), gfx950: two persistent launches.
 //
-//   gate/up launch:  h_l = SiLU(W2gate x_l + s B_g t_g) * (W2up x_l + s B_u t_u)
+//   gate/up launch:  t_l = [A_g; A_u] x_l, then
+//                    h_l = SiLU(W2gate x_l + s B_g t_g) * (W2up x_l + s B_u t_u)
 //                    for every block l of the batch (Sec. 3.1 Eq. (1),
 //                    Sec. 3.3, Sec. 4.2);
 //   down launch:     y_l = W4down h_l (Sec. 3.3).
 //
 // Decode is bound by loading weights (Sec. 1, Sec. 3.3).  The blocks of a
 // batch do not depend on each other, so every workgroup owns one contiguous
-// range of the batch's rows (flattened over blocks) and streams it: no
-// workgroup ever waits for another inside a launch, and the activation of
-// the few blocks a range touches (x for gate/up, h for down) is staged in
-// LDS once per launch.  Each wave walks its share of the range with two
+// range of the batch's rows (flattened over blocks) and streams it, and the
+// activation of the few blocks a range touches (x for gate/up, h for down)
+// is staged in LDS once per launch.  The one hand-off inside a launch is t:
+// each gate/up workgroup also computes a share of the batch's LoRA-A rows
+// (one per wave, its loads issued ahead of the weights) and publishes them
+// as tagged words, then reads the t of its own range's blocks before its
+// staging barrier (the workgroups, one per compute unit, are all resident;
+// the wait is bounded).  Each wave walks its share of the range with two
 // register sets: the loads of its next step go out before the current
 // step's arithmetic, in straight-line code with exact unit counts (the
 // prefetch of a wave's last step re-reads a valid address and is dropped),
