@@ -885,7 +885,7 @@ def main(argv=None):
             "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
             "alg_bytes_per_mlp_step": B,
             "mode": "hip_graph" if args.mode == "graph" else "eager",
-            "path": {"streamed": "streamed launches (LoRA-A, gate/up, down over every block)",
+            "path": {"streamed": "streamed launches (gate/up with LoRA-A, then down, over every block)",
                      "mfma": "matrix-core launches (LoRA-A, gate/up, down over every block)",
                      "batched": "batched stand-alone kernels"}[path],
             "eager_us_per_mlp_step": round(eager_step * 1e3 / L, 3),

@@ -259,10 +259,10 @@ __global__ void __launch_bounds__(NW * 64) gu_stream_kernel(BatchArgs b, int nb,
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
     // LoRA-A: the workgroup's share [c0, c1) of the rows of the batch's
-    // [nb][2R] t (at most one per wave, the host checks), each computed by
-    // one wave whose loads go out first and whose product is published as a
-    // tagged word (fp32 | tag << 32, tag = the call counter plus one) after
-    // the staging; every workgroup then reads the t of its range's blocks,
+    // [nb][2R] t, row c0 + w on wave w, whose loads go out first and whose
+    // product is published as a tagged word (fp32 | tag << 32, tag = the
+    // call counter plus one) after the staging (rows past the waves follow
+    // one per wave at a time); every workgroup then reads the t of its range's blocks,
     // which other workgroups of this launch (all resident: one per compute
     // unit) publish.
     constexpr int KA = JC * NCH;                 // 8-element chunks of a row per lane (d / 512)
@@ -342,6 +342,17 @@ __global__ void __launch_bounds__(NW * 64) gu_stream_kernel(BatchArgs b, int nb,
             acc = group_sum<64>(acc);
             if (lane == 0)
                 __hip_atomic_store(t64 + lc, (unsigned long long)__float_as_uint(acc) | (tag << 32),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        // a share longer than the waves (many blocks at rank 32): the rest,
+        // one row per wave at a time
+        for (int c = lc + NW; c < c1; c += NW) {
+            KBatch* kb = kbatch();
+            const int l = c / (2 * R), row = c - l * 2 * R;
+            const uint16_t* arow = row < R ? kb->lay[l].Ag + (long)row * b.d : kb->lay[l].Au + (long)(row - R) * b.d;
+            const float v = lora_a_dot<KA>(arow, b.x + (long)l * b.d, b.d, lane);
+            if (lane == 0)
+                __hip_atomic_store(t64 + c, (unsigned long long)__float_as_uint(v) | (tag << 32),
                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
@@ -694,10 +705,6 @@ bool stream_supported(int M, int d, int f, int gg, int bg, int gd, int bd, int r
         return false;
     const int sg = gu_span(nb, f, gu_grid(nb, f)), sd = dn_span(nb, d, dn_grid(nb, d));
     if (sg > kStreamSpan || sd > kStreamSpan)
-        return false;
-    // the gate/up workgroups' LoRA-A shares: at most one row per wave
-    const int gw = gu_steps(d / 64, jc) == 1 ? gu_waves<1>() : gu_waves<2>();
-    if (((long)nb * 2 * r + gu_grid(nb, f) - 1) / gu_grid(nb, f) > gw)
         return false;
     return gu_lds(sg, d / 64, r, nb, f, gu_grid(nb, f)) <= 64 * 1024 &&
            dn_lds(sd, 64 * dn_slots(f), nb, d, dn_grid(nb, d)) <= 64 * 1024;

@@ -262,6 +262,7 @@ def test_forward_batch_forces_standalone_kernels(q):
     (2048, 3072, 64, 32, 6),        # JC = 4
     (3072, 1024, 128, 8, 2),        # two steps per row (JC = 3), few rows
     (4096, 1536, 64, 16, 5),        # two steps per row (JC = 4)
+    (3072, 1024, 128, 32, 36),      # 2304 LoRA-A rows over 256 workgroups of 8 waves: 9 per workgroup
 ])
 def test_layers_streamed_shapes_match_oracle(q, d, f, g, r, L):
     """The streamed launches over widths of one and two steps per row, ranks
