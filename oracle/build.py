@@ -1,7 +1,7 @@
 """Compile the C oracle into ``oracle/libqmlp_oracle.so`` with gcc.
 
 No FMA contraction and no fast-math, so every fp64 operation is one IEEE
-rounding.  Building the checker is not using it: the graft ``build()`` step
+rounding.  Building the checker is not using it: the top-level ``build()`` entry point
 compiles it alongside the HIP library.
 """
 import os
