@@ -188,3 +188,27 @@ def test_moe_wide_activation_takes_the_chunked_staging(q):
     err = _run(q, cfg, 3, 2, 2, layer=5)
     print("max-rel %.2e" % err)
     assert err <= Y_TOL
+
+
+@pytest.mark.parametrize("r,k,M", [(32, 4, 2), (16, 2, 5), (0, 4, 1)])
+def test_moe_ranks_and_slots(q, r, k, M):
+    """Rank 32 (sixteen LoRA-A columns per instance, t read by 64 threads),
+    rank 16 at two slots and five tokens (two row groups per down
+    workgroup), and rank 0 (no LoRA-A columns, no t) against the oracle,
+    with the control block's error bits clear afterwards."""
+    cfg = wl.Config("moe_r%d" % r, M=1, d=1024, f=1536, g=64, r=r or 8, L=1)
+    print("\n[case] moe r %d k %d M %d" % (r, k, M), flush=True)
+    E = 6
+    lays = [wl.layer(cfg, e) for e in range(E)]
+    experts = q.Layers([gpu_mlp(lay, rank=r > 0) for lay in lays])
+    ws = torch.zeros(q.moe_workspace_bytes(experts, M, k), dtype=torch.uint8, device="cuda")
+    x = wl.activations(cfg, 60 + r, 0, M=M)
+    idx, w = wl.routing(M, E, k, r)
+    y = q.forward_moe(experts, act_tensor(x), torch.from_numpy(idx).cuda(), torch.from_numpy(w).cuda(), ws=ws)
+    torch.cuda.synchronize()
+    oq = [oracle_q(lay) + ((lay.A_gate, lay.B_gate, lay.A_up, lay.B_up) if r > 0 else (None,) * 4)
+          for lay in lays]
+    err = orc.max_rel_err(values_of(y), orc.moe_forward(oq, idx, w, x, lora_scale=cfg.lora_scale))
+    print("max-rel %.2e" % err)
+    assert err <= Y_TOL
+    assert q.workspace_errors(ws) == 0
