@@ -339,3 +339,37 @@ def test_layers_mfma_full_depth_sampled(q, name):
     worst = max(orc.max_rel_err(values_of(y[i]), values_of(yb[i])) for i in range(cfg.L))
     print("max-rel vs stand-alone kernels: %.2e" % worst)
     assert worst <= Y_TOL
+
+
+def test_layers_streamed_graph_replays_match_eager(q):
+    """The streamed launches captured in a HIP graph and replayed several
+    times, with eager work in between: the call counter that tags t advances
+    on the device, so every replay reads its own t and gives the eager
+    bits; the error bits stay clear and the counter counts every call."""
+    cfg = wl.CONFIGS["qwen3_4b"]
+    _announce("layers streamed graph replay", cfg.name, "L", 4)
+    layers, mlps, ls, x = _blocks(q, cfg, 4, first=20)
+    assert q.layers_path(ls, 1) == "streamed"
+    ws = q.layers_workspace(ls, 1)
+    y = torch.empty_like(x)
+    q.forward_layers(ls, x, y=y, ws=ws)
+    torch.cuda.synchronize()
+    ey = y.clone()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            q.forward_layers(ls, x, y=y, ws=ws)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        y.fill_(0)
+        junk = torch.randn(1 << 20, device="cuda").sum()
+        g.replay()
+        torch.cuda.synchronize()
+        assert float(junk) == float(junk)
+        assert torch.equal(y.view(torch.int16), ey.view(torch.int16)), rep
+    assert q.workspace_errors(ws) == 0
+    # the eager call, the captured one (capture runs nothing) and four replays
+    assert int(ws[0:4].view(torch.int32).item()) == 5
